@@ -1,0 +1,287 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle itself.
+
+Every check here is chosen so that a plausible slip in the oracle (a dropped
+term, a wrong sign, a transposed operand, an off-by-one in the causal mask or
+the slicing) fails at least one of them; test_oracle_mutations.py plants such
+slips and confirms it.
+
+* finite differences of the forward definition pin every analytic gradient;
+* the causal mask and the normaliser are pinned by closed forms: Y_1 = v_1,
+  constant keys give a running mean, constant values give a constant output;
+* the FAVOR+ map is pinned by its defining property, E_w[g(q)^T g(k)] =
+  exp(q^T k) for w ~ N(0, I_d), and by the limit M -> inf, where causal
+  linear attention approaches causal softmax attention (eq. 1; scipy's
+  softmax is the reference);
+* the slice-wise algorithm (Algorithms 1-2) is pinned by its exactness claim:
+  the result does not depend on C (Sec. 1, Sec. 4), so it must equal the
+  definition for C in {1, 2, 3, 7, L};
+* the token-by-token recurrence of Appendix B (with the gradS term restored)
+  must equal the definition as well.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle as O
+from synth import orthogonal_gaussian_features
+
+
+def _rand(shape, seed, scale=1.0):
+    return np.random.default_rng(seed).standard_normal(shape) * scale
+
+
+def _problem(B=1, H=2, L=9, d=3, M=5, seed=0, kind=O.FAVOR_PLUS):
+    rng = np.random.default_rng(seed)
+    s = d ** -0.25
+    Q = rng.standard_normal((B, H, L, d)) * s
+    K = rng.standard_normal((B, H, L, d)) * s
+    V = rng.standard_normal((B, H, L, d))
+    dY = rng.standard_normal((B, H, L, d))
+    W = orthogonal_gaussian_features(M, d, rng)
+    return Q, K, V, W, dY
+
+
+def _loss(Q, K, V, W, dY, kind):
+    return float(np.sum(dY * O.attention_forward(Q, K, V, W, kind)))
+
+
+def _fd_grad(f, X, h=1e-6):
+    g = np.zeros_like(X)
+    it = np.nditer(X, flags=["multi_index"])
+    for _ in it:
+        i = it.multi_index
+        x0 = X[i]
+        X[i] = x0 + h
+        fp = f()
+        X[i] = x0 - h
+        fm = f()
+        X[i] = x0
+        g[i] = (fp - fm) / (2 * h)
+    return g
+
+
+def _rel(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300))
+
+
+# ---------------------------------------------------------------- P1: finite differences
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+def test_gradients_match_finite_differences(kind):
+    Q, K, V, W, dY = _problem(B=1, H=2, L=6, d=3, M=5, seed=1)
+    dQ, dK, dV, dW = O.attention_backward(Q, K, V, W, dY, kind)
+    for name, X, g in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV), ("W", W, dW)):
+        fd = _fd_grad(lambda: _loss(Q, K, V, W, dY, kind), X)
+        assert _rel(g, fd) < 1e-7, name
+
+
+# ---------------------------------------------------------------- closed forms
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+def test_first_output_is_first_value(kind):
+    """Only l' = 1 contributes to Y_1, whatever the features (eq. 2)."""
+    Q, K, V, W, _ = _problem(L=8, seed=2)
+    Y = O.attention_forward(Q, K, V, W, kind)
+    assert np.max(np.abs(Y[:, :, 0] - V[:, :, 0])) < 1e-14
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+def test_constant_keys_give_running_mean(kind):
+    """Equal keys make every weight in row l equal: Y_l is the mean of V_1..V_l,
+    Y does not depend on Q, and dV_j = sum_{l >= j} dY_l / l."""
+    Q, K, V, W, dY = _problem(L=10, seed=3)
+    K[:] = K[:, :, :1]
+    Y = O.attention_forward(Q, K, V, W, kind)
+    counts = np.arange(1, 11)[None, None, :, None]
+    assert np.max(np.abs(Y - np.cumsum(V, axis=2) / counts)) < 1e-13
+    dQ, dK, dV, dW = O.attention_backward(Q, K, V, W, dY, kind)
+    assert np.max(np.abs(dQ)) < 1e-12
+    ref_dV = np.flip(np.cumsum(np.flip(dY / counts, axis=2), axis=2), axis=2)
+    assert np.max(np.abs(dV - ref_dV)) < 1e-13
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+def test_constant_values_give_constant_output(kind):
+    Q, K, V, W, dY = _problem(L=9, seed=4)
+    V[:] = V[:, :, :1]
+    Y = O.attention_forward(Q, K, V, W, kind)
+    assert np.max(np.abs(Y - V)) < 1e-13
+    dQ, dK, dV, dW = O.attention_backward(Q, K, V, W, dY, kind)
+    for g in (dQ, dK, dW):
+        assert np.max(np.abs(g)) < 1e-12
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+def test_value_gradient_sums_to_output_gradient(kind):
+    """Rows of the attention matrix sum to one, so sum_j dV_j = sum_l dY_l."""
+    Q, K, V, W, dY = _problem(L=11, seed=5)
+    _, _, dV, _ = O.attention_backward(Q, K, V, W, dY, kind)
+    assert np.max(np.abs(dV.sum(axis=2) - dY.sum(axis=2))) < 1e-12
+
+
+def test_euler_identities_of_feature_gradients():
+    """Y is homogeneous of degree 0 in each g(Q_l) and jointly in all g(K_l')."""
+    rng = np.random.default_rng(6)
+    Qf, Kf = rng.random((12, 7)) + 0.1, rng.random((12, 7)) + 0.1
+    V, dY = rng.standard_normal((12, 4)), rng.standard_normal((12, 4))
+    dQf, dKf, _ = O.quadratic_backward_features(Qf, Kf, V, dY)
+    assert np.max(np.abs(np.sum(Qf * dQf, axis=1))) < 1e-12
+    assert abs(np.sum(Kf * dKf)) < 1e-12
+
+
+def test_scale_invariances_and_linearity():
+    rng = np.random.default_rng(7)
+    Qf, Kf = rng.random((10, 6)) + 0.1, rng.random((10, 6)) + 0.1
+    V = rng.standard_normal((10, 3))
+    Y = O.quadratic_forward_features(Qf, Kf, V)[0]
+    c = rng.random((10, 1)) + 0.5
+    assert _rel(O.quadratic_forward_features(c * Qf, Kf, V)[0], Y) < 1e-14
+    assert _rel(O.quadratic_forward_features(Qf, 3.7 * Kf, V)[0], Y) < 1e-14
+    # a per-row key scale is not a symmetry
+    assert _rel(O.quadratic_forward_features(Qf, c * Kf, V)[0], Y) > 1e-3
+    V2 = rng.standard_normal((10, 3))
+    Y2 = O.quadratic_forward_features(Qf, Kf, V2)[0]
+    Y12 = O.quadratic_forward_features(Qf, Kf, 2.0 * V - 0.5 * V2)[0]
+    assert _rel(Y12, 2.0 * Y - 0.5 * Y2) < 1e-13
+
+
+# ---------------------------------------------------------------- feature maps
+
+
+def test_favor_plus_is_unbiased_for_the_exponential_kernel():
+    """E_w[g(q)^T g(k)] = exp(q^T k) for iid w ~ N(0, I) (Gaussian MGF)."""
+    rng = np.random.default_rng(8)
+    d, M = 4, 1 << 17
+    q = rng.standard_normal((6, d)) * 0.5
+    k = rng.standard_normal((6, d)) * 0.5
+    W = rng.standard_normal((M, d))
+    ratio = (O.feature_map(q, W, O.FAVOR_PLUS) @ O.feature_map(k, W, O.FAVOR_PLUS).T) / np.exp(q @ k.T)
+    assert abs(np.mean(ratio) - 1.0) < 0.02
+    assert np.max(np.abs(ratio - 1.0)) < 0.25
+
+
+def test_favor_plus_attention_approaches_softmax_attention():
+    """With many features the map recovers causal softmax attention (eq. 1)."""
+    rng = np.random.default_rng(9)
+    d, L, M = 4, 8, 1 << 18
+    q = rng.standard_normal((L, d)) * d ** -0.25
+    k = rng.standard_normal((L, d)) * d ** -0.25
+    v = rng.standard_normal((L, d))
+    W = orthogonal_gaussian_features(M, d, rng)
+    Y = O.attention_forward(q[None, None], k[None, None], v[None, None], W, O.FAVOR_PLUS)[0, 0]
+    logits = np.where(np.tril(np.ones((L, L))) > 0, q @ k.T, -np.inf)
+    Ys = scipy.special.softmax(logits, axis=1) @ v
+    assert np.max(np.abs(Y - Ys)) < 0.05
+
+
+def test_relu_map_with_identity_features():
+    """W = I reduces the ReLU map to max(x, 0) + eps, coordinate by coordinate."""
+    X = np.array([[0.5, -2.0, 0.0], [1.25, 3.0, -0.1]])
+    out = O.feature_map(X, np.eye(3), O.RELU)
+    assert np.array_equal(out, np.array([[0.501, 0.001, 0.001], [1.251, 3.001, 0.001]]))
+
+
+def test_relu_map_gradient_mask():
+    X = np.array([[0.5, -2.0]])
+    W = np.eye(2)
+    Phi = O.feature_map(X, W, O.RELU)
+    dX, dW = O.feature_map_vjp(X, W, Phi, np.array([[1.0, 1.0]]), O.RELU)
+    assert np.array_equal(dX, np.array([[1.0, 0.0]]))
+    assert np.array_equal(dW, np.array([[0.5, -2.0], [0.0, 0.0]]))
+
+
+# ---------------------------------------------------------------- Algorithm 1: C-invariance
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("within", ["ps", "quadratic"])
+@pytest.mark.parametrize("C", [1, 2, 3, 7, 20])
+def test_slicewise_equals_definition_for_every_slice_length(kind, within, C):
+    Q, K, V, W, dY = _problem(B=2, H=1, L=20, d=3, M=6, seed=10)
+    Y0 = O.attention_forward(Q, K, V, W, kind)
+    g0 = O.attention_backward(Q, K, V, W, dY, kind)
+    Y, st = O.slim_forward(Q, K, V, W, C, kind, within=within)
+    assert _rel(Y, Y0) < 1e-12
+    # the final state is the full prefix sum of T_l = (V_l g(K_l)^T, g(K_l))
+    Kf = O.feature_map(K, W, kind)
+    R = np.einsum("bhld,bhlm->bhdm", V, Kf)
+    assert _rel(st, O.pack_state(R, Kf.sum(axis=2))) < 1e-12
+    dQ, dK, dV, dW, gst = O.slim_backward(Q, K, V, W, dY, C, kind, st, within=within)
+    for g, r in zip((dQ, dK, dV, dW), g0):
+        assert _rel(g, r) < 1e-11
+
+
+def test_slice_bounds_ragged_tail():
+    assert O.slice_bounds(10, 4) == [(0, 4), (4, 8), (8, 10)]
+    assert O.slice_bounds(10, 10) == [(0, 10)]
+    assert O.slice_bounds(10, 64) == [(0, 10)]
+    assert O.slice_bounds(4096, 1366)[-1] == (2732, 4096)
+    with pytest.raises(ValueError):
+        O.slice_bounds(10, 0)
+
+
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+def test_state_gradient_matches_finite_differences(kind):
+    """G^(0) = dL/dB^(0), with L = sum dY.Y + <G^(N), B^(N)> (eqs. 17-18)."""
+    Q, K, V, W, dY = _problem(B=1, H=1, L=7, d=3, M=4, seed=11)
+    rng = np.random.default_rng(12)
+    st0 = np.abs(rng.standard_normal((1, 1, 4, 4))) + 0.2
+    gN = rng.standard_normal((1, 1, 4, 4))
+
+    def loss():
+        Y, st = O.slim_forward(Q, K, V, W, 3, kind, state_in=st0)
+        return float(np.sum(dY * Y) + np.sum(gN * st))
+
+    Y, st = O.slim_forward(Q, K, V, W, 3, kind, state_in=st0)
+    dQ, dK, dV, dW, g0 = O.slim_backward(Q, K, V, W, dY, 3, kind, st, dstate_out=gN)
+    assert _rel(g0, _fd_grad(loss, st0)) < 1e-7
+    assert _rel(dQ, _fd_grad(loss, Q)) < 1e-7
+    assert _rel(dK, _fd_grad(loss, K)) < 1e-7
+    assert _rel(dW, _fd_grad(loss, W)) < 1e-7
+
+
+@pytest.mark.parametrize("within", ["ps", "quadratic"])
+def test_streaming_in_two_calls_equals_one_call(within):
+    """B^(n) is an exact checkpoint of the scan: split the sequence, hand the
+    state forward and the state cotangent backward."""
+    Q, K, V, W, dY = _problem(B=1, H=2, L=13, d=3, M=5, seed=13)
+    kind, C, cut = O.FAVOR_PLUS, 4, 6
+    Y, st = O.slim_forward(Q, K, V, W, C, kind, within=within)
+    g = O.slim_backward(Q, K, V, W, dY, C, kind, st, within=within)
+    p1 = [x[:, :, :cut] for x in (Q, K, V, dY)]
+    p2 = [x[:, :, cut:] for x in (Q, K, V, dY)]
+    Y1, st1 = O.slim_forward(*p1[:3], W, C, kind, within=within)
+    Y2, st2 = O.slim_forward(*p2[:3], W, C, kind, state_in=st1, within=within)
+    assert _rel(np.concatenate([Y1, Y2], axis=2), Y) < 1e-13
+    assert _rel(st2, st) < 1e-13
+    dQ2, dK2, dV2, dW2, g1 = O.slim_backward(*p2[:3], W, p2[3], C, kind, st2, within=within)
+    dQ1, dK1, dV1, dW1, g0 = O.slim_backward(*p1[:3], W, p1[3], C, kind, st1, dstate_out=g1, within=within)
+    assert _rel(np.concatenate([dQ1, dQ2], axis=2), g[0]) < 1e-12
+    assert _rel(np.concatenate([dK1, dK2], axis=2), g[1]) < 1e-12
+    assert _rel(np.concatenate([dV1, dV2], axis=2), g[2]) < 1e-12
+    assert _rel(dW1 + dW2, g[3]) < 1e-12
+    assert _rel(g0, g[4]) < 1e-12
+
+
+# ---------------------------------------------------------------- Appendix B recurrence
+
+
+def test_token_recurrence_equals_definition():
+    rng = np.random.default_rng(14)
+    L, M, d = 15, 6, 4
+    Qf, Kf = rng.random((L, M)) + 0.05, rng.random((L, M)) + 0.05
+    V, dY = rng.standard_normal((L, d)), rng.standard_normal((L, d))
+    Y0, A, D0 = O.quadratic_forward_features(Qf, Kf, V)
+    Y, N, D, curR, curS = O.iterative_forward_features(Qf, Kf, V)
+    assert _rel(Y, Y0) < 1e-13
+    dN = dY / D[:, None]
+    dD = -np.sum(dY * Y, axis=1) / D
+    dQf, dKf, dV = O.iterative_backward_features(Qf, Kf, V, dN, dD, curR, curS)
+    r = O.quadratic_backward_features(Qf, Kf, V, dY)
+    for g, ref in zip((dQf, dKf, dV), r):
+        assert _rel(g, ref) < 1e-12
