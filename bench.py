@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of slice-wise causal FAVOR+ attention, forward + backward, on one GPU.
+
+One step = slim_fwd + slim_bwd over one batch of the L = 32768 workload
+(B=4, H=8, d=64, M=256, bf16 inputs, FAVOR+), inputs resident in device memory.
+Prints one JSON line with throughput (tokens/s = B*L / step time), a roofline
+entry for the dominant kernel, the fp64 CPU oracle timed on a bounded sample,
+and a slice-length sweep with peak device memory per C.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--C 64] [--no-sweep] [--no-cpu]
+"""
+
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "causal FAVOR+ fwd+bwd tokens/sec at L=32k, d=64, M=256; peak mem vs slice C"
+PEAK_BF16_FLOPS = 2.5e15  # MI355X dense bf16 matrix-core peak
+PEAK_HBM_BYTES = 8.0e12
+TILE_ROWS = 32  # rows per tile of the kernels (block of the in-slice evaluation)
+
+
+def algo_flops_per_token_head(d: int, M: int, C: int, tile: int = TILE_ROWS):
+    """Algorithmic flops (2 per multiply-add) per token and head.
+
+    The in-slice prefix sum is evaluated block-iteratively with blocks of
+    c = min(C, tile) rows; inside a block the causal quadratic form costs half
+    of the c x c products (c + 1 per row).
+      fwd: 4dM (Q, K logits) + 4M(d+1) (state read + update) + (M+d+1)(c+1)
+      bwd: 24dM + 10M + (3M+3d+1)(c+1) (recompute, downdate, gradients, chain
+           rule through the feature map, dW)
+    """
+    c = min(C, tile)
+    fwd = 4 * d * M + 4 * M * (d + 1) + (M + d + 1) * (c + 1)
+    bwd = 24 * d * M + 10 * M + (3 * M + 3 * d + 1) * (c + 1)
+    return fwd, bwd
+
+
+def kernel_sources_sha() -> str:
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2012_11346_amd", "csrc", "*"))):
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, units_per_launch: float):
+    """HBM traffic of a kernel from the committed counter summary, if it was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except Exception:
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if k is None or rec.get("sources_sha") != kernel_sources_sha():
+        return None
+    return k.get("bytes_per_launch")
+
+
+def cpu_baseline(x, C: int, H: int, L: int):
+    """Time the fp64 oracle (Algorithm 1 with the in-slice quadratic form) on
+    batch element 0: all heads, full length.  Returns the record and the
+    oracle's Y/gradients for a parity spot check."""
+    import numpy as np
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    Q, K, V, dY = (x[k][:1] for k in ("Q", "K", "V", "dY"))
+    t0 = time.perf_counter()
+    Y, st = O.slim_forward(Q, K, V, x["W"], C, "favor+", within="quadratic")
+    g = O.slim_backward(Q, K, V, x["W"], dY, C, "favor+", st, within="quadratic")
+    t = time.perf_counter() - t0
+    rec = {
+        "value": L / t,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"batch element 0 of the workload (all {H} heads, L={L}), fp64 Algorithm 1 with the "
+        f"in-slice quadratic form at C={C}; {t:.1f} s on the host",
+        "seconds": t,
+        "host_cpus": os.cpu_count(),
+    }
+    return rec, Y, g
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--C", type=int, default=64)
+    ap.add_argument("--workload", default="sweep_32k")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sweep-steps", type=int, default=3)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path runs on a single "
+              "MI355X; see DESIGN.md for how it would shard)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2012_11346_amd import slim
+    from synth import make_inputs, workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    wl = workload(args.workload)
+    B, H, L, d, M = wl.B, wl.H, wl.L, wl.d, wl.M
+    kind = wl.kind
+    t0 = time.perf_counter()
+    x = make_inputs(wl)
+    print(f"[bench] inputs generated in {time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
+    dev = torch.device("cuda", 0)
+    Q, K, V, dY = (x[k].to(dev) for k in ("Q", "K", "V", "dY"))
+    W = x["W"].to(dev)
+    torch.cuda.synchronize()
+    io_bytes = torch.cuda.memory_allocated()
+
+    def buffers(C):
+        p = slim.problem(B, H, L, d, M, C, Q.dtype, kind)
+        bufs = dict(
+            Y=torch.empty_like(Q),
+            st=torch.empty((B, H, M, d + 1), dtype=torch.float32, device=dev),
+            ks=torch.empty((B, H), dtype=torch.float32, device=dev),
+            dQ=torch.empty_like(Q),
+            dK=torch.empty_like(K),
+            dV=torch.empty_like(V),
+            dW=torch.empty((M, d), dtype=torch.float32, device=dev),
+            wsf=torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_FWD)), dtype=torch.uint8, device=dev),
+            wsb=torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_BWD)), dtype=torch.uint8, device=dev),
+        )
+        return p, bufs
+
+    def step(C, b):
+        slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
+        slim.bwd(Q, K, V, W, dY, C, b["st"], b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
+                 dW=b["dW"])
+
+    def timed(C, steps, warmup):
+        p, b = buffers(C)
+        for _ in range(warmup):
+            step(C, b)
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        stream = torch.cuda.current_stream()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for i in range(steps):
+            ev[i][0].record(stream)
+            slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
+            ev[i][1].record(stream)
+            slim.bwd(Q, K, V, W, dY, C, b["st"], b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
+                     dW=b["dW"])
+            ev[i][2].record(stream)
+        end.record(stream)
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+        fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+        bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
+        peak = torch.cuda.max_memory_allocated()
+        out_bytes = sum(t.numel() * t.element_size() for k, t in b.items() if not k.startswith("ws"))
+        return dict(total_ms=total_ms, ms=total_ms / steps, fwd_ms=fwd_ms, bwd_ms=bwd_ms, peak=peak,
+                    extra=peak - io_bytes - out_bytes, out_bytes=out_bytes, ws_fwd=b["wsf"].numel(),
+                    ws_bwd=b["wsb"].numel(), segments=slim.num_segments(p)), b
+
+    C = args.C
+    print(f"[bench] timing C={C}: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
+    r, b = timed(C, args.steps, args.warmup)
+    tokens = B * L
+    value = tokens / (r["ms"] / 1e3)
+    fl_f, fl_b = algo_flops_per_token_head(d, M, C)
+    units = B * H * L  # token-heads per launch
+    bwd_flops = fl_b * units
+    achieved = bwd_flops / (r["bwd_ms"] / 1e3)
+    dominant = "bwd_walk_kernel" if r["bwd_ms"] >= r["fwd_ms"] else "fwd_walk_kernel"
+    dom_ms = max(r["bwd_ms"], r["fwd_ms"])
+    dom_flops = bwd_flops if dominant == "bwd_walk_kernel" else fl_f * units
+    achieved = dom_flops / (dom_ms / 1e3)
+    traffic = load_traffic(dominant, units)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: causal FAVOR+ attention fwd+bwd, B={B} H={H} L={L} d={d} M={M}, "
+            f"bf16 inputs with fp32 accumulation, slice length C={C}",
+            "B": B, "H": H, "L": L, "d": d, "M": M, "C": C, "kind": kind,
+            "segments_per_head": r["segments"],
+        },
+        "fwd_ms": r["fwd_ms"],
+        "bwd_ms": r["bwd_ms"],
+        "roofline": {
+            "kernel": dominant,
+            "bound": "mfma",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_BF16_FLOPS / 1e12,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_FLOPS,
+            "traffic": traffic,
+            "flops_per_token_head": {"fwd": fl_f, "bwd": fl_b},
+            "launch_ms": dom_ms,
+        },
+        "mfma_frac_fwd_bwd": (fl_f + fl_b) * units / (r["ms"] / 1e3) / PEAK_BF16_FLOPS,
+        "peak_mem": {"peak_bytes": r["peak"], "input_bytes": io_bytes, "output_bytes": r["out_bytes"],
+                     "beyond_io_bytes": r["extra"],
+                     "workspace_fwd": r["ws_fwd"], "workspace_bwd": r["ws_bwd"]},
+    }
+    print(f"[bench] C={C}: {r['ms']:.3f} ms/step (fwd {r['fwd_ms']:.3f}, bwd {r['bwd_ms']:.3f}), "
+          f"{value:.3e} tokens/s", file=sys.stderr, flush=True)
+
+    if not args.no_sweep:
+        sweep = []
+        for Cs in wl.C:
+            rs, _ = timed(Cs, args.sweep_steps, 1)
+            sweep.append({"C": Cs, "tokens_per_s": tokens / (rs["ms"] / 1e3), "ms_per_step": rs["ms"],
+                          "peak_bytes": rs["peak"], "beyond_io_bytes": rs["extra"], "workspace_bwd": rs["ws_bwd"]})
+            print(f"[bench] sweep C={Cs}: {rs['ms']:.3f} ms/step, extra memory {rs['extra'] / 2**20:.1f} MiB",
+                  file=sys.stderr, flush=True)
+        out["sweep"] = sweep
+
+    if not args.no_cpu:
+        print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
+        rec, Yo, go = cpu_baseline(x, C, H, L)
+        out["cpu_baseline"] = rec
+        # spot check of the timed configuration against the oracle (batch element 0)
+        Yg = b["Y"][:1].double().cpu().numpy()
+
+        def mr(a, ref):
+            return float(np.max(np.abs(a - ref)) / np.max(np.abs(ref)))
+
+        out["parity_batch0"] = {
+            "Y": mr(Yg, Yo),
+            "dQ": mr(b["dQ"][:1].double().cpu().numpy(), go[0]),
+            "dK": mr(b["dK"][:1].double().cpu().numpy(), go[1]),
+            "dV": mr(b["dV"][:1].double().cpu().numpy(), go[2]),
+        }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,159 @@
+/*
+ * slim.h - C ABI of the slice-wise causal linear attention library (gfx950).
+ *
+ * The library computes exact causal linear attention with a positive random
+ * feature map g (Sec. 2.1, eq. 2) for a batch of heads,
+ *
+ *     Y_l = sum_{l' <= l} (g(Q_l) . g(K_l')) V_l' / sum_{l' <= l} g(Q_l) . g(K_l'),
+ *
+ * slice by slice in the manner of Algorithm 1 (Sec. 3.2-3.3): the forward
+ * pass carries the running state B = (sum_l g(K_l) V_l^T, sum_l g(K_l)) from
+ * slice to slice (eqs. 14-16); the backward pass walks the slices in reverse,
+ * downdating B by each slice's contribution (eq. 17), recomputing the slice
+ * and carrying the state cotangent G (eq. 18).  Extra device memory is
+ * state-sized: it does not grow with the sequence length L.
+ *
+ * Feature maps (W in R^{M x d}, one row w_m per feature):
+ *   SLIM_FAVOR_PLUS  g(x)_m = exp(w_m . x - |x|^2 / 2) / sqrt(M)
+ *   SLIM_RELU        g(x)_m = max(w_m . x, 0) + relu_eps
+ * The FAVOR+ map is evaluated with max-stabilisers that cancel exactly:
+ * one shift per query row and one shift per (batch, head) shared by all keys;
+ * the state is stored relative to the key shift (true state =
+ * stored state * exp(kshift)).  The ReLU map uses no shifts.
+ *
+ * Conventions for every entry point:
+ *   - Tensors are dense, contiguous, row-major, in device memory:
+ *       Q, K, V, Y, dY, dQ, dK, dV : [B, H, L, d], element type `dtype`
+ *       W, dW                      : [M, d] float32, W shared by all heads
+ *       state tensors              : [B, H, M, d + 1] float32; column j < d of
+ *                                    row m holds sum_l g(K_l)_m V_l[j], column
+ *                                    d holds sum_l g(K_l)_m
+ *       kshift tensors             : [B, H] float32 (FAVOR+ only)
+ *   - The caller owns every buffer.  The library never allocates or frees
+ *     device memory; scratch space is the caller's workspace `ws`, whose size
+ *     slim_workspace_bytes() gives.  The workspace holds nothing between calls.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
+ *     the default stream).  No call synchronises the device.
+ *   - Arguments are validated on the host before anything is launched; on a
+ *     validation error nothing is launched and the output buffers are untouched.
+ *     The return value is a slim_status; slim_last_error() describes the last
+ *     failure of the calling thread.
+ *   - The library keeps no state between calls and may be called from several
+ *     threads; calls that share a workspace or outputs must not overlap.
+ */
+#ifndef SLIM_H_
+#define SLIM_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SLIM_OK = 0,
+  SLIM_EINVAL = -1,       /* null pointer, size < 1, unknown enum value */
+  SLIM_EUNSUPPORTED = -2, /* well-formed problem outside the kernels' coverage */
+  SLIM_EWORKSPACE = -3,   /* workspace null or smaller than slim_workspace_bytes() */
+  SLIM_EHIP = -4          /* a HIP runtime call or a kernel launch failed */
+} slim_status;
+
+typedef enum { SLIM_FAVOR_PLUS = 0, SLIM_RELU = 1 } slim_kind;
+typedef enum { SLIM_F32 = 0, SLIM_BF16 = 1 } slim_dtype;
+typedef enum { SLIM_QUERY = 0, SLIM_KEY = 1 } slim_role;
+typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
+
+/* Problem description shared by all entry points.
+ *   B, H, L  batch, heads, sequence length (each >= 1)
+ *   d        head dimension: 32 or 64
+ *   M        number of features: 64, 128 or 256
+ *   C        slice length (Sec. 3.2): >= 1; values above L act as L.  The
+ *            sequence is cut into N = ceil(L / C) slices, the last one ragged.
+ *   dtype    slim_dtype of Q, K, V, Y, dY, dQ, dK, dV.  With SLIM_BF16 every
+ *            product runs on bf16 matrix cores with float32 accumulation and
+ *            W is rounded to bf16 once; with SLIM_F32 products are float32.
+ *   kind     slim_kind
+ *   relu_eps additive constant of the ReLU map (the usual value is 1e-3) */
+typedef struct {
+  int64_t B, H, L;
+  int32_t d, M, C;
+  int32_t dtype;
+  int32_t kind;
+  float relu_eps;
+} slim_problem;
+
+/* Bytes of device workspace slim_fwd (phase SLIM_PHASE_FWD) or slim_bwd
+ * (SLIM_PHASE_BWD) need for problem *p.  Independent of L beyond the point
+ * where the sequence is split into its maximum number of segments.  Returns 0
+ * for an invalid problem (slim_last_error() says why).  Memory-only query:
+ * makes no HIP call. */
+size_t slim_workspace_bytes(const slim_problem* p, int phase);
+
+/* Feature map of Sec. 2.1 (the map g of eq. 2) on its own, for inspection.
+ *   X      [B, H, L, d] queries (role SLIM_QUERY) or keys (role SLIM_KEY), dtype
+ *   W      [M, d] float32
+ *   phi    out [B, H, L, M] float32: the stabilised map phi_hat
+ *   shift  out, FAVOR+ only (NULL allowed for ReLU): queries [B, H, L], keys
+ *          [B, H].  g(x) = phi_hat * exp(shift).  The query shift of row l is
+ *          max_m(w_m . x_l) - |x_l|^2 / 2; the key shift of a head is the same
+ *          maximum taken over all its rows.
+ * The products use the same precision as slim_fwd (bf16 matrix cores for
+ * SLIM_BF16). */
+int slim_featmap(const slim_problem* p, const void* X, const float* W, int role, float* phi,
+                 float* shift, void* stream);
+
+/* Forward sweep of Algorithm 1 (one layer): Y for every row, and the state
+ * B^(N) after the last slice.
+ *   state_in   optional [B, H, M, d + 1]: the state B^(0) the sequence starts
+ *              from (a previous call's state_out); NULL means zero
+ *   kshift_in  [B, H], required with state_in for FAVOR+: the key shift
+ *              state_in is relative to
+ *   Y          out [B, H, L, d]
+ *   state_out  out [B, H, M, d + 1], may be NULL: B^(N) relative to kshift_out
+ *   kshift_out out [B, H] (FAVOR+: required; ReLU: ignored, may be NULL)
+ *   ws         workspace of at least slim_workspace_bytes(p, SLIM_PHASE_FWD) */
+int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+             const float* state_in, const float* kshift_in, void* Y, float* state_out,
+             float* kshift_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward sweep of Algorithm 1 (one layer) for the loss
+ * sum(dY * Y) + <dstate_out, state_out>.
+ *   Q, K, V, W, state_in, kshift_in  as given to slim_fwd
+ *   state_out  [B, H, M, d + 1]: B^(N), the state_out slim_fwd returned; the
+ *              reverse walk starts from it and downdates slice by slice
+ *   kshift     [B, H]: kshift_out of slim_fwd (FAVOR+; ignored for ReLU)
+ *   dY         [B, H, L, d] cotangent of Y
+ *   dstate_out optional [B, H, M, d + 1]: cotangent G^(N) of state_out (in the
+ *              same kshift scaling as state_out); NULL means zero
+ *   dQ, dK, dV out [B, H, L, d]
+ *   dW         out [M, d] float32, overwritten: summed over heads, rows and the
+ *              query and key branches
+ *   dstate_in  out, may be NULL: [B, H, M, d + 1] cotangent G^(0) of state_in
+ *              (relative to kshift_in); the zero initial state when state_in
+ *              is NULL
+ *   ws         workspace of at least slim_workspace_bytes(p, SLIM_PHASE_BWD)
+ * The key shifts are constants of the computation (stop-gradient); they
+ * cancel exactly in Y.  The pass recomputes every slice (Alg. 2); nothing
+ * of size O(L) is kept between slim_fwd and slim_bwd. */
+int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+             const float* state_in, const float* kshift_in, const float* state_out, const float* kshift,
+             const void* dY, const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
+             void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* slim_status_string(int status);
+
+/* Description of the last failure of the calling thread ("" if none). */
+const char* slim_last_error(void);
+
+/* Number of segments the sequence of each head is split into for parallel
+ * processing (1 means one workgroup walks the whole sequence), or 0 for an
+ * invalid problem.  Memory-only query. */
+int slim_num_segments(const slim_problem* p);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SLIM_H_ */

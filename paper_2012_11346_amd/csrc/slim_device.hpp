@@ -1,0 +1,209 @@
+// Device building blocks for the slice-wise causal linear attention kernels
+// (gfx950, wave64).
+//
+// Matrix-core conventions.  A wave computes 16x16 fp32 result tiles with
+// v_mfma_f32_16x16x32_bf16 (bf16 problems) or 8 chained
+// v_mfma_f32_16x16x4_f32 (fp32 problems).  With lane = 16 g + c
+// (g in 0..3, c in 0..15):
+//
+//   result tile  X[16 x 16]     lane (g, c), register r  <->  X[4g + r][c]
+//   operand      "fragment"     lane (g, c), slot s      <->  row/col c, k = kp(g, s)
+//
+// where a fragment covers one 32-deep block of the contraction index k and
+//
+//   kp(g, s) = 16 (s / 4) + 4 g + (s % 4)
+//
+// is the slot order used everywhere in this library (A and B operands of one
+// product must agree on it; the sum over k does not care about the order).
+// With this order two result tiles stacked along their rows, X0 = rows
+// [0, 16) and X1 = rows [16, 32), are directly an operand fragment that
+// contracts over those 32 rows (tile_pair_frag), so results can feed the next
+// product without leaving registers whenever the next contraction runs over
+// the result's row index.  When it runs over the column index instead, the
+// tile goes through LDS: store_tile_T writes X transposed (one 8-byte store
+// per lane for bf16) and frag_tr reads it back with ds_read_b64_tr_b16, whose
+// per-16-lane semantics (lane j supplies the address of 4 consecutive 16-bit
+// values a_j; lane i receives slot r = mem[a_{4r + i/4} + i % 4]) turn a
+// "k-major" LDS matrix (rows = contraction index, columns contiguous) into a
+// fragment.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace slim {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+#define SLIM_LDS __attribute__((address_space(3)))
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int lane_g() { return (threadIdx.x & 63) >> 4; }
+__device__ __forceinline__ int lane_c() { return threadIdx.x & 15; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+// k offset of slot s of lane group g inside a 32-deep block
+__device__ __forceinline__ int kp(int g, int s) { return 16 * (s >> 2) + 4 * g + (s & 3); }
+
+template <typename T>
+struct FragT;
+template <>
+struct FragT<bf16> {
+  typedef bf16x8 type;
+};
+template <>
+struct FragT<float> {
+  typedef f32x8 type;
+};
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// acc += A * B over one 32-deep block
+__device__ __forceinline__ f32x4 mma(f32x4 acc, bf16x8 a, bf16x8 b) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma(f32x4 acc, f32x8 a, f32x8 b) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], acc, 0, 0, 0);
+  return acc;
+}
+
+template <typename T>
+__device__ __forceinline__ T cvt(float x);
+template <>
+__device__ __forceinline__ bf16 cvt<bf16>(float x) {
+  return (bf16)x;
+}
+template <>
+__device__ __forceinline__ float cvt<float>(float x) {
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T x) {
+  return (float)x;
+}
+
+// ------------------------------------------------------------- fragments
+
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type frag_zero() {
+  typename FragT<T>::type f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f[s] = cvt<T>(0.f);
+  return f;
+}
+
+// two result tiles (rows [0,16) and [16,32) of a 32-row block, same columns)
+// as an operand contracting over those rows
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type tile_pair_frag(const f32x4& x0, const f32x4& x1) {
+  typename FragT<T>::type f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = cvt<T>(x0[r]);
+    f[4 + r] = cvt<T>(x1[r]);
+  }
+  return f;
+}
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type tile_half_frag(const f32x4& x0) {
+  typename FragT<T>::type f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = cvt<T>(x0[r]);
+    f[4 + r] = cvt<T>(0.f);
+  }
+  return f;
+}
+
+// Fragment from an LDS matrix stored with the contraction index contiguous:
+// slot s = Z[row0 + c][k0 + kp(g, s)]  (pitch ld elements).
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type frag_rm(const T* Z, int ld, int row0, int k0) {
+  const int g = lane_g(), c = lane_c();
+  const T* p = Z + (row0 + c) * ld + k0 + 4 * g;
+  typename FragT<T>::type f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = p[r];
+    f[4 + r] = p[16 + r];
+  }
+  return f;
+}
+
+// Fragment from an LDS matrix stored k-major (contraction index = row):
+// slot s = Z[k0 + kp(g, s)][col0 + c]  (pitch ld elements).
+__device__ __forceinline__ bf16x8 frag_tr(const bf16* Z, int ld, int k0, int col0) {
+  const int g = lane_g(), c = lane_c();
+  const bf16* p0 = Z + (k0 + 4 * g + (c >> 2)) * ld + col0 + 4 * (c & 3);
+  const bf16* p1 = p0 + 16 * ld;
+  typedef SLIM_LDS i16x4 lds_i16x4;
+  i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(SLIM_LDS void*)(uintptr_t)p0);
+  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(SLIM_LDS void*)(uintptr_t)p1);
+  bf16x8 f;
+  bf16x4 av = __builtin_bit_cast(bf16x4, a);
+  bf16x4 bv = __builtin_bit_cast(bf16x4, b);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = av[r];
+    f[4 + r] = bv[r];
+  }
+  return f;
+}
+__device__ __forceinline__ f32x8 frag_tr(const float* Z, int ld, int k0, int col0) {
+  const int g = lane_g(), c = lane_c();
+  f32x8 f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f[s] = Z[(k0 + kp(g, s)) * ld + col0 + c];
+  return f;
+}
+
+// Store result tile X[row0 + 4g + r][col0 + c] transposed: Z[col0 + c][row0 + 4g + r].
+template <typename T>
+__device__ __forceinline__ void store_tile_T(T* Z, int ld, const f32x4& x, int row0, int col0) {
+  const int g = lane_g(), c = lane_c();
+  T* p = Z + (col0 + c) * ld + row0 + 4 * g;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) p[r] = cvt<T>(x[r]);
+}
+
+// ------------------------------------------------------------- wave reductions
+
+__device__ __forceinline__ float wave_max_over_g(float v) {
+  // max over the 4 lanes that share c (lanes c, c+16, c+32, c+48)
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  v = fmaxf(v, __shfl_xor(v, 32, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum_over_g(float v) {
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max_over_c(float v) {
+  v = fmaxf(v, __shfl_xor(v, 1, 64));
+  v = fmaxf(v, __shfl_xor(v, 2, 64));
+  v = fmaxf(v, __shfl_xor(v, 4, 64));
+  v = fmaxf(v, __shfl_xor(v, 8, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum_over_c(float v) {
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 8, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) { return wave_max_over_c(wave_max_over_g(v)); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+}  // namespace slim

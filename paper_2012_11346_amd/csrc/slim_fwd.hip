@@ -1,0 +1,491 @@
+// Forward sweep (Algorithm 1, one layer) and the stand-alone feature map.
+//
+// fwd_walk: one workgroup per (batch, head, segment) walks its tiles in
+// order.  Per tile of C_t <= TR rows (never straddling a slice), with the
+// state B = (S, z) of everything before the tile held in registers:
+//   a1  logits of Q and K against W on the matrix cores, with -|x|^2/2 folded
+//       into the accumulator start; FAVOR+ features are exp2 of the shifted
+//       logits (one shift per query row, one running shift per head for keys;
+//       when the key shift grows the state is rescaled, so that all keys seen
+//       so far share one shift).  ReLU: max(., 0) + eps.
+//   a2  scores A^T = tril(K~ Q~^T) restricted to the tile (eq. 2, first line)
+//   a3+a4  N^T = [V|1]^T A^T + [S|z]^T Q~^T, per wave over its features
+//   a5  cross-wave sum of N, then Y = N / D
+//   a6  [S|z] += K~^T [V|1]                       (eqs. 14-16, carried state)
+// For slices longer than TR rows the tiles of a slice are chained through
+// the same running state, which is the block-iterative evaluation of the
+// in-slice prefix sum (Appendix B) with block TR.
+#include "slim_common.hpp"
+#include "slim_kernels.hpp"
+
+namespace slim {
+
+template <class G>
+__device__ __forceinline__ void load_w_frags(typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+                                             const float* W, int w) {
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int mt = 0; mt < G::MT; ++mt)
+#pragma unroll
+    for (int kb = 0; kb < G::EB; ++kb)
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        Wf[mt][kb][s] = cvt<typename G::T>(W[(size_t)(w * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)]);
+}
+
+// operand fragment of [V|1] over rows [k0, k0 + 32) for value tile et (et ==
+// ET is the all-ones column block, zero on rows >= count)
+template <class G>
+__device__ __forceinline__ typename FragT<typename G::T>::type v_frag(const typename G::T* Vs, int k0, int et,
+                                                                        int count) {
+  typedef typename G::T T;
+  if (et < G::ET) return frag_tr(Vs, G::LDQ, k0, 16 * et);
+  typename FragT<T>::type f;
+  const int g = lane_g();
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f[s] = cvt<T>((k0 + kp(g, s) < count) ? 1.f : 0.f);
+  return f;
+}
+
+// Query logits, transposed: Lq[mt][tt] holds rows m (features of this wave),
+// columns t.  The accumulator starts at -|q_t|^2/2 for FAVOR+.
+template <class G>
+__device__ __forceinline__ void query_logits(f32x4 (&Lq)[G::MT][G::RT],
+                                             const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+                                             const typename G::T* Qs, const float* qn) {
+  const int c = lane_c();
+#pragma unroll
+  for (int tt = 0; tt < G::RT; ++tt) {
+    const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
+#pragma unroll
+    for (int mt = 0; mt < G::MT; ++mt) {
+      f32x4 acc = {init, init, init, init};
+#pragma unroll
+      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(Qs, G::LDQ, 16 * tt, 32 * kb));
+      Lq[mt][tt] = acc;
+    }
+  }
+}
+
+// Key logits: Lk[st][mt] holds rows s, columns m (features of this wave).
+template <class G>
+__device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
+                                           const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+                                           const typename G::T* Ks, const float* kn) {
+  const int g = lane_g();
+#pragma unroll
+  for (int st = 0; st < G::RT; ++st) {
+    f32x4 init;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) init[r] = (G::KIND == kFavor) ? -0.5f * kn[16 * st + 4 * g + r] : 0.f;
+#pragma unroll
+    for (int mt = 0; mt < G::MT; ++mt) {
+      f32x4 acc = init;
+#pragma unroll
+      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, frag_rm(Ks, G::LDQ, 16 * st, 32 * kb), Wf[mt][kb]);
+      Lk[st][mt] = acc;
+    }
+  }
+}
+
+template <class G>
+__global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
+  typedef typename G::T T;
+  typedef typename FragT<T>::type F;
+  constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
+                RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDZ = G::LDZ, ZR = G::ZR, LDR = G::LDR;
+  __shared__ __attribute__((aligned(16))) T Qs[TR * LDQ];
+  __shared__ __attribute__((aligned(16))) T Ks[TR * LDQ];
+  __shared__ __attribute__((aligned(16))) T Vs[TR * LDQ];
+  __shared__ __attribute__((aligned(16))) T Zk[4][ZR * LDZ];
+  __shared__ __attribute__((aligned(16))) float Red[4][TR * LDR];
+  __shared__ float qn[TR], kn[TR], qmx[4][TR], kmx[4];
+
+  const int w = wave_id(), g = lane_g(), c = lane_c();
+  const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const size_t head = (size_t)b * a.H + h;
+  const T* Qh = (const T*)a.Q + head * (size_t)a.L * D;
+  const T* Kh = (const T*)a.K + head * (size_t)a.L * D;
+  const T* Vh = (const T*)a.V + head * (size_t)a.L * D;
+  T* Yh = (T*)a.Y + head * (size_t)a.L * D;
+
+  F Wf[MT][EB];
+  load_w_frags<G>(Wf, a.W, w);
+
+  // running state of this wave's features: S[mt][et] rows m, columns e;
+  // S[mt][ET] holds z replicated over its 16 columns
+  f32x4 S[MT][ET + 1];
+  float cur = -INFINITY;  // key shift the state is relative to (FAVOR+)
+  const float* sin = a.seg_state ? a.seg_state + (head * a.P + p) * (size_t)M * (D + 1) : nullptr;
+  if (sin != nullptr) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
+#pragma unroll
+        for (int et = 0; et < ET; ++et) S[mt][et][r] = sin[row + 16 * et + c];
+        S[mt][ET][r] = sin[row + D];
+      }
+    if (G::KIND == kFavor) cur = a.seg_shift[head * a.P + p];
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et) S[mt][et] = zero4();
+  }
+
+  // pad rows of the transposed key buffer stay zero
+  for (int i = FW * LDZ + threadIdx.x % 64; i < ZR * LDZ; i += 64) Zk[w][i] = cvt<T>(0.f);
+
+  const TileMap tm(a.L, a.C, TR);
+  const int n_tiles = tm.count_tiles();
+  const int j0 = (int)((int64_t)p * n_tiles / a.P), j1 = (int)((int64_t)(p + 1) * n_tiles / a.P);
+  const float half_log2M = 0.5f * __log2f((float)M);
+
+  for (int j = j0; j < j1; ++j) {
+    int start, count;
+    tm.tile(j, start, count);
+    load_rows<T, D, TR, LDQ, 256>(Qs, Qh + (size_t)start * D, count, G::KIND == kFavor ? qn : nullptr);
+    load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, G::KIND == kFavor ? kn : nullptr);
+    load_rows<T, D, TR, LDQ, 256>(Vs, Vh + (size_t)start * D, count, nullptr);
+    __syncthreads();
+
+    f32x4 Lq[MT][RT], Lk[RT][MT];
+    query_logits<G>(Lq, Wf, Qs, qn);
+    key_logits<G>(Lk, Wf, Ks, kn);
+
+    if (G::KIND == kFavor) {
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) {
+        float v = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
+        v = wave_max_over_g(v);
+        if (g == 0) qmx[w][16 * tt + c] = v;
+      }
+      float v = -INFINITY;
+#pragma unroll
+      for (int st = 0; st < RT; ++st)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (16 * st + 4 * g + r < count) v = fmaxf(v, Lk[st][mt][r]);
+      v = wave_max(v);
+      if (lane_id() == 0) kmx[w] = v;
+    }
+    __syncthreads();
+
+    if (G::KIND == kFavor) {
+      const float km = fmaxf(fmaxf(kmx[0], kmx[1]), fmaxf(kmx[2], kmx[3]));
+      if (km > cur) {
+        const float sc = fast_exp2((cur - km) * kLog2e);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int et = 0; et <= ET; ++et) S[mt][et] *= sc;
+        cur = km;
+      }
+      const float koff = cur * kLog2e + half_log2M;
+#pragma unroll
+      for (int st = 0; st < RT; ++st)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? fast_exp2(Lk[st][mt][r] * kLog2e - koff) : 0.f;
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) {
+        const int t = 16 * tt + c;
+        const float qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t])) * kLog2e;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) Lq[mt][tt][r] = (t < count) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs) : 0.f;
+      }
+    } else {
+#pragma unroll
+      for (int st = 0; st < RT; ++st)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? fmaxf(Lk[st][mt][r], 0.f) + a.relu_eps : 0.f;
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Lq[mt][tt][r] = (16 * tt + c < count) ? fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps : 0.f;
+    }
+
+    // keys transposed into this wave's buffer: Zk[m][s]
+#pragma unroll
+    for (int st = 0; st < RT; ++st)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
+    __syncthreads();
+
+    F qf[MB][RT];
+#pragma unroll
+    for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt)
+        qf[kb][tt] = (2 * kb + 1 < MT) ? tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt])
+                                       : tile_half_frag<T>(Lq[2 * kb][tt]);
+
+    // scores A^T[s][t] = sum_m K~[s][m] Q~[t][m], causal
+    f32x4 At[RT][RT];
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+      for (int st = 0; st < RT; ++st) {
+        At[st][tt] = zero4();
+        if (st > tt) continue;
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb) At[st][tt] = mma(At[st][tt], frag_tr(Zk[w], LDZ, 32 * kb, 16 * st), qf[kb][tt]);
+        if (st == tt) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (4 * g + r > c) At[st][tt][r] = 0.f;
+        }
+      }
+
+    F vf[RB][ET + 1];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et) vf[rb][et] = v_frag<G>(Vs, 32 * rb, et, count);
+
+    F sf[MB][ET + 1];
+#pragma unroll
+    for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et)
+        sf[kb][et] = (2 * kb + 1 < MT) ? tile_pair_frag<T>(S[2 * kb][et], S[2 * kb + 1][et])
+                                       : tile_half_frag<T>(S[2 * kb][et]);
+
+    // N^T[e][t] over this wave's features, into the reduction buffer as [t][e]
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          if (2 * rb > tt) continue;
+          const F af = (2 * rb + 1 <= tt) ? tile_pair_frag<T>(At[2 * rb][tt], At[2 * rb + 1][tt])
+                                          : tile_half_frag<T>(At[2 * rb][tt]);
+          acc = mma(acc, vf[rb][et], af);
+        }
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sf[kb][et], qf[kb][tt]);
+        if (et < ET) {
+          store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * tt);
+        } else if (g == 0) {
+          Red[w][(16 * tt + c) * LDR + D] = acc[0];
+        }
+      }
+
+    // state update [S|z] += K~^T [V|1]
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          S[mt][et] = mma(S[mt][et], tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]), vf[rb][et]);
+    __syncthreads();
+
+    // Y = N / D over all features
+    {
+      constexpr int TPR = 256 / TR, EPT = D / TPR;
+      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      if (t < count) {
+        const float den = Red[0][t * LDR + D] + Red[1][t * LDR + D] + Red[2][t * LDR + D] + Red[3][t * LDR + D];
+        const float inv = 1.f / den;
+        T y[EPT];
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          const int e = q * EPT + i;
+          const float n = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
+          y[i] = cvt<T>(n * inv);
+        }
+        T* dst = Yh + (size_t)(start + t) * D + q * EPT;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) dst[i] = y[i];
+      }
+    }
+    __syncthreads();
+  }
+
+  // segment end state (segment sums mode) or final state
+  float* sout = nullptr;
+  if (a.seg_sum_out != nullptr) {
+    sout = a.seg_sum_out + (head * a.P + p) * (size_t)M * (D + 1);
+  } else if (p == a.P - 1) {
+    sout = a.state_out;
+    if (sout != nullptr) sout += head * (size_t)M * (D + 1);
+  }
+  if (sout != nullptr) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
+#pragma unroll
+        for (int et = 0; et < ET; ++et) sout[row + 16 * et + c] = S[mt][et][r];
+        if (c == 0) sout[row + D] = S[mt][ET][r];
+      }
+  }
+  if (G::KIND == kFavor && threadIdx.x == 0) {
+    if (a.seg_sum_out != nullptr) {
+      a.seg_shift_out[head * a.P + p] = cur;
+    } else if (p == a.P - 1 && a.kshift_out != nullptr) {
+      a.kshift_out[head] = cur;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Stand-alone feature map.
+
+// per-head key shift: max over rows and features of w_m . k - |k|^2 / 2
+template <class G>
+__global__ __launch_bounds__(256, 1) void key_shift_kernel(FeatArgs a) {
+  typedef typename G::T T;
+  typedef typename FragT<T>::type F;
+  constexpr int D = G::D, TR = G::TR, MT = G::MT, EB = G::EB, RT = G::RT, LDQ = G::LDQ;
+  __shared__ __attribute__((aligned(16))) T Ks[TR * LDQ];
+  __shared__ float kn[TR], kmx[4];
+  const int w = wave_id(), g = lane_g();
+  const size_t head = (size_t)blockIdx.z * a.H + blockIdx.y;
+  const T* Kh = (const T*)a.X + head * (size_t)a.L * D;
+  F Wf[MT][EB];
+  load_w_frags<G>(Wf, a.W, w);
+  float best = -INFINITY;
+  for (int start = 0; start < a.L; start += TR) {
+    const int count = min(TR, a.L - start);
+    load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, kn);
+    __syncthreads();
+    f32x4 Lk[RT][MT];
+    key_logits<G>(Lk, Wf, Ks, kn);
+#pragma unroll
+    for (int st = 0; st < RT; ++st)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (16 * st + 4 * g + r < count) best = fmaxf(best, Lk[st][mt][r]);
+    __syncthreads();
+  }
+  best = wave_max(best);
+  if (lane_id() == 0) kmx[w] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) a.shift[head] = fmaxf(fmaxf(kmx[0], kmx[1]), fmaxf(kmx[2], kmx[3]));
+}
+
+// phi_hat for one tile of TR rows per workgroup
+template <class G>
+__global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
+  typedef typename G::T T;
+  typedef typename FragT<T>::type F;
+  constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, EB = G::EB, RT = G::RT, LDQ = G::LDQ;
+  __shared__ __attribute__((aligned(16))) T Xs[TR * LDQ];
+  __shared__ float xn[TR], qmx[4][TR];
+  const int w = wave_id(), g = lane_g(), c = lane_c();
+  const size_t head = (size_t)blockIdx.z * a.H + blockIdx.y;
+  const int start = blockIdx.x * TR;
+  const int count = min(TR, a.L - start);
+  const T* Xh = (const T*)a.X + head * (size_t)a.L * D;
+  float* Ph = a.phi + head * (size_t)a.L * M;
+  F Wf[MT][EB];
+  load_w_frags<G>(Wf, a.W, w);
+  load_rows<T, D, TR, LDQ, 256>(Xs, Xh + (size_t)start * D, count, G::KIND == kFavor ? xn : nullptr);
+  __syncthreads();
+  const float half_log2M = 0.5f * __log2f((float)M);
+  if (a.role == 0) {
+    f32x4 Lq[MT][RT];
+    query_logits<G>(Lq, Wf, Xs, xn);
+    if (G::KIND == kFavor) {
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) {
+        float v = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
+        v = wave_max_over_g(v);
+        if (g == 0) qmx[w][16 * tt + c] = v;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt) {
+      const int t = 16 * tt + c;
+      if (t >= count) continue;
+      float qs = 0.f;
+      if (G::KIND == kFavor) {
+        qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t]));
+        if (w == 0 && g == 0 && a.shift != nullptr) a.shift[head * a.L + start + t] = qs;
+      }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = w * FW + 16 * mt + 4 * g + r;
+          const float x = Lq[mt][tt][r];
+          Ph[(size_t)(start + t) * M + m] =
+              (G::KIND == kFavor) ? fast_exp2((x - qs) * kLog2e - half_log2M) : fmaxf(x, 0.f) + a.relu_eps;
+        }
+    }
+  } else {
+    f32x4 Lk[RT][MT];
+    key_logits<G>(Lk, Wf, Xs, xn);
+    const float ks = (G::KIND == kFavor) ? a.shift[head] : 0.f;
+#pragma unroll
+    for (int st = 0; st < RT; ++st)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int s = 16 * st + 4 * g + r;
+          if (s >= count) continue;
+          const int m = w * FW + 16 * mt + c;
+          const float x = Lk[st][mt][r];
+          Ph[(size_t)(start + s) * M + m] =
+              (G::KIND == kFavor) ? fast_exp2((x - ks) * kLog2e - half_log2M) : fmaxf(x, 0.f) + a.relu_eps;
+        }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+
+template <class G>
+hipError_t launch_fwd_walk(const FwdArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(fwd_walk_kernel<G>, dim3(a.P, a.H, a.B), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <class G>
+hipError_t launch_featmap(const FeatArgs& a, hipStream_t s) {
+  if (a.role == 1 && G::KIND == kFavor) {
+    hipLaunchKernelGGL(key_shift_kernel<G>, dim3(1, a.H, a.B), dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(featmap_kernel<G>, dim3((a.L + G::TR - 1) / G::TR, a.H, a.B), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+#define SLIM_INST_FWD(T, D, FW, TR, KIND)                                                     \
+  template hipError_t launch_fwd_walk<Cfg<T, D, FW, TR, KIND>>(const FwdArgs&, hipStream_t); \
+  template hipError_t launch_featmap<Cfg<T, D, FW, TR, KIND>>(const FeatArgs&, hipStream_t);
+SLIM_FOR_EACH_CONFIG(SLIM_INST_FWD)
+
+}  // namespace slim

@@ -1,0 +1,215 @@
+"""ctypes binding of libslim.so (include/slim.h) on torch tensors.
+
+Argument marshalling only: every step of the computation runs in the HIP
+library.  torch provides device memory and the current stream.  When the
+library is missing this module raises at import time; there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libslim.so")
+
+SLIM_OK, SLIM_EINVAL, SLIM_EUNSUPPORTED, SLIM_EWORKSPACE, SLIM_EHIP = 0, -1, -2, -3, -4
+FAVOR_PLUS, RELU = 0, 1
+F32, BF16 = 0, 1
+QUERY, KEY = 0, 1
+PHASE_FWD, PHASE_BWD = 0, 1
+
+KINDS = {"favor+": FAVOR_PLUS, "relu": RELU}
+DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
+
+
+class SlimError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"slim status {status}: {msg}")
+        self.status = status
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int64),
+        ("H", ctypes.c_int64),
+        ("L", ctypes.c_int64),
+        ("d", ctypes.c_int32),
+        ("M", ctypes.c_int32),
+        ("C", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("kind", ctypes.c_int32),
+        ("relu_eps", ctypes.c_float),
+    ]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'` "
+            "or `python paper_2012_11346_amd/build.py`"
+        )
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(Problem)
+    vp, fp, i32, sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    lib.slim_workspace_bytes.argtypes = [P, i32]
+    lib.slim_workspace_bytes.restype = sz
+    lib.slim_num_segments.argtypes = [P]
+    lib.slim_num_segments.restype = i32
+    lib.slim_featmap.argtypes = [P, vp, fp, i32, fp, fp, vp]
+    lib.slim_featmap.restype = i32
+    lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, vp, sz, vp]
+    lib.slim_fwd.restype = i32
+    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, fp, vp, fp, vp, vp, vp, fp, fp, vp, sz, vp]
+    lib.slim_bwd.restype = i32
+    lib.slim_status_string.argtypes = [i32]
+    lib.slim_status_string.restype = ctypes.c_char_p
+    lib.slim_last_error.argtypes = []
+    lib.slim_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+LIB = _load()
+
+EXPORTED = (
+    "slim_workspace_bytes",
+    "slim_featmap",
+    "slim_fwd",
+    "slim_bwd",
+    "slim_status_string",
+    "slim_last_error",
+    "slim_num_segments",
+)
+
+
+def _check(status: int):
+    if status != SLIM_OK:
+        raise SlimError(status, LIB.slim_last_error().decode())
+
+
+def problem(B, H, L, d, M, C, dtype=BF16, kind=FAVOR_PLUS, relu_eps=1e-3) -> Problem:
+    if isinstance(dtype, torch.dtype):
+        dtype = DTYPES[dtype]
+    if isinstance(kind, str):
+        kind = KINDS[kind]
+    return Problem(int(B), int(H), int(L), int(d), int(M), int(C), int(dtype), int(kind), float(relu_eps))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _problem_of(Q: torch.Tensor, W: torch.Tensor, C: int, kind, relu_eps: float) -> Problem:
+    if Q.dim() != 4:
+        raise ValueError("Q must be [B, H, L, d]")
+    B, H, L, d = Q.shape
+    return problem(B, H, L, d, W.shape[0], C, DTYPES[Q.dtype], kind, relu_eps)
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def workspace_bytes(p: Problem, phase: int) -> int:
+    n = LIB.slim_workspace_bytes(ctypes.byref(p), int(phase))
+    if n == 0:
+        err = LIB.slim_last_error().decode()
+        if err:
+            raise SlimError(SLIM_EINVAL, err)
+    return int(n)
+
+
+def num_segments(p: Problem) -> int:
+    return int(LIB.slim_num_segments(ctypes.byref(p)))
+
+
+def _workspace(p: Problem, phase: int, device, ws: Optional[torch.Tensor]):
+    n = workspace_bytes(p, phase)
+    if ws is None:
+        ws = torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    elif ws.numel() * ws.element_size() < n:
+        raise ValueError(f"workspace needs {n} bytes")
+    return ws
+
+
+def featmap(X: torch.Tensor, W: torch.Tensor, role: int, kind="favor+", relu_eps: float = 1e-3):
+    """phi_hat [B, H, L, M] float32 and shift (queries [B, H, L], keys [B, H]; None for ReLU)."""
+    p = _problem_of(X, W, 1, kind, relu_eps)
+    _need(X, "X", X.dtype)
+    _need(W, "W", torch.float32, (p.M, p.d))
+    phi = torch.empty((p.B, p.H, p.L, p.M), dtype=torch.float32, device=X.device)
+    shift = None
+    if p.kind == FAVOR_PLUS:
+        shift = torch.empty((p.B, p.H, p.L) if role == QUERY else (p.B, p.H), dtype=torch.float32, device=X.device)
+    _check(LIB.slim_featmap(ctypes.byref(p), _ptr(X), _ptr(W), int(role), _ptr(phi), _ptr(shift), _stream()))
+    return phi, shift
+
+
+def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3, ws=None,
+        Y=None, state_out=None, kshift_out=None):
+    """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None)."""
+    p = _problem_of(Q, W, C, kind, relu_eps)
+    shp = (p.B, p.H, p.L, p.d)
+    for n, t in (("Q", Q), ("K", K), ("V", V)):
+        _need(t, n, Q.dtype, shp)
+    _need(W, "W", torch.float32, (p.M, p.d))
+    sshape = (p.B, p.H, p.M, p.d + 1)
+    if state_in is not None:
+        _need(state_in, "state_in", torch.float32, sshape)
+    if kshift_in is not None:
+        _need(kshift_in, "kshift_in", torch.float32, (p.B, p.H))
+    dev = Q.device
+    Y = torch.empty_like(Q) if Y is None else Y
+    state_out = torch.empty(sshape, dtype=torch.float32, device=dev) if state_out is None else state_out
+    if p.kind == FAVOR_PLUS and kshift_out is None:
+        kshift_out = torch.empty((p.B, p.H), dtype=torch.float32, device=dev)
+    ws = _workspace(p, PHASE_FWD, dev, ws)
+    _check(LIB.slim_fwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
+                        _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ws), ws.numel(), _stream()))
+    return Y, state_out, kshift_out
+
+
+def bwd(Q, K, V, W, dY, C: int, state_out, kshift=None, kind="favor+", state_in=None, kshift_in=None,
+        dstate_out=None, want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None,
+        dW=None):
+    """Backward sweep from the forward's state_out (and kshift_out for FAVOR+).
+
+    Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
+    p = _problem_of(Q, W, C, kind, relu_eps)
+    shp = (p.B, p.H, p.L, p.d)
+    for n, t in (("Q", Q), ("K", K), ("V", V), ("dY", dY)):
+        _need(t, n, Q.dtype, shp)
+    _need(W, "W", torch.float32, (p.M, p.d))
+    sshape = (p.B, p.H, p.M, p.d + 1)
+    _need(state_out, "state_out", torch.float32, sshape)
+    for n, t in (("state_in", state_in), ("dstate_out", dstate_out)):
+        if t is not None:
+            _need(t, n, torch.float32, sshape)
+    for n, t in (("kshift", kshift), ("kshift_in", kshift_in)):
+        if t is not None:
+            _need(t, n, torch.float32, (p.B, p.H))
+    dev = Q.device
+    dQ = torch.empty_like(Q) if dQ is None else dQ
+    dK = torch.empty_like(K) if dK is None else dK
+    dV = torch.empty_like(V) if dV is None else dV
+    dW = torch.empty((p.M, p.d), dtype=torch.float32, device=dev) if dW is None else dW
+    dstate_in = torch.empty(sshape, dtype=torch.float32, device=dev) if want_dstate_in else None
+    ws = _workspace(p, PHASE_BWD, dev, ws)
+    _check(LIB.slim_bwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
+                        _ptr(state_out), _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
+                        _ptr(dW), _ptr(dstate_in), _ptr(ws), ws.numel(), _stream()))
+    return dQ, dK, dV, dW, dstate_in

@@ -13,8 +13,10 @@ on its own):
   ceil(M/d) independent blocks; each block is the orthogonal factor of a
   d x d Gaussian matrix (sign-fixed by diag(R)) whose rows are rescaled to
   the norms of independent N(0, I_d) draws; blocks are stacked and cut to M
-  rows, then stored as float32.  W is an input of the method, so the
-  results do not depend on this choice.
+  rows, then stored as float32.  For bf16 workloads W is rounded to bf16
+  (RNE) like every other input, so the oracle and the kernels see the same
+  features; the kernels consume W at bf16 precision in bf16 mode.  W is an
+  input of the method, so the results do not depend on this choice.
 
 The paper benchmarks random byte strings pushed through a randomly
 initialised model (Sec. 4.1); the per-head Q, K, V of such a model are close
@@ -138,7 +140,10 @@ def make_inputs(
             import torch
 
             W = orthogonal_gaussian_features(wl.M, wl.d, _stream(wl.wid, layer, "W", seed))
-            out["W"] = torch.from_numpy(W.astype(np.float32))
+            Wt = torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32))
+            if wl.dtype == "bf16":
+                Wt = Wt.to(torch.bfloat16).to(torch.float32)
+            out["W"] = Wt
             continue
         scale = 1.0 if name == "dY" else s
         if name in ("Q", "K") and scale_qk is not None:

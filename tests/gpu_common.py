@@ -1,0 +1,42 @@
+"""Helpers shared by the GPU parity tests: device placement, error metrics."""
+
+import numpy as np
+import pytest
+import torch
+
+# max-relative-error bars (error = max|x - ref| / max|ref|, per tensor)
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def dev(t):
+    return t.to("cuda")
+
+
+def host64(t):
+    return t.detach().to("cpu").double().numpy()
+
+
+def max_rel(x, ref) -> float:
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = float(np.max(np.abs(ref)))
+    return float(np.max(np.abs(x - ref)) / (den if den > 0 else 1.0))
+
+
+def l2_rel(x, ref) -> float:
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.linalg.norm(x - ref) / max(np.linalg.norm(ref), 1e-300))
+
+
+def report(name, x, ref, tol):
+    e = max_rel(x, ref)
+    print(f"  {name}: max_rel={e:.3e} l2_rel={l2_rel(x, ref):.3e} (tol {tol:g})", flush=True)
+    assert np.all(np.isfinite(np.asarray(x))), f"{name} has non-finite values"
+    assert e <= tol, f"{name}: max_rel {e:.3e} > {tol:g}"
+    return e

@@ -1,0 +1,79 @@
+"""GPU parity of the backward sweep against the fp64 oracle.
+
+dQ, dK, dV, dW are checked against the analytic gradients of the definition
+(eq. 2); the state cotangent against Algorithm 1 in the oracle.  Bars as in
+test_gpu_forward.py: max-relative error <= 1e-5 (fp32), <= 2e-2 (bf16).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from tests.gpu_common import TOL, dev, host64, need_gpu, report
+from tests.test_gpu_forward import CASES, _inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(x, C, kind, state_in=None, kshift_in=None, dstate_out=None, want_dstate_in=False):
+    from paper_2012_11346_amd import slim
+
+    Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+    Y, st, ks = slim.fwd(Q, K, V, W, C, kind, state_in=state_in, kshift_in=kshift_in)
+    g = slim.bwd(Q, K, V, W, dY, C, st, ks, kind, state_in=state_in, kshift_in=kshift_in, dstate_out=dstate_out,
+                 want_dstate_in=want_dstate_in)
+    torch.cuda.synchronize()
+    return Y, st, ks, g
+
+
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_backward_matches_definition(i):
+    need_gpu()
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[backward] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    _, _, _, (dQ, dK, dV, dW, _) = _run(x, C, kind)
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    tol = TOL[dtype]
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), (dQ, dK, dV, dW), ref):
+        report(n, host64(a), r, tol)
+
+
+@pytest.mark.parametrize("i", [0, 1, 4])
+def test_state_cotangent_and_chaining(i):
+    """Backward of the second half, fed G^(0) into the backward of the first
+    half, equals the backward of the whole sequence; G^(0) matches Algorithm 1."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[chaining] case={name}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    cut = (L // 2) // 16 * 16 + 3
+    tol = TOL[dtype]
+    Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+    half = lambda t, a, b: t[:, :, a:b].contiguous()
+    Y1, st1, ks1 = slim.fwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, C, kind)
+    Y2, st2, ks2 = slim.fwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, C, kind, state_in=st1,
+                            kshift_in=ks1)
+    g2 = slim.bwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, half(dY, cut, L), C, st2, ks2, kind,
+                  state_in=st1, kshift_in=ks1, want_dstate_in=True)
+    g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, st1, ks1, kind,
+                  dstate_out=g2[4])
+    torch.cuda.synchronize()
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    report("dQ (chained)", np.concatenate([host64(g1[0]), host64(g2[0])], axis=2), ref[0], tol)
+    report("dK (chained)", np.concatenate([host64(g1[1]), host64(g2[1])], axis=2), ref[1], tol)
+    report("dV (chained)", np.concatenate([host64(g1[2]), host64(g2[2])], axis=2), ref[2], tol)
+    report("dW (chained)", host64(g1[3]) + host64(g2[3]), ref[3], tol)
+    # G^(0) of the second half, in the oracle's units (true state, no shift)
+    Yo, sto = O.slim_forward(x["Q"][:, :, :cut], x["K"][:, :, :cut], x["V"][:, :, :cut], x["W"], C, kind)
+    st_full = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind)[1]
+    go = O.slim_backward(x["Q"][:, :, cut:], x["K"][:, :, cut:], x["V"][:, :, cut:], x["W"], x["dY"][:, :, cut:], C,
+                         kind, st_full)[4]
+    g0 = host64(g2[4])
+    if kind == "favor+":
+        # dL/d(stored state_in) = dL/d(true state) * exp(kshift_in)
+        g0 = g0 * np.exp(-host64(ks1))[:, :, None, None]
+    report("dstate_in", g0, go, tol)

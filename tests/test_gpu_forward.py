@@ -1,0 +1,136 @@
+"""GPU parity of the feature map and the forward sweep against the fp64 oracle.
+
+Inputs come from the seeded generators in synth/; the oracle consumes the
+same rounded values (bf16 inputs upcast), so the error measures the kernels.
+Bars: max-relative error (max|x - ref| / max|ref| per tensor) <= 1e-5 for fp32
+problems and <= 2e-2 for bf16 problems.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from synth import Workload, make_inputs
+from tests.gpu_common import TOL, dev, host64, need_gpu, report
+
+pytestmark = pytest.mark.gpu
+
+# name, B, H, L, d, M, C, dtype, kind
+CASES = [
+    ("tiny_exact", 1, 1, 256, 32, 64, 32, "f32", "favor+"),
+    ("f32_relu_c7", 1, 2, 100, 32, 64, 7, "f32", "relu"),
+    ("f32_d64_c1", 2, 1, 45, 64, 64, 1, "f32", "favor+"),
+    ("f32_m128_c100", 1, 1, 230, 32, 128, 100, "f32", "favor+"),
+    ("bf16_ragged_c64", 2, 3, 300, 64, 256, 64, "bf16", "favor+"),
+    ("bf16_c100", 1, 2, 250, 64, 256, 100, "bf16", "favor+"),
+    ("bf16_relu_cL", 2, 2, 200, 64, 128, 256, "bf16", "relu"),
+    ("bf16_d32_c3", 1, 2, 130, 32, 64, 3, "bf16", "favor+"),
+]
+
+
+def _inputs(i, B, H, L, d, M, C, dtype, kind, scale_qk=None):
+    wl = Workload(f"case{i}", 100 + i, B, H, L, d, M, (C,), dtype, kind)
+    return make_inputs(wl, scale_qk=scale_qk)
+
+
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_forward_matches_definition(i):
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[forward] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    Y, st, ks = slim.fwd(dev(x["Q"]), dev(x["K"]), dev(x["V"]), dev(x["W"]), C, kind)
+    torch.cuda.synchronize()
+    Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
+    _, stref = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind, within="quadratic")
+    tol = TOL[dtype]
+    report("Y", host64(Y), Yref, tol)
+    st = host64(st)
+    if kind == "favor+":
+        st = st * np.exp(host64(ks))[:, :, None, None]
+    report("state_out", st, stref, tol)
+
+
+@pytest.mark.parametrize("i", [0, 4, 6])
+def test_forward_two_calls_equal_one(i):
+    """state_out and kshift_out of a first call resume the scan exactly."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    Q, K, V, W = (dev(x[k]) for k in ("Q", "K", "V", "W"))
+    cut = (L // 3) // 16 * 16 + 5
+    Y, st, ks = slim.fwd(Q, K, V, W, C, kind)
+    Y1, st1, ks1 = slim.fwd(Q[:, :, :cut].contiguous(), K[:, :, :cut].contiguous(), V[:, :, :cut].contiguous(), W,
+                            C, kind)
+    Y2, st2, ks2 = slim.fwd(Q[:, :, cut:].contiguous(), K[:, :, cut:].contiguous(), V[:, :, cut:].contiguous(), W,
+                            C, kind, state_in=st1, kshift_in=ks1)
+    torch.cuda.synchronize()
+    Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
+    report("Y (two calls)", np.concatenate([host64(Y1), host64(Y2)], axis=2), Yref, TOL[dtype])
+    a, b = host64(st2), host64(st)
+    if kind == "favor+":
+        a = a * np.exp(host64(ks2))[:, :, None, None]
+        b = b * np.exp(host64(ks))[:, :, None, None]
+    report("state_out (two calls)", a, b, TOL[dtype])
+
+
+def test_forward_stress_large_logits():
+    """Q, K scaled by 3: exponents of size ~50; the shifts keep fp32 in range."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    B, H, L, d, M, C = 1, 2, 160, 64, 256, 64
+    x = _inputs(50, B, H, L, d, M, C, "bf16", "favor+", scale_qk=3.0)
+    Y, st, ks = slim.fwd(dev(x["Q"]), dev(x["K"]), dev(x["V"]), dev(x["W"]), C, "favor+")
+    torch.cuda.synchronize()
+    Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], "favor+")
+    report("Y (x3 logits)", host64(Y), Yref, TOL["bf16"])
+
+
+def _logit_bound(X, W, dtype):
+    """Bound on the logit error: bf16 W costs 2^-9 relative per product (plus
+    fp32 rounding); fp32 products cost ~ d ulps."""
+    Xa = np.abs(host64(X))
+    Wa = np.abs(W.double().numpy())
+    s = Xa @ Wa.T
+    if dtype == "bf16":
+        return 2.0 ** -8 * s + 1e-4
+    return 1e-6 * s + 1e-5
+
+
+@pytest.mark.parametrize("i", [0, 1, 4, 6])
+@pytest.mark.parametrize("role", [0, 1])
+def test_feature_map_matches_definition(i, role):
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[featmap] case={name} role={'key' if role else 'query'}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    X = x["Q"] if role == 0 else x["K"]
+    phi, shift = slim.featmap(dev(X), dev(x["W"]), role, kind)
+    torch.cuda.synchronize()
+    ref = O.feature_map(X, x["W"], kind)
+    bound = _logit_bound(X, x["W"], dtype)
+    phi = host64(phi)
+    if kind == "favor+":
+        sh = host64(shift)
+        sh = sh[..., None] if role == 0 else sh[:, :, None, None]
+        # the query shift is the row maximum of the exponent; the key shift the head maximum
+        logits = O.feature_logits(X, x["W"]) - 0.5 * np.sum(host64(X) ** 2, axis=-1, keepdims=True)
+        ref_shift = logits.max(axis=-1) if role == 0 else logits.max(axis=(-1, -2))
+        assert np.max(np.abs(host64(shift) - ref_shift)) <= np.max(bound)
+        keep = phi > 1e-30
+        err = np.abs(np.log(np.where(keep, phi, 1.0)) + sh - np.log(ref))
+        assert np.all(err[keep] <= bound[keep] + 1e-6), float(np.max(err[keep] - bound[keep]))
+        # anything flushed to zero is negligible next to its row maximum
+        assert np.all(ref[~keep] <= np.exp(-60) * np.max(ref))
+    else:
+        assert np.all(np.abs(phi - ref) <= bound)
