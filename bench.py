@@ -153,7 +153,7 @@ def main():
 
     def step(C, b):
         slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
-        slim.bwd(Q, K, V, W, dY, C, b["st"], b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
+        slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
                  dW=b["dW"])
 
     def timed(C, steps, warmup):
@@ -172,7 +172,7 @@ def main():
             ev[i][0].record(stream)
             slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
             ev[i][1].record(stream)
-            slim.bwd(Q, K, V, W, dY, C, b["st"], b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
+            slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
                      dW=b["dW"])
             ev[i][2].record(stream)
         end.record(stream)

@@ -120,8 +120,6 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
 /* Backward sweep of Algorithm 1 (one layer) for the loss
  * sum(dY * Y) + <dstate_out, state_out>.
  *   Q, K, V, W, state_in, kshift_in  as given to slim_fwd
- *   state_out  [B, H, M, d + 1]: B^(N), the state_out slim_fwd returned; the
- *              reverse walk starts from it and downdates slice by slice
  *   kshift     [B, H]: kshift_out of slim_fwd (FAVOR+; ignored for ReLU)
  *   dY         [B, H, L, d] cotangent of Y
  *   dstate_out optional [B, H, M, d + 1]: cotangent G^(N) of state_out (in the
@@ -130,15 +128,17 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
  *   dW         out [M, d] float32, overwritten: summed over heads, rows and the
  *              query and key branches
  *   dstate_in  out, may be NULL: [B, H, M, d + 1] cotangent G^(0) of state_in
- *              (relative to kshift_in); the zero initial state when state_in
- *              is NULL
+ *              (relative to kshift_in; relative to kshift when state_in is NULL)
  *   ws         workspace of at least slim_workspace_bytes(p, SLIM_PHASE_BWD)
- * The key shifts are constants of the computation (stop-gradient); they
- * cancel exactly in Y.  The pass recomputes every slice (Alg. 2); nothing
- * of size O(L) is kept between slim_fwd and slim_bwd. */
+ * The reverse walk starts from B^(N) and downdates it tile by tile (eq. 17).
+ * B^(N) and the states at the segment boundaries are rebuilt here from the
+ * keys and values with the key shift `kshift`, so that each downdate
+ * subtracts exactly the rounded features that were added; nothing of size
+ * O(L) is kept between slim_fwd and slim_bwd.  The key shifts are constants
+ * of the computation (stop-gradient); they cancel exactly in Y. */
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, const float* state_out, const float* kshift,
-             const void* dY, const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
+             const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
+             const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
              void* ws, size_t ws_bytes, void* stream);
 
 /* Static description of a status code. */

@@ -6,6 +6,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
+#include <cstdlib>
 #include <string>
 
 #include "../../include/slim.h"
@@ -57,30 +59,85 @@ int check_problem(const slim_problem* p) {
 
 int clamp_C(const slim_problem* p) { return (int)(p->C > p->L ? p->L : p->C); }
 
-// Segments per head: 1 for now; the walk is sequential per head.
+// Workgroups per device the segment plan aims for: one per compute unit (the
+// walk kernels run one workgroup per CU).
+constexpr int kTargetWorkgroups = 256;
+// Segments shorter than this many tiles are not worth their start-up cost.
+constexpr int kMinTilesPerSegment = 4;
+
+int count_tiles(const slim_problem* p) {
+  return slim::TileMap((int)p->L, clamp_C(p), kTileRows).count_tiles();
+}
+
+// Segments per head.  The walk inside a segment is sequential; segments run
+// in parallel and are stitched together by exact scans of their states.  The
+// count depends on B*H and the device size, not on L once L is long enough,
+// so workspace stays flat in L.  SLIM_SEGMENTS (debugging) forces a count.
 int plan_segments(const slim_problem* p) {
-  (void)p;
-  return 1;
+  const int n_tiles = count_tiles(p);
+  const char* env = getenv("SLIM_SEGMENTS");
+  if (env != nullptr && atoi(env) > 0) return std::max(1, std::min(atoi(env), n_tiles));
+  const int64_t heads = p->B * p->H;
+  int P = (int)((kTargetWorkgroups + heads - 1) / heads);
+  P = std::min(P, std::max(1, n_tiles / kMinTilesPerSegment));
+  return std::max(1, P);
 }
 
 size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
 
-struct FwdWs {
-  size_t bytes;
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// forward workspace: segment sums and shifts, segment starts and shifts
+struct FwdLayout {
+  size_t seg_sum, seg_shift, starts, start_shift, total;
 };
-
-size_t fwd_ws_bytes(const slim_problem* p) {
-  (void)p;
-  return 0;
+FwdLayout fwd_layout(const slim_problem* p, int P) {
+  FwdLayout l{0, 0, 0, 0, 0};
+  if (P <= 1) return l;
+  const size_t n = (size_t)p->B * p->H * P;
+  size_t off = 0;
+  l.seg_sum = off;
+  off += align256(n * state_elems(p) * sizeof(float));
+  l.seg_shift = off;
+  off += align256(n * sizeof(float));
+  l.starts = off;
+  off += align256(n * state_elems(p) * sizeof(float));
+  l.start_shift = off;
+  off += align256(n * sizeof(float));
+  l.total = off;
+  return l;
 }
 
-size_t bwd_ws_bytes(const slim_problem* p, int P) {
-  // dW partials per workgroup
-  const size_t heads = (size_t)p->B * (size_t)p->H;
-  return heads * (size_t)P * (size_t)p->M * (size_t)p->d * sizeof(float);
+// backward workspace: segment sums, segment boundaries, per-segment
+// cotangent contributions and cotangents after each segment, dW partials
+struct BwdLayout {
+  size_t seg_sum, bounds, gc, gend, dw_part, total;
+};
+BwdLayout bwd_layout(const slim_problem* p, int P) {
+  BwdLayout l{0, 0, 0, 0, 0, 0};
+  const size_t heads = (size_t)p->B * p->H;
+  const size_t se = state_elems(p) * sizeof(float);
+  size_t off = 0;
+  l.seg_sum = off;
+  off += align256(heads * P * se);
+  l.bounds = off;
+  off += align256(heads * (P + 1) * se);
+  if (P > 1) {
+    l.gc = off;
+    off += align256(heads * P * se);
+    l.gend = off;
+    off += align256(heads * P * se);
+  }
+  l.dw_part = off;
+  off += align256(heads * P * (size_t)p->M * p->d * sizeof(float));
+  l.total = off;
+  return l;
 }
 
-typedef hipError_t (*fwd_fn)(const slim::FwdArgs&, hipStream_t);
+size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_segments(p)).total; }
+size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
+
+typedef hipError_t (*fwd_fn)(const slim::FwdArgs&, int, hipStream_t);
 typedef hipError_t (*feat_fn)(const slim::FeatArgs&, hipStream_t);
 typedef hipError_t (*bwd_fn)(const slim::BwdArgs&, hipStream_t);
 
@@ -153,7 +210,7 @@ int slim_num_segments(const slim_problem* p) {
 size_t slim_workspace_bytes(const slim_problem* p, int phase) {
   if (check_problem(p) != SLIM_OK) return 0;
   if (phase == SLIM_PHASE_FWD) return fwd_ws_bytes(p);
-  if (phase == SLIM_PHASE_BWD) return bwd_ws_bytes(p, plan_segments(p));
+  if (phase == SLIM_PHASE_BWD) return bwd_ws_bytes(p);
   fail(SLIM_EINVAL, "unknown phase %d", phase);
   return 0;
 }
@@ -191,50 +248,150 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift_out == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift_out");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
-  const size_t need = fwd_ws_bytes(p);
-  if (need > 0 && (ws == nullptr || ws_bytes < need))
-    return fail(SLIM_EWORKSPACE, "forward workspace needs %zu bytes, got %zu", need, ws == nullptr ? 0 : ws_bytes);
   const int P = plan_segments(p);
+  const FwdLayout lay = fwd_layout(p, P);
+  if (lay.total > 0 && (ws == nullptr || ws_bytes < lay.total))
+    return fail(SLIM_EWORKSPACE, "forward workspace needs %zu bytes, got %zu", lay.total, ws == nullptr ? 0 : ws_bytes);
+  const Dispatch dp = dispatch(p);
+  const bool favor = p->kind == SLIM_FAVOR_PLUS;
+  hipStream_t s = (hipStream_t)stream;
+  char* w = (char*)ws;
   slim::FwdArgs a;
   std::memset(&a, 0, sizeof(a));
   a.Q = Q;
   a.K = K;
   a.V = V;
   a.W = W;
-  a.Y = Y;
-  a.state_out = state_out;
-  a.kshift_out = (p->kind == SLIM_FAVOR_PLUS) ? kshift_out : nullptr;
-  a.seg_state = state_in;
-  a.seg_shift = kshift_in;
   a.B = (int)p->B;
   a.H = (int)p->H;
   a.L = (int)p->L;
   a.C = clamp_C(p);
   a.P = P;
   a.relu_eps = p->relu_eps;
-  hipError_t e = dispatch(p).fwd(a, (hipStream_t)stream);
+  hipError_t e = hipSuccess;
+  if (P > 1) {
+    // (1) what each segment adds, with its own running key shift
+    slim::FwdArgs k = a;
+    k.seg_out = (float*)(w + lay.seg_sum);
+    k.seg_shift_out = (float*)(w + lay.seg_shift);
+    e = dp.fwd(k, slim::kWalkSums, s);
+    if (e != hipSuccess) return hip_fail(e, "segment-sum launch");
+    // (2) the exact state each segment starts from
+    slim::ScanArgs sc;
+    std::memset(&sc, 0, sizeof(sc));
+    sc.seg = k.seg_out;
+    sc.seg_shift = favor ? k.seg_shift_out : nullptr;
+    sc.init = state_in;
+    sc.init_shift = favor ? kshift_in : nullptr;
+    sc.out = (float*)(w + lay.starts);
+    sc.out_shift = (float*)(w + lay.start_shift);
+    sc.BH = (int)(p->B * p->H);
+    sc.P = P;
+    sc.SZ = (int)state_elems(p);
+    sc.favor = favor ? 1 : 0;
+    e = slim::launch_scan_fwd(sc, s);
+    if (e != hipSuccess) return hip_fail(e, "segment-scan launch");
+    a.seg_state = sc.out;
+    a.seg_shift = sc.out_shift;
+    a.seg_stride = P;
+  } else {
+    a.seg_state = state_in;
+    a.seg_shift = kshift_in;
+    a.seg_stride = 1;
+  }
+  // (3) the walk proper
+  a.Y = Y;
+  a.state_out = state_out;
+  a.kshift_out = favor ? kshift_out : nullptr;
+  e = dp.fwd(a, slim::kWalkOutputs, s);
   if (e != hipSuccess) return hip_fail(e, "forward launch");
   return ok();
 }
 
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, const float* state_out, const float* kshift,
-             const void* dY, const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
-             void* ws, size_t ws_bytes, void* stream) {
+             const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
+             const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in, void* ws,
+             size_t ws_bytes, void* stream) {
   int st = check_problem(p);
   if (st != SLIM_OK) return st;
   if (Q == nullptr || K == nullptr || V == nullptr || W == nullptr || dY == nullptr || dQ == nullptr ||
       dK == nullptr || dV == nullptr || dW == nullptr)
     return fail(SLIM_EINVAL, "Q, K, V, W, dY, dQ, dK, dV and dW must be non-NULL");
-  if (state_out == nullptr) return fail(SLIM_EINVAL, "state_out (B^(N) from slim_fwd) must be non-NULL");
-  if (p->kind == SLIM_FAVOR_PLUS) {
+  const bool favor = p->kind == SLIM_FAVOR_PLUS;
+  if (favor) {
     if (kshift == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift (kshift_out of slim_fwd)");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
   const int P = plan_segments(p);
-  const size_t need = bwd_ws_bytes(p, P);
-  if (ws == nullptr || ws_bytes < need)
-    return fail(SLIM_EWORKSPACE, "backward workspace needs %zu bytes, got %zu", need, ws == nullptr ? 0 : ws_bytes);
+  const BwdLayout lay = bwd_layout(p, P);
+  if (ws == nullptr || ws_bytes < lay.total)
+    return fail(SLIM_EWORKSPACE, "backward workspace needs %zu bytes, got %zu", lay.total,
+                ws == nullptr ? 0 : ws_bytes);
+  const Dispatch dp = dispatch(p);
+  hipStream_t s = (hipStream_t)stream;
+  char* w = (char*)ws;
+  const int BH = (int)(p->B * p->H);
+  const int SZ = (int)state_elems(p);
+  hipError_t e;
+
+  slim::FwdArgs f;
+  std::memset(&f, 0, sizeof(f));
+  f.Q = Q;
+  f.K = K;
+  f.V = V;
+  f.dY = dY;
+  f.W = W;
+  f.fixed_shift = favor ? kshift : nullptr;
+  f.B = (int)p->B;
+  f.H = (int)p->H;
+  f.L = (int)p->L;
+  f.C = clamp_C(p);
+  f.P = P;
+  f.relu_eps = p->relu_eps;
+
+  // (1) segment sums with the shift the reverse walk uses, so that every
+  //     downdate subtracts exactly the rounded features that were added
+  slim::FwdArgs k = f;
+  k.seg_out = (float*)(w + lay.seg_sum);
+  e = dp.fwd(k, slim::kWalkSums, s);
+  if (e != hipSuccess) return hip_fail(e, "segment-sum launch");
+  // (2) exact states at the segment boundaries
+  slim::ScanArgs sc;
+  std::memset(&sc, 0, sizeof(sc));
+  sc.seg = k.seg_out;
+  sc.init = state_in;
+  sc.init_shift = favor ? kshift_in : nullptr;
+  sc.shift = favor ? kshift : nullptr;
+  sc.out = (float*)(w + lay.bounds);
+  sc.BH = BH;
+  sc.P = P;
+  sc.SZ = SZ;
+  sc.favor = favor ? 1 : 0;
+  e = slim::launch_scan_bwd(sc, s);
+  if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
+  const float* gend = dstate_out;
+  if (P > 1) {
+    // (3) each segment's contribution to the state cotangent, then the
+    //     cotangent after each segment by a reverse scan (eq. 18)
+    slim::FwdArgs gg = f;
+    gg.seg_state = sc.out;
+    gg.seg_stride = P + 1;
+    gg.seg_out = (float*)(w + lay.gc);
+    e = dp.fwd(gg, slim::kWalkGrad, s);
+    if (e != hipSuccess) return hip_fail(e, "cotangent-sum launch");
+    slim::ScanArgs rv;
+    std::memset(&rv, 0, sizeof(rv));
+    rv.seg = gg.seg_out;
+    rv.init = dstate_out;
+    rv.out = (float*)(w + lay.gend);
+    rv.BH = BH;
+    rv.P = P;
+    rv.SZ = SZ;
+    e = slim::launch_scan_rev(rv, s);
+    if (e != hipSuccess) return hip_fail(e, "cotangent-scan launch");
+    gend = rv.out;
+  }
+  // (4) the reverse walk
   slim::BwdArgs a;
   std::memset(&a, 0, sizeof(a));
   a.Q = Q;
@@ -242,16 +399,15 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.V = V;
   a.dY = dY;
   a.W = W;
-  a.kshift = (p->kind == SLIM_FAVOR_PLUS) ? kshift : nullptr;
-  a.seg_start = state_in;
-  a.start_shift = (p->kind == SLIM_FAVOR_PLUS) ? kshift_in : nullptr;
-  a.seg_end = state_out;
-  a.seg_gend = dstate_out;
-  a.seg_gstart = dstate_in;
+  a.kshift = favor ? kshift : nullptr;
+  a.bounds = sc.out;
+  a.seg_gend = gend;
+  a.init_shift = favor ? kshift_in : nullptr;
+  a.dstate_in = dstate_in;
   a.dQ = dQ;
   a.dK = dK;
   a.dV = dV;
-  a.dW_part = (float*)ws;
+  a.dW_part = (float*)(w + lay.dw_part);
   a.dW = dW;
   a.B = (int)p->B;
   a.H = (int)p->H;
@@ -259,7 +415,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.C = clamp_C(p);
   a.P = P;
   a.relu_eps = p->relu_eps;
-  hipError_t e = dispatch(p).bwd(a, (hipStream_t)stream);
+  e = dp.bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "backward launch");
   return ok();
 }

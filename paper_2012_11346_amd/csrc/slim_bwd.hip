@@ -106,25 +106,27 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   F WT[MB][ET];
   load_wt_frags<G>(WT, a.W, w);
 
-  const size_t sidx = (head * a.P + p) * (size_t)M * (D + 1);
-  // start-state scale: the segment-start state may be relative to another key shift
+  const size_t SZ = (size_t)M * (D + 1);
+  const size_t sidx = (head * a.P + p) * SZ;                 // per-segment arrays
+  const float* bstart = a.bounds + (head * (a.P + 1) + p) * SZ;  // state before the segment
+  const float* bend = bstart + SZ;                            // state after the segment
+  // dstate_in is relative to the caller's initial key shift
   float r0 = 1.f;
-  if (G::KIND == kFavor && a.seg_start != nullptr && a.start_shift != nullptr)
-    r0 = fast_exp2((a.start_shift[head * a.P + p] - a.kshift[head]) * kLog2e);
+  if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
   f32x4 S[MT][ET + 1], Gs[MT][ET + 1], dWacc[MT][ET];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const size_t row = sidx + (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
+      const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
 #pragma unroll
       for (int et = 0; et < ET; ++et) {
-        S[mt][et][r] = a.seg_end[row + 16 * et + c];
-        Gs[mt][et][r] = a.seg_gend ? a.seg_gend[row + 16 * et + c] : 0.f;
+        S[mt][et][r] = bend[row + 16 * et + c];
+        Gs[mt][et][r] = a.seg_gend ? a.seg_gend[sidx + row + 16 * et + c] : 0.f;
       }
-      S[mt][ET][r] = a.seg_end[row + D];
-      Gs[mt][ET][r] = a.seg_gend ? a.seg_gend[row + D] : 0.f;
+      S[mt][ET][r] = bend[row + D];
+      Gs[mt][ET][r] = a.seg_gend ? a.seg_gend[sidx + row + D] : 0.f;
     }
 #pragma unroll
     for (int et = 0; et < ET; ++et) dWacc[mt][et] = zero4();
@@ -229,14 +231,15 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 
     // ---- b1: state before the tile
     if (j == j0) {
+      // the exact state before the segment replaces the downdated one
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const size_t row = sidx + (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
+          const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
 #pragma unroll
-          for (int et = 0; et < ET; ++et) S[mt][et][r] = a.seg_start ? r0 * a.seg_start[row + 16 * et + c] : 0.f;
-          S[mt][ET][r] = a.seg_start ? r0 * a.seg_start[row + D] : 0.f;
+          for (int et = 0; et < ET; ++et) S[mt][et][r] = bstart[row + 16 * et + c];
+          S[mt][ET][r] = bstart[row + D];
         }
     } else {
 #pragma unroll
@@ -605,16 +608,17 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     for (int et = 0; et < ET; ++et)
 #pragma unroll
       for (int r = 0; r < 4; ++r) dwp[(size_t)(w * FW + 16 * mt + 4 * g + r) * D + 16 * et + c] = dWacc[mt][et][r];
-  // state cotangent at the segment start
-  if (a.seg_gstart != nullptr) {
+  // state cotangent before the sequence
+  if (p == 0 && a.dstate_in != nullptr) {
+    float* gout = a.dstate_in + head * SZ;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const size_t row = sidx + (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
+        const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
 #pragma unroll
-        for (int et = 0; et < ET; ++et) a.seg_gstart[row + 16 * et + c] = r0 * Gs[mt][et][r];
-        if (c == 0) a.seg_gstart[row + D] = r0 * Gs[mt][ET][r];
+        for (int et = 0; et < ET; ++et) gout[row + 16 * et + c] = r0 * Gs[mt][et][r];
+        if (c == 0) gout[row + D] = r0 * Gs[mt][ET][r];
       }
   }
 }

@@ -88,17 +88,26 @@ __device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
   }
 }
 
-template <class G>
+// MODE kWalkOutputs: Y and the final state; kWalkSums: only the keys, the
+// state each segment adds; kWalkGrad: the per-segment sum of Q~^T [dN|dD]
+// (needs dY), i.e. what the segment contributes to the state cotangent of
+// the segments before it (eq. 18 accumulated over the segment).
+template <class G, int MODE>
 __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
-                RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDZ = G::LDZ, ZR = G::ZR, LDR = G::LDR;
-  __shared__ __attribute__((aligned(16))) T Qs[TR * LDQ];
+                RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDZ = G::LDZ, ZR = G::ZR, LDR = G::LDR, LDF = G::LDF;
+  constexpr bool QSIDE = MODE != kWalkSums;
+  constexpr bool GRAD = MODE == kWalkGrad;
+  __shared__ __attribute__((aligned(16))) T Qs[QSIDE ? TR * LDQ : 8];
   __shared__ __attribute__((aligned(16))) T Ks[TR * LDQ];
   __shared__ __attribute__((aligned(16))) T Vs[TR * LDQ];
-  __shared__ __attribute__((aligned(16))) T Zk[4][ZR * LDZ];
-  __shared__ __attribute__((aligned(16))) float Red[4][TR * LDR];
+  __shared__ __attribute__((aligned(16))) T Zk[4][QSIDE ? ZR * LDZ : 8];
+  __shared__ __attribute__((aligned(16))) float Red[4][QSIDE ? TR * LDR : 4];
+  __shared__ __attribute__((aligned(16))) T dNs[GRAD ? TR * LDQ : 8];
+  __shared__ __attribute__((aligned(16))) T Zq[4][GRAD ? TR * LDF : 8];
+  __shared__ __attribute__((aligned(16))) T dDb[GRAD ? TR + 8 : 8];
   __shared__ float qn[TR], kn[TR], qmx[4][TR], kmx[4];
 
   const int w = wave_id(), g = lane_g(), c = lane_c();
@@ -107,7 +116,6 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   const T* Qh = (const T*)a.Q + head * (size_t)a.L * D;
   const T* Kh = (const T*)a.K + head * (size_t)a.L * D;
   const T* Vh = (const T*)a.V + head * (size_t)a.L * D;
-  T* Yh = (T*)a.Y + head * (size_t)a.L * D;
 
   F Wf[MT][EB];
   load_w_frags<G>(Wf, a.W, w);
@@ -116,7 +124,10 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   // S[mt][ET] holds z replicated over its 16 columns
   f32x4 S[MT][ET + 1];
   float cur = -INFINITY;  // key shift the state is relative to (FAVOR+)
-  const float* sin = a.seg_state ? a.seg_state + (head * a.P + p) * (size_t)M * (D + 1) : nullptr;
+  const bool fixed = a.fixed_shift != nullptr;
+  if (G::KIND == kFavor && fixed) cur = a.fixed_shift[head];
+  const size_t sidx = (head * a.P + p) * (size_t)M * (D + 1);
+  const float* sin = a.seg_state ? a.seg_state + (head * a.seg_stride + p) * (size_t)M * (D + 1) : nullptr;
   if (sin != nullptr) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -127,67 +138,82 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
         for (int et = 0; et < ET; ++et) S[mt][et][r] = sin[row + 16 * et + c];
         S[mt][ET][r] = sin[row + D];
       }
-    if (G::KIND == kFavor) cur = a.seg_shift[head * a.P + p];
+    if (G::KIND == kFavor && !fixed) cur = a.seg_shift[head * a.P + p];
   } else {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int et = 0; et <= ET; ++et) S[mt][et] = zero4();
   }
+  f32x4 Gs[GRAD ? MT : 1][ET + 1];
+  if constexpr (GRAD) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et) Gs[mt][et] = zero4();
+  }
 
   // pad rows of the transposed key buffer stay zero
-  for (int i = FW * LDZ + threadIdx.x % 64; i < ZR * LDZ; i += 64) Zk[w][i] = cvt<T>(0.f);
+  if constexpr (QSIDE)
+    for (int i = FW * LDZ + lane_id(); i < ZR * LDZ; i += 64) Zk[w][i] = cvt<T>(0.f);
 
   const TileMap tm(a.L, a.C, TR);
   const int n_tiles = tm.count_tiles();
   const int j0 = (int)((int64_t)p * n_tiles / a.P), j1 = (int)((int64_t)(p + 1) * n_tiles / a.P);
   const float half_log2M = 0.5f * __log2f((float)M);
+  constexpr int TPR = 256 / TR, EPT = D / TPR;
 
   for (int j = j0; j < j1; ++j) {
     int start, count;
     tm.tile(j, start, count);
-    load_rows<T, D, TR, LDQ, 256>(Qs, Qh + (size_t)start * D, count, G::KIND == kFavor ? qn : nullptr);
+    if constexpr (QSIDE) load_rows<T, D, TR, LDQ, 256>(Qs, Qh + (size_t)start * D, count, G::KIND == kFavor ? qn : nullptr);
     load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, G::KIND == kFavor ? kn : nullptr);
     load_rows<T, D, TR, LDQ, 256>(Vs, Vh + (size_t)start * D, count, nullptr);
     __syncthreads();
 
-    f32x4 Lq[MT][RT], Lk[RT][MT];
-    query_logits<G>(Lq, Wf, Qs, qn);
+    f32x4 Lq[QSIDE ? MT : 1][RT], Lk[RT][MT];
+    if constexpr (QSIDE) query_logits<G>(Lq, Wf, Qs, qn);
     key_logits<G>(Lk, Wf, Ks, kn);
 
     if (G::KIND == kFavor) {
+      if constexpr (QSIDE) {
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) {
+        for (int tt = 0; tt < RT; ++tt) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
+          v = wave_max_over_g(v);
+          if (g == 0) qmx[w][16 * tt + c] = v;
+        }
+      }
+      if (!fixed) {
         float v = -INFINITY;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int st = 0; st < RT; ++st)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
-        v = wave_max_over_g(v);
-        if (g == 0) qmx[w][16 * tt + c] = v;
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (16 * st + 4 * g + r < count) v = fmaxf(v, Lk[st][mt][r]);
+        v = wave_max(v);
+        if (lane_id() == 0) kmx[w] = v;
       }
-      float v = -INFINITY;
-#pragma unroll
-      for (int st = 0; st < RT; ++st)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (16 * st + 4 * g + r < count) v = fmaxf(v, Lk[st][mt][r]);
-      v = wave_max(v);
-      if (lane_id() == 0) kmx[w] = v;
     }
     __syncthreads();
 
     if (G::KIND == kFavor) {
-      const float km = fmaxf(fmaxf(kmx[0], kmx[1]), fmaxf(kmx[2], kmx[3]));
-      if (km > cur) {
-        const float sc = fast_exp2((cur - km) * kLog2e);
+      if (!fixed) {
+        const float km = fmaxf(fmaxf(kmx[0], kmx[1]), fmaxf(kmx[2], kmx[3]));
+        if (km > cur) {
+          const float sc = fast_exp2((cur - km) * kLog2e);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+          for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int et = 0; et <= ET; ++et) S[mt][et] *= sc;
-        cur = km;
+            for (int et = 0; et <= ET; ++et) S[mt][et] *= sc;
+          cur = km;
+        }
       }
       const float koff = cur * kLog2e + half_log2M;
 #pragma unroll
@@ -197,14 +223,17 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? fast_exp2(Lk[st][mt][r] * kLog2e - koff) : 0.f;
+      if constexpr (QSIDE) {
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) {
-        const int t = 16 * tt + c;
-        const float qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t])) * kLog2e;
+        for (int tt = 0; tt < RT; ++tt) {
+          const int t = 16 * tt + c;
+          const float qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t])) * kLog2e;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+          for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) Lq[mt][tt][r] = (t < count) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs) : 0.f;
+            for (int r = 0; r < 4; ++r)
+              Lq[mt][tt][r] = (t < count) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs) : 0.f;
+        }
       }
     } else {
 #pragma unroll
@@ -214,46 +243,16 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? fmaxf(Lk[st][mt][r], 0.f) + a.relu_eps : 0.f;
+      if constexpr (QSIDE) {
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt)
+        for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+          for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            Lq[mt][tt][r] = (16 * tt + c < count) ? fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps : 0.f;
-    }
-
-    // keys transposed into this wave's buffer: Zk[m][s]
-#pragma unroll
-    for (int st = 0; st < RT; ++st)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
-    __syncthreads();
-
-    F qf[MB][RT];
-#pragma unroll
-    for (int kb = 0; kb < MB; ++kb)
-#pragma unroll
-      for (int tt = 0; tt < RT; ++tt)
-        qf[kb][tt] = (2 * kb + 1 < MT) ? tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt])
-                                       : tile_half_frag<T>(Lq[2 * kb][tt]);
-
-    // scores A^T[s][t] = sum_m K~[s][m] Q~[t][m], causal
-    f32x4 At[RT][RT];
-#pragma unroll
-    for (int tt = 0; tt < RT; ++tt)
-#pragma unroll
-      for (int st = 0; st < RT; ++st) {
-        At[st][tt] = zero4();
-        if (st > tt) continue;
-#pragma unroll
-        for (int kb = 0; kb < MB; ++kb) At[st][tt] = mma(At[st][tt], frag_tr(Zk[w], LDZ, 32 * kb, 16 * st), qf[kb][tt]);
-        if (st == tt) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (4 * g + r > c) At[st][tt][r] = 0.f;
-        }
+            for (int r = 0; r < 4; ++r)
+              Lq[mt][tt][r] = (16 * tt + c < count) ? fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps : 0.f;
       }
+    }
 
     F vf[RB][ET + 1];
 #pragma unroll
@@ -261,35 +260,77 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
       for (int et = 0; et <= ET; ++et) vf[rb][et] = v_frag<G>(Vs, 32 * rb, et, count);
 
-    F sf[MB][ET + 1];
+    if constexpr (QSIDE) {
+      // keys transposed into this wave's buffer: Zk[m][s]
 #pragma unroll
-    for (int kb = 0; kb < MB; ++kb)
+      for (int st = 0; st < RT; ++st)
 #pragma unroll
-      for (int et = 0; et <= ET; ++et)
-        sf[kb][et] = (2 * kb + 1 < MT) ? tile_pair_frag<T>(S[2 * kb][et], S[2 * kb + 1][et])
-                                       : tile_half_frag<T>(S[2 * kb][et]);
-
-    // N^T[e][t] over this wave's features, into the reduction buffer as [t][e]
+        for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
+      if constexpr (GRAD) {
+        // Q~ as [t][m] for the cotangent update
 #pragma unroll
-    for (int tt = 0; tt < RT; ++tt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int et = 0; et <= ET; ++et) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          if (2 * rb > tt) continue;
-          const F af = (2 * rb + 1 <= tt) ? tile_pair_frag<T>(At[2 * rb][tt], At[2 * rb + 1][tt])
-                                          : tile_half_frag<T>(At[2 * rb][tt]);
-          acc = mma(acc, vf[rb][et], af);
-        }
-#pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sf[kb][et], qf[kb][tt]);
-        if (et < ET) {
-          store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * tt);
-        } else if (g == 0) {
-          Red[w][(16 * tt + c) * LDR + D] = acc[0];
-        }
+          for (int tt = 0; tt < RT; ++tt) store_tile_T<T>(Zq[w], LDF, Lq[mt][tt], 16 * mt, 16 * tt);
       }
+      __syncthreads();
+
+      F qf[MB][RT];
+#pragma unroll
+      for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt)
+          qf[kb][tt] = (2 * kb + 1 < MT) ? tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt])
+                                         : tile_half_frag<T>(Lq[2 * kb][tt]);
+
+      // scores A^T[s][t] = sum_m K~[s][m] Q~[t][m], causal
+      f32x4 At[RT][RT];
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+        for (int st = 0; st < RT; ++st) {
+          At[st][tt] = zero4();
+          if (st > tt) continue;
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb)
+            At[st][tt] = mma(At[st][tt], frag_tr(Zk[w], LDZ, 32 * kb, 16 * st), qf[kb][tt]);
+          if (st == tt) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (4 * g + r > c) At[st][tt][r] = 0.f;
+          }
+        }
+
+      F sf[MB][ET + 1];
+#pragma unroll
+      for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+        for (int et = 0; et <= ET; ++et)
+          sf[kb][et] = (2 * kb + 1 < MT) ? tile_pair_frag<T>(S[2 * kb][et], S[2 * kb + 1][et])
+                                         : tile_half_frag<T>(S[2 * kb][et]);
+
+      // N^T[e][t] over this wave's features, into the reduction buffer as [t][e]
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+        for (int et = 0; et <= ET; ++et) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            if (2 * rb > tt) continue;
+            const F af = (2 * rb + 1 <= tt) ? tile_pair_frag<T>(At[2 * rb][tt], At[2 * rb + 1][tt])
+                                            : tile_half_frag<T>(At[2 * rb][tt]);
+            acc = mma(acc, vf[rb][et], af);
+          }
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sf[kb][et], qf[kb][tt]);
+          if (et < ET) {
+            store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * tt);
+          } else if (g == 0) {
+            Red[w][(16 * tt + c) * LDR + D] = acc[0];
+          }
+        }
+    }
 
     // state update [S|z] += K~^T [V|1]
 #pragma unroll
@@ -299,37 +340,71 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
           S[mt][et] = mma(S[mt][et], tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]), vf[rb][et]);
-    __syncthreads();
 
-    // Y = N / D over all features
-    {
-      constexpr int TPR = 256 / TR, EPT = D / TPR;
+    if constexpr (QSIDE) {
+      __syncthreads();
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
-      if (t < count) {
-        const float den = Red[0][t * LDR + D] + Red[1][t * LDR + D] + Red[2][t * LDR + D] + Red[3][t * LDR + D];
-        const float inv = 1.f / den;
-        T y[EPT];
+      const bool ok = t < count;
+      const float den = Red[0][t * LDR + D] + Red[1][t * LDR + D] + Red[2][t * LDR + D] + Red[3][t * LDR + D];
+      const float inv = ok ? 1.f / den : 0.f;
+      if constexpr (!GRAD) {
+        // Y = N / D over all features
+        if (ok) {
+          T* dst = (T*)a.Y + head * (size_t)a.L * D + (size_t)(start + t) * D + q * EPT;
+#pragma unroll
+          for (int i = 0; i < EPT; ++i) {
+            const int e = q * EPT + i;
+            const float n = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
+            dst[i] = cvt<T>(n * inv);
+          }
+        }
+      } else {
+        // dN = dY / D, dD = -(dY . Y) / D
+        const T* dYh = (const T*)a.dY + head * (size_t)a.L * D;
+        float dy[EPT];
+        float dot = 0.f;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
+          dy[i] = ok ? to_f32(dYh[(size_t)(start + t) * D + e]) : 0.f;
           const float n = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-          y[i] = cvt<T>(n * inv);
+          dot += dy[i] * (n * inv);
         }
-        T* dst = Yh + (size_t)(start + t) * D + q * EPT;
 #pragma unroll
-        for (int i = 0; i < EPT; ++i) dst[i] = y[i];
+        for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * inv);
+        if (q == 0) dDb[t] = cvt<T>(ok ? -dot * inv : 0.f);
+      }
+      __syncthreads();
+      if constexpr (GRAD) {
+        // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e]
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int et = 0; et <= ET; ++et)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+              F bfr;
+              if (et < ET) {
+                bfr = frag_tr(dNs, LDQ, 32 * rb, 16 * et);
+              } else {
+#pragma unroll
+                for (int s = 0; s < 8; ++s) bfr[s] = dDb[32 * rb + kp(g, s)];
+              }
+              Gs[mt][et] = mma(Gs[mt][et], frag_tr(Zq[w], LDF, 32 * rb, 16 * mt), bfr);
+            }
       }
     }
     __syncthreads();
   }
 
-  // segment end state (segment sums mode) or final state
+  // outputs of the segment
   float* sout = nullptr;
-  if (a.seg_sum_out != nullptr) {
-    sout = a.seg_sum_out + (head * a.P + p) * (size_t)M * (D + 1);
-  } else if (p == a.P - 1) {
-    sout = a.state_out;
-    if (sout != nullptr) sout += head * (size_t)M * (D + 1);
+  if (MODE == kWalkOutputs) {
+    if (p == a.P - 1 && a.state_out != nullptr) sout = a.state_out + head * (size_t)M * (D + 1);
+  } else {
+    sout = a.seg_out + sidx;
   }
   if (sout != nullptr) {
 #pragma unroll
@@ -338,16 +413,13 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
 #pragma unroll
-        for (int et = 0; et < ET; ++et) sout[row + 16 * et + c] = S[mt][et][r];
-        if (c == 0) sout[row + D] = S[mt][ET][r];
+        for (int et = 0; et < ET; ++et) sout[row + 16 * et + c] = GRAD ? Gs[mt][et][r] : S[mt][et][r];
+        if (c == 0) sout[row + D] = GRAD ? Gs[mt][ET][r] : S[mt][ET][r];
       }
   }
   if (G::KIND == kFavor && threadIdx.x == 0) {
-    if (a.seg_sum_out != nullptr) {
-      a.seg_shift_out[head * a.P + p] = cur;
-    } else if (p == a.P - 1 && a.kshift_out != nullptr) {
-      a.kshift_out[head] = cur;
-    }
+    if (MODE == kWalkSums && a.seg_shift_out != nullptr) a.seg_shift_out[head * a.P + p] = cur;
+    if (MODE == kWalkOutputs && p == a.P - 1 && a.kshift_out != nullptr) a.kshift_out[head] = cur;
   }
 }
 
@@ -467,8 +539,15 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
 // launchers
 
 template <class G>
-hipError_t launch_fwd_walk(const FwdArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(fwd_walk_kernel<G>, dim3(a.P, a.H, a.B), dim3(256), 0, s, a);
+hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s) {
+  const dim3 grid(a.P, a.H, a.B);
+  if (mode == kWalkOutputs) {
+    hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkOutputs>), grid, dim3(256), 0, s, a);
+  } else if (mode == kWalkSums) {
+    hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkSums>), grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkGrad>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -484,7 +563,7 @@ hipError_t launch_featmap(const FeatArgs& a, hipStream_t s) {
 }
 
 #define SLIM_INST_FWD(T, D, FW, TR, KIND)                                                     \
-  template hipError_t launch_fwd_walk<Cfg<T, D, FW, TR, KIND>>(const FwdArgs&, hipStream_t); \
+  template hipError_t launch_fwd_walk<Cfg<T, D, FW, TR, KIND>>(const FwdArgs&, int, hipStream_t); \
   template hipError_t launch_featmap<Cfg<T, D, FW, TR, KIND>>(const FeatArgs&, hipStream_t);
 SLIM_FOR_EACH_CONFIG(SLIM_INST_FWD)
 

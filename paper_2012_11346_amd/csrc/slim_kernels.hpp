@@ -7,20 +7,41 @@
 
 namespace slim {
 
+// Walk modes of the forward kernel
+enum WalkMode {
+  kWalkOutputs = 0,  // Y and the final state (forward sweep)
+  kWalkSums = 1,     // keys only: the state each segment adds (segment sums)
+  kWalkGrad = 2,     // per-segment sum of Q~^T [dN|dD] (state-cotangent contributions)
+};
+
 struct FwdArgs {
   const void* Q;
   const void* K;
   const void* V;
+  const void* dY;           // kWalkGrad
   const float* W;
-  void* Y;                 // nullptr: segment-sum mode (no outputs, only seg_sum_out)
-  float* state_out;        // [B,H,M,D+1] or nullptr
-  float* kshift_out;       // [B,H] or nullptr
-  const float* seg_state;  // [B,H,P,M,D+1] state each segment starts from, or nullptr (zero)
-  const float* seg_shift;  // [B,H,P] key shift of seg_state
-  float* seg_sum_out;      // segment-sum mode: [B,H,P,M,D+1] state after the segment
-  float* seg_shift_out;    // segment-sum mode: [B,H,P]
+  void* Y;                  // kWalkOutputs
+  float* state_out;         // kWalkOutputs: [B,H,M,D+1] or nullptr (written by the last segment)
+  float* kshift_out;        // kWalkOutputs: [B,H] or nullptr
+  const float* seg_state;   // [B,H,seg_stride,M,D+1] state each segment starts from, or nullptr (zero)
+  int seg_stride;           // states per head in seg_state (P, or P + 1 for segment boundaries)
+  const float* seg_shift;   // [B,H,P] key shift of seg_state (FAVOR+)
+  const float* fixed_shift; // [B,H] key shift used throughout (no online rescaling), or nullptr
+  float* seg_out;           // kWalkSums / kWalkGrad: [B,H,P,M,D+1]
+  float* seg_shift_out;     // kWalkSums: [B,H,P]
   int B, H, L, C, P;
   float relu_eps;
+};
+
+struct ScanArgs {
+  const float* seg;        // [B,H,P,M,D+1] per-segment sums
+  const float* seg_shift;  // [B,H,P] their key shifts (forward), or nullptr (common shift)
+  const float* init;       // [B,H,M,D+1] state before the first segment, or nullptr (zero)
+  const float* init_shift; // [B,H] key shift of init (forward) / of init relative to `shift` (backward)
+  const float* shift;      // [B,H] common key shift (backward), or nullptr
+  float* out;              // forward: [B,H,P,...] segment starts; backward: [B,H,P+1,...] boundaries
+  float* out_shift;        // forward: [B,H,P]
+  int BH, P, SZ, favor;
 };
 
 struct FeatArgs {
@@ -38,24 +59,28 @@ struct BwdArgs {
   const void* V;
   const void* dY;
   const float* W;
-  const float* kshift;      // [B,H] (FAVOR+)
-  const float* seg_start;   // [B,H,P,M,D+1] exact state at each segment start (nullptr: zero)
-  const float* start_shift; // [B,H,P] key shift seg_start is relative to (nullptr: kshift)
-  const float* seg_end;     // [B,H,P,M,D+1] state at each segment end
-  const float* seg_gend;    // [B,H,P,M,D+1] state cotangent at each segment end (nullptr: zero)
-  float* seg_gstart;        // [B,H,P,M,D+1] state cotangent at each segment start (out), or nullptr
+  const float* kshift;      // [B,H] key shift of every state below (FAVOR+)
+  const float* bounds;      // [B,H,P+1,M,D+1] exact state at each segment boundary
+  const float* seg_gend;    // [B,H,P,M,D+1] state cotangent after each segment
+  const float* init_shift;  // [B,H] key shift of the caller's initial state (scales dstate_in), or nullptr
+  float* dstate_in;         // [B,H,M,D+1] state cotangent before the sequence (written by segment 0), or nullptr
   void* dQ;
   void* dK;
   void* dV;
   float* dW_part;           // [B,H,P,M,D] per-workgroup partial dW
   float* dW;                // [M,D] sum of the partials
-  float* gsum_out;          // G-contribution mode: [B,H,P,M,D+1] sum over the segment of Q~^T [dN|dD]
   int B, H, L, C, P;
   float relu_eps;
 };
 
 template <class G>
-hipError_t launch_fwd_walk(const FwdArgs& a, hipStream_t s);
+hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s);
+// exclusive scan of segment states (forward: with key-shift rescaling)
+hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s);
+// inclusive boundaries of segment states under one common shift (backward)
+hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s);
+// reverse scan of state cotangents: out[p] = init + sum_{q > p} seg[q]
+hipError_t launch_scan_rev(const ScanArgs& a, hipStream_t s);
 template <class G>
 hipError_t launch_featmap(const FeatArgs& a, hipStream_t s);
 template <class G>

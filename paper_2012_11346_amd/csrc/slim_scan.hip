@@ -1,0 +1,80 @@
+// Scans over segment states: the sequence of each head is split into P
+// segments walked in parallel; these kernels turn per-segment sums into the
+// exact state each segment starts from (forward and backward) and into the
+// state cotangent each segment ends with (backward).  One workgroup per head,
+// threads over the M (d + 1) state entries, segments in order.
+#include "slim_common.hpp"
+#include "slim_kernels.hpp"
+
+namespace slim {
+
+// out[p] = state before segment p, with key shift out_shift[p]:
+//   s_0 = init (shift init_shift) or zero; s_{p+1} = s_p (+) seg_p, where (+)
+//   brings both operands to the larger shift before adding.
+__global__ __launch_bounds__(256) void scan_fwd_kernel(ScanArgs a) {
+  const int head = blockIdx.x;
+  const size_t SZ = a.SZ;
+  for (int el = threadIdx.x; el < a.SZ; el += 256) {
+    float v = a.init ? a.init[head * SZ + el] : 0.f;
+    float vs = a.favor ? (a.init ? a.init_shift[head] : -INFINITY) : 0.f;
+    for (int p = 0; p < a.P; ++p) {
+      const size_t idx = ((size_t)head * a.P + p) * SZ + el;
+      a.out[idx] = v;
+      if (a.favor) {
+        if (el == 0) a.out_shift[(size_t)head * a.P + p] = vs;
+        const float ss = a.seg_shift[(size_t)head * a.P + p];
+        const float m = fmaxf(vs, ss);
+        v = v * fast_exp2((vs - m) * kLog2e) + a.seg[idx] * fast_exp2((ss - m) * kLog2e);
+        vs = m;
+      } else {
+        v += a.seg[idx];
+      }
+    }
+  }
+}
+
+// out[p] for p = 0..P: state at the boundary before segment p (p = P: after the
+// last one), all relative to the common shift; init is relative to init_shift.
+__global__ __launch_bounds__(256) void scan_bwd_kernel(ScanArgs a) {
+  const int head = blockIdx.x;
+  const size_t SZ = a.SZ;
+  float r0 = 1.f;
+  if (a.favor && a.init != nullptr) r0 = fast_exp2((a.init_shift[head] - a.shift[head]) * kLog2e);
+  for (int el = threadIdx.x; el < a.SZ; el += 256) {
+    float v = a.init ? r0 * a.init[head * SZ + el] : 0.f;
+    for (int p = 0; p < a.P; ++p) {
+      a.out[((size_t)head * (a.P + 1) + p) * SZ + el] = v;
+      v += a.seg[((size_t)head * a.P + p) * SZ + el];
+    }
+    a.out[((size_t)head * (a.P + 1) + a.P) * SZ + el] = v;
+  }
+}
+
+// out[p] = init + sum_{q > p} seg[q]: the state cotangent after segment p
+__global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
+  const int head = blockIdx.x;
+  const size_t SZ = a.SZ;
+  for (int el = threadIdx.x; el < a.SZ; el += 256) {
+    float v = a.init ? a.init[head * SZ + el] : 0.f;
+    for (int p = a.P - 1; p >= 0; --p) {
+      const size_t idx = ((size_t)head * a.P + p) * SZ + el;
+      a.out[idx] = v;
+      v += a.seg[idx];
+    }
+  }
+}
+
+hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(scan_fwd_kernel, dim3(a.BH), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(scan_bwd_kernel, dim3(a.BH), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_scan_rev(const ScanArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(scan_rev_kernel, dim3(a.BH), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace slim

@@ -63,7 +63,7 @@ def _load() -> ctypes.CDLL:
     lib.slim_featmap.restype = i32
     lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, vp, sz, vp]
     lib.slim_fwd.restype = i32
-    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, fp, vp, fp, vp, vp, vp, fp, fp, vp, sz, vp]
+    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, fp, vp, vp, vp, fp, fp, vp, sz, vp]
     lib.slim_bwd.restype = i32
     lib.slim_status_string.argtypes = [i32]
     lib.slim_status_string.restype = ctypes.c_char_p
@@ -183,10 +183,9 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
     return Y, state_out, kshift_out
 
 
-def bwd(Q, K, V, W, dY, C: int, state_out, kshift=None, kind="favor+", state_in=None, kshift_in=None,
-        dstate_out=None, want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None,
-        dW=None):
-    """Backward sweep from the forward's state_out (and kshift_out for FAVOR+).
+def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshift_in=None, dstate_out=None,
+        want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None):
+    """Backward sweep; kshift is the forward's kshift_out (FAVOR+).
 
     Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
     p = _problem_of(Q, W, C, kind, relu_eps)
@@ -195,7 +194,6 @@ def bwd(Q, K, V, W, dY, C: int, state_out, kshift=None, kind="favor+", state_in=
         _need(t, n, Q.dtype, shp)
     _need(W, "W", torch.float32, (p.M, p.d))
     sshape = (p.B, p.H, p.M, p.d + 1)
-    _need(state_out, "state_out", torch.float32, sshape)
     for n, t in (("state_in", state_in), ("dstate_out", dstate_out)):
         if t is not None:
             _need(t, n, torch.float32, sshape)
@@ -210,6 +208,6 @@ def bwd(Q, K, V, W, dY, C: int, state_out, kshift=None, kind="favor+", state_in=
     dstate_in = torch.empty(sshape, dtype=torch.float32, device=dev) if want_dstate_in else None
     ws = _workspace(p, PHASE_BWD, dev, ws)
     _check(LIB.slim_bwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
-                        _ptr(state_out), _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
+                        _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
                         _ptr(dW), _ptr(dstate_in), _ptr(ws), ws.numel(), _stream()))
     return dQ, dK, dV, dW, dstate_in

@@ -21,7 +21,7 @@ def _run(x, C, kind, state_in=None, kshift_in=None, dstate_out=None, want_dstate
 
     Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
     Y, st, ks = slim.fwd(Q, K, V, W, C, kind, state_in=state_in, kshift_in=kshift_in)
-    g = slim.bwd(Q, K, V, W, dY, C, st, ks, kind, state_in=state_in, kshift_in=kshift_in, dstate_out=dstate_out,
+    g = slim.bwd(Q, K, V, W, dY, C, ks, kind, state_in=state_in, kshift_in=kshift_in, dstate_out=dstate_out,
                  want_dstate_in=want_dstate_in)
     torch.cuda.synchronize()
     return Y, st, ks, g
@@ -57,9 +57,9 @@ def test_state_cotangent_and_chaining(i):
     Y1, st1, ks1 = slim.fwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, C, kind)
     Y2, st2, ks2 = slim.fwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, C, kind, state_in=st1,
                             kshift_in=ks1)
-    g2 = slim.bwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, half(dY, cut, L), C, st2, ks2, kind,
+    g2 = slim.bwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, half(dY, cut, L), C, ks2, kind,
                   state_in=st1, kshift_in=ks1, want_dstate_in=True)
-    g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, st1, ks1, kind,
+    g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, ks1, kind,
                   dstate_out=g2[4])
     torch.cuda.synchronize()
     ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)

@@ -1,0 +1,84 @@
+"""GPU parity of the segmented walks: the sequence of each head is split into
+P segments processed in parallel and stitched by exact scans of their states.
+
+The results must not depend on P (up to rounding): the tests force P through
+the SLIM_SEGMENTS debugging variable and compare every output with the fp64
+oracle.  Longer sequences check that downdates do not drift.
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from synth import Workload, make_inputs
+from tests.gpu_common import TOL, dev, host64, need_gpu, report
+
+pytestmark = pytest.mark.gpu
+
+
+def _fwd_bwd(x, C, kind, segments=None):
+    from paper_2012_11346_amd import slim
+
+    old = os.environ.get("SLIM_SEGMENTS")
+    try:
+        if segments is not None:
+            os.environ["SLIM_SEGMENTS"] = str(segments)
+        Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+        Y, st, ks = slim.fwd(Q, K, V, W, C, kind)
+        g = slim.bwd(Q, K, V, W, dY, C, ks, kind)
+        torch.cuda.synchronize()
+    finally:
+        if old is None:
+            os.environ.pop("SLIM_SEGMENTS", None)
+        else:
+            os.environ["SLIM_SEGMENTS"] = old
+    return Y, st, ks, g
+
+
+SEG_CASES = [
+    # name, B, H, L, d, M, C, dtype, kind, segment counts
+    ("f32_c32", 1, 2, 256, 32, 64, 32, "f32", "favor+", (1, 2, 3, 8)),
+    ("f32_relu_c5", 1, 1, 200, 32, 64, 5, "f32", "relu", (1, 7, 40)),
+    ("bf16_c64", 2, 2, 700, 64, 256, 64, "bf16", "favor+", (1, 2, 5, 22)),
+    ("bf16_relu_c256", 1, 2, 600, 64, 128, 256, "bf16", "relu", (1, 4, 19)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(SEG_CASES)))
+def test_results_do_not_depend_on_segments(i):
+    need_gpu()
+    name, B, H, L, d, M, C, dtype, kind, segs = SEG_CASES[i]
+    x = make_inputs(Workload(name, 300 + i, B, H, L, d, M, (C,), dtype, kind))
+    Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
+    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    _, stref = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind, within="quadratic")
+    tol = TOL[dtype]
+    for P in segs:
+        print(f"[segments] case={name} P={P}", flush=True)
+        Y, st, ks, g = _fwd_bwd(x, C, kind, P)
+        report(f"Y P={P}", host64(Y), Yref, tol)
+        s = host64(st)
+        if kind == "favor+":
+            s = s * np.exp(host64(ks))[:, :, None, None]
+        report(f"state P={P}", s, stref, tol)
+        for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], gref):
+            report(f"{n} P={P}", host64(a), r, tol)
+
+
+@pytest.mark.parametrize("kind", ["favor+", "relu"])
+def test_long_sequence_against_definition(kind):
+    """L = 4096: the reverse walk downdates over many tiles per segment."""
+    need_gpu()
+    M = 256 if kind == "favor+" else 128
+    x = make_inputs(Workload("long", 320, 1, 2, 4096, 64, M, (64,), "bf16", kind))
+    Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
+    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    for P in (None, 1):
+        print(f"[long] kind={kind} P={P}", flush=True)
+        Y, st, ks, g = _fwd_bwd(x, 64, kind, P)
+        report("Y", host64(Y), Yref, TOL["bf16"])
+        for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], gref):
+            report(n, host64(a), r, TOL["bf16"])
