@@ -111,13 +111,16 @@ FwdLayout fwd_layout(const slim_problem* p, int P) {
 // backward workspace: segment sums, segment boundaries, per-segment
 // cotangent contributions and cotangents after each segment, dW partials
 struct BwdLayout {
-  size_t seg_sum, bounds, gc, gend, dw_part, total;
+  size_t wfrag, seg_sum, bounds, gc, gend, dw_part, total;
 };
+size_t wfrag_bytes_of(const slim_problem* p);
 BwdLayout bwd_layout(const slim_problem* p, int P) {
-  BwdLayout l{0, 0, 0, 0, 0, 0};
+  BwdLayout l{0, 0, 0, 0, 0, 0, 0};
   const size_t heads = (size_t)p->B * p->H;
   const size_t se = state_elems(p) * sizeof(float);
   size_t off = 0;
+  l.wfrag = off;
+  off += align256(wfrag_bytes_of(p));
   l.seg_sum = off;
   off += align256(heads * P * se);
   l.bounds = off;
@@ -134,23 +137,25 @@ BwdLayout bwd_layout(const slim_problem* p, int P) {
   return l;
 }
 
-size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_segments(p)).total; }
-size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
-
 typedef hipError_t (*fwd_fn)(const slim::FwdArgs&, int, hipStream_t);
 typedef hipError_t (*feat_fn)(const slim::FeatArgs&, hipStream_t);
 typedef hipError_t (*bwd_fn)(const slim::BwdArgs&, hipStream_t);
+typedef hipError_t (*wfrag_fn)(const slim::WfragArgs&, hipStream_t);
+typedef size_t (*size_fn)();
 
 struct Dispatch {
   fwd_fn fwd;
   feat_fn feat;
   bwd_fn bwd;
+  wfrag_fn wfrag;
+  size_fn wfrag_bytes;
 };
 
 template <class T, int D, int FW, int KIND>
 Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
-  return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>};
+  return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>,
+                  &slim::launch_wfrag<G>, &slim::wfrag_bytes<G>};
 }
 
 template <int KIND>
@@ -172,12 +177,17 @@ Dispatch pick_f32(int d, int M) {
   return make_dispatch<float, 32, 16, KIND>();
 }
 
-// callers have checked supported(p)
+// callers have checked check_problem(p)
 Dispatch dispatch(const slim_problem* p) {
   if (p->dtype == SLIM_BF16) return p->kind == SLIM_FAVOR_PLUS ? pick_bf16<slim::kFavor>(p->d, p->M)
                                                                : pick_bf16<slim::kRelu>(p->d, p->M);
   return p->kind == SLIM_FAVOR_PLUS ? pick_f32<slim::kFavor>(p->d, p->M) : pick_f32<slim::kRelu>(p->d, p->M);
 }
+
+size_t wfrag_bytes_of(const slim_problem* p) { return dispatch(p).wfrag_bytes(); }
+
+size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_segments(p)).total; }
+size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
 
 }  // namespace
 
@@ -391,7 +401,12 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (e != hipSuccess) return hip_fail(e, "cotangent-scan launch");
     gend = rv.out;
   }
-  // (4) the reverse walk
+  // (4) W in fragment order, then the reverse walk
+  slim::WfragArgs wf;
+  wf.W = W;
+  wf.out = w + lay.wfrag;
+  e = dp.wfrag(wf, s);
+  if (e != hipSuccess) return hip_fail(e, "W-fragment launch");
   slim::BwdArgs a;
   std::memset(&a, 0, sizeof(a));
   a.Q = Q;
@@ -399,6 +414,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.V = V;
   a.dY = dY;
   a.W = W;
+  a.Wfrag = wf.out;
   a.kshift = favor ? kshift : nullptr;
   a.bounds = sc.out;
   a.seg_gend = gend;

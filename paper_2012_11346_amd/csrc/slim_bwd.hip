@@ -15,8 +15,12 @@
 //   b8  G += Q~^T [dN|dD]                                (eq. 18)
 //   b9  feature-map chain rule: dq = (dQ~ . Q~) W - q rowsum(dQ~ . Q~) for
 //       FAVOR+ (masked for ReLU), same for keys; dW partial sums
-// Cross-feature sums (N, D, dV, dq, dk) go through a cross-wave reduction in
-// LDS.  dW partials of every workgroup are summed by dw_reduce in a fixed
+// After the exponentials, Q~ and K~ live only in LDS (bf16 for bf16
+// problems) and every later product reads its operand fragments from there;
+// this keeps the per-wave register set to the state, the cotangent, the dW
+// accumulators and the W fragments.  Cross-feature sums (N, D, dV, dq, dk) go
+// through a cross-wave reduction in LDS that reuses each wave's transpose
+// buffer.  dW partials of every workgroup are summed by dw_reduce in a fixed
 // order, so results are deterministic.
 #include "slim_common.hpp"
 #include "slim_kernels.hpp"
@@ -24,7 +28,7 @@
 namespace slim {
 
 template <class G>
-__device__ __forceinline__ void load_w_frags_b(typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+__device__ __forceinline__ void load_w_frags_b_unused(typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
                                                const float* W, int w) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
@@ -58,33 +62,102 @@ __device__ __forceinline__ typename FragT<typename G::T>::type pair_or_half(cons
   return has_b ? tile_pair_frag<typename G::T>(a, b) : tile_half_frag<typename G::T>(a);
 }
 
+// fragment slot s = Z[row0 + c][k0 + kp(g, s)], with slots 4..7 zero when the
+// 32-deep block has only its first 16 entries
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type frag_rm_h(const T* Z, int ld, int row0, int k0, bool half) {
+  if (!half) return frag_rm(Z, ld, row0, k0);
+  const int g = lane_g(), c = lane_c();
+  const T* p = Z + (row0 + c) * ld + k0 + 4 * g;
+  typename FragT<T>::type f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = p[r];
+    f[4 + r] = cvt<T>(0.f);
+  }
+  return f;
+}
+
+// result-tile values of a matrix stored transposed by store_tile_T:
+// X[row0 + 4g + r][col0 + c] = Z[col0 + c][row0 + 4g + r]
+template <typename T>
+__device__ __forceinline__ f32x4 load_tile_T(const T* Z, int ld, int row0, int col0) {
+  const int g = lane_g(), c = lane_c();
+  const T* p = Z + (col0 + c) * ld + row0 + 4 * g;
+  f32x4 x;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) x[r] = to_f32(p[r]);
+  return x;
+}
+
+constexpr size_t al16(size_t n) { return (n + 15) & ~(size_t)15; }
+
+template <class G>
+struct BwdLds {
+  typedef typename G::T T;
+  static constexpr int D = G::D, FW = G::FW, TR = G::TR, ZR = G::ZR, LDQ = G::LDQ, LDR = G::LDR;
+  static constexpr int LDZK = TR + 8;  // [feature][row] buffers (K~, dK~.K~)
+  static constexpr int LDZF = FW + 8;  // [row or e][feature] buffers (Q~, S, G, dQ~.Q~)
+  static constexpr int LDZT = TR + 8;  // [row][row] buffers (A^T, dA^T)
+  // shared tiles
+  static constexpr size_t TILE = al16((size_t)TR * LDQ * sizeof(T));
+  static constexpr size_t oQ = 0, oK = oQ + TILE, oV = oK + TILE, odY = oV + TILE, odN = odY + TILE;
+  static constexpr size_t oF = odN + TILE;  // floats: qn kn qmx[4] dDs rsum[4] dzs[4]
+  static constexpr size_t NF = 2 * TR + 4 * TR + TR + 4 * TR + 4 * FW;
+  static constexpr size_t odDb = oF + al16(NF * sizeof(float));
+  static constexpr size_t oW = odDb + al16((TR + 8) * sizeof(T));
+  // per-wave regions
+  static constexpr size_t ZK = al16((size_t)ZR * LDZK * sizeof(T));
+  static constexpr size_t ZQ = al16((size_t)TR * LDZF * sizeof(T));
+  static constexpr size_t X1 = (size_t)TR * LDZT * sizeof(T), X2 = (size_t)TR * LDZF * sizeof(T),
+                          X3 = (size_t)ZR * LDZK * sizeof(T);
+  static constexpr size_t ZX = al16(X1 > X2 ? (X1 > X3 ? X1 : X3) : (X2 > X3 ? X2 : X3));
+  static constexpr size_t ZDA = al16((size_t)TR * LDZT * sizeof(T));
+  static constexpr size_t R1 = (size_t)TR * LDR * sizeof(float), R2 = (size_t)D * LDZF * sizeof(T);
+  static constexpr size_t ZRS = al16(R1 > R2 ? R1 : R2);
+  static constexpr size_t oZk = 0, oZq = oZk + ZK, oZx = oZq + ZQ, oZdA = oZx + ZX, oZrs = oZdA + ZDA;
+  static constexpr size_t WAVE = oZrs + ZRS;
+  static constexpr size_t TOTAL = oW + 4 * WAVE;
+};
+
 template <class G>
 __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
+  typedef BwdLds<G> Lay;
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
-                RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDR = G::LDR;
-  // per-wave buffers (element pitches)
-  constexpr int LDZK = TR + 8;  // [m][s] and [m][s] for K~, (dK~.K~)
-  constexpr int LDZF = FW + 8;  // [e][m], [t][m] buffers
-  constexpr int LDZT = TR + 8;  // [t][s] buffers
-  constexpr int ZR = G::ZR;
-  constexpr int REG_A = (ZR * LDZK > D * LDZF) ? ZR * LDZK : D * LDZF;  // Zk | ZS | ZG
-  constexpr int REG_B = (TR * LDZT > TR * LDZF) ? TR * LDZT : TR * LDZF;  // ZA | ZP | Zq
-  constexpr int REG_C = TR * LDZT;                                        // ZdA
-  constexpr int REG_D = ZR * LDZK;                                        // ZPk
-  constexpr int REG = REG_A + REG_B + REG_C + REG_D;
+                RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDR = G::LDR, ZR = G::ZR;
+  constexpr int LDZK = Lay::LDZK, LDZF = Lay::LDZF, LDZT = Lay::LDZT;
+  constexpr bool ODD = (MT & 1) != 0;  // last 32-deep feature block holds 16 features
 
-  __shared__ __attribute__((aligned(16))) T Qs[TR * LDQ];
-  __shared__ __attribute__((aligned(16))) T Ks[TR * LDQ];
-  __shared__ __attribute__((aligned(16))) T Vs[TR * LDQ];
-  __shared__ __attribute__((aligned(16))) T dNs[TR * LDQ];
-  __shared__ __attribute__((aligned(16))) T Zw[4][REG];
-  __shared__ __attribute__((aligned(16))) float Red[4][TR * LDR];
-  __shared__ float qn[TR], kn[TR], qmx[4][TR], dDs[TR], rsum[4][TR], dzs[4][FW];
-  __shared__ __attribute__((aligned(16))) T dDb[TR + 8];
+  // one arena, so that the compiler sees every alias between phases
+  __shared__ __attribute__((aligned(16))) char arena[Lay::TOTAL];
+  T* Qs = (T*)(arena + Lay::oQ);
+  T* Ks = (T*)(arena + Lay::oK);
+  T* Vs = (T*)(arena + Lay::oV);
+  T* dYs = (T*)(arena + Lay::odY);
+  T* dNs = (T*)(arena + Lay::odN);
+  float* fl = (float*)(arena + Lay::oF);
+  float* qn = fl;
+  float* kn = qn + TR;
+  float* qmx = kn + TR;        // [4][TR]
+  float* dDs = qmx + 4 * TR;   // [TR]
+  float* rsum = dDs + TR;      // [4][TR]
+  float* dzs = rsum + 4 * TR;  // [4][FW]
+  T* dDb = (T*)(arena + Lay::odDb);
 
   const int w = wave_id(), g = lane_g(), c = lane_c();
+  char* wz = arena + Lay::oW + (size_t)w * Lay::WAVE;
+  T* Zk = (T*)(wz + Lay::oZk);    // K~ as [m][s], whole tile
+  T* Zq = (T*)(wz + Lay::oZq);    // Q~ as [t][m], whole tile
+  T* ZA = (T*)(wz + Lay::oZx);    // A^T as [t][s]; then dQ~.Q~ as [t][m]; then dK~.K~ as [m][s]
+  T* ZP = ZA;
+  T* ZPk = ZA;
+  T* ZdA = (T*)(wz + Lay::oZdA);  // dA^T as [t][s]
+  T* ZS = (T*)(wz + Lay::oZrs);   // S as [e][m]; G as [e][m]
+  float* Redw = (float*)(wz + Lay::oZrs);  // this wave's partial sums [row][e]
+  auto red = [&](int ww) -> float* { return (float*)(arena + Lay::oW + (size_t)ww * Lay::WAVE + Lay::oZrs); };
+
   const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const size_t head = (size_t)b * a.H + h;
   const size_t hoff = head * (size_t)a.L * D;
@@ -96,21 +169,16 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   T* dKh = (T*)a.dK + hoff;
   T* dVh = (T*)a.dV + hoff;
 
-  T* ZA_ = Zw[w];                     // region A
-  T* ZB_ = Zw[w] + REG_A;             // region B
-  T* ZC_ = Zw[w] + REG_A + REG_B;     // region C
-  T* ZD_ = ZC_ + REG_C;               // region D
-
-  F Wf[MT][EB];
-  load_w_frags_b<G>(Wf, a.W, w);
-  F WT[MB][ET];
-  load_wt_frags<G>(WT, a.W, w);
+  // W fragments come from the fragment-ordered copy (L2-resident), loaded
+  // where they are used instead of being held for the whole walk
+  typedef WFragLayout<G> WL;
+  const F* Wfr = reinterpret_cast<const F*>(a.Wfrag);
+  const int lane = lane_id();
 
   const size_t SZ = (size_t)M * (D + 1);
-  const size_t sidx = (head * a.P + p) * SZ;                 // per-segment arrays
-  const float* bstart = a.bounds + (head * (a.P + 1) + p) * SZ;  // state before the segment
-  const float* bend = bstart + SZ;                            // state after the segment
-  // dstate_in is relative to the caller's initial key shift
+  const size_t sidx = (head * a.P + p) * SZ;
+  const float* bstart = a.bounds + (head * (a.P + 1) + p) * SZ;
+  const float* bend = bstart + SZ;
   float r0 = 1.f;
   if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
@@ -132,8 +200,8 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     for (int et = 0; et < ET; ++et) dWacc[mt][et] = zero4();
   }
 
-  // zero all per-wave buffers once: pad rows must read as zero
-  for (int i = lane_id(); i < REG; i += 64) Zw[w][i] = cvt<T>(0.f);
+  // this wave's buffers start at zero: pad rows of Zk must read as zero
+  for (size_t i = lane_id() * 16; i < Lay::WAVE; i += 64 * 16) *reinterpret_cast<uint4*>(wz + i) = uint4{0, 0, 0, 0};
 
   const TileMap tm(a.L, a.C, TR);
   const int n_tiles = tm.count_tiles();
@@ -142,17 +210,51 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   const float koff = (G::KIND == kFavor) ? a.kshift[head] * kLog2e + half_log2M : 0.f;
   constexpr int TPR = 256 / TR, EPT = D / TPR;
 
+  RowStage<T, D, TR, 256> sq, sk, sv, sdy;
+  if (j1 > j0) {
+    int st0, cn0;
+    tm.tile(j1 - 1, st0, cn0);
+    sq.fetch(Qh + (size_t)st0 * D, cn0);
+    sk.fetch(Kh + (size_t)st0 * D, cn0);
+    sv.fetch(Vh + (size_t)st0 * D, cn0);
+    sdy.fetch(dYh + (size_t)st0 * D, cn0);
+  }
+
+  // [V|1] operand over rows [32 rb, 32 rb + 32) for value tile et (et == ET: ones)
+  auto v_frag = [&](int rb, int et, int count) -> F {
+    if (et < ET) return frag_tr(Vs, LDQ, 32 * rb, 16 * et);
+    F f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) f[s] = cvt<T>((32 * rb + kp(g, s) < count) ? 1.f : 0.f);
+    return f;
+  };
+  auto half_m = [&](int kb) -> bool { return ODD && kb == MB - 1; };
+
   for (int j = j1 - 1; j >= j0; --j) {
     int start, count;
     tm.tile(j, start, count);
-    load_rows<T, D, TR, LDQ, 256>(Qs, Qh + (size_t)start * D, count, G::KIND == kFavor ? qn : nullptr);
-    load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, G::KIND == kFavor ? kn : nullptr);
-    load_rows<T, D, TR, LDQ, 256>(Vs, Vh + (size_t)start * D, count, nullptr);
+    F Wf[MT][EB];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = Wfr[WL::a(w, mt, kb) * 64 + lane];
+    sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr);
+    sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr);
+    sv.template store<LDQ>(Vs, nullptr);
+    sdy.template store<LDQ>(dYs, nullptr);
+    if (j > j0) {  // next tile's loads overlap this tile's compute
+      int sn, cnn;
+      tm.tile(j - 1, sn, cnn);
+      sq.fetch(Qh + (size_t)sn * D, cnn);
+      sk.fetch(Kh + (size_t)sn * D, cnn);
+      sv.fetch(Vh + (size_t)sn * D, cnn);
+      sdy.fetch(dYh + (size_t)sn * D, cnn);
+    }
     __syncthreads();
 
-    // ---- b2 (features)
-    f32x4 Lq[MT][RT], Lk[RT][MT];
+    // ---- features: logits, shifts, exponentials; Q~ -> Zq[t][m], K~ -> Zk[m][s]
     {
+      f32x4 Lq[MT][RT], Lk[RT][MT];
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
         const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
@@ -177,61 +279,51 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           Lk[st][mt] = acc;
         }
       }
-    }
-    if (G::KIND == kFavor) {
+      if (G::KIND == kFavor) {
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
+          v = wave_max_over_g(v);
+          if (g == 0) qmx[w * TR + 16 * tt + c] = v;
+        }
+      }
+#pragma unroll
+      for (int st = 0; st < RT; ++st)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          f32x4 kv = Lk[st][mt];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool ok = 16 * st + 4 * g + r < count;
+            kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : fmaxf(kv[r], 0.f) + a.relu_eps;
+          }
+          store_tile_T<T>(Zk, LDZK, kv, 16 * st, 16 * mt);
+        }
+      __syncthreads();
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
-        float v = -INFINITY;
+        const int t = 16 * tt + c;
+        float qs = 0.f;
+        if (G::KIND == kFavor)
+          qs = fmaxf(fmaxf(qmx[t], qmx[TR + t]), fmaxf(qmx[2 * TR + t], qmx[3 * TR + t])) * kLog2e;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt) {
+          f32x4 qv = Lq[mt][tt];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
-        v = wave_max_over_g(v);
-        if (g == 0) qmx[w][16 * tt + c] = v;
+          for (int r = 0; r < 4; ++r)
+            qv[r] = (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(qv[r] * kLog2e - qs) : fmaxf(qv[r], 0.f) + a.relu_eps;
+          store_tile_T<T>(Zq, LDZF, qv, 16 * mt, 16 * tt);
+        }
       }
     }
     __syncthreads();
-#pragma unroll
-    for (int st = 0; st < RT; ++st)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const bool ok = 16 * st + 4 * g + r < count;
-          const float x = Lk[st][mt][r];
-          Lk[st][mt][r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(x * kLog2e - koff) : fmaxf(x, 0.f) + a.relu_eps;
-        }
-#pragma unroll
-    for (int tt = 0; tt < RT; ++tt) {
-      const int t = 16 * tt + c;
-      float qs = 0.f;
-      if (G::KIND == kFavor) qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t])) * kLog2e;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float x = Lq[mt][tt][r];
-          Lq[mt][tt][r] =
-              (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(x * kLog2e - qs) : fmaxf(x, 0.f) + a.relu_eps;
-        }
-    }
-
-    F vf[RB][ET + 1];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int et = 0; et <= ET; ++et) {
-        if (et < ET) {
-          vf[rb][et] = frag_tr(Vs, LDQ, 32 * rb, 16 * et);
-        } else {
-#pragma unroll
-          for (int s = 0; s < 8; ++s) vf[rb][et][s] = cvt<T>((32 * rb + kp(g, s) < count) ? 1.f : 0.f);
-        }
-      }
 
     // ---- b1: state before the tile
     if (j == j0) {
-      // the exact state before the segment replaces the downdated one
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -243,97 +335,73 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
         }
     } else {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int et = 0; et <= ET; ++et)
+        for (int et = 0; et <= ET; ++et) {
+          const F vf = v_frag(rb, et, count);
 #pragma unroll
-          for (int rb = 0; rb < RB; ++rb) {
-            F kf = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
+          for (int mt = 0; mt < MT; ++mt) {
+            F kf = frag_rm(Zk, LDZK, 16 * mt, 32 * rb);  // K~ contracting over rows
 #pragma unroll
             for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
-            S[mt][et] = mma(S[mt][et], kf, vf[rb][et]);
+            S[mt][et] = mma(S[mt][et], kf, vf);
           }
+        }
     }
 
-    // K~ transposed: Zk[m][s]
-    T* Zk = ZA_;
-#pragma unroll
-    for (int st = 0; st < RT; ++st)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk, LDZK, Lk[st][mt], 16 * st, 16 * mt);
-    __syncthreads();
-
-    F qf[MB][RT];
-#pragma unroll
-    for (int kb = 0; kb < MB; ++kb)
-#pragma unroll
-      for (int tt = 0; tt < RT; ++tt) qf[kb][tt] = pair_or_half<G>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt], 2 * kb + 1 < MT);
-
-    // ---- b2: scores A^T[s][t] (this wave's features), causal
-    f32x4 At[RT][RT];
+    // ---- b2: scores A^T[s][t] (this wave's features), causal, -> ZA[t][s]
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
       for (int st = 0; st < RT; ++st) {
-        At[st][tt] = zero4();
-        if (st > tt) continue;
+        f32x4 acc = zero4();
+        if (st <= tt) {
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) At[st][tt] = mma(At[st][tt], frag_tr(Zk, LDZK, 32 * kb, 16 * st), qf[kb][tt]);
-        if (st == tt) {
+          for (int kb = 0; kb < MB; ++kb)
+            acc = mma(acc, frag_tr(Zk, LDZK, 32 * kb, 16 * st), frag_rm_h(Zq, LDZF, 16 * tt, 32 * kb, half_m(kb)));
+          if (st == tt) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (4 * g + r > c) At[st][tt][r] = 0.f;
+            for (int r = 0; r < 4; ++r)
+              if (4 * g + r > c) acc[r] = 0.f;
+          }
+        }
+        store_tile_T<T>(ZA, LDZT, acc, 16 * st, 16 * tt);
+      }
+    // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T, this wave's features; reduction rows [t][e]
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+      for (int et = 0; et <= ET; ++et) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          if (2 * rb <= tt) acc = mma(acc, v_frag(rb, et, count), frag_rm(ZA, LDZT, 16 * tt, 32 * rb));
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb)
+          acc = mma(acc, pair_or_half<G>(S[2 * kb][et], S[half_m(kb) ? 2 * kb : 2 * kb + 1][et], !half_m(kb)),
+                    frag_rm_h(Zq, LDZF, 16 * tt, 32 * kb, half_m(kb)));
+        if (et < ET) {
+          store_tile_T<float>(Redw, LDR, acc, 16 * et, 16 * tt);
+        } else if (g == 0) {
+          Redw[(16 * tt + c) * LDR + D] = acc[0];
         }
       }
-    // A^T transposed: ZA[t][s]
-    T* ZA = ZB_;
-#pragma unroll
-    for (int st = 0; st < RT; ++st)
-#pragma unroll
-      for (int tt = 0; tt < RT; ++tt) store_tile_T<T>(ZA, LDZT, At[st][tt], 16 * st, 16 * tt);
-
-    // N^T[e][t] partial into Red as [t][e]
-    {
-      F sf[MB][ET + 1];
-#pragma unroll
-      for (int kb = 0; kb < MB; ++kb)
-#pragma unroll
-        for (int et = 0; et <= ET; ++et) sf[kb][et] = pair_or_half<G>(S[2 * kb][et], S[2 * kb + 1][et], 2 * kb + 1 < MT);
-#pragma unroll
-      for (int tt = 0; tt < RT; ++tt)
-#pragma unroll
-        for (int et = 0; et <= ET; ++et) {
-          f32x4 acc = zero4();
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) {
-            if (2 * rb > tt) continue;
-            acc = mma(acc, vf[rb][et], pair_or_half<G>(At[2 * rb][tt], At[2 * rb + 1][tt], 2 * rb + 1 <= tt));
-          }
-#pragma unroll
-          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sf[kb][et], qf[kb][tt]);
-          if (et < ET) {
-            store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * tt);
-          } else if (g == 0) {
-            Red[w][(16 * tt + c) * LDR + D] = acc[0];
-          }
-        }
-    }
     __syncthreads();
 
     // ---- b3: dN, dD per row (threads: TPR per row)
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
-      float dy[EPT], n[EPT];
-      float den = 1.f, dot = 0.f;
       const bool ok = t < count;
-      den = Red[0][t * LDR + D] + Red[1][t * LDR + D] + Red[2][t * LDR + D] + Red[3][t * LDR + D];
+      float dy[EPT];
+      float dot = 0.f;
+      const float den = red(0)[t * LDR + D] + red(1)[t * LDR + D] + red(2)[t * LDR + D] + red(3)[t * LDR + D];
       const float inv = ok ? 1.f / den : 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i) {
         const int e = q * EPT + i;
-        dy[i] = ok ? to_f32(dYh[(size_t)(start + t) * D + e]) : 0.f;
-        n[i] = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-        dot += dy[i] * (n[i] * inv);
+        dy[i] = to_f32(dYs[t * LDQ + e]);
+        const float n = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
+        dot += dy[i] * (n * inv);
       }
 #pragma unroll
       for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
@@ -347,52 +415,43 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     }
     __syncthreads();
 
-    // ---- b4: dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal
-    f32x4 dAt[RT][RT];
+    // ---- b4: dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal, -> ZdA[t][s]
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
       const float ddt = dDs[16 * tt + c];
 #pragma unroll
       for (int st = 0; st < RT; ++st) {
-        dAt[st][tt] = zero4();
-        if (st > tt) continue;
-        f32x4 acc = {ddt, ddt, ddt, ddt};
+        f32x4 acc = zero4();
+        if (st <= tt) {
+          acc = f32x4{ddt, ddt, ddt, ddt};
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_rm(Vs, LDQ, 16 * st, 32 * kb), frag_rm(dNs, LDQ, 16 * tt, 32 * kb));
+          for (int kb = 0; kb < EB; ++kb)
+            acc = mma(acc, frag_rm(Vs, LDQ, 16 * st, 32 * kb), frag_rm(dNs, LDQ, 16 * tt, 32 * kb));
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int s = 16 * st + 4 * g + r;
-          if (st == tt && 4 * g + r > c) acc[r] = 0.f;
-          if (s >= count) acc[r] = 0.f;
+          for (int r = 0; r < 4; ++r) {
+            const int sr = 16 * st + 4 * g + r;
+            if ((st == tt && 4 * g + r > c) || sr >= count) acc[r] = 0.f;
+          }
         }
-        dAt[st][tt] = acc;
+        store_tile_T<T>(ZdA, LDZT, acc, 16 * st, 16 * tt);
       }
     }
-    // dA^T transposed: ZdA[t][s]
-    T* ZdA = ZC_;
+
+    // ---- b7: dV^T[e][s] = sum_m dS[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t]; reduction rows [s][e]
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) store_tile_T<T>(ZdA, LDZT, dAt[st][tt], 16 * st, 16 * tt);
-
-    // ---- b7: dV^T[e][s] = sum_m dS[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t]  (Red as [s][e])
-    {
+      for (int et = 0; et < ET; ++et) {
+        f32x4 acc = zero4();
 #pragma unroll
-      for (int st = 0; st < RT; ++st)
+        for (int kb = 0; kb < MB; ++kb)
+          acc = mma(acc, pair_or_half<G>(Gs[2 * kb][et], Gs[half_m(kb) ? 2 * kb : 2 * kb + 1][et], !half_m(kb)),
+                    frag_tr(Zk, LDZK, 32 * kb, 16 * st));
 #pragma unroll
-        for (int et = 0; et < ET; ++et) {
-          f32x4 acc = zero4();
-#pragma unroll
-          for (int kb = 0; kb < MB; ++kb)
-            acc = mma(acc, pair_or_half<G>(Gs[2 * kb][et], Gs[2 * kb + 1][et], 2 * kb + 1 < MT),
-                      frag_tr(Zk, LDZK, 32 * kb, 16 * st));
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-            acc = mma(acc, frag_tr(dNs, LDQ, 32 * rb, 16 * et), frag_tr(ZA, LDZT, 32 * rb, 16 * st));
-          store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * st);
-        }
-    }
+        for (int rb = 0; rb < RB; ++rb)
+          acc = mma(acc, frag_tr(dNs, LDQ, 32 * rb, 16 * et), frag_tr(ZA, LDZT, 32 * rb, 16 * st));
+        store_tile_T<float>(Redw, LDR, acc, 16 * et, 16 * st);
+      }
     __syncthreads();
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
@@ -400,7 +459,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
-          const float v = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
+          const float v = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
           dVh[(size_t)(start + t) * D + e] = cvt<T>(v);
         }
       }
@@ -408,50 +467,48 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     __syncthreads();
 
     // ---- b5: dQ~^T[m][t] = sum_e S[m][e] dN[t][e] + z[m] dD[t] + sum_s K~[s][m] dA^T[s][t]
-    T* ZS = ZA_;  // S transposed [e][m] (Zk no longer needed)
+    //          P = dQ~ . Q~ (FAVOR+) or dQ~ masked (ReLU) -> ZP[t][m]
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int et = 0; et < ET; ++et) store_tile_T<T>(ZS, LDZF, S[mt][et], 16 * mt, 16 * et);
     __syncthreads();
-    f32x4 Pq[MT][RT];
+    {
+      float rs[RT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int tt = 0; tt < RT; ++tt) rs[tt] = 0.f;
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) {
-        const float ddt = dDs[16 * tt + c];
-        f32x4 acc;
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] = S[mt][ET][r] * ddt;
+        for (int tt = 0; tt < RT; ++tt) {
+          const float ddt = dDs[16 * tt + c];
+          f32x4 acc;
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_tr(ZS, LDZF, 32 * kb, 16 * mt), frag_rm(dNs, LDQ, 16 * tt, 32 * kb));
+          for (int r = 0; r < 4; ++r) acc[r] = S[mt][ET][r] * ddt;
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          acc = mma(acc, tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]),
-                    pair_or_half<G>(dAt[2 * rb][tt], dAt[2 * rb + 1][tt], 2 * rb + 1 <= tt));
-        // chain rule through the feature map (shift treated as a constant)
+          for (int kb = 0; kb < EB; ++kb)
+            acc = mma(acc, frag_tr(ZS, LDZF, 32 * kb, 16 * mt), frag_rm(dNs, LDQ, 16 * tt, 32 * kb));
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float qv = Lq[mt][tt][r];
-          acc[r] = (G::KIND == kFavor) ? acc[r] * qv : (qv > a.relu_eps ? acc[r] : 0.f);
+          for (int rb = 0; rb < RB; ++rb)
+            acc = mma(acc, frag_rm(Zk, LDZK, 16 * mt, 32 * rb), frag_rm(ZdA, LDZT, 16 * tt, 32 * rb));
+          const f32x4 qv = load_tile_T(Zq, LDZF, 16 * mt, 16 * tt);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
+            rs[tt] += acc[r];
+          }
+          store_tile_T<T>(ZP, LDZF, acc, 16 * mt, 16 * tt);
         }
-        Pq[mt][tt] = acc;
-      }
-    // row sums over features (FAVOR+ needs q * rowsum)
-    if (G::KIND == kFavor) {
+      if (G::KIND == kFavor) {
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) {
-        float v = 0.f;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v += Pq[mt][tt][r];
-        v = wave_sum_over_g(v);
-        if (g == 0) rsum[w][16 * tt + c] = v;
+        for (int tt = 0; tt < RT; ++tt) {
+          const float v = wave_sum_over_g(rs[tt]);
+          if (g == 0) rsum[w * TR + 16 * tt + c] = v;
+        }
       }
     }
-    // dq^T[e][t] = sum_m W[m][e] Pq[m][t]  (Red as [t][e])
+    __syncthreads();  // ZS reads done before the reduction rows are rewritten; ZP visible
+    // dq^T[e][t] = sum_m W[m][e] P[m][t]; reduction rows [t][e]
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
@@ -459,32 +516,28 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
         f32x4 acc = zero4();
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, WT[kb][et], pair_or_half<G>(Pq[2 * kb][tt], Pq[2 * kb + 1][tt], 2 * kb + 1 < MT));
-        store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * tt);
+          acc = mma(acc, Wfr[WL::b(w, kb, et) * 64 + lane], frag_rm_h(ZP, LDZF, 16 * tt, 32 * kb, half_m(kb)));
+        store_tile_T<float>(Redw, LDR, acc, 16 * et, 16 * tt);
       }
-    // dW[m][e] += sum_t Pq[m][t] Q[t][e]: Pq transposed into ZP[t][m]
-    T* ZP = ZB_;
+    // dW[m][e] += sum_t P[m][t] Q[t][e]
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) store_tile_T<T>(ZP, LDZF, Pq[mt][tt], 16 * mt, 16 * tt);
+      for (int mt = 0; mt < MT; ++mt) {
+        const F pf = frag_tr(ZP, LDZF, 32 * rb, 16 * mt);
+#pragma unroll
+        for (int et = 0; et < ET; ++et) dWacc[mt][et] = mma(dWacc[mt][et], pf, frag_tr(Qs, LDQ, 32 * rb, 16 * et));
+      }
     __syncthreads();
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int et = 0; et < ET; ++et)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          dWacc[mt][et] = mma(dWacc[mt][et], frag_tr(ZP, LDZF, 32 * rb, 16 * mt), frag_tr(Qs, LDQ, 32 * rb, 16 * et));
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
-        const float rs = (G::KIND == kFavor) ? rsum[0][t] + rsum[1][t] + rsum[2][t] + rsum[3][t] : 0.f;
+        const float rsv = (G::KIND == kFavor) ? rsum[t] + rsum[TR + t] + rsum[2 * TR + t] + rsum[3 * TR + t] : 0.f;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
-          float v = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-          if (G::KIND == kFavor) v -= to_f32(Qs[t * LDQ + e]) * rs;
+          float v = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
+          if (G::KIND == kFavor) v -= to_f32(Qs[t * LDQ + e]) * rsv;
           dQh[(size_t)(start + t) * D + e] = cvt<T>(v);
         }
       }
@@ -492,90 +545,87 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     __syncthreads();
 
     // ---- b6: dK~[s][m] = sum_e V[s][e] G[m][e] + dz[m] + sum_t dA^T[s][t] Q~[t][m]
-    T* ZG = ZA_;  // G transposed [e][m]
-    T* Zq = ZB_;  // Q~ as [t][m]
+    //          Pk = dK~ . K~ (FAVOR+) or masked (ReLU) -> ZPk[m][s]
+    T* ZG = ZS;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
       for (int et = 0; et < ET; ++et) store_tile_T<T>(ZG, LDZF, Gs[mt][et], 16 * mt, 16 * et);
-#pragma unroll
-      for (int tt = 0; tt < RT; ++tt) store_tile_T<T>(Zq, LDZF, Lq[mt][tt], 16 * mt, 16 * tt);
       if (c == 0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dzs[w][16 * mt + 4 * g + r] = Gs[mt][ET][r];
+        for (int r = 0; r < 4; ++r) dzs[w * FW + 16 * mt + 4 * g + r] = Gs[mt][ET][r];
       }
     }
     __syncthreads();
-    f32x4 Pk[RT][MT];
-#pragma unroll
-    for (int st = 0; st < RT; ++st)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 acc;
-        const float dz = dzs[w][16 * mt + c];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] = (16 * st + 4 * g + r < count) ? dz : 0.f;
-#pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_rm(Vs, LDQ, 16 * st, 32 * kb), frag_tr(ZG, LDZF, 32 * kb, 16 * mt));
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          acc = mma(acc, frag_tr(ZdA, LDZT, 32 * rb, 16 * st), frag_tr(Zq, LDZF, 32 * rb, 16 * mt));
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float kv = Lk[st][mt][r];
-          acc[r] = (G::KIND == kFavor) ? acc[r] * kv : (kv > a.relu_eps ? acc[r] : 0.f);
-        }
-        Pk[st][mt] = acc;
-      }
-    if (G::KIND == kFavor) {
+    {
+      float rk[RT][4];
 #pragma unroll
       for (int st = 0; st < RT; ++st)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float v = 0.f;
+        for (int r = 0; r < 4; ++r) rk[st][r] = 0.f;
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) v += Pk[st][mt][r];
-          v = wave_sum_over_c(v);
-          if (c == 0) rsum[w][16 * st + 4 * g + r] = v;
+      for (int st = 0; st < RT; ++st)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          f32x4 acc;
+          const float dz = dzs[w * FW + 16 * mt + c];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[r] = (16 * st + 4 * g + r < count) ? dz : 0.f;
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb)
+            acc = mma(acc, frag_rm(Vs, LDQ, 16 * st, 32 * kb), frag_tr(ZG, LDZF, 32 * kb, 16 * mt));
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            acc = mma(acc, frag_tr(ZdA, LDZT, 32 * rb, 16 * st), frag_tr(Zq, LDZF, 32 * rb, 16 * mt));
+          const f32x4 kv = load_tile_T(Zk, LDZK, 16 * st, 16 * mt);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
+            rk[st][r] += acc[r];
+          }
+          store_tile_T<T>(ZPk, LDZK, acc, 16 * st, 16 * mt);
         }
+      if (G::KIND == kFavor) {
+#pragma unroll
+        for (int st = 0; st < RT; ++st)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = wave_sum_over_c(rk[st][r]);
+            if (c == 0) rsum[w * TR + 16 * st + 4 * g + r] = v;
+          }
+      }
     }
-    // Pk transposed: ZPk[m][s]
-    T* ZPk = ZD_;
-#pragma unroll
-    for (int st = 0; st < RT; ++st)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(ZPk, LDZK, Pk[st][mt], 16 * st, 16 * mt);
+    __syncthreads();  // ZG reads done before the reduction rows are rewritten; ZPk visible
     // dW[m][e] += sum_s Pk[s][m] K[s][e]
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int et = 0; et < ET; ++et)
+      for (int mt = 0; mt < MT; ++mt) {
+        const F pf = frag_rm(ZPk, LDZK, 16 * mt, 32 * rb);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          dWacc[mt][et] = mma(dWacc[mt][et], tile_pair_frag<T>(Pk[2 * rb][mt], Pk[2 * rb + 1][mt]),
-                              frag_tr(Ks, LDQ, 32 * rb, 16 * et));
-    __syncthreads();
-    // dk^T[e][s] = sum_m W[m][e] Pk[s][m]  (Red as [s][e])
+        for (int et = 0; et < ET; ++et) dWacc[mt][et] = mma(dWacc[mt][et], pf, frag_tr(Ks, LDQ, 32 * rb, 16 * et));
+      }
+    // dk^T[e][s] = sum_m W[m][e] Pk[s][m]; reduction rows [s][e]
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
       for (int et = 0; et < ET; ++et) {
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, WT[kb][et], frag_tr(ZPk, LDZK, 32 * kb, 16 * st));
-        store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * st);
+        for (int kb = 0; kb < MB; ++kb)
+          acc = mma(acc, Wfr[WL::b(w, kb, et) * 64 + lane], frag_tr(ZPk, LDZK, 32 * kb, 16 * st));
+        store_tile_T<float>(Redw, LDR, acc, 16 * et, 16 * st);
       }
     __syncthreads();
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
-        const float rs = (G::KIND == kFavor) ? rsum[0][t] + rsum[1][t] + rsum[2][t] + rsum[3][t] : 0.f;
+        const float rsv = (G::KIND == kFavor) ? rsum[t] + rsum[TR + t] + rsum[2 * TR + t] + rsum[3 * TR + t] : 0.f;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
-          float v = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-          if (G::KIND == kFavor) v -= to_f32(Ks[t * LDQ + e]) * rs;
+          float v = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
+          if (G::KIND == kFavor) v -= to_f32(Ks[t * LDQ + e]) * rsv;
           dKh[(size_t)(start + t) * D + e] = cvt<T>(v);
         }
       }
@@ -583,11 +633,12 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 
     // ---- b8: G[m][e] += sum_t Q~[t][m] [dN|dD][t][e]
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int et = 0; et <= ET; ++et)
+      for (int mt = 0; mt < MT; ++mt) {
+        const F qf = frag_tr(Zq, LDZF, 32 * rb, 16 * mt);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
+        for (int et = 0; et <= ET; ++et) {
           F bfr;
           if (et < ET) {
             bfr = frag_tr(dNs, LDQ, 32 * rb, 16 * et);
@@ -595,8 +646,9 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 #pragma unroll
             for (int s = 0; s < 8; ++s) bfr[s] = dDb[32 * rb + kp(g, s)];
           }
-          Gs[mt][et] = mma(Gs[mt][et], frag_tr(Zq, LDZF, 32 * rb, 16 * mt), bfr);
+          Gs[mt][et] = mma(Gs[mt][et], qf, bfr);
         }
+      }
     __syncthreads();
   }
 
@@ -623,7 +675,8 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   }
 }
 
-// dW[m][e] = sum over workgroups of the partials, in a fixed order
+// dW[m][e] = sum over workgroups of the partials, in a fixed order; each
+// block sums a column slab of the partials for 256 entries
 __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* part, int nparts, int n, float* dW) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;

@@ -37,6 +37,21 @@ struct Cfg {
   static_assert(TR == 32 || TR == 64, "tile rows");
 };
 
+// Fragment-ordered copy of W, prepared once per call (wfrag_kernel): every
+// operand fragment of W a wave uses is 64 lanes x 8 elements, contiguous, so
+// a lane fetches it with one 16-byte (bf16) load.
+//   block A  [wave][mt][kb]: slot s = W[w FW + 16 mt + c][32 kb + kp(g, s)]   (contracting over d)
+//   block B  [wave][kb][et]: slot s = W[w FW + 32 kb + kp(g, s)][16 et + c]   (contracting over features)
+template <class G>
+struct WFragLayout {
+  static constexpr int NA = G::MT * G::EB;  // fragments of block A per wave
+  static constexpr int NB = G::MB * G::ET;  // fragments of block B per wave
+  static constexpr int PER_WAVE = NA + NB;
+  static constexpr int TOTAL = 4 * PER_WAVE;  // fragments
+  __device__ static int a(int w, int mt, int kb) { return w * PER_WAVE + mt * G::EB + kb; }
+  __device__ static int b(int w, int kb, int et) { return w * PER_WAVE + NA + kb * G::ET + et; }
+};
+
 // Row range of tile j of a head, for slices of length C (already clamped to
 // [1, L]).  Slices longer than TR are cut into TR-row tiles from the slice
 // start; the last slice may be ragged.
@@ -94,5 +109,50 @@ __device__ __forceinline__ void load_rows(T* dst, const T* src, int count, float
     }
   }
 }
+
+// Register staging of a [count x D] row block (rows >= count read as zero):
+// fetch() issues the global loads, store() writes LDS (pitch LD) and
+// optionally the squared row norms.  Splitting the two lets the loads of the
+// next tile overlap the compute of the current one.
+template <typename T, int D, int TR, int NT>
+struct RowStage {
+  static constexpr int VEC = 16 / sizeof(T);
+  static constexpr int CPR = D / VEC;  // 16-byte chunks per row
+  static constexpr int NCH = TR * CPR;
+  static constexpr int PER = (NCH + NT - 1) / NT;
+  uint4 v[PER];
+
+  __device__ __forceinline__ void fetch(const T* src, int count) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int ch = threadIdx.x + i * NT;
+      const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
+      v[i] = uint4{0u, 0u, 0u, 0u};
+      if (ch < NCH && r < count) v[i] = *reinterpret_cast<const uint4*>(src + (size_t)r * D + cc * VEC);
+    }
+  }
+  template <int LD>
+  __device__ __forceinline__ void store(T* dst, float* norms) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int ch = threadIdx.x + i * NT;
+      const bool active = ch < NCH;
+      const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
+      if (active) *reinterpret_cast<uint4*>(dst + r * LD + cc * VEC) = v[i];
+      if (norms != nullptr) {
+        float s = 0.f;
+        const T* e = reinterpret_cast<const T*>(&v[i]);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+          const float x = to_f32(e[k]);
+          s += x * x;
+        }
+#pragma unroll
+        for (int o = 1; o < CPR; o <<= 1) s += __shfl_xor(s, o, 64);
+        if (active && cc == 0) norms[r] = s;
+      }
+    }
+  }
+};
 
 }  // namespace slim

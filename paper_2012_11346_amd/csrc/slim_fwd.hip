@@ -536,7 +536,46 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Fragment-ordered copy of W: one block per fragment, one thread per lane.
+template <class G>
+__global__ __launch_bounds__(64) void wfrag_kernel(WfragArgs a) {
+  typedef typename G::T T;
+  typedef typename FragT<T>::type F;
+  typedef WFragLayout<G> WL;
+  const int f = blockIdx.x, lane = threadIdx.x;
+  const int g = lane >> 4, c = lane & 15;
+  const int w = f / WL::PER_WAVE;
+  int i = f - w * WL::PER_WAVE;
+  F v;
+  if (i < WL::NA) {
+    const int mt = i / G::EB, kb = i - (i / G::EB) * G::EB;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) v[s] = cvt<T>(a.W[(size_t)(w * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)]);
+  } else {
+    i -= WL::NA;
+    const int kb = i / G::ET, et = i - (i / G::ET) * G::ET;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int m = 32 * kb + kp(g, s);
+      v[s] = cvt<T>(m < G::FW ? a.W[(size_t)(w * G::FW + m) * G::D + 16 * et + c] : 0.f);
+    }
+  }
+  reinterpret_cast<F*>(a.out)[(size_t)f * 64 + lane] = v;
+}
+
+// ---------------------------------------------------------------------------
 // launchers
+
+template <class G>
+size_t wfrag_bytes() {
+  return (size_t)WFragLayout<G>::TOTAL * 64 * sizeof(typename FragT<typename G::T>::type);
+}
+
+template <class G>
+hipError_t launch_wfrag(const WfragArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(wfrag_kernel<G>, dim3(WFragLayout<G>::TOTAL), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
 
 template <class G>
 hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s) {
@@ -563,6 +602,8 @@ hipError_t launch_featmap(const FeatArgs& a, hipStream_t s) {
 }
 
 #define SLIM_INST_FWD(T, D, FW, TR, KIND)                                                     \
+  template size_t wfrag_bytes<Cfg<T, D, FW, TR, KIND>>();                                     \
+  template hipError_t launch_wfrag<Cfg<T, D, FW, TR, KIND>>(const WfragArgs&, hipStream_t);  \
   template hipError_t launch_fwd_walk<Cfg<T, D, FW, TR, KIND>>(const FwdArgs&, int, hipStream_t); \
   template hipError_t launch_featmap<Cfg<T, D, FW, TR, KIND>>(const FeatArgs&, hipStream_t);
 SLIM_FOR_EACH_CONFIG(SLIM_INST_FWD)

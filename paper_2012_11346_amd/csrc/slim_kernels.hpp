@@ -20,6 +20,7 @@ struct FwdArgs {
   const void* V;
   const void* dY;           // kWalkGrad
   const float* W;
+  const void* Wfrag;        // fragment-ordered W (WFragLayout)
   void* Y;                  // kWalkOutputs
   float* state_out;         // kWalkOutputs: [B,H,M,D+1] or nullptr (written by the last segment)
   float* kshift_out;        // kWalkOutputs: [B,H] or nullptr
@@ -44,6 +45,11 @@ struct ScanArgs {
   int BH, P, SZ, favor;
 };
 
+struct WfragArgs {
+  const float* W;
+  void* out;  // fragment-ordered W (WFragLayout), element type of the problem
+};
+
 struct FeatArgs {
   const void* X;
   const float* W;
@@ -59,6 +65,7 @@ struct BwdArgs {
   const void* V;
   const void* dY;
   const float* W;
+  const void* Wfrag;        // fragment-ordered W (WFragLayout)
   const float* kshift;      // [B,H] key shift of every state below (FAVOR+)
   const float* bounds;      // [B,H,P+1,M,D+1] exact state at each segment boundary
   const float* seg_gend;    // [B,H,P,M,D+1] state cotangent after each segment
@@ -83,6 +90,10 @@ hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s);
 hipError_t launch_scan_rev(const ScanArgs& a, hipStream_t s);
 template <class G>
 hipError_t launch_featmap(const FeatArgs& a, hipStream_t s);
+template <class G>
+hipError_t launch_wfrag(const WfragArgs& a, hipStream_t s);
+template <class G>
+size_t wfrag_bytes();
 template <class G>
 hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s);
 
