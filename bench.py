@@ -68,11 +68,11 @@ def load_traffic(kernel: str, units_per_launch: float):
     return k.get("bytes_per_launch")
 
 
-def cpu_baseline(x, C: int, H: int, L: int):
+def cpu_baseline(x, C: int, B: int, H: int, L: int):
     """Time the fp64 oracle (Algorithm 1 with the in-slice quadratic form) on
-    batch element 0: all heads, full length.  Returns the record and the
-    oracle's Y/gradients for a parity spot check."""
-    import numpy as np
+    the whole batch of the workload (every batch element and head, full
+    length).  Returns the record and the oracle's Y/gradients for a parity
+    check of the timed configuration."""
     import oracle as O
 
     try:
@@ -81,18 +81,18 @@ def cpu_baseline(x, C: int, H: int, L: int):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    Q, K, V, dY = (x[k][:1] for k in ("Q", "K", "V", "dY"))
+    Q, K, V, dY = (x[k] for k in ("Q", "K", "V", "dY"))
     t0 = time.perf_counter()
     Y, st = O.slim_forward(Q, K, V, x["W"], C, "favor+", within="quadratic")
     g = O.slim_backward(Q, K, V, x["W"], dY, C, "favor+", st, within="quadratic")
     t = time.perf_counter() - t0
     rec = {
-        "value": L / t,
+        "value": B * L / t,
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"batch element 0 of the workload (all {H} heads, L={L}), fp64 Algorithm 1 with the "
-        f"in-slice quadratic form at C={C}; {t:.1f} s on the host",
+        "sample": f"the whole workload batch (B={B}, H={H}, L={L}), fp64 Algorithm 1 forward + backward with "
+        f"the in-slice quadratic form at C={C}; {t:.1f} s on the host",
         "seconds": t,
         "host_cpus": os.cpu_count(),
     }
@@ -157,34 +157,41 @@ def main():
                  dW=b["dW"])
 
     def timed(C, steps, warmup):
+        """warmup + `steps` timed steps.  Per step: the whole step, the
+        forward and backward calls, and each call's walk kernel alone
+        (events the library records around that launch)."""
+        torch.cuda.synchronize()
+        pre = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
         p, b = buffers(C)
         for _ in range(warmup):
             step(C, b)
-        torch.cuda.synchronize()
-        torch.cuda.reset_peak_memory_stats()
-        base = torch.cuda.memory_allocated()
         stream = torch.cuda.current_stream()
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        mk = lambda: torch.cuda.Event(enable_timing=True)
+        ev = [[mk() for _ in range(7)] for _ in range(steps)]
+        for e in ev:  # create every event before the timed region
+            for x_ in e:
+                x_.record(stream)
         torch.cuda.synchronize()
-        start.record(stream)
         for i in range(steps):
-            ev[i][0].record(stream)
+            e = ev[i]
+            e[0].record(stream)
+            slim.time_walk(slim.PHASE_FWD, e[1], e[2])
             slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
-            ev[i][1].record(stream)
+            e[3].record(stream)
+            slim.time_walk(slim.PHASE_BWD, e[4], e[5])
             slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
                      dW=b["dW"])
-            ev[i][2].record(stream)
-        end.record(stream)
+            e[6].record(stream)
         torch.cuda.synchronize()
-        total_ms = start.elapsed_time(end)
-        fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
-        bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
+        total_ms = ev[0][0].elapsed_time(ev[-1][6])
+        avg = lambda i, j: sum(e[i].elapsed_time(e[j]) for e in ev) / steps
         peak = torch.cuda.max_memory_allocated()
         out_bytes = sum(t.numel() * t.element_size() for k, t in b.items() if not k.startswith("ws"))
-        return dict(total_ms=total_ms, ms=total_ms / steps, fwd_ms=fwd_ms, bwd_ms=bwd_ms, peak=peak,
-                    extra=peak - io_bytes - out_bytes, out_bytes=out_bytes, ws_fwd=b["wsf"].numel(),
-                    ws_bwd=b["wsb"].numel(), segments=slim.num_segments(p)), b
+        return dict(total_ms=total_ms, ms=total_ms / steps, fwd_ms=avg(0, 3), bwd_ms=avg(3, 6),
+                    fwd_walk_ms=avg(1, 2), bwd_walk_ms=avg(4, 5), peak=peak, extra=peak - pre - out_bytes,
+                    out_bytes=out_bytes, ws_fwd=b["wsf"].numel(), ws_bwd=b["wsb"].numel(),
+                    segments=slim.num_segments(p)), b
 
     C = args.C
     print(f"[bench] timing C={C}: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
@@ -192,12 +199,13 @@ def main():
     tokens = B * L
     value = tokens / (r["ms"] / 1e3)
     fl_f, fl_b = algo_flops_per_token_head(d, M, C)
-    units = B * H * L  # token-heads per launch
-    bwd_flops = fl_b * units
-    achieved = bwd_flops / (r["bwd_ms"] / 1e3)
-    dominant = "bwd_walk_kernel" if r["bwd_ms"] >= r["fwd_ms"] else "fwd_walk_kernel"
-    dom_ms = max(r["bwd_ms"], r["fwd_ms"])
-    dom_flops = bwd_flops if dominant == "bwd_walk_kernel" else fl_f * units
+    units = B * H * L  # token-heads per launch of either walk kernel
+    # the walk kernels do all of the algorithmic work of their phase; the
+    # segment pre-passes and scans are extra work of the parallel split
+    if r["bwd_walk_ms"] >= r["fwd_walk_ms"]:
+        dominant, dom_ms, dom_flops = "bwd_walk_kernel", r["bwd_walk_ms"], fl_b * units
+    else:
+        dominant, dom_ms, dom_flops = "fwd_walk_kernel", r["fwd_walk_ms"], fl_f * units
     achieved = dom_flops / (dom_ms / 1e3)
     traffic = load_traffic(dominant, units)
     out = {
@@ -221,6 +229,8 @@ def main():
         },
         "fwd_ms": r["fwd_ms"],
         "bwd_ms": r["bwd_ms"],
+        "fwd_walk_ms": r["fwd_walk_ms"],
+        "bwd_walk_ms": r["bwd_walk_ms"],
         "roofline": {
             "kernel": dominant,
             "bound": "mfma",
@@ -230,6 +240,7 @@ def main():
             "frac": achieved / PEAK_BF16_FLOPS,
             "traffic": traffic,
             "flops_per_token_head": {"fwd": fl_f, "bwd": fl_b},
+            "token_heads_per_launch": units,
             "launch_ms": dom_ms,
         },
         "mfma_frac_fwd_bwd": (fl_f + fl_b) * units / (r["ms"] / 1e3) / PEAK_BF16_FLOPS,
@@ -237,13 +248,14 @@ def main():
                      "beyond_io_bytes": r["extra"],
                      "workspace_fwd": r["ws_fwd"], "workspace_bwd": r["ws_bwd"]},
     }
-    print(f"[bench] C={C}: {r['ms']:.3f} ms/step (fwd {r['fwd_ms']:.3f}, bwd {r['bwd_ms']:.3f}), "
-          f"{value:.3e} tokens/s", file=sys.stderr, flush=True)
+    print(f"[bench] C={C}: {r['ms']:.3f} ms/step (fwd {r['fwd_ms']:.3f}, bwd {r['bwd_ms']:.3f}; walks "
+          f"{r['fwd_walk_ms']:.3f} / {r['bwd_walk_ms']:.3f}), {value:.3e} tokens/s", file=sys.stderr, flush=True)
 
     if not args.no_sweep:
         sweep = []
         for Cs in wl.C:
-            rs, _ = timed(Cs, args.sweep_steps, 1)
+            rs, bs = timed(Cs, args.sweep_steps, 1)
+            del bs
             sweep.append({"C": Cs, "tokens_per_s": tokens / (rs["ms"] / 1e3), "ms_per_step": rs["ms"],
                           "peak_bytes": rs["peak"], "beyond_io_bytes": rs["extra"], "workspace_bwd": rs["ws_bwd"]})
             print(f"[bench] sweep C={Cs}: {rs['ms']:.3f} ms/step, extra memory {rs['extra'] / 2**20:.1f} MiB",
@@ -252,20 +264,15 @@ def main():
 
     if not args.no_cpu:
         print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
-        rec, Yo, go = cpu_baseline(x, C, H, L)
+        rec, Yo, go = cpu_baseline(x, C, B, H, L)
         out["cpu_baseline"] = rec
-        # spot check of the timed configuration against the oracle (batch element 0)
-        Yg = b["Y"][:1].double().cpu().numpy()
 
+        # parity of the timed configuration against the oracle, whole batch
         def mr(a, ref):
-            return float(np.max(np.abs(a - ref)) / np.max(np.abs(ref)))
+            return float(np.max(np.abs(a.double().cpu().numpy() - ref)) / np.max(np.abs(ref)))
 
-        out["parity_batch0"] = {
-            "Y": mr(Yg, Yo),
-            "dQ": mr(b["dQ"][:1].double().cpu().numpy(), go[0]),
-            "dK": mr(b["dK"][:1].double().cpu().numpy(), go[1]),
-            "dV": mr(b["dV"][:1].double().cpu().numpy(), go[2]),
-        }
+        out["parity"] = {"Y": mr(b["Y"], Yo), "dQ": mr(b["dQ"], go[0]), "dK": mr(b["dK"], go[1]),
+                         "dV": mr(b["dV"], go[2]), "dW": mr(b["dW"], go[3])}
     print(json.dumps(out), flush=True)
 
 

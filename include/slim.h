@@ -141,6 +141,17 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
              const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
              void* ws, size_t ws_bytes, void* stream);
 
+/* Kernel-timing instrumentation.  before and after are hipEvent_t handles
+ * (passed as void*) created by the caller with timing enabled.  The next
+ * slim_fwd (phase SLIM_PHASE_FWD) or slim_bwd (SLIM_PHASE_BWD) call made by
+ * this host thread records `before` and `after` on its stream immediately
+ * around the launch of its main walk kernel (the forward walk that writes Y,
+ * the reverse walk of the backward), so the caller can read that kernel's
+ * own duration; the other launches of the call fall outside the pair.  The
+ * setting is consumed by that one call.  NULL for both clears it.
+ * Returns SLIM_OK, or SLIM_EINVAL for an unknown phase or only one NULL. */
+int slim_time_walk(int phase, void* before, void* after);
+
 /* Static description of a status code. */
 const char* slim_status_string(int status);
 

@@ -18,6 +18,25 @@ namespace {
 
 thread_local std::string g_last_error;
 
+// events set by slim_time_walk, per phase; consumed by the next call
+struct WalkTimer {
+  hipEvent_t before = nullptr, after = nullptr;
+};
+thread_local WalkTimer g_timer[2];
+
+// launch `run` between the phase's timing events, if any were set
+template <class F>
+hipError_t timed_launch(int phase, hipStream_t s, F run) {
+  WalkTimer t = g_timer[phase];
+  g_timer[phase] = WalkTimer();
+  hipError_t e = hipSuccess;
+  if (t.before != nullptr && (e = hipEventRecord(t.before, s)) != hipSuccess) return e;
+  e = run();
+  if (e != hipSuccess) return e;
+  if (t.after != nullptr) e = hipEventRecord(t.after, s);
+  return e;
+}
+
 int fail(int status, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -212,6 +231,14 @@ const char* slim_status_string(int status) {
 
 const char* slim_last_error(void) { return g_last_error.c_str(); }
 
+int slim_time_walk(int phase, void* before, void* after) {
+  if (phase != SLIM_PHASE_FWD && phase != SLIM_PHASE_BWD) return fail(SLIM_EINVAL, "unknown phase %d", phase);
+  if ((before == nullptr) != (after == nullptr)) return fail(SLIM_EINVAL, "set both events or neither");
+  g_timer[phase].before = (hipEvent_t)before;
+  g_timer[phase].after = (hipEvent_t)after;
+  return ok();
+}
+
 int slim_num_segments(const slim_problem* p) {
   if (check_problem(p) != SLIM_OK) return 0;
   return plan_segments(p);
@@ -313,7 +340,7 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.Y = Y;
   a.state_out = state_out;
   a.kshift_out = favor ? kshift_out : nullptr;
-  e = dp.fwd(a, slim::kWalkOutputs, s);
+  e = timed_launch(SLIM_PHASE_FWD, s, [&] { return dp.fwd(a, slim::kWalkOutputs, s); });
   if (e != hipSuccess) return hip_fail(e, "forward launch");
   return ok();
 }
@@ -431,8 +458,11 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.C = clamp_C(p);
   a.P = P;
   a.relu_eps = p->relu_eps;
-  e = dp.bwd(a, s);
+  e = timed_launch(SLIM_PHASE_BWD, s, [&] { return dp.bwd(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward launch");
+  // (5) dW: the workgroups' partials summed in a fixed order
+  e = slim::launch_dw_reduce(a.dW_part, BH * P, (int)(p->M * p->d), dW, s);
+  if (e != hipSuccess) return hip_fail(e, "dW-reduction launch");
   return ok();
 }
 

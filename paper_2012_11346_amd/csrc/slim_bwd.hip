@@ -688,10 +688,11 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* part, int n
 template <class G>
 hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(bwd_walk_kernel<G>, dim3(a.P, a.H, a.B), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int n = G::M * G::D;
-  hipLaunchKernelGGL(dw_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a.dW_part, a.B * a.H * a.P, n, a.dW);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s) {
+  hipLaunchKernelGGL(dw_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, s, part, n_parts, n, dW);
   return hipGetLastError();
 }
 

@@ -96,6 +96,8 @@ template <class G>
 size_t wfrag_bytes();
 template <class G>
 hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s);
+// dW = sum of the n_parts partials [n_parts][n], in a fixed order
+hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s);
 
 // every compiled (element type, head dim, features per wave, tile rows, kind);
 // fp32 problems serve exactness checks and are compiled for d * M <= 4096

@@ -69,6 +69,8 @@ def _load() -> ctypes.CDLL:
     lib.slim_status_string.restype = ctypes.c_char_p
     lib.slim_last_error.argtypes = []
     lib.slim_last_error.restype = ctypes.c_char_p
+    lib.slim_time_walk.argtypes = [i32, vp, vp]
+    lib.slim_time_walk.restype = i32
     return lib
 
 
@@ -82,6 +84,7 @@ EXPORTED = (
     "slim_status_string",
     "slim_last_error",
     "slim_num_segments",
+    "slim_time_walk",
 )
 
 
@@ -135,6 +138,17 @@ def workspace_bytes(p: Problem, phase: int) -> int:
 
 def num_segments(p: Problem) -> int:
     return int(LIB.slim_num_segments(ctypes.byref(p)))
+
+
+def time_walk(phase: int, before: "torch.cuda.Event", after: "torch.cuda.Event") -> None:
+    """Have the next fwd (phase PHASE_FWD) or bwd (PHASE_BWD) call of this
+    thread record the two timing events around its walk kernel only.  Events
+    not yet created (torch creates them lazily) are recorded once here on the
+    current stream so that they exist."""
+    for ev in (before, after):
+        if ev.cuda_event == 0:
+            ev.record()
+    _check(LIB.slim_time_walk(int(phase), ctypes.c_void_p(before.cuda_event), ctypes.c_void_p(after.cuda_event)))
 
 
 def _workspace(p: Problem, phase: int, device, ws: Optional[torch.Tensor]):

@@ -106,3 +106,12 @@ def test_relu_needs_positive_eps(S):
     p = _p(S, kind=S.RELU)
     p.relu_eps = 0.0
     assert S.LIB.slim_num_segments(ctypes.byref(p)) == 0
+
+
+def test_walk_timer_arguments(S):
+    """slim_time_walk validates its arguments on the host (no HIP call)."""
+    ev = ctypes.c_void_p(0x1000)
+    assert S.LIB.slim_time_walk(7, ev, ev) == S.SLIM_EINVAL
+    assert S.LIB.slim_time_walk(S.PHASE_BWD, ev, None) == S.SLIM_EINVAL
+    assert S.LIB.slim_time_walk(S.PHASE_FWD, None, None) == S.SLIM_OK
+    assert S.LIB.slim_time_walk(S.PHASE_BWD, None, None) == S.SLIM_OK
