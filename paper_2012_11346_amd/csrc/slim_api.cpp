@@ -165,7 +165,8 @@ typedef size_t (*size_fn)();
 struct Dispatch {
   fwd_fn fwd;
   feat_fn feat;
-  bwd_fn bwd;
+  bwd_fn bwd4;  // backward walk, 4 waves per workgroup
+  bwd_fn bwd8;  // backward walk, 8 waves per workgroup (nullptr where not built)
   wfrag_fn wfrag;
   size_fn wfrag_bytes;
 };
@@ -173,19 +174,34 @@ struct Dispatch {
 template <class T, int D, int FW, int KIND>
 Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
-  return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>,
+  return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>, nullptr,
                   &slim::launch_wfrag<G>, &slim::wfrag_bytes<G>};
+}
+template <int D, int FW, int KIND>
+Dispatch make_dispatch8() {
+  Dispatch d = make_dispatch<slim::bf16, D, FW, KIND>();
+  d.bwd8 = &slim::launch_bwd_walk8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
+  return d;
+}
+
+// Backward walk kernel: the 8-wave form where it is built (bf16, 32 or 64
+// features per slice), else the 4-wave form.  SLIM_BWD_WAVES=4 (debugging)
+// forces the 4-wave form.
+bwd_fn pick_bwd(const Dispatch& d) {
+  const char* env = getenv("SLIM_BWD_WAVES");
+  if (d.bwd8 != nullptr && !(env != nullptr && atoi(env) == 4)) return d.bwd8;
+  return d.bwd4;
 }
 
 template <int KIND>
 Dispatch pick_bf16(int d, int M) {
   if (d == 64) {
-    if (M == 256) return make_dispatch<slim::bf16, 64, 64, KIND>();
-    if (M == 128) return make_dispatch<slim::bf16, 64, 32, KIND>();
+    if (M == 256) return make_dispatch8<64, 64, KIND>();
+    if (M == 128) return make_dispatch8<64, 32, KIND>();
     return make_dispatch<slim::bf16, 64, 16, KIND>();
   }
-  if (M == 256) return make_dispatch<slim::bf16, 32, 64, KIND>();
-  if (M == 128) return make_dispatch<slim::bf16, 32, 32, KIND>();
+  if (M == 256) return make_dispatch8<32, 64, KIND>();
+  if (M == 128) return make_dispatch8<32, 32, KIND>();
   return make_dispatch<slim::bf16, 32, 16, KIND>();
 }
 
@@ -458,7 +474,8 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.C = clamp_C(p);
   a.P = P;
   a.relu_eps = p->relu_eps;
-  e = timed_launch(SLIM_PHASE_BWD, s, [&] { return dp.bwd(a, s); });
+  const bwd_fn walk = pick_bwd(dp);
+  e = timed_launch(SLIM_PHASE_BWD, s, [&] { return walk(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward launch");
   // (5) dW: the workgroups' partials summed in a fixed order
   e = slim::launch_dw_reduce(a.dW_part, BH * P, (int)(p->M * p->d), dW, s);

@@ -28,71 +28,6 @@
 namespace slim {
 
 template <class G>
-__device__ __forceinline__ void load_w_frags_b_unused(typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
-                                               const float* W, int w) {
-  const int g = lane_g(), c = lane_c();
-#pragma unroll
-  for (int mt = 0; mt < G::MT; ++mt)
-#pragma unroll
-    for (int kb = 0; kb < G::EB; ++kb)
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        Wf[mt][kb][s] = cvt<typename G::T>(W[(size_t)(w * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)]);
-}
-
-// W fragments contracting over features: slot s = W[w FW + 32 kb + kp][16 et + c]
-template <class G>
-__device__ __forceinline__ void load_wt_frags(typename FragT<typename G::T>::type (&WT)[G::MB][G::ET],
-                                              const float* W, int w) {
-  const int g = lane_g(), c = lane_c();
-#pragma unroll
-  for (int kb = 0; kb < G::MB; ++kb)
-#pragma unroll
-    for (int et = 0; et < G::ET; ++et)
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int m = 32 * kb + kp(g, s);
-        WT[kb][et][s] = cvt<typename G::T>(m < G::FW ? W[(size_t)(w * G::FW + m) * G::D + 16 * et + c] : 0.f);
-      }
-}
-
-template <class G>
-__device__ __forceinline__ typename FragT<typename G::T>::type pair_or_half(const f32x4& a, const f32x4& b,
-                                                                             bool has_b) {
-  return has_b ? tile_pair_frag<typename G::T>(a, b) : tile_half_frag<typename G::T>(a);
-}
-
-// fragment slot s = Z[row0 + c][k0 + kp(g, s)], with slots 4..7 zero when the
-// 32-deep block has only its first 16 entries
-template <typename T>
-__device__ __forceinline__ typename FragT<T>::type frag_rm_h(const T* Z, int ld, int row0, int k0, bool half) {
-  if (!half) return frag_rm(Z, ld, row0, k0);
-  const int g = lane_g(), c = lane_c();
-  const T* p = Z + (row0 + c) * ld + k0 + 4 * g;
-  typename FragT<T>::type f;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    f[r] = p[r];
-    f[4 + r] = cvt<T>(0.f);
-  }
-  return f;
-}
-
-// result-tile values of a matrix stored transposed by store_tile_T:
-// X[row0 + 4g + r][col0 + c] = Z[col0 + c][row0 + 4g + r]
-template <typename T>
-__device__ __forceinline__ f32x4 load_tile_T(const T* Z, int ld, int row0, int col0) {
-  const int g = lane_g(), c = lane_c();
-  const T* p = Z + (col0 + c) * ld + row0 + 4 * g;
-  f32x4 x;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) x[r] = to_f32(p[r]);
-  return x;
-}
-
-constexpr size_t al16(size_t n) { return (n + 15) & ~(size_t)15; }
-
-template <class G>
 struct BwdLds {
   typedef typename G::T T;
   static constexpr int D = G::D, FW = G::FW, TR = G::TR, ZR = G::ZR, LDQ = G::LDQ, LDR = G::LDR;
@@ -214,10 +149,10 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   if (j1 > j0) {
     int st0, cn0;
     tm.tile(j1 - 1, st0, cn0);
-    sq.fetch(Qh + (size_t)st0 * D, cn0);
-    sk.fetch(Kh + (size_t)st0 * D, cn0);
-    sv.fetch(Vh + (size_t)st0 * D, cn0);
-    sdy.fetch(dYh + (size_t)st0 * D, cn0);
+    sq.fetch(Qh + (size_t)st0 * D, cn0, threadIdx.x);
+    sk.fetch(Kh + (size_t)st0 * D, cn0, threadIdx.x);
+    sv.fetch(Vh + (size_t)st0 * D, cn0, threadIdx.x);
+    sdy.fetch(dYh + (size_t)st0 * D, cn0, threadIdx.x);
   }
 
   // [V|1] operand over rows [32 rb, 32 rb + 32) for value tile et (et == ET: ones)
@@ -238,17 +173,17 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = Wfr[WL::a(w, mt, kb) * 64 + lane];
-    sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr);
-    sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr);
-    sv.template store<LDQ>(Vs, nullptr);
-    sdy.template store<LDQ>(dYs, nullptr);
+    sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr, threadIdx.x);
+    sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, threadIdx.x);
+    sv.template store<LDQ>(Vs, nullptr, threadIdx.x);
+    sdy.template store<LDQ>(dYs, nullptr, threadIdx.x);
     if (j > j0) {  // next tile's loads overlap this tile's compute
       int sn, cnn;
       tm.tile(j - 1, sn, cnn);
-      sq.fetch(Qh + (size_t)sn * D, cnn);
-      sk.fetch(Kh + (size_t)sn * D, cnn);
-      sv.fetch(Vh + (size_t)sn * D, cnn);
-      sdy.fetch(dYh + (size_t)sn * D, cnn);
+      sq.fetch(Qh + (size_t)sn * D, cnn, threadIdx.x);
+      sk.fetch(Kh + (size_t)sn * D, cnn, threadIdx.x);
+      sv.fetch(Vh + (size_t)sn * D, cnn, threadIdx.x);
+      sdy.fetch(dYh + (size_t)sn * D, cnn, threadIdx.x);
     }
     __syncthreads();
 
@@ -378,7 +313,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           if (2 * rb <= tt) acc = mma(acc, v_frag(rb, et, count), frag_rm(ZA, LDZT, 16 * tt, 32 * rb));
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, pair_or_half<G>(S[2 * kb][et], S[half_m(kb) ? 2 * kb : 2 * kb + 1][et], !half_m(kb)),
+          acc = mma(acc, pair_or_half<T>(S[2 * kb][et], S[half_m(kb) ? 2 * kb : 2 * kb + 1][et], !half_m(kb)),
                     frag_rm_h(Zq, LDZF, 16 * tt, 32 * kb, half_m(kb)));
         if (et < ET) {
           store_tile_T<float>(Redw, LDR, acc, 16 * et, 16 * tt);
@@ -445,7 +380,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
         f32x4 acc = zero4();
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, pair_or_half<G>(Gs[2 * kb][et], Gs[half_m(kb) ? 2 * kb : 2 * kb + 1][et], !half_m(kb)),
+          acc = mma(acc, pair_or_half<T>(Gs[2 * kb][et], Gs[half_m(kb) ? 2 * kb : 2 * kb + 1][et], !half_m(kb)),
                     frag_tr(Zk, LDZK, 32 * kb, 16 * st));
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)

@@ -1,0 +1,660 @@
+// Backward sweep (Algorithm 1, one layer) with 8 waves per workgroup.
+//
+// Same computation as bwd_walk_kernel (reverse walk over the tiles of one
+// segment: downdate of the state B by eq. 17, recomputation of the tile,
+// gradients, update of the state cotangent G by eq. 18), with the work of a
+// feature slice shared by a pair of waves so that each wave holds half of
+// the running state:
+//
+//   wave w = 4 h + f   feature slice f (features [f FW, (f + 1) FW)), half h
+//   value columns      wave h owns the columns [16 EH h, 16 EH (h + 1)) of
+//                      S = sum K~^T V, of G and of its dW rows; half 0 also
+//                      owns the ones column (z = sum K~ and its cotangent)
+//   tile rows          products whose output rows are tile rows and whose
+//                      contraction runs over all value columns (dQ~, dK~) are
+//                      split by 16-row halves of the tile: half h takes rows
+//                      [16 h, 16 h + 16)
+//
+// Both waves of a pair compute the query features of the whole tile and
+// write identical values into the pair's LDS copy; the same holds for the
+// in-tile scores A^T and their cotangent dA^T.  Cross-slice sums (N, dV, dq,
+// dk) go through per-wave reduction rows in LDS.  The per-wave register set
+// (state half, cotangent half, dW half) is about half of the 4-wave kernel's,
+// which removes its register spills at M = 256 and puts two waves on every
+// SIMD.
+//
+// Phases of one tile (| = workgroup barrier):
+//   features (Q~ logits of the tile, K~ of this wave's 16 rows) | Q~ -> LDS,
+//   downdate, scores, N partials | dN, dD | dA^T, dV partials | dV sums,
+//   S -> LDS | dQ~ (this wave's 16 rows), P = dQ~ . Q~ | dq partials, dW | dq
+//   sums, G -> LDS | dK~ (16 rows), Pk, G update | dk partials, dW | dk sums,
+//   next tile's rows -> LDS |
+#include "slim_common.hpp"
+#include "slim_kernels.hpp"
+
+namespace slim {
+
+template <class G>
+struct Bwd8Lds {
+  typedef typename G::T T;
+  static constexpr int D = G::D, FW = G::FW, TR = G::TR, ZR = G::ZR, LDQ = G::LDQ;
+  static constexpr int EH = G::ET / 2;          // value tiles per wave
+  static constexpr int LDZK = TR + 8;           // [feature][row] buffers (K~, Pk)
+  static constexpr int LDZF = FW + 8;           // [row or value column][feature] buffers (Q~, P, S, G)
+  static constexpr int LDZT = TR + 8;           // [row][row] buffers (A^T, dA^T)
+  static constexpr int LDRH = 16 * EH + 4;      // reduction row pitch (floats): own columns, then the ones column
+  // shared: Q, K, V, dY (dN overwrites dY), floats, dD as T
+  static constexpr size_t TILE = al16((size_t)TR * LDQ * sizeof(T));
+  static constexpr size_t oQ = 0, oK = TILE, oV = 2 * TILE, odY = 3 * TILE, oF = 4 * TILE;
+  // floats: qn[TR] kn[TR] qmx[4][TR] dDs[TR] rsum[4][TR] zs[4][FW] dzs[4][FW]
+  static constexpr size_t NF = 2 * TR + 4 * TR + TR + 4 * TR + 8 * FW;
+  static constexpr size_t odDb = oF + al16(NF * sizeof(float));
+  static constexpr size_t oP = odDb + al16((TR + 8) * sizeof(T));
+  // per pair: one block holding all of the pair's buffers, so that a lane
+  // reaches every buffer of its pair from one address register per access
+  // pattern plus immediate offsets
+  static constexpr size_t ZK = al16((size_t)ZR * LDZK * sizeof(T));
+  static constexpr size_t ZQ = al16((size_t)TR * LDZF * sizeof(T));
+  static constexpr size_t ZDA = al16((size_t)TR * LDZT * sizeof(T));
+  static constexpr size_t max3(size_t a, size_t b, size_t c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
+  static constexpr size_t RED = 2 * (size_t)TR * LDRH * sizeof(float);  // reduction rows of both waves
+  static constexpr size_t ZSG = (size_t)D * LDZF * sizeof(T);
+  // Y: N / dV reduction rows, then P (as [t][m]), then G (as [e][m]), then dk reduction rows
+  static constexpr size_t ZY = al16(max3(RED, (size_t)TR * LDZF * sizeof(T), ZSG));
+  // X: A^T, then S (as [e][m]), then dq reduction rows, then Pk (as [m][s])
+  static constexpr size_t ZX = al16(max3((size_t)TR * LDZT * sizeof(T), ZSG,
+                                         RED > (size_t)ZR * LDZK * sizeof(T) ? RED : (size_t)ZR * LDZK * sizeof(T)));
+  static constexpr size_t pY = 0, pX = ZY, pZk = pX + ZX, pZq = pZk + ZK, pZdA = pZq + ZQ, PAIR = pZdA + ZDA;
+  static constexpr size_t TOTAL = oP + 4 * PAIR;
+  static_assert(TOTAL <= 160 * 1024, "LDS budget of one workgroup");
+};
+
+template <class G>
+__global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
+  typedef typename G::T T;
+  typedef typename FragT<T>::type F;
+  typedef Bwd8Lds<G> Lay;
+  typedef WFragLayout<G> WL;
+  constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
+                RT = G::RT, LDQ = G::LDQ;
+  constexpr int EH = Lay::EH, LDZK = Lay::LDZK, LDZF = Lay::LDZF, LDZT = Lay::LDZT, LDRH = Lay::LDRH;
+  constexpr bool ODD = (MT & 1) != 0;  // last 32-deep feature block holds 16 features
+  constexpr int NT = 512, TPR = NT / TR, EPT = D / TPR;
+  static_assert(RT == 2 && G::RB == 1, "the two waves of a pair take one 16-row half of the tile each");
+  static_assert(ET % 2 == 0 && EPT >= 1, "");
+  // (an odd tile count would leave pad rows in buffers that alias float rows)
+  static_assert(!ODD, "features per wave must be a multiple of 32");
+
+  __shared__ __attribute__((aligned(16))) char arena[Lay::TOTAL];
+  T* Qs = (T*)(arena + Lay::oQ);
+  T* Ks = (T*)(arena + Lay::oK);
+  T* Vs = (T*)(arena + Lay::oV);
+  T* dYs = (T*)(arena + Lay::odY);
+  T* dNs = dYs;  // dN = dY / D overwrites dY row by row
+  float* fl = (float*)(arena + Lay::oF);
+  float* qn = fl;
+  float* kn = qn + TR;
+  float* qmx = kn + TR;        // [4][TR]
+  float* dDs = qmx + 4 * TR;   // [TR]
+  float* rsum = dDs + TR;      // [4][TR]
+  float* zs = rsum + 4 * TR;   // [4][FW]
+  float* dzs = zs + 4 * FW;    // [4][FW]
+  T* dDb = (T*)(arena + Lay::odDb);
+
+  // wave-uniform indices live in scalar registers
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), f = w & 3, h = w >> 2;
+  const int g = lane_g(), c = lane_c(), lane = lane_id();
+  const bool zown = (h == 0);  // this wave carries the ones column
+  char* pz = arena + Lay::oP + f * Lay::PAIR;
+  T* Zk = (T*)(pz + Lay::pZk);     // K~ as [m][s]
+  T* Zq = (T*)(pz + Lay::pZq);     // Q~ as [t][m]
+  T* ZdA = (T*)(pz + Lay::pZdA);  // dA^T as [t][s]
+  T* ZA = (T*)(pz + Lay::pX);      // A^T as [t][s]
+  T* ZS = ZA;                                       // S as [e][m]
+  T* ZPk = ZA;                                      // Pk as [m][s]
+  float* RedX = (float*)(pz + Lay::pX) + h * TR * LDRH;  // dq partial rows [t][e']
+  T* ZP = (T*)(pz + Lay::pY);      // P as [t][m]
+  T* ZG = ZP;                                       // G as [e][m]
+  float* RedY = (float*)(pz + Lay::pY) + h * TR * LDRH;  // N, dV, dk partial rows [t][e']
+  // sum over the 4 slices of reduction entry [t][col] of value half hh
+  auto sum_x = [&](int hh, int idx) -> float {
+    const float* r = (const float*)(arena + Lay::oP + Lay::pX) + hh * TR * LDRH + idx;
+    constexpr int S4 = Lay::PAIR / sizeof(float);
+    return (r[0] + r[S4]) + (r[2 * S4] + r[3 * S4]);
+  };
+  auto sum_y = [&](int hh, int idx) -> float {
+    const float* r = (const float*)(arena + Lay::oP + Lay::pY) + hh * TR * LDRH + idx;
+    constexpr int S4 = Lay::PAIR / sizeof(float);
+    return (r[0] + r[S4]) + (r[2 * S4] + r[3 * S4]);
+  };
+
+  const int p = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
+  const size_t head = (size_t)b * a.H + hd;
+  const size_t hoff = head * (size_t)a.L * D;
+  const T* Qh = (const T*)a.Q + hoff;
+  const T* Kh = (const T*)a.K + hoff;
+  const T* Vh = (const T*)a.V + hoff;
+  const T* dYh = (const T*)a.dY + hoff;
+  T* dQh = (T*)a.dQ + hoff;
+  T* dKh = (T*)a.dK + hoff;
+  T* dVh = (T*)a.dV + hoff;
+  // W fragments through a buffer resource: scalar base and fragment offset,
+  // one lane offset register for every fragment
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.Wfrag), (short)0, (int)(WL::TOTAL * 64 * sizeof(F)), 0x00020000);
+  const int wlane = lane * (int)sizeof(F);
+  auto wfrag = [&](int idx) -> F {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 v[sizeof(F) / 16];
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(F) / 16); ++i)
+      v[i] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane + 16 * i, idx * 64 * (int)sizeof(F), 0);
+    return __builtin_bit_cast(F, v);
+  };
+  const int e0 = 16 * EH * h;  // first value column of this wave
+
+  const size_t SZ = (size_t)M * (D + 1);
+  const size_t sidx = (head * a.P + p) * SZ;
+  const float* bstart = a.bounds + (head * (a.P + 1) + p) * SZ;
+  const float* bend = bstart + SZ;
+  float r0 = 1.f;
+  if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
+
+  // running state after the current tile (this wave's columns), its cotangent, dW rows
+  f32x4 S[MT][EH], Sz[MT], Gs[MT][EH], Gz[MT], dWacc[MT][EH];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const size_t row = (size_t)(f * FW + 16 * mt + 4 * g + r) * (D + 1);
+#pragma unroll
+      for (int et = 0; et < EH; ++et) {
+        S[mt][et][r] = bend[row + e0 + 16 * et + c];
+        Gs[mt][et][r] = a.seg_gend ? a.seg_gend[sidx + row + e0 + 16 * et + c] : 0.f;
+      }
+      Sz[mt][r] = zown ? bend[row + D] : 0.f;
+      Gz[mt][r] = (zown && a.seg_gend) ? a.seg_gend[sidx + row + D] : 0.f;
+    }
+#pragma unroll
+    for (int et = 0; et < EH; ++et) dWacc[mt][et] = zero4();
+  }
+
+  // every buffer starts at zero: pad rows of the [feature][row] buffers must read as zero
+  for (size_t i = (size_t)threadIdx.x * 16; i < Lay::TOTAL; i += (size_t)NT * 16)
+    *reinterpret_cast<uint4*>(arena + i) = uint4{0, 0, 0, 0};
+
+  const TileMap tm(a.L, a.C, TR);
+  const int n_tiles = tm.count_tiles();
+  const int j0 = (int)((int64_t)p * n_tiles / a.P), j1 = (int)((int64_t)(p + 1) * n_tiles / a.P);
+  const float half_log2M = 0.5f * __log2f((float)M);
+  const float koff = (G::KIND == kFavor) ? a.kshift[head] * kLog2e + half_log2M : 0.f;
+
+  // row staging: threads 0..255 carry Q and K, threads 256..511 carry V and dY
+  const int sh = threadIdx.x >> 8, stid = threadIdx.x & 255;
+  const T* srcA = sh ? Vh : Qh;
+  const T* srcB = sh ? dYh : Kh;
+  T* dstA = sh ? Vs : Qs;
+  T* dstB = sh ? dYs : Ks;
+  float* nrmA = (G::KIND == kFavor && !sh) ? qn : nullptr;
+  float* nrmB = (G::KIND == kFavor && !sh) ? kn : nullptr;
+  RowStage<T, D, TR, 256> stA, stB;
+  __syncthreads();  // zero fill done
+  if (j1 > j0) {
+    int s0, n0;
+    tm.tile(j1 - 1, s0, n0);
+    stA.fetch(srcA + (size_t)s0 * D, n0, stid);
+    stB.fetch(srcB + (size_t)s0 * D, n0, stid);
+    stA.template store<LDQ>(dstA, nrmA, stid);
+    stB.template store<LDQ>(dstB, nrmB, stid);
+    if (j1 - 1 > j0) {
+      tm.tile(j1 - 2, s0, n0);
+      stA.fetch(srcA + (size_t)s0 * D, n0, stid);
+      stB.fetch(srcB + (size_t)s0 * D, n0, stid);
+    }
+  }
+  __syncthreads();
+
+  // [V|1] operand over the tile's 32 rows for value tile et (et == ET: ones)
+  auto v_frag = [&](int et, int count) -> F {
+    if (et < ET) return frag_tr(Vs, LDQ, 0, 16 * et);
+    F v;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) v[s] = cvt<T>(kp(g, s) < count ? 1.f : 0.f);
+    return v;
+  };
+  // operand contracting over this slice's features m in [32 kb, 32 kb + 32),
+  // columns = own value tile el of X (el == EH: the ones column Xz)
+  auto feat_frag = [&](const f32x4 (&X)[MT][EH], const f32x4 (&Xz)[MT], int el, int kb) -> F {
+    return tile_pair_frag<T>(el < EH ? X[2 * kb][el] : Xz[2 * kb], el < EH ? X[2 * kb + 1][el] : Xz[2 * kb + 1]);
+  };
+
+  for (int j = j1 - 1; j >= j0; --j) {
+    int start, count;
+    tm.tile(j, start, count);
+
+    // ---- features: Q logits of the whole tile (both waves of the pair), K
+    //      logits of this wave's 16 rows; K~ -> Zk[m][s]
+    f32x4 Lq[MT][RT];
+    {
+      F Wf[MT][EB];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = wfrag(WL::a(f, mt, kb));
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) {
+        const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          f32x4 acc = {init, init, init, init};
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(Qs, LDQ, 16 * tt, 32 * kb));
+          Lq[mt][tt] = acc;
+        }
+      }
+      f32x4 kinit;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) kinit[r] = (G::KIND == kFavor) ? -0.5f * kn[16 * h + 4 * g + r] : 0.f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 kv = kinit;
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, frag_rm(Ks, LDQ, 16 * h, 32 * kb), Wf[mt][kb]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = 16 * h + 4 * g + r < count;
+          kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : fmaxf(kv[r], 0.f) + a.relu_eps;
+        }
+        store_tile_T<T>(Zk, LDZK, kv, 16 * h, 16 * mt);
+      }
+      if (G::KIND == kFavor && zown) {
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
+          v = wave_max_over_g(v);
+          if (g == 0) qmx[f * TR + 16 * tt + c] = v;
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair)
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt) {
+      const int t = 16 * tt + c;
+      float qs = 0.f;
+      if (G::KIND == kFavor) qs = fmaxf(fmaxf(qmx[t], qmx[TR + t]), fmaxf(qmx[2 * TR + t], qmx[3 * TR + t])) * kLog2e;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 qv = Lq[mt][tt];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          qv[r] = (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(qv[r] * kLog2e - qs) : fmaxf(qv[r], 0.f) + a.relu_eps;
+        store_tile_T<T>(Zq, LDZF, qv, 16 * mt, 16 * tt);
+      }
+    }
+
+    // ---- state before the tile: downdate (eq. 17), or the exact segment start
+    if (j == j0) {
+      const float* bs = bstart + (size_t)(f * FW) * (D + 1) + e0;
+      int lo = 4 * g * (D + 1) + c;
+      asm volatile("" : "+v"(lo));  // lane offsets are formed here, not kept live through the walk
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float* row = bs + lo + (16 * mt + r) * (D + 1);
+#pragma unroll
+          for (int et = 0; et < EH; ++et) S[mt][et][r] = row[16 * et];
+          if (zown) Sz[mt][r] = row[D - e0 - c];
+        }
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        F kf = frag_rm(Zk, LDZK, 16 * mt, 0);  // K~ contracting over rows
+#pragma unroll
+        for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
+#pragma unroll
+        for (int et = 0; et < EH; ++et) S[mt][et] = mma(S[mt][et], kf, v_frag(h * EH + et, count));
+        if (zown) Sz[mt] = mma(Sz[mt], kf, v_frag(ET, count));
+      }
+    }
+
+    // ---- scores A^T[s][t] over this slice's features, causal -> ZA[t][s]
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+      for (int st = 0; st < RT; ++st) {
+        f32x4 acc = zero4();
+        if (st <= tt) {
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb)
+            acc = mma(acc, frag_tr(Zk, LDZK, 32 * kb, 16 * st), frag_rm(Zq, LDZF, 16 * tt, 32 * kb));
+        }
+        if (st == tt) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (4 * g + r > c) acc[r] = 0.f;
+        }
+        store_tile_T<T>(ZA, LDZT, acc, 16 * st, 16 * tt);
+      }
+    // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+      for (int el = 0; el <= EH; ++el) {
+        if (el == EH && !zown) continue;
+        const int et = (el < EH) ? h * EH + el : ET;
+        f32x4 acc = mma(zero4(), v_frag(et, count), frag_rm(ZA, LDZT, 16 * tt, 0));
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), frag_rm(Zq, LDZF, 16 * tt, 32 * kb));
+        if (el < EH) {
+          store_tile_T<float>(RedY, LDRH, acc, 16 * el, 16 * tt);
+        } else if (g == 0) {
+          RedY[(16 * tt + c) * LDRH + 16 * EH] = acc[0];
+        }
+      }
+    __syncthreads();
+
+    // ---- dN = dY / D, dD = -(dY . N) / D^2 per row (TPR threads per row)
+    {
+      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      const bool ok = t < count;
+      const float den = sum_y(0, t * LDRH + 16 * EH);
+      const float inv = ok ? 1.f / den : 0.f;
+      float dy[EPT];
+      float dot = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) {
+        const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
+        dy[i] = to_f32(dYs[t * LDQ + e]);
+        const float n = sum_y(hh, t * LDRH + col);
+        dot += dy[i] * (n * inv);
+      }
+#pragma unroll
+      for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * inv);
+      if (q == 0) {
+        const float dd = ok ? -dot * inv : 0.f;
+        dDs[t] = dd;
+        dDb[t] = cvt<T>(dd);
+      }
+    }
+    __syncthreads();
+
+    // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal, rows < count -> ZdA[t][s]
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt) {
+      const float ddt = dDs[16 * tt + c];
+#pragma unroll
+      for (int st = 0; st <= tt; ++st) {
+        f32x4 acc = f32x4{ddt, ddt, ddt, ddt};
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb)
+          acc = mma(acc, frag_rm(Vs, LDQ, 16 * st, 32 * kb), frag_rm(dNs, LDQ, 16 * tt, 32 * kb));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int sr = 16 * st + 4 * g + r;
+          if ((st == tt && 4 * g + r > c) || sr >= count) acc[r] = 0.f;
+        }
+        store_tile_T<T>(ZdA, LDZT, acc, 16 * st, 16 * tt);
+      }
+      if (tt == 0) store_tile_T<T>(ZdA, LDZT, zero4(), 16, 0);  // s in [16, 32) for t in [0, 16)
+    }
+    // dV^T[e][s] = sum_m G[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t], own columns -> RedY[s][e']
+#pragma unroll
+    for (int st = 0; st < RT; ++st)
+#pragma unroll
+      for (int el = 0; el < EH; ++el) {
+        f32x4 acc = mma(zero4(), frag_tr(dNs, LDQ, 0, 16 * (h * EH + el)), frag_tr(ZA, LDZT, 0, 16 * st));
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), frag_tr(Zk, LDZK, 32 * kb, 16 * st));
+        store_tile_T<float>(RedY, LDRH, acc, 16 * el, 16 * st);
+      }
+    __syncthreads();
+
+    // ---- dV = sum over slices; S (own columns) -> ZS[e][m], z -> zs
+    {
+      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      if (t < count) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
+          const float v = sum_y(hh, t * LDRH + col);
+          dVh[(size_t)(start + t) * D + e] = cvt<T>(v);
+        }
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+      for (int el = 0; el < EH; ++el) store_tile_T<T>(ZS, LDZF, S[mt][el], 16 * mt, e0 + 16 * el);
+      if (zown && c == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) zs[f * FW + 16 * mt + 4 * g + r] = Sz[mt][r];
+      }
+    }
+    __syncthreads();
+
+    // ---- dQ~^T[m][t] = sum_e S[m][e] dN[t][e] + z[m] dD[t] + sum_s K~[s][m] dA^T[s][t]
+    //      for this wave's rows t in [16 h, 16 h + 16); P = dQ~ . Q~ (FAVOR+) or
+    //      dQ~ masked (ReLU) -> ZP[t][m]; row sums of P over the slice -> rsum
+    {
+      const float ddt = dDs[16 * h + c];
+      float rs = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 acc;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] = zs[f * FW + 16 * mt + 4 * g + r] * ddt;
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb)
+          acc = mma(acc, frag_tr(ZS, LDZF, 32 * kb, 16 * mt), frag_rm(dNs, LDQ, 16 * h, 32 * kb));
+        acc = mma(acc, frag_rm(Zk, LDZK, 16 * mt, 0), frag_rm(ZdA, LDZT, 16 * h, 0));
+        const f32x4 qv = load_tile_T(Zq, LDZF, 16 * mt, 16 * h);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
+          rs += acc[r];
+        }
+        store_tile_T<T>(ZP, LDZF, acc, 16 * mt, 16 * h);
+      }
+      if (G::KIND == kFavor) {
+        rs = wave_sum_over_g(rs);
+        if (g == 0) rsum[f * TR + 16 * h + c] = rs;
+      }
+    }
+    __syncthreads();
+
+    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] - q[t][e] rowsum_f(P)[t], own columns -> RedX[t][e'];
+    //      dW[m][e] += sum_t P[t][m] Q[t][e]
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt) {
+      const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * tt + c] : 0.f;
+#pragma unroll
+      for (int el = 0; el < EH; ++el) {
+        const int et = h * EH + el;
+        f32x4 acc;
+        if (G::KIND == kFavor) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Qs[(16 * tt + c) * LDQ + 16 * et + 4 * g + r]) * rsv;
+        } else {
+          acc = zero4();
+        }
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb)
+          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_rm(ZP, LDZF, 16 * tt, 32 * kb));
+        store_tile_T<float>(RedX, LDRH, acc, 16 * el, 16 * tt);
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const F pf = frag_tr(ZP, LDZF, 0, 16 * mt);
+#pragma unroll
+      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(Qs, LDQ, 0, e0 + 16 * el));
+    }
+    __syncthreads();
+
+    // ---- dq = sum over slices; G (own columns) -> ZG[e][m], dz -> dzs
+    {
+      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      if (t < count) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
+          const float v = sum_x(hh, t * LDRH + col);
+          dQh[(size_t)(start + t) * D + e] = cvt<T>(v);
+        }
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+      for (int el = 0; el < EH; ++el) store_tile_T<T>(ZG, LDZF, Gs[mt][el], 16 * mt, e0 + 16 * el);
+      if (zown && c == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dzs[f * FW + 16 * mt + 4 * g + r] = Gz[mt][r];
+      }
+    }
+    __syncthreads();
+
+    // ---- dK~[s][m] = sum_e V[s][e] G[m][e] + dz[m] + sum_t dA^T[s][t] Q~[t][m] for this
+    //      wave's rows s in [16 h, 16 h + 16); Pk = dK~ . K~ (FAVOR+) or masked (ReLU)
+    //      -> ZPk[m][s]; row sums -> rsum
+    {
+      float rk[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 acc;
+        const float dz = dzs[f * FW + 16 * mt + c];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] = (16 * h + 4 * g + r < count) ? dz : 0.f;
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb)
+          acc = mma(acc, frag_rm(Vs, LDQ, 16 * h, 32 * kb), frag_tr(ZG, LDZF, 32 * kb, 16 * mt));
+        acc = mma(acc, frag_tr(ZdA, LDZT, 0, 16 * h), frag_tr(Zq, LDZF, 0, 16 * mt));
+        const f32x4 kv = load_tile_T(Zk, LDZK, 16 * h, 16 * mt);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
+          rk[r] += acc[r];
+        }
+        store_tile_T<T>(ZPk, LDZK, acc, 16 * h, 16 * mt);
+      }
+      if (G::KIND == kFavor) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float v = wave_sum_over_c(rk[r]);
+          if (c == 0) rsum[f * TR + 16 * h + 4 * g + r] = v;
+        }
+      }
+    }
+    // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const F qf = frag_tr(Zq, LDZF, 0, 16 * mt);
+#pragma unroll
+      for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, frag_tr(dNs, LDQ, 0, e0 + 16 * el));
+      if (zown) {
+        F dd;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) dd[s] = dDb[kp(g, s)];
+        Gz[mt] = mma(Gz[mt], qf, dd);
+      }
+    }
+    __syncthreads();
+
+    // ---- dW[m][e] += sum_s Pk[s][m] K[s][e]; dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum_f(Pk)[s]
+    //      own columns -> RedY[s][e']
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const F pf = frag_rm(ZPk, LDZK, 16 * mt, 0);
+#pragma unroll
+      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(Ks, LDQ, 0, e0 + 16 * el));
+    }
+#pragma unroll
+    for (int st = 0; st < RT; ++st) {
+      const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * st + c] : 0.f;
+#pragma unroll
+      for (int el = 0; el < EH; ++el) {
+        const int et = h * EH + el;
+        f32x4 acc;
+        if (G::KIND == kFavor) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Ks[(16 * st + c) * LDQ + 16 * et + 4 * g + r]) * rsv;
+        } else {
+          acc = zero4();
+        }
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb)
+          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_tr(ZPk, LDZK, 32 * kb, 16 * st));
+        store_tile_T<float>(RedY, LDRH, acc, 16 * el, 16 * st);
+      }
+    }
+    __syncthreads();
+
+    // ---- dk = sum over slices; rows of the next tile -> LDS (their readers are done)
+    {
+      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      if (t < count) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
+          const float v = sum_y(hh, t * LDRH + col);
+          dKh[(size_t)(start + t) * D + e] = cvt<T>(v);
+        }
+      }
+    }
+    if (j > j0) {
+      stA.template store<LDQ>(dstA, nrmA, stid);
+      stB.template store<LDQ>(dstB, nrmB, stid);
+      if (j - 1 > j0) {
+        int sn, cn;
+        tm.tile(j - 2, sn, cn);
+        stA.fetch(srcA + (size_t)sn * D, cn, stid);
+        stB.fetch(srcB + (size_t)sn * D, cn, stid);
+      }
+    }
+    __syncthreads();
+  }
+
+  // per-workgroup dW partial: this wave's rows and columns
+  float* dwp = a.dW_part + (head * a.P + p) * (size_t)M * D;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int el = 0; el < EH; ++el)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        dwp[(size_t)(f * FW + 16 * mt + 4 * g + r) * D + e0 + 16 * el + c] = dWacc[mt][el][r];
+  // state cotangent before the sequence
+  if (p == 0 && a.dstate_in != nullptr) {
+    float* gout = a.dstate_in + head * SZ;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t row = (size_t)(f * FW + 16 * mt + 4 * g + r) * (D + 1);
+#pragma unroll
+        for (int el = 0; el < EH; ++el) gout[row + e0 + 16 * el + c] = r0 * Gs[mt][el][r];
+        if (zown && c == 0) gout[row + D] = r0 * Gz[mt][r];
+      }
+  }
+}
+
+template <class G>
+hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(bwd_walk8_kernel<G>, dim3(a.P, a.H, a.B), dim3(512), 0, s, a);
+  return hipGetLastError();
+}
+
+#define SLIM_INST_BWD8(T, D, FW, TR, KIND) \
+  template hipError_t launch_bwd_walk8<Cfg<T, D, FW, TR, KIND>>(const BwdArgs&, hipStream_t);
+SLIM_FOR_EACH_BF16_CONFIG(SLIM_INST_BWD8)
+
+}  // namespace slim

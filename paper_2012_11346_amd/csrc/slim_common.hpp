@@ -110,32 +110,36 @@ __device__ __forceinline__ void load_rows(T* dst, const T* src, int count, float
   }
 }
 
-// Register staging of a [count x D] row block (rows >= count read as zero):
-// fetch() issues the global loads, store() writes LDS (pitch LD) and
-// optionally the squared row norms.  Splitting the two lets the loads of the
-// next tile overlap the compute of the current one.
+constexpr size_t al16(size_t n) { return (n + 15) & ~(size_t)15; }
+
+// Register staging of a [count x D] row block (rows >= count read as zero)
+// by NT threads numbered tid = 0 .. NT-1: fetch() issues the global loads,
+// store() writes LDS (pitch LD) and optionally the squared row norms.
+// Splitting the two lets the loads of the next tile overlap the compute of
+// the current one.
 template <typename T, int D, int TR, int NT>
 struct RowStage {
   static constexpr int VEC = 16 / sizeof(T);
   static constexpr int CPR = D / VEC;  // 16-byte chunks per row
   static constexpr int NCH = TR * CPR;
   static constexpr int PER = (NCH + NT - 1) / NT;
+  static_assert(CPR <= 16, "a row's chunks must sit in consecutive lanes of one wave");
   uint4 v[PER];
 
-  __device__ __forceinline__ void fetch(const T* src, int count) {
+  __device__ __forceinline__ void fetch(const T* src, int count, int tid) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int ch = threadIdx.x + i * NT;
+      const int ch = tid + i * NT;
       const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
       v[i] = uint4{0u, 0u, 0u, 0u};
       if (ch < NCH && r < count) v[i] = *reinterpret_cast<const uint4*>(src + (size_t)r * D + cc * VEC);
     }
   }
   template <int LD>
-  __device__ __forceinline__ void store(T* dst, float* norms) const {
+  __device__ __forceinline__ void store(T* dst, float* norms, int tid) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int ch = threadIdx.x + i * NT;
+      const int ch = tid + i * NT;
       const bool active = ch < NCH;
       const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
       if (active) *reinterpret_cast<uint4*>(dst + r * LD + cc * VEC) = v[i];

@@ -144,8 +144,8 @@ __device__ __forceinline__ bf16x8 frag_tr(const bf16* Z, int ld, int k0, int col
   const bf16* p0 = Z + (k0 + 4 * g + (c >> 2)) * ld + col0 + 4 * (c & 3);
   const bf16* p1 = p0 + 16 * ld;
   typedef SLIM_LDS i16x4 lds_i16x4;
-  i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(SLIM_LDS void*)(uintptr_t)p0);
-  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(SLIM_LDS void*)(uintptr_t)p1);
+  i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+  i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
   bf16x8 f;
   bf16x4 av = __builtin_bit_cast(bf16x4, a);
   bf16x4 bv = __builtin_bit_cast(bf16x4, b);
@@ -171,6 +171,41 @@ __device__ __forceinline__ void store_tile_T(T* Z, int ld, const f32x4& x, int r
   T* p = Z + (col0 + c) * ld + row0 + 4 * g;
 #pragma unroll
   for (int r = 0; r < 4; ++r) p[r] = cvt<T>(x[r]);
+}
+
+// two stacked result tiles as an operand (has_b), or the first one with the
+// second 16 entries of the 32-deep block zero
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type pair_or_half(const f32x4& a, const f32x4& b, bool has_b) {
+  return has_b ? tile_pair_frag<T>(a, b) : tile_half_frag<T>(a);
+}
+
+// fragment slot s = Z[row0 + c][k0 + kp(g, s)], with slots 4..7 zero when the
+// 32-deep block has only its first 16 entries
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type frag_rm_h(const T* Z, int ld, int row0, int k0, bool half) {
+  if (!half) return frag_rm(Z, ld, row0, k0);
+  const int g = lane_g(), c = lane_c();
+  const T* p = Z + (row0 + c) * ld + k0 + 4 * g;
+  typename FragT<T>::type f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = p[r];
+    f[4 + r] = cvt<T>(0.f);
+  }
+  return f;
+}
+
+// result-tile values of a matrix stored transposed by store_tile_T:
+// X[row0 + 4g + r][col0 + c] = Z[col0 + c][row0 + 4g + r]
+template <typename T>
+__device__ __forceinline__ f32x4 load_tile_T(const T* Z, int ld, int row0, int col0) {
+  const int g = lane_g(), c = lane_c();
+  const T* p = Z + (col0 + c) * ld + row0 + 4 * g;
+  f32x4 x;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) x[r] = to_f32(p[r]);
+  return x;
 }
 
 // ------------------------------------------------------------- wave reductions

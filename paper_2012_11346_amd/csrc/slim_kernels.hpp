@@ -96,6 +96,10 @@ template <class G>
 size_t wfrag_bytes();
 template <class G>
 hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s);
+// the same walk with 8 waves per workgroup (two per feature slice); bf16
+// problems with 32 or 64 features per slice
+template <class G>
+hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s);
 // dW = sum of the n_parts partials [n_parts][n], in a fixed order
 hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s);
 
@@ -108,5 +112,11 @@ hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hi
   X(bf16, 32, 64, 32, kRelu) X(bf16, 32, 32, 32, kRelu) X(bf16, 32, 16, 32, kRelu)    \
   X(float, 64, 16, 32, kFavor) X(float, 32, 32, 32, kFavor) X(float, 32, 16, 32, kFavor) \
   X(float, 64, 16, 32, kRelu) X(float, 32, 32, 32, kRelu) X(float, 32, 16, 32, kRelu)
+
+// configurations served by the 8-wave backward walk
+#define SLIM_FOR_EACH_BF16_CONFIG(X)                                                  \
+  X(bf16, 64, 64, 32, kFavor) X(bf16, 64, 32, 32, kFavor) X(bf16, 32, 64, 32, kFavor) \
+  X(bf16, 32, 32, 32, kFavor) X(bf16, 64, 64, 32, kRelu) X(bf16, 64, 32, 32, kRelu)  \
+  X(bf16, 32, 64, 32, kRelu) X(bf16, 32, 32, 32, kRelu)
 
 }  // namespace slim

@@ -77,3 +77,27 @@ def test_state_cotangent_and_chaining(i):
         # dL/d(stored state_in) = dL/d(true state) * exp(kshift_in)
         g0 = g0 * np.exp(-host64(ks1))[:, :, None, None]
     report("dstate_in", g0, go, tol)
+
+
+@pytest.mark.parametrize("i", [4, 6])
+def test_backward_four_wave_form(i):
+    """The 4-wave form of the reverse walk (forced with SLIM_BWD_WAVES=4) on
+    problems the 8-wave form serves by default."""
+    need_gpu()
+    import os
+
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[backward 4-wave] case={name}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    old = os.environ.get("SLIM_BWD_WAVES")
+    os.environ["SLIM_BWD_WAVES"] = "4"
+    try:
+        _, _, _, (dQ, dK, dV, dW, _) = _run(x, C, kind)
+    finally:
+        if old is None:
+            os.environ.pop("SLIM_BWD_WAVES", None)
+        else:
+            os.environ["SLIM_BWD_WAVES"] = old
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), (dQ, dK, dV, dW), ref):
+        report(n, host64(a), r, TOL[dtype])

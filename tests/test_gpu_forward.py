@@ -28,6 +28,8 @@ CASES = [
     ("bf16_c100", 1, 2, 250, 64, 256, 100, "bf16", "favor+"),
     ("bf16_relu_cL", 2, 2, 200, 64, 128, 256, "bf16", "relu"),
     ("bf16_d32_c3", 1, 2, 130, 32, 64, 3, "bf16", "favor+"),
+    ("bf16_d32_m256_c40", 1, 2, 333, 32, 256, 40, "bf16", "favor+"),
+    ("bf16_d32_m128_relu_c16", 2, 1, 170, 32, 128, 16, "bf16", "relu"),
 ]
 
 
