@@ -610,14 +610,19 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   }
 }
 
-// dW[m][e] = sum over workgroups of the partials, in a fixed order; each
-// block sums a column slab of the partials for 256 entries
+// dW[m][e] = sum over workgroups of the partials, in a fixed order: a block
+// covers 64 entries; its 4 thread groups sum interleaved quarters of the
+// partials, then the 4 group sums are added in group order
 __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* part, int nparts, int n, float* dW) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
+  __shared__ float acc[4][64];
+  const int e = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int i = blockIdx.x * 64 + e;
   float s = 0.f;
-  for (int k = 0; k < nparts; ++k) s += part[(size_t)k * n + i];
-  dW[i] = s;
+  if (i < n)
+    for (int k = q; k < nparts; k += 4) s += part[(size_t)k * n + i];
+  acc[q][e] = s;
+  __syncthreads();
+  if (q == 0 && i < n) dW[i] = (acc[0][e] + acc[1][e]) + (acc[2][e] + acc[3][e]);
 }
 
 template <class G>
@@ -627,7 +632,7 @@ hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s) {
-  hipLaunchKernelGGL(dw_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, s, part, n_parts, n, dW);
+  hipLaunchKernelGGL(dw_reduce_kernel, dim3((n + 63) / 64), dim3(256), 0, s, part, n_parts, n, dW);
   return hipGetLastError();
 }
 

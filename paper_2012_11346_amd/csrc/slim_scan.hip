@@ -1,8 +1,8 @@
 // Scans over segment states: the sequence of each head is split into P
 // segments walked in parallel; these kernels turn per-segment sums into the
 // exact state each segment starts from (forward and backward) and into the
-// state cotangent each segment ends with (backward).  One workgroup per head,
-// threads over the M (d + 1) state entries, segments in order.
+// state cotangent each segment ends with (backward).  Grid: (state entries /
+// 256, heads); one thread per state entry walks the segments in order.
 #include "slim_common.hpp"
 #include "slim_kernels.hpp"
 
@@ -12,9 +12,10 @@ namespace slim {
 //   s_0 = init (shift init_shift) or zero; s_{p+1} = s_p (+) seg_p, where (+)
 //   brings both operands to the larger shift before adding.
 __global__ __launch_bounds__(256) void scan_fwd_kernel(ScanArgs a) {
-  const int head = blockIdx.x;
+  const int head = blockIdx.y;
   const size_t SZ = a.SZ;
-  for (int el = threadIdx.x; el < a.SZ; el += 256) {
+  const int el = blockIdx.x * 256 + threadIdx.x;
+  if (el < a.SZ) {
     float v = a.init ? a.init[head * SZ + el] : 0.f;
     float vs = a.favor ? (a.init ? a.init_shift[head] : -INFINITY) : 0.f;
     for (int p = 0; p < a.P; ++p) {
@@ -36,11 +37,12 @@ __global__ __launch_bounds__(256) void scan_fwd_kernel(ScanArgs a) {
 // out[p] for p = 0..P: state at the boundary before segment p (p = P: after the
 // last one), all relative to the common shift; init is relative to init_shift.
 __global__ __launch_bounds__(256) void scan_bwd_kernel(ScanArgs a) {
-  const int head = blockIdx.x;
+  const int head = blockIdx.y;
   const size_t SZ = a.SZ;
   float r0 = 1.f;
   if (a.favor && a.init != nullptr) r0 = fast_exp2((a.init_shift[head] - a.shift[head]) * kLog2e);
-  for (int el = threadIdx.x; el < a.SZ; el += 256) {
+  const int el = blockIdx.x * 256 + threadIdx.x;
+  if (el < a.SZ) {
     float v = a.init ? r0 * a.init[head * SZ + el] : 0.f;
     for (int p = 0; p < a.P; ++p) {
       a.out[((size_t)head * (a.P + 1) + p) * SZ + el] = v;
@@ -52,9 +54,10 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(ScanArgs a) {
 
 // out[p] = init + sum_{q > p} seg[q]: the state cotangent after segment p
 __global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
-  const int head = blockIdx.x;
+  const int head = blockIdx.y;
   const size_t SZ = a.SZ;
-  for (int el = threadIdx.x; el < a.SZ; el += 256) {
+  const int el = blockIdx.x * 256 + threadIdx.x;
+  if (el < a.SZ) {
     float v = a.init ? a.init[head * SZ + el] : 0.f;
     for (int p = a.P - 1; p >= 0; --p) {
       const size_t idx = ((size_t)head * a.P + p) * SZ + el;
@@ -64,16 +67,18 @@ __global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
   }
 }
 
+static dim3 scan_grid(const ScanArgs& a) { return dim3((a.SZ + 255) / 256, a.BH); }
+
 hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(scan_fwd_kernel, dim3(a.BH), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(scan_fwd_kernel, scan_grid(a), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(scan_bwd_kernel, dim3(a.BH), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(scan_bwd_kernel, scan_grid(a), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_scan_rev(const ScanArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(scan_rev_kernel, dim3(a.BH), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(scan_rev_kernel, scan_grid(a), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
