@@ -163,12 +163,29 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   const float half_log2M = 0.5f * __log2f((float)M);
   constexpr int TPR = 256 / TR, EPT = D / TPR;
 
+  // rows of the next tile are fetched while the current one is computed
+  RowStage<T, D, TR, 256> sq, sk, sv;
+  if (j1 > j0) {
+    int s0, n0;
+    tm.tile(j0, s0, n0);
+    if constexpr (QSIDE) sq.fetch(Qh + (size_t)s0 * D, n0, threadIdx.x);
+    sk.fetch(Kh + (size_t)s0 * D, n0, threadIdx.x);
+    sv.fetch(Vh + (size_t)s0 * D, n0, threadIdx.x);
+  }
+
   for (int j = j0; j < j1; ++j) {
     int start, count;
     tm.tile(j, start, count);
-    if constexpr (QSIDE) load_rows<T, D, TR, LDQ, 256>(Qs, Qh + (size_t)start * D, count, G::KIND == kFavor ? qn : nullptr);
-    load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, G::KIND == kFavor ? kn : nullptr);
-    load_rows<T, D, TR, LDQ, 256>(Vs, Vh + (size_t)start * D, count, nullptr);
+    if constexpr (QSIDE) sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr, threadIdx.x);
+    sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, threadIdx.x);
+    sv.template store<LDQ>(Vs, nullptr, threadIdx.x);
+    if (j + 1 < j1) {
+      int sn, cn;
+      tm.tile(j + 1, sn, cn);
+      if constexpr (QSIDE) sq.fetch(Qh + (size_t)sn * D, cn, threadIdx.x);
+      sk.fetch(Kh + (size_t)sn * D, cn, threadIdx.x);
+      sv.fetch(Vh + (size_t)sn * D, cn, threadIdx.x);
+    }
     __syncthreads();
 
     f32x4 Lq[QSIDE ? MT : 1][RT], Lk[RT][MT];
