@@ -116,16 +116,35 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   T* ZP = (T*)(pz + Lay::pY);      // P as [t][m]
   T* ZG = ZP;                                       // G as [e][m]
   float* RedY = (float*)(pz + Lay::pY) + h * TR * LDRH;  // N, dV, dk partial rows [t][e']
-  // sum over the 4 slices of reduction entry [t][col] of value half hh
-  auto sum_x = [&](int hh, int idx) -> float {
-    const float* r = (const float*)(arena + Lay::oP + Lay::pX) + hh * TR * LDRH + idx;
+  // sums over the 4 slices of the EPT consecutive reduction entries
+  // [t][col .. col + EPT) of value half hh (vector reads: one row of 16
+  // threads covers all banks)
+  typedef float fvec __attribute__((ext_vector_type(EPT)));
+  static_assert((16 * EH) % EPT == 0 && (LDRH * 4) % 16 == 0, "");
+  auto sum_x = [&](int hh, int idx) -> fvec {
+    const char* r = arena + Lay::oP + Lay::pX + (hh * TR * LDRH + idx) * 4;
+    const fvec a0 = *(const fvec*)r, a1 = *(const fvec*)(r + Lay::PAIR);
+    const fvec a2 = *(const fvec*)(r + 2 * Lay::PAIR), a3 = *(const fvec*)(r + 3 * Lay::PAIR);
+    return (a0 + a1) + (a2 + a3);
+  };
+  auto sum_y = [&](int hh, int idx) -> fvec {
+    const char* r = arena + Lay::oP + Lay::pY + (hh * TR * LDRH + idx) * 4;
+    const fvec a0 = *(const fvec*)r, a1 = *(const fvec*)(r + Lay::PAIR);
+    const fvec a2 = *(const fvec*)(r + 2 * Lay::PAIR), a3 = *(const fvec*)(r + 3 * Lay::PAIR);
+    return (a0 + a1) + (a2 + a3);
+  };
+  auto sum_y1 = [&](int idx) -> float {
+    const float* r = (const float*)(arena + Lay::oP + Lay::pY) + idx;
     constexpr int S4 = Lay::PAIR / sizeof(float);
     return (r[0] + r[S4]) + (r[2 * S4] + r[3 * S4]);
   };
-  auto sum_y = [&](int hh, int idx) -> float {
-    const float* r = (const float*)(arena + Lay::oP + Lay::pY) + hh * TR * LDRH + idx;
-    constexpr int S4 = Lay::PAIR / sizeof(float);
-    return (r[0] + r[S4]) + (r[2 * S4] + r[3 * S4]);
+  // EPT consecutive values of row t of a [.][D] output, as one store
+  auto store_row = [&](T* dst, const fvec& v) {
+    typedef T tvec __attribute__((ext_vector_type(EPT)));
+    tvec o;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) o[i] = cvt<T>(v[i]);
+    *(tvec*)dst = o;
   };
 
   const int p = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
@@ -364,16 +383,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       const bool ok = t < count;
-      const float den = sum_y(0, t * LDRH + 16 * EH);
+      const float den = sum_y1(t * LDRH + 16 * EH);
       const float inv = ok ? 1.f / den : 0.f;
+      const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+      const fvec n = sum_y(hh, t * LDRH + col);
       float dy[EPT];
       float dot = 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i) {
-        const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
-        dy[i] = to_f32(dYs[t * LDQ + e]);
-        const float n = sum_y(hh, t * LDRH + col);
-        dot += dy[i] * (n * inv);
+        dy[i] = to_f32(dYs[t * LDQ + e + i]);
+        dot += dy[i] * (n[i] * inv);
       }
 #pragma unroll
       for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
@@ -422,12 +441,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
-#pragma unroll
-        for (int i = 0; i < EPT; ++i) {
-          const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
-          const float v = sum_y(hh, t * LDRH + col);
-          dVh[(size_t)(start + t) * D + e] = cvt<T>(v);
-        }
+        const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+        store_row(dVh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
       }
     }
 #pragma unroll
@@ -504,12 +519,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
-#pragma unroll
-        for (int i = 0; i < EPT; ++i) {
-          const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
-          const float v = sum_x(hh, t * LDRH + col);
-          dQh[(size_t)(start + t) * D + e] = cvt<T>(v);
-        }
+        const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+        store_row(dQh + (size_t)(start + t) * D + e, sum_x(hh, t * LDRH + col));
       }
     }
 #pragma unroll
@@ -602,12 +613,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
-#pragma unroll
-        for (int i = 0; i < EPT; ++i) {
-          const int e = q * EPT + i, hh = e / (16 * EH), col = e - hh * 16 * EH;
-          const float v = sum_y(hh, t * LDRH + col);
-          dKh[(size_t)(start + t) * D + e] = cvt<T>(v);
-        }
+        const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+        store_row(dKh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
       }
     }
     if (j > j0) {
