@@ -127,8 +127,9 @@ FwdLayout fwd_layout(const slim_problem* p, int P) {
   return l;
 }
 
-// backward workspace: segment sums, segment boundaries, per-segment
-// cotangent contributions and cotangents after each segment, dW partials
+// backward workspace: W in fragment order, segment sums, segment
+// boundaries, the cotangent each segment's walk ends with and the cotangent
+// after each segment (several segments), dW partials
 struct BwdLayout {
   size_t wfrag, seg_sum, bounds, gc, gend, dw_part, total;
 };
@@ -161,6 +162,7 @@ typedef hipError_t (*feat_fn)(const slim::FeatArgs&, hipStream_t);
 typedef hipError_t (*bwd_fn)(const slim::BwdArgs&, hipStream_t);
 typedef hipError_t (*wfrag_fn)(const slim::WfragArgs&, hipStream_t);
 typedef size_t (*size_fn)();
+typedef hipError_t (*carry_fn)(const slim::CarryArgs&, hipStream_t);
 
 struct Dispatch {
   fwd_fn fwd;
@@ -169,13 +171,14 @@ struct Dispatch {
   bwd_fn bwd8;  // backward walk, 8 waves per workgroup (nullptr where not built)
   wfrag_fn wfrag;
   size_fn wfrag_bytes;
+  carry_fn carry;
 };
 
 template <class T, int D, int FW, int KIND>
 Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
   return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>, nullptr,
-                  &slim::launch_wfrag<G>, &slim::wfrag_bytes<G>};
+                  &slim::launch_wfrag<G>, &slim::wfrag_bytes<G>,      &slim::launch_carry<G>};
 }
 template <int D, int FW, int KIND>
 Dispatch make_dispatch8() {
@@ -422,29 +425,8 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   sc.favor = favor ? 1 : 0;
   e = slim::launch_scan_bwd(sc, s);
   if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
-  const float* gend = dstate_out;
-  if (P > 1) {
-    // (3) each segment's contribution to the state cotangent, then the
-    //     cotangent after each segment by a reverse scan (eq. 18)
-    slim::FwdArgs gg = f;
-    gg.seg_state = sc.out;
-    gg.seg_stride = P + 1;
-    gg.seg_out = (float*)(w + lay.gc);
-    e = dp.fwd(gg, slim::kWalkGrad, s);
-    if (e != hipSuccess) return hip_fail(e, "cotangent-sum launch");
-    slim::ScanArgs rv;
-    std::memset(&rv, 0, sizeof(rv));
-    rv.seg = gg.seg_out;
-    rv.init = dstate_out;
-    rv.out = (float*)(w + lay.gend);
-    rv.BH = BH;
-    rv.P = P;
-    rv.SZ = SZ;
-    e = slim::launch_scan_rev(rv, s);
-    if (e != hipSuccess) return hip_fail(e, "cotangent-scan launch");
-    gend = rv.out;
-  }
-  // (4) W in fragment order, then the reverse walk
+  // (3) W in fragment order, then the reverse walk of every segment; each
+  //     starts from a zero cotangent except the last (dstate_out)
   slim::WfragArgs wf;
   wf.W = W;
   wf.out = w + lay.wfrag;
@@ -460,9 +442,10 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.Wfrag = wf.out;
   a.kshift = favor ? kshift : nullptr;
   a.bounds = sc.out;
-  a.seg_gend = gend;
+  a.dstate_out = dstate_out;
+  a.g_final = P > 1 ? (float*)(w + lay.gc) : nullptr;
   a.init_shift = favor ? kshift_in : nullptr;
-  a.dstate_in = dstate_in;
+  a.dstate_in = P > 1 ? nullptr : dstate_in;
   a.dQ = dQ;
   a.dK = dK;
   a.dV = dV;
@@ -477,6 +460,42 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   const bwd_fn walk = pick_bwd(dp);
   e = timed_launch(SLIM_PHASE_BWD, s, [&] { return walk(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward launch");
+  if (P > 1) {
+    // (4) cotangent after each segment (reverse scan of what the walks ended
+    //     with; eq. 18 summed over the later segments) and before the
+    //     sequence; then its contribution to the rows of each earlier segment
+    slim::ScanArgs rv;
+    std::memset(&rv, 0, sizeof(rv));
+    rv.seg = a.g_final;
+    rv.out = (float*)(w + lay.gend);
+    rv.total = dstate_in;
+    rv.init_shift = favor ? kshift_in : nullptr;
+    rv.shift = favor ? kshift : nullptr;
+    rv.BH = BH;
+    rv.P = P;
+    rv.SZ = SZ;
+    rv.favor = favor ? 1 : 0;
+    e = slim::launch_scan_rev(rv, s);
+    if (e != hipSuccess) return hip_fail(e, "cotangent-scan launch");
+    slim::CarryArgs ca;
+    std::memset(&ca, 0, sizeof(ca));
+    ca.K = K;
+    ca.V = V;
+    ca.Wfrag = a.Wfrag;
+    ca.kshift = favor ? kshift : nullptr;
+    ca.gend = rv.out;
+    ca.dK = dK;
+    ca.dV = dV;
+    ca.dW_part = a.dW_part;
+    ca.B = a.B;
+    ca.H = a.H;
+    ca.L = a.L;
+    ca.C = a.C;
+    ca.P = P;
+    ca.relu_eps = p->relu_eps;
+    e = dp.carry(ca, s);
+    if (e != hipSuccess) return hip_fail(e, "carry launch");
+  }
   // (5) dW: the workgroups' partials summed in a fixed order
   e = slim::launch_dw_reduce(a.dW_part, BH * P, (int)(p->M * p->d), dW, s);
   if (e != hipSuccess) return hip_fail(e, "dW-reduction launch");

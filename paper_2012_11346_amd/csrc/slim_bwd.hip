@@ -117,6 +117,9 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   float r0 = 1.f;
   if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
+  // the cotangent starts at dstate_out in the last segment, else at zero
+  // (earlier segments get the cotangent of later ones added by carry_kernel)
+  const float* g0 = (p == a.P - 1 && a.dstate_out != nullptr) ? a.dstate_out + head * SZ : nullptr;
   f32x4 S[MT][ET + 1], Gs[MT][ET + 1], dWacc[MT][ET];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
@@ -126,10 +129,10 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 #pragma unroll
       for (int et = 0; et < ET; ++et) {
         S[mt][et][r] = bend[row + 16 * et + c];
-        Gs[mt][et][r] = a.seg_gend ? a.seg_gend[sidx + row + 16 * et + c] : 0.f;
+        Gs[mt][et][r] = g0 ? g0[row + 16 * et + c] : 0.f;
       }
       S[mt][ET][r] = bend[row + D];
-      Gs[mt][ET][r] = a.seg_gend ? a.seg_gend[sidx + row + D] : 0.f;
+      Gs[mt][ET][r] = g0 ? g0[row + D] : 0.f;
     }
 #pragma unroll
     for (int et = 0; et < ET; ++et) dWacc[mt][et] = zero4();
@@ -595,9 +598,12 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     for (int et = 0; et < ET; ++et)
 #pragma unroll
       for (int r = 0; r < 4; ++r) dwp[(size_t)(w * FW + 16 * mt + 4 * g + r) * D + 16 * et + c] = dWacc[mt][et][r];
-  // state cotangent before the sequence
-  if (p == 0 && a.dstate_in != nullptr) {
-    float* gout = a.dstate_in + head * SZ;
+  // cotangent the walk ends with (several segments), or the state cotangent
+  // before the sequence (one segment)
+  float* gout = a.g_final != nullptr ? a.g_final + sidx
+                                     : ((p == 0 && a.dstate_in != nullptr) ? a.dstate_in + head * SZ : nullptr);
+  if (a.g_final != nullptr) r0 = 1.f;
+  if (gout != nullptr) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll

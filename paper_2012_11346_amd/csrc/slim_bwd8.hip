@@ -179,6 +179,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   float r0 = 1.f;
   if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
+  // the cotangent starts at dstate_out in the last segment, else at zero
+  // (earlier segments get the cotangent of later ones added by carry_kernel)
+  const float* g0 = (p == a.P - 1 && a.dstate_out != nullptr) ? a.dstate_out + head * SZ : nullptr;
   // running state after the current tile (this wave's columns), its cotangent, dW rows
   f32x4 S[MT][EH], Sz[MT], Gs[MT][EH], Gz[MT], dWacc[MT][EH];
 #pragma unroll
@@ -189,10 +192,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
       for (int et = 0; et < EH; ++et) {
         S[mt][et][r] = bend[row + e0 + 16 * et + c];
-        Gs[mt][et][r] = a.seg_gend ? a.seg_gend[sidx + row + e0 + 16 * et + c] : 0.f;
+        Gs[mt][et][r] = g0 ? g0[row + e0 + 16 * et + c] : 0.f;
       }
       Sz[mt][r] = zown ? bend[row + D] : 0.f;
-      Gz[mt][r] = (zown && a.seg_gend) ? a.seg_gend[sidx + row + D] : 0.f;
+      Gz[mt][r] = (zown && g0) ? g0[row + D] : 0.f;
     }
 #pragma unroll
     for (int et = 0; et < EH; ++et) dWacc[mt][et] = zero4();
@@ -639,9 +642,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         dwp[(size_t)(f * FW + 16 * mt + 4 * g + r) * D + e0 + 16 * el + c] = dWacc[mt][el][r];
-  // state cotangent before the sequence
-  if (p == 0 && a.dstate_in != nullptr) {
-    float* gout = a.dstate_in + head * SZ;
+  // cotangent the walk ends with (several segments), or the state cotangent
+  // before the sequence (one segment)
+  float* gout = a.g_final != nullptr ? a.g_final + sidx
+                                     : ((p == 0 && a.dstate_in != nullptr) ? a.dstate_in + head * SZ : nullptr);
+  if (a.g_final != nullptr) r0 = 1.f;
+  if (gout != nullptr) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll

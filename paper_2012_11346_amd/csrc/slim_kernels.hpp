@@ -42,6 +42,7 @@ struct ScanArgs {
   const float* shift;      // [B,H] common key shift (backward), or nullptr
   float* out;              // forward: [B,H,P,...] segment starts; backward: [B,H,P+1,...] boundaries
   float* out_shift;        // forward: [B,H,P]
+  float* total;            // reverse scan: [B,H,M,D+1] scaled total, or nullptr
   int BH, P, SZ, favor;
 };
 
@@ -68,14 +69,30 @@ struct BwdArgs {
   const void* Wfrag;        // fragment-ordered W (WFragLayout)
   const float* kshift;      // [B,H] key shift of every state below (FAVOR+)
   const float* bounds;      // [B,H,P+1,M,D+1] exact state at each segment boundary
-  const float* seg_gend;    // [B,H,P,M,D+1] state cotangent after each segment
+  const float* dstate_out;  // [B,H,M,D+1] cotangent of the final state (segment P-1 starts from it), or nullptr
+  float* g_final;           // [B,H,P,M,D+1] cotangent each segment's walk ends with (P > 1), or nullptr
   const float* init_shift;  // [B,H] key shift of the caller's initial state (scales dstate_in), or nullptr
-  float* dstate_in;         // [B,H,M,D+1] state cotangent before the sequence (written by segment 0), or nullptr
+  float* dstate_in;         // [B,H,M,D+1] state cotangent before the sequence (P == 1 only), or nullptr
   void* dQ;
   void* dK;
   void* dV;
   float* dW_part;           // [B,H,P,M,D] per-workgroup partial dW
   float* dW;                // [M,D] sum of the partials
+  int B, H, L, C, P;
+  float relu_eps;
+};
+
+// Carried cotangent: adds the contribution of G_end(p) (the cotangent after
+// segment p, from all later segments) to dK, dV and dW of segment p's rows.
+struct CarryArgs {
+  const void* K;
+  const void* V;
+  const void* Wfrag;
+  const float* kshift;  // [B,H] (FAVOR+)
+  const float* gend;    // [B,H,P,M,D+1] G_end(p)
+  void* dK;             // in/out
+  void* dV;             // in/out
+  float* dW_part;       // [B,H,P,M,D] in/out
   int B, H, L, C, P;
   float relu_eps;
 };
@@ -86,7 +103,9 @@ hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s);
 hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s);
 // inclusive boundaries of segment states under one common shift (backward)
 hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s);
-// reverse scan of state cotangents: out[p] = init + sum_{q > p} seg[q]
+// reverse scan of state cotangents: out[p] = init + sum_{q > p} seg[q]; with
+// `total` also total = r0 (init + sum_q seg[q]), r0 = exp(init_shift - shift)
+// (FAVOR+, when init_shift is given) else 1
 hipError_t launch_scan_rev(const ScanArgs& a, hipStream_t s);
 template <class G>
 hipError_t launch_featmap(const FeatArgs& a, hipStream_t s);
@@ -100,6 +119,8 @@ hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s);
 // problems with 32 or 64 features per slice
 template <class G>
 hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s);
+template <class G>
+hipError_t launch_carry(const CarryArgs& a, hipStream_t s);
 // dW = sum of the n_parts partials [n_parts][n], in a fixed order
 hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s);
 

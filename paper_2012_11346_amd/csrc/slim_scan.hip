@@ -52,7 +52,8 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(ScanArgs a) {
   }
 }
 
-// out[p] = init + sum_{q > p} seg[q]: the state cotangent after segment p
+// out[p] = init + sum_{q > p} seg[q]: the state cotangent after segment p;
+// total = r0 (init + sum over all segments): the cotangent before segment 0
 __global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
   const int head = blockIdx.y;
   const size_t SZ = a.SZ;
@@ -63,6 +64,11 @@ __global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
       const size_t idx = ((size_t)head * a.P + p) * SZ + el;
       a.out[idx] = v;
       v += a.seg[idx];
+    }
+    if (a.total != nullptr) {
+      float r0 = 1.f;
+      if (a.favor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.shift[head]) * kLog2e);
+      a.total[head * SZ + el] = r0 * v;
     }
   }
 }

@@ -82,3 +82,42 @@ def test_long_sequence_against_definition(kind):
         report("Y", host64(Y), Yref, TOL["bf16"])
         for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], gref):
             report(n, host64(a), r, TOL["bf16"])
+
+
+@pytest.mark.parametrize("kind", ["favor+", "relu"])
+def test_cotangent_chaining_with_segments(kind):
+    """dstate_out into a segmented backward (the last segment starts from it,
+    earlier ones receive it through the carried cotangent) and dstate_in out
+    of one (the scaled total of every segment's cotangent)."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    M = 256 if kind == "favor+" else 128
+    B, H, L, C = 1, 2, 700, 48
+    x = make_inputs(Workload("chain", 330, B, H, L, 64, M, (C,), "bf16", kind))
+    cut = 351
+    half = lambda t, a, b: t[:, :, a:b].contiguous()
+    old = os.environ.get("SLIM_SEGMENTS")
+    os.environ["SLIM_SEGMENTS"] = "3"
+    try:
+        print(f"[chaining segments] kind={kind}", flush=True)
+        Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+        Y1, st1, ks1 = slim.fwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, C, kind)
+        Y2, st2, ks2 = slim.fwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, C, kind, state_in=st1,
+                                kshift_in=ks1)
+        g2 = slim.bwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, half(dY, cut, L), C, ks2, kind,
+                      state_in=st1, kshift_in=ks1, want_dstate_in=True)
+        g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, ks1, kind,
+                      dstate_out=g2[4])
+        torch.cuda.synchronize()
+    finally:
+        if old is None:
+            os.environ.pop("SLIM_SEGMENTS", None)
+        else:
+            os.environ["SLIM_SEGMENTS"] = old
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    tol = TOL["bf16"]
+    report("dQ (chained)", np.concatenate([host64(g1[0]), host64(g2[0])], axis=2), ref[0], tol)
+    report("dK (chained)", np.concatenate([host64(g1[1]), host64(g2[1])], axis=2), ref[1], tol)
+    report("dV (chained)", np.concatenate([host64(g1[2]), host64(g2[2])], axis=2), ref[2], tol)
+    report("dW (chained)", host64(g1[3]) + host64(g2[3]), ref[3], tol)
