@@ -237,11 +237,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   __syncthreads();
 
   // [V|1] operand over the tile's 32 rows for value tile et (et == ET: ones)
-  auto v_frag = [&](int et, int count) -> F {
-    if (et < ET) return frag_tr(Vs, LDQ, 0, 16 * et);
+  auto v_frag = [&](const Lane& L, int et, int count) -> F {
+    if (et < ET) return frag_tr(L, Vs, LDQ, 0, 16 * et);
     F v;
+    const int rem = count - 4 * L.g;  // rows kp(g, s) < count
 #pragma unroll
-    for (int s = 0; s < 8; ++s) v[s] = cvt<T>(kp(g, s) < count ? 1.f : 0.f);
+    for (int s = 0; s < 8; ++s) v[s] = cvt<T>((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
     return v;
   };
   // operand contracting over this slice's features m in [32 kb, 32 kb + 32),
@@ -251,6 +252,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   };
 
   for (int j = j1 - 1; j >= j0; --j) {
+    Lane L = fresh_lane();
+    int g = L.g, c = L.c;
     int start, count;
     tm.tile(j, start, count);
 
@@ -270,7 +273,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int mt = 0; mt < MT; ++mt) {
           f32x4 acc = {init, init, init, init};
 #pragma unroll
-          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(Qs, LDQ, 16 * tt, 32 * kb));
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(L, Qs, LDQ, 16 * tt, 32 * kb));
           Lq[mt][tt] = acc;
         }
       }
@@ -281,13 +284,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 kv = kinit;
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, frag_rm(Ks, LDQ, 16 * h, 32 * kb), Wf[mt][kb]);
+        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, frag_rm(L, Ks, LDQ, 16 * h, 32 * kb), Wf[mt][kb]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool ok = 16 * h + 4 * g + r < count;
           kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : fmaxf(kv[r], 0.f) + a.relu_eps;
         }
-        store_tile_T<T>(Zk, LDZK, kv, 16 * h, 16 * mt);
+        store_tile_T<T>(L, Zk, LDZK, kv, 16 * h, 16 * mt);
       }
       if (G::KIND == kFavor && zown) {
 #pragma unroll
@@ -303,6 +306,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair)
 #pragma unroll
@@ -316,7 +322,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           qv[r] = (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(qv[r] * kLog2e - qs) : fmaxf(qv[r], 0.f) + a.relu_eps;
-        store_tile_T<T>(Zq, LDZF, qv, 16 * mt, 16 * tt);
+        store_tile_T<T>(L, Zq, LDZF, qv, 16 * mt, 16 * tt);
       }
     }
 
@@ -337,12 +343,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     } else {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        F kf = frag_rm(Zk, LDZK, 16 * mt, 0);  // K~ contracting over rows
+        F kf = frag_rm(L, Zk, LDZK, 16 * mt, 0);  // K~ contracting over rows
 #pragma unroll
         for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
 #pragma unroll
-        for (int et = 0; et < EH; ++et) S[mt][et] = mma(S[mt][et], kf, v_frag(h * EH + et, count));
-        if (zown) Sz[mt] = mma(Sz[mt], kf, v_frag(ET, count));
+        for (int et = 0; et < EH; ++et) S[mt][et] = mma(S[mt][et], kf, v_frag(L, h * EH + et, count));
+        if (zown) Sz[mt] = mma(Sz[mt], kf, v_frag(L, ET, count));
       }
     }
 
@@ -355,14 +361,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         if (st <= tt) {
 #pragma unroll
           for (int kb = 0; kb < MB; ++kb)
-            acc = mma(acc, frag_tr(Zk, LDZK, 32 * kb, 16 * st), frag_rm(Zq, LDZF, 16 * tt, 32 * kb));
+            acc = mma(acc, frag_tr(L, Zk, LDZK, 32 * kb, 16 * st), frag_rm(L, Zq, LDZF, 16 * tt, 32 * kb));
         }
         if (st == tt) {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (4 * g + r > c) acc[r] = 0.f;
         }
-        store_tile_T<T>(ZA, LDZT, acc, 16 * st, 16 * tt);
+        store_tile_T<T>(L, ZA, LDZT, acc, 16 * st, 16 * tt);
       }
     // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
 #pragma unroll
@@ -371,20 +377,24 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int el = 0; el <= EH; ++el) {
         if (el == EH && !zown) continue;
         const int et = (el < EH) ? h * EH + el : ET;
-        f32x4 acc = mma(zero4(), v_frag(et, count), frag_rm(ZA, LDZT, 16 * tt, 0));
+        f32x4 acc = mma(zero4(), v_frag(L, et, count), frag_rm(L, ZA, LDZT, 16 * tt, 0));
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), frag_rm(Zq, LDZF, 16 * tt, 32 * kb));
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), frag_rm(L, Zq, LDZF, 16 * tt, 32 * kb));
         if (el < EH) {
-          store_tile_T<float>(RedY, LDRH, acc, 16 * el, 16 * tt);
+          store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * tt);
         } else if (g == 0) {
           RedY[(16 * tt + c) * LDRH + 16 * EH] = acc[0];
         }
       }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dN = dY / D, dD = -(dY . N) / D^2 per row (TPR threads per row)
     {
-      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      const int tid = fresh_tid();
+      const int t = tid / TPR, q = tid % TPR;
       const bool ok = t < count;
       const float den = sum_y1(t * LDRH + 16 * EH);
       const float inv = ok ? 1.f / den : 0.f;
@@ -408,6 +418,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal, rows < count -> ZdA[t][s]
 #pragma unroll
@@ -418,31 +431,35 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc = f32x4{ddt, ddt, ddt, ddt};
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_rm(Vs, LDQ, 16 * st, 32 * kb), frag_rm(dNs, LDQ, 16 * tt, 32 * kb));
+          acc = mma(acc, frag_rm(L, Vs, LDQ, 16 * st, 32 * kb), frag_rm(L, dNs, LDQ, 16 * tt, 32 * kb));
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int sr = 16 * st + 4 * g + r;
           if ((st == tt && 4 * g + r > c) || sr >= count) acc[r] = 0.f;
         }
-        store_tile_T<T>(ZdA, LDZT, acc, 16 * st, 16 * tt);
+        store_tile_T<T>(L, ZdA, LDZT, acc, 16 * st, 16 * tt);
       }
-      if (tt == 0) store_tile_T<T>(ZdA, LDZT, zero4(), 16, 0);  // s in [16, 32) for t in [0, 16)
+      if (tt == 0) store_tile_T<T>(L, ZdA, LDZT, zero4(), 16, 0);  // s in [16, 32) for t in [0, 16)
     }
     // dV^T[e][s] = sum_m G[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t], own columns -> RedY[s][e']
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
       for (int el = 0; el < EH; ++el) {
-        f32x4 acc = mma(zero4(), frag_tr(dNs, LDQ, 0, 16 * (h * EH + el)), frag_tr(ZA, LDZT, 0, 16 * st));
+        f32x4 acc = mma(zero4(), frag_tr(L, dNs, LDQ, 0, 16 * (h * EH + el)), frag_tr(L, ZA, LDZT, 0, 16 * st));
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), frag_tr(Zk, LDZK, 32 * kb, 16 * st));
-        store_tile_T<float>(RedY, LDRH, acc, 16 * el, 16 * st);
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), frag_tr(L, Zk, LDZK, 32 * kb, 16 * st));
+        store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
       }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dV = sum over slices; S (own columns) -> ZS[e][m], z -> zs
     {
-      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      const int tid = fresh_tid();
+      const int t = tid / TPR, q = tid % TPR;
       if (t < count) {
         const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
         store_row(dVh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
@@ -451,13 +468,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-      for (int el = 0; el < EH; ++el) store_tile_T<T>(ZS, LDZF, S[mt][el], 16 * mt, e0 + 16 * el);
+      for (int el = 0; el < EH; ++el) store_tile_T<T>(L, ZS, LDZF, S[mt][el], 16 * mt, e0 + 16 * el);
       if (zown && c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) zs[f * FW + 16 * mt + 4 * g + r] = Sz[mt][r];
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dQ~^T[m][t] = sum_e S[m][e] dN[t][e] + z[m] dD[t] + sum_s K~[s][m] dA^T[s][t]
     //      for this wave's rows t in [16 h, 16 h + 16); P = dQ~ . Q~ (FAVOR+) or
@@ -472,15 +492,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int r = 0; r < 4; ++r) acc[r] = zs[f * FW + 16 * mt + 4 * g + r] * ddt;
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_tr(ZS, LDZF, 32 * kb, 16 * mt), frag_rm(dNs, LDQ, 16 * h, 32 * kb));
-        acc = mma(acc, frag_rm(Zk, LDZK, 16 * mt, 0), frag_rm(ZdA, LDZT, 16 * h, 0));
-        const f32x4 qv = load_tile_T(Zq, LDZF, 16 * mt, 16 * h);
+          acc = mma(acc, frag_tr(L, ZS, LDZF, 32 * kb, 16 * mt), frag_rm(L, dNs, LDQ, 16 * h, 32 * kb));
+        acc = mma(acc, frag_rm(L, Zk, LDZK, 16 * mt, 0), frag_rm(L, ZdA, LDZT, 16 * h, 0));
+        const f32x4 qv = load_tile_T(L, Zq, LDZF, 16 * mt, 16 * h);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
           rs += acc[r];
         }
-        store_tile_T<T>(ZP, LDZF, acc, 16 * mt, 16 * h);
+        store_tile_T<T>(L, ZP, LDZF, acc, 16 * mt, 16 * h);
       }
       if (G::KIND == kFavor) {
         rs = wave_sum_over_g(rs);
@@ -488,6 +508,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] - q[t][e] rowsum_f(P)[t], own columns -> RedX[t][e'];
     //      dW[m][e] += sum_t P[t][m] Q[t][e]
@@ -506,21 +529,25 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_rm(ZP, LDZF, 16 * tt, 32 * kb));
-        store_tile_T<float>(RedX, LDRH, acc, 16 * el, 16 * tt);
+          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_rm(L, ZP, LDZF, 16 * tt, 32 * kb));
+        store_tile_T<float>(L, RedX, LDRH, acc, 16 * el, 16 * tt);
       }
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F pf = frag_tr(ZP, LDZF, 0, 16 * mt);
+      const F pf = frag_tr(L, ZP, LDZF, 0, 16 * mt);
 #pragma unroll
-      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(Qs, LDQ, 0, e0 + 16 * el));
+      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(L, Qs, LDQ, 0, e0 + 16 * el));
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dq = sum over slices; G (own columns) -> ZG[e][m], dz -> dzs
     {
-      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      const int tid = fresh_tid();
+      const int t = tid / TPR, q = tid % TPR;
       if (t < count) {
         const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
         store_row(dQh + (size_t)(start + t) * D + e, sum_x(hh, t * LDRH + col));
@@ -529,13 +556,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-      for (int el = 0; el < EH; ++el) store_tile_T<T>(ZG, LDZF, Gs[mt][el], 16 * mt, e0 + 16 * el);
+      for (int el = 0; el < EH; ++el) store_tile_T<T>(L, ZG, LDZF, Gs[mt][el], 16 * mt, e0 + 16 * el);
       if (zown && c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) dzs[f * FW + 16 * mt + 4 * g + r] = Gz[mt][r];
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dK~[s][m] = sum_e V[s][e] G[m][e] + dz[m] + sum_t dA^T[s][t] Q~[t][m] for this
     //      wave's rows s in [16 h, 16 h + 16); Pk = dK~ . K~ (FAVOR+) or masked (ReLU)
@@ -550,15 +580,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int r = 0; r < 4; ++r) acc[r] = (16 * h + 4 * g + r < count) ? dz : 0.f;
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_rm(Vs, LDQ, 16 * h, 32 * kb), frag_tr(ZG, LDZF, 32 * kb, 16 * mt));
-        acc = mma(acc, frag_tr(ZdA, LDZT, 0, 16 * h), frag_tr(Zq, LDZF, 0, 16 * mt));
-        const f32x4 kv = load_tile_T(Zk, LDZK, 16 * h, 16 * mt);
+          acc = mma(acc, frag_rm(L, Vs, LDQ, 16 * h, 32 * kb), frag_tr(L, ZG, LDZF, 32 * kb, 16 * mt));
+        acc = mma(acc, frag_tr(L, ZdA, LDZT, 0, 16 * h), frag_tr(L, Zq, LDZF, 0, 16 * mt));
+        const f32x4 kv = load_tile_T(L, Zk, LDZK, 16 * h, 16 * mt);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
           rk[r] += acc[r];
         }
-        store_tile_T<T>(ZPk, LDZK, acc, 16 * h, 16 * mt);
+        store_tile_T<T>(L, ZPk, LDZK, acc, 16 * h, 16 * mt);
       }
       if (G::KIND == kFavor) {
 #pragma unroll
@@ -571,9 +601,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F qf = frag_tr(Zq, LDZF, 0, 16 * mt);
+      const F qf = frag_tr(L, Zq, LDZF, 0, 16 * mt);
 #pragma unroll
-      for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, frag_tr(dNs, LDQ, 0, e0 + 16 * el));
+      for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, frag_tr(L, dNs, LDQ, 0, e0 + 16 * el));
       if (zown) {
         F dd;
 #pragma unroll
@@ -582,14 +612,17 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dW[m][e] += sum_s Pk[s][m] K[s][e]; dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum_f(Pk)[s]
     //      own columns -> RedY[s][e']
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F pf = frag_rm(ZPk, LDZK, 16 * mt, 0);
+      const F pf = frag_rm(L, ZPk, LDZK, 16 * mt, 0);
 #pragma unroll
-      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(Ks, LDQ, 0, e0 + 16 * el));
+      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(L, Ks, LDQ, 0, e0 + 16 * el));
     }
 #pragma unroll
     for (int st = 0; st < RT; ++st) {
@@ -606,31 +639,39 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_tr(ZPk, LDZK, 32 * kb, 16 * st));
-        store_tile_T<float>(RedY, LDRH, acc, 16 * el, 16 * st);
+          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_tr(L, ZPk, LDZK, 32 * kb, 16 * st));
+        store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
 
     // ---- dk = sum over slices; rows of the next tile -> LDS (their readers are done)
     {
-      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      const int tid = fresh_tid();
+      const int t = tid / TPR, q = tid % TPR;
       if (t < count) {
         const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
         store_row(dKh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
       }
     }
     if (j > j0) {
-      stA.template store<LDQ>(dstA, nrmA, stid);
-      stB.template store<LDQ>(dstB, nrmB, stid);
+      const int st2 = fresh_tid() & 255;
+      stA.template store<LDQ>(dstA, nrmA, st2);
+      stB.template store<LDQ>(dstB, nrmB, st2);
       if (j - 1 > j0) {
         int sn, cn;
         tm.tile(j - 2, sn, cn);
-        stA.fetch(srcA + (size_t)sn * D, cn, stid);
-        stB.fetch(srcB + (size_t)sn * D, cn, stid);
+        stA.fetch(srcA + (size_t)sn * D, cn, st2);
+        stB.fetch(srcB + (size_t)sn * D, cn, st2);
       }
     }
     __syncthreads();
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
   }
 
   // per-workgroup dW partial: this wave's rows and columns

@@ -45,6 +45,24 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int lane_g() { return (threadIdx.x & 63) >> 4; }
 __device__ __forceinline__ int lane_c() { return threadIdx.x & 15; }
+
+// Lane coordinates (g, c) as explicit values.  A kernel may rebuild them from
+// an opaque copy of the thread index (fresh_lane) at the start of a phase, so
+// that the compiler forms the lane-dependent addresses of that phase inside
+// it instead of keeping every one of them live across a long loop.
+struct Lane {
+  int g, c;
+};
+__device__ __forceinline__ int fresh_tid() {
+  int x = threadIdx.x;
+  asm volatile("" : "+v"(x));
+  return x;
+}
+__device__ __forceinline__ Lane fresh_lane() {
+  const int x = fresh_tid();
+  return Lane{(x & 63) >> 4, x & 15};
+}
+__device__ __forceinline__ Lane this_lane() { return Lane{lane_g(), lane_c()}; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 
 // k offset of slot s of lane group g inside a 32-deep block
@@ -125,8 +143,8 @@ __device__ __forceinline__ typename FragT<T>::type tile_half_frag(const f32x4& x
 // Fragment from an LDS matrix stored with the contraction index contiguous:
 // slot s = Z[row0 + c][k0 + kp(g, s)]  (pitch ld elements).
 template <typename T>
-__device__ __forceinline__ typename FragT<T>::type frag_rm(const T* Z, int ld, int row0, int k0) {
-  const int g = lane_g(), c = lane_c();
+__device__ __forceinline__ typename FragT<T>::type frag_rm(const Lane& L, const T* Z, int ld, int row0, int k0) {
+  const int g = L.g, c = L.c;
   const T* p = Z + (row0 + c) * ld + k0 + 4 * g;
   typename FragT<T>::type f;
 #pragma unroll
@@ -136,11 +154,15 @@ __device__ __forceinline__ typename FragT<T>::type frag_rm(const T* Z, int ld, i
   }
   return f;
 }
+template <typename T>
+__device__ __forceinline__ typename FragT<T>::type frag_rm(const T* Z, int ld, int row0, int k0) {
+  return frag_rm(this_lane(), Z, ld, row0, k0);
+}
 
 // Fragment from an LDS matrix stored k-major (contraction index = row):
 // slot s = Z[k0 + kp(g, s)][col0 + c]  (pitch ld elements).
-__device__ __forceinline__ bf16x8 frag_tr(const bf16* Z, int ld, int k0, int col0) {
-  const int g = lane_g(), c = lane_c();
+__device__ __forceinline__ bf16x8 frag_tr(const Lane& L, const bf16* Z, int ld, int k0, int col0) {
+  const int g = L.g, c = L.c;
   const bf16* p0 = Z + (k0 + 4 * g + (c >> 2)) * ld + col0 + 4 * (c & 3);
   const bf16* p1 = p0 + 16 * ld;
   typedef SLIM_LDS i16x4 lds_i16x4;
@@ -156,21 +178,30 @@ __device__ __forceinline__ bf16x8 frag_tr(const bf16* Z, int ld, int k0, int col
   }
   return f;
 }
-__device__ __forceinline__ f32x8 frag_tr(const float* Z, int ld, int k0, int col0) {
-  const int g = lane_g(), c = lane_c();
+__device__ __forceinline__ f32x8 frag_tr(const Lane& L, const float* Z, int ld, int k0, int col0) {
+  const int g = L.g, c = L.c;
   f32x8 f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) f[s] = Z[(k0 + kp(g, s)) * ld + col0 + c];
   return f;
 }
+__device__ __forceinline__ bf16x8 frag_tr(const bf16* Z, int ld, int k0, int col0) {
+  return frag_tr(this_lane(), Z, ld, k0, col0);
+}
+__device__ __forceinline__ f32x8 frag_tr(const float* Z, int ld, int k0, int col0) {
+  return frag_tr(this_lane(), Z, ld, k0, col0);
+}
 
 // Store result tile X[row0 + 4g + r][col0 + c] transposed: Z[col0 + c][row0 + 4g + r].
 template <typename T>
-__device__ __forceinline__ void store_tile_T(T* Z, int ld, const f32x4& x, int row0, int col0) {
-  const int g = lane_g(), c = lane_c();
-  T* p = Z + (col0 + c) * ld + row0 + 4 * g;
+__device__ __forceinline__ void store_tile_T(const Lane& L, T* Z, int ld, const f32x4& x, int row0, int col0) {
+  T* p = Z + (col0 + L.c) * ld + row0 + 4 * L.g;
 #pragma unroll
   for (int r = 0; r < 4; ++r) p[r] = cvt<T>(x[r]);
+}
+template <typename T>
+__device__ __forceinline__ void store_tile_T(T* Z, int ld, const f32x4& x, int row0, int col0) {
+  store_tile_T(this_lane(), Z, ld, x, row0, col0);
 }
 
 // two stacked result tiles as an operand (has_b), or the first one with the
@@ -199,13 +230,16 @@ __device__ __forceinline__ typename FragT<T>::type frag_rm_h(const T* Z, int ld,
 // result-tile values of a matrix stored transposed by store_tile_T:
 // X[row0 + 4g + r][col0 + c] = Z[col0 + c][row0 + 4g + r]
 template <typename T>
-__device__ __forceinline__ f32x4 load_tile_T(const T* Z, int ld, int row0, int col0) {
-  const int g = lane_g(), c = lane_c();
-  const T* p = Z + (col0 + c) * ld + row0 + 4 * g;
+__device__ __forceinline__ f32x4 load_tile_T(const Lane& L, const T* Z, int ld, int row0, int col0) {
+  const T* p = Z + (col0 + L.c) * ld + row0 + 4 * L.g;
   f32x4 x;
 #pragma unroll
   for (int r = 0; r < 4; ++r) x[r] = to_f32(p[r]);
   return x;
+}
+template <typename T>
+__device__ __forceinline__ f32x4 load_tile_T(const T* Z, int ld, int row0, int col0) {
+  return load_tile_T(this_lane(), Z, ld, row0, col0);
 }
 
 // ------------------------------------------------------------- wave reductions
