@@ -169,8 +169,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int i = 0; i < (int)(sizeof(F) / 16); ++i)
       v[i] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane + 16 * i, idx * 64 * (int)sizeof(F), 0);
     return __builtin_bit_cast(F, v);
-  };
-  const int e0 = 16 * EH * h;  // first value column of this wave
+  };  const int e0 = 16 * EH * h;  // first value column of this wave
 
   const size_t SZ = (size_t)M * (D + 1);
   const size_t sidx = (head * a.P + p) * SZ;
@@ -310,7 +309,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     g = L.g;
     c = L.c;
 
-    // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair)
+    // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair); the
+    //      features stay in registers as operands of the scores and of N
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
       const int t = 16 * tt + c;
@@ -318,13 +318,19 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       if (G::KIND == kFavor) qs = fmaxf(fmaxf(qmx[t], qmx[TR + t]), fmaxf(qmx[2 * TR + t], qmx[3 * TR + t])) * kLog2e;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        f32x4 qv = Lq[mt][tt];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          qv[r] = (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(qv[r] * kLog2e - qs) : fmaxf(qv[r], 0.f) + a.relu_eps;
-        store_tile_T<T>(L, Zq, LDZF, qv, 16 * mt, 16 * tt);
+          Lq[mt][tt][r] = (t >= count) ? 0.f
+                          : (G::KIND == kFavor) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs)
+                                                : fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
+        store_tile_T<T>(L, Zq, LDZF, Lq[mt][tt], 16 * mt, 16 * tt);
       }
     }
+    F qf[MB][RT];  // Q~ contracting over this slice's features, columns t
+#pragma unroll
+    for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) qf[kb][tt] = tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt]);
 
     // ---- state before the tile: downdate (eq. 17), or the exact segment start
     if (j == j0) {
@@ -352,7 +358,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
     }
 
-    // ---- scores A^T[s][t] over this slice's features, causal -> ZA[t][s]
+    // ---- scores A^T[s][t] over this slice's features, causal -> ZA[t][s] (for dV)
+    f32x4 At[RT][RT];
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
@@ -360,32 +367,34 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc = zero4();
         if (st <= tt) {
 #pragma unroll
-          for (int kb = 0; kb < MB; ++kb)
-            acc = mma(acc, frag_tr(L, Zk, LDZK, 32 * kb, 16 * st), frag_rm(L, Zq, LDZF, 16 * tt, 32 * kb));
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, frag_tr(L, Zk, LDZK, 32 * kb, 16 * st), qf[kb][tt]);
         }
         if (st == tt) {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (4 * g + r > c) acc[r] = 0.f;
         }
+        At[st][tt] = acc;
         store_tile_T<T>(L, ZA, LDZT, acc, 16 * st, 16 * tt);
       }
     // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
 #pragma unroll
-    for (int tt = 0; tt < RT; ++tt)
+    for (int tt = 0; tt < RT; ++tt) {
+      const F af = tile_pair_frag<T>(At[0][tt], At[1][tt]);  // A^T contracting over rows s
 #pragma unroll
       for (int el = 0; el <= EH; ++el) {
         if (el == EH && !zown) continue;
         const int et = (el < EH) ? h * EH + el : ET;
-        f32x4 acc = mma(zero4(), v_frag(L, et, count), frag_rm(L, ZA, LDZT, 16 * tt, 0));
+        f32x4 acc = mma(zero4(), v_frag(L, et, count), af);
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), frag_rm(L, Zq, LDZF, 16 * tt, 32 * kb));
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
         if (el < EH) {
           store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * tt);
         } else if (g == 0) {
           RedY[(16 * tt + c) * LDRH + 16 * EH] = acc[0];
         }
       }
+    }
     __syncthreads();
     L = fresh_lane();
     g = L.g;
