@@ -395,7 +395,6 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   f.Q = Q;
   f.K = K;
   f.V = V;
-  f.dY = dY;
   f.W = W;
   f.fixed_shift = favor ? kshift : nullptr;
   f.B = (int)p->B;

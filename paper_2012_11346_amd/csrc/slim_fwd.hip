@@ -89,9 +89,7 @@ __device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
 }
 
 // MODE kWalkOutputs: Y and the final state; kWalkSums: only the keys, the
-// state each segment adds; kWalkGrad: the per-segment sum of Q~^T [dN|dD]
-// (needs dY), i.e. what the segment contributes to the state cotangent of
-// the segments before it (eq. 18 accumulated over the segment).
+// state each segment adds.
 template <class G, int MODE>
 __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   typedef typename G::T T;
@@ -99,15 +97,11 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
                 RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDZ = G::LDZ, ZR = G::ZR, LDR = G::LDR, LDF = G::LDF;
   constexpr bool QSIDE = MODE != kWalkSums;
-  constexpr bool GRAD = MODE == kWalkGrad;
   __shared__ __attribute__((aligned(16))) T Qs[QSIDE ? TR * LDQ : 8];
   __shared__ __attribute__((aligned(16))) T Ks[TR * LDQ];
   __shared__ __attribute__((aligned(16))) T Vs[TR * LDQ];
   __shared__ __attribute__((aligned(16))) T Zk[4][QSIDE ? ZR * LDZ : 8];
   __shared__ __attribute__((aligned(16))) float Red[4][QSIDE ? TR * LDR : 4];
-  __shared__ __attribute__((aligned(16))) T dNs[GRAD ? TR * LDQ : 8];
-  __shared__ __attribute__((aligned(16))) T Zq[4][GRAD ? TR * LDF : 8];
-  __shared__ __attribute__((aligned(16))) T dDb[GRAD ? TR + 8 : 8];
   __shared__ float qn[TR], kn[TR], qmx[4][TR], kmx[4];
 
   const int w = wave_id(), g = lane_g(), c = lane_c();
@@ -144,13 +138,6 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int et = 0; et <= ET; ++et) S[mt][et] = zero4();
-  }
-  f32x4 Gs[GRAD ? MT : 1][ET + 1];
-  if constexpr (GRAD) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int et = 0; et <= ET; ++et) Gs[mt][et] = zero4();
   }
 
   // pad rows of the transposed key buffer stay zero
@@ -283,13 +270,6 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
       for (int st = 0; st < RT; ++st)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
-      if constexpr (GRAD) {
-        // Q~ as [t][m] for the cotangent update
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int tt = 0; tt < RT; ++tt) store_tile_T<T>(Zq[w], LDF, Lq[mt][tt], 16 * mt, 16 * tt);
-      }
       __syncthreads();
 
       F qf[MB][RT];
@@ -364,53 +344,15 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
       const bool ok = t < count;
       const float den = Red[0][t * LDR + D] + Red[1][t * LDR + D] + Red[2][t * LDR + D] + Red[3][t * LDR + D];
       const float inv = ok ? 1.f / den : 0.f;
-      if constexpr (!GRAD) {
-        // Y = N / D over all features
-        if (ok) {
-          T* dst = (T*)a.Y + head * (size_t)a.L * D + (size_t)(start + t) * D + q * EPT;
-#pragma unroll
-          for (int i = 0; i < EPT; ++i) {
-            const int e = q * EPT + i;
-            const float n = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-            dst[i] = cvt<T>(n * inv);
-          }
-        }
-      } else {
-        // dN = dY / D, dD = -(dY . Y) / D
-        const T* dYh = (const T*)a.dY + head * (size_t)a.L * D;
-        float dy[EPT];
-        float dot = 0.f;
+      // Y = N / D over all features
+      if (ok) {
+        T* dst = (T*)a.Y + head * (size_t)a.L * D + (size_t)(start + t) * D + q * EPT;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
-          dy[i] = ok ? to_f32(dYh[(size_t)(start + t) * D + e]) : 0.f;
           const float n = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-          dot += dy[i] * (n * inv);
+          dst[i] = cvt<T>(n * inv);
         }
-#pragma unroll
-        for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
-#pragma unroll
-        for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * inv);
-        if (q == 0) dDb[t] = cvt<T>(ok ? -dot * inv : 0.f);
-      }
-      __syncthreads();
-      if constexpr (GRAD) {
-        // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e]
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int et = 0; et <= ET; ++et)
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-              F bfr;
-              if (et < ET) {
-                bfr = frag_tr(dNs, LDQ, 32 * rb, 16 * et);
-              } else {
-#pragma unroll
-                for (int s = 0; s < 8; ++s) bfr[s] = dDb[32 * rb + kp(g, s)];
-              }
-              Gs[mt][et] = mma(Gs[mt][et], frag_tr(Zq[w], LDF, 32 * rb, 16 * mt), bfr);
-            }
       }
     }
     __syncthreads();
@@ -430,8 +372,8 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
 #pragma unroll
-        for (int et = 0; et < ET; ++et) sout[row + 16 * et + c] = GRAD ? Gs[mt][et][r] : S[mt][et][r];
-        if (c == 0) sout[row + D] = GRAD ? Gs[mt][ET][r] : S[mt][ET][r];
+        for (int et = 0; et < ET; ++et) sout[row + 16 * et + c] = S[mt][et][r];
+        if (c == 0) sout[row + D] = S[mt][ET][r];
       }
   }
   if (G::KIND == kFavor && threadIdx.x == 0) {
@@ -601,8 +543,6 @@ hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s) {
     hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkOutputs>), grid, dim3(256), 0, s, a);
   } else if (mode == kWalkSums) {
     hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkSums>), grid, dim3(256), 0, s, a);
-  } else {
-    hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkGrad>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

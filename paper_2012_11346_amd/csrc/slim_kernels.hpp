@@ -11,14 +11,12 @@ namespace slim {
 enum WalkMode {
   kWalkOutputs = 0,  // Y and the final state (forward sweep)
   kWalkSums = 1,     // keys only: the state each segment adds (segment sums)
-  kWalkGrad = 2,     // per-segment sum of Q~^T [dN|dD] (state-cotangent contributions)
 };
 
 struct FwdArgs {
   const void* Q;
   const void* K;
   const void* V;
-  const void* dY;           // kWalkGrad
   const float* W;
   const void* Wfrag;        // fragment-ordered W (WFragLayout)
   void* Y;                  // kWalkOutputs
@@ -28,7 +26,7 @@ struct FwdArgs {
   int seg_stride;           // states per head in seg_state (P, or P + 1 for segment boundaries)
   const float* seg_shift;   // [B,H,P] key shift of seg_state (FAVOR+)
   const float* fixed_shift; // [B,H] key shift used throughout (no online rescaling), or nullptr
-  float* seg_out;           // kWalkSums / kWalkGrad: [B,H,P,M,D+1]
+  float* seg_out;           // kWalkSums: [B,H,P,M,D+1]
   float* seg_shift_out;     // kWalkSums: [B,H,P]
   int B, H, L, C, P;
   float relu_eps;
