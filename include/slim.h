@@ -29,6 +29,8 @@
  *                                    row m holds sum_l g(K_l)_m V_l[j], column
  *                                    d holds sum_l g(K_l)_m
  *       kshift tensors             : [B, H] float32 (FAVOR+ only)
+ *     Q, K, V, Y, dY, dQ, dK, dV and the workspace must be 16-byte aligned
+ *     (rows are moved as 16-byte vectors); other tensors 4-byte aligned.
  *   - The caller owns every buffer.  The library never allocates or frees
  *     device memory; scratch space is the caller's workspace `ws`, whose size
  *     slim_workspace_bytes() gives.  The workspace holds nothing between calls.

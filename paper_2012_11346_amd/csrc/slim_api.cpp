@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 
 #include <climits>
+#include <cstdint>
+#include <initializer_list>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -73,6 +75,16 @@ int check_problem(const slim_problem* p) {
   if (p->kind == SLIM_RELU && !(p->relu_eps > 0.f)) return fail(SLIM_EINVAL, "relu_eps must be > 0");
   if (p->dtype == SLIM_F32 && (int64_t)p->d * p->M > 4096)
     return fail(SLIM_EUNSUPPORTED, "fp32 problems need d*M <= 4096 (got d=%d, M=%d)", (int)p->d, (int)p->M);
+  return SLIM_OK;
+}
+
+bool misaligned(const void* ptr, size_t a) { return ptr != nullptr && ((uintptr_t)ptr & (a - 1)) != 0; }
+
+int check_alignment(std::initializer_list<const void*> rows, std::initializer_list<const void*> words) {
+  for (const void* q : rows)
+    if (misaligned(q, 16)) return fail(SLIM_EINVAL, "row tensors and the workspace must be 16-byte aligned");
+  for (const void* q : words)
+    if (misaligned(q, 4)) return fail(SLIM_EINVAL, "float tensors must be 4-byte aligned");
   return SLIM_OK;
 }
 
@@ -278,6 +290,8 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
   if (X == nullptr || W == nullptr || phi == nullptr) return fail(SLIM_EINVAL, "X, W and phi must be non-NULL");
   if (role != SLIM_QUERY && role != SLIM_KEY) return fail(SLIM_EINVAL, "unknown role %d", role);
   if (p->kind == SLIM_FAVOR_PLUS && shift == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs a shift buffer");
+  st = check_alignment({X}, {W, phi, shift});
+  if (st != SLIM_OK) return st;
   slim::FeatArgs a;
   a.X = X;
   a.W = W;
@@ -304,6 +318,8 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift_out == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift_out");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
+  st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out});
+  if (st != SLIM_OK) return st;
   const int P = plan_segments(p);
   const FwdLayout lay = fwd_layout(p, P);
   if (lay.total > 0 && (ws == nullptr || ws_bytes < lay.total))
@@ -378,6 +394,8 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift (kshift_out of slim_fwd)");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
+  st = check_alignment({Q, K, V, dY, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in});
+  if (st != SLIM_OK) return st;
   const int P = plan_segments(p);
   const BwdLayout lay = bwd_layout(p, P);
   if (ws == nullptr || ws_bytes < lay.total)

@@ -76,29 +76,49 @@ def test_invalid_problems_are_rejected(S, kw, code):
     assert S.LIB.slim_last_error().decode()
 
 
+# a fake, suitably aligned device address: validation rejects before any use
+A = 1 << 12
+
+
 def test_null_pointers_are_rejected_before_any_launch(S):
     p = _p(S)
-    st = S.LIB.slim_fwd(ctypes.byref(p), None, 1, 1, 1, None, None, 1, 1, 1, 1, 1 << 30, None)
+    # arguments: p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ws, ws_bytes, stream
+    st = S.LIB.slim_fwd(ctypes.byref(p), None, A, A, A, None, None, A, A, A, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # FAVOR+ needs a key-shift output
-    st = S.LIB.slim_fwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, 1, None, 1, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # a state without its shift
-    st = S.LIB.slim_fwd(ctypes.byref(p), 1, 1, 1, 1, 1, None, 1, 1, 1, 1, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, A, None, A, A, A, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # arguments: p, Q, K, V, W, state_in, kshift_in, kshift, dY, dstate_out, dQ, dK, dV, dW, dstate_in,
     # ws, ws_bytes, stream
-    st = S.LIB.slim_bwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, 1, None, None, 1, 1, 1, None, 1, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # dQ missing
-    st = S.LIB.slim_bwd(ctypes.byref(p), 1, 1, 1, 1, None, None, None, 1, None, 1, 1, 1, 1, None, 1, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, A, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # kshift missing (FAVOR+)
-    st = S.LIB.slim_bwd(ctypes.byref(p), 1, 1, 1, 1, 1, None, 1, 1, None, 1, 1, 1, 1, None, 1, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, A, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # state_in without kshift_in
-    st = S.LIB.slim_bwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, 1, None, 1, 1, 1, 1, None, 1, 0, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, A, A, A, None, A, 0, None)
     assert st == S.SLIM_EWORKSPACE
-    st = S.LIB.slim_featmap(ctypes.byref(p), None, 1, 0, 1, 1, None)
+    st = S.LIB.slim_featmap(ctypes.byref(p), None, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL
-    st = S.LIB.slim_featmap(ctypes.byref(p), 1, 1, 5, 1, 1, None)
+    st = S.LIB.slim_featmap(ctypes.byref(p), A, A, 5, A, A, None)
+    assert st == S.SLIM_EINVAL
+
+
+def test_misaligned_tensors_are_rejected_before_any_launch(S):
+    p = _p(S)
+    # a row tensor (dY) 8 bytes off a 16-byte boundary
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, A, A, A, A, None, A, 1 << 30, None)
+    assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
+    # the workspace
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A, A + 4, 1 << 30, None)
+    assert st == S.SLIM_EINVAL
+    # a float tensor (W) off a 4-byte boundary
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A + 2, None, None, A, A, A, A, 1 << 30, None)
+    assert st == S.SLIM_EINVAL
+    st = S.LIB.slim_featmap(ctypes.byref(p), A + 8, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL
 
 
