@@ -97,12 +97,14 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
                 RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDZ = G::LDZ, ZR = G::ZR, LDR = G::LDR, LDF = G::LDF;
   constexpr bool QSIDE = MODE != kWalkSums;
-  __shared__ __attribute__((aligned(16))) T Qs[QSIDE ? TR * LDQ : 8];
-  __shared__ __attribute__((aligned(16))) T Ks[TR * LDQ];
-  __shared__ __attribute__((aligned(16))) T Vs[TR * LDQ];
+  // rows of the tile, double-buffered: tile j reads buffer (j - j0) & 1
+  constexpr int TQ = TR * LDQ;
+  __shared__ __attribute__((aligned(16))) T Qbuf[QSIDE ? 2 * TQ : 8];
+  __shared__ __attribute__((aligned(16))) T Kbuf[2 * TQ];
+  __shared__ __attribute__((aligned(16))) T Vbuf[2 * TQ];
   __shared__ __attribute__((aligned(16))) T Zk[4][QSIDE ? ZR * LDZ : 8];
   __shared__ __attribute__((aligned(16))) float Red[4][QSIDE ? TR * LDR : 4];
-  __shared__ float qn[TR], kn[TR], qmx[4][TR], kmx[4];
+  __shared__ float qnb[2][TR], knb[2][TR], qmx[4][TR], kmx[4];
 
   const int w = wave_id(), g = lane_g(), c = lane_c();
   const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -150,30 +152,43 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   const float half_log2M = 0.5f * __log2f((float)M);
   constexpr int TPR = 256 / TR, EPT = D / TPR;
 
-  // rows of the next tile are fetched while the current one is computed
+  // Rows two tiles ahead are fetched into registers; at the start of tile j
+  // the rows of tile j + 1 go into the other buffer (its readers, tile j - 1,
+  // finished before tile j - 1's last barrier) and become visible at tile j's
+  // barriers.
   RowStage<T, D, TR, 256> sq, sk, sv;
-  if (j1 > j0) {
+  auto fetch = [&](int jj) {
     int s0, n0;
-    tm.tile(j0, s0, n0);
+    tm.tile(jj, s0, n0);
     if constexpr (QSIDE) sq.fetch(Qh + (size_t)s0 * D, n0, threadIdx.x);
     sk.fetch(Kh + (size_t)s0 * D, n0, threadIdx.x);
     sv.fetch(Vh + (size_t)s0 * D, n0, threadIdx.x);
+  };
+  auto store = [&](int bf) {
+    if constexpr (QSIDE) sq.template store<LDQ>(Qbuf + bf * TQ, G::KIND == kFavor ? qnb[bf] : nullptr, threadIdx.x);
+    sk.template store<LDQ>(Kbuf + bf * TQ, G::KIND == kFavor ? knb[bf] : nullptr, threadIdx.x);
+    sv.template store<LDQ>(Vbuf + bf * TQ, nullptr, threadIdx.x);
+  };
+  if (j1 > j0) {
+    fetch(j0);
+    store(0);
+    if (j0 + 1 < j1) fetch(j0 + 1);
   }
+  __syncthreads();
 
   for (int j = j0; j < j1; ++j) {
     int start, count;
     tm.tile(j, start, count);
-    if constexpr (QSIDE) sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr, threadIdx.x);
-    sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, threadIdx.x);
-    sv.template store<LDQ>(Vs, nullptr, threadIdx.x);
+    const int bf = (j - j0) & 1;
     if (j + 1 < j1) {
-      int sn, cn;
-      tm.tile(j + 1, sn, cn);
-      if constexpr (QSIDE) sq.fetch(Qh + (size_t)sn * D, cn, threadIdx.x);
-      sk.fetch(Kh + (size_t)sn * D, cn, threadIdx.x);
-      sv.fetch(Vh + (size_t)sn * D, cn, threadIdx.x);
+      store(bf ^ 1);
+      if (j + 2 < j1) fetch(j + 2);
     }
-    __syncthreads();
+    const T* Qs = Qbuf + bf * TQ;
+    const T* Ks = Kbuf + bf * TQ;
+    const T* Vs = Vbuf + bf * TQ;
+    const float* qn = qnb[bf];
+    const float* kn = knb[bf];
 
     f32x4 Lq[QSIDE ? MT : 1][RT], Lk[RT][MT];
     if constexpr (QSIDE) query_logits<G>(Lq, Wf, Qs, qn);
@@ -205,7 +220,9 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
         if (lane_id() == 0) kmx[w] = v;
       }
     }
-    __syncthreads();
+    // row maxima of all waves (and, with queries, the previous tile's
+    // reduction reads are finished before N overwrites them)
+    if (QSIDE || (G::KIND == kFavor && !fixed)) __syncthreads();
 
     if (G::KIND == kFavor) {
       if (!fixed) {
@@ -270,7 +287,6 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
       for (int st = 0; st < RT; ++st)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
-      __syncthreads();
 
       F qf[MB][RT];
 #pragma unroll
@@ -338,24 +354,26 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
         for (int rb = 0; rb < RB; ++rb)
           S[mt][et] = mma(S[mt][et], tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]), vf[rb][et]);
 
+    __syncthreads();
     if constexpr (QSIDE) {
-      __syncthreads();
+      // Y = N / D over all features (vector reads of the reduction rows)
+      static_assert(EPT % 4 == 0, "");
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
-      const bool ok = t < count;
-      const float den = Red[0][t * LDR + D] + Red[1][t * LDR + D] + Red[2][t * LDR + D] + Red[3][t * LDR + D];
-      const float inv = ok ? 1.f / den : 0.f;
-      // Y = N / D over all features
-      if (ok) {
-        T* dst = (T*)a.Y + head * (size_t)a.L * D + (size_t)(start + t) * D + q * EPT;
+      if (t < count) {
+        const float inv = 1.f / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
+        typedef T tvec __attribute__((ext_vector_type(EPT)));
+        tvec o;
 #pragma unroll
-        for (int i = 0; i < EPT; ++i) {
-          const int e = q * EPT + i;
-          const float n = Red[0][t * LDR + e] + Red[1][t * LDR + e] + Red[2][t * LDR + e] + Red[3][t * LDR + e];
-          dst[i] = cvt<T>(n * inv);
+        for (int h4 = 0; h4 < EPT / 4; ++h4) {
+          const int idx = t * LDR + q * EPT + 4 * h4;
+          const f32x4 n = (*(const f32x4*)&Red[0][idx] + *(const f32x4*)&Red[1][idx]) +
+                          (*(const f32x4*)&Red[2][idx] + *(const f32x4*)&Red[3][idx]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[4 * h4 + i] = cvt<T>(n[i] * inv);
         }
+        *(tvec*)((T*)a.Y + head * (size_t)a.L * D + (size_t)(start + t) * D + q * EPT) = o;
       }
     }
-    __syncthreads();
   }
 
   // outputs of the segment
