@@ -68,6 +68,13 @@ def load_traffic(kernel: str, units_per_launch: float):
     return k.get("bytes_per_launch")
 
 
+def bwd_walk_name(wl, d: int, M: int) -> str:
+    """Name of the reverse-walk kernel the library launches for this problem:
+    the 8-wave form for bf16 problems with 32 or 64 features per wave."""
+    forced4 = os.environ.get("SLIM_BWD_WAVES") == "4"
+    return "bwd_walk8_kernel" if (wl.dtype == "bf16" and M // 4 in (32, 64) and not forced4) else "bwd_walk_kernel"
+
+
 def cpu_baseline(x, C: int, B: int, H: int, L: int):
     """Time the fp64 oracle (Algorithm 1 with the in-slice quadratic form) on
     the whole batch of the workload (every batch element and head, full
@@ -109,6 +116,8 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--sweep-steps", type=int, default=3)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="only copy a device buffer of this many MiB (calibration of memory counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path runs on a single "
@@ -124,6 +133,16 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.copy_mib > 0:
+        # a plain copy of known size: reads and writes copy_mib MiB once per launch
+        n = args.copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "launches": 3}), flush=True)
+        return
     wl = workload(args.workload)
     B, H, L, d, M = wl.B, wl.H, wl.L, wl.d, wl.M
     kind = wl.kind
@@ -203,7 +222,7 @@ def main():
     # the walk kernels do all of the algorithmic work of their phase; the
     # segment pre-passes and scans are extra work of the parallel split
     if r["bwd_walk_ms"] >= r["fwd_walk_ms"]:
-        dominant, dom_ms, dom_flops = "bwd_walk_kernel", r["bwd_walk_ms"], fl_b * units
+        dominant, dom_ms, dom_flops = bwd_walk_name(wl, d, M), r["bwd_walk_ms"], fl_b * units
     else:
         dominant, dom_ms, dom_flops = "fwd_walk_kernel", r["fwd_walk_ms"], fl_f * units
     achieved = dom_flops / (dom_ms / 1e3)
