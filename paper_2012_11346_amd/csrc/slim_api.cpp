@@ -114,6 +114,17 @@ int plan_segments(const slim_problem* p) {
   return std::max(1, P);
 }
 
+// Sub-segments per segment for the key-sum pass: the sums are associative,
+// and the pass fits two workgroups per compute unit, so each segment's sum
+// is split in two when that leaves at least two tiles per part.
+// SLIM_SUM_SPLIT (debugging) forces 1 or 2.
+int plan_sum_split(const slim_problem* p, int P) {
+  const char* env = getenv("SLIM_SUM_SPLIT");
+  const int n_tiles = count_tiles(p);
+  if (env != nullptr && (atoi(env) == 1 || atoi(env) == 2)) return n_tiles >= 2 * P ? atoi(env) : 1;
+  return n_tiles >= 4 * P ? 2 : 1;
+}
+
 size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
@@ -125,7 +136,7 @@ struct FwdLayout {
 FwdLayout fwd_layout(const slim_problem* p, int P) {
   FwdLayout l{0, 0, 0, 0, 0};
   if (P <= 1) return l;
-  const size_t n = (size_t)p->B * p->H * P;
+  const size_t n = (size_t)p->B * p->H * P * plan_sum_split(p, P);
   size_t off = 0;
   l.seg_sum = off;
   off += align256(n * state_elems(p) * sizeof(float));
@@ -153,10 +164,11 @@ BwdLayout bwd_layout(const slim_problem* p, int P) {
   size_t off = 0;
   l.wfrag = off;
   off += align256(wfrag_bytes_of(p));
+  const int P2 = P * plan_sum_split(p, P);
   l.seg_sum = off;
-  off += align256(heads * P * se);
+  off += align256(heads * P2 * se);
   l.bounds = off;
-  off += align256(heads * (P + 1) * se);
+  off += align256(heads * (P2 + 1) * se);
   if (P > 1) {
     l.gc = off;
     off += align256(heads * P * se);
@@ -342,8 +354,10 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.relu_eps = p->relu_eps;
   hipError_t e = hipSuccess;
   if (P > 1) {
-    // (1) what each segment adds, with its own running key shift
+    // (1) what each sub-segment adds, with its own running key shift
+    const int S2 = plan_sum_split(p, P), P2 = P * S2;
     slim::FwdArgs k = a;
+    k.P = P2;
     k.seg_out = (float*)(w + lay.seg_sum);
     k.seg_shift_out = (float*)(w + lay.seg_shift);
     e = dp.fwd(k, slim::kWalkSums, s);
@@ -358,18 +372,20 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     sc.out = (float*)(w + lay.starts);
     sc.out_shift = (float*)(w + lay.start_shift);
     sc.BH = (int)(p->B * p->H);
-    sc.P = P;
+    sc.P = P2;
     sc.SZ = (int)state_elems(p);
     sc.favor = favor ? 1 : 0;
     e = slim::launch_scan_fwd(sc, s);
     if (e != hipSuccess) return hip_fail(e, "segment-scan launch");
     a.seg_state = sc.out;
     a.seg_shift = sc.out_shift;
-    a.seg_stride = P;
+    a.seg_stride = P2;
+    a.seg_step = S2;
   } else {
     a.seg_state = state_in;
     a.seg_shift = kshift_in;
     a.seg_stride = 1;
+    a.seg_step = 1;
   }
   // (3) the walk proper
   a.Y = Y;
@@ -424,7 +440,9 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
 
   // (1) segment sums with the shift the reverse walk uses, so that every
   //     downdate subtracts exactly the rounded features that were added
+  const int S2 = plan_sum_split(p, P), P2 = P * S2;
   slim::FwdArgs k = f;
+  k.P = P2;
   k.seg_out = (float*)(w + lay.seg_sum);
   e = dp.fwd(k, slim::kWalkSums, s);
   if (e != hipSuccess) return hip_fail(e, "segment-sum launch");
@@ -437,7 +455,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   sc.shift = favor ? kshift : nullptr;
   sc.out = (float*)(w + lay.bounds);
   sc.BH = BH;
-  sc.P = P;
+  sc.P = P2;
   sc.SZ = SZ;
   sc.favor = favor ? 1 : 0;
   e = slim::launch_scan_bwd(sc, s);
@@ -459,6 +477,8 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.Wfrag = wf.out;
   a.kshift = favor ? kshift : nullptr;
   a.bounds = sc.out;
+  a.bound_stride = P2 + 1;
+  a.bound_step = S2;
   a.dstate_out = dstate_out;
   a.g_final = P > 1 ? (float*)(w + lay.gc) : nullptr;
   a.init_shift = favor ? kshift_in : nullptr;

@@ -112,8 +112,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 
   const size_t SZ = (size_t)M * (D + 1);
   const size_t sidx = (head * a.P + p) * SZ;
-  const float* bstart = a.bounds + (head * (a.P + 1) + p) * SZ;
-  const float* bend = bstart + SZ;
+  const float* bend = a.bounds + (head * a.bound_stride + (size_t)(p + 1) * a.bound_step) * SZ;
   float r0 = 1.f;
   if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
@@ -144,6 +143,12 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   const TileMap tm(a.L, a.C, TR);
   const int n_tiles = tm.count_tiles();
   const int j0 = (int)((int64_t)p * n_tiles / a.P), j1 = (int)((int64_t)(p + 1) * n_tiles / a.P);
+  // exact states at the starts of the sub-segments inside this segment: the
+  // walk resets to them instead of downdating, so downdates never run past
+  // one sub-segment (the last reset is the segment's own start)
+  const int P2 = a.bound_stride - 1;
+  int qreset = (p + 1) * a.bound_step - 1;
+  int jreset = (int)((int64_t)qreset * n_tiles / P2);
   const float half_log2M = 0.5f * __log2f((float)M);
   const float koff = (G::KIND == kFavor) ? a.kshift[head] * kLog2e + half_log2M : 0.f;
   constexpr int TPR = 256 / TR, EPT = D / TPR;
@@ -261,15 +266,18 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     __syncthreads();
 
     // ---- b1: state before the tile
-    if (j == j0) {
+    if (j == jreset) {
+      const float* bq = a.bounds + (head * a.bound_stride + (size_t)qreset) * SZ;
+      --qreset;
+      jreset = (int)((int64_t)qreset * n_tiles / P2);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t row = (size_t)(w * FW + 16 * mt + 4 * g + r) * (D + 1);
 #pragma unroll
-          for (int et = 0; et < ET; ++et) S[mt][et][r] = bstart[row + 16 * et + c];
-          S[mt][ET][r] = bstart[row + D];
+          for (int et = 0; et < ET; ++et) S[mt][et][r] = bq[row + 16 * et + c];
+          S[mt][ET][r] = bq[row + D];
         }
     } else {
 #pragma unroll

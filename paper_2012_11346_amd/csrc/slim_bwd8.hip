@@ -173,8 +173,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
   const size_t SZ = (size_t)M * (D + 1);
   const size_t sidx = (head * a.P + p) * SZ;
-  const float* bstart = a.bounds + (head * (a.P + 1) + p) * SZ;
-  const float* bend = bstart + SZ;
+  const float* bend = a.bounds + (head * a.bound_stride + (size_t)(p + 1) * a.bound_step) * SZ;
   float r0 = 1.f;
   if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
@@ -207,6 +206,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const TileMap tm(a.L, a.C, TR);
   const int n_tiles = tm.count_tiles();
   const int j0 = (int)((int64_t)p * n_tiles / a.P), j1 = (int)((int64_t)(p + 1) * n_tiles / a.P);
+  // exact states at the starts of the sub-segments inside this segment: the
+  // walk resets to them instead of downdating, so downdates never run past
+  // one sub-segment (the last reset is the segment's own start)
+  const int P2 = a.bound_stride - 1;
+  int qreset = (p + 1) * a.bound_step - 1;
+  int jreset = (int)((int64_t)qreset * n_tiles / P2);
   const float half_log2M = 0.5f * __log2f((float)M);
   const float koff = (G::KIND == kFavor) ? a.kshift[head] * kLog2e + half_log2M : 0.f;
 
@@ -333,8 +338,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int tt = 0; tt < RT; ++tt) qf[kb][tt] = tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt]);
 
     // ---- state before the tile: downdate (eq. 17), or the exact segment start
-    if (j == j0) {
-      const float* bs = bstart + (size_t)(f * FW) * (D + 1) + e0;
+    if (j == jreset) {
+      const float* bs = a.bounds + (head * a.bound_stride + (size_t)qreset) * SZ + (size_t)(f * FW) * (D + 1) + e0;
+      --qreset;
+      jreset = (int)((int64_t)qreset * n_tiles / P2);
       int lo = 4 * g * (D + 1) + c;
       asm volatile("" : "+v"(lo));  // lane offsets are formed here, not kept live through the walk
 #pragma unroll

@@ -91,7 +91,8 @@ __device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
 // MODE kWalkOutputs: Y and the final state; kWalkSums: only the keys, the
 // state each segment adds.
 template <class G, int MODE>
-__global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
+// (the key-only pass fits two workgroups per compute unit)
+__global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kernel(FwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
@@ -123,7 +124,8 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
   const bool fixed = a.fixed_shift != nullptr;
   if (G::KIND == kFavor && fixed) cur = a.fixed_shift[head];
   const size_t sidx = (head * a.P + p) * (size_t)M * (D + 1);
-  const float* sin = a.seg_state ? a.seg_state + (head * a.seg_stride + p) * (size_t)M * (D + 1) : nullptr;
+  const size_t sstate = head * a.seg_stride + (size_t)p * a.seg_step;
+  const float* sin = a.seg_state ? a.seg_state + sstate * (size_t)M * (D + 1) : nullptr;
   if (sin != nullptr) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -134,7 +136,7 @@ __global__ __launch_bounds__(256, 1) void fwd_walk_kernel(FwdArgs a) {
         for (int et = 0; et < ET; ++et) S[mt][et][r] = sin[row + 16 * et + c];
         S[mt][ET][r] = sin[row + D];
       }
-    if (G::KIND == kFavor && !fixed) cur = a.seg_shift[head * a.P + p];
+    if (G::KIND == kFavor && !fixed) cur = a.seg_shift[sstate];
   } else {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)

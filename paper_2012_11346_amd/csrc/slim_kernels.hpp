@@ -23,8 +23,9 @@ struct FwdArgs {
   float* state_out;         // kWalkOutputs: [B,H,M,D+1] or nullptr (written by the last segment)
   float* kshift_out;        // kWalkOutputs: [B,H] or nullptr
   const float* seg_state;   // [B,H,seg_stride,M,D+1] state each segment starts from, or nullptr (zero)
-  int seg_stride;           // states per head in seg_state (P, or P + 1 for segment boundaries)
-  const float* seg_shift;   // [B,H,P] key shift of seg_state (FAVOR+)
+  int seg_stride;           // states per head in seg_state
+  int seg_step;             // segment p starts from state p * seg_step of its head
+  const float* seg_shift;   // [B,H,seg_stride] key shift of seg_state (FAVOR+), same indexing
   const float* fixed_shift; // [B,H] key shift used throughout (no online rescaling), or nullptr
   float* seg_out;           // kWalkSums: [B,H,P,M,D+1]
   float* seg_shift_out;     // kWalkSums: [B,H,P]
@@ -66,7 +67,8 @@ struct BwdArgs {
   const float* W;
   const void* Wfrag;        // fragment-ordered W (WFragLayout)
   const float* kshift;      // [B,H] key shift of every state below (FAVOR+)
-  const float* bounds;      // [B,H,P+1,M,D+1] exact state at each segment boundary
+  const float* bounds;      // [B,H,bound_stride,M,D+1] exact states at (sub-)segment boundaries
+  int bound_stride, bound_step;  // segment p spans boundaries p * bound_step .. (p + 1) * bound_step
   const float* dstate_out;  // [B,H,M,D+1] cotangent of the final state (segment P-1 starts from it), or nullptr
   float* g_final;           // [B,H,P,M,D+1] cotangent each segment's walk ends with (P > 1), or nullptr
   const float* init_shift;  // [B,H] key shift of the caller's initial state (scales dstate_in), or nullptr

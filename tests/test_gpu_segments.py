@@ -19,13 +19,16 @@ from tests.gpu_common import TOL, dev, host64, need_gpu, report
 pytestmark = pytest.mark.gpu
 
 
-def _fwd_bwd(x, C, kind, segments=None):
+def _fwd_bwd(x, C, kind, segments=None, sum_split=None):
     from paper_2012_11346_amd import slim
 
     old = os.environ.get("SLIM_SEGMENTS")
+    old_split = os.environ.get("SLIM_SUM_SPLIT")
     try:
         if segments is not None:
             os.environ["SLIM_SEGMENTS"] = str(segments)
+        if sum_split is not None:
+            os.environ["SLIM_SUM_SPLIT"] = str(sum_split)
         Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
         Y, st, ks = slim.fwd(Q, K, V, W, C, kind)
         g = slim.bwd(Q, K, V, W, dY, C, ks, kind)
@@ -35,6 +38,10 @@ def _fwd_bwd(x, C, kind, segments=None):
             os.environ.pop("SLIM_SEGMENTS", None)
         else:
             os.environ["SLIM_SEGMENTS"] = old
+        if old_split is None:
+            os.environ.pop("SLIM_SUM_SPLIT", None)
+        else:
+            os.environ["SLIM_SUM_SPLIT"] = old_split
     return Y, st, ks, g
 
 
@@ -47,8 +54,10 @@ SEG_CASES = [
 ]
 
 
+@pytest.mark.parametrize("split", [1, 2])
 @pytest.mark.parametrize("i", range(len(SEG_CASES)))
-def test_results_do_not_depend_on_segments(i):
+def test_results_do_not_depend_on_segments(i, split):
+    """Segments P and the split of each segment's key sums (1 or 2 parts)."""
     need_gpu()
     name, B, H, L, d, M, C, dtype, kind, segs = SEG_CASES[i]
     x = make_inputs(Workload(name, 300 + i, B, H, L, d, M, (C,), dtype, kind))
@@ -57,8 +66,8 @@ def test_results_do_not_depend_on_segments(i):
     _, stref = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind, within="quadratic")
     tol = TOL[dtype]
     for P in segs:
-        print(f"[segments] case={name} P={P}", flush=True)
-        Y, st, ks, g = _fwd_bwd(x, C, kind, P)
+        print(f"[segments] case={name} P={P} split={split}", flush=True)
+        Y, st, ks, g = _fwd_bwd(x, C, kind, P, split)
         report(f"Y P={P}", host64(Y), Yref, tol)
         s = host64(st)
         if kind == "favor+":
