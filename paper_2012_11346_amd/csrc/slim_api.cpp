@@ -90,9 +90,10 @@ int check_alignment(std::initializer_list<const void*> rows, std::initializer_li
 
 int clamp_C(const slim_problem* p) { return (int)(p->C > p->L ? p->L : p->C); }
 
-// Workgroups per device the segment plan aims for: one per compute unit (the
-// walk kernels run one workgroup per CU).
+// Workgroups per device the segment plans aim for: the reverse walk runs one
+// workgroup per compute unit (256 CUs), the forward-family walks two.
 constexpr int kTargetWorkgroups = 256;
+constexpr int kTargetWorkgroupsForward = 512;
 // Segments shorter than this many tiles are not worth their start-up cost.
 constexpr int kMinTilesPerSegment = 4;
 
@@ -104,15 +105,19 @@ int count_tiles(const slim_problem* p) {
 // in parallel and are stitched together by exact scans of their states.  The
 // count depends on B*H and the device size, not on L once L is long enough,
 // so workspace stays flat in L.  SLIM_SEGMENTS (debugging) forces a count.
-int plan_segments(const slim_problem* p) {
+int plan_segments_for(const slim_problem* p, int target) {
   const int n_tiles = count_tiles(p);
   const char* env = getenv("SLIM_SEGMENTS");
   if (env != nullptr && atoi(env) > 0) return std::max(1, std::min(atoi(env), n_tiles));
   const int64_t heads = p->B * p->H;
-  int P = (int)((kTargetWorkgroups + heads - 1) / heads);
+  int P = (int)((target + heads - 1) / heads);
   P = std::min(P, std::max(1, n_tiles / kMinTilesPerSegment));
   return std::max(1, P);
 }
+// segments of the backward (and of slim_num_segments)
+int plan_segments(const slim_problem* p) { return plan_segments_for(p, kTargetWorkgroups); }
+// segments of the forward
+int plan_fwd_segments(const slim_problem* p) { return plan_segments_for(p, kTargetWorkgroupsForward); }
 
 // Sub-segments per segment for the key-sum pass: the sums are associative,
 // and the pass fits two workgroups per compute unit, so each segment's sum
@@ -122,7 +127,8 @@ int plan_sum_split(const slim_problem* p, int P) {
   const char* env = getenv("SLIM_SUM_SPLIT");
   const int n_tiles = count_tiles(p);
   if (env != nullptr && (atoi(env) == 1 || atoi(env) == 2)) return n_tiles >= 2 * P ? atoi(env) : 1;
-  return n_tiles >= 4 * P ? 2 : 1;
+  const int64_t wgs = p->B * p->H * (int64_t)P;
+  return (n_tiles >= 4 * P && 2 * wgs <= kTargetWorkgroupsForward) ? 2 : 1;
 }
 
 size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
@@ -248,7 +254,7 @@ Dispatch dispatch(const slim_problem* p) {
 
 size_t wfrag_bytes_of(const slim_problem* p) { return dispatch(p).wfrag_bytes(); }
 
-size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_segments(p)).total; }
+size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_fwd_segments(p)).total; }
 size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
 
 }  // namespace
@@ -332,7 +338,7 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   }
   st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out});
   if (st != SLIM_OK) return st;
-  const int P = plan_segments(p);
+  const int P = plan_fwd_segments(p);
   const FwdLayout lay = fwd_layout(p, P);
   if (lay.total > 0 && (ws == nullptr || ws_bytes < lay.total))
     return fail(SLIM_EWORKSPACE, "forward workspace needs %zu bytes, got %zu", lay.total, ws == nullptr ? 0 : ws_bytes);

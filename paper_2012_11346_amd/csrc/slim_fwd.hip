@@ -36,24 +36,24 @@ __device__ __forceinline__ void load_w_frags(typename FragT<typename G::T>::type
 // operand fragment of [V|1] over rows [k0, k0 + 32) for value tile et (et ==
 // ET is the all-ones column block, zero on rows >= count)
 template <class G>
-__device__ __forceinline__ typename FragT<typename G::T>::type v_frag(const typename G::T* Vs, int k0, int et,
-                                                                        int count) {
+__device__ __forceinline__ typename FragT<typename G::T>::type v_frag(const Lane& L, const typename G::T* Vs, int k0,
+                                                                        int et, int count) {
   typedef typename G::T T;
-  if (et < G::ET) return frag_tr(Vs, G::LDQ, k0, 16 * et);
+  if (et < G::ET) return frag_tr(L, Vs, G::LDQ, k0, 16 * et);
   typename FragT<T>::type f;
-  const int g = lane_g();
+  const int rem = count - k0 - 4 * L.g;  // rows k0 + kp(g, s) < count
 #pragma unroll
-  for (int s = 0; s < 8; ++s) f[s] = cvt<T>((k0 + kp(g, s) < count) ? 1.f : 0.f);
+  for (int s = 0; s < 8; ++s) f[s] = cvt<T>(((s & 3) + 16 * (s >> 2) < rem) ? 1.f : 0.f);
   return f;
 }
 
 // Query logits, transposed: Lq[mt][tt] holds rows m (features of this wave),
 // columns t.  The accumulator starts at -|q_t|^2/2 for FAVOR+.
 template <class G>
-__device__ __forceinline__ void query_logits(f32x4 (&Lq)[G::MT][G::RT],
+__device__ __forceinline__ void query_logits(const Lane& L, f32x4 (&Lq)[G::MT][G::RT],
                                              const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
                                              const typename G::T* Qs, const float* qn) {
-  const int c = lane_c();
+  const int c = L.c;
 #pragma unroll
   for (int tt = 0; tt < G::RT; ++tt) {
     const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
@@ -61,7 +61,7 @@ __device__ __forceinline__ void query_logits(f32x4 (&Lq)[G::MT][G::RT],
     for (int mt = 0; mt < G::MT; ++mt) {
       f32x4 acc = {init, init, init, init};
 #pragma unroll
-      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(Qs, G::LDQ, 16 * tt, 32 * kb));
+      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(L, Qs, G::LDQ, 16 * tt, 32 * kb));
       Lq[mt][tt] = acc;
     }
   }
@@ -69,10 +69,10 @@ __device__ __forceinline__ void query_logits(f32x4 (&Lq)[G::MT][G::RT],
 
 // Key logits: Lk[st][mt] holds rows s, columns m (features of this wave).
 template <class G>
-__device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
+__device__ __forceinline__ void key_logits(const Lane& L, f32x4 (&Lk)[G::RT][G::MT],
                                            const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
                                            const typename G::T* Ks, const float* kn) {
-  const int g = lane_g();
+  const int g = L.g;
 #pragma unroll
   for (int st = 0; st < G::RT; ++st) {
     f32x4 init;
@@ -82,7 +82,7 @@ __device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
     for (int mt = 0; mt < G::MT; ++mt) {
       f32x4 acc = init;
 #pragma unroll
-      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, frag_rm(Ks, G::LDQ, 16 * st, 32 * kb), Wf[mt][kb]);
+      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, frag_rm(L, Ks, G::LDQ, 16 * st, 32 * kb), Wf[mt][kb]);
       Lk[st][mt] = acc;
     }
   }
@@ -91,16 +91,17 @@ __device__ __forceinline__ void key_logits(f32x4 (&Lk)[G::RT][G::MT],
 // MODE kWalkOutputs: Y and the final state; kWalkSums: only the keys, the
 // state each segment adds.
 template <class G, int MODE>
-// (the key-only pass fits two workgroups per compute unit)
-__global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kernel(FwdArgs a) {
+// (two workgroups per compute unit)
+__global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
                 RT = G::RT, RB = G::RB, LDQ = G::LDQ, LDZ = G::LDZ, ZR = G::ZR, LDR = G::LDR, LDF = G::LDF;
   constexpr bool QSIDE = MODE != kWalkSums;
-  // rows of the tile, double-buffered: tile j reads buffer (j - j0) & 1
+  // rows of the tile: keys and values double-buffered (tile j reads buffer
+  // (j - j0) & 1), queries single-buffered (read only before the first barrier)
   constexpr int TQ = TR * LDQ;
-  __shared__ __attribute__((aligned(16))) T Qbuf[QSIDE ? 2 * TQ : 8];
+  __shared__ __attribute__((aligned(16))) T Qbuf[QSIDE ? TQ : 8];
   __shared__ __attribute__((aligned(16))) T Kbuf[2 * TQ];
   __shared__ __attribute__((aligned(16))) T Vbuf[2 * TQ];
   __shared__ __attribute__((aligned(16))) T Zk[4][QSIDE ? ZR * LDZ : 8];
@@ -162,18 +163,23 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
   auto fetch = [&](int jj) {
     int s0, n0;
     tm.tile(jj, s0, n0);
-    if constexpr (QSIDE) sq.fetch(Qh + (size_t)s0 * D, n0, threadIdx.x);
-    sk.fetch(Kh + (size_t)s0 * D, n0, threadIdx.x);
-    sv.fetch(Vh + (size_t)s0 * D, n0, threadIdx.x);
+    const int tid = fresh_tid();
+    if constexpr (QSIDE) sq.fetch(Qh + (size_t)s0 * D, n0, tid);
+    sk.fetch(Kh + (size_t)s0 * D, n0, tid);
+    sv.fetch(Vh + (size_t)s0 * D, n0, tid);
   };
-  auto store = [&](int bf) {
-    if constexpr (QSIDE) sq.template store<LDQ>(Qbuf + bf * TQ, G::KIND == kFavor ? qnb[bf] : nullptr, threadIdx.x);
-    sk.template store<LDQ>(Kbuf + bf * TQ, G::KIND == kFavor ? knb[bf] : nullptr, threadIdx.x);
-    sv.template store<LDQ>(Vbuf + bf * TQ, nullptr, threadIdx.x);
+  auto store_q = [&](int bf) {
+    if constexpr (QSIDE) sq.template store<LDQ>(Qbuf, G::KIND == kFavor ? qnb[bf] : nullptr, fresh_tid());
+  };
+  auto store_kv = [&](int bf) {
+    const int tid = fresh_tid();
+    sk.template store<LDQ>(Kbuf + bf * TQ, G::KIND == kFavor ? knb[bf] : nullptr, tid);
+    sv.template store<LDQ>(Vbuf + bf * TQ, nullptr, tid);
   };
   if (j1 > j0) {
     fetch(j0);
-    store(0);
+    store_q(0);
+    store_kv(0);
     if (j0 + 1 < j1) fetch(j0 + 1);
   }
   __syncthreads();
@@ -182,19 +188,18 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
     int start, count;
     tm.tile(j, start, count);
     const int bf = (j - j0) & 1;
-    if (j + 1 < j1) {
-      store(bf ^ 1);
-      if (j + 2 < j1) fetch(j + 2);
-    }
-    const T* Qs = Qbuf + bf * TQ;
+    Lane L = fresh_lane();
+    int g = L.g, c = L.c;
+    if (j + 1 < j1) store_kv(bf ^ 1);
+    const T* Qs = Qbuf;
     const T* Ks = Kbuf + bf * TQ;
     const T* Vs = Vbuf + bf * TQ;
     const float* qn = qnb[bf];
     const float* kn = knb[bf];
 
     f32x4 Lq[QSIDE ? MT : 1][RT], Lk[RT][MT];
-    if constexpr (QSIDE) query_logits<G>(Lq, Wf, Qs, qn);
-    key_logits<G>(Lk, Wf, Ks, kn);
+    if constexpr (QSIDE) query_logits<G>(L, Lq, Wf, Qs, qn);
+    key_logits<G>(L, Lk, Wf, Ks, kn);
 
     if (G::KIND == kFavor) {
       if constexpr (QSIDE) {
@@ -219,12 +224,22 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
             for (int r = 0; r < 4; ++r)
               if (16 * st + 4 * g + r < count) v = fmaxf(v, Lk[st][mt][r]);
         v = wave_max(v);
-        if (lane_id() == 0) kmx[w] = v;
+        if ((fresh_tid() & 63) == 0) kmx[w] = v;
       }
     }
     // row maxima of all waves (and, with queries, the previous tile's
     // reduction reads are finished before N overwrites them)
-    if (QSIDE || (G::KIND == kFavor && !fixed)) __syncthreads();
+    if (QSIDE || (G::KIND == kFavor && !fixed)) {
+      __syncthreads();
+      L = fresh_lane();
+      g = L.g;
+      c = L.c;
+    }
+    // queries of the next tile: every wave has read this tile's
+    if (j + 1 < j1) {
+      store_q(bf ^ 1);
+      if (j + 2 < j1) fetch(j + 2);
+    }
 
     if (G::KIND == kFavor) {
       if (!fixed) {
@@ -281,14 +296,14 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int et = 0; et <= ET; ++et) vf[rb][et] = v_frag<G>(Vs, 32 * rb, et, count);
+      for (int et = 0; et <= ET; ++et) vf[rb][et] = v_frag<G>(L, Vs, 32 * rb, et, count);
 
     if constexpr (QSIDE) {
       // keys transposed into this wave's buffer: Zk[m][s]
 #pragma unroll
       for (int st = 0; st < RT; ++st)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
+        for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(L, Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
 
       F qf[MB][RT];
 #pragma unroll
@@ -308,7 +323,7 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
           if (st > tt) continue;
 #pragma unroll
           for (int kb = 0; kb < MB; ++kb)
-            At[st][tt] = mma(At[st][tt], frag_tr(Zk[w], LDZ, 32 * kb, 16 * st), qf[kb][tt]);
+            At[st][tt] = mma(At[st][tt], frag_tr(L, Zk[w], LDZ, 32 * kb, 16 * st), qf[kb][tt]);
           if (st == tt) {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
@@ -340,7 +355,7 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
 #pragma unroll
           for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sf[kb][et], qf[kb][tt]);
           if (et < ET) {
-            store_tile_T<float>(Red[w], LDR, acc, 16 * et, 16 * tt);
+            store_tile_T<float>(L, Red[w], LDR, acc, 16 * et, 16 * tt);
           } else if (g == 0) {
             Red[w][(16 * tt + c) * LDR + D] = acc[0];
           }
@@ -360,7 +375,8 @@ __global__ __launch_bounds__(256, MODE == kWalkSums ? 2 : 1) void fwd_walk_kerne
     if constexpr (QSIDE) {
       // Y = N / D over all features (vector reads of the reduction rows)
       static_assert(EPT % 4 == 0, "");
-      const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
+      const int tid = fresh_tid();
+      const int t = tid / TPR, q = tid % TPR;
       if (t < count) {
         const float inv = 1.f / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
         typedef T tvec __attribute__((ext_vector_type(EPT)));
@@ -424,7 +440,7 @@ __global__ __launch_bounds__(256, 1) void key_shift_kernel(FeatArgs a) {
     load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, kn);
     __syncthreads();
     f32x4 Lk[RT][MT];
-    key_logits<G>(Lk, Wf, Ks, kn);
+    key_logits<G>(this_lane(), Lk, Wf, Ks, kn);
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
@@ -461,7 +477,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
   const float half_log2M = 0.5f * __log2f((float)M);
   if (a.role == 0) {
     f32x4 Lq[MT][RT];
-    query_logits<G>(Lq, Wf, Xs, xn);
+    query_logits<G>(this_lane(), Lq, Wf, Xs, xn);
     if (G::KIND == kFavor) {
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
@@ -496,7 +512,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
     }
   } else {
     f32x4 Lk[RT][MT];
-    key_logits<G>(Lk, Wf, Xs, xn);
+    key_logits<G>(this_lane(), Lk, Wf, Xs, xn);
     const float ks = (G::KIND == kFavor) ? a.shift[head] : 0.f;
 #pragma unroll
     for (int st = 0; st < RT; ++st)
