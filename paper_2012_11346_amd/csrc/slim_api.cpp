@@ -131,6 +131,19 @@ int plan_sum_split(const slim_problem* p, int P) {
   return (n_tiles >= 4 * P && 2 * wgs <= kTargetWorkgroupsForward) ? 2 : 1;
 }
 
+// Row parts per segment of the carry pass (several segments): enough
+// workgroups to give two per compute unit, at least one tile per part.
+// SLIM_CARRY_SPLIT (debugging) forces a count from 1 to 4.
+int plan_carry_split(const slim_problem* p, int P) {
+  if (P < 2) return 1;
+  const int per_seg = count_tiles(p) / P;
+  const int64_t wgs = p->B * p->H * (int64_t)(P - 1);
+  const char* env = getenv("SLIM_CARRY_SPLIT");
+  int cs = (env != nullptr && atoi(env) >= 1 && atoi(env) <= 4) ? atoi(env)
+                                                                : (int)std::max<int64_t>(1, std::min<int64_t>(4, kTargetWorkgroupsForward / wgs));
+  return std::max(1, std::min(cs, per_seg));
+}
+
 size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
@@ -163,6 +176,10 @@ struct BwdLayout {
   size_t wfrag, seg_sum, bounds, gc, gend, dw_part, total;
 };
 size_t wfrag_bytes_of(const slim_problem* p);
+size_t dw_slots(const slim_problem* p, int P) {
+  const size_t heads = (size_t)p->B * p->H;
+  return heads * P + (P > 1 ? heads * (P - 1) * (plan_carry_split(p, P) - 1) : 0);
+}
 BwdLayout bwd_layout(const slim_problem* p, int P) {
   BwdLayout l{0, 0, 0, 0, 0, 0, 0};
   const size_t heads = (size_t)p->B * p->H;
@@ -181,8 +198,8 @@ BwdLayout bwd_layout(const slim_problem* p, int P) {
     l.gend = off;
     off += align256(heads * P * se);
   }
-  l.dw_part = off;
-  off += align256(heads * P * (size_t)p->M * p->d * sizeof(float));
+  l.dw_part = off;  // the walk's B H P partials, then the carry's extra row parts
+  off += align256(dw_slots(p, P) * (size_t)p->M * p->d * sizeof(float));
   l.total = off;
   return l;
 }
@@ -535,12 +552,13 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     ca.L = a.L;
     ca.C = a.C;
     ca.P = P;
+    ca.CS = plan_carry_split(p, P);
     ca.relu_eps = p->relu_eps;
     e = dp.carry(ca, s);
     if (e != hipSuccess) return hip_fail(e, "carry launch");
   }
   // (5) dW: the workgroups' partials summed in a fixed order
-  e = slim::launch_dw_reduce(a.dW_part, BH * P, (int)(p->M * p->d), dW, s);
+  e = slim::launch_dw_reduce(a.dW_part, (int)dw_slots(p, P), (int)(p->M * p->d), dW, s);
   if (e != hipSuccess) return hip_fail(e, "dW-reduction launch");
   return ok();
 }

@@ -2,6 +2,8 @@
 // feature-map kernels.
 #pragma once
 
+#include <climits>
+
 #include "slim_device.hpp"
 
 namespace slim {
@@ -42,14 +44,18 @@ struct Cfg {
 // a lane fetches it with one 16-byte (bf16) load.
 //   block A  [wave][mt][kb]: slot s = W[w FW + 16 mt + c][32 kb + kp(g, s)]   (contracting over d)
 //   block B  [wave][kb][et]: slot s = W[w FW + 32 kb + kp(g, s)][16 et + c]   (contracting over features)
+//   block C  [kb][et], after the waves' blocks: slot s = W[32 kb + kp(g, s)][16 et + c]
+//            (contracting over all M features)
 template <class G>
 struct WFragLayout {
   static constexpr int NA = G::MT * G::EB;  // fragments of block A per wave
   static constexpr int NB = G::MB * G::ET;  // fragments of block B per wave
   static constexpr int PER_WAVE = NA + NB;
-  static constexpr int TOTAL = 4 * PER_WAVE;  // fragments
+  static constexpr int NC = (G::M / 32) * G::ET;  // fragments of block C
+  static constexpr int TOTAL = 4 * PER_WAVE + NC;  // fragments
   __device__ static int a(int w, int mt, int kb) { return w * PER_WAVE + mt * G::EB + kb; }
   __device__ static int b(int w, int kb, int et) { return w * PER_WAVE + NA + kb * G::ET + et; }
+  __device__ static int c(int kb, int et) { return 4 * PER_WAVE + kb * G::ET + et; }
 };
 
 // Row range of tile j of a head, for slices of length C (already clamped to
@@ -112,6 +118,32 @@ __device__ __forceinline__ void load_rows(T* dst, const T* src, int count, float
 
 constexpr size_t al16(size_t n) { return (n + 15) & ~(size_t)15; }
 
+// Raw buffer resource over [base, base + bytes): the hardware's range check
+// makes loads past the end read zero and drops stores past the end, so
+// accesses to a ragged last row block need no branch (and the compiler can
+// count outstanding memory operations exactly).  bytes < 2^31.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t range_rsrc(const void* base, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// N bytes (8 or 16) at byte offset off of a range resource
+template <int N>
+struct BufIO {
+  static_assert(N == 8 || N == 16, "8- or 16-byte accesses");
+  typedef unsigned u32v __attribute__((ext_vector_type(N / 4)));
+  template <class V>
+  __device__ __forceinline__ static V load(__amdgpu_buffer_rsrc_t rs, int off) {
+    static_assert(sizeof(V) == N, "size");
+    if constexpr (N == 8) return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+    else return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+  }
+  template <class V>
+  __device__ __forceinline__ static void store(const V& v, __amdgpu_buffer_rsrc_t rs, int off) {
+    static_assert(sizeof(V) == N, "size");
+    if constexpr (N == 8) __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32v, v), rs, off, 0, 0);
+    else __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32v, v), rs, off, 0, 0);
+  }
+};
+
 // Register staging of a [count x D] row block (rows >= count read as zero)
 // by NT threads numbered tid = 0 .. NT-1: fetch() issues the global loads,
 // store() writes LDS (pitch LD) and optionally the squared row norms.
@@ -133,6 +165,18 @@ struct RowStage {
       const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
       v[i] = uint4{0u, 0u, 0u, 0u};
       if (ch < NCH && r < count) v[i] = *reinterpret_cast<const uint4*>(src + (size_t)r * D + cc * VEC);
+    }
+  }
+  // rows [row0, row0 + TR) of a range resource over whole rows; rows past
+  // its end read as zero
+  __device__ __forceinline__ void fetch(__amdgpu_buffer_rsrc_t rs, int row0, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int ch = tid + i * NT;
+      const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
+      // chunks past the block get an offset beyond any range
+      const int off = ch < NCH ? ((row0 + r) * D + cc * VEC) * (int)sizeof(T) : INT_MAX - 15;
+      v[i] = BufIO<16>::load<uint4>(rs, off);
     }
   }
   template <int LD>

@@ -542,7 +542,12 @@ __global__ __launch_bounds__(64) void wfrag_kernel(WfragArgs a) {
   const int w = f / WL::PER_WAVE;
   int i = f - w * WL::PER_WAVE;
   F v;
-  if (i < WL::NA) {
+  if (w >= 4) {
+    i = f - 4 * WL::PER_WAVE;
+    const int kb = i / G::ET, et = i - (i / G::ET) * G::ET;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) v[s] = cvt<T>(a.W[(size_t)(32 * kb + kp(g, s)) * G::D + 16 * et + c]);
+  } else if (i < WL::NA) {
     const int mt = i / G::EB, kb = i - (i / G::EB) * G::EB;
 #pragma unroll
     for (int s = 0; s < 8; ++s) v[s] = cvt<T>(a.W[(size_t)(w * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)]);

@@ -92,8 +92,9 @@ struct CarryArgs {
   const float* gend;    // [B,H,P,M,D+1] G_end(p)
   void* dK;             // in/out
   void* dV;             // in/out
-  float* dW_part;       // [B,H,P,M,D] in/out
+  float* dW_part;       // [B,H,P,M,D] in/out, then (CS-1) x [B,H,P-1,M,D] written
   int B, H, L, C, P;
+  int CS;  // workgroups (row parts) per segment
   float relu_eps;
 };
 
