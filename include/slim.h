@@ -67,7 +67,8 @@ typedef enum { SLIM_QUERY = 0, SLIM_KEY = 1 } slim_role;
 typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
 
 /* Problem description shared by all entry points.
- *   B, H, L  batch, heads, sequence length (each >= 1)
+ *   B, H, L  batch, heads, sequence length (each >= 1; B H <= 65535 and one
+ *            head's rows, L d elements, within 1 GiB, else SLIM_EUNSUPPORTED)
  *   d        head dimension: 32 or 64
  *   M        number of features: 64, 128 or 256
  *   C        slice length (Sec. 3.2): >= 1; values above L act as L.  The

@@ -70,6 +70,9 @@ int check_problem(const slim_problem* p) {
   if (p->M != 64 && p->M != 128 && p->M != 256)
     return fail(SLIM_EUNSUPPORTED, "feature count M=%d not supported (64, 128 or 256)", (int)p->M);
   if (p->L > (int64_t)INT_MAX / 2) return fail(SLIM_EUNSUPPORTED, "L=%lld too long", (long long)p->L);
+  // one head's rows are addressed with 32-bit byte offsets (range-checked buffer accesses)
+  if (p->L * p->d * (p->dtype == SLIM_F32 ? 4 : 2) > ((int64_t)1 << 30))
+    return fail(SLIM_EUNSUPPORTED, "L=%lld too long: one head's rows must fit in 1 GiB", (long long)p->L);
   if (p->B * p->H > 65535) return fail(SLIM_EUNSUPPORTED, "B*H=%lld too large", (long long)(p->B * p->H));
   if (p->B > 65535 || p->H > 65535) return fail(SLIM_EUNSUPPORTED, "B or H above 65535");
   if (p->kind == SLIM_RELU && !(p->relu_eps > 0.f)) return fail(SLIM_EINVAL, "relu_eps must be > 0");

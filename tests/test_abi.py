@@ -65,6 +65,8 @@ def test_workspace_is_flat_in_L(S):
         (dict(d=48), -2),
         (dict(M=96), -2),
         (dict(M=512), -2),
+        (dict(L=(1 << 23) + 1), -2),  # one bf16 head of d=64 rows above 1 GiB
+        (dict(B=300, H=300), -2),
     ],
 )
 def test_invalid_problems_are_rejected(S, kw, code):
