@@ -37,12 +37,18 @@ namespace slim {
 template <class G>
 struct Bwd8Lds {
   typedef typename G::T T;
-  static constexpr int D = G::D, FW = G::FW, TR = G::TR, ZR = G::ZR, LDQ = G::LDQ;
+  static constexpr int D = G::D, FW = G::FW, TR = G::TR, ZR = G::ZR;
   static constexpr int EH = G::ET / 2;          // value tiles per wave
-  static constexpr int LDZK = TR + 8;           // [feature][row] buffers (K~, Pk)
-  static constexpr int LDZF = FW + 8;           // [row or value column][feature] buffers (Q~, P, S, G)
-  static constexpr int LDZT = TR + 8;           // [row][row] buffers (A^T, dA^T)
-  static constexpr int LDRH = 16 * EH + 4;      // reduction row pitch (floats): own columns, then the ones column
+  // bf16 tiles are swizzled (SwzLane): rows padded by 16 elements
+  static constexpr int LDQ = D + 16;            // Q, K, V, dY / dN rows (kSwzRows)
+  static constexpr int LDZK = TR + 16;          // [feature][row] buffers (K~, Pk)
+  static constexpr int LDZF = FW + 16;          // [row or value column][feature] buffers (Q~, P, S, G)
+  static constexpr int LDZT = TR + 16;          // [row][row] buffers (A^T, dA^T)
+  static_assert(LDZT == LDZK, "A^T, dA^T share the lane offsets of K~");
+  static constexpr int LDRH = 16 * EH + 4;      // reduction row pitch (floats)
+  // floats between the reduction rows of the two value halves (d = 32: the
+  // offset keeps the halves of a row in different banks for 8-byte reads)
+  static constexpr int REDH = TR * LDRH + (D == 32 ? 16 : 0);
   // shared: Q, K, V, dY (dN overwrites dY), floats, dD as T
   static constexpr size_t TILE = al16((size_t)TR * LDQ * sizeof(T));
   static constexpr size_t oQ = 0, oK = TILE, oV = 2 * TILE, odY = 3 * TILE, oF = 4 * TILE;
@@ -57,10 +63,12 @@ struct Bwd8Lds {
   static constexpr size_t ZQ = al16((size_t)TR * LDZF * sizeof(T));
   static constexpr size_t ZDA = al16((size_t)TR * LDZT * sizeof(T));
   static constexpr size_t max3(size_t a, size_t b, size_t c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
-  static constexpr size_t RED = 2 * (size_t)TR * LDRH * sizeof(float);  // reduction rows of both waves
+  static constexpr size_t RED = 2 * (size_t)REDH * sizeof(float);  // reduction rows of both waves
+  static constexpr size_t REDZ = RED + (size_t)TR * sizeof(float);  // then the ones column of N
   static constexpr size_t ZSG = (size_t)D * LDZF * sizeof(T);
-  // Y: N / dV reduction rows, then P (as [t][m]), then G (as [e][m]), then dk reduction rows
-  static constexpr size_t ZY = al16(max3(RED, (size_t)TR * LDZF * sizeof(T), ZSG));
+  // Y: N / dV reduction rows (+ the ones column of N), then P (as [t][m]), then G (as [e][m]),
+  // then dk reduction rows
+  static constexpr size_t ZY = al16(max3(REDZ, (size_t)TR * LDZF * sizeof(T), ZSG));
   // X: A^T, then S (as [e][m]), then dq reduction rows, then Pk (as [m][s])
   static constexpr size_t ZX = al16(max3((size_t)TR * LDZT * sizeof(T), ZSG,
                                          RED > (size_t)ZR * LDZK * sizeof(T) ? RED : (size_t)ZR * LDZK * sizeof(T)));
@@ -76,8 +84,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   typedef Bwd8Lds<G> Lay;
   typedef WFragLayout<G> WL;
   constexpr int D = G::D, FW = G::FW, M = G::M, TR = G::TR, MT = G::MT, MB = G::MB, ET = G::ET, EB = G::EB,
-                RT = G::RT, LDQ = G::LDQ;
-  constexpr int EH = Lay::EH, LDZK = Lay::LDZK, LDZF = Lay::LDZF, LDZT = Lay::LDZT, LDRH = Lay::LDRH;
+                RT = G::RT;
+  constexpr int EH = Lay::EH, LDQ = Lay::LDQ, LDZK = Lay::LDZK, LDZF = Lay::LDZF, LDRH = Lay::LDRH,
+                REDH = Lay::REDH;
+  typedef SwzLane<LDQ, kSwzRows> OR;   // row tiles
+  typedef SwzLane<LDZK, kSwzInter> OK;  // K~, Pk, A^T, dA^T
+  typedef SwzLane<LDZF, kSwzInter> OF;  // Q~, P, S, G
   constexpr bool ODD = (MT & 1) != 0;  // last 32-deep feature block holds 16 features
   constexpr int NT = 512, TPR = NT / TR, EPT = D / TPR;
   static_assert(RT == 2 && G::RB == 1, "the two waves of a pair take one 16-row half of the tile each");
@@ -104,6 +116,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   // wave-uniform indices live in scalar registers
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), f = w & 3, h = w >> 2;
   const int g = lane_g(), c = lane_c(), lane = lane_id();
+  // per-lane offsets of the swizzled tiles; refreshed through an opaque copy
+  // at every phase so that addresses derived from them are formed per phase
+  OR oR(this_lane());
+  OK oK(this_lane());
+  OF oF(this_lane());
+  auto fresh_offsets = [&]() {
+    asm volatile("" : "+v"(oR.a), "+v"(oR.b), "+v"(oK.a), "+v"(oK.b), "+v"(oF.a), "+v"(oF.b));
+  };
   const bool zown = (h == 0);  // this wave carries the ones column
   char* pz = arena + Lay::oP + f * Lay::PAIR;
   T* Zk = (T*)(pz + Lay::pZk);     // K~ as [m][s]
@@ -112,29 +132,35 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   T* ZA = (T*)(pz + Lay::pX);      // A^T as [t][s]
   T* ZS = ZA;                                       // S as [e][m]
   T* ZPk = ZA;                                      // Pk as [m][s]
-  float* RedX = (float*)(pz + Lay::pX) + h * TR * LDRH;  // dq partial rows [t][e']
+  float* RedX = (float*)(pz + Lay::pX) + h * REDH;  // dq partial rows [t][e']
   T* ZP = (T*)(pz + Lay::pY);      // P as [t][m]
   T* ZG = ZP;                                       // G as [e][m]
-  float* RedY = (float*)(pz + Lay::pY) + h * TR * LDRH;  // N, dV, dk partial rows [t][e']
+  float* RedY = (float*)(pz + Lay::pY) + h * REDH;  // N, dV, dk partial rows [t][e']
+  float* RedYz = (float*)(pz + Lay::pY) + 2 * REDH;  // ones column of N [t]
+  // row of the reduction threads: the TPR = 16 threads of a row are 16
+  // consecutive lanes, and lanes 16 apart take rows 8 apart (their 16-byte
+  // reads of the reduction rows then fall into different banks)
+  static_assert(TPR == 16 && TR == 32, "reduction thread mapping");
+  auto red_row = [](int tid) -> int { return (tid >> 6) + 8 * ((tid >> 4) & 3); };
   // sums over the 4 slices of the EPT consecutive reduction entries
   // [t][col .. col + EPT) of value half hh (vector reads: one row of 16
   // threads covers all banks)
   typedef float fvec __attribute__((ext_vector_type(EPT)));
   static_assert((16 * EH) % EPT == 0 && (LDRH * 4) % 16 == 0, "");
   auto sum_x = [&](int hh, int idx) -> fvec {
-    const char* r = arena + Lay::oP + Lay::pX + (hh * TR * LDRH + idx) * 4;
+    const char* r = arena + Lay::oP + Lay::pX + (hh * REDH + idx) * 4;
     const fvec a0 = *(const fvec*)r, a1 = *(const fvec*)(r + Lay::PAIR);
     const fvec a2 = *(const fvec*)(r + 2 * Lay::PAIR), a3 = *(const fvec*)(r + 3 * Lay::PAIR);
     return (a0 + a1) + (a2 + a3);
   };
   auto sum_y = [&](int hh, int idx) -> fvec {
-    const char* r = arena + Lay::oP + Lay::pY + (hh * TR * LDRH + idx) * 4;
+    const char* r = arena + Lay::oP + Lay::pY + (hh * REDH + idx) * 4;
     const fvec a0 = *(const fvec*)r, a1 = *(const fvec*)(r + Lay::PAIR);
     const fvec a2 = *(const fvec*)(r + 2 * Lay::PAIR), a3 = *(const fvec*)(r + 3 * Lay::PAIR);
     return (a0 + a1) + (a2 + a3);
   };
-  auto sum_y1 = [&](int idx) -> float {
-    const float* r = (const float*)(arena + Lay::oP + Lay::pY) + idx;
+  auto sum_y1 = [&](int t) -> float {
+    const float* r = (const float*)(arena + Lay::oP + Lay::pY) + 2 * REDH + t;
     constexpr int S4 = Lay::PAIR / sizeof(float);
     return (r[0] + r[S4]) + (r[2 * S4] + r[3 * S4]);
   };
@@ -230,8 +256,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     tm.tile(j1 - 1, s0, n0);
     stA.fetch(srcA + (size_t)s0 * D, n0, stid);
     stB.fetch(srcB + (size_t)s0 * D, n0, stid);
-    stA.template store<LDQ>(dstA, nrmA, stid);
-    stB.template store<LDQ>(dstB, nrmB, stid);
+    stA.template store_swz<LDQ>(dstA, nrmA, stid);
+    stB.template store_swz<LDQ>(dstB, nrmB, stid);
     if (j1 - 1 > j0) {
       tm.tile(j1 - 2, s0, n0);
       stA.fetch(srcA + (size_t)s0 * D, n0, stid);
@@ -242,7 +268,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
   // [V|1] operand over the tile's 32 rows for value tile et (et == ET: ones)
   auto v_frag = [&](const Lane& L, int et, int count) -> F {
-    if (et < ET) return frag_tr(L, Vs, LDQ, 0, 16 * et);
+    if (et < ET) return sfrag_tr(oR, Vs, 0, 16 * et);
     F v;
     const int rem = count - 4 * L.g;  // rows kp(g, s) < count
 #pragma unroll
@@ -258,6 +284,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   for (int j = j1 - 1; j >= j0; --j) {
     Lane L = fresh_lane();
     int g = L.g, c = L.c;
+    fresh_offsets();
     int start, count;
     tm.tile(j, start, count);
 
@@ -277,7 +304,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int mt = 0; mt < MT; ++mt) {
           f32x4 acc = {init, init, init, init};
 #pragma unroll
-          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(L, Qs, LDQ, 16 * tt, 32 * kb));
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], sfrag_rm(oR, Qs, 16 * tt, 32 * kb));
           Lq[mt][tt] = acc;
         }
       }
@@ -288,13 +315,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 kv = kinit;
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, frag_rm(L, Ks, LDQ, 16 * h, 32 * kb), Wf[mt][kb]);
+        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, sfrag_rm(oR, Ks, 16 * h, 32 * kb), Wf[mt][kb]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool ok = 16 * h + 4 * g + r < count;
           kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : fmaxf(kv[r], 0.f) + a.relu_eps;
         }
-        store_tile_T<T>(L, Zk, LDZK, kv, 16 * h, 16 * mt);
+        sstore_tile_T(oK, Zk, kv, 16 * h, 16 * mt);
       }
       if (G::KIND == kFavor && zown) {
 #pragma unroll
@@ -313,6 +340,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair); the
     //      features stay in registers as operands of the scores and of N
@@ -328,7 +356,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
           Lq[mt][tt][r] = (t >= count) ? 0.f
                           : (G::KIND == kFavor) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs)
                                                 : fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
-        store_tile_T<T>(L, Zq, LDZF, Lq[mt][tt], 16 * mt, 16 * tt);
+        sstore_tile_T(oF, Zq, Lq[mt][tt], 16 * mt, 16 * tt);
       }
     }
     F qf[MB][RT];  // Q~ contracting over this slice's features, columns t
@@ -356,7 +384,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     } else {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        F kf = frag_rm(L, Zk, LDZK, 16 * mt, 0);  // K~ contracting over rows
+        F kf = sfrag_rm(oK, Zk, 16 * mt, 0);  // K~ contracting over rows
 #pragma unroll
         for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
 #pragma unroll
@@ -374,7 +402,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc = zero4();
         if (st <= tt) {
 #pragma unroll
-          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, frag_tr(L, Zk, LDZK, 32 * kb, 16 * st), qf[kb][tt]);
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sfrag_tr(oK, Zk, 32 * kb, 16 * st), qf[kb][tt]);
         }
         if (st == tt) {
 #pragma unroll
@@ -382,7 +410,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
             if (4 * g + r > c) acc[r] = 0.f;
         }
         At[st][tt] = acc;
-        store_tile_T<T>(L, ZA, LDZT, acc, 16 * st, 16 * tt);
+        sstore_tile_T(oK, ZA, acc, 16 * st, 16 * tt);
       }
     // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
 #pragma unroll
@@ -398,7 +426,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         if (el < EH) {
           store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * tt);
         } else if (g == 0) {
-          RedY[(16 * tt + c) * LDRH + 16 * EH] = acc[0];
+          RedYz[16 * tt + c] = acc[0];
         }
       }
     }
@@ -406,13 +434,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dN = dY / D, dD = -(dY . N) / D^2 per row (TPR threads per row)
     {
       const int tid = fresh_tid();
-      const int t = tid / TPR, q = tid % TPR;
+      const int t = red_row(tid), q = tid % TPR;
       const bool ok = t < count;
-      const float den = sum_y1(t * LDRH + 16 * EH);
+      const float den = sum_y1(t);
       const float inv = ok ? 1.f / den : 0.f;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
       const fvec n = sum_y(hh, t * LDRH + col);
@@ -420,13 +449,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       float dot = 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i) {
-        dy[i] = to_f32(dYs[t * LDQ + e + i]);
+        dy[i] = to_f32(dYs[swz_off<LDQ, kSwzRows>(t, e) + i]);
         dot += dy[i] * (n[i] * inv);
       }
 #pragma unroll
       for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * inv);
+      for (int i = 0; i < EPT; ++i) dNs[swz_off<LDQ, kSwzRows>(t, e) + i] = cvt<T>(dy[i] * inv);
       if (q == 0) {
         const float dd = ok ? -dot * inv : 0.f;
         dDs[t] = dd;
@@ -437,6 +466,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal, rows < count -> ZdA[t][s]
 #pragma unroll
@@ -447,35 +477,36 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc = f32x4{ddt, ddt, ddt, ddt};
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_rm(L, Vs, LDQ, 16 * st, 32 * kb), frag_rm(L, dNs, LDQ, 16 * tt, 32 * kb));
+          acc = mma(acc, sfrag_rm(oR, Vs, 16 * st, 32 * kb), sfrag_rm(oR, dNs, 16 * tt, 32 * kb));
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int sr = 16 * st + 4 * g + r;
           if ((st == tt && 4 * g + r > c) || sr >= count) acc[r] = 0.f;
         }
-        store_tile_T<T>(L, ZdA, LDZT, acc, 16 * st, 16 * tt);
+        sstore_tile_T(oK, ZdA, acc, 16 * st, 16 * tt);
       }
-      if (tt == 0) store_tile_T<T>(L, ZdA, LDZT, zero4(), 16, 0);  // s in [16, 32) for t in [0, 16)
+      if (tt == 0) sstore_tile_T(oK, ZdA, zero4(), 16, 0);  // s in [16, 32) for t in [0, 16)
     }
     // dV^T[e][s] = sum_m G[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t], own columns -> RedY[s][e']
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
       for (int el = 0; el < EH; ++el) {
-        f32x4 acc = mma(zero4(), frag_tr(L, dNs, LDQ, 0, 16 * (h * EH + el)), frag_tr(L, ZA, LDZT, 0, 16 * st));
+        f32x4 acc = mma(zero4(), sfrag_tr(oR, dNs, 0, 16 * (h * EH + el)), sfrag_tr(oK, ZA, 0, 16 * st));
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), frag_tr(L, Zk, LDZK, 32 * kb, 16 * st));
+        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), sfrag_tr(oK, Zk, 32 * kb, 16 * st));
         store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
       }
     __syncthreads();
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dV = sum over slices; S (own columns) -> ZS[e][m], z -> zs
     {
       const int tid = fresh_tid();
-      const int t = tid / TPR, q = tid % TPR;
+      const int t = red_row(tid), q = tid % TPR;
       if (t < count) {
         const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
         store_row(dVh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
@@ -484,7 +515,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-      for (int el = 0; el < EH; ++el) store_tile_T<T>(L, ZS, LDZF, S[mt][el], 16 * mt, e0 + 16 * el);
+      for (int el = 0; el < EH; ++el) sstore_tile_T(oF, ZS, S[mt][el], 16 * mt, e0 + 16 * el);
       if (zown && c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) zs[f * FW + 16 * mt + 4 * g + r] = Sz[mt][r];
@@ -494,6 +525,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dQ~^T[m][t] = sum_e S[m][e] dN[t][e] + z[m] dD[t] + sum_s K~[s][m] dA^T[s][t]
     //      for this wave's rows t in [16 h, 16 h + 16); P = dQ~ . Q~ (FAVOR+) or
@@ -508,15 +540,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int r = 0; r < 4; ++r) acc[r] = zs[f * FW + 16 * mt + 4 * g + r] * ddt;
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_tr(L, ZS, LDZF, 32 * kb, 16 * mt), frag_rm(L, dNs, LDQ, 16 * h, 32 * kb));
-        acc = mma(acc, frag_rm(L, Zk, LDZK, 16 * mt, 0), frag_rm(L, ZdA, LDZT, 16 * h, 0));
-        const f32x4 qv = load_tile_T(L, Zq, LDZF, 16 * mt, 16 * h);
+          acc = mma(acc, sfrag_tr(oF, ZS, 32 * kb, 16 * mt), sfrag_rm(oR, dNs, 16 * h, 32 * kb));
+        acc = mma(acc, sfrag_rm(oK, Zk, 16 * mt, 0), sfrag_rm(oK, ZdA, 16 * h, 0));
+        const f32x4 qv = sload_tile_T(oF, Zq, 16 * mt, 16 * h);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
           rs += acc[r];
         }
-        store_tile_T<T>(L, ZP, LDZF, acc, 16 * mt, 16 * h);
+        sstore_tile_T(oF, ZP, acc, 16 * mt, 16 * h);
       }
       if (G::KIND == kFavor) {
         rs = wave_sum_over_g(rs);
@@ -527,6 +559,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] - q[t][e] rowsum_f(P)[t], own columns -> RedX[t][e'];
     //      dW[m][e] += sum_t P[t][m] Q[t][e]
@@ -539,31 +572,32 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc;
         if (G::KIND == kFavor) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Qs[(16 * tt + c) * LDQ + 16 * et + 4 * g + r]) * rsv;
+          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Qs[oR.a + 16 * tt * LDQ + 16 * et + r]) * rsv;
         } else {
           acc = zero4();
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_rm(L, ZP, LDZF, 16 * tt, 32 * kb));
+          acc = mma(acc, wfrag(WL::b(f, kb, et)), sfrag_rm(oF, ZP, 16 * tt, 32 * kb));
         store_tile_T<float>(L, RedX, LDRH, acc, 16 * el, 16 * tt);
       }
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F pf = frag_tr(L, ZP, LDZF, 0, 16 * mt);
+      const F pf = sfrag_tr(oF, ZP, 0, 16 * mt);
 #pragma unroll
-      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(L, Qs, LDQ, 0, e0 + 16 * el));
+      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, sfrag_tr(oR, Qs, 0, e0 + 16 * el));
     }
     __syncthreads();
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dq = sum over slices; G (own columns) -> ZG[e][m], dz -> dzs
     {
       const int tid = fresh_tid();
-      const int t = tid / TPR, q = tid % TPR;
+      const int t = red_row(tid), q = tid % TPR;
       if (t < count) {
         const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
         store_row(dQh + (size_t)(start + t) * D + e, sum_x(hh, t * LDRH + col));
@@ -572,7 +606,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-      for (int el = 0; el < EH; ++el) store_tile_T<T>(L, ZG, LDZF, Gs[mt][el], 16 * mt, e0 + 16 * el);
+      for (int el = 0; el < EH; ++el) sstore_tile_T(oF, ZG, Gs[mt][el], 16 * mt, e0 + 16 * el);
       if (zown && c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) dzs[f * FW + 16 * mt + 4 * g + r] = Gz[mt][r];
@@ -582,6 +616,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dK~[s][m] = sum_e V[s][e] G[m][e] + dz[m] + sum_t dA^T[s][t] Q~[t][m] for this
     //      wave's rows s in [16 h, 16 h + 16); Pk = dK~ . K~ (FAVOR+) or masked (ReLU)
@@ -596,15 +631,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int r = 0; r < 4; ++r) acc[r] = (16 * h + 4 * g + r < count) ? dz : 0.f;
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, frag_rm(L, Vs, LDQ, 16 * h, 32 * kb), frag_tr(L, ZG, LDZF, 32 * kb, 16 * mt));
-        acc = mma(acc, frag_tr(L, ZdA, LDZT, 0, 16 * h), frag_tr(L, Zq, LDZF, 0, 16 * mt));
-        const f32x4 kv = load_tile_T(L, Zk, LDZK, 16 * h, 16 * mt);
+          acc = mma(acc, sfrag_rm(oR, Vs, 16 * h, 32 * kb), sfrag_tr(oF, ZG, 32 * kb, 16 * mt));
+        acc = mma(acc, sfrag_tr(oK, ZdA, 0, 16 * h), sfrag_tr(oF, Zq, 0, 16 * mt));
+        const f32x4 kv = sload_tile_T(oK, Zk, 16 * h, 16 * mt);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
           rk[r] += acc[r];
         }
-        store_tile_T<T>(L, ZPk, LDZK, acc, 16 * h, 16 * mt);
+        sstore_tile_T(oK, ZPk, acc, 16 * h, 16 * mt);
       }
       if (G::KIND == kFavor) {
 #pragma unroll
@@ -617,9 +652,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F qf = frag_tr(L, Zq, LDZF, 0, 16 * mt);
+      const F qf = sfrag_tr(oF, Zq, 0, 16 * mt);
 #pragma unroll
-      for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, frag_tr(L, dNs, LDQ, 0, e0 + 16 * el));
+      for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, sfrag_tr(oR, dNs, 0, e0 + 16 * el));
       if (zown) {
         F dd;
 #pragma unroll
@@ -631,14 +666,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dW[m][e] += sum_s Pk[s][m] K[s][e]; dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum_f(Pk)[s]
     //      own columns -> RedY[s][e']
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const F pf = frag_rm(L, ZPk, LDZK, 16 * mt, 0);
+      const F pf = sfrag_rm(oK, ZPk, 16 * mt, 0);
 #pragma unroll
-      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, frag_tr(L, Ks, LDQ, 0, e0 + 16 * el));
+      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, sfrag_tr(oR, Ks, 0, e0 + 16 * el));
     }
 #pragma unroll
     for (int st = 0; st < RT; ++st) {
@@ -649,13 +685,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc;
         if (G::KIND == kFavor) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Ks[(16 * st + c) * LDQ + 16 * et + 4 * g + r]) * rsv;
+          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Ks[oR.a + 16 * st * LDQ + 16 * et + r]) * rsv;
         } else {
           acc = zero4();
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, wfrag(WL::b(f, kb, et)), frag_tr(L, ZPk, LDZK, 32 * kb, 16 * st));
+          acc = mma(acc, wfrag(WL::b(f, kb, et)), sfrag_tr(oK, ZPk, 32 * kb, 16 * st));
         store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
       }
     }
@@ -663,11 +699,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
 
     // ---- dk = sum over slices; rows of the next tile -> LDS (their readers are done)
     {
       const int tid = fresh_tid();
-      const int t = tid / TPR, q = tid % TPR;
+      const int t = red_row(tid), q = tid % TPR;
       if (t < count) {
         const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
         store_row(dKh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
@@ -675,8 +712,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     }
     if (j > j0) {
       const int st2 = fresh_tid() & 255;
-      stA.template store<LDQ>(dstA, nrmA, st2);
-      stB.template store<LDQ>(dstB, nrmB, st2);
+      stA.template store_swz<LDQ>(dstA, nrmA, st2);
+      stB.template store_swz<LDQ>(dstB, nrmB, st2);
       if (j - 1 > j0) {
         int sn, cn;
         tm.tile(j - 2, sn, cn);
@@ -688,6 +725,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     L = fresh_lane();
     g = L.g;
     c = L.c;
+    fresh_offsets();
   }
 
   // per-workgroup dW partial: this wave's rows and columns

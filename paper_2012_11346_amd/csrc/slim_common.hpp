@@ -179,6 +179,30 @@ struct RowStage {
       v[i] = BufIO<16>::load<uint4>(rs, off);
     }
   }
+  // into a row tile swizzled as kSwzRows (pitch LD): chunk cc of row r goes
+  // to chunk cc ^ sw(r) / 2
+  template <int LD>
+  __device__ __forceinline__ void store_swz(T* dst, float* norms, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int ch = tid + i * NT;
+      const bool active = ch < NCH;
+      const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
+      if (active) *reinterpret_cast<uint4*>(dst + r * LD + VEC * (cc ^ ((r >> 3) & 1))) = v[i];
+      if (norms != nullptr) {
+        float s = 0.f;
+        const T* e = reinterpret_cast<const T*>(&v[i]);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+          const float x = to_f32(e[k]);
+          s += x * x;
+        }
+#pragma unroll
+        for (int o = 1; o < CPR; o <<= 1) s += __shfl_xor(s, o, 64);
+        if (active && cc == 0) norms[r] = s;
+      }
+    }
+  }
   template <int LD>
   __device__ __forceinline__ void store(T* dst, float* norms, int tid) const {
 #pragma unroll

@@ -275,4 +275,95 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// ------------------------------------------------------------- swizzled LDS tiles
+//
+// LDS of gfx950 serves reads from 64 four-byte banks (256 B per clock) and
+// writes from 32 banks (128 B per clock).  A bf16 tile whose rows are read
+// both as fragments (frag_rm: row c, k = 4g..) and transposed (frag_tr: rows
+// 4g + c/4) and written by store_tile_T (row c, columns 4g..) cannot be
+// conflict-free for all three patterns by padding alone.  The swizzled tile
+// pads each row by 16 elements and XORs the 8-byte granule index (4 bf16)
+// with a value sw(r) in [0, 4) taken from row bits 2..3:
+//
+//   element (r, e)  at  r * P + 4 * ((e >> 2) ^ sw(r)) + (e & 3),  P = row length + 16
+//
+// Row tiles staged from global memory in 16-byte chunks use sw(r) in {0, 2}
+// (bit 3 of r), which keeps every chunk contiguous.  sw depends on r mod 16
+// only and touches only the low two granule bits, so an access to rows
+// starting at a multiple of 16 and columns starting at a multiple of 16 is a
+// per-lane offset (SwzLane) plus a compile-time offset.
+enum SwzMode { kSwzInter = 0, kSwzRows = 1 };
+
+template <int MODE>
+__device__ __forceinline__ int swz(int r) {
+  return MODE == kSwzInter ? ((r >> 2) & 3) : (((r >> 3) & 1) << 1);
+}
+
+// per-lane element offsets of the three access patterns of a swizzled tile
+template <int P, int MODE>
+struct SwzLane {
+  int a;  // row c, granule g (frag_rm, store_tile_T, load_tile_T)
+  int b;  // row 4g + c/4, granule c % 4 (frag_tr)
+  __device__ __forceinline__ explicit SwzLane(const Lane& L) {
+    a = L.c * P + 4 * (L.g ^ swz<MODE>(L.c));
+    const int r = 4 * L.g + (L.c >> 2);
+    b = r * P + 4 * ((L.c & 3) ^ swz<MODE>(r));
+  }
+};
+
+// element offset of (r, e) in a swizzled tile
+template <int P, int MODE>
+__device__ __forceinline__ int swz_off(int r, int e) {
+  return r * P + 4 * ((e >> 2) ^ swz<MODE>(r)) + (e & 3);
+}
+
+// fragment slot s = Z[row0 + c][k0 + kp(g, s)]   (row0, k0 multiples of 16)
+template <int P, int MODE>
+__device__ __forceinline__ bf16x8 sfrag_rm(const SwzLane<P, MODE>& o, const bf16* Z, int row0, int k0) {
+  const bf16* p = Z + o.a + row0 * P + k0;
+  bf16x8 f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = p[r];
+    f[4 + r] = p[16 + r];
+  }
+  return f;
+}
+
+// fragment slot s = Z[k0 + kp(g, s)][col0 + c]   (k0, col0 multiples of 16)
+template <int P, int MODE>
+__device__ __forceinline__ bf16x8 sfrag_tr(const SwzLane<P, MODE>& o, const bf16* Z, int k0, int col0) {
+  typedef SLIM_LDS i16x4 lds_i16x4;
+  const bf16* p0 = Z + o.b + k0 * P + col0;
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 16 * P));
+  const bf16x4 av = __builtin_bit_cast(bf16x4, a), bv = __builtin_bit_cast(bf16x4, b);
+  bf16x8 f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = av[r];
+    f[4 + r] = bv[r];
+  }
+  return f;
+}
+
+// result tile X[row0 + 4g + r][col0 + c] stored transposed: Z[col0 + c][row0 + 4g + r]
+template <int P, int MODE>
+__device__ __forceinline__ void sstore_tile_T(const SwzLane<P, MODE>& o, bf16* Z, const f32x4& x, int row0, int col0) {
+  bf16x4 v;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) v[r] = (bf16)x[r];
+  *(bf16x4*)(Z + o.a + col0 * P + row0) = v;
+}
+
+// X[row0 + 4g + r][col0 + c] of a tile stored transposed by sstore_tile_T
+template <int P, int MODE>
+__device__ __forceinline__ f32x4 sload_tile_T(const SwzLane<P, MODE>& o, const bf16* Z, int row0, int col0) {
+  const bf16x4 v = *(const bf16x4*)(Z + o.a + col0 * P + row0);
+  f32x4 x;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) x[r] = (float)v[r];
+  return x;
+}
+
 }  // namespace slim
