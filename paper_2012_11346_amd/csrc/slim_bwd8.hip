@@ -258,11 +258,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     stB.fetch(srcB + (size_t)s0 * D, n0, stid);
     stA.template store_swz<LDQ>(dstA, nrmA, stid);
     stB.template store_swz<LDQ>(dstB, nrmB, stid);
-    if (j1 - 1 > j0) {
-      tm.tile(j1 - 2, s0, n0);
-      stA.fetch(srcA + (size_t)s0 * D, n0, stid);
-      stB.fetch(srcB + (size_t)s0 * D, n0, stid);
-    }
   }
   __syncthreads();
 
@@ -297,6 +292,18 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = wfrag(WL::a(f, mt, kb));
+      // rows of the next tile, stored into LDS at the end of this one; issued
+      // after the W fragments so that waiting for those does not wait for
+      // these.  Range-checked loads without branches (an empty range after
+      // the last tile) keep the count of outstanding loads exact.
+      {
+        const int st2 = fresh_tid() & 255;
+        int sn, cn;
+        tm.tile(j > j0 ? j - 1 : j, sn, cn);
+        const size_t nb = j > j0 ? (size_t)cn * D * sizeof(T) : 0;
+        stA.fetch(range_rsrc(srcA + (size_t)sn * D, nb), 0, st2);
+        stB.fetch(range_rsrc(srcB + (size_t)sn * D, nb), 0, st2);
+      }
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
         const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
@@ -563,6 +570,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
     // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] - q[t][e] rowsum_f(P)[t], own columns -> RedX[t][e'];
     //      dW[m][e] += sum_t P[t][m] Q[t][e]
+    {
+      // the W fragments of this product, fetched together (once per tile)
+      F Wb[MB][EH];
+#pragma unroll
+      for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+        for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
       const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * tt + c] : 0.f;
@@ -578,9 +592,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, wfrag(WL::b(f, kb, et)), sfrag_rm(oF, ZP, 16 * tt, 32 * kb));
+          acc = mma(acc, Wb[kb][el], sfrag_rm(oF, ZP, 16 * tt, 32 * kb));
         store_tile_T<float>(L, RedX, LDRH, acc, 16 * el, 16 * tt);
       }
+    }
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -676,6 +691,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
       for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, sfrag_tr(oR, Ks, 0, e0 + 16 * el));
     }
+    {
+      F Wb[MB][EH];
+#pragma unroll
+      for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+        for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
 #pragma unroll
     for (int st = 0; st < RT; ++st) {
       const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * st + c] : 0.f;
@@ -691,9 +712,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, wfrag(WL::b(f, kb, et)), sfrag_tr(oK, ZPk, 32 * kb, 16 * st));
+          acc = mma(acc, Wb[kb][el], sfrag_tr(oK, ZPk, 32 * kb, 16 * st));
         store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
       }
+    }
     }
     __syncthreads();
     L = fresh_lane();
@@ -714,12 +736,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const int st2 = fresh_tid() & 255;
       stA.template store_swz<LDQ>(dstA, nrmA, st2);
       stB.template store_swz<LDQ>(dstB, nrmB, st2);
-      if (j - 1 > j0) {
-        int sn, cn;
-        tm.tile(j - 2, sn, cn);
-        stA.fetch(srcA + (size_t)sn * D, cn, st2);
-        stB.fetch(srcB + (size_t)sn * D, cn, st2);
-      }
     }
     __syncthreads();
     L = fresh_lane();
