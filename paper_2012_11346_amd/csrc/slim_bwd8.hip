@@ -164,14 +164,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     constexpr int S4 = Lay::PAIR / sizeof(float);
     return (r[0] + r[S4]) + (r[2 * S4] + r[3 * S4]);
   };
-  // EPT consecutive values of row t of a [.][D] output, as one store
-  auto store_row = [&](T* dst, const fvec& v) {
-    typedef T tvec __attribute__((ext_vector_type(EPT)));
-    tvec o;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) o[i] = cvt<T>(v[i]);
-    *(tvec*)dst = o;
-  };
 
   const int p = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
   const size_t head = (size_t)b * a.H + hd;
@@ -276,12 +268,35 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     return tile_pair_frag<T>(el < EH ? X[2 * kb][el] : Xz[2 * kb], el < EH ? X[2 * kb + 1][el] : Xz[2 * kb + 1]);
   };
 
+  // Output rows are written with range-checked stores (rows past the tile
+  // are dropped, no branches) and after the waits for this wave's W
+  // fragments in program order: on gfx9 a wait for a load also waits for
+  // every earlier store.  dV is held from its reduction to the dq store; dk
+  // of a tile is stored in the next tile after its logits.
+  typedef T tvec __attribute__((ext_vector_type(EPT)));
+  typedef unsigned u32e __attribute__((ext_vector_type(EPT / 2)));
+  static_assert(EPT == 2 || EPT == 4, "8- or 4-byte row pieces");
+  auto cvt_row = [&](const fvec& v) -> u32e {
+    tvec o;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) o[i] = cvt<T>(v[i]);
+    return __builtin_bit_cast(u32e, o);
+  };
+  auto store_piece = [&](const u32e& v, __amdgpu_buffer_rsrc_t rs, int off) {
+    if constexpr (EPT == 4) __builtin_amdgcn_raw_buffer_store_b64(v, rs, off, 0, 0);
+    else __builtin_amdgcn_raw_buffer_store_b32(v[0], rs, off, 0, 0);
+  };
+  u32e dk_hold = {};
+  __amdgpu_buffer_rsrc_t dk_rs = range_rsrc(dKh, 0);
+  int dk_off = 0;
   for (int j = j1 - 1; j >= j0; --j) {
     Lane L = fresh_lane();
     int g = L.g, c = L.c;
     fresh_offsets();
     int start, count;
     tm.tile(j, start, count);
+    u32e dv_hold;
+    F Wb[MB][EH];  // W fragments of the dq and dk products
 
     // ---- features: Q logits of the whole tile (both waves of the pair), K
     //      logits of this wave's 16 rows; K~ -> Zk[m][s]
@@ -348,6 +363,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     g = L.g;
     c = L.c;
     fresh_offsets();
+
+    // dk of the previous tile (an empty range before the first)
+    store_piece(dk_hold, dk_rs, dk_off);
 
     // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair); the
     //      features stay in registers as operands of the scores and of N
@@ -510,14 +528,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dV = sum over slices; S (own columns) -> ZS[e][m], z -> zs
+    // ---- dV = sum over slices (held); S (own columns) -> ZS[e][m], z -> zs
     {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
-      if (t < count) {
-        const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
-        store_row(dVh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
-      }
+      const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+      dv_hold = cvt_row(sum_y(hh, t * LDRH + col));
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -571,8 +587,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] - q[t][e] rowsum_f(P)[t], own columns -> RedX[t][e'];
     //      dW[m][e] += sum_t P[t][m] Q[t][e]
     {
-      // the W fragments of this product, fetched together (once per tile)
-      F Wb[MB][EH];
+      // the W fragments of the dq and dk products, fetched together
 #pragma unroll
       for (int kb = 0; kb < MB; ++kb)
 #pragma unroll
@@ -613,10 +628,11 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
-      if (t < count) {
-        const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
-        store_row(dQh + (size_t)(start + t) * D + e, sum_x(hh, t * LDRH + col));
-      }
+      const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+      const int off = (t * D + e) * (int)sizeof(T);
+      const size_t nb = (size_t)count * D * sizeof(T);
+      store_piece(cvt_row(sum_x(hh, t * LDRH + col)), range_rsrc(dQh + (size_t)start * D, nb), off);
+      store_piece(dv_hold, range_rsrc(dVh + (size_t)start * D, nb), off);
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -692,11 +708,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, sfrag_tr(oR, Ks, 0, e0 + 16 * el));
     }
     {
-      F Wb[MB][EH];
-#pragma unroll
-      for (int kb = 0; kb < MB; ++kb)
-#pragma unroll
-        for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
 #pragma unroll
     for (int st = 0; st < RT; ++st) {
       const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * st + c] : 0.f;
@@ -723,14 +734,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dk = sum over slices; rows of the next tile -> LDS (their readers are done)
+    // ---- dk = sum over slices (held); rows of the next tile -> LDS (their readers are done)
     {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
-      if (t < count) {
-        const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
-        store_row(dKh + (size_t)(start + t) * D + e, sum_y(hh, t * LDRH + col));
-      }
+      const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
+      dk_hold = cvt_row(sum_y(hh, t * LDRH + col));
+      dk_rs = range_rsrc(dKh + (size_t)start * D, (size_t)count * D * sizeof(T));
+      dk_off = (t * D + e) * (int)sizeof(T);
     }
     if (j > j0) {
       const int st2 = fresh_tid() & 255;
@@ -743,6 +754,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
   }
+
+  store_piece(dk_hold, dk_rs, dk_off);
 
   // per-workgroup dW partial: this wave's rows and columns
   float* dwp = a.dW_part + (head * a.P + p) * (size_t)M * D;
