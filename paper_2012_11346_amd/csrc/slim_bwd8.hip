@@ -239,7 +239,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const T* srcB = sh ? dYh : Kh;
   T* dstA = sh ? Vs : Qs;
   T* dstB = sh ? dYs : Ks;
-  float* nrmA = (G::KIND == kFavor && !sh) ? qn : nullptr;
+  // (the query norm cancels against the query row shift: only key norms are kept)
+  float* nrmA = nullptr;
   float* nrmB = (G::KIND == kFavor && !sh) ? kn : nullptr;
   RowStage<T, D, TR, 256> stA, stB;
   __syncthreads();  // zero fill done
@@ -319,29 +320,30 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         stA.fetch(range_rsrc(srcA + (size_t)sn * D, nb), 0, st2);
         stB.fetch(range_rsrc(srcB + (size_t)sn * D, nb), 0, st2);
       }
+      // raw logits w.q: the query row shift max_m(w.q - |q|^2/2) absorbs the norm term
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
-        const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          f32x4 acc = {init, init, init, init};
+          f32x4 acc = zero4();
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], sfrag_rm(oR, Qs, 16 * tt, 32 * kb));
           Lq[mt][tt] = acc;
         }
       }
-      f32x4 kinit;
+      // key rows: exp2(log2e (w.k - |k|^2/2 - shift) - log2(M)/2), the row term folded into the exponent
+      float kc[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) kinit[r] = (G::KIND == kFavor) ? -0.5f * kn[16 * h + 4 * g + r] : 0.f;
+      for (int r = 0; r < 4; ++r) kc[r] = (G::KIND == kFavor) ? koff + 0.5f * kLog2e * kn[16 * h + 4 * g + r] : 0.f;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        f32x4 kv = kinit;
+        f32x4 kv = zero4();
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb) kv = mma(kv, sfrag_rm(oR, Ks, 16 * h, 32 * kb), Wf[mt][kb]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool ok = 16 * h + 4 * g + r < count;
-          kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : fmaxf(kv[r], 0.f) + a.relu_eps;
+          kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - kc[r]) : fmaxf(kv[r], 0.f) + a.relu_eps;
         }
         sstore_tile_T(oK, Zk, kv, 16 * h, 16 * mt);
       }
@@ -368,7 +370,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     store_piece(dk_hold, dk_rs, dk_off);
 
     // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair); the
-    //      features stay in registers as operands of the scores and of N
+    //      features stay in registers as operands of the scores and of N.
+    //      Rows past the tile (zero in LDS) get finite features and need no
+    //      mask: their dN, dD are zero, so they add nothing to G, dA, P or dW.
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
       const int t = 16 * tt + c;
@@ -378,9 +382,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          Lq[mt][tt][r] = (t >= count) ? 0.f
-                          : (G::KIND == kFavor) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs)
-                                                : fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
+          Lq[mt][tt][r] = (G::KIND == kFavor) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs)
+                                              : fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
         sstore_tile_T(oF, Zq, Lq[mt][tt], 16 * mt, 16 * tt);
       }
     }
@@ -493,7 +496,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal, rows < count -> ZdA[t][s]
+    // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal -> ZdA[t][s]; a row s
+    //      past the tile has V[s] = 0 and is reached only from rows t >= s, whose dD is zero
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
       const float ddt = dDs[16 * tt + c];
@@ -505,8 +509,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
           acc = mma(acc, sfrag_rm(oR, Vs, 16 * st, 32 * kb), sfrag_rm(oR, dNs, 16 * tt, 32 * kb));
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int sr = 16 * st + 4 * g + r;
-          if ((st == tt && 4 * g + r > c) || sr >= count) acc[r] = 0.f;
+          if (st == tt && 4 * g + r > c) acc[r] = 0.f;
         }
         sstore_tile_T(oK, ZdA, acc, 16 * st, 16 * tt);
       }
@@ -552,10 +555,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
     // ---- dQ~^T[m][t] = sum_e S[m][e] dN[t][e] + z[m] dD[t] + sum_s K~[s][m] dA^T[s][t]
     //      for this wave's rows t in [16 h, 16 h + 16); P = dQ~ . Q~ (FAVOR+) or
-    //      dQ~ masked (ReLU) -> ZP[t][m]; row sums of P over the slice -> rsum
+    //      dQ~ masked (ReLU) -> ZP[t][m]
     {
       const float ddt = dDs[16 * h + c];
-      float rs = 0.f;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 acc;
@@ -567,15 +569,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         acc = mma(acc, sfrag_rm(oK, Zk, 16 * mt, 0), sfrag_rm(oK, ZdA, 16 * h, 0));
         const f32x4 qv = sload_tile_T(oF, Zq, 16 * mt, 16 * h);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
+        for (int r = 0; r < 4; ++r)
           acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
-          rs += acc[r];
-        }
         sstore_tile_T(oF, ZP, acc, 16 * mt, 16 * h);
-      }
-      if (G::KIND == kFavor) {
-        rs = wave_sum_over_g(rs);
-        if (g == 0) rsum[f * TR + 16 * h + c] = rs;
       }
     }
     __syncthreads();
@@ -584,8 +580,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] - q[t][e] rowsum_f(P)[t], own columns -> RedX[t][e'];
-    //      dW[m][e] += sum_t P[t][m] Q[t][e]
+    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m], own columns -> RedX[t][e'];
+    //      dW[m][e] += sum_t P[t][m] Q[t][e].  The FAVOR+ chain rule also has
+    //      -q[t] sum_m P[t][m], which is zero: Y is homogeneous of degree 0 in
+    //      each query feature vector, so sum_m Q~[t][m] dQ~[t][m] = 0.
     {
       // the W fragments of the dq and dk products, fetched together
 #pragma unroll
@@ -594,17 +592,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
-      const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * tt + c] : 0.f;
 #pragma unroll
       for (int el = 0; el < EH; ++el) {
-        const int et = h * EH + el;
-        f32x4 acc;
-        if (G::KIND == kFavor) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Qs[oR.a + 16 * tt * LDQ + 16 * et + r]) * rsv;
-        } else {
-          acc = zero4();
-        }
+        f32x4 acc = zero4();
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
           acc = mma(acc, Wb[kb][el], sfrag_rm(oF, ZP, 16 * tt, 32 * kb));
