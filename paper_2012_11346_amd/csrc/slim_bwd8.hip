@@ -124,7 +124,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   auto fresh_offsets = [&]() {
     asm volatile("" : "+v"(oR.a), "+v"(oR.b), "+v"(oK.a), "+v"(oK.b), "+v"(oF.a), "+v"(oF.b));
   };
-  const bool zown = (h == 0);  // this wave carries the ones column
+  // Both waves of a pair carry the ones column (z = sum K~ and its
+  // cotangent) with identical arithmetic, so they hold identical values and
+  // need no branches; only wave h = 0 writes it out.
+  const bool zown = (h == 0);
   char* pz = arena + Lay::oP + f * Lay::PAIR;
   T* Zk = (T*)(pz + Lay::pZk);     // K~ as [m][s]
   T* Zq = (T*)(pz + Lay::pZq);     // Q~ as [t][m]
@@ -210,8 +213,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         S[mt][et][r] = bend[row + e0 + 16 * et + c];
         Gs[mt][et][r] = g0 ? g0[row + e0 + 16 * et + c] : 0.f;
       }
-      Sz[mt][r] = zown ? bend[row + D] : 0.f;
-      Gz[mt][r] = (zown && g0) ? g0[row + D] : 0.f;
+      Sz[mt][r] = bend[row + D];
+      Gz[mt][r] = g0 ? g0[row + D] : 0.f;
     }
 #pragma unroll
     for (int et = 0; et < EH; ++et) dWacc[mt][et] = zero4();
@@ -254,9 +257,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   }
   __syncthreads();
 
-  // [V|1] operand over the tile's 32 rows for value tile et (et == ET: ones)
-  auto v_frag = [&](const Lane& L, int et, int count) -> F {
-    if (et < ET) return sfrag_tr(oR, Vs, 0, 16 * et);
+  // V operand over the tile's 32 rows, value columns [col, col + 16)
+  auto v_frag = [&](int col) -> F { return sfrag_tr(oR, Vs, 0, col); };
+  // the ones column of [V|1] over the tile's rows (zero past the tile)
+  auto ones_frag = [&](const Lane& L, int count) -> F {
     F v;
     const int rem = count - 4 * L.g;  // rows kp(g, s) < count
 #pragma unroll
@@ -347,7 +351,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
         sstore_tile_T(oK, Zk, kv, 16 * h, 16 * mt);
       }
-      if (G::KIND == kFavor && zown) {
+      if (G::KIND == kFavor) {
 #pragma unroll
         for (int tt = 0; tt < RT; ++tt) {
           float v = -INFINITY;
@@ -407,17 +411,18 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
           const float* row = bs + lo + (16 * mt + r) * (D + 1);
 #pragma unroll
           for (int et = 0; et < EH; ++et) S[mt][et][r] = row[16 * et];
-          if (zown) Sz[mt][r] = row[D - e0 - c];
+          Sz[mt][r] = row[D - e0 - c];
         }
     } else {
+      const F ones = ones_frag(L, count);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         F kf = sfrag_rm(oK, Zk, 16 * mt, 0);  // K~ contracting over rows
 #pragma unroll
         for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
 #pragma unroll
-        for (int et = 0; et < EH; ++et) S[mt][et] = mma(S[mt][et], kf, v_frag(L, h * EH + et, count));
-        if (zown) Sz[mt] = mma(Sz[mt], kf, v_frag(L, ET, count));
+        for (int el = 0; el < EH; ++el) S[mt][el] = mma(S[mt][el], kf, v_frag(e0 + 16 * el));
+        Sz[mt] = mma(Sz[mt], kf, ones);
       }
     }
 
@@ -446,9 +451,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const F af = tile_pair_frag<T>(At[0][tt], At[1][tt]);  // A^T contracting over rows s
 #pragma unroll
       for (int el = 0; el <= EH; ++el) {
-        if (el == EH && !zown) continue;
-        const int et = (el < EH) ? h * EH + el : ET;
-        f32x4 acc = mma(zero4(), v_frag(L, et, count), af);
+        f32x4 acc = mma(zero4(), el < EH ? v_frag(e0 + 16 * el) : ones_frag(L, count), af);
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
         if (el < EH) {
@@ -542,7 +545,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
       for (int el = 0; el < EH; ++el) sstore_tile_T(oF, ZS, S[mt][el], 16 * mt, e0 + 16 * el);
-      if (zown && c == 0) {
+      if (c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) zs[f * FW + 16 * mt + 4 * g + r] = Sz[mt][r];
       }
@@ -628,7 +631,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
       for (int el = 0; el < EH; ++el) sstore_tile_T(oF, ZG, Gs[mt][el], 16 * mt, e0 + 16 * el);
-      if (zown && c == 0) {
+      if (c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) dzs[f * FW + 16 * mt + 4 * g + r] = Gz[mt][r];
       }
@@ -676,12 +679,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const F qf = sfrag_tr(oF, Zq, 0, 16 * mt);
 #pragma unroll
       for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, sfrag_tr(oR, dNs, 0, e0 + 16 * el));
-      if (zown) {
-        F dd;
+      F dd;
 #pragma unroll
-        for (int s = 0; s < 8; ++s) dd[s] = dDb[kp(g, s)];
-        Gz[mt] = mma(Gz[mt], qf, dd);
-      }
+      for (int s = 0; s < 8; ++s) dd[s] = dDb[kp(g, s)];
+      Gz[mt] = mma(Gz[mt], qf, dd);
     }
     __syncthreads();
     L = fresh_lane();
