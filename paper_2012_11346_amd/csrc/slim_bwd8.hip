@@ -336,9 +336,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
       }
       // key rows: exp2(log2e (w.k - |k|^2/2 - shift) - log2(M)/2), the row term folded into the exponent
+      // (rows past the tile: an infinite offset gives exactly zero features)
       float kc[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) kc[r] = (G::KIND == kFavor) ? koff + 0.5f * kLog2e * kn[16 * h + 4 * g + r] : 0.f;
+      for (int r = 0; r < 4; ++r)
+        kc[r] = (G::KIND == kFavor) ? (16 * h + 4 * g + r < count ? koff + 0.5f * kLog2e * kn[16 * h + 4 * g + r] : INFINITY)
+                                    : 0.f;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 kv = zero4();
@@ -346,8 +349,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int kb = 0; kb < EB; ++kb) kv = mma(kv, sfrag_rm(oR, Ks, 16 * h, 32 * kb), Wf[mt][kb]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const bool ok = 16 * h + 4 * g + r < count;
-          kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - kc[r]) : fmaxf(kv[r], 0.f) + a.relu_eps;
+          if (G::KIND == kFavor) {
+            kv[r] = fast_exp2(kv[r] * kLog2e - kc[r]);
+          } else {
+            const bool ok = 16 * h + 4 * g + r < count;
+            kv[r] = ok ? fmaxf(kv[r], 0.f) + a.relu_eps : 0.f;
+          }
         }
         sstore_tile_T(oK, Zk, kv, 16 * h, 16 * mt);
       }
@@ -388,14 +395,17 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int r = 0; r < 4; ++r)
           Lq[mt][tt][r] = (G::KIND == kFavor) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs)
                                               : fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
-        sstore_tile_T(oF, Zq, Lq[mt][tt], 16 * mt, 16 * tt);
       }
     }
-    F qf[MB][RT];  // Q~ contracting over this slice's features, columns t
+    F qf[MB][RT];  // Q~ contracting over this slice's features, columns t (rounded once, also -> Zq)
 #pragma unroll
     for (int kb = 0; kb < MB; ++kb)
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) qf[kb][tt] = tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt]);
+      for (int tt = 0; tt < RT; ++tt) {
+        qf[kb][tt] = tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt]);
+        sstore_half_T(oF, Zq, frag_lo(qf[kb][tt]), 32 * kb, 16 * tt);
+        sstore_half_T(oF, Zq, frag_hi(qf[kb][tt]), 32 * kb + 16, 16 * tt);
+      }
 
     // ---- state before the tile: downdate (eq. 17), or the exact segment start
     if (j == jreset) {
@@ -443,15 +453,20 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
             if (4 * g + r > c) acc[r] = 0.f;
         }
         At[st][tt] = acc;
-        sstore_tile_T(oK, ZA, acc, 16 * st, 16 * tt);
       }
+    F af[RT];  // A^T contracting over rows s, columns t (rounded once, also -> ZA)
+#pragma unroll
+    for (int tt = 0; tt < RT; ++tt) {
+      af[tt] = tile_pair_frag<T>(At[0][tt], At[1][tt]);
+      sstore_half_T(oK, ZA, frag_lo(af[tt]), 0, 16 * tt);
+      sstore_half_T(oK, ZA, frag_hi(af[tt]), 16, 16 * tt);
+    }
     // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
-      const F af = tile_pair_frag<T>(At[0][tt], At[1][tt]);  // A^T contracting over rows s
 #pragma unroll
       for (int el = 0; el <= EH; ++el) {
-        f32x4 acc = mma(zero4(), el < EH ? v_frag(e0 + 16 * el) : ones_frag(L, count), af);
+        f32x4 acc = mma(zero4(), el < EH ? v_frag(e0 + 16 * el) : ones_frag(L, count), af[tt]);
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
         if (el < EH) {
@@ -644,33 +659,21 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
     // ---- dK~[s][m] = sum_e V[s][e] G[m][e] + dz[m] + sum_t dA^T[s][t] Q~[t][m] for this
     //      wave's rows s in [16 h, 16 h + 16); Pk = dK~ . K~ (FAVOR+) or masked (ReLU)
-    //      -> ZPk[m][s]; row sums -> rsum
+    //      -> ZPk[m][s] (rows past the tile have K~ = 0, hence Pk = 0)
     {
-      float rk[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        f32x4 acc;
         const float dz = dzs[f * FW + 16 * mt + c];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] = (16 * h + 4 * g + r < count) ? dz : 0.f;
+        f32x4 acc = {dz, dz, dz, dz};
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb)
           acc = mma(acc, sfrag_rm(oR, Vs, 16 * h, 32 * kb), sfrag_tr(oF, ZG, 32 * kb, 16 * mt));
         acc = mma(acc, sfrag_tr(oK, ZdA, 0, 16 * h), sfrag_tr(oF, Zq, 0, 16 * mt));
         const f32x4 kv = sload_tile_T(oK, Zk, 16 * h, 16 * mt);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
+        for (int r = 0; r < 4; ++r)
           acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
-          rk[r] += acc[r];
-        }
         sstore_tile_T(oK, ZPk, acc, 16 * h, 16 * mt);
-      }
-      if (G::KIND == kFavor) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float v = wave_sum_over_c(rk[r]);
-          if (c == 0) rsum[f * TR + 16 * h + 4 * g + r] = v;
-        }
       }
     }
     // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns
@@ -691,7 +694,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     fresh_offsets();
 
     // ---- dW[m][e] += sum_s Pk[s][m] K[s][e]; dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum_f(Pk)[s]
-    //      own columns -> RedY[s][e']
+    //      own columns -> RedY[s][e'], with rowsum_f(Pk)[s] (over this slice's features) from
+    //      a product with an all-ones operand
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const F pf = sfrag_rm(oK, ZPk, 16 * mt, 0);
@@ -701,7 +705,19 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     {
 #pragma unroll
     for (int st = 0; st < RT; ++st) {
-      const float rsv = (G::KIND == kFavor) ? rsum[f * TR + 16 * st + c] : 0.f;
+      F pk[MB];
+#pragma unroll
+      for (int kb = 0; kb < MB; ++kb) pk[kb] = sfrag_tr(oK, ZPk, 32 * kb, 16 * st);
+      float rsv = 0.f;
+      if (G::KIND == kFavor) {
+        F ones;
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2) ones[s2] = cvt<T>(1.f);
+        f32x4 rs = zero4();
+#pragma unroll
+        for (int kb = 0; kb < MB; ++kb) rs = mma(rs, ones, pk[kb]);
+        rsv = rs[0];  // every row of the product holds the sums of the columns s
+      }
 #pragma unroll
       for (int el = 0; el < EH; ++el) {
         const int et = h * EH + el;
@@ -714,7 +730,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, Wb[kb][el], sfrag_tr(oK, ZPk, 32 * kb, 16 * st));
+          acc = mma(acc, Wb[kb][el], pk[kb]);
         store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
       }
     }

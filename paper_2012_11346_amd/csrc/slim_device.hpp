@@ -356,6 +356,14 @@ __device__ __forceinline__ void sstore_tile_T(const SwzLane<P, MODE>& o, bf16* Z
   *(bf16x4*)(Z + o.a + col0 * P + row0) = v;
 }
 
+// the same store for values already rounded (half of an operand fragment)
+template <int P, int MODE>
+__device__ __forceinline__ void sstore_half_T(const SwzLane<P, MODE>& o, bf16* Z, const bf16x4& v, int row0, int col0) {
+  *(bf16x4*)(Z + o.a + col0 * P + row0) = v;
+}
+__device__ __forceinline__ bf16x4 frag_lo(const bf16x8& f) { return __builtin_shufflevector(f, f, 0, 1, 2, 3); }
+__device__ __forceinline__ bf16x4 frag_hi(const bf16x8& f) { return __builtin_shufflevector(f, f, 4, 5, 6, 7); }
+
 // X[row0 + 4g + r][col0 + c] of a tile stored transposed by sstore_tile_T
 template <int P, int MODE>
 __device__ __forceinline__ f32x4 sload_tile_T(const SwzLane<P, MODE>& o, const bf16* Z, int row0, int col0) {
