@@ -292,6 +292,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     else __builtin_amdgcn_raw_buffer_store_b32(v[0], rs, off, 0, 0);
   };
   u32e dk_hold = {};
+  // W fragments of the logits, fetched one tile ahead (at the end of the
+  // previous tile) so that the features phase starts with them resident
+  F Wf[MT][EB];
+  auto fetch_wf = [&]() {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = wfrag(WL::a(f, mt, kb));
+  };
+  fetch_wf();
   __amdgpu_buffer_rsrc_t dk_rs = range_rsrc(dKh, 0);
   int dk_off = 0;
   for (int j = j1 - 1; j >= j0; --j) {
@@ -307,11 +317,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      logits of this wave's 16 rows; K~ -> Zk[m][s]
     f32x4 Lq[MT][RT];
     {
-      F Wf[MT][EB];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = wfrag(WL::a(f, mt, kb));
       // rows of the next tile, stored into LDS at the end of this one; issued
       // after the W fragments so that waiting for those does not wait for
       // these.  Range-checked loads without branches (an empty range after
@@ -755,6 +760,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       stA.template store_swz<LDQ>(dstA, nrmA, st2);
       stB.template store_swz<LDQ>(dstB, nrmB, st2);
     }
+    fetch_wf();
     __syncthreads();
     L = fresh_lane();
     g = L.g;
