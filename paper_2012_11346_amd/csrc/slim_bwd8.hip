@@ -579,6 +579,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // ---- dQ~^T[m][t] = sum_e S[m][e] dN[t][e] + z[m] dD[t] + sum_s K~[s][m] dA^T[s][t]
     //      for this wave's rows t in [16 h, 16 h + 16); P = dQ~ . Q~ (FAVOR+) or
     //      dQ~ masked (ReLU) -> ZP[t][m]
+    // (the W fragments of the dq and dk products are fetched here, a phase
+    // ahead of their first use)
+#pragma unroll
+    for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+      for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
     {
       const float ddt = dDs[16 * h + c];
 #pragma unroll
@@ -608,11 +614,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      -q[t] sum_m P[t][m], which is zero: Y is homogeneous of degree 0 in
     //      each query feature vector, so sum_m Q~[t][m] dQ~[t][m] = 0.
     {
-      // the W fragments of the dq and dk products, fetched together
-#pragma unroll
-      for (int kb = 0; kb < MB; ++kb)
-#pragma unroll
-        for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
 #pragma unroll
