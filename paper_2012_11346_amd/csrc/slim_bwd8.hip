@@ -428,6 +428,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
           for (int et = 0; et < EH; ++et) S[mt][et][r] = row[16 * et];
           Sz[mt][r] = row[D - e0 - c];
         }
+      // complete these loads here: otherwise the first use of S after the
+      // branches would wait for every outstanding load on the common path
+      // too, including the next tile's rows (gfx9 encoding: vmcnt(0) only)
+      __builtin_amdgcn_s_waitcnt(0x0F70);
     } else {
       const F ones = ones_frag(L, count);
 #pragma unroll
