@@ -237,7 +237,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const float koff = (G::KIND == kFavor) ? a.kshift[head] * kLog2e + half_log2M : 0.f;
 
   // row staging: threads 0..255 carry Q and K, threads 256..511 carry V and dY
-  const int sh = threadIdx.x >> 8, stid = threadIdx.x & 255;
+  // (wave-uniform: the range resources of the prefetch live in scalar registers)
+  const int sh = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8), stid = threadIdx.x & 255;
   const T* srcA = sh ? Vh : Qh;
   const T* srcB = sh ? dYh : Kh;
   T* dstA = sh ? Vs : Qs;
@@ -343,15 +344,22 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       // key rows: exp2(log2e (w.k - |k|^2/2 - shift) - log2(M)/2), the row term folded into the exponent
       // (rows past the tile: an infinite offset gives exactly zero features)
       float kc[4];
+      if (G::KIND == kFavor) {
+        const f32x4 knv = *(const f32x4*)&kn[16 * h + 4 * g];
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        kc[r] = (G::KIND == kFavor) ? (16 * h + 4 * g + r < count ? koff + 0.5f * kLog2e * kn[16 * h + 4 * g + r] : INFINITY)
-                                    : 0.f;
+        for (int r = 0; r < 4; ++r) {
+          const float v = koff + 0.5f * kLog2e * knv[r];
+          kc[r] = 16 * h + 4 * g + r < count ? v : INFINITY;
+        }
+      }
+      F kfr[EB];  // this wave's 16 key rows as operands
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) kfr[kb] = sfrag_rm(oR, Ks, 16 * h, 32 * kb);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 kv = zero4();
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, sfrag_rm(oR, Ks, 16 * h, 32 * kb), Wf[mt][kb]);
+        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, kfr[kb], Wf[mt][kb]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           if (G::KIND == kFavor) {
