@@ -164,8 +164,8 @@ FwdLayout fwd_layout(const slim_problem* p, int P) {
   off += align256(n * state_elems(p) * sizeof(float));
   l.seg_shift = off;
   off += align256(n * sizeof(float));
-  l.starts = off;
-  off += align256(n * state_elems(p) * sizeof(float));
+  l.starts = off;  // segment starts, or the P2 + 1 boundaries of each head (fixed key shift)
+  off += align256((n + (size_t)p->B * p->H) * state_elems(p) * sizeof(float));
   l.start_shift = off;
   off += align256(n * sizeof(float));
   l.total = off;
@@ -213,6 +213,7 @@ typedef hipError_t (*bwd_fn)(const slim::BwdArgs&, hipStream_t);
 typedef hipError_t (*wfrag_fn)(const slim::WfragArgs&, hipStream_t);
 typedef size_t (*size_fn)();
 typedef hipError_t (*carry_fn)(const slim::CarryArgs&, hipStream_t);
+typedef hipError_t (*ksum_fn)(const slim::KsumArgs&, int, hipStream_t);
 
 struct Dispatch {
   fwd_fn fwd;
@@ -222,18 +223,20 @@ struct Dispatch {
   wfrag_fn wfrag;
   size_fn wfrag_bytes;
   carry_fn carry;
+  ksum_fn ksum;  // key sums of row ranges (nullptr where not built: the key-only walk serves)
 };
 
 template <class T, int D, int FW, int KIND>
 Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
   return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>, nullptr,
-                  &slim::launch_wfrag<G>, &slim::wfrag_bytes<G>,      &slim::launch_carry<G>};
+                  &slim::launch_wfrag<G>,    &slim::wfrag_bytes<G>,     &slim::launch_carry<G>,    nullptr};
 }
 template <int D, int FW, int KIND>
 Dispatch make_dispatch8() {
   Dispatch d = make_dispatch<slim::bf16, D, FW, KIND>();
   d.bwd8 = &slim::launch_bwd_walk8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
+  d.ksum = &slim::launch_ksum<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   return d;
 }
 
@@ -379,6 +382,58 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.P = P;
   a.relu_eps = p->relu_eps;
   hipError_t e = hipSuccess;
+  if (P > 1 && dp.ksum != nullptr) {
+    // One key shift for the whole head: (0) the largest key exponent of every
+    // part and of the initial state; (1) what each part adds relative to it;
+    // (2) the exact state at every part boundary; (3) the walk, each segment
+    // starting from its boundary, with no rescaling.
+    const int S2 = plan_sum_split(p, P), P2 = P * S2;
+    const int BH = (int)(p->B * p->H);
+    slim::KsumArgs ks;
+    std::memset(&ks, 0, sizeof(ks));
+    ks.K = K;
+    ks.V = V;
+    ks.W = W;
+    ks.B = (int)p->B;
+    ks.H = (int)p->H;
+    ks.L = (int)p->L;
+    ks.C = clamp_C(p);
+    ks.P2 = P2;
+    ks.relu_eps = p->relu_eps;
+    if (favor) {
+      ks.out = (float*)(w + lay.seg_shift);
+      e = dp.ksum(ks, slim::kSumMax, s);
+      if (e != hipSuccess) return hip_fail(e, "key-maximum launch");
+      e = slim::launch_kshift_reduce(ks.out, P2, state_in != nullptr ? kshift_in : nullptr, kshift_out, BH, s);
+      if (e != hipSuccess) return hip_fail(e, "key-shift launch");
+      ks.shift = kshift_out;
+    }
+    ks.out = (float*)(w + lay.seg_sum);
+    e = dp.ksum(ks, slim::kSumStates, s);
+    if (e != hipSuccess) return hip_fail(e, "key-sum launch");
+    slim::ScanArgs sc;
+    std::memset(&sc, 0, sizeof(sc));
+    sc.seg = ks.out;
+    sc.init = state_in;
+    sc.init_shift = favor ? kshift_in : nullptr;
+    sc.shift = favor ? kshift_out : nullptr;
+    sc.out = (float*)(w + lay.starts);
+    sc.BH = BH;
+    sc.P = P2;
+    sc.SZ = (int)state_elems(p);
+    sc.favor = favor ? 1 : 0;
+    e = slim::launch_scan_bwd(sc, s);
+    if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
+    a.seg_state = sc.out;
+    a.seg_stride = P2 + 1;
+    a.seg_step = S2;
+    a.fixed_shift = favor ? kshift_out : nullptr;
+    a.Y = Y;
+    a.state_out = state_out;
+    e = timed_launch(SLIM_PHASE_FWD, s, [&] { return dp.fwd(a, slim::kWalkOutputs, s); });
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+    return ok();
+  }
   if (P > 1) {
     // (1) what each sub-segment adds, with its own running key shift
     const int S2 = plan_sum_split(p, P), P2 = P * S2;
@@ -467,15 +522,32 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   // (1) segment sums with the shift the reverse walk uses, so that every
   //     downdate subtracts exactly the rounded features that were added
   const int S2 = plan_sum_split(p, P), P2 = P * S2;
-  slim::FwdArgs k = f;
-  k.P = P2;
-  k.seg_out = (float*)(w + lay.seg_sum);
-  e = dp.fwd(k, slim::kWalkSums, s);
+  if (dp.ksum != nullptr) {
+    slim::KsumArgs ks;
+    std::memset(&ks, 0, sizeof(ks));
+    ks.K = K;
+    ks.V = V;
+    ks.W = W;
+    ks.shift = favor ? kshift : nullptr;
+    ks.out = (float*)(w + lay.seg_sum);
+    ks.B = (int)p->B;
+    ks.H = (int)p->H;
+    ks.L = (int)p->L;
+    ks.C = clamp_C(p);
+    ks.P2 = P2;
+    ks.relu_eps = p->relu_eps;
+    e = dp.ksum(ks, slim::kSumStates, s);
+  } else {
+    slim::FwdArgs k = f;
+    k.P = P2;
+    k.seg_out = (float*)(w + lay.seg_sum);
+    e = dp.fwd(k, slim::kWalkSums, s);
+  }
   if (e != hipSuccess) return hip_fail(e, "segment-sum launch");
   // (2) exact states at the segment boundaries
   slim::ScanArgs sc;
   std::memset(&sc, 0, sizeof(sc));
-  sc.seg = k.seg_out;
+  sc.seg = (float*)(w + lay.seg_sum);
   sc.init = state_in;
   sc.init_shift = favor ? kshift_in : nullptr;
   sc.shift = favor ? kshift : nullptr;

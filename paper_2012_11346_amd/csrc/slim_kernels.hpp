@@ -98,8 +98,26 @@ struct CarryArgs {
   float relu_eps;
 };
 
+// Key sums of contiguous parts of each head (ksum_kernel): per part, the
+// state it adds relative to a fixed key shift, or the largest key exponent.
+enum KsumMode { kSumStates = 0, kSumMax = 1 };
+struct KsumArgs {
+  const void* K;
+  const void* V;
+  const float* W;
+  const float* shift;  // kSumStates, FAVOR+: [B,H] key shift of the sums
+  float* out;          // kSumStates: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
+  int B, H, L, C, P2;
+  float relu_eps;
+};
+
 template <class G>
 hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s);
+template <class G>
+hipError_t launch_ksum(const KsumArgs& a, int mode, hipStream_t s);
+// kshift[h] = max(init_shift[h] (if given), max_p part_max[h][p])
+hipError_t launch_kshift_reduce(const float* part_max, int P2, const float* init_shift, float* kshift, int BH,
+                                hipStream_t s);
 // exclusive scan of segment states (forward: with key-shift rescaling)
 hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s);
 // inclusive boundaries of segment states under one common shift (backward)

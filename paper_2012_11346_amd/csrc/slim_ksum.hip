@@ -1,0 +1,238 @@
+// Key sums of contiguous row ranges: the state each part of a segmented
+// sequence adds (eqs. 14-16 summed over the part), and the largest key
+// exponent of each part.
+//
+// Each head's sequence is cut into P2 parts at the 32-row tile boundaries
+// the walks use (part p holds tiles [p n / P2, (p + 1) n / P2)).  A part's
+// contribution to the state is a plain sum over its rows,
+//   [S | z] = sum_s K~[s]^T [V[s] | 1],
+// with no causal structure, so this pass streams the part's rows in 64-row
+// chunks with one barrier per chunk.  Four waves split the M features; per
+// chunk a wave computes the key logits of its features on the matrix cores
+// (W in registers), the features (FAVOR+: exp2 of the logit shifted by the
+// head's fixed key shift and the row's -|k|^2/2; ReLU: max(., 0) + eps) and
+// accumulates K~^T [V|1] into its share of the state in registers.  Rows
+// move through double-buffered, swizzled LDS tiles; the rows two chunks
+// ahead are fetched with range-checked loads (zero past the part).
+//
+// KS_MAX mode computes only the logits and returns, per part, the maximum of
+// w_m.k - |k|^2/2 over its rows and all features: the maximum over a head's
+// parts is the key shift of that head.
+#include "slim_common.hpp"
+#include "slim_kernels.hpp"
+
+namespace slim {
+
+template <class G, int MODE>
+__global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
+  typedef typename G::T T;
+  typedef typename FragT<T>::type F;
+  constexpr int D = G::D, FW = G::FW, M = G::M, MT = G::MT, ET = G::ET, EB = G::EB;
+  constexpr int CR = 64;          // rows per chunk
+  constexpr int CT = CR / 16;     // 16-row tiles per chunk
+  constexpr int LDQ = D + 16;     // row tiles, swizzled (kSwzRows)
+  constexpr int TQ = CR * LDQ;
+  constexpr bool SUMS = MODE == kSumStates;
+  typedef SwzLane<LDQ, kSwzRows> OR;
+  static_assert(sizeof(T) == 2 && (MT % 2) == 0, "bf16, 32-feature blocks");
+
+  __shared__ __attribute__((aligned(16))) T Kb[2 * TQ];
+  __shared__ __attribute__((aligned(16))) T Vb[SUMS ? 2 * TQ : 8];
+  __shared__ float knb[2][CR];
+  __shared__ float wmax[4];
+
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int part = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
+  const size_t head = (size_t)b * a.H + hd;
+  const T* Kh = (const T*)a.K + head * (size_t)a.L * D;
+  const T* Vh = (const T*)a.V + head * (size_t)a.L * D;
+
+  // W fragments of this wave's features: slot s = W[w FW + 16 mt + c][32 kb + kp(g, s)]
+  F Wf[MT][EB];
+  {
+    const Lane L = this_lane();
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb)
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          Wf[mt][kb][s] = cvt<T>(a.W[(size_t)(w * FW + 16 * mt + L.c) * D + 32 * kb + kp(L.g, s)]);
+  }
+
+  // rows of this part
+  const TileMap tm(a.L, a.C, 32);
+  const int n_tiles = tm.count_tiles();
+  const int j0 = (int)((int64_t)part * n_tiles / a.P2), j1 = (int)((int64_t)(part + 1) * n_tiles / a.P2);
+  int r0 = 0, r1 = 0;
+  if (j1 > j0) {
+    int s_, c_;
+    tm.tile(j0, r0, c_);
+    tm.tile(j1 - 1, s_, c_);
+    r1 = s_ + c_;
+  }
+  const int nrows = r1 - r0, nch = (nrows + CR - 1) / CR;
+  const size_t nbytes = (size_t)nrows * D * sizeof(T);
+  const __amdgpu_buffer_rsrc_t rK = range_rsrc(Kh + (size_t)r0 * D, nbytes);
+  const __amdgpu_buffer_rsrc_t rV = range_rsrc(Vh + (size_t)r0 * D, nbytes);
+
+  const float half_log2M = 0.5f * __log2f((float)M);
+  const float koff = (SUMS && G::KIND == kFavor) ? a.shift[head] * kLog2e + half_log2M : 0.f;
+
+  f32x4 S[SUMS ? MT : 1][SUMS ? ET : 1], Sz[SUMS ? MT : 1];
+  if constexpr (SUMS) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+      for (int et = 0; et < ET; ++et) S[mt][et] = zero4();
+      Sz[mt] = zero4();
+    }
+  }
+  float vmax = -INFINITY;
+
+  RowStage<T, D, CR, 256> sk, sv;
+  const int tid = threadIdx.x;
+  float* const knorm = G::KIND == kFavor ? knb[0] : nullptr;
+  sk.fetch(rK, 0, tid);
+  if constexpr (SUMS) sv.fetch(rV, 0, tid);
+  sk.template store_swz<LDQ>(Kb, knorm, tid);
+  if constexpr (SUMS) sv.template store_swz<LDQ>(Vb, nullptr, tid);
+  sk.fetch(rK, CR, tid);
+  if constexpr (SUMS) sv.fetch(rV, CR, tid);
+  __syncthreads();
+
+  for (int ci = 0; ci < nch; ++ci) {
+    const int bf = ci & 1;
+    const int cnt = min(CR, nrows - ci * CR);
+    // rows of chunk ci + 1 into the other buffer (its readers, chunk ci - 1,
+    // finished before the last barrier); rows of chunk ci + 2 into registers
+    {
+      const int t2 = fresh_tid();
+      sk.template store_swz<LDQ>(Kb + (bf ^ 1) * TQ, G::KIND == kFavor ? knb[bf ^ 1] : nullptr, t2);
+      if constexpr (SUMS) sv.template store_swz<LDQ>(Vb + (bf ^ 1) * TQ, nullptr, t2);
+      sk.fetch(rK, (ci + 2) * CR, t2);
+      if constexpr (SUMS) sv.fetch(rV, (ci + 2) * CR, t2);
+    }
+    const T* Ks = Kb + bf * TQ;
+    const T* Vs = Vb + bf * TQ;
+    const float* kn = knb[bf];
+    const Lane L = fresh_lane();
+    const OR oR(L);
+
+    // logits: Lk[st][mt] rows s = 16 st + 4 g + r, columns m = w FW + 16 mt + c
+    f32x4 Lk[CT][MT];
+#pragma unroll
+    for (int st = 0; st < CT; ++st) {
+      F kf[EB];
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) kf[kb] = sfrag_rm(oR, Ks, 16 * st, 32 * kb);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[kb], Wf[mt][kb]);
+        Lk[st][mt] = acc;
+      }
+    }
+
+    if constexpr (!SUMS) {
+      // the key exponent w.k - |k|^2/2 of the chunk's rows
+#pragma unroll
+      for (int st = 0; st < CT; ++st) {
+        const f32x4 knv = *(const f32x4*)&kn[16 * st + 4 * L.g];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) v = fmaxf(v, Lk[st][mt][r]);
+          vmax = fmaxf(vmax, 16 * st + 4 * L.g + r < cnt ? v - 0.5f * knv[r] : -INFINITY);
+        }
+      }
+    } else {
+      // features (rows past the chunk: zero)
+#pragma unroll
+      for (int st = 0; st < CT; ++st) {
+        const f32x4 knv = *(const f32x4*)&kn[16 * st + 4 * L.g];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = 16 * st + 4 * L.g + r < cnt;
+          const float kc = ok ? koff + 0.5f * kLog2e * knv[r] : INFINITY;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            float x = Lk[st][mt][r];
+            if (G::KIND == kFavor) x = fast_exp2(x * kLog2e - kc);
+            else x = ok ? fmaxf(x, 0.f) + a.relu_eps : 0.f;
+            Lk[st][mt][r] = x;
+          }
+        }
+      }
+      // [S | z] += K~^T [V | 1] over the chunk's rows, 32 rows per product
+#pragma unroll
+      for (int rb = 0; rb < CT / 2; ++rb) {
+        F vf[ET];
+#pragma unroll
+        for (int et = 0; et < ET; ++et) vf[et] = sfrag_tr(oR, Vs, 32 * rb, 16 * et);
+        F ones;
+        const int rem = cnt - 32 * rb - 4 * L.g;  // rows 32 rb + kp(g, s) < cnt
+#pragma unroll
+        for (int s = 0; s < 8; ++s) ones[s] = cvt<T>((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const F kt = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
+#pragma unroll
+          for (int et = 0; et < ET; ++et) S[mt][et] = mma(S[mt][et], kt, vf[et]);
+          Sz[mt] = mma(Sz[mt], kt, ones);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  if constexpr (SUMS) {
+    float* out = a.out + (head * a.P2 + part) * (size_t)M * (D + 1);
+    const Lane L = this_lane();
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t row = (size_t)(w * FW + 16 * mt + 4 * L.g + r) * (D + 1);
+#pragma unroll
+        for (int et = 0; et < ET; ++et) out[row + 16 * et + L.c] = S[mt][et][r];
+        if (L.c == 0) out[row + D] = Sz[mt][r];
+      }
+  } else {
+    vmax = wave_max(vmax);
+    if ((threadIdx.x & 63) == 0) wmax[w] = vmax;
+    __syncthreads();
+    if (threadIdx.x == 0) a.out[head * a.P2 + part] = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+  }
+}
+
+// kshift[head] = max over the head's parts (and over init_shift, when given)
+__global__ void kshift_reduce_kernel(const float* part_max, int P2, const float* init_shift, float* kshift, int BH) {
+  const int head = blockIdx.x * blockDim.x + threadIdx.x;
+  if (head >= BH) return;
+  float v = init_shift != nullptr ? init_shift[head] : -INFINITY;
+  for (int p = 0; p < P2; ++p) v = fmaxf(v, part_max[(size_t)head * P2 + p]);
+  kshift[head] = v;
+}
+
+template <class G>
+hipError_t launch_ksum(const KsumArgs& a, int mode, hipStream_t s) {
+  const dim3 grid(a.P2, a.H, a.B);
+  if (mode == kSumStates) hipLaunchKernelGGL((ksum_kernel<G, kSumStates>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((ksum_kernel<G, kSumMax>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kshift_reduce(const float* part_max, int P2, const float* init_shift, float* kshift, int BH,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(kshift_reduce_kernel, dim3((BH + 63) / 64), dim3(64), 0, s, part_max, P2, init_shift, kshift, BH);
+  return hipGetLastError();
+}
+
+#define SLIM_INST_KSUM(T, D, FW, TR, KIND) \
+  template hipError_t launch_ksum<Cfg<T, D, FW, TR, KIND>>(const KsumArgs&, int, hipStream_t);
+SLIM_FOR_EACH_BF16_CONFIG(SLIM_INST_KSUM)
+
+}  // namespace slim
