@@ -168,12 +168,17 @@ def main():
             wsf=torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_FWD)), dtype=torch.uint8, device=dev),
             wsb=torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_BWD)), dtype=torch.uint8, device=dev),
         )
+        # the forward's segment boundary states, handed to the backward (state-sized)
+        n_ctx = slim.context_bytes(p)
+        if n_ctx > 0:
+            bufs["wsctx"] = torch.empty(n_ctx // 4, dtype=torch.float32, device=dev)
         return p, bufs
 
     def step(C, b):
-        slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
+        slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"],
+                 ctx=b.get("wsctx"))
         slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
-                 dW=b["dW"])
+                 dW=b["dW"], ctx=b.get("wsctx"))
 
     def timed(C, steps, warmup):
         """warmup + `steps` timed steps.  Per step: the whole step, the
@@ -196,11 +201,12 @@ def main():
             e = ev[i]
             e[0].record(stream)
             slim.time_walk(slim.PHASE_FWD, e[1], e[2])
-            slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"])
+            slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"],
+                     ctx=b.get("wsctx"))
             e[3].record(stream)
             slim.time_walk(slim.PHASE_BWD, e[4], e[5])
             slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
-                     dW=b["dW"])
+                     dW=b["dW"], ctx=b.get("wsctx"))
             e[6].record(stream)
         torch.cuda.synchronize()
         total_ms = ev[0][0].elapsed_time(ev[-1][6])
@@ -210,6 +216,7 @@ def main():
         return dict(total_ms=total_ms, ms=total_ms / steps, fwd_ms=avg(0, 3), bwd_ms=avg(3, 6),
                     fwd_walk_ms=avg(1, 2), bwd_walk_ms=avg(4, 5), peak=peak, extra=peak - pre - out_bytes,
                     out_bytes=out_bytes, ws_fwd=b["wsf"].numel(), ws_bwd=b["wsb"].numel(),
+                    ctx=b["wsctx"].numel() * 4 if "wsctx" in b else 0,
                     segments=slim.num_segments(p)), b
 
     C = args.C
@@ -265,7 +272,7 @@ def main():
         "mfma_frac_fwd_bwd": (fl_f + fl_b) * units / (r["ms"] / 1e3) / PEAK_BF16_FLOPS,
         "peak_mem": {"peak_bytes": r["peak"], "input_bytes": io_bytes, "output_bytes": r["out_bytes"],
                      "beyond_io_bytes": r["extra"],
-                     "workspace_fwd": r["ws_fwd"], "workspace_bwd": r["ws_bwd"]},
+                     "workspace_fwd": r["ws_fwd"], "workspace_bwd": r["ws_bwd"], "context": r["ctx"]},
     }
     print(f"[bench] C={C}: {r['ms']:.3f} ms/step (fwd {r['fwd_ms']:.3f}, bwd {r['bwd_ms']:.3f}; walks "
           f"{r['fwd_walk_ms']:.3f} / {r['bwd_walk_ms']:.3f}), {value:.3e} tokens/s", file=sys.stderr, flush=True)

@@ -93,6 +93,15 @@ typedef struct {
  * makes no HIP call. */
 size_t slim_workspace_bytes(const slim_problem* p, int phase);
 
+/* Bytes of the optional context slim_fwd can hand to slim_bwd for problem
+ * *p, or 0 when the problem uses none (then ctx is ignored and may be NULL).
+ * The context holds the exact states at the segment boundaries of every
+ * head ([B, H, P2 + 1, M, d + 1] float32: the state B^(n) of eqs. 14-16 at
+ * each of the P2 + 1 boundaries of the head's parts, relative to kshift_out).
+ * Its size depends on B H and the device, not on L: like the state itself it
+ * is flat in the sequence length.  Memory-only query: makes no HIP call. */
+size_t slim_context_bytes(const slim_problem* p);
+
 /* Feature map of Sec. 2.1 (the map g of eq. 2) on its own, for inspection.
  *   X      [B, H, L, d] queries (role SLIM_QUERY) or keys (role SLIM_KEY), dtype
  *   W      [M, d] float32
@@ -115,10 +124,13 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
  *   Y          out [B, H, L, d]
  *   state_out  out [B, H, M, d + 1], may be NULL: B^(N) relative to kshift_out
  *   kshift_out out [B, H] (FAVOR+: required; ReLU: ignored, may be NULL)
+ *   ctx        optional out of slim_context_bytes(p) bytes (NULL: none): the
+ *              segment boundary states, for the slim_bwd call on the same
+ *              inputs
  *   ws         workspace of at least slim_workspace_bytes(p, SLIM_PHASE_FWD) */
 int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, void* Y, float* state_out,
-             float* kshift_out, void* ws, size_t ws_bytes, void* stream);
+             float* kshift_out, float* ctx, void* ws, size_t ws_bytes, void* stream);
 
 /* Backward sweep of Algorithm 1 (one layer) for the loss
  * sum(dY * Y) + <dstate_out, state_out>.
@@ -132,17 +144,20 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
  *              query and key branches
  *   dstate_in  out, may be NULL: [B, H, M, d + 1] cotangent G^(0) of state_in
  *              (relative to kshift_in; relative to kshift when state_in is NULL)
+ *   ctx        optional: the context slim_fwd wrote for these inputs (and the
+ *              same state_in, kshift_in), or NULL
  *   ws         workspace of at least slim_workspace_bytes(p, SLIM_PHASE_BWD)
  * The reverse walk starts from B^(N) and downdates it tile by tile (eq. 17).
- * B^(N) and the states at the segment boundaries are rebuilt here from the
- * keys and values with the key shift `kshift`, so that each downdate
- * subtracts exactly the rounded features that were added; nothing of size
- * O(L) is kept between slim_fwd and slim_bwd.  The key shifts are constants
- * of the computation (stop-gradient); they cancel exactly in Y. */
+ * B^(N) and the states at the segment boundaries come from ctx, or, without
+ * one, are rebuilt here from the keys and values with the key shift
+ * `kshift`; either way each downdate subtracts exactly the rounded features
+ * that were added.  Nothing of size O(L) is kept between slim_fwd and
+ * slim_bwd.  The key shifts are constants of the computation
+ * (stop-gradient); they cancel exactly in Y. */
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
              const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
-             void* ws, size_t ws_bytes, void* stream);
+             const float* ctx, void* ws, size_t ws_bytes, void* stream);
 
 /* Kernel-timing instrumentation.  before and after are hipEvent_t handles
  * (passed as void*) created by the caller with timing enabled.  The next

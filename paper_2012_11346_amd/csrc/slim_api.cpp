@@ -107,31 +107,44 @@ int count_tiles(const slim_problem* p) {
 // Segments per head.  The walk inside a segment is sequential; segments run
 // in parallel and are stitched together by exact scans of their states.  The
 // count depends on B*H and the device size, not on L once L is long enough,
-// so workspace stays flat in L.  SLIM_SEGMENTS (debugging) forces a count.
+// so workspace stays flat in L.  It is rounded down, so that the workgroups
+// fit the device in one round.  SLIM_SEGMENTS (debugging) forces a count.
 int plan_segments_for(const slim_problem* p, int target) {
   const int n_tiles = count_tiles(p);
   const char* env = getenv("SLIM_SEGMENTS");
   if (env != nullptr && atoi(env) > 0) return std::max(1, std::min(atoi(env), n_tiles));
   const int64_t heads = p->B * p->H;
-  int P = (int)((target + heads - 1) / heads);
+  int P = (int)std::min<int64_t>(target / heads, 1 << 20);
   P = std::min(P, std::max(1, n_tiles / kMinTilesPerSegment));
   return std::max(1, P);
 }
+bool has_ksum(const slim_problem* p);
 // segments of the backward (and of slim_num_segments)
 int plan_segments(const slim_problem* p) { return plan_segments_for(p, kTargetWorkgroups); }
-// segments of the forward
-int plan_fwd_segments(const slim_problem* p) { return plan_segments_for(p, kTargetWorkgroupsForward); }
 
-// Sub-segments per segment for the key-sum pass: the sums are associative,
+// Parts per backward segment for the key-sum pass: the sums are associative,
 // and the pass fits two workgroups per compute unit, so each segment's sum
-// is split in two when that leaves at least two tiles per part.
+// is split in two when that leaves enough tiles per part.
 // SLIM_SUM_SPLIT (debugging) forces 1 or 2.
 int plan_sum_split(const slim_problem* p, int P) {
   const char* env = getenv("SLIM_SUM_SPLIT");
   const int n_tiles = count_tiles(p);
   if (env != nullptr && (atoi(env) == 1 || atoi(env) == 2)) return n_tiles >= 2 * P ? atoi(env) : 1;
+  if (has_ksum(p)) return 2 * P <= std::max(1, n_tiles / kMinTilesPerSegment) ? 2 : 1;
   const int64_t wgs = p->B * p->H * (int64_t)P;
   return (n_tiles >= 4 * P && 2 * wgs <= kTargetWorkgroupsForward) ? 2 : 1;
+}
+
+// Segments of the forward.  Problems on the key-sum kernel walk one segment
+// per part of the backward (two workgroups per compute unit), so that the
+// boundary states serve both passes; the others aim for twice the
+// backward's workgroups on their own.
+int plan_fwd_segments(const slim_problem* p) {
+  if (has_ksum(p)) {
+    const int P = plan_segments(p);
+    return P * plan_sum_split(p, P);
+  }
+  return plan_segments_for(p, kTargetWorkgroupsForward);
 }
 
 // Row parts per segment of the carry pass (several segments): enough
@@ -149,6 +162,18 @@ int plan_carry_split(const slim_problem* p, int P) {
 
 size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
 
+// Parts of the backward's segment boundaries: P segments, each split in S2.
+int bwd_parts(const slim_problem* p) {
+  const int P = plan_segments(p);
+  return P * plan_sum_split(p, P);
+}
+// The forward hands its boundary states to the backward (slim_context_bytes)
+// when it computes them with one key shift per head (the key-sum kernel):
+// then its segments are the backward's parts.
+bool context_used(const slim_problem* p) { return has_ksum(p) && plan_fwd_segments(p) > 1; }
+// Parts of the forward's boundaries on the one-shift path
+int fwd_parts(const slim_problem* p) { return plan_fwd_segments(p); }
+
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
 // forward workspace: segment sums and shifts, segment starts and shifts
@@ -158,7 +183,7 @@ struct FwdLayout {
 FwdLayout fwd_layout(const slim_problem* p, int P) {
   FwdLayout l{0, 0, 0, 0, 0};
   if (P <= 1) return l;
-  const size_t n = (size_t)p->B * p->H * P * plan_sum_split(p, P);
+  const size_t n = (size_t)p->B * p->H * (has_ksum(p) ? P : P * plan_sum_split(p, P));
   size_t off = 0;
   l.seg_sum = off;
   off += align256(n * state_elems(p) * sizeof(float));
@@ -276,6 +301,11 @@ Dispatch dispatch(const slim_problem* p) {
 }
 
 size_t wfrag_bytes_of(const slim_problem* p) { return dispatch(p).wfrag_bytes(); }
+bool has_ksum(const slim_problem* p) { return dispatch(p).ksum != nullptr; }
+size_t context_bytes(const slim_problem* p) {
+  if (!context_used(p)) return 0;
+  return (size_t)p->B * p->H * (bwd_parts(p) + 1) * state_elems(p) * sizeof(float);
+}
 
 size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_fwd_segments(p)).total; }
 size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
@@ -316,6 +346,11 @@ int slim_num_segments(const slim_problem* p) {
   return plan_segments(p);
 }
 
+size_t slim_context_bytes(const slim_problem* p) {
+  if (check_problem(p) != SLIM_OK) return 0;
+  return context_bytes(p);
+}
+
 size_t slim_workspace_bytes(const slim_problem* p, int phase) {
   if (check_problem(p) != SLIM_OK) return 0;
   if (phase == SLIM_PHASE_FWD) return fwd_ws_bytes(p);
@@ -349,8 +384,8 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
 }
 
 int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, void* ws,
-             size_t ws_bytes, void* stream) {
+             const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, float* ctx,
+             void* ws, size_t ws_bytes, void* stream) {
   int st = check_problem(p);
   if (st != SLIM_OK) return st;
   if (Q == nullptr || K == nullptr || V == nullptr || W == nullptr || Y == nullptr)
@@ -359,8 +394,9 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift_out == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift_out");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
-  st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out});
+  st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out, ctx});
   if (st != SLIM_OK) return st;
+  if (!context_used(p)) ctx = nullptr;
   const int P = plan_fwd_segments(p);
   const FwdLayout lay = fwd_layout(p, P);
   if (lay.total > 0 && (ws == nullptr || ws_bytes < lay.total))
@@ -387,7 +423,7 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     // part and of the initial state; (1) what each part adds relative to it;
     // (2) the exact state at every part boundary; (3) the walk, each segment
     // starting from its boundary, with no rescaling.
-    const int S2 = plan_sum_split(p, P), P2 = P * S2;
+    const int P2 = fwd_parts(p), S2 = P2 / P;
     const int BH = (int)(p->B * p->H);
     slim::KsumArgs ks;
     std::memset(&ks, 0, sizeof(ks));
@@ -417,7 +453,7 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     sc.init = state_in;
     sc.init_shift = favor ? kshift_in : nullptr;
     sc.shift = favor ? kshift_out : nullptr;
-    sc.out = (float*)(w + lay.starts);
+    sc.out = ctx != nullptr ? ctx : (float*)(w + lay.starts);
     sc.BH = BH;
     sc.P = P2;
     sc.SZ = (int)state_elems(p);
@@ -479,8 +515,8 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
 
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
-             const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in, void* ws,
-             size_t ws_bytes, void* stream) {
+             const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
+             const float* ctx, void* ws, size_t ws_bytes, void* stream) {
   int st = check_problem(p);
   if (st != SLIM_OK) return st;
   if (Q == nullptr || K == nullptr || V == nullptr || W == nullptr || dY == nullptr || dQ == nullptr ||
@@ -491,8 +527,9 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift (kshift_out of slim_fwd)");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
-  st = check_alignment({Q, K, V, dY, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in});
+  st = check_alignment({Q, K, V, dY, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in, ctx});
   if (st != SLIM_OK) return st;
+  if (!context_used(p)) ctx = nullptr;
   const int P = plan_segments(p);
   const BwdLayout lay = bwd_layout(p, P);
   if (ws == nullptr || ws_bytes < lay.total)
@@ -520,8 +557,12 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   f.relu_eps = p->relu_eps;
 
   // (1) segment sums with the shift the reverse walk uses, so that every
-  //     downdate subtracts exactly the rounded features that were added
+  //     downdate subtracts exactly the rounded features that were added;
+  //     (2) exact states at the segment boundaries.  Both come from the
+  //     forward's context when the caller passes it.
   const int S2 = plan_sum_split(p, P), P2 = P * S2;
+  const float* bounds = ctx;
+  if (bounds == nullptr) {
   if (dp.ksum != nullptr) {
     slim::KsumArgs ks;
     std::memset(&ks, 0, sizeof(ks));
@@ -558,6 +599,8 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   sc.favor = favor ? 1 : 0;
   e = slim::launch_scan_bwd(sc, s);
   if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
+  bounds = sc.out;
+  }
   // (3) W in fragment order, then the reverse walk of every segment; each
   //     starts from a zero cotangent except the last (dstate_out)
   slim::WfragArgs wf;
@@ -574,7 +617,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.W = W;
   a.Wfrag = wf.out;
   a.kshift = favor ? kshift : nullptr;
-  a.bounds = sc.out;
+  a.bounds = bounds;
   a.bound_stride = P2 + 1;
   a.bound_step = S2;
   a.dstate_out = dstate_out;

@@ -61,9 +61,11 @@ def _load() -> ctypes.CDLL:
     lib.slim_num_segments.restype = i32
     lib.slim_featmap.argtypes = [P, vp, fp, i32, fp, fp, vp]
     lib.slim_featmap.restype = i32
-    lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, vp, sz, vp]
+    lib.slim_context_bytes.argtypes = [P]
+    lib.slim_context_bytes.restype = sz
+    lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, vp, sz, vp]
     lib.slim_fwd.restype = i32
-    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, fp, vp, vp, vp, fp, fp, vp, sz, vp]
+    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, fp, vp, vp, vp, fp, fp, fp, vp, sz, vp]
     lib.slim_bwd.restype = i32
     lib.slim_status_string.argtypes = [i32]
     lib.slim_status_string.restype = ctypes.c_char_p
@@ -78,6 +80,7 @@ LIB = _load()
 
 EXPORTED = (
     "slim_workspace_bytes",
+    "slim_context_bytes",
     "slim_featmap",
     "slim_fwd",
     "slim_bwd",
@@ -136,6 +139,17 @@ def workspace_bytes(p: Problem, phase: int) -> int:
     return int(n)
 
 
+def context_bytes(p: Problem) -> int:
+    """Bytes of the forward-to-backward context (0: the problem uses none)."""
+    return int(LIB.slim_context_bytes(ctypes.byref(p)))
+
+
+def new_context(Q: torch.Tensor, W: torch.Tensor, C: int, kind="favor+", relu_eps: float = 1e-3):
+    """A context buffer for fwd(..., ctx=) and bwd(..., ctx=), or None when the problem uses none."""
+    n = context_bytes(_problem_of(Q, W, C, kind, relu_eps))
+    return None if n == 0 else torch.empty(n // 4, dtype=torch.float32, device=Q.device)
+
+
 def num_segments(p: Problem) -> int:
     return int(LIB.slim_num_segments(ctypes.byref(p)))
 
@@ -173,9 +187,18 @@ def featmap(X: torch.Tensor, W: torch.Tensor, role: int, kind="favor+", relu_eps
     return phi, shift
 
 
+def _need_ctx(p: Problem, ctx: Optional[torch.Tensor]):
+    if ctx is None:
+        return
+    _need(ctx, "ctx", torch.float32)
+    if ctx.numel() * 4 < LIB.slim_context_bytes(ctypes.byref(p)):
+        raise ValueError("ctx is smaller than slim_context_bytes")
+
+
 def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3, ws=None,
-        Y=None, state_out=None, kshift_out=None):
-    """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None)."""
+        Y=None, state_out=None, kshift_out=None, ctx=None):
+    """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None).
+    ctx (optional, from new_context) receives the segment boundary states for bwd."""
     p = _problem_of(Q, W, C, kind, relu_eps)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V)):
@@ -191,15 +214,18 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
     state_out = torch.empty(sshape, dtype=torch.float32, device=dev) if state_out is None else state_out
     if p.kind == FAVOR_PLUS and kshift_out is None:
         kshift_out = torch.empty((p.B, p.H), dtype=torch.float32, device=dev)
+    _need_ctx(p, ctx)
     ws = _workspace(p, PHASE_FWD, dev, ws)
     _check(LIB.slim_fwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
-                        _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ws), ws.numel(), _stream()))
+                        _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _ptr(ws), ws.numel(), _stream()))
     return Y, state_out, kshift_out
 
 
 def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshift_in=None, dstate_out=None,
-        want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None):
-    """Backward sweep; kshift is the forward's kshift_out (FAVOR+).
+        want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None,
+        ctx=None):
+    """Backward sweep; kshift is the forward's kshift_out (FAVOR+); ctx (optional)
+    is the context the forward wrote for the same inputs.
 
     Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
     p = _problem_of(Q, W, C, kind, relu_eps)
@@ -220,8 +246,9 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
     dV = torch.empty_like(V) if dV is None else dV
     dW = torch.empty((p.M, p.d), dtype=torch.float32, device=dev) if dW is None else dW
     dstate_in = torch.empty(sshape, dtype=torch.float32, device=dev) if want_dstate_in else None
+    _need_ctx(p, ctx)
     ws = _workspace(p, PHASE_BWD, dev, ws)
     _check(LIB.slim_bwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
                         _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
-                        _ptr(dW), _ptr(dstate_in), _ptr(ws), ws.numel(), _stream()))
+                        _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), ws.numel(), _stream()))
     return dQ, dK, dV, dW, dstate_in

@@ -54,6 +54,20 @@ def test_workspace_is_flat_in_L(S):
     assert S.num_segments(_p(S, L=32768)) == S.num_segments(_p(S, L=1 << 21)) > 1
 
 
+def test_context_is_state_sized_and_flat_in_L(S):
+    """The forward-to-backward context holds P2 + 1 boundary states per head:
+    its size depends on B H, M, d and the device, not on L."""
+    sizes = [S.context_bytes(_p(S, L=L)) for L in (32768, 262144, 1 << 21)]
+    assert len(set(sizes)) == 1 and sizes[0] > 0
+    per_state = 256 * 65 * 4
+    assert sizes[0] % (2 * 3 * per_state) == 0
+    # bf16 problems on the key-sum kernel only; fp32 problems and unsegmented
+    # sequences use none
+    assert S.context_bytes(_p(S, dtype=S.F32, d=32, M=64)) == 0
+    assert S.context_bytes(_p(S, L=64)) == 0
+    assert S.context_bytes(_p(S, C=0)) == 0
+
+
 @pytest.mark.parametrize(
     "kw, code",
     [
@@ -73,7 +87,7 @@ def test_invalid_problems_are_rejected(S, kw, code):
     p = _p(S, **kw)
     assert S.LIB.slim_workspace_bytes(ctypes.byref(p), 0) == 0
     assert S.LIB.slim_num_segments(ctypes.byref(p)) == 0
-    st = S.LIB.slim_fwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, 1, 1, 1, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, 1, 1, None, 1, 1 << 30, None)
     assert st == code
     assert S.LIB.slim_last_error().decode()
 
@@ -85,23 +99,23 @@ A = 1 << 12
 def test_null_pointers_are_rejected_before_any_launch(S):
     p = _p(S)
     # arguments: p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ws, ws_bytes, stream
-    st = S.LIB.slim_fwd(ctypes.byref(p), None, A, A, A, None, None, A, A, A, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), None, A, A, A, None, None, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # FAVOR+ needs a key-shift output
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # a state without its shift
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, A, None, A, A, A, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, A, None, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # arguments: p, Q, K, V, W, state_in, kshift_in, kshift, dY, dstate_out, dQ, dK, dV, dW, dstate_in,
     # ws, ws_bytes, stream
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, A, A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # dQ missing
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, A, A, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, A, A, A, A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # kshift missing (FAVOR+)
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, A, A, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, A, A, A, A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # state_in without kshift_in
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, A, A, A, None, A, 0, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, A, A, A, None, None, A, 0, None)
     assert st == S.SLIM_EWORKSPACE
     st = S.LIB.slim_featmap(ctypes.byref(p), None, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL
@@ -112,13 +126,13 @@ def test_null_pointers_are_rejected_before_any_launch(S):
 def test_misaligned_tensors_are_rejected_before_any_launch(S):
     p = _p(S)
     # a row tensor (dY) 8 bytes off a 16-byte boundary
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, A, A, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, A, A, A, A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
     # the workspace
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A, A + 4, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A, None, A + 4, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # a float tensor (W) off a 4-byte boundary
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A + 2, None, None, A, A, A, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A + 2, None, None, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     st = S.LIB.slim_featmap(ctypes.byref(p), A + 8, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL
