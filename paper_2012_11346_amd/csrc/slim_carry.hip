@@ -177,30 +177,36 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
       for (int st = 0; st < RT; ++st) {
         const bool col_ok = 16 * st + L.c < count;
         f32x4 kt[MT];
-        const float init = (G::KIND == kFavor) ? -0.5f * kn[16 * st + L.c] : 0.f;
+        // exponent offset of the column's key row, the row term -|k|^2/2
+        // included; rows past the block: infinite (features exactly zero)
+        const float kc = (G::KIND == kFavor) ? (col_ok ? koff + 0.5f * kLog2e * kn[16 * st + L.c] : INFINITY) : 0.f;
+        F kfr[EB];
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) kfr[kb] = frag_rm(L, Ks, LDQ, 16 * st, 32 * kb);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          f32x4 acc = {init, init, init, init};
+          f32x4 acc = zero4();
 #pragma unroll
-          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(L, Ks, LDQ, 16 * st, 32 * kb));
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], kfr[kb]);
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            acc[r] = !col_ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(acc[r] * kLog2e - koff) : fmaxf(acc[r], 0.f) + a.relu_eps;
+            acc[r] = (G::KIND == kFavor) ? fast_exp2(acc[r] * kLog2e - kc) : (col_ok ? fmaxf(acc[r], 0.f) + a.relu_eps : 0.f);
           kt[mt] = acc;
           store_tile_T<T>(L, Kt, LDK, acc, w * FW + 16 * mt, 16 * st);
         }
         // dK~^T[m][s] = sum_e G[m][e] V[s][e] + z-cotangent[m]; Pk^T = dK~^T . K~^T (FAVOR+) or masked (ReLU)
+        // (columns past the block have K~ = 0, hence Pk = 0)
         float sum = 0.f;
+        F vfr[EB];
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) vfr[kb] = frag_rm(L, Vs, LDQ, 16 * st, 32 * kb);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          f32x4 acc = zero4();
-          if (col_ok) {
+          f32x4 acc;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) acc[r] = *(const float*)&Gs[(w * FW + 16 * mt + 4 * L.g + r) * LDG + D];
-          }
+          for (int r = 0; r < 4; ++r) acc[r] = *(const float*)&Gs[(w * FW + 16 * mt + 4 * L.g + r) * LDG + D];
 #pragma unroll
-          for (int kb = 0; kb < EB; ++kb)
-            acc = mma(acc, frag_rm(L, Gs, LDG, w * FW + 16 * mt, 32 * kb), frag_rm(L, Vs, LDQ, 16 * st, 32 * kb));
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, frag_rm(L, Gs, LDG, w * FW + 16 * mt, 32 * kb), vfr[kb]);
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             acc[r] = (G::KIND == kFavor) ? acc[r] * kt[mt][r] : (kt[mt][r] > a.relu_eps ? acc[r] : 0.f);

@@ -47,19 +47,18 @@ __device__ __forceinline__ typename FragT<typename G::T>::type v_frag(const Lane
   return f;
 }
 
-// Query logits, transposed: Lq[mt][tt] holds rows m (features of this wave),
-// columns t.  The accumulator starts at -|q_t|^2/2 for FAVOR+.
+// Query logits w_m . q_t, transposed: Lq[mt][tt] holds rows m (features of
+// this wave), columns t.  (The FAVOR+ term -|q_t|^2/2 cancels against the
+// query row shift, so it is never formed.)
 template <class G>
 __device__ __forceinline__ void query_logits(const Lane& L, f32x4 (&Lq)[G::MT][G::RT],
                                              const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
-                                             const typename G::T* Qs, const float* qn) {
-  const int c = L.c;
+                                             const typename G::T* Qs) {
 #pragma unroll
   for (int tt = 0; tt < G::RT; ++tt) {
-    const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
 #pragma unroll
     for (int mt = 0; mt < G::MT; ++mt) {
-      f32x4 acc = {init, init, init, init};
+      f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(L, Qs, G::LDQ, 16 * tt, 32 * kb));
       Lq[mt][tt] = acc;
@@ -67,22 +66,22 @@ __device__ __forceinline__ void query_logits(const Lane& L, f32x4 (&Lq)[G::MT][G
   }
 }
 
-// Key logits: Lk[st][mt] holds rows s, columns m (features of this wave).
+// Key logits w_m . k_s: Lk[st][mt] holds rows s, columns m (features of this
+// wave).  The FAVOR+ row term -|k_s|^2/2 enters with the exponent.
 template <class G>
 __device__ __forceinline__ void key_logits(const Lane& L, f32x4 (&Lk)[G::RT][G::MT],
                                            const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
-                                           const typename G::T* Ks, const float* kn) {
-  const int g = L.g;
+                                           const typename G::T* Ks) {
 #pragma unroll
   for (int st = 0; st < G::RT; ++st) {
-    f32x4 init;
+    typename FragT<typename G::T>::type kf[G::EB];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) init[r] = (G::KIND == kFavor) ? -0.5f * kn[16 * st + 4 * g + r] : 0.f;
+    for (int kb = 0; kb < G::EB; ++kb) kf[kb] = frag_rm(L, Ks, G::LDQ, 16 * st, 32 * kb);
 #pragma unroll
     for (int mt = 0; mt < G::MT; ++mt) {
-      f32x4 acc = init;
+      f32x4 acc = zero4();
 #pragma unroll
-      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, frag_rm(L, Ks, G::LDQ, 16 * st, 32 * kb), Wf[mt][kb]);
+      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, kf[kb], Wf[mt][kb]);
       Lk[st][mt] = acc;
     }
   }
@@ -106,7 +105,8 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) T Vbuf[2 * TQ];
   __shared__ __attribute__((aligned(16))) T Zk[4][QSIDE ? ZR * LDZ : 8];
   __shared__ __attribute__((aligned(16))) float Red[4][QSIDE ? TR * LDR : 4];
-  __shared__ float qnb[2][TR], knb[2][TR], qmx[4][TR], kmx[4];
+  __shared__ __attribute__((aligned(16))) float knb[2][TR];  // key row norms, read as 16-byte vectors
+  __shared__ float qmx[4][TR], kmx[4];
 
   const int w = wave_id(), g = lane_g(), c = lane_c();
   const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -169,7 +169,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     sv.fetch(Vh + (size_t)s0 * D, n0, tid);
   };
   auto store_q = [&](int bf) {
-    if constexpr (QSIDE) sq.template store<LDQ>(Qbuf, G::KIND == kFavor ? qnb[bf] : nullptr, fresh_tid());
+    if constexpr (QSIDE) sq.template store<LDQ>(Qbuf, nullptr, fresh_tid());
   };
   auto store_kv = [&](int bf) {
     const int tid = fresh_tid();
@@ -194,12 +194,11 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     const T* Qs = Qbuf;
     const T* Ks = Kbuf + bf * TQ;
     const T* Vs = Vbuf + bf * TQ;
-    const float* qn = qnb[bf];
     const float* kn = knb[bf];
 
     f32x4 Lq[QSIDE ? MT : 1][RT], Lk[RT][MT];
-    if constexpr (QSIDE) query_logits<G>(L, Lq, Wf, Qs, qn);
-    key_logits<G>(L, Lk, Wf, Ks, kn);
+    if constexpr (QSIDE) query_logits<G>(L, Lq, Wf, Qs);
+    key_logits<G>(L, Lk, Wf, Ks);
 
     if (G::KIND == kFavor) {
       if constexpr (QSIDE) {
@@ -219,10 +218,12 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
         for (int st = 0; st < RT; ++st)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
+          for (int r = 0; r < 4; ++r) {
+            float u = -INFINITY;
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (16 * st + 4 * g + r < count) v = fmaxf(v, Lk[st][mt][r]);
+            for (int mt = 0; mt < MT; ++mt) u = fmaxf(u, Lk[st][mt][r]);
+            if (16 * st + 4 * g + r < count) v = fmaxf(v, u - 0.5f * kn[16 * st + 4 * g + r]);
+          }
         v = wave_max(v);
         if ((fresh_tid() & 63) == 0) kmx[w] = v;
       }
@@ -253,24 +254,29 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
           cur = km;
         }
       }
+      // exponent offsets of the key rows (row term included); rows past the
+      // tile: infinite, so their features are exactly zero
       const float koff = cur * kLog2e + half_log2M;
 #pragma unroll
-      for (int st = 0; st < RT; ++st)
+      for (int st = 0; st < RT; ++st) {
+        const f32x4 knv = *(const f32x4*)&kn[16 * st + 4 * g];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int r = 0; r < 4; ++r) {
+          const float kc = 16 * st + 4 * g + r < count ? koff + 0.5f * kLog2e * knv[r] : INFINITY;
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? fast_exp2(Lk[st][mt][r] * kLog2e - koff) : 0.f;
+          for (int mt = 0; mt < MT; ++mt) Lk[st][mt][r] = fast_exp2(Lk[st][mt][r] * kLog2e - kc);
+        }
+      }
       if constexpr (QSIDE) {
 #pragma unroll
         for (int tt = 0; tt < RT; ++tt) {
           const int t = 16 * tt + c;
           const float qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t])) * kLog2e;
+          // (rows past the tile get finite features; their outputs are not stored)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              Lq[mt][tt][r] = (t < count) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs) : 0.f;
+            for (int r = 0; r < 4; ++r) Lq[mt][tt][r] = fast_exp2(Lq[mt][tt][r] * kLog2e - qs);
         }
       }
     } else {
@@ -287,8 +293,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              Lq[mt][tt][r] = (16 * tt + c < count) ? fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps : 0.f;
+            for (int r = 0; r < 4; ++r) Lq[mt][tt][r] = fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
       }
     }
 
@@ -440,14 +445,16 @@ __global__ __launch_bounds__(256, 1) void key_shift_kernel(FeatArgs a) {
     load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, kn);
     __syncthreads();
     f32x4 Lk[RT][MT];
-    key_logits<G>(this_lane(), Lk, Wf, Ks, kn);
+    key_logits<G>(this_lane(), Lk, Wf, Ks);
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (16 * st + 4 * g + r < count) best = fmaxf(best, Lk[st][mt][r]);
+        for (int r = 0; r < 4; ++r) {
+          const int s = 16 * st + 4 * g + r;
+          if (s < count) best = fmaxf(best, Lk[st][mt][r] - 0.5f * kn[s]);
+        }
     __syncthreads();
   }
   best = wave_max(best);
@@ -477,7 +484,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
   const float half_log2M = 0.5f * __log2f((float)M);
   if (a.role == 0) {
     f32x4 Lq[MT][RT];
-    query_logits<G>(this_lane(), Lq, Wf, Xs, xn);
+    query_logits<G>(this_lane(), Lq, Wf, Xs);
     if (G::KIND == kFavor) {
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
@@ -498,7 +505,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
       float qs = 0.f;
       if (G::KIND == kFavor) {
         qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t]));
-        if (w == 0 && g == 0 && a.shift != nullptr) a.shift[head * a.L + start + t] = qs;
+        if (w == 0 && g == 0 && a.shift != nullptr) a.shift[head * a.L + start + t] = qs - 0.5f * xn[t];
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -512,7 +519,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
     }
   } else {
     f32x4 Lk[RT][MT];
-    key_logits<G>(this_lane(), Lk, Wf, Xs, xn);
+    key_logits<G>(this_lane(), Lk, Wf, Xs);
     const float ks = (G::KIND == kFavor) ? a.shift[head] : 0.f;
 #pragma unroll
     for (int st = 0; st < RT; ++st)
@@ -523,7 +530,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
           const int s = 16 * st + 4 * g + r;
           if (s >= count) continue;
           const int m = w * FW + 16 * mt + c;
-          const float x = Lk[st][mt][r];
+          const float x = Lk[st][mt][r] - (G::KIND == kFavor ? 0.5f * xn[s] : 0.f);
           Ph[(size_t)(start + s) * M + m] =
               (G::KIND == kFavor) ? fast_exp2((x - ks) * kLog2e - half_log2M) : fmaxf(x, 0.f) + a.relu_eps;
         }

@@ -38,7 +38,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
 
   __shared__ __attribute__((aligned(16))) T Kb[2 * TQ];
   __shared__ __attribute__((aligned(16))) T Vb[SUMS ? 2 * TQ : 8];
-  __shared__ float knb[2][CR];
+  __shared__ __attribute__((aligned(16))) float knb[2][CR];  // key row norms, read as 16-byte vectors
   __shared__ float wmax[4];
 
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
