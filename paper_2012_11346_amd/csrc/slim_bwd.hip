@@ -627,16 +627,25 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 // dW[m][e] = sum over workgroups of the partials, in a fixed order: a block
 // covers 64 entries; its 4 thread groups sum interleaved quarters of the
 // partials, then the 4 group sums are added in group order
-__global__ __launch_bounds__(256) void dw_reduce_kernel(const float* part, int nparts, int n, float* dW) {
-  __shared__ float acc[4][64];
+// dW = sum of the n_parts partials [n_parts][n] in a fixed order: block b
+// takes 64 groups of 4 consecutive entries (16-byte loads); its 16 waves sum
+// every 16th partial each, and the 16 wave sums are added in wave order.
+__global__ __launch_bounds__(1024) void dw_reduce_kernel(const float* part, int nparts, int n, float* dW) {
+  __shared__ f32x4 acc[16][64];
   const int e = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int i = blockIdx.x * 64 + e;
-  float s = 0.f;
+  const int i = (blockIdx.x * 64 + e) * 4;  // n is a multiple of 4
+  f32x4 s = zero4();
   if (i < n)
-    for (int k = q; k < nparts; k += 4) s += part[(size_t)k * n + i];
+    for (int k = q; k < nparts; k += 16) s += *(const f32x4*)&part[(size_t)k * n + i];
   acc[q][e] = s;
   __syncthreads();
-  if (q == 0 && i < n) dW[i] = (acc[0][e] + acc[1][e]) + (acc[2][e] + acc[3][e]);
+  if (q == 0 && i < n) {
+    f32x4 t = acc[0][e];
+#pragma unroll
+    for (int j = 1; j < 16; ++j) t += acc[j][e];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dW[i + j] = t[j];  // dW is only 4-byte aligned
+  }
 }
 
 template <class G>
@@ -646,7 +655,7 @@ hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s) {
-  hipLaunchKernelGGL(dw_reduce_kernel, dim3((n + 63) / 64), dim3(256), 0, s, part, n_parts, n, dW);
+  hipLaunchKernelGGL(dw_reduce_kernel, dim3((n / 4 + 63) / 64), dim3(1024), 0, s, part, n_parts, n, dW);
   return hipGetLastError();
 }
 
