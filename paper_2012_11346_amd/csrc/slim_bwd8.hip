@@ -318,18 +318,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      logits of this wave's 16 rows; K~ -> Zk[m][s]
     f32x4 Lq[MT][RT];
     {
-      // rows of the next tile, stored into LDS at the end of this one; issued
-      // after the W fragments so that waiting for those does not wait for
-      // these.  Range-checked loads without branches (an empty range after
-      // the last tile) keep the count of outstanding loads exact.
-      {
-        const int st2 = fresh_tid() & 255;
-        int sn, cn;
-        tm.tile(j > j0 ? j - 1 : j, sn, cn);
-        const size_t nb = j > j0 ? (size_t)cn * D * sizeof(T) : 0;
-        stA.fetch(range_rsrc(srcA + (size_t)sn * D, nb), 0, st2);
-        stB.fetch(range_rsrc(srcB + (size_t)sn * D, nb), 0, st2);
-      }
       // raw logits w.q: the query row shift max_m(w.q - |q|^2/2) absorbs the norm term
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
@@ -597,6 +585,20 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int kb = 0; kb < MB; ++kb)
 #pragma unroll
       for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
+    // rows of the next tile, stored into LDS at the end of this one; issued
+    // after the W fragments so that waiting for those does not wait for
+    // these, and half a tile ahead of the logits' W fragments (fetched at the
+    // end of the tile), so that those do not queue behind them.  Range-checked
+    // loads without branches (an empty range after the last tile) keep the
+    // count of outstanding loads exact.
+    {
+      const int st2 = fresh_tid() & 255;
+      int sn, cn;
+      tm.tile(j > j0 ? j - 1 : j, sn, cn);
+      const size_t nb = j > j0 ? (size_t)cn * D * sizeof(T) : 0;
+      stA.fetch(range_rsrc(srcA + (size_t)sn * D, nb), 0, st2);
+      stB.fetch(range_rsrc(srcB + (size_t)sn * D, nb), 0, st2);
+    }
     {
       const float ddt = dDs[16 * h + c];
 #pragma unroll
