@@ -314,20 +314,20 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     u32e dv_hold;
     F Wb[MB][EH];  // W fragments of the dq and dk products
 
-    // ---- features: Q logits of the whole tile (both waves of the pair), K
-    //      logits of this wave's 16 rows; K~ -> Zk[m][s]
-    f32x4 Lq[MT][RT];
+    // ---- features: Q and K logits of this wave's 16 rows (the pair splits
+    //      the tile's rows); K~ -> Zk[m][s], row maxima of the query logits -> qmx
+    f32x4 Lq[MT];  // rows m, columns t = 16 h + c
     {
       // raw logits w.q: the query row shift max_m(w.q - |q|^2/2) absorbs the norm term
+      F qfr[EB];
 #pragma unroll
-      for (int tt = 0; tt < RT; ++tt) {
+      for (int kb = 0; kb < EB; ++kb) qfr[kb] = sfrag_rm(oR, Qs, 16 * h, 32 * kb);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          f32x4 acc = zero4();
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4 acc = zero4();
 #pragma unroll
-          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], sfrag_rm(oR, Qs, 16 * tt, 32 * kb));
-          Lq[mt][tt] = acc;
-        }
+        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], qfr[kb]);
+        Lq[mt] = acc;
       }
       // key rows: exp2(log2e (w.k - |k|^2/2 - shift) - log2(M)/2), the row term folded into the exponent
       // (rows past the tile: an infinite offset gives exactly zero features)
@@ -360,16 +360,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         sstore_tile_T(oK, Zk, kv, 16 * h, 16 * mt);
       }
       if (G::KIND == kFavor) {
+        float v = -INFINITY;
 #pragma unroll
-        for (int tt = 0; tt < RT; ++tt) {
-          float v = -INFINITY;
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
-          v = wave_max_over_g(v);
-          if (g == 0) qmx[f * TR + 16 * tt + c] = v;
-        }
+          for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][r]);
+        v = wave_max_over_g(v);
+        if (g == 0) qmx[f * TR + 16 * h + c] = v;
       }
     }
     __syncthreads();
@@ -381,32 +378,26 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // dk of the previous tile (an empty range before the first)
     store_piece(dk_hold, dk_rs, dk_off);
 
-    // ---- Q~ -> Zq[t][m] (identical copies from both waves of the pair); the
-    //      features stay in registers as operands of the scores and of N.
-    //      Rows past the tile (zero in LDS) get finite features and need no
-    //      mask: their dN, dD are zero, so they add nothing to G, dA, P or dW.
-#pragma unroll
-    for (int tt = 0; tt < RT; ++tt) {
-      const int t = 16 * tt + c;
+    // ---- Q~ of this wave's 16 rows -> Zq[t][m].  Rows past the tile (zero
+    //      in LDS) get finite features and need no mask: their dN, dD are
+    //      zero, so they add nothing to G, dA, P or dW.
+    {
+      const int t = 16 * h + c;
       float qs = 0.f;
       if (G::KIND == kFavor) qs = fmaxf(fmaxf(qmx[t], qmx[TR + t]), fmaxf(qmx[2 * TR + t], qmx[3 * TR + t])) * kLog2e;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          Lq[mt][tt][r] = (G::KIND == kFavor) ? fast_exp2(Lq[mt][tt][r] * kLog2e - qs)
-                                              : fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
+          Lq[mt][r] = (G::KIND == kFavor) ? fast_exp2(Lq[mt][r] * kLog2e - qs) : fmaxf(Lq[mt][r], 0.f) + a.relu_eps;
+      }
+#pragma unroll
+      for (int kb = 0; kb < MB; ++kb) {
+        const F q = tile_pair_frag<T>(Lq[2 * kb], Lq[2 * kb + 1]);
+        sstore_half_T(oF, Zq, frag_lo(q), 32 * kb, 16 * h);
+        sstore_half_T(oF, Zq, frag_hi(q), 32 * kb + 16, 16 * h);
       }
     }
-    F qf[MB][RT];  // Q~ contracting over this slice's features, columns t (rounded once, also -> Zq)
-#pragma unroll
-    for (int kb = 0; kb < MB; ++kb)
-#pragma unroll
-      for (int tt = 0; tt < RT; ++tt) {
-        qf[kb][tt] = tile_pair_frag<T>(Lq[2 * kb][tt], Lq[2 * kb + 1][tt]);
-        sstore_half_T(oF, Zq, frag_lo(qf[kb][tt]), 32 * kb, 16 * tt);
-        sstore_half_T(oF, Zq, frag_hi(qf[kb][tt]), 32 * kb + 16, 16 * tt);
-      }
 
     // ---- state before the tile: downdate (eq. 17), or the exact segment start
     if (j == jreset) {
@@ -440,6 +431,17 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         Sz[mt] = mma(Sz[mt], kf, ones);
       }
     }
+
+    __syncthreads();  // both halves of Q~ in Zq
+    L = fresh_lane();
+    g = L.g;
+    c = L.c;
+    fresh_offsets();
+    F qf[MB][RT];  // Q~ contracting over this slice's features, columns t
+#pragma unroll
+    for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) qf[kb][tt] = sfrag_rm(oF, Zq, 16 * tt, 32 * kb);
 
     // ---- scores A^T[s][t] over this slice's features, causal -> ZA[t][s] (for dV)
     f32x4 At[RT][RT];
