@@ -204,6 +204,21 @@ __device__ __forceinline__ void store_tile_T(T* Z, int ld, const f32x4& x, int r
   store_tile_T(this_lane(), Z, ld, x, row0, col0);
 }
 
+// halves of an operand fragment built by tile_pair_frag (the rounded values
+// of its first and second result tile)
+__device__ __forceinline__ bf16x4 frag_lo(const bf16x8& f) { return __builtin_shufflevector(f, f, 0, 1, 2, 3); }
+__device__ __forceinline__ bf16x4 frag_hi(const bf16x8& f) { return __builtin_shufflevector(f, f, 4, 5, 6, 7); }
+__device__ __forceinline__ f32x4 frag_lo(const f32x8& f) { return __builtin_shufflevector(f, f, 0, 1, 2, 3); }
+__device__ __forceinline__ f32x4 frag_hi(const f32x8& f) { return __builtin_shufflevector(f, f, 4, 5, 6, 7); }
+
+// store_tile_T of values already rounded (half of an operand fragment)
+__device__ __forceinline__ void store_half_T(const Lane& L, bf16* Z, int ld, const bf16x4& v, int row0, int col0) {
+  *(bf16x4*)(Z + (col0 + L.c) * ld + row0 + 4 * L.g) = v;
+}
+__device__ __forceinline__ void store_half_T(const Lane& L, float* Z, int ld, const f32x4& v, int row0, int col0) {
+  *(f32x4*)(Z + (col0 + L.c) * ld + row0 + 4 * L.g) = v;
+}
+
 // two stacked result tiles as an operand (has_b), or the first one with the
 // second 16 entries of the 32-deep block zero
 template <typename T>
@@ -361,9 +376,6 @@ template <int P, int MODE>
 __device__ __forceinline__ void sstore_half_T(const SwzLane<P, MODE>& o, bf16* Z, const bf16x4& v, int row0, int col0) {
   *(bf16x4*)(Z + o.a + col0 * P + row0) = v;
 }
-__device__ __forceinline__ bf16x4 frag_lo(const bf16x8& f) { return __builtin_shufflevector(f, f, 0, 1, 2, 3); }
-__device__ __forceinline__ bf16x4 frag_hi(const bf16x8& f) { return __builtin_shufflevector(f, f, 4, 5, 6, 7); }
-
 // X[row0 + 4g + r][col0 + c] of a tile stored transposed by sstore_tile_T
 template <int P, int MODE>
 __device__ __forceinline__ f32x4 sload_tile_T(const SwzLane<P, MODE>& o, const bf16* Z, int row0, int col0) {

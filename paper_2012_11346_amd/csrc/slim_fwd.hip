@@ -160,13 +160,17 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   // finished before tile j - 1's last barrier) and become visible at tile j's
   // barriers.
   RowStage<T, D, TR, 256> sq, sk, sv;
+  // range-checked loads without branches (an empty range past the last
+  // tile), so that waits for them count exactly and never include the
+  // output stores issued after them
   auto fetch = [&](int jj) {
     int s0, n0;
-    tm.tile(jj, s0, n0);
+    tm.tile(min(jj, j1 - 1), s0, n0);
+    const size_t nb = jj < j1 ? (size_t)n0 * D * sizeof(T) : 0;
     const int tid = fresh_tid();
-    if constexpr (QSIDE) sq.fetch(Qh + (size_t)s0 * D, n0, tid);
-    sk.fetch(Kh + (size_t)s0 * D, n0, tid);
-    sv.fetch(Vh + (size_t)s0 * D, n0, tid);
+    if constexpr (QSIDE) sq.fetch(range_rsrc(Qh + (size_t)s0 * D, nb), 0, tid);
+    sk.fetch(range_rsrc(Kh + (size_t)s0 * D, nb), 0, tid);
+    sv.fetch(range_rsrc(Vh + (size_t)s0 * D, nb), 0, tid);
   };
   auto store_q = [&](int bf) {
     if constexpr (QSIDE) sq.template store<LDQ>(Qbuf, nullptr, fresh_tid());
@@ -180,7 +184,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     fetch(j0);
     store_q(0);
     store_kv(0);
-    if (j0 + 1 < j1) fetch(j0 + 1);
+    fetch(j0 + 1);
   }
   __syncthreads();
 
@@ -237,10 +241,8 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
       c = L.c;
     }
     // queries of the next tile: every wave has read this tile's
-    if (j + 1 < j1) {
-      store_q(bf ^ 1);
-      if (j + 2 < j1) fetch(j + 2);
-    }
+    if (j + 1 < j1) store_q(bf ^ 1);
+    fetch(j + 2);
 
     if (G::KIND == kFavor) {
       if (!fixed) {
@@ -297,6 +299,14 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
       }
     }
 
+    // K~ contracting over the tile's rows, rounded once for the state update
+    // and (with queries) for the transposed copy the scores read
+    F kt[RB][MT];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) kt[rb][mt] = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
+
     F vf[RB][ET + 1];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
@@ -306,9 +316,12 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     if constexpr (QSIDE) {
       // keys transposed into this wave's buffer: Zk[m][s]
 #pragma unroll
-      for (int st = 0; st < RT; ++st)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) store_tile_T<T>(L, Zk[w], LDZ, Lk[st][mt], 16 * st, 16 * mt);
+        for (int mt = 0; mt < MT; ++mt) {
+          store_half_T(L, Zk[w], LDZ, frag_lo(kt[rb][mt]), 32 * rb, 16 * mt);
+          store_half_T(L, Zk[w], LDZ, frag_hi(kt[rb][mt]), 32 * rb + 16, 16 * mt);
+        }
 
       F qf[MB][RT];
 #pragma unroll
@@ -374,28 +387,36 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
       for (int et = 0; et <= ET; ++et)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
-          S[mt][et] = mma(S[mt][et], tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]), vf[rb][et]);
+          S[mt][et] = mma(S[mt][et], kt[rb][mt], vf[rb][et]);
 
     __syncthreads();
     if constexpr (QSIDE) {
       // Y = N / D over all features (vector reads of the reduction rows)
       static_assert(EPT % 4 == 0, "");
+      // (rows past the tile are computed and dropped by the range-checked
+      // stores: no branch, so later waits count exactly)
       const int tid = fresh_tid();
       const int t = tid / TPR, q = tid % TPR;
-      if (t < count) {
-        const float inv = 1.f / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
-        typedef T tvec __attribute__((ext_vector_type(EPT)));
-        tvec o;
+      const float inv = 1.f / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
+      typedef T tvec __attribute__((ext_vector_type(EPT)));
+      tvec o;
 #pragma unroll
-        for (int h4 = 0; h4 < EPT / 4; ++h4) {
-          const int idx = t * LDR + q * EPT + 4 * h4;
-          const f32x4 n = (*(const f32x4*)&Red[0][idx] + *(const f32x4*)&Red[1][idx]) +
-                          (*(const f32x4*)&Red[2][idx] + *(const f32x4*)&Red[3][idx]);
+      for (int h4 = 0; h4 < EPT / 4; ++h4) {
+        const int idx = t * LDR + q * EPT + 4 * h4;
+        const f32x4 n = (*(const f32x4*)&Red[0][idx] + *(const f32x4*)&Red[1][idx]) +
+                        (*(const f32x4*)&Red[2][idx] + *(const f32x4*)&Red[3][idx]);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[4 * h4 + i] = cvt<T>(n[i] * inv);
-        }
-        *(tvec*)((T*)a.Y + head * (size_t)a.L * D + (size_t)(start + t) * D + q * EPT) = o;
+        for (int i = 0; i < 4; ++i) o[4 * h4 + i] = cvt<T>(n[i] * inv);
       }
+      const __amdgpu_buffer_rsrc_t ry =
+          range_rsrc((T*)a.Y + head * (size_t)a.L * D + (size_t)start * D, (size_t)count * D * sizeof(T));
+      constexpr int PB = sizeof(tvec) >= 16 ? 16 : (int)sizeof(tvec);  // bytes per store (8 or 16)
+      constexpr int NV = (int)(sizeof(tvec) / PB);
+      static_assert(sizeof(tvec) % PB == 0 && (PB == 8 || PB == 16), "8- or 16-byte pieces");
+      typedef unsigned pvec __attribute__((ext_vector_type(PB / 4)));
+      const pvec* ov = (const pvec*)&o;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) BufIO<PB>::store(ov[v], ry, ((t * D + q * EPT) * (int)sizeof(T)) + PB * v);
     }
   }
 
