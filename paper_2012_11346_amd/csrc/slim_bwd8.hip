@@ -131,7 +131,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   char* pz = arena + Lay::oP + f * Lay::PAIR;
   T* Zk = (T*)(pz + Lay::pZk);     // K~ as [m][s]
   T* Zq = (T*)(pz + Lay::pZq);     // Q~ as [t][m]
-  T* ZdA = (T*)(pz + Lay::pZdA);  // dA^T as [t][s]
+  // dA^T as [t][s]: one copy for the workgroup (in pair 0's block); its
+  // upper-right quarter (s in [16, 32), t in [0, 16)) is never written and
+  // stays zero from the initial fill
+  T* ZdA = (T*)(arena + Lay::oP + Lay::pZdA);
   T* ZA = (T*)(pz + Lay::pX);      // A^T as [t][s]
   T* ZS = ZA;                                       // S as [e][m]
   T* ZPk = ZA;                                      // Pk as [m][s]
@@ -521,24 +524,23 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal -> ZdA[t][s]; a row s
-    //      past the tile has V[s] = 0 and is reached only from rows t >= s, whose dD is zero
-#pragma unroll
-    for (int tt = 0; tt < RT; ++tt) {
+    // ---- dA^T[s][t] = sum_e V[s][e] dN[t][e] + dD[t], causal -> ZdA[t][s], once per
+    //      workgroup: wave 0 takes the tile (s, t) in ([0,16), [0,16)), wave 1
+    //      ([0,16), [16,32)), wave 2 ([16,32), [16,32)).  A row s past the tile has
+    //      V[s] = 0 and is reached only from rows t >= s, whose dD is zero.
+    if (w < 3) {
+      const int st = w >> 1, tt = (w + 1) >> 1;
       const float ddt = dDs[16 * tt + c];
+      f32x4 acc = f32x4{ddt, ddt, ddt, ddt};
 #pragma unroll
-      for (int st = 0; st <= tt; ++st) {
-        f32x4 acc = f32x4{ddt, ddt, ddt, ddt};
+      for (int kb = 0; kb < EB; ++kb)
+        acc = mma(acc, sfrag_rm(oR, Vs, 16 * st, 32 * kb), sfrag_rm(oR, dNs, 16 * tt, 32 * kb));
+      if (st == tt) {
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, sfrag_rm(oR, Vs, 16 * st, 32 * kb), sfrag_rm(oR, dNs, 16 * tt, 32 * kb));
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (st == tt && 4 * g + r > c) acc[r] = 0.f;
-        }
-        sstore_tile_T(oK, ZdA, acc, 16 * st, 16 * tt);
+        for (int r = 0; r < 4; ++r)
+          if (4 * g + r > c) acc[r] = 0.f;
       }
-      if (tt == 0) sstore_tile_T(oK, ZdA, zero4(), 16, 0);  // s in [16, 32) for t in [0, 16)
+      sstore_tile_T(oK, ZdA, acc, 16 * st, 16 * tt);
     }
     // dV^T[e][s] = sum_m G[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t], own columns -> RedY[s][e']
 #pragma unroll
