@@ -204,8 +204,23 @@ struct BwdLayout {
   size_t wfrag, seg_sum, bounds, gc, gend, dw_part, total;
 };
 size_t wfrag_bytes_of(const slim_problem* p);
+bool has_carry8(const slim_problem* p);
+// Workgroups of the 8-wave carry pass: one per compute unit, or one per
+// chunk when there are fewer chunks.  SLIM_CARRY_WORKGROUPS (debugging)
+// forces a smaller count, so that each workgroup's run crosses segments and
+// heads.
+int carry8_workgroups(const slim_problem* p, int P) {
+  if (P < 2) return 0;
+  const int64_t chunks = p->B * p->H * (int64_t)slim::carry8_chunks_per_head((int)p->L, clamp_C(p), P);
+  int64_t n = std::min<int64_t>(kTargetWorkgroups, chunks);
+  const char* env = getenv("SLIM_CARRY_WORKGROUPS");
+  if (env != nullptr && atoi(env) >= 1) n = std::min<int64_t>(n, atoi(env));
+  return (int)n;
+}
+// dW partials: one per (head, segment) from the walk, then the carry's
 size_t dw_slots(const slim_problem* p, int P) {
   const size_t heads = (size_t)p->B * p->H;
+  if (has_carry8(p)) return heads * P + carry8_workgroups(p, P);
   return heads * P + (P > 1 ? heads * (P - 1) * (plan_carry_split(p, P) - 1) : 0);
 }
 BwdLayout bwd_layout(const slim_problem* p, int P) {
@@ -248,6 +263,7 @@ struct Dispatch {
   wfrag_fn wfrag;
   size_fn wfrag_bytes;
   carry_fn carry;
+  carry_fn carry8;  // 8-wave carry pass (nullptr where not built)
   ksum_fn ksum;  // key sums of row ranges (nullptr where not built: the key-only walk serves)
 };
 
@@ -255,13 +271,15 @@ template <class T, int D, int FW, int KIND>
 Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
   return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>, nullptr,
-                  &slim::launch_wfrag<G>,    &slim::wfrag_bytes<G>,     &slim::launch_carry<G>,    nullptr};
+                  &slim::launch_wfrag<G>,    &slim::wfrag_bytes<G>,     &slim::launch_carry<G>,    nullptr,
+                  nullptr};
 }
 template <int D, int FW, int KIND>
 Dispatch make_dispatch8() {
   Dispatch d = make_dispatch<slim::bf16, D, FW, KIND>();
   d.bwd8 = &slim::launch_bwd_walk8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   d.ksum = &slim::launch_ksum<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
+  d.carry8 = &slim::launch_carry8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   return d;
 }
 
@@ -302,6 +320,7 @@ Dispatch dispatch(const slim_problem* p) {
 
 size_t wfrag_bytes_of(const slim_problem* p) { return dispatch(p).wfrag_bytes(); }
 bool has_ksum(const slim_problem* p) { return dispatch(p).ksum != nullptr; }
+bool has_carry8(const slim_problem* p) { return dispatch(p).carry8 != nullptr; }
 size_t context_bytes(const slim_problem* p) {
   if (!context_used(p)) return 0;
   return (size_t)p->B * p->H * (bwd_parts(p) + 1) * state_elems(p) * sizeof(float);
@@ -672,7 +691,13 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     ca.P = P;
     ca.CS = plan_carry_split(p, P);
     ca.relu_eps = p->relu_eps;
-    e = dp.carry(ca, s);
+    if (dp.carry8 != nullptr) {
+      ca.nch_head = slim::carry8_chunks_per_head(a.L, a.C, P);
+      ca.NWG = carry8_workgroups(p, P);
+      e = dp.carry8(ca, s);
+    } else {
+      e = dp.carry(ca, s);
+    }
     if (e != hipSuccess) return hip_fail(e, "carry launch");
   }
   // (5) dW: the workgroups' partials summed in a fixed order

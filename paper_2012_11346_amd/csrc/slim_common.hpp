@@ -109,8 +109,7 @@ __device__ __forceinline__ void load_rows(T* dst, const T* src, int count, float
         const float x = to_f32(e[i]);
         s += x * x;
       }
-#pragma unroll
-      for (int o = 1; o < CPR; o <<= 1) s += __shfl_xor(s, o, 64);
+      s = sum_lane_group<CPR>(s);
       if (active && cc == 0) norms[r] = s;
     }
   }
@@ -197,8 +196,7 @@ struct RowStage {
           const float x = to_f32(e[k]);
           s += x * x;
         }
-#pragma unroll
-        for (int o = 1; o < CPR; o <<= 1) s += __shfl_xor(s, o, 64);
+        s = sum_lane_group<CPR>(s);
         if (active && cc == 0) norms[r] = s;
       }
     }
@@ -219,8 +217,7 @@ struct RowStage {
           const float x = to_f32(e[k]);
           s += x * x;
         }
-#pragma unroll
-        for (int o = 1; o < CPR; o <<= 1) s += __shfl_xor(s, o, 64);
+        s = sum_lane_group<CPR>(s);
         if (active && cc == 0) norms[r] = s;
       }
     }

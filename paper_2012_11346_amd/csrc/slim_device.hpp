@@ -286,6 +286,26 @@ __device__ __forceinline__ float wave_sum_over_c(float v) {
 }
 __device__ __forceinline__ float wave_max(float v) { return wave_max_over_c(wave_max_over_g(v)); }
 
+// x of another lane of the same row of 16 lanes (DPP control CTRL)
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+// sum over aligned groups of N consecutive lanes (N = 1, 2, 4, 8 or 16),
+// with DPP lane moves: quad permutations [1,0,3,2] and [2,3,0,1], then the
+// mirror of each half row and of the row.  Each step adds the partial sum
+// a butterfly over lane bits 0, 1, 2, 3 would add, so the results are the
+// same, bit for bit.
+template <int N>
+__device__ __forceinline__ float sum_lane_group(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16, "groups inside one row");
+  if constexpr (N >= 2) v += dpp_f32<0xB1>(v);
+  if constexpr (N >= 4) v += dpp_f32<0x4E>(v);
+  if constexpr (N >= 8) v += dpp_f32<0x141>(v);
+  if constexpr (N >= 16) v += dpp_f32<0x140>(v);
+  return v;
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 constexpr float kLog2e = 1.4426950408889634f;

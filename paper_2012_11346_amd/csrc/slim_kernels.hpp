@@ -94,7 +94,9 @@ struct CarryArgs {
   void* dV;             // in/out
   float* dW_part;       // [B,H,P,M,D] in/out, then (CS-1) x [B,H,P-1,M,D] written
   int B, H, L, C, P;
-  int CS;  // workgroups (row parts) per segment
+  int CS;  // workgroups (row parts) per segment (carry_kernel)
+  int nch_head;  // 32-row chunks per head over segments 0 .. P-2 (carry8_kernel)
+  int NWG;       // workgroups (carry8_kernel); dW_part slot B H P + i is workgroup i's
   float relu_eps;
 };
 
@@ -140,6 +142,11 @@ template <class G>
 hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s);
 template <class G>
 hipError_t launch_carry(const CarryArgs& a, hipStream_t s);
+// the same pass with 8 waves and a balanced run of 32-row chunks per
+// workgroup; bf16 problems with 32 or 64 features per 4-wave slice
+template <class G>
+hipError_t launch_carry8(const CarryArgs& a, hipStream_t s);
+int carry8_chunks_per_head(int L, int C, int P);
 // dW = sum of the n_parts partials [n_parts][n], in a fixed order
 hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s);
 

@@ -19,29 +19,25 @@ from tests.gpu_common import TOL, dev, host64, need_gpu, report
 pytestmark = pytest.mark.gpu
 
 
-def _fwd_bwd(x, C, kind, segments=None, sum_split=None):
+def _fwd_bwd(x, C, kind, segments=None, sum_split=None, carry_wgs=None):
     from paper_2012_11346_amd import slim
 
-    old = os.environ.get("SLIM_SEGMENTS")
-    old_split = os.environ.get("SLIM_SUM_SPLIT")
+    env = {"SLIM_SEGMENTS": segments, "SLIM_SUM_SPLIT": sum_split, "SLIM_CARRY_WORKGROUPS": carry_wgs}
+    old = {k: os.environ.get(k) for k in env}
     try:
-        if segments is not None:
-            os.environ["SLIM_SEGMENTS"] = str(segments)
-        if sum_split is not None:
-            os.environ["SLIM_SUM_SPLIT"] = str(sum_split)
+        for k, v in env.items():
+            if v is not None:
+                os.environ[k] = str(v)
         Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
         Y, st, ks = slim.fwd(Q, K, V, W, C, kind)
         g = slim.bwd(Q, K, V, W, dY, C, ks, kind)
         torch.cuda.synchronize()
     finally:
-        if old is None:
-            os.environ.pop("SLIM_SEGMENTS", None)
-        else:
-            os.environ["SLIM_SEGMENTS"] = old
-        if old_split is None:
-            os.environ.pop("SLIM_SUM_SPLIT", None)
-        else:
-            os.environ["SLIM_SUM_SPLIT"] = old_split
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
     return Y, st, ks, g
 
 
@@ -75,6 +71,31 @@ def test_results_do_not_depend_on_segments(i, split):
         report(f"state P={P}", s, stref, tol)
         for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], gref):
             report(f"{n} P={P}", host64(a), r, tol)
+
+
+CARRY_CASES = [
+    # name, B, H, L, d, M, C, kind, segments
+    ("carry_d64", 1, 3, 900, 64, 256, 64, "favor+", 5),
+    ("carry_d64_relu", 2, 1, 777, 64, 128, 40, "relu", 4),
+    ("carry_d32", 1, 3, 650, 32, 256, 32, "favor+", 6),
+    ("carry_d32_relu", 1, 2, 1000, 32, 128, 100, "relu", 7),
+]
+
+
+@pytest.mark.parametrize("wgs", [1, 5])
+@pytest.mark.parametrize("i", range(len(CARRY_CASES)))
+def test_carry_runs_cross_segments_and_heads(i, wgs):
+    """The carried cotangent of bf16 problems is dealt to workgroups in runs
+    of 32-row chunks; with few workgroups every run crosses segment and head
+    boundaries (ragged segment ends included)."""
+    need_gpu()
+    name, B, H, L, d, M, C, kind, P = CARRY_CASES[i]
+    x = make_inputs(Workload(name, 340 + i, B, H, L, d, M, (C,), "bf16", kind))
+    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    print(f"[carry runs] case={name} P={P} workgroups={wgs}", flush=True)
+    _, _, _, g = _fwd_bwd(x, C, kind, P, carry_wgs=wgs)
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], gref):
+        report(f"{n} wgs={wgs}", host64(a), r, TOL["bf16"])
 
 
 @pytest.mark.parametrize("kind", ["favor+", "relu"])
