@@ -349,8 +349,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
         const float n = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
         dot += dy[i] * (n * inv);
       }
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
+      dot = sum_lane_group<TPR>(dot);
 #pragma unroll
       for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * inv);
       if (q == 0) {

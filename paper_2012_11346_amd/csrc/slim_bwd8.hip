@@ -508,8 +508,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         dy[i] = to_f32(dYs[swz_off<LDQ, kSwzRows>(t, e) + i]);
         dot += dy[i] * (n[i] * inv);
       }
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) dot += __shfl_xor(dot, o, 64);
+      dot = sum_lane_group<TPR>(dot);
 #pragma unroll
       for (int i = 0; i < EPT; ++i) dNs[swz_off<LDQ, kSwzRows>(t, e) + i] = cvt<T>(dy[i] * inv);
       if (q == 0) {

@@ -270,22 +270,6 @@ __device__ __forceinline__ float wave_sum_over_g(float v) {
   v += __shfl_xor(v, 32, 64);
   return v;
 }
-__device__ __forceinline__ float wave_max_over_c(float v) {
-  v = fmaxf(v, __shfl_xor(v, 1, 64));
-  v = fmaxf(v, __shfl_xor(v, 2, 64));
-  v = fmaxf(v, __shfl_xor(v, 4, 64));
-  v = fmaxf(v, __shfl_xor(v, 8, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum_over_c(float v) {
-  v += __shfl_xor(v, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  v += __shfl_xor(v, 4, 64);
-  v += __shfl_xor(v, 8, 64);
-  return v;
-}
-__device__ __forceinline__ float wave_max(float v) { return wave_max_over_c(wave_max_over_g(v)); }
-
 // x of another lane of the same row of 16 lanes (DPP control CTRL)
 template <int CTRL>
 __device__ __forceinline__ float dpp_f32(float x) {
@@ -305,6 +289,21 @@ __device__ __forceinline__ float sum_lane_group(float v) {
   if constexpr (N >= 16) v += dpp_f32<0x140>(v);
   return v;
 }
+// the same for the maximum
+template <int N>
+__device__ __forceinline__ float max_lane_group(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16, "groups inside one row");
+  if constexpr (N >= 2) v = fmaxf(v, dpp_f32<0xB1>(v));
+  if constexpr (N >= 4) v = fmaxf(v, dpp_f32<0x4E>(v));
+  if constexpr (N >= 8) v = fmaxf(v, dpp_f32<0x141>(v));
+  if constexpr (N >= 16) v = fmaxf(v, dpp_f32<0x140>(v));
+  return v;
+}
+
+// over the 16 lanes that share g (a row of the wave)
+__device__ __forceinline__ float wave_max_over_c(float v) { return max_lane_group<16>(v); }
+__device__ __forceinline__ float wave_sum_over_c(float v) { return sum_lane_group<16>(v); }
+__device__ __forceinline__ float wave_max(float v) { return wave_max_over_c(wave_max_over_g(v)); }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
