@@ -542,15 +542,27 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       sstore_tile_T(oK, ZdA, acc, 16 * st, 16 * tt);
     }
     // dV^T[e][s] = sum_m G[m][e] K~[s][m] + sum_t dN[t][e] A^T[s][t], own columns -> RedY[s][e']
+    // (per row tile, its operands are read before its products)
+    {
+      F dnT[EH];
 #pragma unroll
-    for (int st = 0; st < RT; ++st)
+      for (int el = 0; el < EH; ++el) dnT[el] = sfrag_tr(oR, dNs, 0, 16 * (h * EH + el));
 #pragma unroll
-      for (int el = 0; el < EH; ++el) {
-        f32x4 acc = mma(zero4(), sfrag_tr(oR, dNs, 0, 16 * (h * EH + el)), sfrag_tr(oK, ZA, 0, 16 * st));
+      for (int st = 0; st < RT; ++st) {
+        const F aT = sfrag_tr(oK, ZA, 0, 16 * st);
+        F kT[MB];
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), sfrag_tr(oK, Zk, 32 * kb, 16 * st));
-        store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
+        for (int kb = 0; kb < MB; ++kb) kT[kb] = sfrag_tr(oK, Zk, 32 * kb, 16 * st);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int el = 0; el < EH; ++el) {
+          f32x4 acc = mma(zero4(), dnT[el], aT);
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(Gs, Gz, el, kb), kT[kb]);
+          store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * st);
+        }
       }
+    }
     __syncthreads();
     L = fresh_lane();
     g = L.g;
@@ -603,17 +615,27 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       stB.fetch(range_rsrc(srcB + (size_t)sn * D, nb), 0, st2);
     }
     {
+      // the operands shared by every feature tile, then per feature tile
+      // all of its operands before its products (the fence keeps the
+      // compiler from putting a wait before each product)
       const float ddt = dDs[16 * h + c];
+      F dnf[EB];
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) dnf[kb] = sfrag_rm(oR, dNs, 16 * h, 32 * kb);
+      const F daf = sfrag_rm(oK, ZdA, 16 * h, 0);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        f32x4 acc;
+        const f32x4 zv = *(const f32x4*)&zs[f * FW + 16 * mt + 4 * g];
+        F zsf[EB];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] = zs[f * FW + 16 * mt + 4 * g + r] * ddt;
-#pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, sfrag_tr(oF, ZS, 32 * kb, 16 * mt), sfrag_rm(oR, dNs, 16 * h, 32 * kb));
-        acc = mma(acc, sfrag_rm(oK, Zk, 16 * mt, 0), sfrag_rm(oK, ZdA, 16 * h, 0));
+        for (int kb = 0; kb < EB; ++kb) zsf[kb] = sfrag_tr(oF, ZS, 32 * kb, 16 * mt);
+        const F zkf = sfrag_rm(oK, Zk, 16 * mt, 0);
         const f32x4 qv = sload_tile_T(oF, Zq, 16 * mt, 16 * h);
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4 acc = zv * ddt;
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, zsf[kb], dnf[kb]);
+        acc = mma(acc, zkf, daf);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
@@ -683,32 +705,42 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // ---- dK~[s][m] = sum_e V[s][e] G[m][e] + dz[m] + sum_t dA^T[s][t] Q~[t][m] for this
     //      wave's rows s in [16 h, 16 h + 16); Pk = dK~ . K~ (FAVOR+) or masked (ReLU)
     //      -> ZPk[m][s] (rows past the tile have K~ = 0, hence Pk = 0)
+    //      and G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns.
+    //      The operands shared by every feature tile are read first, then per
+    //      feature tile all of its operands before its products (the fence
+    //      keeps the compiler from putting a wait before each product); the
+    //      Q~ operand serves both products.
     {
+      F vfr[EB], dnT[EH];
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) vfr[kb] = sfrag_rm(oR, Vs, 16 * h, 32 * kb);
+      const F daT = sfrag_tr(oK, ZdA, 0, 16 * h);
+#pragma unroll
+      for (int el = 0; el < EH; ++el) dnT[el] = sfrag_tr(oR, dNs, 0, e0 + 16 * el);
+      F dd;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) dd[s] = dDb[kp(g, s)];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const float dz = dzs[f * FW + 16 * mt + c];
+        F gfr[EB];
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) gfr[kb] = sfrag_tr(oF, ZG, 32 * kb, 16 * mt);
+        const F qf = sfrag_tr(oF, Zq, 0, 16 * mt);
+        const f32x4 kv = sload_tile_T(oK, Zk, 16 * h, 16 * mt);
+        __builtin_amdgcn_sched_barrier(0);
         f32x4 acc = {dz, dz, dz, dz};
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb)
-          acc = mma(acc, sfrag_rm(oR, Vs, 16 * h, 32 * kb), sfrag_tr(oF, ZG, 32 * kb, 16 * mt));
-        acc = mma(acc, sfrag_tr(oK, ZdA, 0, 16 * h), sfrag_tr(oF, Zq, 0, 16 * mt));
-        const f32x4 kv = sload_tile_T(oK, Zk, 16 * h, 16 * mt);
+        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, vfr[kb], gfr[kb]);
+        acc = mma(acc, daT, qf);
+#pragma unroll
+        for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, dnT[el]);
+        Gz[mt] = mma(Gz[mt], qf, dd);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
         sstore_tile_T(oK, ZPk, acc, 16 * h, 16 * mt);
       }
-    }
-    // G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const F qf = sfrag_tr(oF, Zq, 0, 16 * mt);
-#pragma unroll
-      for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, sfrag_tr(oR, dNs, 0, e0 + 16 * el));
-      F dd;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) dd[s] = dDb[kp(g, s)];
-      Gz[mt] = mma(Gz[mt], qf, dd);
     }
     __syncthreads();
     L = fresh_lane();
@@ -719,11 +751,19 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // ---- dW[m][e] += sum_s Pk[s][m] K[s][e]; dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum_f(Pk)[s]
     //      own columns -> RedY[s][e'], with rowsum_f(Pk)[s] (over this slice's features) from
     //      a product with an all-ones operand
+    {
+      // the key operands first, then per feature tile its Pk operand
+      F kT[EH];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const F pf = sfrag_rm(oK, ZPk, 16 * mt, 0);
+      for (int el = 0; el < EH; ++el) kT[el] = sfrag_tr(oR, Ks, 0, e0 + 16 * el);
+      F pf[MT];
 #pragma unroll
-      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, sfrag_tr(oR, Ks, 0, e0 + 16 * el));
+      for (int mt = 0; mt < MT; ++mt) pf[mt] = sfrag_rm(oK, ZPk, 16 * mt, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf[mt], kT[el]);
     }
     {
 #pragma unroll
