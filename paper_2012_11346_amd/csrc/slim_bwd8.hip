@@ -445,6 +445,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int kb = 0; kb < MB; ++kb)
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) qf[kb][tt] = sfrag_rm(oF, Zq, 16 * tt, 32 * kb);
+    F kT[MB][RT];  // K~ contracting over this slice's features, columns s
+#pragma unroll
+    for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+      for (int st = 0; st < RT; ++st) kT[kb][st] = sfrag_tr(oK, Zk, 32 * kb, 16 * st);
+    F vT[EH];  // V contracting over the tile's rows, own value columns
+#pragma unroll
+    for (int el = 0; el < EH; ++el) vT[el] = v_frag(e0 + 16 * el);
+    // (every operand of the phase is read before its first product)
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- scores A^T[s][t] over this slice's features, causal -> ZA[t][s] (for dV)
     f32x4 At[RT][RT];
@@ -455,7 +465,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc = zero4();
         if (st <= tt) {
 #pragma unroll
-          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, sfrag_tr(oK, Zk, 32 * kb, 16 * st), qf[kb][tt]);
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, kT[kb][st], qf[kb][tt]);
         }
         if (st == tt) {
 #pragma unroll
@@ -476,7 +486,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int tt = 0; tt < RT; ++tt) {
 #pragma unroll
       for (int el = 0; el <= EH; ++el) {
-        f32x4 acc = mma(zero4(), el < EH ? v_frag(e0 + 16 * el) : ones_frag(L, count), af[tt]);
+        f32x4 acc = mma(zero4(), el < EH ? vT[el < EH ? el : 0] : ones_frag(L, count), af[tt]);
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
         if (el < EH) {
@@ -653,23 +663,31 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      -q[t] sum_m P[t][m], which is zero: Y is homogeneous of degree 0 in
     //      each query feature vector, so sum_m Q~[t][m] dQ~[t][m] = 0.
     {
+      // every operand of the phase is read before its first product
+      F pr[RT][MB], pT[MT], qT[EH];
 #pragma unroll
-    for (int tt = 0; tt < RT; ++tt) {
+      for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
-      for (int el = 0; el < EH; ++el) {
-        f32x4 acc = zero4();
+        for (int kb = 0; kb < MB; ++kb) pr[tt][kb] = sfrag_rm(oF, ZP, 16 * tt, 32 * kb);
 #pragma unroll
-        for (int kb = 0; kb < MB; ++kb)
-          acc = mma(acc, Wb[kb][el], sfrag_rm(oF, ZP, 16 * tt, 32 * kb));
-        store_tile_T<float>(L, RedX, LDRH, acc, 16 * el, 16 * tt);
+      for (int mt = 0; mt < MT; ++mt) pT[mt] = sfrag_tr(oF, ZP, 0, 16 * mt);
+#pragma unroll
+      for (int el = 0; el < EH; ++el) qT[el] = sfrag_tr(oR, Qs, 0, e0 + 16 * el);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) {
+#pragma unroll
+        for (int el = 0; el < EH; ++el) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, Wb[kb][el], pr[tt][kb]);
+          store_tile_T<float>(L, RedX, LDRH, acc, 16 * el, 16 * tt);
+        }
       }
-    }
-    }
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const F pf = sfrag_tr(oF, ZP, 0, 16 * mt);
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf, sfrag_tr(oR, Qs, 0, e0 + 16 * el));
+        for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pT[mt], qT[el]);
     }
     __syncthreads();
     L = fresh_lane();
