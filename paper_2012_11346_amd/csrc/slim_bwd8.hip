@@ -384,10 +384,17 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // ---- Q~ of this wave's 16 rows -> Zq[t][m].  Rows past the tile (zero
     //      in LDS) get finite features and need no mask: their dN, dD are
     //      zero, so they add nothing to G, dA, P or dW.
+    // (the operands of the downdate are read first, ahead of their use)
+    F kfd[MT], vfd[EH];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) kfd[mt] = sfrag_rm(oK, Zk, 16 * mt, 0);  // K~ contracting over rows
+#pragma unroll
+    for (int el = 0; el < EH; ++el) vfd[el] = v_frag(e0 + 16 * el);
     {
       const int t = 16 * h + c;
       float qs = 0.f;
       if (G::KIND == kFavor) qs = fmaxf(fmaxf(qmx[t], qmx[TR + t]), fmaxf(qmx[2 * TR + t], qmx[3 * TR + t])) * kLog2e;
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -426,11 +433,11 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const F ones = ones_frag(L, count);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        F kf = sfrag_rm(oK, Zk, 16 * mt, 0);  // K~ contracting over rows
+        F kf = kfd[mt];
 #pragma unroll
         for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
 #pragma unroll
-        for (int el = 0; el < EH; ++el) S[mt][el] = mma(S[mt][el], kf, v_frag(e0 + 16 * el));
+        for (int el = 0; el < EH; ++el) S[mt][el] = mma(S[mt][el], kf, vfd[el]);
         Sz[mt] = mma(Sz[mt], kf, ones);
       }
     }
@@ -540,10 +547,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     if (w < 3) {
       const int st = w >> 1, tt = (w + 1) >> 1;
       const float ddt = dDs[16 * tt + c];
+      F vr[EB], dr[EB];
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) {
+        vr[kb] = sfrag_rm(oR, Vs, 16 * st, 32 * kb);
+        dr[kb] = sfrag_rm(oR, dNs, 16 * tt, 32 * kb);
+      }
+      __builtin_amdgcn_sched_barrier(0);
       f32x4 acc = f32x4{ddt, ddt, ddt, ddt};
 #pragma unroll
-      for (int kb = 0; kb < EB; ++kb)
-        acc = mma(acc, sfrag_rm(oR, Vs, 16 * st, 32 * kb), sfrag_rm(oR, dNs, 16 * tt, 32 * kb));
+      for (int kb = 0; kb < EB; ++kb) acc = mma(acc, vr[kb], dr[kb]);
       if (st == tt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -784,11 +797,21 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf[mt], kT[el]);
     }
     {
+    // every operand of the dk products first: Pk over this slice and the key entries
+    F pkk[RT][MB];
+    bf16x4 kent[RT][EH];
 #pragma unroll
     for (int st = 0; st < RT; ++st) {
-      F pk[MB];
 #pragma unroll
-      for (int kb = 0; kb < MB; ++kb) pk[kb] = sfrag_tr(oK, ZPk, 32 * kb, 16 * st);
+      for (int kb = 0; kb < MB; ++kb) pkk[st][kb] = sfrag_tr(oK, ZPk, 32 * kb, 16 * st);
+#pragma unroll
+      for (int el = 0; el < EH; ++el)
+        kent[st][el] = G::KIND == kFavor ? *(const bf16x4*)&Ks[oR.a + 16 * st * LDQ + 16 * (h * EH + el)] : bf16x4{};
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int st = 0; st < RT; ++st) {
+      const F (&pk)[MB] = pkk[st];
       float rsv = 0.f;
       if (G::KIND == kFavor) {
         F ones;
@@ -801,11 +824,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
 #pragma unroll
       for (int el = 0; el < EH; ++el) {
-        const int et = h * EH + el;
         f32x4 acc;
         if (G::KIND == kFavor) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[r] = -to_f32(Ks[oR.a + 16 * st * LDQ + 16 * et + r]) * rsv;
+          for (int r = 0; r < 4; ++r) acc[r] = -(float)kent[st][el][r] * rsv;
         } else {
           acc = zero4();
         }
