@@ -119,18 +119,35 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
     const Lane L = fresh_lane();
     const OR oR(L);
 
+    // every operand of the chunk is read before the first product (the
+    // fence keeps the compiler from putting a wait before each product):
+    // key rows, row norms and (sums) the value rows
+    F kf[CT][EB];
+#pragma unroll
+    for (int st = 0; st < CT; ++st)
+#pragma unroll
+      for (int kb = 0; kb < EB; ++kb) kf[st][kb] = sfrag_rm(oR, Ks, 16 * st, 32 * kb);
+    f32x4 knv[CT];
+#pragma unroll
+    for (int st = 0; st < CT; ++st) knv[st] = *(const f32x4*)&kn[16 * st + 4 * L.g];
+    F vf[SUMS ? CT / 2 : 1][SUMS ? ET : 1];
+    if constexpr (SUMS) {
+#pragma unroll
+      for (int rb = 0; rb < CT / 2; ++rb)
+#pragma unroll
+        for (int et = 0; et < ET; ++et) vf[rb][et] = sfrag_tr(oR, Vs, 32 * rb, 16 * et);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
     // logits: Lk[st][mt] rows s = 16 st + 4 g + r, columns m = w FW + 16 mt + c
     f32x4 Lk[CT][MT];
 #pragma unroll
     for (int st = 0; st < CT; ++st) {
-      F kf[EB];
-#pragma unroll
-      for (int kb = 0; kb < EB; ++kb) kf[kb] = sfrag_rm(oR, Ks, 16 * st, 32 * kb);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[kb], Wf[mt][kb]);
+        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wf[mt][kb]);
         Lk[st][mt] = acc;
       }
     }
@@ -139,24 +156,22 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
       // the key exponent w.k - |k|^2/2 of the chunk's rows
 #pragma unroll
       for (int st = 0; st < CT; ++st) {
-        const f32x4 knv = *(const f32x4*)&kn[16 * st + 4 * L.g];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           float v = -INFINITY;
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) v = fmaxf(v, Lk[st][mt][r]);
-          vmax = fmaxf(vmax, 16 * st + 4 * L.g + r < cnt ? v - 0.5f * knv[r] : -INFINITY);
+          vmax = fmaxf(vmax, 16 * st + 4 * L.g + r < cnt ? v - 0.5f * knv[st][r] : -INFINITY);
         }
       }
     } else {
       // features (rows past the chunk: zero)
 #pragma unroll
       for (int st = 0; st < CT; ++st) {
-        const f32x4 knv = *(const f32x4*)&kn[16 * st + 4 * L.g];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool ok = 16 * st + 4 * L.g + r < cnt;
-          const float kc = ok ? koff + 0.5f * kLog2e * knv[r] : INFINITY;
+          const float kc = ok ? koff + 0.5f * kLog2e * knv[st][r] : INFINITY;
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             float x = Lk[st][mt][r];
@@ -169,9 +184,6 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
       // [S | z] += K~^T [V | 1] over the chunk's rows, 32 rows per product
 #pragma unroll
       for (int rb = 0; rb < CT / 2; ++rb) {
-        F vf[ET];
-#pragma unroll
-        for (int et = 0; et < ET; ++et) vf[et] = sfrag_tr(oR, Vs, 32 * rb, 16 * et);
         F ones;
         const int rem = cnt - 32 * rb - 4 * L.g;  // rows 32 rb + kp(g, s) < cnt
 #pragma unroll
@@ -180,7 +192,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
         for (int mt = 0; mt < MT; ++mt) {
           const F kt = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
 #pragma unroll
-          for (int et = 0; et < ET; ++et) S[mt][et] = mma(S[mt][et], kt, vf[et]);
+          for (int et = 0; et < ET; ++et) S[mt][et] = mma(S[mt][et], kt, vf[rb][et]);
           Sz[mt] = mma(Sz[mt], kt, ones);
         }
       }
