@@ -264,13 +264,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   // V operand over the tile's 32 rows, value columns [col, col + 16)
   auto v_frag = [&](int col) -> F { return sfrag_tr(oR, Vs, 0, col); };
   // the ones column of [V|1] over the tile's rows (zero past the tile)
-  auto ones_frag = [&](const Lane& L, int count) -> F {
-    F v;
-    const int rem = count - 4 * L.g;  // rows kp(g, s) < count
-#pragma unroll
-    for (int s = 0; s < 8; ++s) v[s] = cvt<T>((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
-    return v;
-  };
+  auto ones_frag = [&](const Lane& L, int count) -> F { return ones_rows_frag(L, 0, count); };
   // operand contracting over this slice's features m in [32 kb, 32 kb + 32),
   // columns = own value tile el of X (el == EH: the ones column Xz)
   auto feat_frag = [&](const f32x4 (&X)[MT][EH], const f32x4 (&Xz)[MT], int el, int kb) -> F {
@@ -282,14 +276,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   // fragments in program order: on gfx9 a wait for a load also waits for
   // every earlier store.  dV is held from its reduction to the dq store; dk
   // of a tile is stored in the next tile after its logits.
-  typedef T tvec __attribute__((ext_vector_type(EPT)));
   typedef unsigned u32e __attribute__((ext_vector_type(EPT / 2)));
   static_assert(EPT == 2 || EPT == 4, "8- or 4-byte row pieces");
   auto cvt_row = [&](const fvec& v) -> u32e {
-    tvec o;
+    u32e o;
 #pragma unroll
-    for (int i = 0; i < EPT; ++i) o[i] = cvt<T>(v[i]);
-    return __builtin_bit_cast(u32e, o);
+    for (int i = 0; i < EPT / 2; ++i) o[i] = __builtin_bit_cast(unsigned, pk_bf16(v[2 * i], v[2 * i + 1]));
+    return o;
   };
   auto store_piece = [&](const u32e& v, __amdgpu_buffer_rsrc_t rs, int off) {
     if constexpr (EPT == 4) __builtin_amdgcn_raw_buffer_store_b64(v, rs, off, 0, 0);
@@ -430,15 +423,19 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       // too, including the next tile's rows (gfx9 encoding: vmcnt(0) only)
       __builtin_amdgcn_s_waitcnt(0x0F70);
     } else {
-      const F ones = ones_frag(L, count);
+      // S -= K~^T [V|1]: the [V|1] operands negated once (sign bits of the
+      // packed pairs), not every K~ operand
+      typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+      auto neg = [](const F& x) { return __builtin_bit_cast(F, __builtin_bit_cast(u32x4, x) ^ 0x80008000u); };
+      const F nones = neg(ones_frag(L, count));
+      F nv[EH];
+#pragma unroll
+      for (int el = 0; el < EH; ++el) nv[el] = neg(vfd[el]);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        F kf = kfd[mt];
 #pragma unroll
-        for (int s = 0; s < 8; ++s) kf[s] = -kf[s];
-#pragma unroll
-        for (int el = 0; el < EH; ++el) S[mt][el] = mma(S[mt][el], kf, vfd[el]);
-        Sz[mt] = mma(Sz[mt], kf, ones);
+        for (int el = 0; el < EH; ++el) S[mt][el] = mma(S[mt][el], kfd[mt], nv[el]);
+        Sz[mt] = mma(Sz[mt], kfd[mt], nones);
       }
     }
 
@@ -526,8 +523,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         dot += dy[i] * (n[i] * inv);
       }
       dot = sum_lane_group<TPR>(dot);
+      u32e dn;
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) dNs[swz_off<LDQ, kSwzRows>(t, e) + i] = cvt<T>(dy[i] * inv);
+      for (int i = 0; i < EPT / 2; ++i) dn[i] = __builtin_bit_cast(unsigned, pk_bf16(dy[2 * i] * inv, dy[2 * i + 1] * inv));
+      *(u32e*)&dNs[swz_off<LDQ, kSwzRows>(t, e)] = dn;
       if (q == 0) {
         const float dd = ok ? -dot * inv : 0.f;
         dDs[t] = dd;
@@ -827,7 +826,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         f32x4 acc;
         if (G::KIND == kFavor) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[r] = -(float)kent[st][el][r] * rsv;
+          for (int r = 0; r < 4; ++r) acc[r] = (float)kent[st][el][r] * (-rsv);
         } else {
           acc = zero4();
         }

@@ -107,6 +107,14 @@ __device__ __forceinline__ float to_f32(T x) {
   return (float)x;
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+// floats to bf16 (round to nearest even) as whole vectors: the compiler then
+// emits one v_cvt_pk_bf16_f32 per pair, where element-wise conversions into a
+// vector can come out as one conversion per element plus byte permutes
+__device__ __forceinline__ bf16x2 pk_bf16(float a, float b) { return __builtin_convertvector(f32x2{a, b}, bf16x2); }
+__device__ __forceinline__ bf16x4 pk_bf16x4(const f32x4& x) { return __builtin_convertvector(x, bf16x4); }
+
 // ------------------------------------------------------------- fragments
 
 template <typename T>
@@ -122,20 +130,30 @@ __device__ __forceinline__ typename FragT<T>::type frag_zero() {
 template <typename T>
 __device__ __forceinline__ typename FragT<T>::type tile_pair_frag(const f32x4& x0, const f32x4& x1) {
   typename FragT<T>::type f;
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 a = pk_bf16x4(x0), b = pk_bf16x4(x1);
+    f = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  } else {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    f[r] = cvt<T>(x0[r]);
-    f[4 + r] = cvt<T>(x1[r]);
+    for (int r = 0; r < 4; ++r) {
+      f[r] = cvt<T>(x0[r]);
+      f[4 + r] = cvt<T>(x1[r]);
+    }
   }
   return f;
 }
 template <typename T>
 __device__ __forceinline__ typename FragT<T>::type tile_half_frag(const f32x4& x0) {
   typename FragT<T>::type f;
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 a = pk_bf16x4(x0), z = {};
+    f = __builtin_shufflevector(a, z, 0, 1, 2, 3, 4, 5, 6, 7);
+  } else {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    f[r] = cvt<T>(x0[r]);
-    f[4 + r] = cvt<T>(0.f);
+    for (int r = 0; r < 4; ++r) {
+      f[r] = cvt<T>(x0[r]);
+      f[4 + r] = cvt<T>(0.f);
+    }
   }
   return f;
 }
@@ -196,8 +214,12 @@ __device__ __forceinline__ f32x8 frag_tr(const float* Z, int ld, int k0, int col
 template <typename T>
 __device__ __forceinline__ void store_tile_T(const Lane& L, T* Z, int ld, const f32x4& x, int row0, int col0) {
   T* p = Z + (col0 + L.c) * ld + row0 + 4 * L.g;
+  if constexpr (sizeof(T) == 2) {
+    *(bf16x4*)p = pk_bf16x4(x);
+  } else {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) p[r] = cvt<T>(x[r]);
+    for (int r = 0; r < 4; ++r) p[r] = cvt<T>(x[r]);
+  }
 }
 template <typename T>
 __device__ __forceinline__ void store_tile_T(T* Z, int ld, const f32x4& x, int row0, int col0) {
@@ -217,6 +239,20 @@ __device__ __forceinline__ void store_half_T(const Lane& L, bf16* Z, int ld, con
 }
 __device__ __forceinline__ void store_half_T(const Lane& L, float* Z, int ld, const f32x4& v, int row0, int col0) {
   *(f32x4*)(Z + (col0 + L.c) * ld + row0 + 4 * L.g) = v;
+}
+
+// bf16 operand fragment of ones over the rows of a 32-deep block: slot s is 1
+// where k0 + kp(g, s) < count, else 0 (count wave-uniform).  A full block
+// (the common case) is a constant.
+__device__ __forceinline__ bf16x8 ones_rows_frag(const Lane& L, int k0, int count) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  constexpr unsigned one2 = 0x3F803F80u;  // two bf16 ones
+  if (count >= k0 + 32) return __builtin_bit_cast(bf16x8, u32x4{one2, one2, one2, one2});
+  const int rem = count - k0 - 4 * L.g;  // rows k0 + kp(g, s) < count
+  bf16x8 f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f[s] = (bf16)((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
+  return f;
 }
 
 // two stacked result tiles as an operand (has_b), or the first one with the
@@ -384,10 +420,7 @@ __device__ __forceinline__ bf16x8 sfrag_tr(const SwzLane<P, MODE>& o, const bf16
 // result tile X[row0 + 4g + r][col0 + c] stored transposed: Z[col0 + c][row0 + 4g + r]
 template <int P, int MODE>
 __device__ __forceinline__ void sstore_tile_T(const SwzLane<P, MODE>& o, bf16* Z, const f32x4& x, int row0, int col0) {
-  bf16x4 v;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) v[r] = (bf16)x[r];
-  *(bf16x4*)(Z + o.a + col0 * P + row0) = v;
+  *(bf16x4*)(Z + o.a + col0 * P + row0) = pk_bf16x4(x);
 }
 
 // the same store for values already rounded (half of an operand fragment)

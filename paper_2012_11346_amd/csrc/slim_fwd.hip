@@ -40,6 +40,7 @@ __device__ __forceinline__ typename FragT<typename G::T>::type v_frag(const Lane
                                                                         int et, int count) {
   typedef typename G::T T;
   if (et < G::ET) return frag_tr(L, Vs, G::LDQ, k0, 16 * et);
+  if constexpr (sizeof(T) == 2) return ones_rows_frag(L, k0, count);
   typename FragT<T>::type f;
   const int rem = count - k0 - 4 * L.g;  // rows k0 + kp(g, s) < count
 #pragma unroll
@@ -405,8 +406,16 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
         const int idx = t * LDR + q * EPT + 4 * h4;
         const f32x4 n = (*(const f32x4*)&Red[0][idx] + *(const f32x4*)&Red[1][idx]) +
                         (*(const f32x4*)&Red[2][idx] + *(const f32x4*)&Red[3][idx]);
+        if constexpr (sizeof(T) == 2) {
+          const bf16x2 lo = pk_bf16(n[0] * inv, n[1] * inv), hi = pk_bf16(n[2] * inv, n[3] * inv);
+          o[4 * h4] = lo[0];
+          o[4 * h4 + 1] = lo[1];
+          o[4 * h4 + 2] = hi[0];
+          o[4 * h4 + 3] = hi[1];
+        } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[4 * h4 + i] = cvt<T>(n[i] * inv);
+          for (int i = 0; i < 4; ++i) o[4 * h4 + i] = cvt<T>(n[i] * inv);
+        }
       }
       const __amdgpu_buffer_rsrc_t ry =
           range_rsrc((T*)a.Y + head * (size_t)a.L * D + (size_t)start * D, (size_t)count * D * sizeof(T));
