@@ -91,6 +91,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   typedef SwzLane<LDZK, kSwzInter> OK;  // K~, Pk, A^T, dA^T
   typedef SwzLane<LDZF, kSwzInter> OF;  // Q~, P, S, G
   constexpr bool ODD = (MT & 1) != 0;  // last 32-deep feature block holds 16 features
+  constexpr bool FULL = (ET == 4);      // d = 64: dq and dk tiles over all features (one per wave)
   constexpr int NT = 512, TPR = NT / TR, EPT = D / TPR;
   static_assert(RT == 2 && G::RB == 1, "the two waves of a pair take one 16-row half of the tile each");
   static_assert(ET % 2 == 0 && EPT >= 1, "");
@@ -198,8 +199,6 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const size_t SZ = (size_t)M * (D + 1);
   const size_t sidx = (head * a.P + p) * SZ;
   const float* bend = a.bounds + (head * a.bound_stride + (size_t)(p + 1) * a.bound_step) * SZ;
-  float r0 = 1.f;
-  if (G::KIND == kFavor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
 
   // the cotangent starts at dstate_out in the last segment, else at zero
   // (earlier segments get the cotangent of later ones added by carry_kernel)
@@ -308,7 +307,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     int start, count;
     tm.tile(j, start, count);
     u32e dv_hold;
-    F Wb[MB][EH];  // W fragments of the dq and dk products
+    // W fragments of the dq and dk products: with d = 64 (FULL) a wave
+    // computes whole output tiles over all M features (value columns
+    // [16 f, 16 f + 16), rows [16 h, 16 h + 16)), reading every slice's P and
+    // Pk from LDS, so dq and dk need no cross-slice sums; with d = 32 each
+    // wave contracts over its slice and the slices are summed in LDS
+    F Wb[FULL ? 1 : MB][FULL ? 1 : EH];
+    F Wc[FULL ? 4 * MB : 1];
+    u32e dq_hold;
 
     // ---- features: Q and K logits of this wave's 16 rows (the pair splits
     //      the tile's rows); K~ -> Zk[m][s], row maxima of the query logits -> qmx
@@ -618,10 +624,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      dQ~ masked (ReLU) -> ZP[t][m]
     // (the W fragments of the dq and dk products are fetched here, a phase
     // ahead of their first use)
+    if constexpr (FULL) {
 #pragma unroll
-    for (int kb = 0; kb < MB; ++kb)
+      for (int kb = 0; kb < 4 * MB; ++kb) Wc[kb] = wfrag(WL::c(kb, f));
+    } else {
 #pragma unroll
-      for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
+      for (int kb = 0; kb < MB; ++kb)
+#pragma unroll
+        for (int el = 0; el < EH; ++el) Wb[kb][el] = wfrag(WL::b(f, kb, h * EH + el));
+    }
     // rows of the next tile, stored into LDS at the end of this one; issued
     // after the W fragments so that waiting for those does not wait for
     // these, and half a tile ahead of the logits' W fragments (fetched at the
@@ -670,11 +681,40 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m], own columns -> RedX[t][e'];
+    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] (FULL: the wave's tile over all
+    //      features, held; else own columns over this slice -> RedX[t][e']);
     //      dW[m][e] += sum_t P[t][m] Q[t][e].  The FAVOR+ chain rule also has
     //      -q[t] sum_m P[t][m], which is zero: Y is homogeneous of degree 0 in
     //      each query feature vector, so sum_m Q~[t][m] dQ~[t][m] = 0.
-    {
+    if constexpr (FULL) {
+      // P of two slices at a time, read before their products
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int f0 = 0; f0 < 4; f0 += 2) {
+        F pa[2][MB];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb)
+            pa[i][kb] = sfrag_rm(oF, (const T*)(arena + Lay::oP + (f0 + i) * Lay::PAIR + Lay::pY), 16 * h, 32 * kb);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, Wc[(f0 + i) * MB + kb], pa[i][kb]);
+      }
+      dq_hold = __builtin_bit_cast(u32e, pk_bf16x4(acc));
+      F pT[MT], qT[EH];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) pT[mt] = sfrag_tr(oF, ZP, 0, 16 * mt);
+#pragma unroll
+      for (int el = 0; el < EH; ++el) qT[el] = sfrag_tr(oR, Qs, 0, e0 + 16 * el);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pT[mt], qT[el]);
+    } else {
       // every operand of the phase is read before its first product
       F pr[RT][MB], pT[MT], qT[EH];
 #pragma unroll
@@ -714,7 +754,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
       const int off = (t * D + e) * (int)sizeof(T);
       const size_t nb = (size_t)count * D * sizeof(T);
-      store_piece(cvt_row(sum_x(hh, t * LDRH + col)), range_rsrc(dQh + (size_t)start * D, nb), off);
+      if constexpr (FULL) {
+        // lane (g, c) of the wave's tile: row 16 h + c, columns 16 f + 4 g + [0, 4)
+        const Lane Lq = fresh_lane();
+        store_piece(dq_hold, range_rsrc(dQh + (size_t)start * D, nb), ((16 * h + Lq.c) * D + 16 * f + 4 * Lq.g) * (int)sizeof(T));
+      } else {
+        store_piece(cvt_row(sum_x(hh, t * LDRH + col)), range_rsrc(dQh + (size_t)start * D, nb), off);
+      }
       store_piece(dv_hold, range_rsrc(dVh + (size_t)start * D, nb), off);
     }
 #pragma unroll
@@ -736,10 +782,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      wave's rows s in [16 h, 16 h + 16); Pk = dK~ . K~ (FAVOR+) or masked (ReLU)
     //      -> ZPk[m][s] (rows past the tile have K~ = 0, hence Pk = 0)
     //      and G[m][e] += sum_t Q~[t][m] [dN|dD][t][e] (eq. 18), own columns.
+    //      (FULL: the W fragments of the dk product are fetched again here, a
+    //      phase ahead, so that they are not held through the phases between)
     //      The operands shared by every feature tile are read first, then per
     //      feature tile all of its operands before its products (the fence
     //      keeps the compiler from putting a wait before each product); the
     //      Q~ operand serves both products.
+    if constexpr (FULL) {
+#pragma unroll
+      for (int kb = 0; kb < 4 * MB; ++kb) Wc[kb] = wfrag(WL::c(kb, f));
+    }
     {
       F vfr[EB], dnT[EH];
 #pragma unroll
@@ -795,7 +847,42 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
         for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf[mt], kT[el]);
     }
-    {
+    if constexpr (FULL) {
+      // dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum(Pk)[s] for the wave's tile
+      // over all features (every slice's Pk from LDS; the rowsum from products
+      // with an all-ones operand), held for the next tile's store
+      const bf16x4 ke = G::KIND == kFavor ? *(const bf16x4*)&Ks[oR.a + 16 * h * LDQ + 16 * f] : bf16x4{};
+      F ones;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) ones[s2] = cvt<T>(1.f);
+      f32x4 acc = zero4(), rs = zero4();
+      // Pk of two slices at a time, read before their products
+#pragma unroll
+      for (int f0 = 0; f0 < 4; f0 += 2) {
+        F pa[2][MB];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb)
+            pa[i][kb] = sfrag_tr(oK, (const T*)(arena + Lay::oP + (f0 + i) * Lay::PAIR + Lay::pX), 32 * kb, 16 * h);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb) {
+            acc = mma(acc, Wc[(f0 + i) * MB + kb], pa[i][kb]);
+            if (G::KIND == kFavor) rs = mma(rs, ones, pa[i][kb]);
+          }
+      }
+      if (G::KIND == kFavor) {
+        const float rsv = rs[0];  // every row of the product holds the sums of the columns s
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] += (float)ke[r] * (-rsv);
+      }
+      dk_hold = __builtin_bit_cast(u32e, pk_bf16x4(acc));
+      dk_rs = range_rsrc(dKh + (size_t)start * D, (size_t)count * D * sizeof(T));
+      dk_off = ((16 * h + c) * D + 16 * f + 4 * g) * (int)sizeof(T);
+    } else {
     // every operand of the dk products first: Pk over this slice and the key entries
     F pkk[RT][MB];
     bf16x4 kent[RT][EH];
@@ -843,8 +930,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dk = sum over slices (held); rows of the next tile -> LDS (their readers are done)
-    {
+    // ---- dk = sum over slices (held; d = 32); rows of the next tile -> LDS (their readers are done)
+    if constexpr (!FULL) {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
@@ -880,7 +967,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   // before the sequence (one segment)
   float* gout = a.g_final != nullptr ? a.g_final + sidx
                                      : ((p == 0 && a.dstate_in != nullptr) ? a.dstate_in + head * SZ : nullptr);
-  if (a.g_final != nullptr) r0 = 1.f;
+  // (the caller's initial state has its own key shift: its cotangent scales by exp(init_shift - kshift))
+  float r0 = 1.f;
+  if (G::KIND == kFavor && a.init_shift != nullptr && a.g_final == nullptr)
+    r0 = fast_exp2((a.init_shift[head] - a.kshift[head]) * kLog2e);
   if (gout != nullptr) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
