@@ -15,16 +15,17 @@
 //                      split by 16-row halves of the tile: half h takes rows
 //                      [16 h, 16 h + 16)
 //
-// Both waves of a pair compute the query features of the whole tile and
-// write identical values into the pair's LDS copy; the same holds for the
-// in-tile scores A^T and their cotangent dA^T.  Cross-slice sums (N, dV, dq,
-// dk) go through per-wave reduction rows in LDS.  The per-wave register set
-// (state half, cotangent half, dW half) is about half of the 4-wave kernel's,
-// which removes its register spills at M = 256 and puts two waves on every
-// SIMD.
+// The features (logits) of a slice are split between the two waves of its
+// pair by feature tiles.  Both waves of a pair compute the in-tile scores A^T
+// of their slice.  Cross-slice sums (N, dV, and dq, dk with d = 32) go
+// through per-wave reduction rows in LDS; with d = 64 the two waves of a pair
+// exchange partial dq and dk tiles over halves of the features.  The
+// per-wave register set (state half, cotangent half, dW half) is about half
+// of the 4-wave kernel's, which removes its register spills at M = 256 and
+// puts two waves on every SIMD.
 //
 // Phases of one tile (| = workgroup barrier):
-//   features (Q~ logits of the tile, K~ of this wave's 16 rows) | Q~ -> LDS,
+//   features (Q and K logits of half of the slice's features) | Q~ -> LDS,
 //   downdate, scores, N partials | dN, dD | dA^T, dV partials | dV sums,
 //   S -> LDS | dQ~ (this wave's 16 rows), P = dQ~ . Q~ | dq partials, dW | dq
 //   sums, G -> LDS | dK~ (16 rows), Pk, G update | dk partials, dW | dk sums,
@@ -52,8 +53,8 @@ struct Bwd8Lds {
   // shared: Q, K, V, dY (dN overwrites dY), floats, dD as T
   static constexpr size_t TILE = al16((size_t)TR * LDQ * sizeof(T));
   static constexpr size_t oQ = 0, oK = TILE, oV = 2 * TILE, odY = 3 * TILE, oF = 4 * TILE;
-  // floats: qn[TR] kn[TR] qmx[4][TR] dDs[TR] rsum[4][TR] zs[4][FW] dzs[4][FW]
-  static constexpr size_t NF = 2 * TR + 4 * TR + TR + 4 * TR + 8 * FW;
+  // floats: kn[TR] qmx[TR][8] dDs[TR] zs[4][FW] dzs[4][FW]
+  static constexpr size_t NF = TR + 8 * TR + TR + 8 * FW;
   static constexpr size_t odDb = oF + al16(NF * sizeof(float));
   static constexpr size_t oP = odDb + al16((TR + 8) * sizeof(T));
   // per pair: one block holding all of the pair's buffers, so that a lane
@@ -91,12 +92,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   typedef SwzLane<LDZK, kSwzInter> OK;  // K~, Pk, A^T, dA^T
   typedef SwzLane<LDZF, kSwzInter> OF;  // Q~, P, S, G
   constexpr bool ODD = (MT & 1) != 0;  // last 32-deep feature block holds 16 features
-  constexpr bool FULL = (ET == 4);      // d = 64: dq and dk tiles over all features (one per wave)
+  constexpr bool FULL = (ET == 4);      // d = 64: dq and dk tiles over half of the features
+  constexpr int MH = MT / 2;            // feature tiles of a wave in the logits
   constexpr int NT = 512, TPR = NT / TR, EPT = D / TPR;
   static_assert(RT == 2 && G::RB == 1, "the two waves of a pair take one 16-row half of the tile each");
   static_assert(ET % 2 == 0 && EPT >= 1, "");
   // (an odd tile count would leave pad rows in buffers that alias float rows)
   static_assert(!ODD, "features per wave must be a multiple of 32");
+  static_assert(MT % 2 == 0, "the pair splits the slice's feature tiles");
 
   __shared__ __attribute__((aligned(16))) char arena[Lay::TOTAL];
   T* Qs = (T*)(arena + Lay::oQ);
@@ -105,12 +108,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   T* dYs = (T*)(arena + Lay::odY);
   T* dNs = dYs;  // dN = dY / D overwrites dY row by row
   float* fl = (float*)(arena + Lay::oF);
-  float* qn = fl;
-  float* kn = qn + TR;
-  float* qmx = kn + TR;        // [4][TR]
-  float* dDs = qmx + 4 * TR;   // [TR]
-  float* rsum = dDs + TR;      // [4][TR]
-  float* zs = rsum + 4 * TR;   // [4][FW]
+  float* kn = fl;
+  float* qmx = kn + TR;        // [TR][8]: row maxima of the query logits per (slice, feature half)
+  float* dDs = qmx + 8 * TR;   // [TR]
+  float* zs = dDs + TR;        // [4][FW]
   float* dzs = zs + 4 * FW;    // [4][FW]
   T* dDb = (T*)(arena + Lay::odDb);
 
@@ -194,7 +195,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int i = 0; i < (int)(sizeof(F) / 16); ++i)
       v[i] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane + 16 * i, idx * 64 * (int)sizeof(F), 0);
     return __builtin_bit_cast(F, v);
-  };  const int e0 = 16 * EH * h;  // first value column of this wave
+  };
+  // d = 64: the partial dq / dk tile of row tile rt computed by the partner
+  // wave, as the result fragment of each lane (X of the pair for dq, Y for dk)
+  auto part_x = [&](int rt) -> f32x4* { return (f32x4*)(pz + Lay::pX + rt * 1024 + wlane); };
+  auto part_y = [&](int rt) -> f32x4* { return (f32x4*)(pz + Lay::pY + rt * 1024 + wlane); };
+  const int e0 = 16 * EH * h;  // first value column of this wave
 
   const size_t SZ = (size_t)M * (D + 1);
   const size_t sidx = (head * a.P + p) * SZ;
@@ -288,14 +294,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     else __builtin_amdgcn_raw_buffer_store_b32(v[0], rs, off, 0, 0);
   };
   u32e dk_hold = {};
+  f32x4 dk_part;
   // W fragments of the logits, fetched one tile ahead (at the end of the
   // previous tile) so that the features phase starts with them resident
-  F Wf[MT][EB];
+  F Wf[MH][EB];
   auto fetch_wf = [&]() {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int i = 0; i < MH; ++i)
 #pragma unroll
-      for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = wfrag(WL::a(f, mt, kb));
+      for (int kb = 0; kb < EB; ++kb) Wf[i][kb] = wfrag(WL::a(f, MH * h + i, kb));
   };
   fetch_wf();
   __amdgpu_buffer_rsrc_t dk_rs = range_rsrc(dKh, 0);
@@ -308,67 +315,84 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     tm.tile(j, start, count);
     u32e dv_hold;
     // W fragments of the dq and dk products: with d = 64 (FULL) a wave
-    // computes whole output tiles over all M features (value columns
-    // [16 f, 16 f + 16), rows [16 h, 16 h + 16)), reading every slice's P and
-    // Pk from LDS, so dq and dk need no cross-slice sums; with d = 32 each
-    // wave contracts over its slice and the slices are summed in LDS
+    // computes the output tiles of value columns [16 f, 16 f + 16) over both
+    // row tiles, contracting over the features of slices 2 h and 2 h + 1 (it
+    // reads their P and Pk from LDS); the pair adds its two halves through
+    // LDS, and wave h keeps the rows [16 h, 16 h + 16).  With d = 32 each wave
+    // contracts over its own slice and the slices are summed in LDS.
     F Wb[FULL ? 1 : MB][FULL ? 1 : EH];
-    F Wc[FULL ? 4 * MB : 1];
-    u32e dq_hold;
+    F Wc[FULL ? 2 * MB : 1];
+    f32x4 dq_part;
 
-    // ---- features: Q and K logits of this wave's 16 rows (the pair splits
-    //      the tile's rows); K~ -> Zk[m][s], row maxima of the query logits -> qmx
-    f32x4 Lq[MT];  // rows m, columns t = 16 h + c
+    // ---- features: Q and K logits of this wave's feature tiles over all tile
+    //      rows (the pair splits the slice's features: wave h takes the tiles
+    //      [MH h, MH (h + 1)), so each wave reads half of the slice's W);
+    //      K~ -> Zk[m][s], row maxima of the query logits -> qmx[t][2 f + h]
+    f32x4 Lq[MH][RT];  // rows m = 16 (MH h + i) + 4 g + r, columns t = 16 tt + c
     {
       // raw logits w.q: the query row shift max_m(w.q - |q|^2/2) absorbs the norm term
-      F qfr[EB];
+      F qfr[RT][EB];
 #pragma unroll
-      for (int kb = 0; kb < EB; ++kb) qfr[kb] = sfrag_rm(oR, Qs, 16 * h, 32 * kb);
+      for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 acc = zero4();
+        for (int kb = 0; kb < EB; ++kb) qfr[tt][kb] = sfrag_rm(oR, Qs, 16 * tt, 32 * kb);
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], qfr[kb]);
-        Lq[mt] = acc;
-      }
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[i][kb], qfr[tt][kb]);
+          Lq[i][tt] = acc;
+        }
       // key rows: exp2(log2e (w.k - |k|^2/2 - shift) - log2(M)/2), the row term folded into the exponent
       // (rows past the tile: an infinite offset gives exactly zero features)
-      float kc[4];
+      float kc[RT][4];
       if (G::KIND == kFavor) {
-        const f32x4 knv = *(const f32x4*)&kn[16 * h + 4 * g];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float v = koff + 0.5f * kLog2e * knv[r];
-          kc[r] = 16 * h + 4 * g + r < count ? v : INFINITY;
-        }
-      }
-      F kfr[EB];  // this wave's 16 key rows as operands
+        for (int st = 0; st < RT; ++st) {
+          const f32x4 knv = *(const f32x4*)&kn[16 * st + 4 * g];
 #pragma unroll
-      for (int kb = 0; kb < EB; ++kb) kfr[kb] = sfrag_rm(oR, Ks, 16 * h, 32 * kb);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 kv = zero4();
-#pragma unroll
-        for (int kb = 0; kb < EB; ++kb) kv = mma(kv, kfr[kb], Wf[mt][kb]);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (G::KIND == kFavor) {
-            kv[r] = fast_exp2(kv[r] * kLog2e - kc[r]);
-          } else {
-            const bool ok = 16 * h + 4 * g + r < count;
-            kv[r] = ok ? fmaxf(kv[r], 0.f) + a.relu_eps : 0.f;
+          for (int r = 0; r < 4; ++r) {
+            const float v = koff + 0.5f * kLog2e * knv[r];
+            kc[st][r] = 16 * st + 4 * g + r < count ? v : INFINITY;
           }
         }
-        sstore_tile_T(oK, Zk, kv, 16 * h, 16 * mt);
       }
+      F kfr[RT][EB];  // the tile's key rows as operands
+#pragma unroll
+      for (int st = 0; st < RT; ++st)
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) kfr[st][kb] = sfrag_rm(oR, Ks, 16 * st, 32 * kb);
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int st = 0; st < RT; ++st) {
+          f32x4 kv = zero4();
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) kv = mma(kv, kfr[st][kb], Wf[i][kb]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (G::KIND == kFavor) {
+              kv[r] = fast_exp2(kv[r] * kLog2e - kc[st][r]);
+            } else {
+              const bool ok = 16 * st + 4 * g + r < count;
+              kv[r] = ok ? fmaxf(kv[r], 0.f) + a.relu_eps : 0.f;
+            }
+          }
+          sstore_tile_T(oK, Zk, kv, 16 * st, 16 * (MH * h + i));
+        }
       if (G::KIND == kFavor) {
-        float v = -INFINITY;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int tt = 0; tt < RT; ++tt) {
+          float v = -INFINITY;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][r]);
-        v = wave_max_over_g(v);
-        if (g == 0) qmx[f * TR + 16 * h + c] = v;
+          for (int i = 0; i < MH; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[i][tt][r]);
+          v = wave_max_over_g(v);
+          if (g == 0) qmx[(16 * tt + c) * 8 + 2 * f + h] = v;
+        }
       }
     }
     __syncthreads();
@@ -380,9 +404,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // dk of the previous tile (an empty range before the first)
     store_piece(dk_hold, dk_rs, dk_off);
 
-    // ---- Q~ of this wave's 16 rows -> Zq[t][m].  Rows past the tile (zero
-    //      in LDS) get finite features and need no mask: their dN, dD are
-    //      zero, so they add nothing to G, dA, P or dW.
+    // ---- Q~ of this wave's feature tiles -> Zq[t][m].  Rows past the tile
+    //      (zero in LDS) get finite features and need no mask: their dN, dD
+    //      are zero, so they add nothing to G, dA, P or dW.
     // (the operands of the downdate are read first, ahead of their use)
     F kfd[MT], vfd[EH];
 #pragma unroll
@@ -390,22 +414,26 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
     for (int el = 0; el < EH; ++el) vfd[el] = v_frag(e0 + 16 * el);
     {
-      const int t = 16 * h + c;
-      float qs = 0.f;
-      if (G::KIND == kFavor) qs = fmaxf(fmaxf(qmx[t], qmx[TR + t]), fmaxf(qmx[2 * TR + t], qmx[3 * TR + t])) * kLog2e;
+      float qs[RT] = {};
+      if (G::KIND == kFavor) {
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt) {
+          const f32x4 m0 = *(const f32x4*)&qmx[(16 * tt + c) * 8], m1 = *(const f32x4*)&qmx[(16 * tt + c) * 8 + 4];
+          qs[tt] = fmaxf(fmaxf(fmaxf(m0[0], m0[1]), fmaxf(m0[2], m0[3])),
+                         fmaxf(fmaxf(m1[0], m1[1]), fmaxf(m1[2], m1[3]))) * kLog2e;
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
+      for (int i = 0; i < MH; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          Lq[mt][r] = (G::KIND == kFavor) ? fast_exp2(Lq[mt][r] * kLog2e - qs) : fmaxf(Lq[mt][r], 0.f) + a.relu_eps;
-      }
+        for (int tt = 0; tt < RT; ++tt) {
+          f32x4 x = Lq[i][tt];
 #pragma unroll
-      for (int kb = 0; kb < MB; ++kb) {
-        const F q = tile_pair_frag<T>(Lq[2 * kb], Lq[2 * kb + 1]);
-        sstore_half_T(oF, Zq, frag_lo(q), 32 * kb, 16 * h);
-        sstore_half_T(oF, Zq, frag_hi(q), 32 * kb + 16, 16 * h);
-      }
+          for (int r = 0; r < 4; ++r)
+            x[r] = (G::KIND == kFavor) ? fast_exp2(x[r] * kLog2e - qs[tt]) : fmaxf(x[r], 0.f) + a.relu_eps;
+          sstore_tile_T(oF, Zq, x, 16 * (MH * h + i), 16 * tt);
+        }
     }
 
     // ---- state before the tile: downdate (eq. 17), or the exact segment start
@@ -626,7 +654,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // ahead of their first use)
     if constexpr (FULL) {
 #pragma unroll
-      for (int kb = 0; kb < 4 * MB; ++kb) Wc[kb] = wfrag(WL::c(kb, f));
+      for (int i = 0; i < 2 * MB; ++i) Wc[i] = wfrag(WL::c(2 * h * MB + i, f));
     } else {
 #pragma unroll
       for (int kb = 0; kb < MB; ++kb)
@@ -681,29 +709,31 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] (FULL: the wave's tile over all
-    //      features, held; else own columns over this slice -> RedX[t][e']);
+    // ---- dq^T[e][t] = sum_m W[m][e] P[t][m] (FULL: columns [16 f, 16 f + 16)
+    //      over the features of slices 2 h, 2 h + 1, the partner's row tile ->
+    //      LDS, the own one held; else own columns over this slice -> RedX[t][e']);
     //      dW[m][e] += sum_t P[t][m] Q[t][e].  The FAVOR+ chain rule also has
     //      -q[t] sum_m P[t][m], which is zero: Y is homogeneous of degree 0 in
     //      each query feature vector, so sum_m Q~[t][m] dQ~[t][m] = 0.
     if constexpr (FULL) {
-      // P of two slices at a time, read before their products
-      f32x4 acc = zero4();
+      // P of one slice at a time (both row tiles), read before its products
+      f32x4 acc[RT] = {};
 #pragma unroll
-      for (int f0 = 0; f0 < 4; f0 += 2) {
-        F pa[2][MB];
+      for (int i = 0; i < 2; ++i) {
+        const T* Ps = (const T*)(arena + Lay::oP + (2 * h + i) * Lay::PAIR + Lay::pY);
+        F pa[RT][MB];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
-          for (int kb = 0; kb < MB; ++kb)
-            pa[i][kb] = sfrag_rm(oF, (const T*)(arena + Lay::oP + (f0 + i) * Lay::PAIR + Lay::pY), 16 * h, 32 * kb);
+          for (int kb = 0; kb < MB; ++kb) pa[tt][kb] = sfrag_rm(oF, Ps, 16 * tt, 32 * kb);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
-          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, Wc[(f0 + i) * MB + kb], pa[i][kb]);
+          for (int kb = 0; kb < MB; ++kb) acc[tt] = mma(acc[tt], Wc[i * MB + kb], pa[tt][kb]);
       }
-      dq_hold = __builtin_bit_cast(u32e, pk_bf16x4(acc));
+      *part_x(1 - h) = h ? acc[0] : acc[1];
+      dq_part = h ? acc[1] : acc[0];
       F pT[MT], qT[EH];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) pT[mt] = sfrag_tr(oF, ZP, 0, 16 * mt);
@@ -757,7 +787,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       if constexpr (FULL) {
         // lane (g, c) of the wave's tile: row 16 h + c, columns 16 f + 4 g + [0, 4)
         const Lane Lq = fresh_lane();
-        store_piece(dq_hold, range_rsrc(dQh + (size_t)start * D, nb), ((16 * h + Lq.c) * D + 16 * f + 4 * Lq.g) * (int)sizeof(T));
+        const u32e dq = __builtin_bit_cast(u32e, pk_bf16x4(dq_part + *part_x(h)));
+        store_piece(dq, range_rsrc(dQh + (size_t)start * D, nb), ((16 * h + Lq.c) * D + 16 * f + 4 * Lq.g) * (int)sizeof(T));
       } else {
         store_piece(cvt_row(sum_x(hh, t * LDRH + col)), range_rsrc(dQh + (size_t)start * D, nb), off);
       }
@@ -790,7 +821,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      Q~ operand serves both products.
     if constexpr (FULL) {
 #pragma unroll
-      for (int kb = 0; kb < 4 * MB; ++kb) Wc[kb] = wfrag(WL::c(kb, f));
+      for (int i = 0; i < 2 * MB; ++i) Wc[i] = wfrag(WL::c(2 * h * MB + i, f));
     }
     {
       F vfr[EB], dnT[EH];
@@ -848,38 +879,47 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         for (int el = 0; el < EH; ++el) dWacc[mt][el] = mma(dWacc[mt][el], pf[mt], kT[el]);
     }
     if constexpr (FULL) {
-      // dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum(Pk)[s] for the wave's tile
-      // over all features (every slice's Pk from LDS; the rowsum from products
-      // with an all-ones operand), held for the next tile's store
-      const bf16x4 ke = G::KIND == kFavor ? *(const bf16x4*)&Ks[oR.a + 16 * h * LDQ + 16 * f] : bf16x4{};
+      // dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum(Pk)[s] for columns
+      // [16 f, 16 f + 16) over the features of slices 2 h, 2 h + 1 (both terms
+      // are sums over features, so the halves add up; the rowsum from products
+      // with an all-ones operand); the partner's row tile -> LDS, the own one
+      // held and completed in the next phase
+      bf16x4 ke[RT];
+#pragma unroll
+      for (int st = 0; st < RT; ++st)
+        ke[st] = G::KIND == kFavor ? *(const bf16x4*)&Ks[oR.a + 16 * st * LDQ + 16 * f] : bf16x4{};
       F ones;
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) ones[s2] = cvt<T>(1.f);
-      f32x4 acc = zero4(), rs = zero4();
-      // Pk of two slices at a time, read before their products
+      f32x4 acc[RT] = {}, rs[RT] = {};
+      // Pk of one slice at a time (both row tiles), read before its products
 #pragma unroll
-      for (int f0 = 0; f0 < 4; f0 += 2) {
-        F pa[2][MB];
+      for (int i = 0; i < 2; ++i) {
+        const T* Pks = (const T*)(arena + Lay::oP + (2 * h + i) * Lay::PAIR + Lay::pX);
+        F pa[RT][MB];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int st = 0; st < RT; ++st)
 #pragma unroll
-          for (int kb = 0; kb < MB; ++kb)
-            pa[i][kb] = sfrag_tr(oK, (const T*)(arena + Lay::oP + (f0 + i) * Lay::PAIR + Lay::pX), 32 * kb, 16 * h);
+          for (int kb = 0; kb < MB; ++kb) pa[st][kb] = sfrag_tr(oK, Pks, 32 * kb, 16 * st);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int st = 0; st < RT; ++st)
 #pragma unroll
           for (int kb = 0; kb < MB; ++kb) {
-            acc = mma(acc, Wc[(f0 + i) * MB + kb], pa[i][kb]);
-            if (G::KIND == kFavor) rs = mma(rs, ones, pa[i][kb]);
+            acc[st] = mma(acc[st], Wc[i * MB + kb], pa[st][kb]);
+            if (G::KIND == kFavor) rs[st] = mma(rs[st], ones, pa[st][kb]);
           }
       }
       if (G::KIND == kFavor) {
-        const float rsv = rs[0];  // every row of the product holds the sums of the columns s
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] += (float)ke[r] * (-rsv);
+        for (int st = 0; st < RT; ++st) {
+          const float rsv = rs[st][0];  // every row of the product holds the sums of the columns s
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[st][r] += (float)ke[st][r] * (-rsv);
+        }
       }
-      dk_hold = __builtin_bit_cast(u32e, pk_bf16x4(acc));
+      *part_y(1 - h) = h ? acc[0] : acc[1];
+      dk_part = h ? acc[1] : acc[0];
       dk_rs = range_rsrc(dKh + (size_t)start * D, (size_t)count * D * sizeof(T));
       dk_off = ((16 * h + c) * D + 16 * f + 4 * g) * (int)sizeof(T);
     } else {
@@ -930,8 +970,11 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     c = L.c;
     fresh_offsets();
 
-    // ---- dk = sum over slices (held; d = 32); rows of the next tile -> LDS (their readers are done)
-    if constexpr (!FULL) {
+    // ---- dk = sum over slices or feature halves (held); rows of the next
+    //      tile -> LDS (their readers are done)
+    if constexpr (FULL) {
+      dk_hold = __builtin_bit_cast(u32e, pk_bf16x4(dk_part + *part_y(h)));
+    } else {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
