@@ -126,9 +126,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   auto fresh_offsets = [&]() {
     asm volatile("" : "+v"(oR.a), "+v"(oR.b), "+v"(oK.a), "+v"(oK.b), "+v"(oF.a), "+v"(oF.b));
   };
-  // Both waves of a pair carry the ones column (z = sum K~ and its
-  // cotangent) with identical arithmetic, so they hold identical values and
-  // need no branches; only wave h = 0 writes it out.
+  // Only wave h = 0 of a pair carries the ones column (z = sum K~ and its
+  // cotangent): its products and its writes are skipped by wave h = 1.
   const bool zown = (h == 0);
   char* pz = arena + Lay::oP + f * Lay::PAIR;
   T* Zk = (T*)(pz + Lay::pZk);     // K~ as [m][s]
@@ -466,10 +465,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
       for (int el = 0; el < EH; ++el) nv[el] = neg(vfd[el]);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int el = 0; el < EH; ++el) S[mt][el] = mma(S[mt][el], kfd[mt], nv[el]);
-        Sz[mt] = mma(Sz[mt], kfd[mt], nones);
+      if (zown) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) Sz[mt] = mma(Sz[mt], kfd[mt], nones);
       }
     }
 
@@ -524,6 +525,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int tt = 0; tt < RT; ++tt) {
 #pragma unroll
       for (int el = 0; el <= EH; ++el) {
+        if (el == EH && !zown) break;
         f32x4 acc = mma(zero4(), el < EH ? vT[el < EH ? el : 0] : ones_frag(L, count), af[tt]);
 #pragma unroll
         for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
@@ -636,7 +638,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
       for (int el = 0; el < EH; ++el) sstore_tile_T(oF, ZS, S[mt][el], 16 * mt, e0 + 16 * el);
-      if (c == 0) {
+      if (zown && c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) zs[f * FW + 16 * mt + 4 * g + r] = Sz[mt][r];
       }
@@ -798,7 +800,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
       for (int el = 0; el < EH; ++el) sstore_tile_T(oF, ZG, Gs[mt][el], 16 * mt, e0 + 16 * el);
-      if (c == 0) {
+      if (zown && c == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) dzs[f * FW + 16 * mt + 4 * g + r] = Gz[mt][r];
       }
@@ -848,7 +850,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         acc = mma(acc, daT, qf);
 #pragma unroll
         for (int el = 0; el < EH; ++el) Gs[mt][el] = mma(Gs[mt][el], qf, dnT[el]);
-        Gz[mt] = mma(Gz[mt], qf, dd);
+        if (zown) Gz[mt] = mma(Gz[mt], qf, dd);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
