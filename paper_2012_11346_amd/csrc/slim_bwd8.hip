@@ -517,8 +517,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
       af[tt] = tile_pair_frag<T>(At[0][tt], At[1][tt]);
-      sstore_half_T(oK, ZA, frag_lo(af[tt]), 0, 16 * tt);
-      sstore_half_T(oK, ZA, frag_hi(af[tt]), 16, 16 * tt);
+      if (zown) {  // (both waves of the pair hold the same scores)
+        sstore_half_T(oK, ZA, frag_lo(af[tt]), 0, 16 * tt);
+        sstore_half_T(oK, ZA, frag_hi(af[tt]), 16, 16 * tt);
+      }
     }
     // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
 #pragma unroll
