@@ -121,7 +121,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path runs on a single "
-              "MI355X; see DESIGN.md for how it would shard)", file=sys.stderr)
+              "MI355X; sharded, GPUs would split the heads and batch rows and sum dW with one all-reduce)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
