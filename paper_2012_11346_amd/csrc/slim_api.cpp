@@ -108,7 +108,7 @@ int count_tiles(const slim_problem* p) {
 // in parallel and are stitched together by exact scans of their states.  The
 // count depends on B*H and the device size, not on L once L is long enough,
 // so workspace stays flat in L.  It is rounded down, so that the workgroups
-// fit the device in one round.  SLIM_SEGMENTS (debugging) forces a count.
+// are all resident on the device at once.  SLIM_SEGMENTS (debugging) forces a count.
 int plan_segments_for(const slim_problem* p, int target) {
   const int n_tiles = count_tiles(p);
   const char* env = getenv("SLIM_SEGMENTS");
