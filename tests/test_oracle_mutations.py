@@ -103,6 +103,20 @@ def _slim_bwd_no_downdate(Q, K, V, W, dY, C, kind, R_N, S_N, gR=None, gS=None, w
 _REAL_BWD = S.slim_backward_head
 
 
+def _pack_no_transpose(R, S_):
+    # R [.., d, M] laid out without the swap (only shape-compatible when d = M)
+    return np.concatenate([R, S_[..., None]], axis=-1)
+
+
+def _unpack_ones_first(P_):
+    P_ = S._f64(P_)
+    return np.swapaxes(P_[..., 1:], -1, -2), P_[..., 0]
+
+
+def _logits_transposed_w(X, W):
+    return S._f64(X) @ S._f64(W)
+
+
 MUTANTS = [
     ("feature_map", _favor_no_sqrtM, lambda: P.test_favor_plus_is_unbiased_for_the_exponential_kernel()),
     ("feature_map", _favor_sign_flip, lambda: P.test_favor_plus_is_unbiased_for_the_exponential_kernel()),
@@ -115,6 +129,9 @@ MUTANTS = [
     ("iterative_backward_features", _iter_bwd_printed, lambda: P.test_token_recurrence_equals_definition()),
     ("slim_backward_head", _slim_bwd_no_downdate,
      lambda: P.test_slicewise_equals_definition_for_every_slice_length(S.FAVOR_PLUS, "quadratic", 3)),
+    ("pack_state", _pack_no_transpose, lambda: P.test_state_layout_written_out_by_loops()),
+    ("unpack_state", _unpack_ones_first, lambda: P.test_state_layout_written_out_by_loops()),
+    ("feature_logits", _logits_transposed_w, lambda: P.test_feature_logits_written_out_by_loops()),
 ]
 
 

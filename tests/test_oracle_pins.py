@@ -285,3 +285,81 @@ def test_token_recurrence_equals_definition():
     r = O.quadratic_backward_features(Qf, Kf, V, dY)
     for g, ref in zip((dQf, dKf, dV), r):
         assert _rel(g, ref) < 1e-12
+
+
+# ---------------------------------------------------------------- state layout and logits, element by element
+
+
+def test_state_layout_written_out_by_loops():
+    """pack_state / unpack_state against the [B, H, M, d + 1] layout written
+    out entry by entry: row m of a head holds sum_l g(K_l)_m V_l[e] in column
+    e < d and sum_l g(K_l)_m in column d (the layout the library's state
+    tensors use, eqs. 14-16)."""
+    rng = np.random.default_rng(21)
+    Bn, Hn, L, d, M = 2, 3, 5, 3, 4
+    Kf = rng.random((Bn, Hn, L, M)) + 0.1
+    V = rng.standard_normal((Bn, Hn, L, d))
+    expect = np.zeros((Bn, Hn, M, d + 1))
+    for b in range(Bn):
+        for h in range(Hn):
+            for m in range(M):
+                for e in range(d):
+                    for l in range(L):
+                        expect[b, h, m, e] += Kf[b, h, l, m] * V[b, h, l, e]
+                for l in range(L):
+                    expect[b, h, m, d] += Kf[b, h, l, m]
+    # R [.., d, M] = sum_l V_l g(K_l)^T and S [.., M] = sum_l g(K_l), formed by loops as well
+    R = np.zeros((Bn, Hn, d, M))
+    S = np.zeros((Bn, Hn, M))
+    for b in range(Bn):
+        for h in range(Hn):
+            for l in range(L):
+                for e in range(d):
+                    for m in range(M):
+                        R[b, h, e, m] += V[b, h, l, e] * Kf[b, h, l, m]
+                S[b, h] += Kf[b, h, l]
+    packed = O.pack_state(R, S)
+    assert packed.shape == (Bn, Hn, M, d + 1)
+    assert _rel(packed, expect) < 1e-14
+    R2, S2 = O.unpack_state(expect)
+    assert _rel(R2, R) < 1e-14 and _rel(S2, S) < 1e-14
+    # the forward sweep's final state is that sum
+    W = orthogonal_gaussian_features(M, d, rng)
+    Q = rng.standard_normal((Bn, Hn, L, d)) * 0.5
+    Kx = rng.standard_normal((Bn, Hn, L, d)) * 0.5
+    _, st = O.slim_forward(Q, Kx, V, W, 2, O.RELU)
+    phi = np.zeros((Bn, Hn, L, M))
+    for b in range(Bn):
+        for h in range(Hn):
+            for l in range(L):
+                for m in range(M):
+                    phi[b, h, l, m] = max(sum(W[m, e] * Kx[b, h, l, e] for e in range(d)), 0.0) + O.RELU_EPS
+    for b in range(Bn):
+        for h in range(Hn):
+            for m in range(M):
+                assert abs(st[b, h, m, d] - phi[b, h, :, m].sum()) < 1e-12
+                for e in range(d):
+                    ref = sum(phi[b, h, l, m] * V[b, h, l, e] for l in range(L))
+                    assert abs(st[b, h, m, e] - ref) < 1e-12
+
+
+def test_feature_logits_written_out_by_loops():
+    """feature_logits(X, W)[.., l, m] = sum_e W[m, e] X[.., l, e], and the
+    FAVOR+ map is exp of it minus |x|^2 / 2, over sqrt(M) (Sec. 2.1)."""
+    rng = np.random.default_rng(22)
+    X = rng.standard_normal((2, 3, 4))
+    W = rng.standard_normal((5, 4))
+    Z = O.feature_logits(X, W)
+    assert Z.shape == (2, 3, 5)
+    Phi = O.feature_map(X, W, O.FAVOR_PLUS)
+    for i in range(2):
+        for l in range(3):
+            n2 = sum(X[i, l, e] ** 2 for e in range(4))
+            for m in range(5):
+                z = sum(W[m, e] * X[i, l, e] for e in range(4))
+                assert abs(Z[i, l, m] - z) < 1e-13
+                assert abs(Phi[i, l, m] - math.exp(z - n2 / 2) / math.sqrt(5)) < 1e-13 * Phi[i, l, m] + 1e-300
+    # a hand-checked value: x = (1, 2), w = (3, -1): w.x = 1, |x|^2/2 = 2.5
+    assert O.feature_logits(np.array([[1.0, 2.0]]), np.array([[3.0, -1.0]]))[0, 0] == 1.0
+    assert abs(O.feature_map(np.array([[1.0, 2.0]]), np.array([[3.0, -1.0]]), O.FAVOR_PLUS)[0, 0]
+               - math.exp(-1.5)) < 1e-15
