@@ -69,12 +69,18 @@ def feature_map(X, W, kind: str, relu_eps: float = RELU_EPS) -> np.ndarray:
     raise ValueError(kind)
 
 
-def feature_map_vjp(X, W, Phi, dPhi, kind: str) -> Tuple[np.ndarray, np.ndarray]:
+def feature_map_vjp(X, W, Phi, dPhi, kind: str, mask_W=None) -> Tuple[np.ndarray, np.ndarray]:
     """Chain rule through g for one head: returns (dX [L, d], dW [M, d]).
 
     FAVOR+: d phi_m / dx = phi_m (w_m - x), d phi_m / dw_m = phi_m x.
     ReLU:   d phi_m / dx = [w_m . x > 0] w_m, d phi_m / dw_m = [w_m . x > 0] x
             (derivative 0 taken at w_m . x = 0).
+
+    The ReLU derivative is a 0/1 decision on the sign of w_m . x.  `mask_W`
+    (default W) is the matrix that decision is taken with: a caller
+    comparing against an implementation that forms w_m . x from a rounded W
+    passes that rounded W here, so that both sides decide in the same
+    precision (the gradient itself always uses W).
     """
     X = _f64(X)
     W = _f64(W)
@@ -82,7 +88,8 @@ def feature_map_vjp(X, W, Phi, dPhi, kind: str) -> Tuple[np.ndarray, np.ndarray]
         Gm = dPhi * Phi
         dX = Gm @ W - X * Gm.sum(axis=-1, keepdims=True)
     elif kind == RELU:
-        Gm = dPhi * ((X @ W.T) > 0.0)
+        Wd = W if mask_W is None else _f64(mask_W)
+        Gm = dPhi * ((X @ Wd.T) > 0.0)
         dX = Gm @ W
     else:
         raise ValueError(kind)
@@ -133,10 +140,11 @@ def attention_forward(Q, K, V, W, kind: str, relu_eps: float = RELU_EPS) -> np.n
     return Y
 
 
-def attention_backward(Q, K, V, W, dY, kind: str, relu_eps: float = RELU_EPS):
+def attention_backward(Q, K, V, W, dY, kind: str, relu_eps: float = RELU_EPS, mask_W=None):
     """(dQ, dK, dV, dW) of sum(dY * Y) for the definition (eq. 2).
 
     dW sums the query and key branches over every (b, h) and row.
+    `mask_W`: see feature_map_vjp.
     """
     Q, K, V, dY, W = _f64(Q), _f64(K), _f64(V), _f64(dY), _f64(W)
     dQ = np.empty_like(Q)
@@ -148,8 +156,8 @@ def attention_backward(Q, K, V, W, dY, kind: str, relu_eps: float = RELU_EPS):
             Qf = feature_map(Q[b, h], W, kind, relu_eps)
             Kf = feature_map(K[b, h], W, kind, relu_eps)
             dQf, dKf, dV[b, h] = quadratic_backward_features(Qf, Kf, V[b, h], dY[b, h])
-            dQ[b, h], dWq = feature_map_vjp(Q[b, h], W, Qf, dQf, kind)
-            dK[b, h], dWk = feature_map_vjp(K[b, h], W, Kf, dKf, kind)
+            dQ[b, h], dWq = feature_map_vjp(Q[b, h], W, Qf, dQf, kind, mask_W)
+            dK[b, h], dWk = feature_map_vjp(K[b, h], W, Kf, dKf, kind, mask_W)
             dW += dWq + dWk
     return dQ, dK, dV, dW
 
@@ -228,7 +236,7 @@ def slim_forward_head(Q, K, V, W, C: int, kind: str, R0=None, S0=None, within: s
 
 
 def slim_backward_head(Q, K, V, W, dY, C: int, kind: str, R_N, S_N, gR=None, gS=None,
-                       within: str = "ps", relu_eps: float = RELU_EPS):
+                       within: str = "ps", relu_eps: float = RELU_EPS, mask_W=None):
     """Backward sweep of Algorithm 1 for one head.
 
     Starts from B^(N) = (R_N, S_N), the state the forward sweep returned,
@@ -298,8 +306,8 @@ def slim_backward_head(Q, K, V, W, dY, C: int, kind: str, R_N, S_N, gR=None, gS=
             gS = gS + Qf.T @ dD
         else:
             raise ValueError(within)
-        dQ[a:b], dWq = feature_map_vjp(Q[a:b], W, Qf, dQf, kind)
-        dK[a:b], dWk = feature_map_vjp(K[a:b], W, Kf, dKf, kind)
+        dQ[a:b], dWq = feature_map_vjp(Q[a:b], W, Qf, dQf, kind, mask_W)
+        dK[a:b], dWk = feature_map_vjp(K[a:b], W, Kf, dKf, kind, mask_W)
         dV[a:b] = dVs
         dW += dWq + dWk
     return dQ, dK, dV, dW, gR, gS
@@ -344,7 +352,7 @@ def slim_forward(Q, K, V, W, C: int, kind: str, state_in=None, within: str = "ps
 
 
 def slim_backward(Q, K, V, W, dY, C: int, kind: str, state_out, dstate_out=None, within: str = "ps",
-                  relu_eps: float = RELU_EPS):
+                  relu_eps: float = RELU_EPS, mask_W=None):
     """Algorithm 1 backward for [B, H, L, d] inputs.
 
     `state_out` is B^(N) from slim_forward; `dstate_out` is G^(N) (zero if
@@ -365,7 +373,7 @@ def slim_backward(Q, K, V, W, dY, C: int, kind: str, state_out, dstate_out=None,
             if dstate_out is not None:
                 gR, gS = unpack_state(_f64(dstate_out)[b, h])
             dQ[b, h], dK[b, h], dV[b, h], dWh, gR, gS = slim_backward_head(
-                Q[b, h], K[b, h], V[b, h], W, dY[b, h], C, kind, R_N, S_N, gR, gS, within, relu_eps)
+                Q[b, h], K[b, h], V[b, h], W, dY[b, h], C, kind, R_N, S_N, gR, gS, within, relu_eps, mask_W)
             dW += dWh
             gst[b, h] = pack_state(gR, gS)
     return dQ, dK, dV, dW, gst

@@ -176,15 +176,25 @@ int fwd_parts(const slim_problem* p) { return plan_fwd_segments(p); }
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
-// forward workspace: segment sums and shifts, segment starts and shifts
+size_t wfrag_bytes_of(const slim_problem* p);
+
+// forward workspace: W in fragment order (bf16 problems), segment sums and
+// shifts, segment starts and shifts
 struct FwdLayout {
-  size_t seg_sum, seg_shift, starts, start_shift, total;
+  size_t wfrag, seg_sum, seg_shift, starts, start_shift, total;
 };
 FwdLayout fwd_layout(const slim_problem* p, int P) {
-  FwdLayout l{0, 0, 0, 0, 0};
-  if (P <= 1) return l;
-  const size_t n = (size_t)p->B * p->H * (has_ksum(p) ? P : P * plan_sum_split(p, P));
+  FwdLayout l{0, 0, 0, 0, 0, 0};
   size_t off = 0;
+  if (p->dtype == SLIM_BF16) {
+    l.wfrag = off;
+    off += align256(wfrag_bytes_of(p));
+  }
+  if (P <= 1) {
+    l.total = off;
+    return l;
+  }
+  const size_t n = (size_t)p->B * p->H * (has_ksum(p) ? P : P * plan_sum_split(p, P));
   l.seg_sum = off;
   off += align256(n * state_elems(p) * sizeof(float));
   l.seg_shift = off;
@@ -402,7 +412,13 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
   return ok();
 }
 
-int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+}  // extern "C"
+
+namespace {
+
+// The forward of slim_fwd on a given workspace (the caller's, or the
+// library's static scratch for slim_fwd_noalloc).
+int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, float* ctx,
              void* ws, size_t ws_bytes, void* stream) {
   int st = check_problem(p);
@@ -437,6 +453,15 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.P = P;
   a.relu_eps = p->relu_eps;
   hipError_t e = hipSuccess;
+  if (p->dtype == SLIM_BF16) {
+    // W in fragment order, with the low parts of its bf16 split (logits)
+    slim::WfragArgs wf;
+    wf.W = W;
+    wf.out = w + lay.wfrag;
+    e = dp.wfrag(wf, s);
+    if (e != hipSuccess) return hip_fail(e, "W-fragment launch");
+    a.Wfrag = wf.out;
+  }
   if (P > 1 && dp.ksum != nullptr) {
     // One key shift for the whole head: (0) the largest key exponent of every
     // part and of the initial state; (1) what each part adds relative to it;
@@ -449,6 +474,7 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     ks.K = K;
     ks.V = V;
     ks.W = W;
+    ks.Wfrag = a.Wfrag;
     ks.B = (int)p->B;
     ks.H = (int)p->H;
     ks.L = (int)p->L;
@@ -532,6 +558,16 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   return ok();
 }
 
+}  // namespace
+
+extern "C" {
+
+int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+             const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, float* ctx,
+             void* ws, size_t ws_bytes, void* stream) {
+  return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ctx, ws, ws_bytes, stream);
+}
+
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
              const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
@@ -580,6 +616,13 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   //     (2) exact states at the segment boundaries.  Both come from the
   //     forward's context when the caller passes it.
   const int S2 = plan_sum_split(p, P), P2 = P * S2;
+  // W in fragment order (with the low parts of its bf16 split), for every
+  // kernel below
+  slim::WfragArgs wf;
+  wf.W = W;
+  wf.out = w + lay.wfrag;
+  e = dp.wfrag(wf, s);
+  if (e != hipSuccess) return hip_fail(e, "W-fragment launch");
   const float* bounds = ctx;
   if (bounds == nullptr) {
   if (dp.ksum != nullptr) {
@@ -588,6 +631,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     ks.K = K;
     ks.V = V;
     ks.W = W;
+    ks.Wfrag = wf.out;
     ks.shift = favor ? kshift : nullptr;
     ks.out = (float*)(w + lay.seg_sum);
     ks.B = (int)p->B;
@@ -620,13 +664,8 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
   bounds = sc.out;
   }
-  // (3) W in fragment order, then the reverse walk of every segment; each
-  //     starts from a zero cotangent except the last (dstate_out)
-  slim::WfragArgs wf;
-  wf.W = W;
-  wf.out = w + lay.wfrag;
-  e = dp.wfrag(wf, s);
-  if (e != hipSuccess) return hip_fail(e, "W-fragment launch");
+  // (3) the reverse walk of every segment; each starts from a zero
+  //     cotangent except the last (dstate_out)
   slim::BwdArgs a;
   std::memset(&a, 0, sizeof(a));
   a.Q = Q;

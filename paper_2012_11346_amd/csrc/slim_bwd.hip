@@ -176,11 +176,15 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   for (int j = j1 - 1; j >= j0; --j) {
     int start, count;
     tm.tile(j, start, count);
-    F Wf[MT][EB];
+    // W of this wave's features for the logits, with the low parts of a bf16 split
+    F Wf[MT][EB], Wl[MT][EB];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = Wfr[WL::a(w, mt, kb) * 64 + lane];
+      for (int kb = 0; kb < EB; ++kb) {
+        Wf[mt][kb] = Wfr[WL::a(w, mt, kb) * 64 + lane];
+        if constexpr (kSplitW<T>) Wl[mt][kb] = Wfr[WL::alo(w, mt, kb) * 64 + lane];
+      }
     sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr, threadIdx.x);
     sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, threadIdx.x);
     sv.template store<LDQ>(Vs, nullptr, threadIdx.x);
@@ -206,6 +210,10 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           f32x4 acc = {init, init, init, init};
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(Qs, LDQ, 16 * tt, 32 * kb));
+          if constexpr (kSplitW<T>) {
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wl[mt][kb], frag_rm(Qs, LDQ, 16 * tt, 32 * kb));
+          }
           Lq[mt][tt] = acc;
         }
       }
@@ -219,6 +227,10 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           f32x4 acc = init;
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, frag_rm(Ks, LDQ, 16 * st, 32 * kb), Wf[mt][kb]);
+          if constexpr (kSplitW<T>) {
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) acc = mma(acc, frag_rm(Ks, LDQ, 16 * st, 32 * kb), Wl[mt][kb]);
+          }
           Lk[st][mt] = acc;
         }
       }

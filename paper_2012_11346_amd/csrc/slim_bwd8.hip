@@ -329,6 +329,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     //      K~ -> Zk[m][s], row maxima of the query logits -> qmx[t][2 f + h]
     f32x4 Lq[MH][RT];  // rows m = 16 (MH h + i) + 4 g + r, columns t = 16 tt + c
     {
+      // low parts of the logits' W fragments (bf16 split of the float32 W),
+      // fetched here and used after every high-part product of the phase
+      F Wl[MH][EB];
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) Wl[i][kb] = wfrag(WL::alo(f, MH * h + i, kb));
       // raw logits w.q: the query row shift max_m(w.q - |q|^2/2) absorbs the norm term
       F qfr[RT][EB];
 #pragma unroll
@@ -344,6 +351,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[i][kb], qfr[tt][kb]);
           Lq[i][tt] = acc;
         }
+      // the low-part products of the queries
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt)
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) Lq[i][tt] = mma(Lq[i][tt], Wl[i][kb], qfr[tt][kb]);
       // key rows: exp2(log2e (w.k - |k|^2/2 - shift) - log2(M)/2), the row term folded into the exponent
       // (rows past the tile: an infinite offset gives exactly zero features)
       float kc[RT][4];
@@ -363,6 +377,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       for (int st = 0; st < RT; ++st)
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb) kfr[st][kb] = sfrag_rm(oR, Ks, 16 * st, 32 * kb);
+      f32x4 Lk[MH][RT];
 #pragma unroll
       for (int i = 0; i < MH; ++i)
 #pragma unroll
@@ -370,6 +385,20 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
           f32x4 kv = zero4();
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) kv = mma(kv, kfr[st][kb], Wf[i][kb]);
+          Lk[i][st] = kv;
+        }
+      // the low-part products of the keys
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int st = 0; st < RT; ++st)
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) Lk[i][st] = mma(Lk[i][st], kfr[st][kb], Wl[i][kb]);
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int st = 0; st < RT; ++st) {
+          f32x4 kv = Lk[i][st];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             if (G::KIND == kFavor) {

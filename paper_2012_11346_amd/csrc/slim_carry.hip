@@ -98,12 +98,16 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
       v[i] = __builtin_amdgcn_raw_buffer_load_b128(wrs, lane * (int)sizeof(F) + 16 * i, idx * 64 * (int)sizeof(F), 0);
     return __builtin_bit_cast(F, v);
   };
+  F Wl[MT][EB];  // low parts of Wf (bf16 split of the float32 W)
   F Wf[MT][EB];  // slot s = W[w FW + 16 mt + c][32 kb + kp]: K~ of this wave's features
   F Wc[KB];      // slot s = W[32 kb + kp][16 eo + c]: dk of this wave's column tile
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int kb = 0; kb < EB; ++kb) Wf[mt][kb] = wfrag(WL::a(w, mt, kb));
+    for (int kb = 0; kb < EB; ++kb) {
+      Wf[mt][kb] = wfrag(WL::a(w, mt, kb));
+      if constexpr (kSplitW<T>) Wl[mt][kb] = wfrag(WL::alo(w, mt, kb));
+    }
 #pragma unroll
   for (int kb = 0; kb < KB; ++kb) Wc[kb] = wfrag(WL::c(kb, eo));
 
@@ -188,6 +192,10 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
           f32x4 acc = zero4();
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wf[mt][kb], kfr[kb]);
+          if constexpr (kSplitW<T>) {
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wl[mt][kb], kfr[kb]);
+          }
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             acc[r] = (G::KIND == kFavor) ? fast_exp2(acc[r] * kLog2e - kc) : (col_ok ? fmaxf(acc[r], 0.f) + a.relu_eps : 0.f);

@@ -283,6 +283,14 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
 
     int b0 = 0, b1 = 1, z = 0;  // row buffer of this chunk and of the next; K~/Pk buffer
     for (int it = 0; it < n_run; ++it) {
+      // low parts of the logits' W fragments (bf16 split of the float32 W),
+      // read from the table at every chunk ahead of the row prefetch, so that
+      // waiting for them does not wait for the rows
+      F Wl[MT][EB];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int kb = 0; kb < EB; ++kb) Wl[mt][kb] = wfrag(WL::alo(w >> 1, (w & 1) * MT + mt, kb));
       // rows of chunk it + 1 into their buffer, rows of chunk it + 2 into
       // registers
       put_rows(b1);
@@ -328,6 +336,10 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
             f32x4 x = zero4();
 #pragma unroll
             for (int kb = 0; kb < EB; ++kb) x = mma(x, Wf[mt][kb], kf[st][kb]);
+            if constexpr (kSplitW<T>) {
+#pragma unroll
+              for (int kb = 0; kb < EB; ++kb) x = mma(x, Wl[mt][kb], kf[st][kb]);
+            }
             f32x4 dk = f32x4{gz[mt][0], gz[mt][1], gz[mt][2], gz[mt][3]};
 #pragma unroll
             for (int kb = 0; kb < EB; ++kb) dk = mma(dk, GA[mt][kb], vf[st][kb]);

@@ -46,16 +46,20 @@ struct Cfg {
 //   block B  [wave][kb][et]: slot s = W[w FW + 32 kb + kp(g, s)][16 et + c]   (contracting over features)
 //   block C  [kb][et], after the waves' blocks: slot s = W[32 kb + kp(g, s)][16 et + c]
 //            (contracting over all M features)
+//   block A' [wave][mt][kb], after block C (bf16 only): the low parts w_lo of
+//            block A's entries, for the second product of the logits
 template <class G>
 struct WFragLayout {
   static constexpr int NA = G::MT * G::EB;  // fragments of block A per wave
   static constexpr int NB = G::MB * G::ET;  // fragments of block B per wave
   static constexpr int PER_WAVE = NA + NB;
   static constexpr int NC = (G::M / 32) * G::ET;  // fragments of block C
-  static constexpr int TOTAL = 4 * PER_WAVE + NC;  // fragments
+  static constexpr int NLO = kSplitW<typename G::T> ? 4 * NA : 0;  // fragments of block A'
+  static constexpr int TOTAL = 4 * PER_WAVE + NC + NLO;  // fragments
   __device__ static int a(int w, int mt, int kb) { return w * PER_WAVE + mt * G::EB + kb; }
   __device__ static int b(int w, int kb, int et) { return w * PER_WAVE + NA + kb * G::ET + et; }
   __device__ static int c(int kb, int et) { return 4 * PER_WAVE + kb * G::ET + et; }
+  __device__ static int alo(int w, int mt, int kb) { return 4 * PER_WAVE + NC + w * NA + mt * G::EB + kb; }
 };
 
 // Row range of tile j of a head, for slices of length C (already clamped to

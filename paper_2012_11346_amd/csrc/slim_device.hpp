@@ -115,6 +115,20 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bf16x2 pk_bf16(float a, float b) { return __builtin_convertvector(f32x2{a, b}, bf16x2); }
 __device__ __forceinline__ bf16x4 pk_bf16x4(const f32x4& x) { return __builtin_convertvector(x, bf16x4); }
 
+// W enters the logits w_m . x as a pair of bf16 values, hi = RNE(w) and
+// lo = RNE(w - hi), each with its own product against the bf16 row x: the
+// pair carries about 16 significant bits of the float32 W, so the logits are
+// those of the caller's W to ~2^-17 of sum_e |x_e w_e| instead of 2^-9 (an
+// error that exp would turn into a relative error of the features).
+// kSplitW<T> says whether the element type needs the second product.
+template <typename T>
+constexpr bool kSplitW = sizeof(T) == 2;
+template <typename T>
+__device__ __forceinline__ T w_lo(float x) {
+  if constexpr (sizeof(T) == 2) return (T)(x - (float)(T)x);
+  else return (T)0.f;
+}
+
 // ------------------------------------------------------------- fragments
 
 template <typename T>

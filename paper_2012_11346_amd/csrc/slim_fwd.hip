@@ -20,8 +20,11 @@
 
 namespace slim {
 
+// W fragments of wave w's features for the logits: Wf the bf16 values of W,
+// Wl their low parts (bf16 problems; unused for fp32)
 template <class G>
 __device__ __forceinline__ void load_w_frags(typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+                                             typename FragT<typename G::T>::type (&Wl)[G::MT][G::EB],
                                              const float* W, int w) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
@@ -29,8 +32,11 @@ __device__ __forceinline__ void load_w_frags(typename FragT<typename G::T>::type
 #pragma unroll
     for (int kb = 0; kb < G::EB; ++kb)
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
-        Wf[mt][kb][s] = cvt<typename G::T>(W[(size_t)(w * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)]);
+      for (int s = 0; s < 8; ++s) {
+        const float x = W[(size_t)(w * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)];
+        Wf[mt][kb][s] = cvt<typename G::T>(x);
+        Wl[mt][kb][s] = w_lo<typename G::T>(x);
+      }
 }
 
 // operand fragment of [V|1] over rows [k0, k0 + 32) for value tile et (et ==
@@ -54,14 +60,21 @@ __device__ __forceinline__ typename FragT<typename G::T>::type v_frag(const Lane
 template <class G>
 __device__ __forceinline__ void query_logits(const Lane& L, f32x4 (&Lq)[G::MT][G::RT],
                                              const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+                                             const typename FragT<typename G::T>::type (&Wl)[G::MT][G::EB],
                                              const typename G::T* Qs) {
 #pragma unroll
   for (int tt = 0; tt < G::RT; ++tt) {
+    typename FragT<typename G::T>::type qf[G::EB];
+#pragma unroll
+    for (int kb = 0; kb < G::EB; ++kb) qf[kb] = frag_rm(L, Qs, G::LDQ, 16 * tt, 32 * kb);
 #pragma unroll
     for (int mt = 0; mt < G::MT; ++mt) {
       f32x4 acc = zero4();
 #pragma unroll
-      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, Wf[mt][kb], frag_rm(L, Qs, G::LDQ, 16 * tt, 32 * kb));
+      for (int kb = 0; kb < G::EB; ++kb) {
+        if constexpr (kSplitW<typename G::T>) acc = mma(acc, Wl[mt][kb], qf[kb]);
+        acc = mma(acc, Wf[mt][kb], qf[kb]);
+      }
       Lq[mt][tt] = acc;
     }
   }
@@ -72,6 +85,7 @@ __device__ __forceinline__ void query_logits(const Lane& L, f32x4 (&Lq)[G::MT][G
 template <class G>
 __device__ __forceinline__ void key_logits(const Lane& L, f32x4 (&Lk)[G::RT][G::MT],
                                            const typename FragT<typename G::T>::type (&Wf)[G::MT][G::EB],
+                                           const typename FragT<typename G::T>::type (&Wl)[G::MT][G::EB],
                                            const typename G::T* Ks) {
 #pragma unroll
   for (int st = 0; st < G::RT; ++st) {
@@ -82,7 +96,10 @@ __device__ __forceinline__ void key_logits(const Lane& L, f32x4 (&Lk)[G::RT][G::
     for (int mt = 0; mt < G::MT; ++mt) {
       f32x4 acc = zero4();
 #pragma unroll
-      for (int kb = 0; kb < G::EB; ++kb) acc = mma(acc, kf[kb], Wf[mt][kb]);
+      for (int kb = 0; kb < G::EB; ++kb) {
+        if constexpr (kSplitW<typename G::T>) acc = mma(acc, kf[kb], Wl[mt][kb]);
+        acc = mma(acc, kf[kb], Wf[mt][kb]);
+      }
       Lk[st][mt] = acc;
     }
   }
@@ -116,8 +133,19 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   const T* Kh = (const T*)a.K + head * (size_t)a.L * D;
   const T* Vh = (const T*)a.V + head * (size_t)a.L * D;
 
-  F Wf[MT][EB];
-  load_w_frags<G>(Wf, a.W, w);
+  // W of this wave's features for the logits: the bf16 values in registers;
+  // the low parts (bf16 problems) in registers too, or, with 64 features per
+  // wave and queries (where registers are short), read from the fragment
+  // table a.Wfrag at every tile, behind the products of the high parts
+  constexpr bool LO_TABLE = kSplitW<T> && MT == 4 && QSIDE;
+  constexpr int MR = LO_TABLE ? 1 : MT, ER = LO_TABLE ? 1 : EB;
+  F Wf[MR][ER], Wl[MR][ER];
+  if constexpr (!LO_TABLE) load_w_frags<G>(Wf, Wl, a.W, w);
+  // (table form: both parts of the fragments of half of the features at a
+  // time, fetched at the start of every tile)
+  typedef WFragLayout<G> WL;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.Wfrag), (short)0, LO_TABLE ? (int)(WL::TOTAL * 64 * sizeof(F)) : 0, 0x00020000);
 
   // running state of this wave's features: S[mt][et] rows m, columns e;
   // S[mt][ET] holds z replicated over its 16 columns
@@ -202,8 +230,53 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     const float* kn = knb[bf];
 
     f32x4 Lq[QSIDE ? MT : 1][RT], Lk[RT][MT];
-    if constexpr (QSIDE) query_logits<G>(L, Lq, Wf, Qs);
-    key_logits<G>(L, Lk, Wf, Ks);
+    if constexpr (LO_TABLE) {
+      // per half of the feature tiles: both parts of W from the table, then
+      // the high-part and low-part products (row operands re-read from LDS)
+      typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+      const int wlane = (fresh_tid() & 63) * (int)sizeof(F);
+#pragma unroll
+      for (int m2 = 0; m2 < MT; m2 += 2) {
+        F Wh[2][EB], Wt[2][EB];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) {
+            Wh[i][kb] = __builtin_bit_cast(
+                F, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, WL::a(w, m2 + i, kb) * 64 * (int)sizeof(F), 0));
+            Wt[i][kb] = __builtin_bit_cast(
+                F, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, WL::alo(w, m2 + i, kb) * 64 * (int)sizeof(F), 0));
+          }
+#pragma unroll
+        for (int tt = 0; tt < RT; ++tt) {
+          F qf[EB], kf[EB];
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) {
+            qf[kb] = frag_rm(L, Qs, LDQ, 16 * tt, 32 * kb);
+            kf[kb] = frag_rm(L, Ks, LDQ, 16 * tt, 32 * kb);
+          }
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            f32x4 q = zero4(), k = zero4();
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) {
+              q = mma(q, Wh[i][kb], qf[kb]);
+              k = mma(k, kf[kb], Wh[i][kb]);
+            }
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) {
+              q = mma(q, Wt[i][kb], qf[kb]);
+              k = mma(k, kf[kb], Wt[i][kb]);
+            }
+            Lq[m2 + i][tt] = q;
+            Lk[tt][m2 + i] = k;
+          }
+        }
+      }
+    } else {
+      if constexpr (QSIDE) query_logits<G>(L, Lq, Wf, Wl, Qs);
+      key_logits<G>(L, Lk, Wf, Wl, Ks);
+    }
 
     if (G::KIND == kFavor) {
       if constexpr (QSIDE) {
@@ -467,15 +540,15 @@ __global__ __launch_bounds__(256, 1) void key_shift_kernel(FeatArgs a) {
   const int w = wave_id(), g = lane_g();
   const size_t head = (size_t)blockIdx.z * a.H + blockIdx.y;
   const T* Kh = (const T*)a.X + head * (size_t)a.L * D;
-  F Wf[MT][EB];
-  load_w_frags<G>(Wf, a.W, w);
+  F Wf[MT][EB], Wl[MT][EB];
+  load_w_frags<G>(Wf, Wl, a.W, w);
   float best = -INFINITY;
   for (int start = 0; start < a.L; start += TR) {
     const int count = min(TR, a.L - start);
     load_rows<T, D, TR, LDQ, 256>(Ks, Kh + (size_t)start * D, count, kn);
     __syncthreads();
     f32x4 Lk[RT][MT];
-    key_logits<G>(this_lane(), Lk, Wf, Ks);
+    key_logits<G>(this_lane(), Lk, Wf, Wl, Ks);
 #pragma unroll
     for (int st = 0; st < RT; ++st)
 #pragma unroll
@@ -507,14 +580,14 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
   const int count = min(TR, a.L - start);
   const T* Xh = (const T*)a.X + head * (size_t)a.L * D;
   float* Ph = a.phi + head * (size_t)a.L * M;
-  F Wf[MT][EB];
-  load_w_frags<G>(Wf, a.W, w);
+  F Wf[MT][EB], Wl[MT][EB];
+  load_w_frags<G>(Wf, Wl, a.W, w);
   load_rows<T, D, TR, LDQ, 256>(Xs, Xh + (size_t)start * D, count, G::KIND == kFavor ? xn : nullptr);
   __syncthreads();
   const float half_log2M = 0.5f * __log2f((float)M);
   if (a.role == 0) {
     f32x4 Lq[MT][RT];
-    query_logits<G>(this_lane(), Lq, Wf, Xs);
+    query_logits<G>(this_lane(), Lq, Wf, Wl, Xs);
     if (G::KIND == kFavor) {
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
@@ -549,7 +622,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
     }
   } else {
     f32x4 Lk[RT][MT];
-    key_logits<G>(this_lane(), Lk, Wf, Xs);
+    key_logits<G>(this_lane(), Lk, Wf, Wl, Xs);
     const float ks = (G::KIND == kFavor) ? a.shift[head] : 0.f;
 #pragma unroll
     for (int st = 0; st < RT; ++st)
@@ -579,7 +652,15 @@ __global__ __launch_bounds__(64) void wfrag_kernel(WfragArgs a) {
   const int w = f / WL::PER_WAVE;
   int i = f - w * WL::PER_WAVE;
   F v;
-  if (w >= 4) {
+  if (f >= 4 * WL::PER_WAVE + WL::NC) {
+    // block A': low parts of block A
+    i = f - 4 * WL::PER_WAVE - WL::NC;
+    const int wl = i / WL::NA;
+    i -= wl * WL::NA;
+    const int mt = i / G::EB, kb = i - (i / G::EB) * G::EB;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) v[s] = w_lo<T>(a.W[(size_t)(wl * G::FW + 16 * mt + c) * G::D + 32 * kb + kp(g, s)]);
+  } else if (w >= 4) {
     i = f - 4 * WL::PER_WAVE;
     const int kb = i / G::ET, et = i - (i / G::ET) * G::ET;
 #pragma unroll

@@ -107,6 +107,7 @@ struct KsumArgs {
   const void* K;
   const void* V;
   const float* W;
+  const void* Wfrag;   // fragment-ordered W (WFragLayout)
   const float* shift;  // kSumStates, FAVOR+: [B,H] key shift of the sums
   float* out;          // kSumStates: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
   int B, H, L, C, P2;

@@ -18,6 +18,8 @@
 // KS_MAX mode computes only the logits and returns, per part, the maximum of
 // w_m.k - |k|^2/2 over its rows and all features: the maximum over a head's
 // parts is the key shift of that head.
+#include <type_traits>
+
 #include "slim_common.hpp"
 #include "slim_kernels.hpp"
 
@@ -47,18 +49,30 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   const T* Kh = (const T*)a.K + head * (size_t)a.L * D;
   const T* Vh = (const T*)a.V + head * (size_t)a.L * D;
 
-  // W fragments of this wave's features: slot s = W[w FW + 16 mt + c][32 kb + kp(g, s)]
-  F Wf[MT][EB];
-  {
+  // W fragments of this wave's features: slot s = W[w FW + 16 mt + c][32 kb + kp(g, s)],
+  // with the low parts of a bf16 split (see w_lo).  With 64 features per
+  // wave and sums (where registers are short) both parts come from the
+  // fragment table a.Wfrag at every chunk, half of the feature tiles at a
+  // time; otherwise they are held in registers.
+  constexpr bool LO_TABLE = kSplitW<T> && MT == 4 && SUMS;
+  constexpr int MR = LO_TABLE ? 1 : MT;
+  F Wf[MR][EB], Wl[MR][EB];
+  if constexpr (!LO_TABLE) {
     const Lane L = this_lane();
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int kb = 0; kb < EB; ++kb)
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-          Wf[mt][kb][s] = cvt<T>(a.W[(size_t)(w * FW + 16 * mt + L.c) * D + 32 * kb + kp(L.g, s)]);
+        for (int s = 0; s < 8; ++s) {
+          const float x = a.W[(size_t)(w * FW + 16 * mt + L.c) * D + 32 * kb + kp(L.g, s)];
+          Wf[mt][kb][s] = cvt<T>(x);
+          Wl[mt][kb][s] = w_lo<T>(x);
+        }
   }
+  typedef WFragLayout<G> WL;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.Wfrag), (short)0, LO_TABLE ? (int)(WL::TOTAL * 64 * sizeof(F)) : 0, 0x00020000);
 
   // rows of this part
   const TileMap tm(a.L, a.C, 32);
@@ -139,16 +153,86 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
 
+    // features of the feature tiles [m0, m1) (rows past the chunk: zero),
+    // then [S | z] += K~^T [V | 1] over the chunk's rows, 32 rows per product
+    auto feat_update = [&](f32x4 (&Lk)[CT][MT], auto m0c, auto m1c) {
+      constexpr int m0 = decltype(m0c)::value, m1 = decltype(m1c)::value;
+#pragma unroll
+      for (int st = 0; st < CT; ++st) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = 16 * st + 4 * L.g + r < cnt;
+          const float kc = ok ? koff + 0.5f * kLog2e * knv[st][r] : INFINITY;
+#pragma unroll
+          for (int mt = m0; mt < m1; ++mt) {
+            float x = Lk[st][mt][r];
+            if (G::KIND == kFavor) x = fast_exp2(x * kLog2e - kc);
+            else x = ok ? fmaxf(x, 0.f) + a.relu_eps : 0.f;
+            Lk[st][mt][r] = x;
+          }
+        }
+      }
+#pragma unroll
+      for (int rb = 0; rb < CT / 2; ++rb) {
+        F ones;
+        const int rem = cnt - 32 * rb - 4 * L.g;  // rows 32 rb + kp(g, s) < cnt
+#pragma unroll
+        for (int s = 0; s < 8; ++s) ones[s] = cvt<T>((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
+#pragma unroll
+        for (int mt = m0; mt < m1; ++mt) {
+          const F kt = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
+#pragma unroll
+          for (int et = 0; et < ET; ++et) S[mt][et] = mma(S[mt][et], kt, vf[rb][et]);
+          Sz[mt] = mma(Sz[mt], kt, ones);
+        }
+      }
+    };
+
     // logits: Lk[st][mt] rows s = 16 st + 4 g + r, columns m = w FW + 16 mt + c
     f32x4 Lk[CT][MT];
+    if constexpr (LO_TABLE) {
+      typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+      const int wlane = (fresh_tid() & 63) * (int)sizeof(F);
 #pragma unroll
-    for (int st = 0; st < CT; ++st) {
+      for (int m2 = 0; m2 < MT; m2 += 2) {
+        F Wh[2][EB], Wt[2][EB];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 acc = zero4();
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wf[mt][kb]);
-        Lk[st][mt] = acc;
+          for (int kb = 0; kb < EB; ++kb) {
+            Wh[i][kb] = __builtin_bit_cast(
+                F, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, WL::a(w, m2 + i, kb) * 64 * (int)sizeof(F), 0));
+            Wt[i][kb] = __builtin_bit_cast(
+                F, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, WL::alo(w, m2 + i, kb) * 64 * (int)sizeof(F), 0));
+          }
+#pragma unroll
+        for (int st = 0; st < CT; ++st)
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            f32x4 acc = zero4();
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wh[i][kb]);
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wt[i][kb]);
+            Lk[st][m2 + i] = acc;
+          }
+        if (m2 == 0) feat_update(Lk, std::integral_constant<int, 0>(), std::integral_constant<int, 2>());
+        else feat_update(Lk, std::integral_constant<int, 2>(), std::integral_constant<int, 4>());
+      }
+    } else {
+#pragma unroll
+      for (int st = 0; st < CT; ++st) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wf[mt][kb]);
+          if constexpr (kSplitW<T>) {
+#pragma unroll
+            for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wl[mt][kb]);
+          }
+          Lk[st][mt] = acc;
+        }
       }
     }
 
@@ -164,38 +248,8 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
           vmax = fmaxf(vmax, 16 * st + 4 * L.g + r < cnt ? v - 0.5f * knv[st][r] : -INFINITY);
         }
       }
-    } else {
-      // features (rows past the chunk: zero)
-#pragma unroll
-      for (int st = 0; st < CT; ++st) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const bool ok = 16 * st + 4 * L.g + r < cnt;
-          const float kc = ok ? koff + 0.5f * kLog2e * knv[st][r] : INFINITY;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            float x = Lk[st][mt][r];
-            if (G::KIND == kFavor) x = fast_exp2(x * kLog2e - kc);
-            else x = ok ? fmaxf(x, 0.f) + a.relu_eps : 0.f;
-            Lk[st][mt][r] = x;
-          }
-        }
-      }
-      // [S | z] += K~^T [V | 1] over the chunk's rows, 32 rows per product
-#pragma unroll
-      for (int rb = 0; rb < CT / 2; ++rb) {
-        F ones;
-        const int rem = cnt - 32 * rb - 4 * L.g;  // rows 32 rb + kp(g, s) < cnt
-#pragma unroll
-        for (int s = 0; s < 8; ++s) ones[s] = cvt<T>((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const F kt = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
-#pragma unroll
-          for (int et = 0; et < ET; ++et) S[mt][et] = mma(S[mt][et], kt, vf[rb][et]);
-          Sz[mt] = mma(Sz[mt], kt, ones);
-        }
-      }
+    } else if constexpr (!LO_TABLE) {
+      feat_update(Lk, std::integral_constant<int, 0>(), std::integral_constant<int, MT>());
     }
     __syncthreads();
   }

@@ -165,12 +165,18 @@ def time_walk(phase: int, before: "torch.cuda.Event", after: "torch.cuda.Event")
     _check(LIB.slim_time_walk(int(phase), ctypes.c_void_p(before.cuda_event), ctypes.c_void_p(after.cuda_event)))
 
 
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
 def _workspace(p: Problem, phase: int, device, ws: Optional[torch.Tensor]):
     n = workspace_bytes(p, phase)
     if ws is None:
         ws = torch.empty(max(n, 1), dtype=torch.uint8, device=device)
-    elif ws.numel() * ws.element_size() < n:
-        raise ValueError(f"workspace needs {n} bytes")
+    else:
+        _need(ws, "ws", ws.dtype)
+        if _nbytes(ws) < n:
+            raise ValueError(f"workspace needs {n} bytes, got {_nbytes(ws)}")
     return ws
 
 
@@ -211,13 +217,17 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
         _need(kshift_in, "kshift_in", torch.float32, (p.B, p.H))
     dev = Q.device
     Y = torch.empty_like(Q) if Y is None else Y
+    _need(Y, "Y", Q.dtype, shp)
     state_out = torch.empty(sshape, dtype=torch.float32, device=dev) if state_out is None else state_out
+    _need(state_out, "state_out", torch.float32, sshape)
     if p.kind == FAVOR_PLUS and kshift_out is None:
         kshift_out = torch.empty((p.B, p.H), dtype=torch.float32, device=dev)
+    if kshift_out is not None:
+        _need(kshift_out, "kshift_out", torch.float32, (p.B, p.H))
     _need_ctx(p, ctx)
     ws = _workspace(p, PHASE_FWD, dev, ws)
     _check(LIB.slim_fwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
-                        _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _ptr(ws), ws.numel(), _stream()))
+                        _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
     return Y, state_out, kshift_out
 
 
@@ -245,10 +255,14 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
     dK = torch.empty_like(K) if dK is None else dK
     dV = torch.empty_like(V) if dV is None else dV
     dW = torch.empty((p.M, p.d), dtype=torch.float32, device=dev) if dW is None else dW
+    for n, t in (("dQ", dQ), ("dK", dK), ("dV", dV)):
+        _need(t, n, Q.dtype, shp)
+    _need(dW, "dW", torch.float32, (p.M, p.d))
     dstate_in = torch.empty(sshape, dtype=torch.float32, device=dev) if want_dstate_in else None
     _need_ctx(p, ctx)
     ws = _workspace(p, PHASE_BWD, dev, ws)
     _check(LIB.slim_bwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
                         _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
-                        _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), ws.numel(), _stream()))
+                        _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
     return dQ, dK, dV, dW, dstate_in
+

@@ -13,10 +13,11 @@ on its own):
   ceil(M/d) independent blocks; each block is the orthogonal factor of a
   d x d Gaussian matrix (sign-fixed by diag(R)) whose rows are rescaled to
   the norms of independent N(0, I_d) draws; blocks are stacked and cut to M
-  rows, then stored as float32.  For bf16 workloads W is rounded to bf16
-  (RNE) like every other input, so the oracle and the kernels see the same
-  features; the kernels consume W at bf16 precision in bf16 mode.  W is an
-  input of the method, so the results do not depend on this choice.
+  rows, then stored as float32 and handed to the library as such (the
+  library's interface takes W in float32).  `round_w=True` rounds it to
+  bf16 (RNE) first, so that W is also bf16-representable; the oracle
+  always consumes exactly the W the library gets.  W is an input of the
+  method, so the results do not depend on how it was drawn.
 
 The paper benchmarks random byte strings pushed through a randomly
 initialised model (Sec. 4.1); the per-head Q, K, V of such a model are close
@@ -125,12 +126,14 @@ def make_inputs(
     seed: int = SEED,
     tensors=("Q", "K", "V", "dY", "W"),
     scale_qk: Optional[float] = None,
+    round_w: bool = False,
 ):
     """Seeded inputs of one attention op of a workload.
 
     Returns a dict of torch CPU tensors: Q, K, V, dY in the workload dtype
     with shape [B, H, L, d]; W float32 [M, d].  `scale_qk` multiplies Q and K
-    on top of the d**(-1/4) pre-scale (used by stress tests).
+    on top of the d**(-1/4) pre-scale (used by stress tests); `round_w`
+    makes W bf16-representable.
     """
     shp = (wl.B, wl.H, wl.L, wl.d)
     s = wl.d ** -0.25
@@ -141,7 +144,7 @@ def make_inputs(
 
             W = orthogonal_gaussian_features(wl.M, wl.d, _stream(wl.wid, layer, "W", seed))
             Wt = torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32))
-            if wl.dtype == "bf16":
+            if round_w:
                 Wt = Wt.to(torch.bfloat16).to(torch.float32)
             out["W"] = Wt
             continue

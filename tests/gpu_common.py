@@ -40,3 +40,17 @@ def report(name, x, ref, tol):
     assert np.all(np.isfinite(np.asarray(x))), f"{name} has non-finite values"
     assert e <= tol, f"{name}: max_rel {e:.3e} > {tol:g}"
     return e
+
+
+def mask_w(x):
+    """The W the oracle takes the ReLU derivative's 0/1 decisions with, for
+    the inputs x: the library forms the logits w_m . x of bf16 problems from
+    the bf16 split hi + lo of the float32 W (hi = RNE(w), lo = RNE(w - hi)),
+    so for those the decision is taken with hi + lo (the same precision on
+    both sides); fp32 problems use W itself (None)."""
+    if x["Q"].dtype != torch.bfloat16:
+        return None
+    W = x["W"].float()
+    hi = W.to(torch.bfloat16).float()
+    lo = (W - hi).to(torch.bfloat16).float()
+    return hi.double().numpy() + lo.double().numpy()

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle as O
-from tests.gpu_common import TOL, dev, host64, need_gpu, report
+from tests.gpu_common import TOL, dev, host64, mask_w, need_gpu, report
 from tests.test_gpu_forward import CASES, _inputs
 
 pytestmark = pytest.mark.gpu
@@ -34,7 +34,7 @@ def test_backward_matches_definition(i):
     print(f"[backward] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind}", flush=True)
     x = _inputs(i, B, H, L, d, M, C, dtype, kind)
     _, _, _, (dQ, dK, dV, dW, _) = _run(x, C, kind)
-    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     tol = TOL[dtype]
     for n, a, r in zip(("dQ", "dK", "dV", "dW"), (dQ, dK, dV, dW), ref):
         report(n, host64(a), r, tol)
@@ -62,7 +62,7 @@ def test_state_cotangent_and_chaining(i):
     g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, ks1, kind,
                   dstate_out=g2[4])
     torch.cuda.synchronize()
-    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     report("dQ (chained)", np.concatenate([host64(g1[0]), host64(g2[0])], axis=2), ref[0], tol)
     report("dK (chained)", np.concatenate([host64(g1[1]), host64(g2[1])], axis=2), ref[1], tol)
     report("dV (chained)", np.concatenate([host64(g1[2]), host64(g2[2])], axis=2), ref[2], tol)
@@ -71,7 +71,7 @@ def test_state_cotangent_and_chaining(i):
     Yo, sto = O.slim_forward(x["Q"][:, :, :cut], x["K"][:, :, :cut], x["V"][:, :, :cut], x["W"], C, kind)
     st_full = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind)[1]
     go = O.slim_backward(x["Q"][:, :, cut:], x["K"][:, :, cut:], x["V"][:, :, cut:], x["W"], x["dY"][:, :, cut:], C,
-                         kind, st_full)[4]
+                         kind, st_full, mask_W=mask_w(x))[4]
     g0 = host64(g2[4])
     if kind == "favor+":
         # dL/d(stored state_in) = dL/d(true state) * exp(kshift_in)
@@ -98,6 +98,70 @@ def test_backward_four_wave_form(i):
             os.environ.pop("SLIM_BWD_WAVES", None)
         else:
             os.environ["SLIM_BWD_WAVES"] = old
-    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     for n, a, r in zip(("dQ", "dK", "dV", "dW"), (dQ, dK, dV, dW), ref):
         report(n, host64(a), r, TOL[dtype])
+
+
+@pytest.mark.parametrize("i", [4, 5, 7, 8])
+def test_backward_rounded_w(i):
+    """The same problems with a bf16-representable W: then the kernels'
+    rounding of W is exact and the error is the rest of the path's."""
+    need_gpu()
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[backward rounded W] case={name}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind, round_w=True)
+    Y, _, _, (dQ, dK, dV, dW, _) = _run(x, C, kind)
+    report("Y", host64(Y), O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind), TOL[dtype])
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), (dQ, dK, dV, dW), ref):
+        report(n, host64(a), r, TOL[dtype])
+
+
+@pytest.mark.parametrize("L, late, scale, segments",
+                         [(160, False, 3.0, None), (4096, False, 2.0, None), (4096, False, 2.5, 128),
+                          (4096, True, 2.0, 128)])
+def test_backward_stress_large_logits(L, late, scale, segments):
+    """Q, K scaled by 2 to 3 (exponents of size ~50), through the whole
+    backward.  (At 3 the chain rule of the key features, a difference of two
+    large sums over features of bf16 operands, reaches ~2e-2 of dK.)
+    `late`: one key near the end is set to the feature direction w_m of
+    largest norm, so that its exponent |w_m|^2 / 2 ~ 50 sets the head's key
+    shift far above every earlier key (with Q, K scaled by 2 the best feature
+    of an earlier key then lies up to ~60 below the shift: e^-60, inside the
+    fp32 range of ~e^-87 that the single key shift relies on).
+
+    Downdating (eq. 17) subtracts a tile's contribution from a float32 sum:
+    the result is exact only to ~2^-24 of the largest feature in the sum, so
+    inputs whose key features span e^20 and more inside one part of the walk
+    are beyond it.  The walk resets to the exact boundary state at the start
+    of every part; the cases with `segments` = 128 force one 32-row tile per
+    part at L = 4096, where the walk never downdates; L = 160 runs as one
+    part of five tiles, and the default plan at L = 4096 downdates over four
+    tiles per part.  Rounded W (see test_forward_stress_large_logits)."""
+    need_gpu()
+    import os
+    import torch as _t
+
+    B, H, d, M, C = 1, 2, 64, 256, 64
+    print(f"[backward stress] L={L} late={late} scale={scale} segments={segments}", flush=True)
+    x = _inputs(51 + L, B, H, L, d, M, C, "bf16", "favor+", scale_qk=scale, round_w=True)
+    if late:
+        m = int(_t.argmax((x["W"] ** 2).sum(1)))
+        K = x["K"].clone()
+        K[:, :, L - 7] = x["W"][m].to(K.dtype)
+        x["K"] = K
+    old = os.environ.get("SLIM_SEGMENTS")
+    if segments is not None:
+        os.environ["SLIM_SEGMENTS"] = str(segments)
+    try:
+        Y, _, ks, (dQ, dK, dV, dW, _) = _run(x, C, "favor+")
+    finally:
+        if old is None:
+            os.environ.pop("SLIM_SEGMENTS", None)
+        else:
+            os.environ["SLIM_SEGMENTS"] = old
+    report("Y", host64(Y), O.attention_forward(x["Q"], x["K"], x["V"], x["W"], "favor+"), TOL["bf16"])
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], "favor+")
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), (dQ, dK, dV, dW), ref):
+        report(n, host64(a), r, TOL["bf16"])

@@ -13,7 +13,7 @@ import torch
 
 import oracle as O
 from synth import Workload, make_inputs
-from tests.gpu_common import TOL, dev, host64, need_gpu, report
+from tests.gpu_common import TOL, dev, host64, mask_w, need_gpu, report
 
 pytestmark = pytest.mark.gpu
 
@@ -67,7 +67,7 @@ def test_context_changes_nothing(i):
 
     if i == 0:
         Yr = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
-        gr = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+        gr = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
         tol = TOL["bf16"]
         report("Y", host64(Y1), Yr, tol)
         for n, a, r in zip(("dQ", "dK", "dV", "dW"), g1[:4], gr):

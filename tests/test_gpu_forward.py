@@ -2,6 +2,9 @@
 
 Inputs come from the seeded generators in synth/; the oracle consumes the
 same rounded values (bf16 inputs upcast), so the error measures the kernels.
+W is the float32 block-orthogonal matrix the library takes at its
+interface (not rounded to bf16 first), so the error includes the kernels'
+own rounding of W; tests marked "rounded W" pass a bf16-representable W.
 Bars: max-relative error (max|x - ref| / max|ref| per tensor) <= 1e-5 for fp32
 problems and <= 2e-2 for bf16 problems.
 """
@@ -33,9 +36,9 @@ CASES = [
 ]
 
 
-def _inputs(i, B, H, L, d, M, C, dtype, kind, scale_qk=None):
+def _inputs(i, B, H, L, d, M, C, dtype, kind, scale_qk=None, round_w=False):
     wl = Workload(f"case{i}", 100 + i, B, H, L, d, M, (C,), dtype, kind)
-    return make_inputs(wl, scale_qk=scale_qk)
+    return make_inputs(wl, scale_qk=scale_qk, round_w=round_w)
 
 
 @pytest.mark.parametrize("i", range(len(CASES)))
@@ -84,12 +87,14 @@ def test_forward_two_calls_equal_one(i):
 
 
 def test_forward_stress_large_logits():
-    """Q, K scaled by 3: exponents of size ~50; the shifts keep fp32 in range."""
+    """Q, K scaled by 3: exponents of size ~50; the shifts keep fp32 in range.
+    Rounded W: at this scale the bf16 rounding of a general float32 W alone
+    moves the logits by up to 2^-9 sum_e |x_e w_e| ~ 0.1, about 2e-2 of Y."""
     need_gpu()
     from paper_2012_11346_amd import slim
 
     B, H, L, d, M, C = 1, 2, 160, 64, 256, 64
-    x = _inputs(50, B, H, L, d, M, C, "bf16", "favor+", scale_qk=3.0)
+    x = _inputs(50, B, H, L, d, M, C, "bf16", "favor+", scale_qk=3.0, round_w=True)
     Y, st, ks = slim.fwd(dev(x["Q"]), dev(x["K"]), dev(x["V"]), dev(x["W"]), C, "favor+")
     torch.cuda.synchronize()
     Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], "favor+")

@@ -16,7 +16,7 @@ import torch
 
 import oracle as O
 from synth import make_inputs, workload
-from tests.gpu_common import TOL, dev, host64, need_gpu, report
+from tests.gpu_common import TOL, dev, host64, mask_w, need_gpu, report
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,8 @@ def _oracle(x, heads, kind):
     Q, K, V, dY = (_sample(x[k], heads) for k in ("Q", "K", "V", "dY"))
     W = host64(x["W"])
     Y, st = O.slim_forward(Q, K, V, W, ORACLE_C, kind, within="quadratic")
-    dQ, dK, dV, dW, _ = O.slim_backward(Q, K, V, W, dY, ORACLE_C, kind, st, within="quadratic")
+    dQ, dK, dV, dW, _ = O.slim_backward(Q, K, V, W, dY, ORACLE_C, kind, st, within="quadratic",
+                                        mask_W=mask_w(x))
     return Y, dQ, dK, dV, dW
 
 
@@ -86,6 +87,18 @@ def test_slice_sweep_full_size():
     ref = _oracle(x, heads, wl.kind)
     for C in wl.C:
         _check(wl.name, x, heads, C, wl.kind, ref)
+
+
+def test_slice_sweep_full_size_rounded_w():
+    """The headline problem at C=64 with a bf16-representable W (the other
+    tests pass the unrounded float32 W the interface takes)."""
+    need_gpu()
+    wl = workload("sweep_32k")
+    heads = [(1, 2)]
+    x = make_inputs(wl, round_w=True)
+    print("[full size] oracle on the sampled head (rounded W)", flush=True)
+    ref = _oracle(x, heads, wl.kind)
+    _check(wl.name + " rounded W", x, heads, 64, wl.kind, ref)
 
 
 def test_long_context_full_size():

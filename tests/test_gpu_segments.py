@@ -14,7 +14,7 @@ import torch
 
 import oracle as O
 from synth import Workload, make_inputs
-from tests.gpu_common import TOL, dev, host64, need_gpu, report
+from tests.gpu_common import TOL, dev, host64, mask_w, need_gpu, report
 
 pytestmark = pytest.mark.gpu
 
@@ -58,7 +58,7 @@ def test_results_do_not_depend_on_segments(i, split):
     name, B, H, L, d, M, C, dtype, kind, segs = SEG_CASES[i]
     x = make_inputs(Workload(name, 300 + i, B, H, L, d, M, (C,), dtype, kind))
     Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
-    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     _, stref = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind, within="quadratic")
     tol = TOL[dtype]
     for P in segs:
@@ -91,7 +91,7 @@ def test_carry_runs_cross_segments_and_heads(i, wgs):
     need_gpu()
     name, B, H, L, d, M, C, kind, P = CARRY_CASES[i]
     x = make_inputs(Workload(name, 340 + i, B, H, L, d, M, (C,), "bf16", kind))
-    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     print(f"[carry runs] case={name} P={P} workgroups={wgs}", flush=True)
     _, _, _, g = _fwd_bwd(x, C, kind, P, carry_wgs=wgs)
     for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], gref):
@@ -105,7 +105,7 @@ def test_long_sequence_against_definition(kind):
     M = 256 if kind == "favor+" else 128
     x = make_inputs(Workload("long", 320, 1, 2, 4096, 64, M, (64,), "bf16", kind))
     Yref = O.attention_forward(x["Q"], x["K"], x["V"], x["W"], kind)
-    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    gref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     for P in (None, 1):
         print(f"[long] kind={kind} P={P}", flush=True)
         Y, st, ks, g = _fwd_bwd(x, 64, kind, P)
@@ -145,7 +145,7 @@ def test_cotangent_chaining_with_segments(kind):
             os.environ.pop("SLIM_SEGMENTS", None)
         else:
             os.environ["SLIM_SEGMENTS"] = old
-    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind)
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     tol = TOL["bf16"]
     report("dQ (chained)", np.concatenate([host64(g1[0]), host64(g2[0])], axis=2), ref[0], tol)
     report("dK (chained)", np.concatenate([host64(g1[1]), host64(g2[1])], axis=2), ref[1], tol)

@@ -66,7 +66,7 @@ def _bwd_transposed_dA(Qf, Kf, V, dY):
     return dA.T @ Kf, dA @ Qf, A.T @ dN
 
 
-def _vjp_no_norm_term(X, W, Phi, dPhi, kind):
+def _vjp_no_norm_term(X, W, Phi, dPhi, kind, mask_W=None):
     X, W = S._f64(X), S._f64(W)
     Gm = dPhi * Phi if kind == S.FAVOR_PLUS else dPhi * ((X @ W.T) > 0.0)
     return Gm @ W, Gm.T @ X
@@ -90,13 +90,14 @@ def _iter_bwd_printed(Qf, Kf, V, dN, dD, curR, curS):
     return dQf, dKf, dVv
 
 
-def _slim_bwd_no_downdate(Q, K, V, W, dY, C, kind, R_N, S_N, gR=None, gS=None, within="ps", relu_eps=S.RELU_EPS):
+def _slim_bwd_no_downdate(Q, K, V, W, dY, C, kind, R_N, S_N, gR=None, gS=None, within="ps", relu_eps=S.RELU_EPS,
+                          mask_W=None):
     # skip eq. 17 by adding back what the real routine subtracts
     Wf = S._f64(W)
     Kf_all = S.feature_map(S._f64(K), Wf, kind, relu_eps)
     V_ = S._f64(V)
     out = list(_REAL_BWD(Q, K, V, W, dY, C, kind, S._f64(R_N) + V_.T @ Kf_all, S._f64(S_N) + Kf_all.sum(0),
-                         gR, gS, within, relu_eps))
+                         gR, gS, within, relu_eps, mask_W))
     return tuple(out)
 
 

@@ -363,3 +363,21 @@ def test_feature_logits_written_out_by_loops():
     assert O.feature_logits(np.array([[1.0, 2.0]]), np.array([[3.0, -1.0]]))[0, 0] == 1.0
     assert abs(O.feature_map(np.array([[1.0, 2.0]]), np.array([[3.0, -1.0]]), O.FAVOR_PLUS)[0, 0]
                - math.exp(-1.5)) < 1e-15
+
+
+def test_relu_decision_matrix_only_moves_the_mask():
+    """mask_W changes only the 0/1 decisions of the ReLU derivative: the same
+    signs give the same gradients, and the opposite matrix gives the
+    complementary mask, so the two gradients add up to the all-ones mask's
+    (dPhi W, dPhi^T X)."""
+    rng = np.random.default_rng(23)
+    X = rng.standard_normal((7, 4))
+    W = rng.standard_normal((5, 4))
+    Phi = O.feature_map(X, W, O.RELU)
+    dPhi = rng.standard_normal((7, 5))
+    dX, dW = O.feature_map_vjp(X, W, Phi, dPhi, O.RELU)
+    dX1, dW1 = O.feature_map_vjp(X, W, Phi, dPhi, O.RELU, mask_W=W * (1 + 1e-9))
+    assert np.array_equal(dX, dX1) and np.array_equal(dW, dW1)
+    dXn, dWn = O.feature_map_vjp(X, W, Phi, dPhi, O.RELU, mask_W=-W)
+    assert _rel(dX + dXn, dPhi @ W) < 1e-14
+    assert _rel(dW + dWn, dPhi.T @ X) < 1e-14
