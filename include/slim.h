@@ -132,6 +132,30 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
              const float* state_in, const float* kshift_in, void* Y, float* state_out,
              float* kshift_out, float* ctx, void* ws, size_t ws_bytes, void* stream);
 
+/* Bytes of the static device scratch slim_fwd_noalloc uses (a compile-time
+ * constant, SLIM_NOALLOC_SCRATCH_BYTES). */
+#define SLIM_NOALLOC_SCRATCH_BYTES ((size_t)72 << 20)
+size_t slim_noalloc_scratch_bytes(void);
+
+/* slim_fwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, results and errors as slim_fwd, except
+ * that the scratch space is a static device array of
+ * SLIM_NOALLOC_SCRATCH_BYTES inside the library: each device the library
+ * runs on holds one copy, from the first call on that device until the
+ * process ends.  The call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine); the caller still passes every input and
+ * output.  Problems whose forward needs more scratch than that
+ * (slim_workspace_bytes(p, SLIM_PHASE_FWD) > SLIM_NOALLOC_SCRATCH_BYTES) are
+ * rejected with SLIM_EUNSUPPORTED before anything is launched.  The scratch
+ * of the current device (hipGetDevice) is used, so `stream` must belong to
+ * it.  All calls on one device share its scratch: calls that may overlap on
+ * one device (other host threads, or streams not ordered with each other)
+ * race and must be serialised by the caller. */
+int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+                     const float* state_in, const float* kshift_in, void* Y, float* state_out,
+                     float* kshift_out, float* ctx, void* stream);
+
 /* Backward sweep of Algorithm 1 (one layer) for the loss
  * sum(dY * Y) + <dstate_out, state_out>.
  *   Q, K, V, W, state_in, kshift_in  as given to slim_fwd

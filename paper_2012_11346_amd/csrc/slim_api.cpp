@@ -10,6 +10,7 @@
 #include <cstring>
 #include <algorithm>
 #include <cstdlib>
+#include <mutex>
 #include <string>
 
 #include "../../include/slim.h"
@@ -558,6 +559,35 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
   return ok();
 }
 
+// Static device scratch of slim_fwd_noalloc: one copy per device, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// the device array: its device address comes from hipGetSymbolAddress (per
+// device, kept in g_scratch), and only that address is passed to kernels.
+constexpr size_t kNoallocScratchBytes = SLIM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// device address of the current device's scratch, looked up once per device
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(SLIM_EUNSUPPORTED, "device index %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (ptr == nullptr) return fail(SLIM_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return SLIM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -566,6 +596,25 @@ int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V,
              const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, float* ctx,
              void* ws, size_t ws_bytes, void* stream) {
   return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ctx, ws, ws_bytes, stream);
+}
+
+size_t slim_noalloc_scratch_bytes(void) { return kNoallocScratchBytes; }
+
+int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+                     const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out,
+                     float* ctx, void* stream) {
+  int st = check_problem(p);
+  if (st != SLIM_OK) return st;
+  const size_t need = fwd_ws_bytes(p);
+  if (need > kNoallocScratchBytes)
+    return fail(SLIM_EUNSUPPORTED, "slim_fwd_noalloc: the forward needs %zu bytes of scratch, the static scratch holds %zu",
+                need, kNoallocScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    st = scratch_address(&ws);
+    if (st != SLIM_OK) return st;
+  }
+  return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ctx, ws, kNoallocScratchBytes, stream);
 }
 
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,

@@ -73,6 +73,10 @@ def _load() -> ctypes.CDLL:
     lib.slim_last_error.restype = ctypes.c_char_p
     lib.slim_time_walk.argtypes = [i32, vp, vp]
     lib.slim_time_walk.restype = i32
+    lib.slim_noalloc_scratch_bytes.argtypes = []
+    lib.slim_noalloc_scratch_bytes.restype = sz
+    lib.slim_fwd_noalloc.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, vp]
+    lib.slim_fwd_noalloc.restype = i32
     return lib
 
 
@@ -88,6 +92,8 @@ EXPORTED = (
     "slim_last_error",
     "slim_num_segments",
     "slim_time_walk",
+    "slim_noalloc_scratch_bytes",
+    "slim_fwd_noalloc",
 )
 
 
@@ -266,3 +272,32 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
                         _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
     return dQ, dK, dV, dW, dstate_in
 
+
+def fwd_noalloc(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3,
+                Y=None, state_out=None, kshift_out=None, ctx=None):
+    """fwd through slim_fwd_noalloc: the library's static device scratch
+    replaces the workspace (outputs not passed in are allocated here, by
+    torch, before the call; the call itself allocates nothing)."""
+    p = _problem_of(Q, W, C, kind, relu_eps)
+    shp = (p.B, p.H, p.L, p.d)
+    for n, t in (("Q", Q), ("K", K), ("V", V)):
+        _need(t, n, Q.dtype, shp)
+    _need(W, "W", torch.float32, (p.M, p.d))
+    sshape = (p.B, p.H, p.M, p.d + 1)
+    if state_in is not None:
+        _need(state_in, "state_in", torch.float32, sshape)
+    if kshift_in is not None:
+        _need(kshift_in, "kshift_in", torch.float32, (p.B, p.H))
+    dev = Q.device
+    Y = torch.empty_like(Q) if Y is None else Y
+    _need(Y, "Y", Q.dtype, shp)
+    state_out = torch.empty(sshape, dtype=torch.float32, device=dev) if state_out is None else state_out
+    _need(state_out, "state_out", torch.float32, sshape)
+    if p.kind == FAVOR_PLUS and kshift_out is None:
+        kshift_out = torch.empty((p.B, p.H), dtype=torch.float32, device=dev)
+    if kshift_out is not None:
+        _need(kshift_out, "kshift_out", torch.float32, (p.B, p.H))
+    _need_ctx(p, ctx)
+    _check(LIB.slim_fwd_noalloc(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in),
+                                _ptr(kshift_in), _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _stream()))
+    return Y, state_out, kshift_out
