@@ -9,6 +9,7 @@ from .slim_oracle import (  # noqa: F401
     FAVOR_PLUS,
     RELU,
     RELU_EPS,
+    SQUARE,
     attention_backward,
     attention_forward,
     feature_logits,

@@ -23,7 +23,10 @@ B (eq. 17), recomputing each slice, and carrying the state cotangent G
 Feature maps.  The paper only cites the randomized map (Sec. 2.1, after eq. 2);
 the FAVOR+ map implemented here is phi(x)_m = exp(w_m . x - |x|^2 / 2) / sqrt(M)
 with W in R^{M x d}, and the ReLU map is phi(x)_m = max(w_m . x, 0) + eps.
-Both are unstabilised: fp64 has the range for the inputs used here.
+Both are unstabilised: fp64 has the range for the inputs used here.  The
+map of the paper's experiments (Sec. 4, setup) is the element-wise square
+g(x) = (x_i^2)_i with M = d; "square" here is phi(x)_m = (w_m . x)^2, which
+is that map for W = I_d.
 
 Arrays are float64 numpy.  Per-head functions take [L, d] arrays; the
 batched wrappers take [B, H, L, d] and loop over (b, h) one head at a time.
@@ -38,6 +41,7 @@ import numpy as np
 
 FAVOR_PLUS = "favor+"
 RELU = "relu"
+SQUARE = "square"
 RELU_EPS = 1e-3
 
 
@@ -58,7 +62,8 @@ def feature_logits(X, W) -> np.ndarray:
 
 
 def feature_map(X, W, kind: str, relu_eps: float = RELU_EPS) -> np.ndarray:
-    """g(X) row by row.  FAVOR+: exp(Wx - |x|^2/2)/sqrt(M); ReLU: max(Wx,0)+eps."""
+    """g(X) row by row.  FAVOR+: exp(Wx - |x|^2/2)/sqrt(M); ReLU: max(Wx,0)+eps;
+    square: (Wx)^2 (the paper's x^2 map when W = I)."""
     X = _f64(X)
     W = _f64(W)
     z = X @ W.T
@@ -66,6 +71,8 @@ def feature_map(X, W, kind: str, relu_eps: float = RELU_EPS) -> np.ndarray:
         return np.exp(z - 0.5 * np.sum(X * X, axis=-1, keepdims=True)) / math.sqrt(W.shape[0])
     if kind == RELU:
         return np.maximum(z, 0.0) + relu_eps
+    if kind == SQUARE:
+        return z * z
     raise ValueError(kind)
 
 
@@ -75,6 +82,7 @@ def feature_map_vjp(X, W, Phi, dPhi, kind: str, mask_W=None) -> Tuple[np.ndarray
     FAVOR+: d phi_m / dx = phi_m (w_m - x), d phi_m / dw_m = phi_m x.
     ReLU:   d phi_m / dx = [w_m . x > 0] w_m, d phi_m / dw_m = [w_m . x > 0] x
             (derivative 0 taken at w_m . x = 0).
+    square: d phi_m / dx = 2 (w_m . x) w_m, d phi_m / dw_m = 2 (w_m . x) x.
 
     The ReLU derivative is a 0/1 decision on the sign of w_m . x.  `mask_W`
     (default W) is the matrix that decision is taken with: a caller
@@ -90,6 +98,9 @@ def feature_map_vjp(X, W, Phi, dPhi, kind: str, mask_W=None) -> Tuple[np.ndarray
     elif kind == RELU:
         Wd = W if mask_W is None else _f64(mask_W)
         Gm = dPhi * ((X @ Wd.T) > 0.0)
+        dX = Gm @ W
+    elif kind == SQUARE:
+        Gm = dPhi * (2.0 * (X @ W.T))
         dX = Gm @ W
     else:
         raise ValueError(kind)

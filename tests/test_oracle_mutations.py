@@ -104,6 +104,18 @@ def _slim_bwd_no_downdate(Q, K, V, W, dY, C, kind, R_N, S_N, gR=None, gS=None, w
 _REAL_BWD = S.slim_backward_head
 
 
+def _vjp_square_no_two(X, W, Phi, dPhi, kind, mask_W=None):
+    # the square map's derivative without its factor 2
+    X, W = S._f64(X), S._f64(W)
+    if kind == S.SQUARE:
+        Gm = dPhi * (X @ W.T)
+        return Gm @ W, Gm.T @ X
+    return _REAL_VJP(X, W, Phi, dPhi, kind, mask_W)
+
+
+_REAL_VJP = S.feature_map_vjp
+
+
 def _pack_no_transpose(R, S_):
     # R [.., d, M] laid out without the swap (only shape-compatible when d = M)
     return np.concatenate([R, S_[..., None]], axis=-1)
@@ -130,6 +142,7 @@ MUTANTS = [
     ("iterative_backward_features", _iter_bwd_printed, lambda: P.test_token_recurrence_equals_definition()),
     ("slim_backward_head", _slim_bwd_no_downdate,
      lambda: P.test_slicewise_equals_definition_for_every_slice_length(S.FAVOR_PLUS, "quadratic", 3)),
+    ("feature_map_vjp", _vjp_square_no_two, lambda: P.test_gradients_match_finite_differences(S.SQUARE)),
     ("pack_state", _pack_no_transpose, lambda: P.test_state_layout_written_out_by_loops()),
     ("unpack_state", _unpack_ones_first, lambda: P.test_state_layout_written_out_by_loops()),
     ("feature_logits", _logits_transposed_w, lambda: P.test_feature_logits_written_out_by_loops()),

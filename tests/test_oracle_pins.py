@@ -70,7 +70,7 @@ def _rel(a, b):
 # ---------------------------------------------------------------- P1: finite differences
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 def test_gradients_match_finite_differences(kind):
     Q, K, V, W, dY = _problem(B=1, H=2, L=6, d=3, M=5, seed=1)
     dQ, dK, dV, dW = O.attention_backward(Q, K, V, W, dY, kind)
@@ -82,7 +82,7 @@ def test_gradients_match_finite_differences(kind):
 # ---------------------------------------------------------------- closed forms
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 def test_first_output_is_first_value(kind):
     """Only l' = 1 contributes to Y_1, whatever the features (eq. 2)."""
     Q, K, V, W, _ = _problem(L=8, seed=2)
@@ -90,7 +90,7 @@ def test_first_output_is_first_value(kind):
     assert np.max(np.abs(Y[:, :, 0] - V[:, :, 0])) < 1e-14
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 def test_constant_keys_give_running_mean(kind):
     """Equal keys make every weight in row l equal: Y_l is the mean of V_1..V_l,
     Y does not depend on Q, and dV_j = sum_{l >= j} dY_l / l."""
@@ -105,7 +105,7 @@ def test_constant_keys_give_running_mean(kind):
     assert np.max(np.abs(dV - ref_dV)) < 1e-13
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 def test_constant_values_give_constant_output(kind):
     Q, K, V, W, dY = _problem(L=9, seed=4)
     V[:] = V[:, :, :1]
@@ -116,7 +116,7 @@ def test_constant_values_give_constant_output(kind):
         assert np.max(np.abs(g)) < 1e-12
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 def test_value_gradient_sums_to_output_gradient(kind):
     """Rows of the attention matrix sum to one, so sum_j dV_j = sum_l dY_l."""
     Q, K, V, W, dY = _problem(L=11, seed=5)
@@ -198,7 +198,7 @@ def test_relu_map_gradient_mask():
 # ---------------------------------------------------------------- Algorithm 1: C-invariance
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 @pytest.mark.parametrize("within", ["ps", "quadratic"])
 @pytest.mark.parametrize("C", [1, 2, 3, 7, 20])
 def test_slicewise_equals_definition_for_every_slice_length(kind, within, C):
@@ -225,7 +225,7 @@ def test_slice_bounds_ragged_tail():
         O.slice_bounds(10, 0)
 
 
-@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU])
+@pytest.mark.parametrize("kind", [O.FAVOR_PLUS, O.RELU, O.SQUARE])
 def test_state_gradient_matches_finite_differences(kind):
     """G^(0) = dL/dB^(0), with L = sum dY.Y + <G^(N), B^(N)> (eqs. 17-18)."""
     Q, K, V, W, dY = _problem(B=1, H=1, L=7, d=3, M=4, seed=11)
@@ -381,3 +381,22 @@ def test_relu_decision_matrix_only_moves_the_mask():
     dXn, dWn = O.feature_map_vjp(X, W, Phi, dPhi, O.RELU, mask_W=-W)
     assert _rel(dX + dXn, dPhi @ W) < 1e-14
     assert _rel(dW + dWn, dPhi.T @ X) < 1e-14
+
+
+def test_square_map_is_the_papers_elementwise_square():
+    """With W = I_d (M = d) the square map is g(x) = (x_i^2)_i, the map of
+    the paper's experiments (Sec. 4, setup); its VJP is 2 x_i dPhi_i."""
+    rng = np.random.default_rng(24)
+    X = rng.standard_normal((6, 5))
+    I = np.eye(5)
+    assert np.array_equal(O.feature_map(X, I, O.SQUARE), X * X)
+    dPhi = rng.standard_normal((6, 5))
+    dX, dW = O.feature_map_vjp(X, I, X * X, dPhi, O.SQUARE)
+    assert _rel(dX, 2.0 * X * dPhi) < 1e-15
+    # dW[m, e] = sum_l 2 x_lm dPhi_lm x_le
+    ref = np.zeros((5, 5))
+    for l in range(6):
+        for m in range(5):
+            for e in range(5):
+                ref[m, e] += 2.0 * X[l, m] * dPhi[l, m] * X[l, e]
+    assert _rel(dW, ref) < 1e-14
