@@ -16,10 +16,12 @@
  * Feature maps (W in R^{M x d}, one row w_m per feature):
  *   SLIM_FAVOR_PLUS  g(x)_m = exp(w_m . x - |x|^2 / 2) / sqrt(M)
  *   SLIM_RELU        g(x)_m = max(w_m . x, 0) + relu_eps
+ *   SLIM_SQUARE      g(x)_m = (w_m . x)^2; with W = I (M = d) this is the
+ *                    element-wise square of the paper's experiments (Sec. 4)
  * The FAVOR+ map is evaluated with max-stabilisers that cancel exactly:
  * one shift per query row and one shift per (batch, head) shared by all keys;
  * the state is stored relative to the key shift (true state =
- * stored state * exp(kshift)).  The ReLU map uses no shifts.
+ * stored state * exp(kshift)).  The ReLU and square maps use no shifts.
  *
  * Conventions for every entry point:
  *   - Tensors are dense, contiguous, row-major, in device memory:
@@ -61,7 +63,7 @@ typedef enum {
   SLIM_EHIP = -4          /* a HIP runtime call or a kernel launch failed */
 } slim_status;
 
-typedef enum { SLIM_FAVOR_PLUS = 0, SLIM_RELU = 1 } slim_kind;
+typedef enum { SLIM_FAVOR_PLUS = 0, SLIM_RELU = 1, SLIM_SQUARE = 2 } slim_kind;
 typedef enum { SLIM_F32 = 0, SLIM_BF16 = 1 } slim_dtype;
 typedef enum { SLIM_QUERY = 0, SLIM_KEY = 1 } slim_role;
 typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
@@ -70,7 +72,7 @@ typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
  *   B, H, L  batch, heads, sequence length (each >= 1; B H <= 65535 and one
  *            head's rows, L d elements, within 1 GiB, else SLIM_EUNSUPPORTED)
  *   d        head dimension: 32 or 64
- *   M        number of features: 64, 128 or 256
+ *   M        number of features: 64, 128 or 256 (SLIM_SQUARE: 64)
  *   C        slice length (Sec. 3.2): >= 1; values above L act as L.  The
  *            sequence is cut into N = ceil(L / C) slices, the last one ragged.
  *   dtype    slim_dtype of Q, K, V, Y, dY, dQ, dK, dV.  With SLIM_BF16 every

@@ -66,7 +66,8 @@ int check_problem(const slim_problem* p) {
   if (p->B < 1 || p->H < 1 || p->L < 1) return fail(SLIM_EINVAL, "B, H, L must be >= 1");
   if (p->C < 1) return fail(SLIM_EINVAL, "slice length C must be >= 1 (got %d)", (int)p->C);
   if (p->dtype != SLIM_F32 && p->dtype != SLIM_BF16) return fail(SLIM_EINVAL, "unknown dtype %d", (int)p->dtype);
-  if (p->kind != SLIM_FAVOR_PLUS && p->kind != SLIM_RELU) return fail(SLIM_EINVAL, "unknown kind %d", (int)p->kind);
+  if (p->kind != SLIM_FAVOR_PLUS && p->kind != SLIM_RELU && p->kind != SLIM_SQUARE)
+    return fail(SLIM_EINVAL, "unknown kind %d", (int)p->kind);
   if (p->d != 32 && p->d != 64) return fail(SLIM_EUNSUPPORTED, "head dim d=%d not supported (32 or 64)", (int)p->d);
   if (p->M != 64 && p->M != 128 && p->M != 256)
     return fail(SLIM_EUNSUPPORTED, "feature count M=%d not supported (64, 128 or 256)", (int)p->M);
@@ -77,6 +78,8 @@ int check_problem(const slim_problem* p) {
   if (p->B * p->H > 65535) return fail(SLIM_EUNSUPPORTED, "B*H=%lld too large", (long long)(p->B * p->H));
   if (p->B > 65535 || p->H > 65535) return fail(SLIM_EUNSUPPORTED, "B or H above 65535");
   if (p->kind == SLIM_RELU && !(p->relu_eps > 0.f)) return fail(SLIM_EINVAL, "relu_eps must be > 0");
+  if (p->kind == SLIM_SQUARE && p->M != 64)
+    return fail(SLIM_EUNSUPPORTED, "the square map is built for M=64 (got M=%d)", (int)p->M);
   if (p->dtype == SLIM_F32 && (int64_t)p->d * p->M > 4096)
     return fail(SLIM_EUNSUPPORTED, "fp32 problems need d*M <= 4096 (got d=%d, M=%d)", (int)p->d, (int)p->M);
   return SLIM_OK;
@@ -322,8 +325,16 @@ Dispatch pick_f32(int d, int M) {
   return make_dispatch<float, 32, 16, KIND>();
 }
 
+// the square map (M = 64): the 4-wave kernels with 16 features per wave
+Dispatch pick_square(int dtype, int d) {
+  if (dtype == SLIM_BF16)
+    return d == 64 ? make_dispatch<slim::bf16, 64, 16, slim::kSquare>() : make_dispatch<slim::bf16, 32, 16, slim::kSquare>();
+  return d == 64 ? make_dispatch<float, 64, 16, slim::kSquare>() : make_dispatch<float, 32, 16, slim::kSquare>();
+}
+
 // callers have checked check_problem(p)
 Dispatch dispatch(const slim_problem* p) {
+  if (p->kind == SLIM_SQUARE) return pick_square(p->dtype, p->d);
   if (p->dtype == SLIM_BF16) return p->kind == SLIM_FAVOR_PLUS ? pick_bf16<slim::kFavor>(p->d, p->M)
                                                                : pick_bf16<slim::kRelu>(p->d, p->M);
   return p->kind == SLIM_FAVOR_PLUS ? pick_f32<slim::kFavor>(p->d, p->M) : pick_f32<slim::kRelu>(p->d, p->M);

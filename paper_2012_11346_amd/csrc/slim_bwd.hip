@@ -200,8 +200,10 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     __syncthreads();
 
     // ---- features: logits, shifts, exponentials; Q~ -> Zq[t][m], K~ -> Zk[m][s]
+    // (the logits stay live for the square map's chain rule; for the other
+    // maps nothing reads them after this phase)
+    f32x4 Lq[MT][RT], Lk[RT][MT];
     {
-      f32x4 Lq[MT][RT], Lk[RT][MT];
 #pragma unroll
       for (int tt = 0; tt < RT; ++tt) {
         const float init = (G::KIND == kFavor) ? -0.5f * qn[16 * tt + c] : 0.f;
@@ -254,7 +256,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const bool ok = 16 * st + 4 * g + r < count;
-            kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : fmaxf(kv[r], 0.f) + a.relu_eps;
+            kv[r] = !ok ? 0.f : (G::KIND == kFavor) ? fast_exp2(kv[r] * kLog2e - koff) : plain_feature<G::KIND>(kv[r], a.relu_eps);
           }
           store_tile_T<T>(Zk, LDZK, kv, 16 * st, 16 * mt);
         }
@@ -270,7 +272,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           f32x4 qv = Lq[mt][tt];
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            qv[r] = (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(qv[r] * kLog2e - qs) : fmaxf(qv[r], 0.f) + a.relu_eps;
+            qv[r] = (t >= count) ? 0.f : (G::KIND == kFavor) ? fast_exp2(qv[r] * kLog2e - qs) : plain_feature<G::KIND>(qv[r], a.relu_eps);
           store_tile_T<T>(Zq, LDZF, qv, 16 * mt, 16 * tt);
         }
       }
@@ -451,7 +453,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           const f32x4 qv = load_tile_T(Zq, LDZF, 16 * mt, 16 * tt);
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            acc[r] = (G::KIND == kFavor) ? acc[r] * qv[r] : (qv[r] > a.relu_eps ? acc[r] : 0.f);
+            acc[r] = vjp_factor<G::KIND>(acc[r], qv[r], Lq[mt][tt][r], a.relu_eps);
             rs[tt] += acc[r];
           }
           store_tile_T<T>(ZP, LDZF, acc, 16 * mt, 16 * tt);
@@ -537,7 +539,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
           const f32x4 kv = load_tile_T(Zk, LDZK, 16 * st, 16 * mt);
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            acc[r] = (G::KIND == kFavor) ? acc[r] * kv[r] : (kv[r] > a.relu_eps ? acc[r] : 0.f);
+            acc[r] = vjp_factor<G::KIND>(acc[r], kv[r], Lk[st][mt][r], a.relu_eps);
             rk[st][r] += acc[r];
           }
           store_tile_T<T>(ZPk, LDZK, acc, 16 * st, 16 * mt);

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
 #pragma unroll
       for (int st = 0; st < RT; ++st) {
         const bool col_ok = 16 * st + L.c < count;
-        f32x4 kt[MT];
+        f32x4 kt[MT], kl[MT];  // features and (square map) logits
         // exponent offset of the column's key row, the row term -|k|^2/2
         // included; rows past the block: infinite (features exactly zero)
         const float kc = (G::KIND == kFavor) ? (col_ok ? koff + 0.5f * kLog2e * kn[16 * st + L.c] : INFINITY) : 0.f;
@@ -196,13 +196,16 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
 #pragma unroll
             for (int kb = 0; kb < EB; ++kb) acc = mma(acc, Wl[mt][kb], kfr[kb]);
           }
+          kl[mt] = acc;
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            acc[r] = (G::KIND == kFavor) ? fast_exp2(acc[r] * kLog2e - kc) : (col_ok ? fmaxf(acc[r], 0.f) + a.relu_eps : 0.f);
+            acc[r] = (G::KIND == kFavor) ? fast_exp2(acc[r] * kLog2e - kc)
+                                         : (col_ok ? plain_feature<G::KIND>(acc[r], a.relu_eps) : 0.f);
           kt[mt] = acc;
           store_tile_T<T>(L, Kt, LDK, acc, w * FW + 16 * mt, 16 * st);
         }
-        // dK~^T[m][s] = sum_e G[m][e] V[s][e] + z-cotangent[m]; Pk^T = dK~^T . K~^T (FAVOR+) or masked (ReLU)
+        // dK~^T[m][s] = sum_e G[m][e] V[s][e] + z-cotangent[m]; Pk^T = dK~^T . K~^T (FAVOR+),
+        // masked (ReLU) or times 2 l (square)
         // (columns past the block have K~ = 0, hence Pk = 0)
         float sum = 0.f;
         F vfr[EB];
@@ -217,7 +220,7 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, frag_rm(L, Gs, LDG, w * FW + 16 * mt, 32 * kb), vfr[kb]);
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            acc[r] = (G::KIND == kFavor) ? acc[r] * kt[mt][r] : (kt[mt][r] > a.relu_eps ? acc[r] : 0.f);
+            acc[r] = vjp_factor<G::KIND>(acc[r], kt[mt][r], kl[mt][r], a.relu_eps);
             sum += acc[r];
           }
           store_tile_T<T>(L, Pk, LDK, acc, w * FW + 16 * mt, 16 * st);

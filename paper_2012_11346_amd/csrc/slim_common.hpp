@@ -8,7 +8,26 @@
 
 namespace slim {
 
-enum Kind { kFavor = 0, kRelu = 1 };
+enum Kind { kFavor = 0, kRelu = 1, kSquare = 2 };
+
+// Features of the maps without shifts, from the logit l = w_m . x:
+// ReLU max(l, 0) + eps, square l^2.
+// (FAVOR+ has shifts and is formed by its callers; l is returned for it)
+template <int KIND>
+__device__ __forceinline__ float plain_feature(float l, float eps) {
+  if constexpr (KIND == kRelu) return fmaxf(l, 0.f) + eps;
+  else if constexpr (KIND == kSquare) return l * l;
+  else return l;
+}
+// The chain-rule factor of a feature's cotangent dphi: FAVOR+ dphi * phi
+// (then times (w - x)), ReLU dphi * [l > 0] (decided from phi > eps), square
+// dphi * 2 l (the logit l itself is needed: phi = l^2 has lost its sign).
+template <int KIND>
+__device__ __forceinline__ float vjp_factor(float dphi, float phi, float l, float eps) {
+  if constexpr (KIND == kFavor) return dphi * phi;
+  else if constexpr (KIND == kRelu) return phi > eps ? dphi : 0.f;
+  else return 2.f * l * dphi;
+}
 
 // Work split: a workgroup of 4 waves owns one (batch, head, segment); wave w
 // owns features [w FW, (w + 1) FW) of the M = 4 FW features and keeps its

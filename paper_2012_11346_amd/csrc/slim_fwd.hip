@@ -362,14 +362,14 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? fmaxf(Lk[st][mt][r], 0.f) + a.relu_eps : 0.f;
+            Lk[st][mt][r] = (16 * st + 4 * g + r < count) ? plain_feature<G::KIND>(Lk[st][mt][r], a.relu_eps) : 0.f;
       if constexpr (QSIDE) {
 #pragma unroll
         for (int tt = 0; tt < RT; ++tt)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) Lq[mt][tt][r] = fmaxf(Lq[mt][tt][r], 0.f) + a.relu_eps;
+            for (int r = 0; r < 4; ++r) Lq[mt][tt][r] = plain_feature<G::KIND>(Lq[mt][tt][r], a.relu_eps);
       }
     }
 
@@ -617,7 +617,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
           const int m = w * FW + 16 * mt + 4 * g + r;
           const float x = Lq[mt][tt][r];
           Ph[(size_t)(start + t) * M + m] =
-              (G::KIND == kFavor) ? fast_exp2((x - qs) * kLog2e - half_log2M) : fmaxf(x, 0.f) + a.relu_eps;
+              (G::KIND == kFavor) ? fast_exp2((x - qs) * kLog2e - half_log2M) : plain_feature<G::KIND>(x, a.relu_eps);
         }
     }
   } else {
@@ -635,7 +635,7 @@ __global__ __launch_bounds__(256, 1) void featmap_kernel(FeatArgs a) {
           const int m = w * FW + 16 * mt + c;
           const float x = Lk[st][mt][r] - (G::KIND == kFavor ? 0.5f * xn[s] : 0.f);
           Ph[(size_t)(start + s) * M + m] =
-              (G::KIND == kFavor) ? fast_exp2((x - ks) * kLog2e - half_log2M) : fmaxf(x, 0.f) + a.relu_eps;
+              (G::KIND == kFavor) ? fast_exp2((x - ks) * kLog2e - half_log2M) : plain_feature<G::KIND>(x, a.relu_eps);
         }
   }
 }

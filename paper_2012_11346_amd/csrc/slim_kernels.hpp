@@ -152,14 +152,17 @@ int carry8_chunks_per_head(int L, int C, int P);
 hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hipStream_t s);
 
 // every compiled (element type, head dim, features per wave, tile rows, kind);
-// fp32 problems serve exactness checks and are compiled for d * M <= 4096
+// fp32 problems serve exactness checks and are compiled for d * M <= 4096;
+// the square map is compiled for M = 64 (16 features per wave)
 #define SLIM_FOR_EACH_CONFIG(X)                                                           \
   X(bf16, 64, 64, 32, kFavor) X(bf16, 64, 32, 32, kFavor) X(bf16, 64, 16, 32, kFavor) \
   X(bf16, 32, 64, 32, kFavor) X(bf16, 32, 32, 32, kFavor) X(bf16, 32, 16, 32, kFavor) \
   X(bf16, 64, 64, 32, kRelu) X(bf16, 64, 32, 32, kRelu) X(bf16, 64, 16, 32, kRelu)    \
   X(bf16, 32, 64, 32, kRelu) X(bf16, 32, 32, 32, kRelu) X(bf16, 32, 16, 32, kRelu)    \
   X(float, 64, 16, 32, kFavor) X(float, 32, 32, 32, kFavor) X(float, 32, 16, 32, kFavor) \
-  X(float, 64, 16, 32, kRelu) X(float, 32, 32, 32, kRelu) X(float, 32, 16, 32, kRelu)
+  X(float, 64, 16, 32, kRelu) X(float, 32, 32, 32, kRelu) X(float, 32, 16, 32, kRelu)    \
+  X(bf16, 64, 16, 32, kSquare) X(bf16, 32, 16, 32, kSquare)                               \
+  X(float, 64, 16, 32, kSquare) X(float, 32, 16, 32, kSquare)
 
 // configurations served by the 8-wave backward walk
 #define SLIM_FOR_EACH_BF16_CONFIG(X)                                                  \

@@ -17,12 +17,12 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libslim.so")
 
 SLIM_OK, SLIM_EINVAL, SLIM_EUNSUPPORTED, SLIM_EWORKSPACE, SLIM_EHIP = 0, -1, -2, -3, -4
-FAVOR_PLUS, RELU = 0, 1
+FAVOR_PLUS, RELU, SQUARE = 0, 1, 2
 F32, BF16 = 0, 1
 QUERY, KEY = 0, 1
 PHASE_FWD, PHASE_BWD = 0, 1
 
-KINDS = {"favor+": FAVOR_PLUS, "relu": RELU}
+KINDS = {"favor+": FAVOR_PLUS, "relu": RELU, "square": SQUARE}
 DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
 
 

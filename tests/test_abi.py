@@ -138,6 +138,16 @@ def test_misaligned_tensors_are_rejected_before_any_launch(S):
     assert st == S.SLIM_EINVAL
 
 
+def test_square_map_needs_64_features(S):
+    import ctypes
+
+    for M in (128, 256):
+        p = _p(S, M=M, kind=S.SQUARE)
+        assert S.LIB.slim_workspace_bytes(ctypes.byref(p), S.PHASE_FWD) == 0
+        assert "square" in S.LIB.slim_last_error().decode()
+    assert S.LIB.slim_workspace_bytes(ctypes.byref(_p(S, M=64, kind=S.SQUARE)), S.PHASE_BWD) > 0
+
+
 def test_relu_needs_positive_eps(S):
     p = _p(S, kind=S.RELU)
     p.relu_eps = 0.0
