@@ -1,13 +1,25 @@
 #!/usr/bin/env python3
-"""Benchmark of slice-wise causal FAVOR+ attention, forward + backward, on one GPU.
+"""Benchmark of slice-wise causal linear attention, forward + backward, on one GPU.
 
 One step = slim_fwd + slim_bwd over one batch of the L = 32768 workload
-(B=4, H=8, d=64, M=256, bf16 inputs, FAVOR+), inputs resident in device memory.
-Prints one JSON line with throughput (tokens/s = B*L / step time), a roofline
-entry for the dominant kernel, the fp64 CPU oracle timed on a bounded sample,
-and a slice-length sweep with peak device memory per C.
+(B=4, H=8, d=64, M=256, bf16 inputs, FAVOR+), inputs resident in device
+memory.  Prints one JSON line with throughput (tokens/s = B*L / step time),
+a roofline entry for the dominant kernel, the fp64 CPU oracle timed on the
+whole batch, and, unless switched off:
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--C 64] [--no-sweep] [--no-cpu]
+* sweep: every slice length C of the headline workload, with the in-slice
+  block the kernels ran, the executed-work roofline fraction of the reverse
+  walk, peak device memory beyond inputs and outputs, the lower bound "L/B"
+  (the same measured on an input of length C) and the L2-relative gradient
+  error against the oracle;
+* configs: the other workloads (tiny fp32 exactness check, B8 H8 L4096,
+  L=262144 long context, the six-layer ReLU stack run forward r=1..6 then
+  backward r=6..1), each with time, roofline and parity on sampled heads;
+* peak memory versus L at fixed C;
+* the paper's own feature map (element-wise square, M = d = 64, W = I) at
+  its per-layer shapes.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--C 64] [--quick]
 """
 
 from __future__ import annotations
@@ -25,21 +37,21 @@ sys.path.insert(0, ROOT)
 
 METRIC = "causal FAVOR+ fwd+bwd tokens/sec at L=32k, d=64, M=256; peak mem vs slice C"
 PEAK_BF16_FLOPS = 2.5e15  # MI355X dense bf16 matrix-core peak
-PEAK_HBM_BYTES = 8.0e12
-TILE_ROWS = 32  # rows per tile of the kernels (block of the in-slice evaluation)
+PEAK_FP32_FLOPS = 157.3e12  # fp32 matrix / vector peak
+TILE_ROWS = 32  # rows per tile of the kernels: the block of the in-slice evaluation
+KIND_LABEL = {"favor+": "causal FAVOR+", "relu": "causal ReLU-feature", "square": "causal square-feature"}
 
 
-def algo_flops_per_token_head(d: int, M: int, C: int, tile: int = TILE_ROWS):
-    """Algorithmic flops (2 per multiply-add) per token and head.
-
-    The in-slice prefix sum is evaluated block-iteratively with blocks of
-    c = min(C, tile) rows; inside a block the causal quadratic form costs half
-    of the c x c products (c + 1 per row).
+def flops_per_token_head(d: int, M: int, c: int):
+    """Flops (2 per multiply-add) per token and head, for an in-slice block
+    of c rows evaluated as a causal quadratic form (c + 1 per row, the
+    causal half), the state carried between blocks:
       fwd: 4dM (Q, K logits) + 4M(d+1) (state read + update) + (M+d+1)(c+1)
       bwd: 24dM + 10M + (3M+3d+1)(c+1) (recompute, downdate, gradients, chain
            rule through the feature map, dW)
-    """
-    c = min(C, tile)
+    With c = C this is the algorithmic count of the method with the whole
+    slice as one quadratic form; with c = min(C, 32) it is the work the
+    kernels execute (their in-slice block is a 32-row tile)."""
     fwd = 4 * d * M + 4 * M * (d + 1) + (M + d + 1) * (c + 1)
     bwd = 24 * d * M + 10 * M + (3 * M + 3 * d + 1) * (c + 1)
     return fwd, bwd
@@ -52,7 +64,7 @@ def kernel_sources_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel: str, units_per_launch: float):
+def load_traffic(kernel: str):
     """HBM traffic of a kernel from the committed counter summary, if it was
     taken on the current kernel sources; else None."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
@@ -68,42 +80,34 @@ def load_traffic(kernel: str, units_per_launch: float):
     return k.get("bytes_per_launch")
 
 
-def bwd_walk_name(wl, d: int, M: int) -> str:
-    """Name of the reverse-walk kernel the library launches for this problem:
-    the 8-wave form for bf16 problems with 32 or 64 features per wave."""
+def bwd_walk_name(dtype: str, M: int, kind: str) -> str:
+    """The reverse-walk kernel the library launches: the 8-wave form for bf16
+    problems with 32 or 64 features per wave, else the 4-wave form."""
     forced4 = os.environ.get("SLIM_BWD_WAVES") == "4"
-    return "bwd_walk8_kernel" if (wl.dtype == "bf16" and M // 4 in (32, 64) and not forced4) else "bwd_walk_kernel"
+    return "bwd_walk8_kernel" if (dtype == "bf16" and M // 4 in (32, 64) and kind != "square" and not forced4) \
+        else "bwd_walk_kernel"
 
 
-def cpu_baseline(x, C: int, B: int, H: int, L: int):
-    """Time the fp64 oracle (Algorithm 1 with the in-slice quadratic form) on
-    the whole batch of the workload (every batch element and head, full
-    length).  Returns the record and the oracle's Y/gradients for a parity
-    check of the timed configuration."""
-    import oracle as O
-
+def threads_used() -> int:
     try:
         from threadpoolctl import threadpool_info
 
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
     except Exception:
-        threads = os.cpu_count() or 1
-    Q, K, V, dY = (x[k] for k in ("Q", "K", "V", "dY"))
-    t0 = time.perf_counter()
-    Y, st = O.slim_forward(Q, K, V, x["W"], C, "favor+", within="quadratic")
-    g = O.slim_backward(Q, K, V, x["W"], dY, C, "favor+", st, within="quadratic")
-    t = time.perf_counter() - t0
-    rec = {
-        "value": B * L / t,
-        "unit": "tokens/s",
-        "cores": int(threads),
-        "kind": "oracle",
-        "sample": f"the whole workload batch (B={B}, H={H}, L={L}), fp64 Algorithm 1 forward + backward with "
-        f"the in-slice quadratic form at C={C}; {t:.1f} s on the host",
-        "seconds": t,
-        "host_cpus": os.cpu_count(),
-    }
-    return rec, Y, g
+        return os.cpu_count() or 1
+
+
+def mask_w(x):
+    """W the oracle takes the ReLU derivative's decisions with: the bf16
+    split hi + lo the kernels form the logits from (bf16), else W."""
+    import torch
+
+    if x["Q"].dtype != torch.bfloat16:
+        return None
+    W = x["W"].float()
+    hi = W.to(torch.bfloat16).float()
+    lo = (W - hi).to(torch.bfloat16).float()
+    return hi.double().numpy() + lo.double().numpy()
 
 
 def main():
@@ -112,16 +116,20 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--C", type=int, default=64)
-    ap.add_argument("--workload", default="sweep_32k")
-    ap.add_argument("--no-sweep", action="store_true")
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--sweep-steps", type=int, default=3)
+    ap.add_argument("--no-sweep", action="store_true", help="skip the slice-length sweep")
+    ap.add_argument("--no-configs", action="store_true", help="skip the other workloads and memory-vs-L")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing and the parity checks")
+    ap.add_argument("--quick", action="store_true", help="headline only (= --no-sweep --no-configs --no-cpu)")
+    ap.add_argument("--sweep-steps", type=int, default=5)
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only copy a device buffer of this many MiB (calibration of memory counters) and exit")
     args = ap.parse_args()
+    if args.quick:
+        args.no_sweep = args.no_configs = args.no_cpu = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path runs on a single "
-              "MI355X; sharded, GPUs would split the heads and batch rows and sum dW with one all-reduce)", file=sys.stderr)
+              "MI355X; sharded, GPUs would split the heads and batch rows and sum dW with one all-reduce)",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -133,120 +141,194 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    dev = torch.device("cuda", 0)
     if args.copy_mib > 0:
         # a plain copy of known size: reads and writes copy_mib MiB once per launch
         n = args.copy_mib << 20
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "launches": 3}), flush=True)
         return
-    wl = workload(args.workload)
-    B, H, L, d, M = wl.B, wl.H, wl.L, wl.d, wl.M
-    kind = wl.kind
-    t0 = time.perf_counter()
-    x = make_inputs(wl)
-    print(f"[bench] inputs generated in {time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
-    dev = torch.device("cuda", 0)
-    Q, K, V, dY = (x[k].to(dev) for k in ("Q", "K", "V", "dY"))
-    W = x["W"].to(dev)
-    torch.cuda.synchronize()
-    io_bytes = torch.cuda.memory_allocated()
 
-    def buffers(C):
-        p = slim.problem(B, H, L, d, M, C, Q.dtype, kind)
-        bufs = dict(
-            Y=torch.empty_like(Q),
-            st=torch.empty((B, H, M, d + 1), dtype=torch.float32, device=dev),
-            ks=torch.empty((B, H), dtype=torch.float32, device=dev),
-            dQ=torch.empty_like(Q),
-            dK=torch.empty_like(K),
-            dV=torch.empty_like(V),
-            dW=torch.empty((M, d), dtype=torch.float32, device=dev),
-            wsf=torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_FWD)), dtype=torch.uint8, device=dev),
-            wsb=torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_BWD)), dtype=torch.uint8, device=dev),
-        )
-        # the forward's segment boundary states, handed to the backward (state-sized)
-        n_ctx = slim.context_bytes(p)
-        if n_ctx > 0:
-            bufs["wsctx"] = torch.empty(n_ctx // 4, dtype=torch.float32, device=dev)
-        return p, bufs
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
-    def step(C, b):
-        slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"],
-                 ctx=b.get("wsctx"))
-        slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
-                 dW=b["dW"], ctx=b.get("wsctx"))
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    stream = torch.cuda.current_stream()
 
-    def timed(C, steps, warmup):
-        """warmup + `steps` timed steps, bracketed by two events.  Inside the
-        timed region only the reverse walk's launches carry events (recorded
-        by the library around that launch: its duration for the roofline);
-        the per-call breakdown (forward, backward, forward walk) comes from a
-        separate pass of the same steps afterwards, so that its events do not
-        add to the timed steps."""
+    class Layer:
+        """Device inputs, outputs and workspaces of one attention op."""
+
+        def __init__(self, x, C, kind):
+            self.kind = kind
+            self.C = C
+            self.x = x
+            self.Q, self.K, self.V, self.dY = (x[k].to(dev) for k in ("Q", "K", "V", "dY"))
+            self.W = x["W"].to(dev)
+            B, H, L, d = self.Q.shape
+            M = self.W.shape[0]
+            self.shape = (B, H, L, d, M)
+            torch.cuda.synchronize()
+
+        def alloc(self):
+            B, H, L, d, M = self.shape
+            p = slim.problem(B, H, L, d, M, self.C, self.Q.dtype, self.kind)
+            self.p = p
+            self.Y = torch.empty_like(self.Q)
+            self.st = torch.empty((B, H, M, d + 1), dtype=torch.float32, device=dev)
+            self.ks = torch.empty((B, H), dtype=torch.float32, device=dev) if self.kind == "favor+" else None
+            self.dQ, self.dK, self.dV = (torch.empty_like(self.Q) for _ in range(3))
+            self.dW = torch.empty((M, d), dtype=torch.float32, device=dev)
+            self.out_bytes = sum(t.numel() * t.element_size() for t in
+                                 (self.Y, self.st, self.dQ, self.dK, self.dV, self.dW) + ((self.ks,) if self.ks is not None else ()))
+            self.wsf = torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_FWD)), dtype=torch.uint8, device=dev)
+            self.wsb = torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_BWD)), dtype=torch.uint8, device=dev)
+            n_ctx = slim.context_bytes(p)
+            self.ctx = torch.empty(n_ctx // 4, dtype=torch.float32, device=dev) if n_ctx > 0 else None
+            self.ws_bytes = self.wsf.numel() + self.wsb.numel() + n_ctx
+            return self
+
+        def free(self):
+            for n in ("Y", "st", "ks", "dQ", "dK", "dV", "dW", "wsf", "wsb", "ctx"):
+                setattr(self, n, None)
+
+        def fwd(self):
+            slim.fwd(self.Q, self.K, self.V, self.W, self.C, self.kind, ws=self.wsf, Y=self.Y, state_out=self.st,
+                     kshift_out=self.ks, ctx=self.ctx)
+
+        def bwd(self, dY=None):
+            slim.bwd(self.Q, self.K, self.V, self.W, self.dY if dY is None else dY, self.C, self.ks, self.kind,
+                     ws=self.wsb, dQ=self.dQ, dK=self.dK, dV=self.dV, dW=self.dW, ctx=self.ctx)
+
+    def run_step(layers):
+        """forward r = 1..n, then backward r = n..1"""
+        for ly in layers:
+            ly.fwd()
+        for ly in reversed(layers):
+            ly.bwd()
+
+    def timed(layers, steps, warmup, breakdown=False):
+        """warmup + `steps` timed steps bracketed by two events.  Inside the
+        timed region only the reverse walks carry events (the library
+        records them around that kernel's launch: its duration for the
+        roofline); with `breakdown`, a second pass of the same number of
+        steps times the calls and the forward walk separately, so that its
+        events do not add to the timed steps."""
         torch.cuda.synchronize()
         pre = torch.cuda.memory_allocated()
         torch.cuda.reset_peak_memory_stats()
-        p, b = buffers(C)
+        for ly in layers:
+            ly.alloc()
         for _ in range(warmup):
-            step(C, b)
-        stream = torch.cuda.current_stream()
-        mk = lambda: torch.cuda.Event(enable_timing=True)
+            run_step(layers)
+        n = len(layers)
         t0, t1 = mk(), mk()
-        wb = [(mk(), mk()) for _ in range(steps)]
-        bd = [[mk() for _ in range(5)] for _ in range(steps)]
-        for e in [t0, t1] + [x_ for pair in wb for x_ in pair] + [x_ for e5 in bd for x_ in e5]:
+        wb = [[(mk(), mk()) for _ in range(n)] for _ in range(steps)]
+        for e in [t0, t1] + [x_ for row in wb for pair in row for x_ in pair]:
             e.record(stream)  # create every event before the timed region
         torch.cuda.synchronize()
         t0.record(stream)
         for i in range(steps):
-            slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"],
-                     ctx=b.get("wsctx"))
-            slim.time_walk(slim.PHASE_BWD, wb[i][0], wb[i][1])
-            slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
-                     dW=b["dW"], ctx=b.get("wsctx"))
+            for ly in layers:
+                ly.fwd()
+            for k, ly in enumerate(reversed(layers)):
+                slim.time_walk(slim.PHASE_BWD, wb[i][k][0], wb[i][k][1])
+                ly.bwd()
         t1.record(stream)
         torch.cuda.synchronize()
         total_ms = t0.elapsed_time(t1)
-        bwd_walk_ms = sum(x.elapsed_time(y) for x, y in wb) / steps
+        walk_ms = sum(a.elapsed_time(b) for row in wb for a, b in row) / (steps * n)
         peak = torch.cuda.max_memory_allocated()
-        # breakdown pass (not timed as steps)
-        for e in bd:
-            e[0].record(stream)
-            slim.time_walk(slim.PHASE_FWD, e[1], e[2])
-            slim.fwd(Q, K, V, W, C, kind, ws=b["wsf"], Y=b["Y"], state_out=b["st"], kshift_out=b["ks"],
-                     ctx=b.get("wsctx"))
-            e[3].record(stream)
-            slim.bwd(Q, K, V, W, dY, C, b["ks"], kind, ws=b["wsb"], dQ=b["dQ"], dK=b["dK"], dV=b["dV"],
-                     dW=b["dW"], ctx=b.get("wsctx"))
-            e[4].record(stream)
-        torch.cuda.synchronize()
-        avg = lambda i, j: sum(e[i].elapsed_time(e[j]) for e in bd) / steps
-        out_bytes = sum(t.numel() * t.element_size() for k, t in b.items() if not k.startswith("ws"))
-        return dict(total_ms=total_ms, ms=total_ms / steps, fwd_ms=avg(0, 3), bwd_ms=avg(3, 4),
-                    fwd_walk_ms=avg(1, 2), bwd_walk_ms=bwd_walk_ms, peak=peak, extra=peak - pre - out_bytes,
-                    out_bytes=out_bytes, ws_fwd=b["wsf"].numel(), ws_bwd=b["wsb"].numel(),
-                    ctx=b["wsctx"].numel() * 4 if "wsctx" in b else 0,
-                    segments=slim.num_segments(p)), b
+        out_bytes = sum(ly.out_bytes for ly in layers)
+        r = dict(ms=total_ms / steps, bwd_walk_ms=walk_ms, peak=peak, extra=peak - pre - out_bytes,
+                 ws=sum(ly.ws_bytes for ly in layers), segments=slim.num_segments(layers[0].p))
+        if breakdown:
+            bd = [[mk() for _ in range(5)] for _ in range(steps)]
+            for e5 in bd:
+                for e in e5:
+                    e.record(stream)
+            torch.cuda.synchronize()
+            for e in bd:
+                e[0].record(stream)
+                slim.time_walk(slim.PHASE_FWD, e[1], e[2])
+                for ly in layers:
+                    ly.fwd()
+                e[3].record(stream)
+                for ly in reversed(layers):
+                    ly.bwd()
+                e[4].record(stream)
+            torch.cuda.synchronize()
+            avg = lambda i, j: sum(e[i].elapsed_time(e[j]) for e in bd) / steps
+            r.update(fwd_ms=avg(0, 3), bwd_ms=avg(3, 4), fwd_walk_ms=avg(1, 2))
+        return r
 
+    def roofline(kernel, dtype, units, flops_per_unit, launch_ms):
+        peak = PEAK_BF16_FLOPS if dtype == "bf16" else PEAK_FP32_FLOPS
+        achieved = units * flops_per_unit / (launch_ms / 1e3)
+        return {"kernel": kernel, "bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / peak, "flops_per_token_head": flops_per_unit,
+                "token_heads_per_launch": units, "launch_ms": launch_ms}
+
+    def rel_errors(a, ref):
+        a = np.asarray(a, dtype=np.float64)
+        ref = np.asarray(ref, dtype=np.float64)
+        return {"max_rel": float(np.max(np.abs(a - ref)) / np.max(np.abs(ref))),
+                "l2_rel": float(np.linalg.norm(a - ref) / np.linalg.norm(ref))}
+
+    def h64(t):
+        return t.detach().double().cpu().numpy()
+
+    def oracle_heads(x, heads, kind):
+        """The fp64 oracle (Algorithm 1 with the in-slice quadratic form; the
+        exact result does not depend on the slice length) on sampled heads."""
+        import oracle as O
+
+        pick = lambda t: np.stack([h64(t[b, h]) for b, h in heads])[None]
+        Q, K, V, dY = (pick(x[k]) for k in ("Q", "K", "V", "dY"))
+        W = h64(x["W"])
+        Y, st = O.slim_forward(Q, K, V, W, 256, kind, within="quadratic")
+        g = O.slim_backward(Q, K, V, W, dY, 256, kind, st, within="quadratic", mask_W=mask_w(x))
+        return {"Y": Y, "dQ": g[0], "dK": g[1], "dV": g[2], "dW": g[3]}
+
+    def parity(layer, heads, ref):
+        """errors of the last run's outputs on the sampled heads; dW from a
+        second backward with dY zero outside them (isolates their share)"""
+        pick = lambda t: np.stack([h64(t[b, h]) for b, h in heads])[None]
+        out = {n: rel_errors(pick(getattr(layer, n)), ref[n]) for n in ("Y", "dQ", "dK", "dV")}
+        mask = torch.zeros(layer.dY.shape[:2], dtype=torch.bool, device=dev)
+        for b, h in heads:
+            mask[b, h] = True
+        dYm = torch.where(mask[:, :, None, None], layer.dY, torch.zeros_like(layer.dY))
+        layer.bwd(dYm)
+        torch.cuda.synchronize()
+        out["dW"] = rel_errors(h64(layer.dW), ref["dW"])
+        return out
+
+    # ------------------------------------------------------------ headline
+    wl = workload("sweep_32k")
+    B, H, L, d, M, kind = wl.B, wl.H, wl.L, wl.d, wl.M, wl.kind
     C = args.C
-    print(f"[bench] timing C={C}: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
-    r, b = timed(C, args.steps, args.warmup)
+    t0 = time.perf_counter()
+    x = make_inputs(wl)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f}s")
+    head = Layer(x, C, kind)
+    log(f"timing C={C}: warmup {args.warmup}, steps {args.steps}")
+    r = timed([head], args.steps, args.warmup, breakdown=True)
     tokens = B * L
+    units = B * H * L  # token-heads per launch of either walk
     value = tokens / (r["ms"] / 1e3)
-    fl_f, fl_b = algo_flops_per_token_head(d, M, C)
-    units = B * H * L  # token-heads per launch of either walk kernel
-    # the walk kernels do all of the algorithmic work of their phase; the
-    # segment pre-passes and scans are extra work of the parallel split
-    if r["bwd_walk_ms"] >= r["fwd_walk_ms"]:
-        dominant, dom_ms, dom_flops = bwd_walk_name(wl, d, M), r["bwd_walk_ms"], fl_b * units
-    else:
-        dominant, dom_ms, dom_flops = "fwd_walk_kernel", r["fwd_walk_ms"], fl_f * units
-    achieved = dom_flops / (dom_ms / 1e3)
-    traffic = load_traffic(dominant, units)
+    alg_f, alg_b = flops_per_token_head(d, M, C)
+    blk = min(C, TILE_ROWS)
+    ex_f, ex_b = flops_per_token_head(d, M, blk)
+    dominant = bwd_walk_name(wl.dtype, M, kind)
+    rl = roofline(dominant, wl.dtype, units, alg_b, r["bwd_walk_ms"])
+    rl["traffic"] = load_traffic(dominant)
+    rl["flops_basis"] = (f"algorithmic count with the slice as one quadratic form (c = C = {C}); the kernel "
+                         f"executes {ex_b} flops per token-head with its {blk}-row in-slice block, frac "
+                         f"{units * ex_b / (r['bwd_walk_ms'] / 1e3) / PEAK_BF16_FLOPS:.3f} on that count")
     out = {
         "metric": METRIC,
         "value": value,
@@ -258,60 +340,176 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": f"{wl.name}: causal FAVOR+ attention fwd+bwd, B={B} H={H} L={L} d={d} M={M}, "
-            f"bf16 inputs with fp32 accumulation, slice length C={C}",
+            "workload": f"{wl.name}: {KIND_LABEL[kind]} attention fwd+bwd, B={B} H={H} L={L} d={d} M={M}, "
+                        f"bf16 inputs with fp32 accumulation, float32 W, slice length C={C}",
             "B": B, "H": H, "L": L, "d": d, "M": M, "C": C, "kind": kind,
-            "segments_per_head": r["segments"],
+            "segments_per_head": r["segments"], "in_slice_block": blk,
         },
         "fwd_ms": r["fwd_ms"],
         "bwd_ms": r["bwd_ms"],
         "fwd_walk_ms": r["fwd_walk_ms"],
         "bwd_walk_ms": r["bwd_walk_ms"],
-        "roofline": {
-            "kernel": dominant,
-            "bound": "mfma",
-            "achieved": achieved / 1e12,
-            "peak": PEAK_BF16_FLOPS / 1e12,
-            "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_FLOPS,
-            "traffic": traffic,
-            "flops_per_token_head": {"fwd": fl_f, "bwd": fl_b},
-            "token_heads_per_launch": units,
-            "launch_ms": dom_ms,
-        },
-        "mfma_frac_fwd_bwd": (fl_f + fl_b) * units / (r["ms"] / 1e3) / PEAK_BF16_FLOPS,
-        "peak_mem": {"peak_bytes": r["peak"], "input_bytes": io_bytes, "output_bytes": r["out_bytes"],
-                     "beyond_io_bytes": r["extra"],
-                     "workspace_fwd": r["ws_fwd"], "workspace_bwd": r["ws_bwd"], "context": r["ctx"]},
+        "roofline": rl,
+        "mfma_frac_fwd_bwd": (alg_f + alg_b) * units / (r["ms"] / 1e3) / PEAK_BF16_FLOPS,
+        "peak_mem": {"peak_bytes": r["peak"], "beyond_io_bytes": r["extra"], "workspace_and_context": r["ws"]},
     }
-    print(f"[bench] C={C}: {r['ms']:.3f} ms/step (fwd {r['fwd_ms']:.3f}, bwd {r['bwd_ms']:.3f}; walks "
-          f"{r['fwd_walk_ms']:.3f} / {r['bwd_walk_ms']:.3f}), {value:.3e} tokens/s", file=sys.stderr, flush=True)
+    log(f"C={C}: {r['ms']:.3f} ms/step (fwd {r['fwd_ms']:.3f}, bwd {r['bwd_ms']:.3f}; walks "
+        f"{r['fwd_walk_ms']:.3f} / {r['bwd_walk_ms']:.3f}), {value:.3e} tokens/s")
+    head.free()
+    torch.cuda.empty_cache()
 
+    ref = None
+    sample = [(0, 0), (3, 7)]
+    if not args.no_cpu:
+        log("oracle on two sampled heads")
+        ref = oracle_heads(x, sample, kind)
+
+    # ------------------------------------------------------------ slice-length sweep
     if not args.no_sweep:
         sweep = []
         for Cs in wl.C:
-            rs, bs = timed(Cs, args.sweep_steps, 5)
-            del bs
-            sweep.append({"C": Cs, "tokens_per_s": tokens / (rs["ms"] / 1e3), "ms_per_step": rs["ms"],
-                          "peak_bytes": rs["peak"], "beyond_io_bytes": rs["extra"], "workspace_bwd": rs["ws_bwd"]})
-            print(f"[bench] sweep C={Cs}: {rs['ms']:.3f} ms/step, extra memory {rs['extra'] / 2**20:.1f} MiB",
-                  file=sys.stderr, flush=True)
+            ly = Layer(x, Cs, kind)
+            rs = timed([ly], args.sweep_steps, 5)
+            blk_s = min(Cs, TILE_ROWS)
+            exf, exb = flops_per_token_head(d, M, blk_s)
+            algf, algb = flops_per_token_head(d, M, Cs)
+            rec = {"C": Cs, "in_slice_block": blk_s, "tokens_per_s": tokens / (rs["ms"] / 1e3),
+                   "ms_per_step": rs["ms"], "bwd_walk_ms": rs["bwd_walk_ms"],
+                   "roofline_executed": roofline(dominant, "bf16", units, exb, rs["bwd_walk_ms"]),
+                   "algorithmic_flops_per_token_head_at_C": algf + algb,
+                   "peak_bytes": rs["peak"], "beyond_io_bytes": rs["extra"]}
+            if ref is not None:
+                e = parity(ly, sample, ref)
+                rec["grad_l2_rel"] = {k: v["l2_rel"] for k, v in e.items() if k != "Y"}
+                rec["max_rel"] = {k: v["max_rel"] for k, v in e.items()}
+            ly.free()
+            del ly
+            torch.cuda.empty_cache()
+            # lower bound "L/B": the same method on an input of length C only
+            xs = {k: (v[:, :, :Cs].contiguous() if k != "W" else v) for k, v in x.items()}
+            lb = Layer(xs, Cs, kind)
+            rb = timed([lb], 1, 1)
+            rec["lower_bound_beyond_io_bytes"] = rb["extra"]
+            lb.free()
+            del lb, xs
+            torch.cuda.empty_cache()
+            sweep.append(rec)
+            log(f"sweep C={Cs} (block {blk_s}): {rs['ms']:.3f} ms/step, beyond inputs/outputs "
+                f"{rs['extra'] / 2**20:.1f} MiB (L/B {rec['lower_bound_beyond_io_bytes'] / 2**20:.1f} MiB)")
         out["sweep"] = sweep
 
+    # ------------------------------------------------------------ headline parity and oracle timing
     if not args.no_cpu:
-        print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
-        rec, Yo, go = cpu_baseline(x, C, B, H, L)
-        out["cpu_baseline"] = rec
+        import oracle as O
 
-        # parity of the timed configuration against the oracle, whole batch
-        def mr(a, ref):
-            return float(np.max(np.abs(a.double().cpu().numpy() - ref)) / np.max(np.abs(ref)))
+        ly = Layer(x, C, kind)
+        timed([ly], 1, 1)
+        out["parity"] = {"unrounded_W": parity(ly, sample, ref)}
+        ly.free()
+        del ly
+        torch.cuda.empty_cache()
+        # the same with a bf16-representable W
+        xr = dict(x)
+        xr["W"] = make_inputs(wl, tensors=("W",), round_w=True)["W"]
+        lr = Layer(xr, C, kind)
+        timed([lr], 1, 1)
+        refr = oracle_heads(xr, sample[:1], kind)
+        out["parity"]["rounded_W"] = parity(lr, sample[:1], refr)
+        lr.free()
+        del lr, xr
+        torch.cuda.empty_cache()
+        log("timing the fp64 oracle on the host (whole batch)")
+        t0 = time.perf_counter()
+        Yo, st = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind, within="quadratic")
+        O.slim_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], C, kind, st, within="quadratic")
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {
+            "value": B * L / t, "unit": "tokens/s", "cores": threads_used(), "kind": "oracle",
+            "sample": f"the whole workload batch (B={B}, H={H}, L={L}), fp64 Algorithm 1 forward + backward, "
+                      f"{kind}, in-slice quadratic form at C={C}; {t:.1f} s on the host",
+            "seconds": t, "host_cpus": os.cpu_count()}
+    del x
+    torch.cuda.empty_cache()
 
-        out["parity"] = {"Y": mr(b["Y"], Yo), "dQ": mr(b["dQ"], go[0]), "dK": mr(b["dK"], go[1]),
-                         "dV": mr(b["dV"], go[2]), "dW": mr(b["dW"], go[3])}
+    # ------------------------------------------------------------ other workloads
+    if not args.no_configs:
+        configs = []
+        for name, heads in (("tiny_exact", [(0, 0)]), ("mid_bf16", [(7, 7)]), ("long_256k", [(0, 5)]),
+                            ("relu_stack", [(1, 11)])):
+            w2 = workload(name)
+            Cw = w2.C[0]
+            t0 = time.perf_counter()
+            xs = [make_inputs(w2, layer=k) for k in range(w2.layers)]
+            layers = [Layer(xk, Cw, w2.kind) for xk in xs]
+            log(f"{name}: inputs in {time.perf_counter() - t0:.1f}s")
+            steps = 5 if w2.L * w2.B * w2.H * w2.layers >= (1 << 21) else 20
+            rc = timed(layers, steps, 5)
+            u = w2.B * w2.H * w2.L
+            blk_w = min(Cw, TILE_ROWS)
+            exf, exb = flops_per_token_head(w2.d, w2.M, blk_w)
+            algf, algb = flops_per_token_head(w2.d, w2.M, Cw)
+            kname = bwd_walk_name(w2.dtype, w2.M, w2.kind)
+            rec = {"workload": f"{name}: {KIND_LABEL[w2.kind]}, {w2.layers} layer(s) x (B={w2.B} H={w2.H} L={w2.L} "
+                               f"d={w2.d} M={w2.M}), {w2.dtype}, C={Cw}"
+                               + (", forward r=1..6 then backward r=6..1" if w2.layers > 1 else ""),
+                   "C": Cw, "in_slice_block": blk_w, "ms_per_step": rc["ms"],
+                   "tokens_per_s": w2.B * w2.L * w2.layers / (rc["ms"] / 1e3),
+                   "tokens_counted": "B*L per layer" if w2.layers > 1 else "B*L",
+                   "roofline": roofline(kname, w2.dtype, u, algb, rc["bwd_walk_ms"]),
+                   "roofline_executed": roofline(kname, w2.dtype, u, exb, rc["bwd_walk_ms"]),
+                   "peak_bytes": rc["peak"], "beyond_io_bytes": rc["extra"], "segments_per_head": rc["segments"]}
+            if not args.no_cpu:
+                # the first layer (its backward runs last in a step) on a sampled head
+                rec["parity_layer1"] = parity(layers[0], heads, oracle_heads(xs[0], heads, w2.kind))
+            configs.append(rec)
+            log(f"{name}: {rc['ms']:.3f} ms/step, {rec['tokens_per_s']:.3e} tokens/s, reverse walk frac "
+                f"{rec['roofline']['frac']:.3f}")
+            for ly in layers:
+                ly.free()
+            del layers, xs
+            torch.cuda.empty_cache()
+        out["configs"] = configs
+
+        # peak memory beyond inputs and outputs versus L at fixed C
+        w4 = workload("long_256k")
+        x4 = make_inputs(w4, tensors=("Q", "K", "V", "dY", "W"))
+        mem = []
+        for Ls in (4096, 32768, 262144):
+            xs = {k: (v[:, :, :Ls].contiguous() if k != "W" else v) for k, v in x4.items()}
+            ly = Layer(xs, 512, w4.kind)
+            rm = timed([ly], 1, 1)
+            mem.append({"L": Ls, "beyond_io_bytes": rm["extra"], "workspace_and_context": rm["ws"]})
+            ly.free()
+            del ly, xs
+            torch.cuda.empty_cache()
+        out["peak_mem_vs_L"] = {"B": w4.B, "H": w4.H, "d": w4.d, "M": w4.M, "C": 512, "rows": mem}
+        del x4
+        log("memory vs L: " + ", ".join(f"L={m['L']}: {m['beyond_io_bytes'] / 2**20:.1f} MiB" for m in mem))
+
+        # the paper's feature map at its per-layer shapes (configurations I-IV)
+        from synth import Workload
+
+        sq = []
+        for Ls, Hs in ((512, 4), (1024, 8), (4096, 16), (16384, 16)):
+            ws = Workload(f"square_{Ls}", 700 + Hs, 1, Hs, Ls, 64, 64, (64,), "bf16", "square")
+            xs = make_inputs(ws)
+            xs["W"] = torch.eye(64, dtype=torch.float32)
+            ly = Layer(xs, 64, "square")
+            rq = timed([ly], 20, 5)
+            u = Hs * Ls
+            f_, b_ = flops_per_token_head(64, 64, 64)
+            sq.append({"L": Ls, "H": Hs, "B": 1, "d": 64, "M": 64, "C": 64, "ms_per_step": rq["ms"],
+                       "tokens_per_s": Ls / (rq["ms"] / 1e3),
+                       "roofline": roofline("bwd_walk_kernel", "bf16", u, b_, rq["bwd_walk_ms"])})
+            ly.free()
+            del ly, xs
+            torch.cuda.empty_cache()
+        out["square_paper_shapes"] = sq
+        log("square map: " + ", ".join(f"L={s['L']} H={s['H']}: {s['tokens_per_s']:.3e} tok/s" for s in sq))
+
     print(json.dumps(out), flush=True)
 
 
