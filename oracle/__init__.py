@@ -27,3 +27,11 @@ from .slim_oracle import (  # noqa: F401
     slim_forward_head,
     unpack_state,
 )
+from .dropout import (  # noqa: F401
+    dropout_backward,
+    dropout_forward,
+    keep_threshold,
+    output_scale,
+    philox4x64_10,
+    value_mask,
+)
