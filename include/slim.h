@@ -79,13 +79,29 @@ typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
  *            product runs on bf16 matrix cores with float32 accumulation and
  *            W is rounded to bf16 once; with SLIM_F32 products are float32.
  *   kind     slim_kind
- *   relu_eps additive constant of the ReLU map (the usual value is 1e-3) */
+ *   relu_eps additive constant of the ReLU map (the usual value is 1e-3)
+ *   dropout  probability p in [0, 1) of value dropout (0: none), and
+ *   seed     its seed.  With dropout (Sec. 5: each slice n has its own
+ *            seed, reused by the forward and the backward pass through it)
+ *            value element (b, h, l, e) enters the attention multiplied by
+ *            m in {0, 1}, and the output is scaled by s = 1 / (1 - p):
+ *                Y_l = s sum_{l' <= l} a_ll' (m_l' * V_l') / sum_{l' <= l} a_ll'.
+ *            m = 1 when 16-bit field e % 16 (word (e % 16) / 4, bits
+ *            16 ((e % 16) % 4) and up) of Philox4x64-10 (Salmon et al.,
+ *            SC 2011) with counter (r, e / 16, b H + h, 0) and key
+ *            (seed, n) is >= round(p 65536), where n = l / C is the slice
+ *            of row l and r = l - n C its row in the slice.  Rows are
+ *            counted from the start of the call.  state_out then holds
+ *            sum_l g(K_l) (m_l * V_l)^T (unscaled) in columns 0 .. d-1; dV
+ *            is the cotangent of V itself (masked). */
 typedef struct {
   int64_t B, H, L;
   int32_t d, M, C;
   int32_t dtype;
   int32_t kind;
   float relu_eps;
+  float dropout;
+  uint64_t seed;
 } slim_problem;
 
 /* Bytes of device workspace slim_fwd (phase SLIM_PHASE_FWD) or slim_bwd

@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <mutex>
 #include <string>
@@ -80,9 +81,28 @@ int check_problem(const slim_problem* p) {
   if (p->kind == SLIM_RELU && !(p->relu_eps > 0.f)) return fail(SLIM_EINVAL, "relu_eps must be > 0");
   if (p->kind == SLIM_SQUARE && p->M != 64)
     return fail(SLIM_EUNSUPPORTED, "the square map is built for M=64 (got M=%d)", (int)p->M);
+  if (!(p->dropout >= 0.f && p->dropout < 1.f)) return fail(SLIM_EINVAL, "dropout must be in [0, 1)");
   if (p->dtype == SLIM_F32 && (int64_t)p->d * p->M > 4096)
     return fail(SLIM_EUNSUPPORTED, "fp32 problems need d*M <= 4096 (got d=%d, M=%d)", (int)p->d, (int)p->M);
   return SLIM_OK;
+}
+
+// value dropout parameters of the kernels: keep threshold t = round(p 65536)
+// on 16-bit fields (0: nothing dropped) and the output scale 1 / (1 - p)
+struct DropPlan {
+  uint64_t seed;
+  uint32_t t;
+  float scale;
+};
+DropPlan drop_plan(const slim_problem* p) {
+  const double q = p->dropout;
+  return DropPlan{p->seed, (uint32_t)std::lround(q * 65536.0), (float)(1.0 / (1.0 - q))};
+}
+template <class A>
+void set_drop(A& a, const DropPlan& d) {
+  a.drop_seed = d.seed;
+  a.drop_t = d.t;
+  a.drop_scale = d.scale;
 }
 
 bool misaligned(const void* ptr, size_t a) { return ptr != nullptr && ((uintptr_t)ptr & (a - 1)) != 0; }
@@ -454,6 +474,7 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
   char* w = (char*)ws;
   slim::FwdArgs a;
   std::memset(&a, 0, sizeof(a));
+  set_drop(a, drop_plan(p));
   a.Q = Q;
   a.K = K;
   a.V = V;
@@ -483,6 +504,7 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
     const int BH = (int)(p->B * p->H);
     slim::KsumArgs ks;
     std::memset(&ks, 0, sizeof(ks));
+    set_drop(ks, drop_plan(p));
     ks.K = K;
     ks.V = V;
     ks.W = W;
@@ -659,6 +681,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
 
   slim::FwdArgs f;
   std::memset(&f, 0, sizeof(f));
+  set_drop(f, drop_plan(p));
   f.Q = Q;
   f.K = K;
   f.V = V;
@@ -688,6 +711,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   if (dp.ksum != nullptr) {
     slim::KsumArgs ks;
     std::memset(&ks, 0, sizeof(ks));
+    set_drop(ks, drop_plan(p));
     ks.K = K;
     ks.V = V;
     ks.W = W;
@@ -728,6 +752,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   //     cotangent except the last (dstate_out)
   slim::BwdArgs a;
   std::memset(&a, 0, sizeof(a));
+  set_drop(a, drop_plan(p));
   a.Q = Q;
   a.K = K;
   a.V = V;
@@ -775,6 +800,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (e != hipSuccess) return hip_fail(e, "cotangent-scan launch");
     slim::CarryArgs ca;
     std::memset(&ca, 0, sizeof(ca));
+    set_drop(ca, drop_plan(p));
     ca.K = K;
     ca.V = V;
     ca.Wfrag = a.Wfrag;

@@ -154,6 +154,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   constexpr int TPR = 256 / TR, EPT = D / TPR;
 
   RowStage<T, D, TR, 256> sq, sk, sv, sdy;
+  const Drop drop{a.drop_seed, a.drop_t, a.C, head};
   if (j1 > j0) {
     int st0, cn0;
     tm.tile(j1 - 1, st0, cn0);
@@ -187,6 +188,8 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
       }
     sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr, threadIdx.x);
     sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, threadIdx.x);
+    // (value dropout: dropped elements of the value rows zeroed when staged)
+    if (drop.t != 0) sv.drop(drop, start, threadIdx.x);
     sv.template store<LDQ>(Vs, nullptr, threadIdx.x);
     sdy.template store<LDQ>(dYs, nullptr, threadIdx.x);
     if (j > j0) {  // next tile's loads overlap this tile's compute
@@ -356,16 +359,18 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
       float dot = 0.f;
       const float den = red(0)[t * LDR + D] + red(1)[t * LDR + D] + red(2)[t * LDR + D] + red(3)[t * LDR + D];
       const float inv = ok ? 1.f / den : 0.f;
+      // (value dropout: Y = s N / D with the output scale s; 1 without dropout)
+      const float invs = inv * a.drop_scale;
 #pragma unroll
       for (int i = 0; i < EPT; ++i) {
         const int e = q * EPT + i;
         dy[i] = to_f32(dYs[t * LDQ + e]);
         const float n = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
-        dot += dy[i] * (n * inv);
+        dot += dy[i] * (n * invs);
       }
       dot = sum_lane_group<TPR>(dot);
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * inv);
+      for (int i = 0; i < EPT; ++i) dNs[t * LDQ + q * EPT + i] = cvt<T>(dy[i] * invs);
       if (q == 0) {
         const float dd = ok ? -dot * inv : 0.f;
         dDs[t] = dd;
@@ -415,11 +420,12 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
+        const unsigned keep = drop.t != 0 ? drop_keep_bits<EPT>(drop, start + t, q * EPT) : ~0u;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
           const float v = red(0)[t * LDR + e] + red(1)[t * LDR + e] + red(2)[t * LDR + e] + red(3)[t * LDR + e];
-          dVh[(size_t)(start + t) * D + e] = cvt<T>(v);
+          dVh[(size_t)(start + t) * D + e] = cvt<T>((keep >> i) & 1u ? v : 0.f);
         }
       }
     }

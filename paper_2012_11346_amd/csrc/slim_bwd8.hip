@@ -254,12 +254,17 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   float* nrmA = nullptr;
   float* nrmB = (G::KIND == kFavor && !sh) ? kn : nullptr;
   RowStage<T, D, TR, 256> stA, stB;
+  // value dropout: the dropped elements of the value rows are zeroed when
+  // staged (threads 256..511 stage V), and those of dV before it is stored
+  const Drop drop{a.drop_seed, a.drop_t, a.C, head};
+  const bool dropv = sh && drop.t != 0;
   __syncthreads();  // zero fill done
   if (j1 > j0) {
     int s0, n0;
     tm.tile(j1 - 1, s0, n0);
     stA.fetch(srcA + (size_t)s0 * D, n0, stid);
     stB.fetch(srcB + (size_t)s0 * D, n0, stid);
+    if (dropv) stA.drop(drop, s0, stid);
     stA.template store_swz<LDQ>(dstA, nrmA, stid);
     stB.template store_swz<LDQ>(dstB, nrmB, stid);
   }
@@ -580,6 +585,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const bool ok = t < count;
       const float den = sum_y1(t);
       const float inv = ok ? 1.f / den : 0.f;
+      // (value dropout: Y = s N / D with the output scale s; 1 without dropout)
+      const float invs = inv * a.drop_scale;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
       const fvec n = sum_y(hh, t * LDRH + col);
       float dy[EPT];
@@ -587,12 +594,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 #pragma unroll
       for (int i = 0; i < EPT; ++i) {
         dy[i] = to_f32(dYs[swz_off<LDQ, kSwzRows>(t, e) + i]);
-        dot += dy[i] * (n[i] * inv);
+        dot += dy[i] * (n[i] * invs);
       }
       dot = sum_lane_group<TPR>(dot);
       u32e dn;
 #pragma unroll
-      for (int i = 0; i < EPT / 2; ++i) dn[i] = __builtin_bit_cast(unsigned, pk_bf16(dy[2 * i] * inv, dy[2 * i + 1] * inv));
+      for (int i = 0; i < EPT / 2; ++i) dn[i] = __builtin_bit_cast(unsigned, pk_bf16(dy[2 * i] * invs, dy[2 * i + 1] * invs));
       *(u32e*)&dNs[swz_off<LDQ, kSwzRows>(t, e)] = dn;
       if (q == 0) {
         const float dd = ok ? -dot * inv : 0.f;
@@ -663,7 +670,13 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
-      dv_hold = cvt_row(sum_y(hh, t * LDRH + col));
+      fvec dvs = sum_y(hh, t * LDRH + col);
+      if (drop.t != 0) {
+        const unsigned keep = drop_keep_bits<EPT>(drop, start + t, e);
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) dvs[i] = (keep >> i) & 1u ? dvs[i] : 0.f;
+      }
+      dv_hold = cvt_row(dvs);
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -1017,6 +1030,11 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     }
     if (j > j0) {
       const int st2 = fresh_tid() & 255;
+      if (dropv) {
+        int sn, cn;
+        tm.tile(j - 1, sn, cn);
+        stA.drop(drop, sn, st2);
+      }
       stA.template store_swz<LDQ>(dstA, nrmA, st2);
       stB.template store_swz<LDQ>(dstB, nrmB, st2);
     }

@@ -159,11 +159,15 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
       pdk[i] = IO::template load<t4>(rdK, out_off(L, r, i));
     }
   };
+  // value dropout: dropped value elements zeroed when staged, and their dV
+  // contributions dropped
+  const Drop drop{a.drop_seed, a.drop_t, a.C, head};
   if (row1 > row0) fetch_block(0);
   for (int start = row0; start < row1; start += TR) {
     const int count = min(TR, row1 - start);
     const int rel = start - row0;
     sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, fresh_tid());
+    if (drop.t != 0) sv.drop(drop, start, fresh_tid());
     sv.template store<LDQ>(Vs, nullptr, fresh_tid());
     t4 cdv[NO], cdk[NO];
 #pragma unroll
@@ -244,9 +248,10 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) acc = mma(acc, frag_tr(L, Gs, LDG, 32 * kb, 16 * eo), frag_rm(L, Kt, LDK, 16 * st, 32 * kb));
         {
+          const unsigned keep = drop.t != 0 ? drop_keep_bits<4>(drop, start + 16 * st + L.c, 16 * eo + 4 * L.g) : ~0u;
           t4 o;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) o[r] = cvt<T>(to_f32(cdv[i][r]) + acc[r]);
+          for (int r = 0; r < 4; ++r) o[r] = cvt<T>(to_f32(cdv[i][r]) + ((keep >> r) & 1u ? acc[r] : 0.f));
           IO::store(o, rdV, out_off(L, rel, i));
         }
         // dk^T[e][s] = sum_m W[m][e] Pk[s][m] - k[s][e] rowsum(Pk[s])

@@ -198,7 +198,11 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
   const int s_loff = srow * LDQ + 8 * (scc ^ ((srow >> 3) & 1));  // kSwzRows: chunk cc of row r at cc ^ sw(r) / 2
   uint4 stage;
   auto fetch_rows = [&](const ChunkPos& c) { stage = BufIO<16>::load<uint4>(c.rsrc(stage_k ? a.K : a.V), s_goff); };
-  auto put_rows = [&](int buf) {
+  // value dropout: dropped value elements zeroed when staged (the chunk's
+  // head and first row give their positions), their dV contributions dropped
+  auto drop_of = [&](const ChunkPos& c) { return Drop{a.drop_seed, a.drop_t, a.C, (uint64_t)c.head}; };
+  auto put_rows = [&](int buf, const ChunkPos& c) {
+    if (stage_v && a.drop_t != 0) drop_chunk<T>(stage, drop_of(c), c.a0 + c.k * CR + srow, scc * 8);
     if (stage_k) {
       *(uint4*)(Kb + buf * TQ + s_loff) = stage;
       if (G::KIND == kFavor) {
@@ -270,7 +274,7 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
     advance(c2, n_run > 2);
     t4 pd[NJ];  // prior dV / dK entries of the current chunk's output tiles
     fetch_rows(cur);
-    put_rows(0);
+    put_rows(0, cur);
     fetch_rows(c1);
 #pragma unroll
     for (int jj = 0; jj < NJ; ++jj) pd[jj] = IO::template load<t4>(cur.rsrc(job_tensor(jj)), out_off);
@@ -293,7 +297,7 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
         for (int kb = 0; kb < EB; ++kb) Wl[mt][kb] = wfrag(WL::alo(w >> 1, (w & 1) * MT + mt, kb));
       // rows of chunk it + 1 into their buffer, rows of chunk it + 2 into
       // registers
-      put_rows(b1);
+      put_rows(b1, c1);
       fetch_rows(c2);
       if (cur.head != g_head || cur.p != g_p) {
         load_g(cur);
@@ -439,6 +443,11 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
         // the same registers receive those of the next chunk
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
+          if (!job_is_dk(jj) && a.drop_t != 0) {
+            const unsigned keep = drop_keep_bits<4>(drop_of(cur), cur.a0 + cur.k * CR + 16 * so + L.c, 16 * eo + 4 * L.g);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[jj][r] = (keep >> r) & 1u ? acc[jj][r] : 0.f;
+          }
           t4 o;
 #pragma unroll
           for (int r = 0; r < 4; ++r) o[r] = (T)((float)pd[jj][r] + acc[jj][r]);

@@ -140,6 +140,77 @@ __device__ __forceinline__ void load_rows(T* dst, const T* src, int count, float
 
 constexpr size_t al16(size_t n) { return (n + 15) & ~(size_t)15; }
 
+// ---------------------------------------------------------------------------
+// Value dropout with per-slice seeds (Sec. 5): element (b, h, l, e) of V is
+// kept when 16-bit field e % 16 of Philox4x64-10 (counter (r, e / 16,
+// b H + h, 0), key (seed, n); n = l / C the slice of row l, r = l - n C) is
+// >= t; the output is scaled by 1 / (1 - p) elsewhere.  t = 0: no dropout.
+struct Drop {
+  uint64_t seed;
+  uint32_t t;
+  int C;
+  uint64_t head;  // b H + h
+};
+
+// Philox4x64-10 (Salmon et al., SC 2011): ten rounds of two 64 x 64 -> 128
+// bit products, the key bumped by the Weyl constants between rounds
+__device__ __forceinline__ void philox4x64_10(uint64_t (&c)[4], uint64_t k0, uint64_t k1) {
+  constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const uint64_t hi0 = __umul64hi(M0, c[0]), lo0 = M0 * c[0];
+    const uint64_t hi1 = __umul64hi(M1, c[2]), lo1 = M1 * c[2];
+    const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+    k0 += W0;
+    k1 += W1;
+  }
+}
+
+// keep bits of the N consecutive elements e0 .. e0 + N - 1 of row l (N = 2,
+// 4 or 8, e0 a multiple of N): bit i set when element e0 + i is kept.  Not
+// inlined: the callers reach it only with dropout on, and its temporaries
+// then do not add to their register budget on the common path.
+template <int N>
+__device__ __attribute__((noinline)) unsigned drop_keep_bits(const Drop& dp, int l, int e0) {
+  const int n = l / dp.C;
+  uint64_t c[4] = {(uint64_t)(l - n * dp.C), (uint64_t)(e0 >> 4), dp.head, 0ull};
+  philox4x64_10(c, dp.seed, (uint64_t)n);
+  unsigned bits = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int j = (e0 & 15) + i;
+    // (word j / 4 of the four outputs, selected with constant indices)
+    const uint64_t wj = (j >> 2) == 0 ? c[0] : (j >> 2) == 1 ? c[1] : (j >> 2) == 2 ? c[2] : c[3];
+    const unsigned f = (unsigned)(wj >> (16 * (j & 3))) & 0xFFFFu;
+    bits |= (f >= dp.t ? 1u : 0u) << i;
+  }
+  return bits;
+}
+
+// zero the dropped elements of a 16-byte row chunk (8 bf16 or 4 floats)
+// holding row l, columns e0 .. e0 + 16 / sizeof(T) - 1
+template <typename T>
+__device__ __forceinline__ void drop_chunk(uint4& v, const Drop& dp, int l, int e0) {
+  constexpr int N = 16 / sizeof(T);
+  const unsigned bits = drop_keep_bits<N>(dp, l, e0);
+  unsigned w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if constexpr (N == 8) {
+      const unsigned m = ((bits >> (2 * q)) & 1u ? 0x0000FFFFu : 0u) | ((bits >> (2 * q + 1)) & 1u ? 0xFFFF0000u : 0u);
+      w[q] &= m;
+    } else {
+      w[q] = (bits >> q) & 1u ? w[q] : 0u;
+    }
+  }
+  v = uint4{w[0], w[1], w[2], w[3]};
+}
+
 // Raw buffer resource over [base, base + bytes): the hardware's range check
 // makes loads past the end read zero and drops stores past the end, so
 // accesses to a ragged last row block need no branch (and the compiler can
@@ -199,6 +270,16 @@ struct RowStage {
       // chunks past the block get an offset beyond any range
       const int off = ch < NCH ? ((row0 + r) * D + cc * VEC) * (int)sizeof(T) : INT_MAX - 15;
       v[i] = BufIO<16>::load<uint4>(rs, off);
+    }
+  }
+  // value dropout of the staged rows: row r of the block is row l0 + r of
+  // the head (rows past the block are zero already)
+  __device__ __forceinline__ void drop(const Drop& dp, int l0, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int ch = tid + i * NT;
+      const int r = ch / CPR, cc = ch - (ch / CPR) * CPR;
+      if (ch < NCH) drop_chunk<T>(v[i], dp, l0 + r, cc * VEC);
     }
   }
   // into a row tile swizzled as kSwzRows (pitch LD): chunk cc of row r goes

@@ -204,15 +204,22 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   auto store_q = [&](int bf) {
     if constexpr (QSIDE) sq.template store<LDQ>(Qbuf, nullptr, fresh_tid());
   };
-  auto store_kv = [&](int bf) {
+  const Drop drop{a.drop_seed, a.drop_t, a.C, head};
+  // value rows of tile jj, dropped elements zeroed (value dropout)
+  auto store_kv = [&](int bf, int jj) {
     const int tid = fresh_tid();
+    if (drop.t != 0) {
+      int s0, n0;
+      tm.tile(jj, s0, n0);
+      sv.drop(drop, s0, tid);
+    }
     sk.template store<LDQ>(Kbuf + bf * TQ, G::KIND == kFavor ? knb[bf] : nullptr, tid);
     sv.template store<LDQ>(Vbuf + bf * TQ, nullptr, tid);
   };
   if (j1 > j0) {
     fetch(j0);
     store_q(0);
-    store_kv(0);
+    store_kv(0, j0);
     fetch(j0 + 1);
   }
   __syncthreads();
@@ -223,7 +230,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     const int bf = (j - j0) & 1;
     Lane L = fresh_lane();
     int g = L.g, c = L.c;
-    if (j + 1 < j1) store_kv(bf ^ 1);
+    if (j + 1 < j1) store_kv(bf ^ 1, j + 1);
     const T* Qs = Qbuf;
     const T* Ks = Kbuf + bf * TQ;
     const T* Vs = Vbuf + bf * TQ;
@@ -471,7 +478,8 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
       // stores: no branch, so later waits count exactly)
       const int tid = fresh_tid();
       const int t = tid / TPR, q = tid % TPR;
-      const float inv = 1.f / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
+      // (value dropout: the output scale 1 / (1 - p) folded in)
+      const float inv = a.drop_scale / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
       typedef T tvec __attribute__((ext_vector_type(EPT)));
       tvec o;
 #pragma unroll

@@ -31,6 +31,10 @@ struct FwdArgs {
   float* seg_shift_out;     // kWalkSums: [B,H,P]
   int B, H, L, C, P;
   float relu_eps;
+  // value dropout (Drop): seed, keep threshold t (0: none), output scale 1 / (1 - p)
+  uint64_t drop_seed;
+  uint32_t drop_t;
+  float drop_scale;
 };
 
 struct ScanArgs {
@@ -80,6 +84,10 @@ struct BwdArgs {
   float* dW;                // [M,D] sum of the partials
   int B, H, L, C, P;
   float relu_eps;
+  // value dropout (Drop): seed, keep threshold t (0: none), output scale 1 / (1 - p)
+  uint64_t drop_seed;
+  uint32_t drop_t;
+  float drop_scale;
 };
 
 // Carried cotangent: adds the contribution of G_end(p) (the cotangent after
@@ -98,6 +106,10 @@ struct CarryArgs {
   int nch_head;  // 32-row chunks per head over segments 0 .. P-2 (carry8_kernel)
   int NWG;       // workgroups (carry8_kernel); dW_part slot B H P + i is workgroup i's
   float relu_eps;
+  // value dropout (Drop): seed, keep threshold t (0: none), output scale 1 / (1 - p)
+  uint64_t drop_seed;
+  uint32_t drop_t;
+  float drop_scale;
 };
 
 // Key sums of contiguous parts of each head (ksum_kernel): per part, the
@@ -112,6 +124,10 @@ struct KsumArgs {
   float* out;          // kSumStates: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
   int B, H, L, C, P2;
   float relu_eps;
+  // value dropout (Drop): seed, keep threshold t (0: none), output scale 1 / (1 - p)
+  uint64_t drop_seed;
+  uint32_t drop_t;
+  float drop_scale;
 };
 
 template <class G>

@@ -107,10 +107,15 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   RowStage<T, D, CR, 256> sk, sv;
   const int tid = threadIdx.x;
   float* const knorm = G::KIND == kFavor ? knb[0] : nullptr;
+  // value dropout: dropped elements of the value rows are zeroed when staged
+  const Drop drop{a.drop_seed, a.drop_t, a.C, head};
   sk.fetch(rK, 0, tid);
   if constexpr (SUMS) sv.fetch(rV, 0, tid);
   sk.template store_swz<LDQ>(Kb, knorm, tid);
-  if constexpr (SUMS) sv.template store_swz<LDQ>(Vb, nullptr, tid);
+  if constexpr (SUMS) {
+    if (drop.t != 0) sv.drop(drop, r0, tid);
+    sv.template store_swz<LDQ>(Vb, nullptr, tid);
+  }
   sk.fetch(rK, CR, tid);
   if constexpr (SUMS) sv.fetch(rV, CR, tid);
   __syncthreads();
@@ -123,7 +128,10 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
     {
       const int t2 = fresh_tid();
       sk.template store_swz<LDQ>(Kb + (bf ^ 1) * TQ, G::KIND == kFavor ? knb[bf ^ 1] : nullptr, t2);
-      if constexpr (SUMS) sv.template store_swz<LDQ>(Vb + (bf ^ 1) * TQ, nullptr, t2);
+      if constexpr (SUMS) {
+        if (drop.t != 0) sv.drop(drop, r0 + (ci + 1) * CR, t2);
+        sv.template store_swz<LDQ>(Vb + (bf ^ 1) * TQ, nullptr, t2);
+      }
       sk.fetch(rK, (ci + 2) * CR, t2);
       if constexpr (SUMS) sv.fetch(rV, (ci + 2) * CR, t2);
     }

@@ -43,6 +43,8 @@ class Problem(ctypes.Structure):
         ("dtype", ctypes.c_int32),
         ("kind", ctypes.c_int32),
         ("relu_eps", ctypes.c_float),
+        ("dropout", ctypes.c_float),
+        ("seed", ctypes.c_uint64),
     ]
 
 
@@ -102,12 +104,13 @@ def _check(status: int):
         raise SlimError(status, LIB.slim_last_error().decode())
 
 
-def problem(B, H, L, d, M, C, dtype=BF16, kind=FAVOR_PLUS, relu_eps=1e-3) -> Problem:
+def problem(B, H, L, d, M, C, dtype=BF16, kind=FAVOR_PLUS, relu_eps=1e-3, dropout=0.0, seed=0) -> Problem:
     if isinstance(dtype, torch.dtype):
         dtype = DTYPES[dtype]
     if isinstance(kind, str):
         kind = KINDS[kind]
-    return Problem(int(B), int(H), int(L), int(d), int(M), int(C), int(dtype), int(kind), float(relu_eps))
+    return Problem(int(B), int(H), int(L), int(d), int(M), int(C), int(dtype), int(kind), float(relu_eps),
+                   float(dropout), int(seed) & ((1 << 64) - 1))
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -118,11 +121,11 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def _problem_of(Q: torch.Tensor, W: torch.Tensor, C: int, kind, relu_eps: float) -> Problem:
+def _problem_of(Q: torch.Tensor, W: torch.Tensor, C: int, kind, relu_eps: float, dropout=0.0, seed=0) -> Problem:
     if Q.dim() != 4:
         raise ValueError("Q must be [B, H, L, d]")
     B, H, L, d = Q.shape
-    return problem(B, H, L, d, W.shape[0], C, DTYPES[Q.dtype], kind, relu_eps)
+    return problem(B, H, L, d, W.shape[0], C, DTYPES[Q.dtype], kind, relu_eps, dropout, seed)
 
 
 def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
@@ -208,10 +211,11 @@ def _need_ctx(p: Problem, ctx: Optional[torch.Tensor]):
 
 
 def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3, ws=None,
-        Y=None, state_out=None, kshift_out=None, ctx=None):
+        Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0):
     """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None).
-    ctx (optional, from new_context) receives the segment boundary states for bwd."""
-    p = _problem_of(Q, W, C, kind, relu_eps)
+    ctx (optional, from new_context) receives the segment boundary states for bwd.
+    dropout / seed: value dropout with per-slice seeds (include/slim.h)."""
+    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V)):
         _need(t, n, Q.dtype, shp)
@@ -239,12 +243,12 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
 
 def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshift_in=None, dstate_out=None,
         want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None,
-        ctx=None):
+        ctx=None, dropout: float = 0.0, seed: int = 0):
     """Backward sweep; kshift is the forward's kshift_out (FAVOR+); ctx (optional)
     is the context the forward wrote for the same inputs.
 
     Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
-    p = _problem_of(Q, W, C, kind, relu_eps)
+    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V), ("dY", dY)):
         _need(t, n, Q.dtype, shp)
@@ -274,11 +278,11 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
 
 
 def fwd_noalloc(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3,
-                Y=None, state_out=None, kshift_out=None, ctx=None):
+                Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0):
     """fwd through slim_fwd_noalloc: the library's static device scratch
     replaces the workspace (outputs not passed in are allocated here, by
     torch, before the call; the call itself allocates nothing)."""
-    p = _problem_of(Q, W, C, kind, relu_eps)
+    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V)):
         _need(t, n, Q.dtype, shp)

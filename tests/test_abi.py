@@ -148,6 +148,15 @@ def test_square_map_needs_64_features(S):
     assert S.LIB.slim_workspace_bytes(ctypes.byref(_p(S, M=64, kind=S.SQUARE)), S.PHASE_BWD) > 0
 
 
+def test_dropout_probability_is_checked(S):
+    import ctypes
+
+    for p in (-0.1, 1.0, float("nan")):
+        assert S.LIB.slim_workspace_bytes(ctypes.byref(_p(S, dropout=p)), S.PHASE_FWD) == 0
+        assert "dropout" in S.LIB.slim_last_error().decode()
+    assert S.LIB.slim_workspace_bytes(ctypes.byref(_p(S, dropout=0.5, seed=2 ** 64 - 1)), S.PHASE_FWD) > 0
+
+
 def test_relu_needs_positive_eps(S):
     p = _p(S, kind=S.RELU)
     p.relu_eps = 0.0
