@@ -55,7 +55,8 @@ struct BwdLds {
   static constexpr size_t TOTAL = oW + 4 * WAVE;
 };
 
-template <class G>
+// DROP: value dropout on (its masks are generated only in that instantiation)
+template <class G, bool DROP>
 __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -189,7 +190,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     sq.template store<LDQ>(Qs, G::KIND == kFavor ? qn : nullptr, threadIdx.x);
     sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, threadIdx.x);
     // (value dropout: dropped elements of the value rows zeroed when staged)
-    if (drop.t != 0) sv.drop(drop, start, threadIdx.x);
+    if (DROP) sv.drop(drop, start, threadIdx.x);
     sv.template store<LDQ>(Vs, nullptr, threadIdx.x);
     sdy.template store<LDQ>(dYs, nullptr, threadIdx.x);
     if (j > j0) {  // next tile's loads overlap this tile's compute
@@ -420,7 +421,7 @@ __global__ __launch_bounds__(256, 1) void bwd_walk_kernel(BwdArgs a) {
     {
       const int t = threadIdx.x / TPR, q = threadIdx.x % TPR;
       if (t < count) {
-        const unsigned keep = drop.t != 0 ? drop_keep_bits<EPT>(drop, start + t, q * EPT) : ~0u;
+        const unsigned keep = DROP ? drop_keep_bits<EPT>(drop, start + t, q * EPT) : ~0u;
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
           const int e = q * EPT + i;
@@ -669,7 +670,8 @@ __global__ __launch_bounds__(1024) void dw_reduce_kernel(const float* part, int 
 
 template <class G>
 hipError_t launch_bwd_walk(const BwdArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(bwd_walk_kernel<G>, dim3(a.P, a.H, a.B), dim3(256), 0, s, a);
+  if (a.drop_t != 0) hipLaunchKernelGGL((bwd_walk_kernel<G, true>), dim3(a.P, a.H, a.B), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((bwd_walk_kernel<G, false>), dim3(a.P, a.H, a.B), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

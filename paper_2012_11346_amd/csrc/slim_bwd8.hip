@@ -78,7 +78,8 @@ struct Bwd8Lds {
   static_assert(TOTAL <= 160 * 1024, "LDS budget of one workgroup");
 };
 
-template <class G>
+// DROP: value dropout on (its masks are generated only in that instantiation)
+template <class G, bool DROP>
 __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -257,7 +258,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   // value dropout: the dropped elements of the value rows are zeroed when
   // staged (threads 256..511 stage V), and those of dV before it is stored
   const Drop drop{a.drop_seed, a.drop_t, a.C, head};
-  const bool dropv = sh && drop.t != 0;
+  const bool dropv = DROP && sh;
   __syncthreads();  // zero fill done
   if (j1 > j0) {
     int s0, n0;
@@ -671,7 +672,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       const int t = red_row(tid), q = tid % TPR;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
       fvec dvs = sum_y(hh, t * LDRH + col);
-      if (drop.t != 0) {
+      if (DROP) {
         const unsigned keep = drop_keep_bits<EPT>(drop, start + t, e);
 #pragma unroll
         for (int i = 0; i < EPT; ++i) dvs[i] = (keep >> i) & 1u ? dvs[i] : 0.f;
@@ -1080,7 +1081,8 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
 template <class G>
 hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(bwd_walk8_kernel<G>, dim3(a.P, a.H, a.B), dim3(512), 0, s, a);
+  if (a.drop_t != 0) hipLaunchKernelGGL((bwd_walk8_kernel<G, true>), dim3(a.P, a.H, a.B), dim3(512), 0, s, a);
+  else hipLaunchKernelGGL((bwd_walk8_kernel<G, false>), dim3(a.P, a.H, a.B), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

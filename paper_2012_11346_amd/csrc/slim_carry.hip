@@ -24,7 +24,8 @@
 
 namespace slim {
 
-template <class G>
+// DROP: value dropout on (its masks are generated only in that instantiation)
+template <class G, bool DROP>
 __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
     const int count = min(TR, row1 - start);
     const int rel = start - row0;
     sk.template store<LDQ>(Ks, G::KIND == kFavor ? kn : nullptr, fresh_tid());
-    if (drop.t != 0) sv.drop(drop, start, fresh_tid());
+    if (DROP) sv.drop(drop, start, fresh_tid());
     sv.template store<LDQ>(Vs, nullptr, fresh_tid());
     t4 cdv[NO], cdk[NO];
 #pragma unroll
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) acc = mma(acc, frag_tr(L, Gs, LDG, 32 * kb, 16 * eo), frag_rm(L, Kt, LDK, 16 * st, 32 * kb));
         {
-          const unsigned keep = drop.t != 0 ? drop_keep_bits<4>(drop, start + 16 * st + L.c, 16 * eo + 4 * L.g) : ~0u;
+          const unsigned keep = DROP ? drop_keep_bits<4>(drop, start + 16 * st + L.c, 16 * eo + 4 * L.g) : ~0u;
           t4 o;
 #pragma unroll
           for (int r = 0; r < 4; ++r) o[r] = cvt<T>(to_f32(cdv[i][r]) + ((keep >> r) & 1u ? acc[r] : 0.f));
@@ -310,7 +311,9 @@ __global__ __launch_bounds__(256, 2) void carry_kernel(CarryArgs a) {
 template <class G>
 hipError_t launch_carry(const CarryArgs& a, hipStream_t s) {
   if (a.P < 2) return hipSuccess;
-  hipLaunchKernelGGL(carry_kernel<G>, dim3((a.P - 1) * a.CS, a.H, a.B), dim3(256), 0, s, a);
+  const dim3 grid((a.P - 1) * a.CS, a.H, a.B);
+  if (a.drop_t != 0) hipLaunchKernelGGL((carry_kernel<G, true>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((carry_kernel<G, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

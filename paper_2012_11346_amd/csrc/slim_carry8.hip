@@ -95,7 +95,8 @@ int carry8_chunks_per_head(int L, int C, int P) {
   return n;
 }
 
-template <class G>
+// DROP: value dropout on (its masks are generated only in that instantiation)
+template <class G, bool DROP>
 __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
   typedef bf16 T;
   typedef bf16x8 F;
@@ -202,7 +203,7 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
   // head and first row give their positions), their dV contributions dropped
   auto drop_of = [&](const ChunkPos& c) { return Drop{a.drop_seed, a.drop_t, a.C, (uint64_t)c.head}; };
   auto put_rows = [&](int buf, const ChunkPos& c) {
-    if (stage_v && a.drop_t != 0) drop_chunk<T>(stage, drop_of(c), c.a0 + c.k * CR + srow, scc * 8);
+    if (DROP && stage_v) drop_chunk<T>(stage, drop_of(c), c.a0 + c.k * CR + srow, scc * 8);
     if (stage_k) {
       *(uint4*)(Kb + buf * TQ + s_loff) = stage;
       if (G::KIND == kFavor) {
@@ -286,15 +287,19 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
     __syncthreads();
 
     int b0 = 0, b1 = 1, z = 0;  // row buffer of this chunk and of the next; K~/Pk buffer
-    for (int it = 0; it < n_run; ++it) {
-      // low parts of the logits' W fragments (bf16 split of the float32 W),
-      // read from the table at every chunk ahead of the row prefetch, so that
-      // waiting for them does not wait for the rows
-      F Wl[MT][EB];
+    // low parts of the logits' W fragments (bf16 split of the float32 W),
+    // read from the table for every chunk at the end of the one before,
+    // ahead of that chunk's output stores and of the next chunk's loads, so
+    // that waiting for them waits for nothing else
+    F Wl[MT][EB];
+    auto fetch_wl = [&]() {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int kb = 0; kb < EB; ++kb) Wl[mt][kb] = wfrag(WL::alo(w >> 1, (w & 1) * MT + mt, kb));
+    };
+    fetch_wl();
+    for (int it = 0; it < n_run; ++it) {
       // rows of chunk it + 1 into their buffer, rows of chunk it + 2 into
       // registers
       put_rows(b1, c1);
@@ -441,9 +446,10 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
         }
         // plus the prior outputs of this chunk (loaded a chunk ago); then
         // the same registers receive those of the next chunk
+        fetch_wl();
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
-          if (!job_is_dk(jj) && a.drop_t != 0) {
+          if (DROP && !job_is_dk(jj)) {
             const unsigned keep = drop_keep_bits<4>(drop_of(cur), cur.a0 + cur.k * CR + 16 * so + L.c, 16 * eo + 4 * L.g);
 #pragma unroll
             for (int r = 0; r < 4; ++r) acc[jj][r] = (keep >> r) & 1u ? acc[jj][r] : 0.f;
@@ -478,7 +484,8 @@ __global__ __launch_bounds__(512, 1) void carry8_kernel(CarryArgs a) {
 template <class G>
 hipError_t launch_carry8(const CarryArgs& a, hipStream_t s) {
   if (a.P < 2 || a.NWG < 1) return hipSuccess;
-  hipLaunchKernelGGL(carry8_kernel<G>, dim3(a.NWG), dim3(512), 0, s, a);
+  if (a.drop_t != 0) hipLaunchKernelGGL((carry8_kernel<G, true>), dim3(a.NWG), dim3(512), 0, s, a);
+  else hipLaunchKernelGGL((carry8_kernel<G, false>), dim3(a.NWG), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

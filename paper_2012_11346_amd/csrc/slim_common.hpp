@@ -172,11 +172,9 @@ __device__ __forceinline__ void philox4x64_10(uint64_t (&c)[4], uint64_t k0, uin
 }
 
 // keep bits of the N consecutive elements e0 .. e0 + N - 1 of row l (N = 2,
-// 4 or 8, e0 a multiple of N): bit i set when element e0 + i is kept.  Not
-// inlined: the callers reach it only with dropout on, and its temporaries
-// then do not add to their register budget on the common path.
+// 4 or 8, e0 a multiple of N): bit i set when element e0 + i is kept
 template <int N>
-__device__ __attribute__((noinline)) unsigned drop_keep_bits(const Drop& dp, int l, int e0) {
+__device__ __forceinline__ unsigned drop_keep_bits(const Drop& dp, int l, int e0) {
   const int n = l / dp.C;
   uint64_t c[4] = {(uint64_t)(l - n * dp.C), (uint64_t)(e0 >> 4), dp.head, 0ull};
   philox4x64_10(c, dp.seed, (uint64_t)n);

@@ -107,8 +107,9 @@ __device__ __forceinline__ void key_logits(const Lane& L, f32x4 (&Lk)[G::RT][G::
 
 // MODE kWalkOutputs: Y and the final state; kWalkSums: only the keys, the
 // state each segment adds.
-template <class G, int MODE>
-// (two workgroups per compute unit)
+// (two workgroups per compute unit; DROP: value dropout on, its masks are
+// generated only in that instantiation)
+template <class G, int MODE, bool DROP>
 __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -208,7 +209,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   // value rows of tile jj, dropped elements zeroed (value dropout)
   auto store_kv = [&](int bf, int jj) {
     const int tid = fresh_tid();
-    if (drop.t != 0) {
+    if (DROP) {
       int s0, n0;
       tm.tile(jj, s0, n0);
       sv.drop(drop, s0, tid);
@@ -223,6 +224,23 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
     fetch(j0 + 1);
   }
   __syncthreads();
+
+  // Y of a tile: EPT consecutive entries of one row per thread, stored as
+  // PB-byte pieces at the end of the tile
+  typedef T tvec __attribute__((ext_vector_type(EPT)));
+  constexpr int PB = sizeof(tvec) >= 16 ? 16 : (int)sizeof(tvec);  // bytes per store (8 or 16)
+  constexpr int NV = (int)(sizeof(tvec) / PB);
+  static_assert(sizeof(tvec) % PB == 0 && (PB == 8 || PB == 16), "8- or 16-byte pieces");
+  typedef unsigned pvec __attribute__((ext_vector_type(PB / 4)));
+  pvec y_hold[NV] = {};
+  __amdgpu_buffer_rsrc_t y_rs = range_rsrc(a.Y, 0);  // empty until the first tile's Y
+  int y_off = 0;
+  auto flush_y = [&]() {
+    if constexpr (QSIDE) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) BufIO<PB>::store(y_hold[v], y_rs, y_off + PB * v);
+    }
+  };
 
   for (int j = j0; j < j1; ++j) {
     int start, count;
@@ -480,7 +498,6 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
       const int t = tid / TPR, q = tid % TPR;
       // (value dropout: the output scale 1 / (1 - p) folded in)
       const float inv = a.drop_scale / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
-      typedef T tvec __attribute__((ext_vector_type(EPT)));
       tvec o;
 #pragma unroll
       for (int h4 = 0; h4 < EPT / 4; ++h4) {
@@ -498,15 +515,12 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
           for (int i = 0; i < 4; ++i) o[4 * h4 + i] = cvt<T>(n[i] * inv);
         }
       }
-      const __amdgpu_buffer_rsrc_t ry =
-          range_rsrc((T*)a.Y + head * (size_t)a.L * D + (size_t)start * D, (size_t)count * D * sizeof(T));
-      constexpr int PB = sizeof(tvec) >= 16 ? 16 : (int)sizeof(tvec);  // bytes per store (8 or 16)
-      constexpr int NV = (int)(sizeof(tvec) / PB);
-      static_assert(sizeof(tvec) % PB == 0 && (PB == 8 || PB == 16), "8- or 16-byte pieces");
-      typedef unsigned pvec __attribute__((ext_vector_type(PB / 4)));
+      y_rs = range_rsrc((T*)a.Y + head * (size_t)a.L * D + (size_t)start * D, (size_t)count * D * sizeof(T));
+      y_off = (t * D + q * EPT) * (int)sizeof(T);
       const pvec* ov = (const pvec*)&o;
 #pragma unroll
-      for (int v = 0; v < NV; ++v) BufIO<PB>::store(ov[v], ry, ((t * D + q * EPT) * (int)sizeof(T)) + PB * v);
+      for (int v = 0; v < NV; ++v) y_hold[v] = ov[v];
+      flush_y();
     }
   }
 
@@ -706,10 +720,13 @@ hipError_t launch_wfrag(const WfragArgs& a, hipStream_t s) {
 template <class G>
 hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s) {
   const dim3 grid(a.P, a.H, a.B);
+  const bool drop = a.drop_t != 0;
   if (mode == kWalkOutputs) {
-    hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkOutputs>), grid, dim3(256), 0, s, a);
+    if (drop) hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkOutputs, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkOutputs, false>), grid, dim3(256), 0, s, a);
   } else if (mode == kWalkSums) {
-    hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkSums>), grid, dim3(256), 0, s, a);
+    if (drop) hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkSums, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((fwd_walk_kernel<G, kWalkSums, false>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

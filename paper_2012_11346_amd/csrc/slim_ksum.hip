@@ -25,7 +25,8 @@
 
 namespace slim {
 
-template <class G, int MODE>
+// DROP: value dropout on (its masks are generated only in that instantiation)
+template <class G, int MODE, bool DROP>
 __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   if constexpr (SUMS) sv.fetch(rV, 0, tid);
   sk.template store_swz<LDQ>(Kb, knorm, tid);
   if constexpr (SUMS) {
-    if (drop.t != 0) sv.drop(drop, r0, tid);
+    if (DROP) sv.drop(drop, r0, tid);
     sv.template store_swz<LDQ>(Vb, nullptr, tid);
   }
   sk.fetch(rK, CR, tid);
@@ -129,7 +130,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
       const int t2 = fresh_tid();
       sk.template store_swz<LDQ>(Kb + (bf ^ 1) * TQ, G::KIND == kFavor ? knb[bf ^ 1] : nullptr, t2);
       if constexpr (SUMS) {
-        if (drop.t != 0) sv.drop(drop, r0 + (ci + 1) * CR, t2);
+        if (DROP) sv.drop(drop, r0 + (ci + 1) * CR, t2);
         sv.template store_swz<LDQ>(Vb + (bf ^ 1) * TQ, nullptr, t2);
       }
       sk.fetch(rK, (ci + 2) * CR, t2);
@@ -294,8 +295,12 @@ __global__ void kshift_reduce_kernel(const float* part_max, int P2, const float*
 template <class G>
 hipError_t launch_ksum(const KsumArgs& a, int mode, hipStream_t s) {
   const dim3 grid(a.P2, a.H, a.B);
-  if (mode == kSumStates) hipLaunchKernelGGL((ksum_kernel<G, kSumStates>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((ksum_kernel<G, kSumMax>), grid, dim3(256), 0, s, a);
+  if (mode == kSumStates) {
+    if (a.drop_t != 0) hipLaunchKernelGGL((ksum_kernel<G, kSumStates, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((ksum_kernel<G, kSumStates, false>), grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((ksum_kernel<G, kSumMax, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
