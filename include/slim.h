@@ -67,6 +67,17 @@ typedef enum { SLIM_FAVOR_PLUS = 0, SLIM_RELU = 1, SLIM_SQUARE = 2 } slim_kind;
 typedef enum { SLIM_F32 = 0, SLIM_BF16 = 1 } slim_dtype;
 typedef enum { SLIM_QUERY = 0, SLIM_KEY = 1 } slim_role;
 typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
+/* How the prefix sums inside a slice are evaluated (Sec. 3.2, Appendix B):
+ *   SLIM_WITHIN_ITER       block-iteratively, the state carried from one
+ *                          32-row tile to the next (the tiles of a slice never
+ *                          leave the chip; the work per row does not depend
+ *                          on C)
+ *   SLIM_WITHIN_QUADRATIC  the slice as one masked quadratic form (eq. 2
+ *                          inside the slice), slices one after another and the
+ *                          32-row tiles of a slice in parallel: the work per
+ *                          row grows with C (bf16 problems with M of 128 or
+ *                          256, FAVOR+ or ReLU) */
+typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1 } slim_within;
 
 /* Problem description shared by all entry points.
  *   B, H, L  batch, heads, sequence length (each >= 1; B H <= 65535 and one
@@ -93,7 +104,9 @@ typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
  *            of row l and r = l - n C its row in the slice.  Rows are
  *            counted from the start of the call.  state_out then holds
  *            sum_l g(K_l) (m_l * V_l)^T (unscaled) in columns 0 .. d-1; dV
- *            is the cotangent of V itself (masked). */
+ *            is the cotangent of V itself (masked).
+ *   within   slim_within: how the slice is evaluated (results agree up to
+ *            rounding). */
 typedef struct {
   int64_t B, H, L;
   int32_t d, M, C;
@@ -102,6 +115,8 @@ typedef struct {
   float relu_eps;
   float dropout;
   uint64_t seed;
+  int32_t within; /* slim_within */
+  int32_t reserved; /* must be 0 */
 } slim_problem;
 
 /* Bytes of device workspace slim_fwd (phase SLIM_PHASE_FWD) or slim_bwd

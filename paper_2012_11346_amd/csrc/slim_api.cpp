@@ -84,8 +84,16 @@ int check_problem(const slim_problem* p) {
   if (!(p->dropout >= 0.f && p->dropout < 1.f)) return fail(SLIM_EINVAL, "dropout must be in [0, 1)");
   if (p->dtype == SLIM_F32 && (int64_t)p->d * p->M > 4096)
     return fail(SLIM_EUNSUPPORTED, "fp32 problems need d*M <= 4096 (got d=%d, M=%d)", (int)p->d, (int)p->M);
+  if (p->within != SLIM_WITHIN_ITER && p->within != SLIM_WITHIN_QUADRATIC)
+    return fail(SLIM_EINVAL, "unknown within-slice mode %d", (int)p->within);
+  if (p->reserved != 0) return fail(SLIM_EINVAL, "reserved field must be 0");
+  if (p->within == SLIM_WITHIN_QUADRATIC &&
+      (p->dtype != SLIM_BF16 || (p->M != 128 && p->M != 256) || p->kind == SLIM_SQUARE))
+    return fail(SLIM_EUNSUPPORTED, "the quadratic within-slice mode is built for bf16, M=128 or 256, FAVOR+ or ReLU");
   return SLIM_OK;
 }
+
+bool quad(const slim_problem* p) { return p->within == SLIM_WITHIN_QUADRATIC; }
 
 // value dropout parameters of the kernels: keep threshold t = round(p 65536)
 // on 16-bit fields (0: nothing dropped) and the output scale 1 / (1 - p)
@@ -194,7 +202,7 @@ int bwd_parts(const slim_problem* p) {
 // The forward hands its boundary states to the backward (slim_context_bytes)
 // when it computes them with one key shift per head (the key-sum kernel):
 // then its segments are the backward's parts.
-bool context_used(const slim_problem* p) { return has_ksum(p) && plan_fwd_segments(p) > 1; }
+bool context_used(const slim_problem* p) { return !quad(p) && has_ksum(p) && plan_fwd_segments(p) > 1; }
 // Parts of the forward's boundaries on the one-shift path
 int fwd_parts(const slim_problem* p) { return plan_fwd_segments(p); }
 
@@ -281,6 +289,55 @@ BwdLayout bwd_layout(const slim_problem* p, int P) {
   return l;
 }
 
+// ---- the quadratic within-slice mode: slices one after another, the 32-row
+// tiles of a slice in parallel
+int quad_slices(const slim_problem* p) { return (int)((p->L + clamp_C(p) - 1) / clamp_C(p)); }
+int quad_tiles(const slim_problem* p) { return (clamp_C(p) + kTileRows - 1) / kTileRows; }
+// workgroups per head of the per-slice passes: one per query (key) tile, up
+// to about eight per compute unit over all heads.  SLIM_QUAD_WORKGROUPS
+// (debugging) forces fewer, so that workgroups take several tiles.
+int quad_workgroups(const slim_problem* p) {
+  int64_t n = std::min<int64_t>(quad_tiles(p), 2048 / (p->B * p->H));
+  const char* env = getenv("SLIM_QUAD_WORKGROUPS");
+  if (env != nullptr && atoi(env) > 0) n = std::min<int64_t>(n, atoi(env));
+  return (int)std::max<int64_t>(1, n);
+}
+// parts of the per-slice key sums, and of the key maxima over the whole head
+int quad_sum_parts(const slim_problem* p) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>((quad_tiles(p) + 3) / 4, kTargetWorkgroupsForward / (p->B * p->H)));
+}
+int quad_max_parts(const slim_problem* p) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, count_tiles(p) / 4), kTargetWorkgroupsForward / (p->B * p->H)));
+}
+// states at exact restarts of the backward's downdates: the slices are cut
+// into this many runs, and each run's downdates start from an exact state
+int quad_runs(const slim_problem* p) {
+  const char* env = getenv("SLIM_QUAD_RUNS");
+  if (env != nullptr && atoi(env) > 0) return std::min(atoi(env), quad_slices(p));
+  return std::min(quad_slices(p), 16);
+}
+
+struct QuadFwdLayout {
+  size_t wfrag, kmax, sa, sb, parts, total;
+};
+QuadFwdLayout quad_fwd_layout(const slim_problem* p) {
+  QuadFwdLayout l{0, 0, 0, 0, 0, 0};
+  const size_t heads = (size_t)p->B * p->H, se = state_elems(p) * sizeof(float);
+  size_t off = 0;
+  l.wfrag = off;
+  off += align256(wfrag_bytes_of(p));
+  l.kmax = off;
+  off += align256(heads * quad_max_parts(p) * sizeof(float));
+  l.sa = off;
+  off += align256(heads * se);
+  l.sb = off;
+  off += align256(heads * se);
+  l.parts = off;
+  off += align256(heads * quad_sum_parts(p) * se);
+  l.total = off;
+  return l;
+}
+
 typedef hipError_t (*fwd_fn)(const slim::FwdArgs&, int, hipStream_t);
 typedef hipError_t (*feat_fn)(const slim::FeatArgs&, hipStream_t);
 typedef hipError_t (*bwd_fn)(const slim::BwdArgs&, hipStream_t);
@@ -288,6 +345,7 @@ typedef hipError_t (*wfrag_fn)(const slim::WfragArgs&, hipStream_t);
 typedef size_t (*size_fn)();
 typedef hipError_t (*carry_fn)(const slim::CarryArgs&, hipStream_t);
 typedef hipError_t (*ksum_fn)(const slim::KsumArgs&, int, hipStream_t);
+typedef hipError_t (*quad_fn)(const slim::QuadArgs&, int, hipStream_t);
 
 struct Dispatch {
   fwd_fn fwd;
@@ -299,6 +357,7 @@ struct Dispatch {
   carry_fn carry;
   carry_fn carry8;  // 8-wave carry pass (nullptr where not built)
   ksum_fn ksum;  // key sums of row ranges (nullptr where not built: the key-only walk serves)
+  quad_fn quad_fwd;  // quadratic within-slice mode (nullptr where not built)
 };
 
 template <class T, int D, int FW, int KIND>
@@ -306,7 +365,7 @@ Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
   return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>, nullptr,
                   &slim::launch_wfrag<G>,    &slim::wfrag_bytes<G>,     &slim::launch_carry<G>,    nullptr,
-                  nullptr};
+                  nullptr,                   nullptr};
 }
 template <int D, int FW, int KIND>
 Dispatch make_dispatch8() {
@@ -314,6 +373,7 @@ Dispatch make_dispatch8() {
   d.bwd8 = &slim::launch_bwd_walk8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   d.ksum = &slim::launch_ksum<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   d.carry8 = &slim::launch_carry8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
+  d.quad_fwd = &slim::launch_quad_fwd<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   return d;
 }
 
@@ -368,7 +428,10 @@ size_t context_bytes(const slim_problem* p) {
   return (size_t)p->B * p->H * (bwd_parts(p) + 1) * state_elems(p) * sizeof(float);
 }
 
-size_t fwd_ws_bytes(const slim_problem* p) { return fwd_layout(p, plan_fwd_segments(p)).total; }
+size_t fwd_ws_bytes(const slim_problem* p) {
+  if (quad(p)) return quad_fwd_layout(p).total;
+  return fwd_layout(p, plan_fwd_segments(p)).total;
+}
 size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
 
 }  // namespace
@@ -448,6 +511,92 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
 
 namespace {
 
+// Forward in the quadratic within-slice mode (arguments checked by fwd_impl):
+//   (0) one key shift per head: the largest key exponent of every part and
+//       of the initial state;
+//   (1) the state before the first slice: the initial state, rescaled to
+//       that shift;
+//   (2) per slice: the outputs of its query tiles from the state before it
+//       and its keys up to each row; what its keys add, in parts; the state
+//       after it = the state before + the parts.
+int quad_fwd_impl(const slim_problem* p, const Dispatch& dp, const void* Q, const void* K, const void* V,
+                  const float* W, const float* state_in, const float* kshift_in, void* Y, float* state_out,
+                  float* kshift_out, char* w, hipStream_t s) {
+  const QuadFwdLayout lay = quad_fwd_layout(p);
+  const bool favor = p->kind == SLIM_FAVOR_PLUS;
+  const int BH = (int)(p->B * p->H), SZ = (int)state_elems(p);
+  const int C = clamp_C(p), NS = quad_slices(p), tps = quad_tiles(p);
+  hipError_t e;
+  slim::WfragArgs wf;
+  wf.W = W;
+  wf.out = w + lay.wfrag;
+  e = dp.wfrag(wf, s);
+  if (e != hipSuccess) return hip_fail(e, "W-fragment launch");
+  slim::KsumArgs ks;
+  std::memset(&ks, 0, sizeof(ks));
+  set_drop(ks, drop_plan(p));
+  ks.K = K;
+  ks.V = V;
+  ks.W = W;
+  ks.Wfrag = wf.out;
+  ks.B = (int)p->B;
+  ks.H = (int)p->H;
+  ks.L = (int)p->L;
+  ks.C = C;
+  ks.relu_eps = p->relu_eps;
+  if (favor) {
+    ks.out = (float*)(w + lay.kmax);
+    ks.P2 = quad_max_parts(p);
+    e = dp.ksum(ks, slim::kSumMax, s);
+    if (e != hipSuccess) return hip_fail(e, "key-maximum launch");
+    e = slim::launch_kshift_reduce(ks.out, ks.P2, state_in != nullptr ? kshift_in : nullptr, kshift_out, BH, s);
+    if (e != hipSuccess) return hip_fail(e, "key-shift launch");
+    ks.shift = kshift_out;
+  }
+  float* Sa = (float*)(w + lay.sa);
+  float* Sb = (float*)(w + lay.sb);
+  float* parts = (float*)(w + lay.parts);
+  e = slim::launch_state_combine(state_in, favor ? kshift_in : nullptr, favor ? kshift_out : nullptr, nullptr, 0, 1.f,
+                                 Sa, BH, SZ, s);
+  if (e != hipSuccess) return hip_fail(e, "state launch");
+  slim::QuadArgs qa;
+  std::memset(&qa, 0, sizeof(qa));
+  set_drop(qa, drop_plan(p));
+  qa.Q = Q;
+  qa.K = K;
+  qa.V = V;
+  qa.Wfrag = wf.out;
+  qa.kshift = favor ? kshift_out : nullptr;
+  qa.Y = Y;
+  qa.B = (int)p->B;
+  qa.H = (int)p->H;
+  qa.L = (int)p->L;
+  qa.C = C;
+  qa.relu_eps = p->relu_eps;
+  ks.out = parts;
+  ks.P2 = quad_sum_parts(p);
+  e = timed_launch(SLIM_PHASE_FWD, s, [&]() -> hipError_t {
+    for (int n = 0; n < NS; ++n) {
+      qa.row0 = n * C;
+      qa.rows = (int)std::min<int64_t>(C, p->L - (int64_t)n * C);
+      qa.S = Sa;
+      hipError_t er = dp.quad_fwd(qa, quad_workgroups(p), s);
+      if (er != hipSuccess) return er;
+      if (n == NS - 1 && state_out == nullptr) break;
+      ks.tile_begin = n * tps;
+      ks.tile_end = n * tps + (qa.rows + kTileRows - 1) / kTileRows;
+      er = dp.ksum(ks, slim::kSumStates, s);
+      if (er != hipSuccess) return er;
+      er = slim::launch_state_combine(Sa, nullptr, nullptr, parts, ks.P2, 1.f, n == NS - 1 ? state_out : Sb, BH, SZ, s);
+      if (er != hipSuccess) return er;
+      std::swap(Sa, Sb);
+    }
+    return hipSuccess;
+  });
+  if (e != hipSuccess) return hip_fail(e, "quadratic-mode forward launches");
+  return ok();
+}
+
 // The forward of slim_fwd on a given workspace (the caller's, or the
 // library's static scratch for slim_fwd_noalloc).
 int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
@@ -464,11 +613,15 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
   st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out, ctx});
   if (st != SLIM_OK) return st;
   if (!context_used(p)) ctx = nullptr;
+  const size_t need = fwd_ws_bytes(p);
+  if (need > 0 && (ws == nullptr || ws_bytes < need))
+    return fail(SLIM_EWORKSPACE, "forward workspace needs %zu bytes, got %zu", need, ws == nullptr ? 0 : ws_bytes);
+  const Dispatch dp = dispatch(p);
+  if (quad(p))
+    return quad_fwd_impl(p, dp, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, (char*)ws,
+                         (hipStream_t)stream);
   const int P = plan_fwd_segments(p);
   const FwdLayout lay = fwd_layout(p, P);
-  if (lay.total > 0 && (ws == nullptr || ws_bytes < lay.total))
-    return fail(SLIM_EWORKSPACE, "forward workspace needs %zu bytes, got %zu", lay.total, ws == nullptr ? 0 : ws_bytes);
-  const Dispatch dp = dispatch(p);
   const bool favor = p->kind == SLIM_FAVOR_PLUS;
   hipStream_t s = (hipStream_t)stream;
   char* w = (char*)ws;

@@ -123,12 +123,47 @@ struct KsumArgs {
   const float* shift;  // kSumStates, FAVOR+: [B,H] key shift of the sums
   float* out;          // kSumStates: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
   int B, H, L, C, P2;
+  int tile_begin, tile_end;  // the parts cover tiles [tile_begin, tile_end) of each head (0, 0: all)
   float relu_eps;
   // value dropout (Drop): seed, keep threshold t (0: none), output scale 1 / (1 - p)
   uint64_t drop_seed;
   uint32_t drop_t;
   float drop_scale;
 };
+
+// In-slice masked quadratic form (the slice evaluated as a whole, Sec. 3.2
+// with eq. 2 inside the slice): slices are processed one after another,
+// the query (or key) tiles of a slice in parallel.
+struct QuadArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const void* dY;
+  const void* Wfrag;      // fragment-ordered W (WFragLayout), with the low parts
+  const float* kshift;    // [B,H] key shift (FAVOR+)
+  const float* S;         // [B,H,M,D+1] state before the slice (relative to kshift)
+  const float* Gc;        // [B,H,M,D+1] state cotangent after the slice (backward)
+  void* Y;                // forward: out [B,H,L,D]
+  float* DN;              // backward: [B,H,C,D+1] dN and dD of the slice's rows (out of the query pass)
+  void* dQ;
+  void* dK;
+  void* dV;
+  float* dW_part;         // [NWG slots of B,H][M,D] partial dW, accumulated (+=)
+  int B, H, L, C;
+  int row0, rows;         // the slice: rows [row0, row0 + rows)
+  float relu_eps;
+  uint64_t drop_seed;
+  uint32_t drop_t;
+  float drop_scale;
+};
+
+// Sum of per-part states: out = f * in + sign * sum_p part[p] per head, with
+// f = exp(in_shift - shift) when both shifts are given (FAVOR+), else 1;
+// in may be nullptr (zero).
+hipError_t launch_state_combine(const float* in, const float* in_shift, const float* shift, const float* part,
+                                int P2, float sign, float* out, int BH, int SZ, hipStream_t s);
+template <class G>
+hipError_t launch_quad_fwd(const QuadArgs& a, int nwg, hipStream_t s);
 
 template <class G>
 hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s);
@@ -179,6 +214,13 @@ hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hi
   X(float, 64, 16, 32, kRelu) X(float, 32, 32, 32, kRelu) X(float, 32, 16, 32, kRelu)    \
   X(bf16, 64, 16, 32, kSquare) X(bf16, 32, 16, 32, kSquare)                               \
   X(float, 64, 16, 32, kSquare) X(float, 32, 16, 32, kSquare)
+
+// configurations of the whole-slice quadratic form (bf16, 32 or 64 features
+// per wave)
+#define SLIM_FOR_EACH_QUAD_CONFIG(X)                                                  \
+  X(bf16, 64, 64, 32, kFavor) X(bf16, 64, 32, 32, kFavor) X(bf16, 32, 64, 32, kFavor) \
+  X(bf16, 32, 32, 32, kFavor) X(bf16, 64, 64, 32, kRelu) X(bf16, 64, 32, 32, kRelu)  \
+  X(bf16, 32, 64, 32, kRelu) X(bf16, 32, 32, 32, kRelu)
 
 // configurations served by the 8-wave backward walk
 #define SLIM_FOR_EACH_BF16_CONFIG(X)                                                  \

@@ -77,8 +77,9 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
 
   // rows of this part
   const TileMap tm(a.L, a.C, 32);
-  const int n_tiles = tm.count_tiles();
-  const int j0 = (int)((int64_t)part * n_tiles / a.P2), j1 = (int)((int64_t)(part + 1) * n_tiles / a.P2);
+  const int tb = a.tile_end > a.tile_begin ? a.tile_begin : 0;
+  const int n_tiles = (a.tile_end > a.tile_begin ? a.tile_end : tm.count_tiles()) - tb;
+  const int j0 = tb + (int)((int64_t)part * n_tiles / a.P2), j1 = tb + (int)((int64_t)(part + 1) * n_tiles / a.P2);
   int r0 = 0, r1 = 0;
   if (j1 > j0) {
     int s_, c_;

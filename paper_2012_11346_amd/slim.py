@@ -21,6 +21,8 @@ FAVOR_PLUS, RELU, SQUARE = 0, 1, 2
 F32, BF16 = 0, 1
 QUERY, KEY = 0, 1
 PHASE_FWD, PHASE_BWD = 0, 1
+WITHIN_ITER, WITHIN_QUADRATIC = 0, 1
+WITHINS = {"iter": WITHIN_ITER, "quadratic": WITHIN_QUADRATIC}
 
 KINDS = {"favor+": FAVOR_PLUS, "relu": RELU, "square": SQUARE}
 DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
@@ -45,6 +47,8 @@ class Problem(ctypes.Structure):
         ("relu_eps", ctypes.c_float),
         ("dropout", ctypes.c_float),
         ("seed", ctypes.c_uint64),
+        ("within", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -104,13 +108,16 @@ def _check(status: int):
         raise SlimError(status, LIB.slim_last_error().decode())
 
 
-def problem(B, H, L, d, M, C, dtype=BF16, kind=FAVOR_PLUS, relu_eps=1e-3, dropout=0.0, seed=0) -> Problem:
+def problem(B, H, L, d, M, C, dtype=BF16, kind=FAVOR_PLUS, relu_eps=1e-3, dropout=0.0, seed=0,
+            within=WITHIN_ITER) -> Problem:
     if isinstance(dtype, torch.dtype):
         dtype = DTYPES[dtype]
     if isinstance(kind, str):
         kind = KINDS[kind]
+    if isinstance(within, str):
+        within = WITHINS[within]
     return Problem(int(B), int(H), int(L), int(d), int(M), int(C), int(dtype), int(kind), float(relu_eps),
-                   float(dropout), int(seed) & ((1 << 64) - 1))
+                   float(dropout), int(seed) & ((1 << 64) - 1), int(within), 0)
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -121,11 +128,12 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def _problem_of(Q: torch.Tensor, W: torch.Tensor, C: int, kind, relu_eps: float, dropout=0.0, seed=0) -> Problem:
+def _problem_of(Q: torch.Tensor, W: torch.Tensor, C: int, kind, relu_eps: float, dropout=0.0, seed=0,
+                within=WITHIN_ITER) -> Problem:
     if Q.dim() != 4:
         raise ValueError("Q must be [B, H, L, d]")
     B, H, L, d = Q.shape
-    return problem(B, H, L, d, W.shape[0], C, DTYPES[Q.dtype], kind, relu_eps, dropout, seed)
+    return problem(B, H, L, d, W.shape[0], C, DTYPES[Q.dtype], kind, relu_eps, dropout, seed, within)
 
 
 def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
@@ -153,9 +161,9 @@ def context_bytes(p: Problem) -> int:
     return int(LIB.slim_context_bytes(ctypes.byref(p)))
 
 
-def new_context(Q: torch.Tensor, W: torch.Tensor, C: int, kind="favor+", relu_eps: float = 1e-3):
+def new_context(Q: torch.Tensor, W: torch.Tensor, C: int, kind="favor+", relu_eps: float = 1e-3, within="iter"):
     """A context buffer for fwd(..., ctx=) and bwd(..., ctx=), or None when the problem uses none."""
-    n = context_bytes(_problem_of(Q, W, C, kind, relu_eps))
+    n = context_bytes(_problem_of(Q, W, C, kind, relu_eps, within=within))
     return None if n == 0 else torch.empty(n // 4, dtype=torch.float32, device=Q.device)
 
 
@@ -211,11 +219,12 @@ def _need_ctx(p: Problem, ctx: Optional[torch.Tensor]):
 
 
 def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3, ws=None,
-        Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0):
+        Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0, within="iter"):
     """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None).
     ctx (optional, from new_context) receives the segment boundary states for bwd.
-    dropout / seed: value dropout with per-slice seeds (include/slim.h)."""
-    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed)
+    dropout / seed: value dropout with per-slice seeds; within: "iter" or
+    "quadratic" (include/slim.h)."""
+    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed, within)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V)):
         _need(t, n, Q.dtype, shp)
@@ -243,12 +252,12 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
 
 def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshift_in=None, dstate_out=None,
         want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None,
-        ctx=None, dropout: float = 0.0, seed: int = 0):
+        ctx=None, dropout: float = 0.0, seed: int = 0, within="iter"):
     """Backward sweep; kshift is the forward's kshift_out (FAVOR+); ctx (optional)
     is the context the forward wrote for the same inputs.
 
     Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
-    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed)
+    p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed, within)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V), ("dY", dY)):
         _need(t, n, Q.dtype, shp)
