@@ -338,6 +338,44 @@ QuadFwdLayout quad_fwd_layout(const slim_problem* p) {
   return l;
 }
 
+// workgroups per head of the backward passes (each holds a dW partial)
+int quad_bwd_workgroups(const slim_problem* p) {
+  return std::min(quad_workgroups(p), (int)std::max<int64_t>(1, 1024 / (p->B * p->H)));
+}
+size_t state_frag_bytes_of(const slim_problem* p);
+// backward workspace: W in fragment order; the run sums and the exact
+// states at the run boundaries; states and cotangents (two each, used in
+// turn); per-slice parts; fragment tables of the state and the cotangent;
+// the query pass's rows [dN|dD|shift]; the dW partials
+struct QuadBwdLayout {
+  size_t wfrag, seg, bounds, s[2], g[2], parts, sfrag, gfrag, dn, dw_part, total;
+};
+QuadBwdLayout quad_bwd_layout(const slim_problem* p) {
+  QuadBwdLayout l;
+  std::memset(&l, 0, sizeof(l));
+  const size_t heads = (size_t)p->B * p->H, se = state_elems(p) * sizeof(float);
+  const int R = quad_runs(p);
+  size_t off = 0;
+  auto take = [&](size_t& at, size_t n) {
+    at = off;
+    off += align256(n);
+  };
+  take(l.wfrag, wfrag_bytes_of(p));
+  take(l.seg, heads * R * se);
+  take(l.bounds, heads * (R + 1) * se);
+  take(l.s[0], heads * se);
+  take(l.s[1], heads * se);
+  take(l.g[0], heads * se);
+  take(l.g[1], heads * se);
+  take(l.parts, heads * std::max(quad_sum_parts(p), 1) * se);
+  take(l.sfrag, heads * state_frag_bytes_of(p));
+  take(l.gfrag, heads * state_frag_bytes_of(p));
+  take(l.dn, heads * (size_t)clamp_C(p) * (p->d + 4) * sizeof(float));
+  take(l.dw_part, heads * quad_bwd_workgroups(p) * (size_t)p->M * p->d * sizeof(float));
+  l.total = off;
+  return l;
+}
+
 typedef hipError_t (*fwd_fn)(const slim::FwdArgs&, int, hipStream_t);
 typedef hipError_t (*feat_fn)(const slim::FeatArgs&, hipStream_t);
 typedef hipError_t (*bwd_fn)(const slim::BwdArgs&, hipStream_t);
@@ -346,6 +384,7 @@ typedef size_t (*size_fn)();
 typedef hipError_t (*carry_fn)(const slim::CarryArgs&, hipStream_t);
 typedef hipError_t (*ksum_fn)(const slim::KsumArgs&, int, hipStream_t);
 typedef hipError_t (*quad_fn)(const slim::QuadArgs&, int, hipStream_t);
+typedef hipError_t (*sfrag_fn)(const float*, void*, const float*, void*, int, hipStream_t);
 
 struct Dispatch {
   fwd_fn fwd;
@@ -358,6 +397,9 @@ struct Dispatch {
   carry_fn carry8;  // 8-wave carry pass (nullptr where not built)
   ksum_fn ksum;  // key sums of row ranges (nullptr where not built: the key-only walk serves)
   quad_fn quad_fwd;  // quadratic within-slice mode (nullptr where not built)
+  quad_fn quad_dq, quad_dk, quad_gsum;
+  sfrag_fn state_frag;
+  size_fn state_frag_bytes;
 };
 
 template <class T, int D, int FW, int KIND>
@@ -365,7 +407,9 @@ Dispatch make_dispatch() {
   typedef slim::Cfg<T, D, FW, kTileRows, KIND> G;
   return Dispatch{&slim::launch_fwd_walk<G>, &slim::launch_featmap<G>, &slim::launch_bwd_walk<G>, nullptr,
                   &slim::launch_wfrag<G>,    &slim::wfrag_bytes<G>,     &slim::launch_carry<G>,    nullptr,
-                  nullptr,                   nullptr};
+                  nullptr,                   nullptr,                   nullptr,
+                  nullptr,                   nullptr,                   nullptr,
+                  nullptr};
 }
 template <int D, int FW, int KIND>
 Dispatch make_dispatch8() {
@@ -373,7 +417,13 @@ Dispatch make_dispatch8() {
   d.bwd8 = &slim::launch_bwd_walk8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   d.ksum = &slim::launch_ksum<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
   d.carry8 = &slim::launch_carry8<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
-  d.quad_fwd = &slim::launch_quad_fwd<slim::Cfg<slim::bf16, D, FW, kTileRows, KIND>>;
+  typedef slim::Cfg<slim::bf16, D, FW, kTileRows, KIND> G;
+  d.quad_fwd = &slim::launch_quad_fwd<G>;
+  d.quad_dq = &slim::launch_quad_dq<G>;
+  d.quad_dk = &slim::launch_quad_dk<G>;
+  d.quad_gsum = &slim::launch_quad_gsum<G>;
+  d.state_frag = &slim::launch_state_frag<G>;
+  d.state_frag_bytes = &slim::state_frag_bytes<G>;
   return d;
 }
 
@@ -421,6 +471,10 @@ Dispatch dispatch(const slim_problem* p) {
 }
 
 size_t wfrag_bytes_of(const slim_problem* p) { return dispatch(p).wfrag_bytes(); }
+size_t state_frag_bytes_of(const slim_problem* p) {
+  const Dispatch d = dispatch(p);
+  return d.state_frag_bytes != nullptr ? d.state_frag_bytes() : 0;
+}
 bool has_ksum(const slim_problem* p) { return dispatch(p).ksum != nullptr; }
 bool has_carry8(const slim_problem* p) { return dispatch(p).carry8 != nullptr; }
 size_t context_bytes(const slim_problem* p) {
@@ -432,7 +486,10 @@ size_t fwd_ws_bytes(const slim_problem* p) {
   if (quad(p)) return quad_fwd_layout(p).total;
   return fwd_layout(p, plan_fwd_segments(p)).total;
 }
-size_t bwd_ws_bytes(const slim_problem* p) { return bwd_layout(p, plan_segments(p)).total; }
+size_t bwd_ws_bytes(const slim_problem* p) {
+  if (quad(p)) return quad_bwd_layout(p).total;
+  return bwd_layout(p, plan_segments(p)).total;
+}
 
 }  // namespace
 
@@ -556,8 +613,8 @@ int quad_fwd_impl(const slim_problem* p, const Dispatch& dp, const void* Q, cons
   float* Sa = (float*)(w + lay.sa);
   float* Sb = (float*)(w + lay.sb);
   float* parts = (float*)(w + lay.parts);
-  e = slim::launch_state_combine(state_in, favor ? kshift_in : nullptr, favor ? kshift_out : nullptr, nullptr, 0, 1.f,
-                                 Sa, BH, SZ, s);
+  e = slim::launch_state_combine(state_in, SZ, favor ? kshift_in : nullptr, favor ? kshift_out : nullptr, nullptr, 0,
+                                 1.f, Sa, BH, SZ, s);
   if (e != hipSuccess) return hip_fail(e, "state launch");
   slim::QuadArgs qa;
   std::memset(&qa, 0, sizeof(qa));
@@ -587,13 +644,170 @@ int quad_fwd_impl(const slim_problem* p, const Dispatch& dp, const void* Q, cons
       ks.tile_end = n * tps + (qa.rows + kTileRows - 1) / kTileRows;
       er = dp.ksum(ks, slim::kSumStates, s);
       if (er != hipSuccess) return er;
-      er = slim::launch_state_combine(Sa, nullptr, nullptr, parts, ks.P2, 1.f, n == NS - 1 ? state_out : Sb, BH, SZ, s);
+      er = slim::launch_state_combine(Sa, SZ, nullptr, nullptr, parts, ks.P2, 1.f, n == NS - 1 ? state_out : Sb, BH, SZ,
+                                      s);
       if (er != hipSuccess) return er;
       std::swap(Sa, Sb);
     }
     return hipSuccess;
   });
   if (e != hipSuccess) return hip_fail(e, "quadratic-mode forward launches");
+  return ok();
+}
+
+// Backward in the quadratic within-slice mode (arguments checked by slim_bwd):
+//   (1) exact states at the boundaries of R runs of whole slices (slice-
+//       aligned key sums, then their prefix from the initial state);
+//   (2) the slices in reverse, each with the state before it (the exact
+//       state at a run's first slice, else the state after it downdated by
+//       what the slice's keys add, eq. 17) and the cotangent after it: the
+//       query pass, the key pass, then the cotangent before it (eq. 18);
+//   (3) dstate_in, and dW from the workgroups' partials in a fixed order.
+int quad_bwd_impl(const slim_problem* p, const Dispatch& dp, const void* Q, const void* K, const void* V,
+                  const float* W, const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
+                  const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in, char* w,
+                  hipStream_t s) {
+  const QuadBwdLayout lay = quad_bwd_layout(p);
+  const bool favor = p->kind == SLIM_FAVOR_PLUS;
+  const int BH = (int)(p->B * p->H), SZ = (int)state_elems(p);
+  const int C = clamp_C(p), NS = quad_slices(p), tps = quad_tiles(p), R = quad_runs(p);
+  const int P2 = quad_sum_parts(p), NW = quad_bwd_workgroups(p);
+  hipError_t e;
+  slim::WfragArgs wf;
+  wf.W = W;
+  wf.out = w + lay.wfrag;
+  e = dp.wfrag(wf, s);
+  if (e != hipSuccess) return hip_fail(e, "W-fragment launch");
+  slim::KsumArgs ks;
+  std::memset(&ks, 0, sizeof(ks));
+  set_drop(ks, drop_plan(p));
+  ks.K = K;
+  ks.V = V;
+  ks.W = W;
+  ks.Wfrag = wf.out;
+  ks.shift = favor ? kshift : nullptr;
+  ks.B = (int)p->B;
+  ks.H = (int)p->H;
+  ks.L = (int)p->L;
+  ks.C = C;
+  ks.relu_eps = p->relu_eps;
+  // (1)
+  ks.out = (float*)(w + lay.seg);
+  ks.P2 = R;
+  ks.align = tps;
+  e = dp.ksum(ks, slim::kSumStates, s);
+  if (e != hipSuccess) return hip_fail(e, "run-sum launch");
+  const float* bounds = (const float*)(w + lay.bounds);
+  const size_t bstride = (size_t)(R + 1) * SZ;  // between heads of one boundary
+  {
+    slim::ScanArgs sc;
+    std::memset(&sc, 0, sizeof(sc));
+    sc.seg = ks.out;
+    sc.init = state_in;
+    sc.init_shift = favor ? kshift_in : nullptr;
+    sc.shift = favor ? kshift : nullptr;
+    sc.out = (float*)(w + lay.bounds);
+    sc.BH = BH;
+    sc.P = R;
+    sc.SZ = SZ;
+    sc.favor = favor ? 1 : 0;
+    e = slim::launch_scan_bwd(sc, s);
+    if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
+  }
+  ks.align = 0;
+  ks.out = (float*)(w + lay.parts);
+  ks.P2 = P2;
+  float* dw_part = (float*)(w + lay.dw_part);
+  e = slim::launch_state_combine(nullptr, 0, nullptr, nullptr, nullptr, 0, 1.f, dw_part, BH * NW, (int)(p->M * p->d), s);
+  if (e != hipSuccess) return hip_fail(e, "dW-partial launch");
+  float* parts = (float*)(w + lay.parts);
+  float* sbuf[2] = {(float*)(w + lay.s[0]), (float*)(w + lay.s[1])};
+  float* gbuf[2] = {(float*)(w + lay.g[0]), (float*)(w + lay.g[1])};
+  const float* Gafter = dstate_out;
+  int gb = 0;
+  if (Gafter == nullptr) {
+    e = slim::launch_state_combine(nullptr, 0, nullptr, nullptr, nullptr, 0, 1.f, gbuf[1], BH, SZ, s);
+    if (e != hipSuccess) return hip_fail(e, "cotangent launch");
+    Gafter = gbuf[1];
+  }
+  slim::QuadArgs qa;
+  std::memset(&qa, 0, sizeof(qa));
+  set_drop(qa, drop_plan(p));
+  qa.Q = Q;
+  qa.K = K;
+  qa.V = V;
+  qa.dY = dY;
+  qa.Wfrag = wf.out;
+  qa.kshift = favor ? kshift : nullptr;
+  qa.Sfrag = w + lay.sfrag;
+  qa.Gfrag = w + lay.gfrag;
+  qa.DN = (float*)(w + lay.dn);
+  qa.dQ = dQ;
+  qa.dK = dK;
+  qa.dV = dV;
+  qa.dW_part = dw_part;
+  qa.out = parts;
+  qa.B = (int)p->B;
+  qa.H = (int)p->H;
+  qa.L = (int)p->L;
+  qa.C = C;
+  qa.relu_eps = p->relu_eps;
+  auto first_of_run = [&](int r) { return (int)((int64_t)r * NS / R); };
+  // (2)
+  e = timed_launch(SLIM_PHASE_BWD, s, [&]() -> hipError_t {
+    hipError_t er;
+    int r = R - 1, sb = 0;
+    const float* Safter = nullptr;  // the state after slice n, unless n ends its run
+    for (int n = NS - 1; n >= 0; --n) {
+      while (first_of_run(r) > n) --r;
+      const int rows = (int)std::min<int64_t>(C, p->L - (int64_t)n * C);
+      const bool run_end = (n == first_of_run(r + 1) - 1);
+      float* Sb = sbuf[sb];
+      sb ^= 1;
+      if (n == first_of_run(r)) {
+        er = slim::launch_state_combine(bounds + (size_t)r * SZ, bstride, nullptr, nullptr, nullptr, 0, 1.f, Sb, BH, SZ,
+                                        s);
+      } else {
+        ks.tile_begin = n * tps;
+        ks.tile_end = n * tps + (rows + kTileRows - 1) / kTileRows;
+        er = dp.ksum(ks, slim::kSumStates, s);
+        if (er != hipSuccess) return er;
+        if (run_end) er = slim::launch_state_combine(bounds + (size_t)(r + 1) * SZ, bstride, nullptr, nullptr, parts, P2,
+                                                     -1.f, Sb, BH, SZ, s);
+        else er = slim::launch_state_combine(Safter, SZ, nullptr, nullptr, parts, P2, -1.f, Sb, BH, SZ, s);
+      }
+      if (er != hipSuccess) return er;
+      Safter = Sb;
+      er = dp.state_frag(Sb, w + lay.sfrag, Gafter, w + lay.gfrag, BH, s);
+      if (er != hipSuccess) return er;
+      qa.S = Sb;
+      qa.Gc = Gafter;
+      qa.row0 = n * C;
+      qa.rows = rows;
+      er = dp.quad_dq(qa, NW, s);
+      if (er != hipSuccess) return er;
+      er = dp.quad_dk(qa, NW, s);
+      if (er != hipSuccess) return er;
+      if (n > 0 || dstate_in != nullptr) {
+        er = dp.quad_gsum(qa, P2, s);
+        if (er != hipSuccess) return er;
+        er = slim::launch_state_combine(Gafter, SZ, nullptr, nullptr, parts, P2, 1.f, gbuf[gb], BH, SZ, s);
+        if (er != hipSuccess) return er;
+        Gafter = gbuf[gb];
+        gb ^= 1;
+      }
+    }
+    return hipSuccess;
+  });
+  if (e != hipSuccess) return hip_fail(e, "quadratic-mode backward launches");
+  // (3) the cotangent of state_in, relative to kshift_in (FAVOR+ with an initial state)
+  if (dstate_in != nullptr) {
+    e = slim::launch_state_combine(Gafter, SZ, favor ? kshift_in : nullptr, favor ? kshift : nullptr, nullptr, 0, 1.f,
+                                   dstate_in, BH, SZ, s);
+    if (e != hipSuccess) return hip_fail(e, "dstate_in launch");
+  }
+  e = slim::launch_dw_reduce(dw_part, BH * NW, (int)(p->M * p->d), dW, s);
+  if (e != hipSuccess) return hip_fail(e, "dW-reduction launch");
   return ok();
 }
 
@@ -820,12 +1034,15 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   st = check_alignment({Q, K, V, dY, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in, ctx});
   if (st != SLIM_OK) return st;
   if (!context_used(p)) ctx = nullptr;
+  const size_t need = bwd_ws_bytes(p);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(SLIM_EWORKSPACE, "backward workspace needs %zu bytes, got %zu", need, ws == nullptr ? 0 : ws_bytes);
+  const Dispatch dp = dispatch(p);
+  if (quad(p))
+    return quad_bwd_impl(p, dp, Q, K, V, W, state_in, kshift_in, kshift, dY, dstate_out, dQ, dK, dV, dW, dstate_in,
+                         (char*)ws, (hipStream_t)stream);
   const int P = plan_segments(p);
   const BwdLayout lay = bwd_layout(p, P);
-  if (ws == nullptr || ws_bytes < lay.total)
-    return fail(SLIM_EWORKSPACE, "backward workspace needs %zu bytes, got %zu", lay.total,
-                ws == nullptr ? 0 : ws_bytes);
-  const Dispatch dp = dispatch(p);
   hipStream_t s = (hipStream_t)stream;
   char* w = (char*)ws;
   const int BH = (int)(p->B * p->H);

@@ -124,6 +124,7 @@ struct KsumArgs {
   float* out;          // kSumStates: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
   int B, H, L, C, P2;
   int tile_begin, tile_end;  // the parts cover tiles [tile_begin, tile_end) of each head (0, 0: all)
+  int align;                 // > 0: parts start at multiples of `align` tiles from tile_begin (slices)
   float relu_eps;
   // value dropout (Drop): seed, keep threshold t (0: none), output scale 1 / (1 - p)
   uint64_t drop_seed;
@@ -142,13 +143,16 @@ struct QuadArgs {
   const void* Wfrag;      // fragment-ordered W (WFragLayout), with the low parts
   const float* kshift;    // [B,H] key shift (FAVOR+)
   const float* S;         // [B,H,M,D+1] state before the slice (relative to kshift)
-  const float* Gc;        // [B,H,M,D+1] state cotangent after the slice (backward)
+  const void* Sfrag;      // its fragment tables (StateFragLayout), backward query pass
+  const float* Gc;        // [B,H,M,D+1] state cotangent after the slice (backward key pass)
+  const void* Gfrag;      // its fragment tables
   void* Y;                // forward: out [B,H,L,D]
-  float* DN;              // backward: [B,H,C,D+1] dN and dD of the slice's rows (out of the query pass)
+  float* DN;              // backward: [B,H,C,D+4] per row of the slice: dN[0,D), dD, the query row shift
   void* dQ;
   void* dK;
   void* dV;
-  float* dW_part;         // [NWG slots of B,H][M,D] partial dW, accumulated (+=)
+  float* dW_part;         // [B,H,gridDim.x][M,D] partial dW per workgroup, accumulated (+=)
+  float* out;             // cotangent sums: [B,H,gridDim.x][M,D+1] per part
   int B, H, L, C;
   int row0, rows;         // the slice: rows [row0, row0 + rows)
   float relu_eps;
@@ -159,11 +163,25 @@ struct QuadArgs {
 
 // Sum of per-part states: out = f * in + sign * sum_p part[p] per head, with
 // f = exp(in_shift - shift) when both shifts are given (FAVOR+), else 1;
-// in may be nullptr (zero).
-hipError_t launch_state_combine(const float* in, const float* in_shift, const float* shift, const float* part,
-                                int P2, float sign, float* out, int BH, int SZ, hipStream_t s);
+// in may be nullptr (zero); head h of `in` starts at in + h * in_stride,
+// of `out` at out + h * SZ, its parts at part + (h * P2 + p) * SZ.
+hipError_t launch_state_combine(const float* in, size_t in_stride, const float* in_shift, const float* shift,
+                                const float* part, int P2, float sign, float* out, int BH, int SZ, hipStream_t s);
 template <class G>
 hipError_t launch_quad_fwd(const QuadArgs& a, int nwg, hipStream_t s);
+// backward of one slice: the query pass (dN, dD, dQ, dW), the key pass
+// (dK, dV, dW), the sum of Q~^T [dN|dD] over the slice in nwg parts
+template <class G>
+hipError_t launch_quad_dq(const QuadArgs& a, int nwg, hipStream_t s);
+template <class G>
+hipError_t launch_quad_dk(const QuadArgs& a, int nwg, hipStream_t s);
+template <class G>
+hipError_t launch_quad_gsum(const QuadArgs& a, int nwg, hipStream_t s);
+// fragment tables of n states [BH][M][D+1] (n = 1 or 2: X0 -> F0, X1 -> F1)
+template <class G>
+hipError_t launch_state_frag(const float* X0, void* F0, const float* X1, void* F1, int BH, hipStream_t s);
+template <class G>
+size_t state_frag_bytes();
 
 template <class G>
 hipError_t launch_fwd_walk(const FwdArgs& a, int mode, hipStream_t s);

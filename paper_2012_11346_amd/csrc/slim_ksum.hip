@@ -3,7 +3,8 @@
 // exponent of each part.
 //
 // Each head's sequence is cut into P2 parts at the 32-row tile boundaries
-// the walks use (part p holds tiles [p n / P2, (p + 1) n / P2)).  A part's
+// the walks use (part p holds tiles [p n / P2, (p + 1) n / P2), or whole
+// slices when the caller asks for slice-aligned parts).  A part's
 // contribution to the state is a plain sum over its rows,
 //   [S | z] = sum_s K~[s]^T [V[s] | 1],
 // with no causal structure, so this pass streams the part's rows in 64-row
@@ -79,7 +80,16 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   const TileMap tm(a.L, a.C, 32);
   const int tb = a.tile_end > a.tile_begin ? a.tile_begin : 0;
   const int n_tiles = (a.tile_end > a.tile_begin ? a.tile_end : tm.count_tiles()) - tb;
-  const int j0 = tb + (int)((int64_t)part * n_tiles / a.P2), j1 = tb + (int)((int64_t)(part + 1) * n_tiles / a.P2);
+  int j0, j1;
+  if (a.align > 0) {
+    // whole units of `align` tiles (slices) per part; the last unit may be short
+    const int nu = (n_tiles + a.align - 1) / a.align;
+    j0 = tb + min(n_tiles, a.align * (int)((int64_t)part * nu / a.P2));
+    j1 = tb + min(n_tiles, a.align * (int)((int64_t)(part + 1) * nu / a.P2));
+  } else {
+    j0 = tb + (int)((int64_t)part * n_tiles / a.P2);
+    j1 = tb + (int)((int64_t)(part + 1) * n_tiles / a.P2);
+  }
   int r0 = 0, r1 = 0;
   if (j1 > j0) {
     int s_, c_;

@@ -300,25 +300,26 @@ __global__ __launch_bounds__(256, 2) void quad_fwd_kernel(QuadArgs a) {
 }
 
 // out = f * in + sign * sum_p part[p], one thread per state entry
-__global__ __launch_bounds__(256) void state_combine_kernel(const float* in, const float* in_shift, const float* shift,
-                                                            const float* part, int P2, float sign, float* out, int SZ) {
+__global__ __launch_bounds__(256) void state_combine_kernel(const float* in, size_t in_stride, const float* in_shift,
+                                                            const float* shift, const float* part, int P2, float sign,
+                                                            float* out, int SZ) {
   const int head = blockIdx.y;
   const int el = blockIdx.x * 256 + threadIdx.x;
   if (el >= SZ) return;
   float v = 0.f;
   if (in != nullptr) {
     const float f = (in_shift != nullptr && shift != nullptr) ? fast_exp2((in_shift[head] - shift[head]) * kLog2e) : 1.f;
-    v = f * in[(size_t)head * SZ + el];
+    v = f * in[(size_t)head * in_stride + el];
   }
   float s = 0.f;
   for (int p = 0; p < P2; ++p) s += part[((size_t)head * P2 + p) * SZ + el];
   out[(size_t)head * SZ + el] = v + sign * s;
 }
 
-hipError_t launch_state_combine(const float* in, const float* in_shift, const float* shift, const float* part,
-                                int P2, float sign, float* out, int BH, int SZ, hipStream_t s) {
-  hipLaunchKernelGGL(state_combine_kernel, dim3((SZ + 255) / 256, BH), dim3(256), 0, s, in, in_shift, shift, part, P2,
-                     sign, out, SZ);
+hipError_t launch_state_combine(const float* in, size_t in_stride, const float* in_shift, const float* shift,
+                                const float* part, int P2, float sign, float* out, int BH, int SZ, hipStream_t s) {
+  hipLaunchKernelGGL(state_combine_kernel, dim3((SZ + 255) / 256, BH), dim3(256), 0, s, in, in_stride, in_shift, shift,
+                     part, P2, sign, out, SZ);
   return hipGetLastError();
 }
 

@@ -117,3 +117,94 @@ def test_quadratic_rejects_unbuilt_problems():
     x = _inputs(22, 1, 1, 64, 32, 64, 32, "favor+")
     with pytest.raises(RuntimeError, match="quadratic"):
         slim.fwd(dev(x["Q"]), dev(x["K"]), dev(x["V"]), dev(x["W"]), 32, within="quadratic")
+
+
+# name, B, H, L, d, M, C, kind, forced workgroups per head, forced runs of the downdates
+BWD_CASES = [
+    ("ragged_c64", 2, 3, 300, 64, 256, 64, "favor+", None, None),
+    ("c100_one_run", 1, 2, 250, 64, 256, 100, "favor+", None, 1),
+    ("relu_c_above_L", 2, 2, 200, 64, 128, 256, "relu", None, None),
+    ("d32_m256_c40", 1, 2, 333, 32, 256, 40, "favor+", None, None),
+    ("d32_m128_relu_c16_runs3", 2, 1, 170, 32, 128, 16, "relu", None, 3),
+    ("c1", 1, 1, 40, 64, 128, 1, "favor+", None, None),
+    ("c512_strided", 1, 2, 1100, 64, 256, 512, "favor+", 3, None),
+    ("relu_c300_strided", 1, 1, 1000, 32, 256, 300, "relu", 2, 2),
+    ("many_slices_c32", 1, 2, 2048, 64, 256, 32, "favor+", None, None),
+]
+
+
+@pytest.mark.parametrize("i", range(len(BWD_CASES)))
+def test_quadratic_backward(i):
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    name, B, H, L, d, M, C, kind, nwg, runs = BWD_CASES[i]
+    print(f"[quadratic bwd] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {kind} workgroups={nwg} runs={runs}",
+          flush=True)
+    x = _inputs(40 + i, B, H, L, d, M, C, kind)
+    Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+    with _env(SLIM_QUAD_WORKGROUPS=nwg, SLIM_QUAD_RUNS=runs):
+        Y, st, ks = slim.fwd(Q, K, V, W, C, kind, within="quadratic")
+        g = slim.bwd(Q, K, V, W, dY, C, ks, kind, within="quadratic")
+    gi = slim.bwd(Q, K, V, W, dY, C, ks, kind)
+    torch.cuda.synchronize()
+    tol = TOL["bf16"]
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
+    for n, a, r, b in zip(("dQ", "dK", "dV", "dW"), g[:4], ref, gi[:4]):
+        report(n, host64(a), r, tol)
+        report(n + " vs tile walk", host64(a), host64(b), tol)
+
+
+def test_quadratic_state_cotangent_and_chaining():
+    """The backward of the second half, its G^(0) fed to the backward of the
+    first half, equals the backward of the whole sequence (both halves in the
+    quadratic mode); G^(0) matches Algorithm 1."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    B, H, L, d, M, C, kind = 1, 2, 400, 64, 256, 64, "favor+"
+    x = _inputs(60, B, H, L, d, M, C, kind)
+    cut = 200 + 3
+    tol = TOL["bf16"]
+    Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+    half = lambda t, a, b: t[:, :, a:b].contiguous()
+    q = "quadratic"
+    Y1, st1, ks1 = slim.fwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, C, kind, within=q)
+    Y2, st2, ks2 = slim.fwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, C, kind, state_in=st1,
+                            kshift_in=ks1, within=q)
+    g2 = slim.bwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, half(dY, cut, L), C, ks2, kind,
+                  state_in=st1, kshift_in=ks1, want_dstate_in=True, within=q)
+    g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, ks1, kind,
+                  dstate_out=g2[4], within=q)
+    torch.cuda.synchronize()
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
+    report("dQ (chained)", np.concatenate([host64(g1[0]), host64(g2[0])], axis=2), ref[0], tol)
+    report("dK (chained)", np.concatenate([host64(g1[1]), host64(g2[1])], axis=2), ref[1], tol)
+    report("dV (chained)", np.concatenate([host64(g1[2]), host64(g2[2])], axis=2), ref[2], tol)
+    report("dW (chained)", host64(g1[3]) + host64(g2[3]), ref[3], tol)
+    st_full = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, kind)[1]
+    go = O.slim_backward(x["Q"][:, :, cut:], x["K"][:, :, cut:], x["V"][:, :, cut:], x["W"], x["dY"][:, :, cut:], C,
+                         kind, st_full, mask_W=mask_w(x))[4]
+    g0 = host64(g2[4]) * np.exp(-host64(ks1))[:, :, None, None]
+    report("dstate_in", g0, go, tol)
+
+
+@pytest.mark.parametrize("kind", ["favor+", "relu"])
+def test_quadratic_backward_dropout(kind):
+    """Value dropout in the backward: the masks regenerated per slice, dropped
+    value elements with exactly zero gradient."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    B, H, L, d, M, C, p, seed = 1, 2, 300, 64, 128, 64, 0.3, 2 ** 62 + 11
+    x = _inputs(61 if kind == "favor+" else 62, B, H, L, d, M, C, kind)
+    Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
+    Y, st, ks = slim.fwd(Q, K, V, W, C, kind, dropout=p, seed=seed, within="quadratic")
+    g = slim.bwd(Q, K, V, W, dY, C, ks, kind, dropout=p, seed=seed, within="quadratic")
+    torch.cuda.synchronize()
+    ref = O.dropout_backward(O.attention_backward, x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, C, p, seed,
+                             mask_W=mask_w(x))
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), g[:4], ref):
+        report(n, host64(a), r, TOL["bf16"])
+    m = O.value_mask(B, H, L, d, C, p, seed)
+    assert torch.count_nonzero(g[2].cpu()[torch.from_numpy(m == 0)]).item() == 0
