@@ -11,7 +11,8 @@ whole batch, and, unless switched off:
   block the kernels ran, the executed-work roofline fraction of the reverse
   walk, peak device memory beyond inputs and outputs, the lower bound "L/B"
   (the same measured on an input of length C) and the L2-relative gradient
-  error against the oracle;
+  error against the oracle; then the same slice lengths with each slice
+  evaluated as one masked quadratic form (the within-slice quadratic mode);
 * configs: the other workloads (tiny fp32 exactness check, B8 H8 L4096,
   L=262144 long context, the six-layer ReLU stack run forward r=1..6 then
   backward r=6..1), each with time, roofline and parity on sampled heads;
@@ -162,9 +163,10 @@ def main():
     class Layer:
         """Device inputs, outputs and workspaces of one attention op."""
 
-        def __init__(self, x, C, kind):
+        def __init__(self, x, C, kind, within="iter"):
             self.kind = kind
             self.C = C
+            self.within = within
             self.x = x
             self.Q, self.K, self.V, self.dY = (x[k].to(dev) for k in ("Q", "K", "V", "dY"))
             self.W = x["W"].to(dev)
@@ -175,7 +177,7 @@ def main():
 
         def alloc(self):
             B, H, L, d, M = self.shape
-            p = slim.problem(B, H, L, d, M, self.C, self.Q.dtype, self.kind)
+            p = slim.problem(B, H, L, d, M, self.C, self.Q.dtype, self.kind, within=self.within)
             self.p = p
             self.Y = torch.empty_like(self.Q)
             self.st = torch.empty((B, H, M, d + 1), dtype=torch.float32, device=dev)
@@ -197,11 +199,11 @@ def main():
 
         def fwd(self):
             slim.fwd(self.Q, self.K, self.V, self.W, self.C, self.kind, ws=self.wsf, Y=self.Y, state_out=self.st,
-                     kshift_out=self.ks, ctx=self.ctx)
+                     kshift_out=self.ks, ctx=self.ctx, within=self.within)
 
         def bwd(self, dY=None):
             slim.bwd(self.Q, self.K, self.V, self.W, self.dY if dY is None else dY, self.C, self.ks, self.kind,
-                     ws=self.wsb, dQ=self.dQ, dK=self.dK, dV=self.dV, dW=self.dW, ctx=self.ctx)
+                     ws=self.wsb, dQ=self.dQ, dK=self.dK, dV=self.dV, dW=self.dW, ctx=self.ctx, within=self.within)
 
     def run_step(layers):
         """forward r = 1..n, then backward r = n..1"""
@@ -400,6 +402,28 @@ def main():
             log(f"sweep C={Cs} (block {blk_s}): {rs['ms']:.3f} ms/step, beyond inputs/outputs "
                 f"{rs['extra'] / 2**20:.1f} MiB (L/B {rec['lower_bound_beyond_io_bytes'] / 2**20:.1f} MiB)")
         out["sweep"] = sweep
+        # the same sweep with each slice evaluated as one masked quadratic form
+        # (slices one after another, the slice's tiles in parallel)
+        qsweep = []
+        for Cs in wl.C:
+            ly = Layer(x, Cs, kind, within="quadratic")
+            steps_q = args.sweep_steps if Cs <= 4096 else 2
+            rs = timed([ly], steps_q, 2)
+            algf, algb = flops_per_token_head(d, M, Cs)
+            rec = {"C": Cs, "in_slice_block": Cs, "tokens_per_s": tokens / (rs["ms"] / 1e3), "ms_per_step": rs["ms"],
+                   "steps": steps_q, "bwd_slices_ms": rs["bwd_walk_ms"],
+                   "mfma_frac_algorithmic": (algf + algb) * units / (rs["ms"] / 1e3) / PEAK_BF16_FLOPS,
+                   "peak_bytes": rs["peak"], "beyond_io_bytes": rs["extra"]}
+            if ref is not None:
+                e = parity(ly, sample, ref)
+                rec["grad_l2_rel"] = {k: v["l2_rel"] for k, v in e.items() if k != "Y"}
+                rec["max_rel"] = {k: v["max_rel"] for k, v in e.items()}
+            ly.free()
+            del ly
+            torch.cuda.empty_cache()
+            qsweep.append(rec)
+            log(f"quadratic sweep C={Cs}: {rs['ms']:.3f} ms/step, beyond inputs/outputs {rs['extra'] / 2**20:.1f} MiB")
+        out["sweep_quadratic"] = qsweep
 
     # ------------------------------------------------------------ headline parity and oracle timing
     if not args.no_cpu:
