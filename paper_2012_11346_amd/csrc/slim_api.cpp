@@ -151,20 +151,39 @@ int plan_segments_for(const slim_problem* p, int target) {
   return std::max(1, P);
 }
 bool has_ksum(const slim_problem* p);
+size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
 // segments of the backward (and of slim_num_segments)
 int plan_segments(const slim_problem* p) { return plan_segments_for(p, kTargetWorkgroups); }
 
-// Parts per backward segment for the key-sum pass: the sums are associative,
-// and the pass fits two workgroups per compute unit, so each segment's sum
-// is split in two when that leaves enough tiles per part.
-// SLIM_SUM_SPLIT (debugging) forces 1 or 2.
+// Boundary states of the parts (one state of M (d + 1) floats per part and
+// head) are the exact restarts of the reverse walk's downdates (eq. 17): a
+// part's downdates start from the exact state at its end, so rounding never
+// accumulates over more than one part.  Parts are made as short as this
+// budget over all heads allows (one tile each for short sequences, where no
+// downdate runs at all); beyond it their number per head stays fixed, so
+// memory stays flat in L.
+constexpr size_t kBoundaryBudgetBytes = (size_t)32 << 20;
+
+// Parts per backward segment: the key sums are associative and the pass fits
+// two workgroups per compute unit, so each segment's sum is split in two
+// when that leaves enough tiles per part; and into more parts, down to one
+// tile each, while the boundary states fit kBoundaryBudgetBytes.  Parts
+// hold at least one tile.  SLIM_SUM_SPLIT (debugging) forces a count.
 int plan_sum_split(const slim_problem* p, int P) {
   const char* env = getenv("SLIM_SUM_SPLIT");
   const int n_tiles = count_tiles(p);
-  if (env != nullptr && (atoi(env) == 1 || atoi(env) == 2)) return n_tiles >= 2 * P ? atoi(env) : 1;
-  if (has_ksum(p)) return 2 * P <= std::max(1, n_tiles / kMinTilesPerSegment) ? 2 : 1;
-  const int64_t wgs = p->B * p->H * (int64_t)P;
-  return (n_tiles >= 4 * P && 2 * wgs <= kTargetWorkgroupsForward) ? 2 : 1;
+  const int most = std::max(1, n_tiles / P);  // parts of at least one tile
+  if (env != nullptr && atoi(env) >= 1) return std::min(atoi(env), most);
+  int s2;
+  if (has_ksum(p)) {
+    s2 = 2 * P <= std::max(1, n_tiles / kMinTilesPerSegment) ? 2 : 1;
+  } else {
+    const int64_t wgs = p->B * p->H * (int64_t)P;
+    s2 = (n_tiles >= 4 * P && 2 * wgs <= kTargetWorkgroupsForward) ? 2 : 1;
+  }
+  const size_t per_part = (size_t)p->B * p->H * state_elems(p) * sizeof(float);
+  const int64_t budget_parts = (int64_t)(kBoundaryBudgetBytes / per_part);  // per head, over all segments
+  return std::max(s2, (int)std::min<int64_t>(most, budget_parts / P));
 }
 
 // Segments of the forward.  Problems on the key-sum kernel walk one segment
@@ -191,8 +210,6 @@ int plan_carry_split(const slim_problem* p, int P) {
                                                                 : (int)std::max<int64_t>(1, std::min<int64_t>(4, kTargetWorkgroupsForward / wgs));
   return std::max(1, std::min(cs, per_seg));
 }
-
-size_t state_elems(const slim_problem* p) { return (size_t)p->M * (size_t)(p->d + 1); }
 
 // Parts of the backward's segment boundaries: P segments, each split in S2.
 int bwd_parts(const slim_problem* p) {

@@ -61,10 +61,12 @@ def test_context_is_state_sized_and_flat_in_L(S):
     assert len(set(sizes)) == 1 and sizes[0] > 0
     per_state = 256 * 65 * 4
     assert sizes[0] % (2 * 3 * per_state) == 0
-    # bf16 problems on the key-sum kernel only; fp32 problems and unsegmented
-    # sequences use none
+    # bf16 problems on the key-sum kernel only; fp32 problems and sequences
+    # of one tile (one part, nothing to hand over) use none
     assert S.context_bytes(_p(S, dtype=S.F32, d=32, M=64)) == 0
-    assert S.context_bytes(_p(S, L=64)) == 0
+    assert S.context_bytes(_p(S, L=32)) == 0
+    # short sequences: one part (one exact boundary state) per tile
+    assert S.context_bytes(_p(S, L=64 * 5)) == 2 * 3 * (10 + 1) * per_state
     assert S.context_bytes(_p(S, C=0)) == 0
 
 
