@@ -22,6 +22,11 @@
  * one shift per query row and one shift per (batch, head) shared by all keys;
  * the state is stored relative to the key shift (true state =
  * stored state * exp(kshift)).  The ReLU and square maps use no shifts.
+ * Range: features are formed in float32, so a key whose exponent
+ * w_m . k - |k|^2 / 2 lies more than about 87 below the head's key shift for
+ * every m contributes exactly zero; a row l whose keys l' <= l all do so has
+ * a zero denominator and a non-finite Y_l (and gradients).  Inputs scaled
+ * like attention projections (entries of order d^-1/4) are far from it.
  *
  * Conventions for every entry point:
  *   - Tensors are dense, contiguous, row-major, in device memory:
@@ -87,8 +92,11 @@ typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1 } slim_within;
  *   C        slice length (Sec. 3.2): >= 1; values above L act as L.  The
  *            sequence is cut into N = ceil(L / C) slices, the last one ragged.
  *   dtype    slim_dtype of Q, K, V, Y, dY, dQ, dK, dV.  With SLIM_BF16 every
- *            product runs on bf16 matrix cores with float32 accumulation and
- *            W is rounded to bf16 once; with SLIM_F32 products are float32.
+ *            product runs on bf16 matrix cores with float32 accumulation: W
+ *            enters the logits w_m . x as the pair hi = bf16(w), lo =
+ *            bf16(w - hi) (one product each, about 16 significant bits of
+ *            W) and the chain rule (dq, dk) as hi; with SLIM_F32 products
+ *            are float32.
  *   kind     slim_kind
  *   relu_eps additive constant of the ReLU map (the usual value is 1e-3)
  *   dropout  probability p in [0, 1) of value dropout (0: none), and
@@ -106,7 +114,17 @@ typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1 } slim_within;
  *            sum_l g(K_l) (m_l * V_l)^T (unscaled) in columns 0 .. d-1; dV
  *            is the cotangent of V itself (masked).
  *   within   slim_within: how the slice is evaluated (results agree up to
- *            rounding). */
+ *            rounding).
+ * Work split: each head's sequence is cut into segments walked in parallel
+ * (slim_num_segments) and each segment into parts whose exact boundary
+ * states restart the backward's downdates; the counts are planned for a
+ * device of 256 compute units (MI355X) and depend on B H, never on L once L
+ * is long enough.  Parts are one tile (32 rows) each while their boundary
+ * states fit 32 MiB over all heads.  A downdate subtracts in float32 what
+ * the part's keys added; where a part's early keys have features orders of
+ * magnitude below its later ones, the early states it recovers lose that
+ * much relative precision (eq. 17 itself; the exact restarts bound it to
+ * one part). */
 typedef struct {
   int64_t B, H, L;
   int32_t d, M, C;
@@ -132,7 +150,10 @@ size_t slim_workspace_bytes(const slim_problem* p, int phase);
  * head ([B, H, P2 + 1, M, d + 1] float32: the state B^(n) of eqs. 14-16 at
  * each of the P2 + 1 boundaries of the head's parts, relative to kshift_out).
  * Its size depends on B H and the device, not on L: like the state itself it
- * is flat in the sequence length.  Memory-only query: makes no HIP call. */
+ * is flat in the sequence length.  This is the state hand-off from the
+ * forward to the backward pass beyond B^(N) (state_out) and the key shift
+ * (kshift_out); the quadratic within-slice mode uses none.  Memory-only
+ * query: makes no HIP call. */
 size_t slim_context_bytes(const slim_problem* p);
 
 /* Feature map of Sec. 2.1 (the map g of eq. 2) on its own, for inspection.
@@ -222,8 +243,10 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
  * this host thread records `before` and `after` on its stream immediately
  * around the launch of its main walk kernel (the forward walk that writes Y,
  * the reverse walk of the backward), so the caller can read that kernel's
- * own duration; the other launches of the call fall outside the pair.  The
- * setting is consumed by that one call.  NULL for both clears it.
+ * own duration; the other launches of the call fall outside the pair (in the
+ * quadratic within-slice mode the pair brackets the launches of all
+ * slices).  The setting is consumed by that one call.  NULL for both clears
+ * it.
  * Returns SLIM_OK, or SLIM_EINVAL for an unknown phase or only one NULL. */
 int slim_time_walk(int phase, void* before, void* after);
 

@@ -58,7 +58,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   // time; otherwise they are held in registers.
   constexpr bool LO_TABLE = kSplitW<T> && MT == 4 && SUMS;
   constexpr int MR = LO_TABLE ? 1 : MT;
-  F Wf[MR][EB], Wl[MR][EB];
+  F Wf[MR][EB], Wl[SUMS ? MR : 1][EB];
   if constexpr (!LO_TABLE) {
     const Lane L = this_lane();
 #pragma unroll
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
         for (int s = 0; s < 8; ++s) {
           const float x = a.W[(size_t)(w * FW + 16 * mt + L.c) * D + 32 * kb + kp(L.g, s)];
           Wf[mt][kb][s] = cvt<T>(x);
-          Wl[mt][kb][s] = w_lo<T>(x);
+          if constexpr (SUMS) Wl[mt][kb][s] = w_lo<T>(x);
         }
   }
   typedef WFragLayout<G> WL;
@@ -247,7 +247,9 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
           f32x4 acc = zero4();
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wf[mt][kb]);
-          if constexpr (kSplitW<T>) {
+          // (the maxima take the bf16 W alone: the shift only has to be
+          // near the maximum, any constant cancels)
+          if constexpr (kSplitW<T> && SUMS) {
 #pragma unroll
             for (int kb = 0; kb < EB; ++kb) acc = mma(acc, kf[st][kb], Wl[mt][kb]);
           }
