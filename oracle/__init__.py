@@ -35,3 +35,9 @@ from .dropout import (  # noqa: F401
     philox4x64_10,
     value_mask,
 )
+from .performer import (  # noqa: F401
+    grad_discrepancy,
+    model_algorithm1,
+    model_full,
+    model_loss,
+)

@@ -15,3 +15,4 @@ from .inputs import (  # noqa: F401
     round_to_dtype,
     workload,
 )
+from .model import MODEL_CONFIGS, ModelConfig, make_model, make_tokens  # noqa: F401
