@@ -56,6 +56,17 @@ int ok() {
   return SLIM_OK;
 }
 
+}  // namespace
+
+// error reporting shared with the other entry points of the library
+int slim::report(int status, const char* msg) {
+  if (status == SLIM_OK) g_last_error.clear();
+  else g_last_error = msg;
+  return status;
+}
+
+namespace {
+
 int hip_fail(hipError_t e, const char* what) {
   return fail(SLIM_EHIP, "%s: %s", what, hipGetErrorString(e));
 }

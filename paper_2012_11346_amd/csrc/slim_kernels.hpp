@@ -7,6 +7,10 @@
 
 namespace slim {
 
+// Sets the calling thread's slim_last_error() text (cleared for SLIM_OK)
+// and returns `status`.
+int report(int status, const char* msg);
+
 // Walk modes of the forward kernel
 enum WalkMode {
   kWalkOutputs = 0,  // Y and the final state (forward sweep)

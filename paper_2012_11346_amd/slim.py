@@ -52,6 +52,21 @@ class Problem(ctypes.Structure):
     ]
 
 
+class ModelDesc(ctypes.Structure):
+    """slim_model of include/slim_model.h."""
+
+    _fields_ = [
+        ("B", ctypes.c_int64),
+        ("L", ctypes.c_int64),
+        ("D", ctypes.c_int32),
+        ("s", ctypes.c_int32),
+        ("vocab", ctypes.c_int32),
+        ("F", ctypes.c_int32),
+        ("C", ctypes.c_int32),
+        ("ln_eps", ctypes.c_float),
+    ]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(
@@ -83,6 +98,13 @@ def _load() -> ctypes.CDLL:
     lib.slim_noalloc_scratch_bytes.restype = sz
     lib.slim_fwd_noalloc.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, vp]
     lib.slim_fwd_noalloc.restype = i32
+    MP = ctypes.POINTER(ModelDesc)
+    lib.slim_model_num_params.argtypes = [MP]
+    lib.slim_model_num_params.restype = i32
+    lib.slim_model_workspace_bytes.argtypes = [MP]
+    lib.slim_model_workspace_bytes.restype = sz
+    lib.slim_model_step.argtypes = [MP, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, sz, vp]
+    lib.slim_model_step.restype = i32
     return lib
 
 
@@ -100,6 +122,9 @@ EXPORTED = (
     "slim_time_walk",
     "slim_noalloc_scratch_bytes",
     "slim_fwd_noalloc",
+    "slim_model_num_params",
+    "slim_model_workspace_bytes",
+    "slim_model_step",
 )
 
 
@@ -314,3 +339,58 @@ def fwd_noalloc(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None
     _check(LIB.slim_fwd_noalloc(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in),
                                 _ptr(kshift_in), _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _stream()))
     return Y, state_out, kshift_out
+
+
+# ---------------------------------------------------------------- the s-layer model (include/slim_model.h)
+
+
+def model_param_names(s: int):
+    """Parameter order of slim_model_step."""
+    names = ["emb"]
+    for r in range(s):
+        names += [f"{n}{r}" for n in ("Wq", "Wk", "Wv", "ln1_g", "ln1_b", "W1", "b1", "W2", "b2", "ln2_g", "ln2_b")]
+    return names + ["Wout", "bout"]
+
+
+def model_desc(B, L, D, s, vocab, F, C, ln_eps=1e-5) -> ModelDesc:
+    return ModelDesc(int(B), int(L), int(D), int(s), int(vocab), int(F), int(C), float(ln_eps))
+
+
+def model_workspace_bytes(m: ModelDesc) -> int:
+    return int(LIB.slim_model_workspace_bytes(ctypes.byref(m)))
+
+
+def model_step(params: dict, tokens, C: int, ln_eps: float = 1e-5, ws=None, grads=None, loss=None):
+    """Loss and gradient of the s-layer Performer language model by
+    Algorithm 1 (include/slim_model.h).  params: float32 device tensors keyed
+    by model_param_names(s); tokens: int32 [B, L].  Returns (loss [1],
+    grads dict)."""
+    s = sum(1 for k in params if k.startswith("Wq"))
+    names = model_param_names(s)
+    emb = params["emb"]
+    vocab, D = emb.shape
+    F = params["W10"].shape[1]
+    if tokens.dim() == 1:
+        tokens = tokens[None]
+    B, L = tokens.shape
+    m = model_desc(B, L, D, s, vocab, F, C, ln_eps)
+    _need(tokens, "tokens", torch.int32, (B, L))
+    dev = emb.device
+    for n in names:
+        t = params[n]
+        if t.dtype != torch.float32 or not t.is_contiguous() or t.device != dev:
+            raise ValueError(f"{n} must be a contiguous float32 tensor on {dev}")
+    if grads is None:
+        grads = {n: torch.empty_like(params[n]) for n in names}
+    for n in names:
+        _need(grads[n], f"grad {n}", torch.float32, tuple(params[n].shape))
+    loss = torch.empty(1, dtype=torch.float32, device=dev) if loss is None else loss
+    need = model_workspace_bytes(m)
+    if need == 0:
+        raise SlimError(SLIM_EINVAL, LIB.slim_last_error().decode())
+    if ws is None or ws.numel() * ws.element_size() < need:
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    P = (ctypes.c_void_p * len(names))(*[params[n].data_ptr() for n in names])
+    G = (ctypes.c_void_p * len(names))(*[grads[n].data_ptr() for n in names])
+    _check(LIB.slim_model_step(ctypes.byref(m), _ptr(tokens), P, G, _ptr(loss), _ptr(ws), _nbytes(ws), _stream()))
+    return loss, grads

@@ -1,4 +1,4 @@
-"""The C ABI library loads, exports what include/slim.h declares, and rejects
+"""The C ABI library loads, exports what include/*.h declare, and rejects
 bad arguments on the host with the documented status codes (no GPU needed:
 validation happens before any HIP call)."""
 
@@ -9,13 +9,15 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "slim.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include"))) if h.endswith(".h")]
 
 
 def _declared():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(slim_[a-z_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(slim_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -172,3 +174,52 @@ def test_walk_timer_arguments(S):
     assert S.LIB.slim_time_walk(S.PHASE_BWD, ev, None) == S.SLIM_EINVAL
     assert S.LIB.slim_time_walk(S.PHASE_FWD, None, None) == S.SLIM_OK
     assert S.LIB.slim_time_walk(S.PHASE_BWD, None, None) == S.SLIM_OK
+
+
+# ---------------------------------------------------------------- the model step (include/slim_model.h)
+
+
+def _m(S, **kw):
+    base = dict(B=1, L=16384, D=1024, s=3, vocab=256, F=4096, C=512)
+    base.update(kw)
+    return S.model_desc(**base)
+
+
+def test_model_workspace_grows_with_C_not_L(S):
+    ws = [S.model_workspace_bytes(_m(S, L=L)) for L in (16384, 65536, 1 << 20)]
+    assert ws[0] > 0 and len(set(ws)) == 1
+    # the activations of one slice scale with C
+    w1, w2 = S.model_workspace_bytes(_m(S, C=512)), S.model_workspace_bytes(_m(S, C=1024))
+    assert 1.8 * w1 < w2 < 2.2 * w1
+    assert S.LIB.slim_model_num_params(ctypes.byref(_m(S))) == 11 * 3 + 3
+    assert S.LIB.slim_model_num_params(None) == 0
+
+
+@pytest.mark.parametrize(
+    "kw",
+    [dict(D=96), dict(D=0), dict(D=8192), dict(vocab=1), dict(vocab=70000), dict(F=6), dict(C=0), dict(L=1),
+     dict(s=0), dict(B=0), dict(ln_eps=0.0)],
+)
+def test_invalid_models_are_rejected(S, kw):
+    m = _m(S, **kw)
+    assert S.model_workspace_bytes(m) == 0
+    n = S.LIB.slim_model_num_params(ctypes.byref(m))
+    arr = (ctypes.c_void_p * max(n, 1))(*([A] * max(n, 1)))
+    st = S.LIB.slim_model_step(ctypes.byref(m), A, arr, arr, A, A, 1 << 40, None)
+    assert st in (S.SLIM_EINVAL, S.SLIM_EUNSUPPORTED)
+
+
+def test_model_step_checks_pointers_and_workspace(S):
+    m = _m(S, L=64, C=16)
+    n = S.LIB.slim_model_num_params(ctypes.byref(m))
+    arr = (ctypes.c_void_p * n)(*([A] * n))
+    need = S.model_workspace_bytes(m)
+    st = S.LIB.slim_model_step(ctypes.byref(m), None, arr, arr, A, A, need, None)
+    assert st == S.SLIM_EINVAL
+    holed = (ctypes.c_void_p * n)(*([A] * (n - 1) + [None]))
+    st = S.LIB.slim_model_step(ctypes.byref(m), A, arr, holed, A, A, need, None)
+    assert st == S.SLIM_EINVAL
+    st = S.LIB.slim_model_step(ctypes.byref(m), A, arr, arr, A, A, need - 1, None)
+    assert st == S.SLIM_EWORKSPACE
+    st = S.LIB.slim_model_step(ctypes.byref(m), A, arr, arr, A, A + 16, need, None)
+    assert st == S.SLIM_EINVAL  # not 256-byte aligned

@@ -1,0 +1,129 @@
+"""The s-layer Performer language model trained by Algorithm 1
+(include/slim_model.h) on the GPU against the fp64 oracle's whole-sequence
+evaluation (eqs. 5-10), on seeded random models and byte strings.
+
+* loss and every parameter gradient for several slice lengths C, ragged last
+  slices, C = 1 (the extreme of Sec. 3.3) and C >= L (one slice);
+* the result does not depend on C (Sec. 3.3): the relative gradient
+  discrepancy between C and C = L on the GPU (the measure of Sec. 4.1);
+* determinism (no atomics): two calls give the same bits;
+* tokens outside the alphabet give a NaN loss instead of a fault.
+
+The bars are float32 ones: the step runs entirely in float32 (GEMMs on the
+float32 matrix cores, layer normalisation, GeLU, cross-entropy, the
+attention of the library), and each layer's attention state is recovered by
+the eq. 17 subtraction, so the error grows with the number of slices.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import ModelConfig, make_model, make_tokens
+from tests.gpu_common import host64, max_rel, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+# (config, slice lengths)
+CASES = [
+    (ModelConfig("tiny", L=37, D=64, s=2, vocab=11, B=2), [1, 5, 16, 37, 100]),
+    (ModelConfig("heads2", L=70, D=128, s=3, vocab=256, B=1), [7, 32, 70]),
+    (ModelConfig("short", L=2, D=64, s=1, vocab=5, B=3), [1, 2]),
+    (ModelConfig("wide", L=130, D=192, s=2, vocab=300, B=2), [64, 33]),
+]
+
+LOSS_TOL = 2e-5  # relative
+L2_TOL = 2e-5  # ||g - g_ref|| / ||g_ref|| over all parameters (Sec. 4.1)
+TENSOR_TOL = 2e-4  # per-tensor max|g - g_ref| / max(max|g_ref|, FLOOR * largest gradient entry)
+FLOOR = 1e-3
+
+_ORACLE = {}
+
+
+def _model(cfg, seed=0):
+    P = make_model(cfg, seed=seed, perturb_ln=True)
+    tok = make_tokens(cfg, seed=seed)
+    return P, tok
+
+
+def _oracle(cfg):
+    if cfg.name not in _ORACLE:
+        P, tok = _model(cfg)
+        _ORACLE[cfg.name] = oracle.model_full(P, tok)
+    return _ORACLE[cfg.name]
+
+
+def _gpu(cfg, C, tok=None):
+    from paper_2012_11346_amd import slim
+
+    P, t = _model(cfg)
+    if tok is not None:
+        t = tok
+    Pd = {k: v.cuda() for k, v in P.items()}
+    loss, g = slim.model_step(Pd, t.cuda(), C)
+    torch.cuda.synchronize()
+    return float(loss.item()), {k: host64(v) for k, v in g.items()}
+
+
+@pytest.mark.parametrize("cfg, C", [(cfg, C) for cfg, Cs in CASES for C in Cs], ids=lambda x: getattr(x, "name", x))
+def test_step_matches_the_whole_sequence(cfg, C):
+    need_gpu()
+    print(f"[model] cfg={cfg} C={C}", flush=True)
+    ref_loss, ref = _oracle(cfg)
+    loss, g = _gpu(cfg, C)
+    el = abs(loss - ref_loss) / abs(ref_loss)
+    disc = oracle.grad_discrepancy(g, ref)
+    worst = max((max_rel(g[k], ref[k]), k) for k in ref)
+    print(f"  loss {loss:.7f} ref {ref_loss:.7f} rel {el:.2e}; discrepancy {disc:.2e}; worst {worst[1]} {worst[0]:.2e}",
+          flush=True)
+    assert el <= LOSS_TOL
+    assert disc <= L2_TOL
+    gmax = max(float(np.max(np.abs(ref[k]))) for k in ref)
+    for k in ref:
+        assert np.all(np.isfinite(g[k])), k
+        err = float(np.max(np.abs(g[k] - ref[k])))
+        scale = max(float(np.max(np.abs(ref[k]))), FLOOR * gmax)
+        assert err <= TENSOR_TOL * scale, (k, err, scale)
+    if cfg.L == 2:
+        # the only row that predicts sees one key: its attention output is
+        # v_0 whatever q_0 and k_0 are (eq. 2 normalises one term), so the
+        # query and key weights get no gradient
+        for r in range(cfg.s):
+            for n in ("Wq", "Wk"):
+                assert np.max(np.abs(ref[f"{n}{r}"])) <= 1e-12 * gmax
+                assert np.max(np.abs(g[f"{n}{r}"])) <= 1e-6 * gmax, n
+
+
+@pytest.mark.parametrize("C", [1, 4, 13])
+def test_gradient_does_not_depend_on_C(C):
+    need_gpu()
+    cfg = CASES[0][0]
+    print(f"[model] C-invariance cfg={cfg.name} C={C} vs C={cfg.L}", flush=True)
+    _, gL = _gpu(cfg, cfg.L)
+    _, gC = _gpu(cfg, C)
+    disc = oracle.grad_discrepancy(gC, gL)
+    print(f"  discrepancy {disc:.2e}", flush=True)
+    assert disc <= L2_TOL
+
+
+def test_deterministic():
+    need_gpu()
+    cfg = CASES[1][0]
+    print(f"[model] determinism cfg={cfg.name}", flush=True)
+    l1, g1 = _gpu(cfg, 7)
+    l2, g2 = _gpu(cfg, 7)
+    assert l1 == l2
+    for k in g1:
+        assert np.array_equal(g1[k], g2[k]), k
+
+
+def test_token_outside_the_alphabet_gives_nan():
+    need_gpu()
+    cfg = CASES[0][0]
+    print(f"[model] bad token cfg={cfg.name}", flush=True)
+    _, tok = _model(cfg)
+    tok = tok.clone()
+    tok[1, 20] = cfg.vocab  # one past the alphabet
+    loss, g = _gpu(cfg, 5, tok=tok)
+    assert np.isnan(loss)
