@@ -121,6 +121,12 @@ def main():
     ap.add_argument("--no-configs", action="store_true", help="skip the other workloads and memory-vs-L")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing and the parity checks")
     ap.add_argument("--quick", action="store_true", help="headline only (= --no-sweep --no-configs --no-cpu)")
+    ap.add_argument("--no-model", action="store_true", help="skip the s-layer language model (Algorithm 1 over eqs. 5-10)")
+    ap.add_argument("--model-only", action="store_true", help="only the s-layer language model section")
+    ap.add_argument("--model-seeds", type=int, default=1, help="seeds of the model's gradient discrepancy")
+    ap.add_argument("--model-configs", default="I,II,III,IV", help="model configurations to run (comma list)")
+    ap.add_argument("--model-C", default="", help="slice lengths of the model section (comma list; default "
+                    "64, 256, 1024, 4096 below L, and L)")
     ap.add_argument("--sweep-steps", type=int, default=5)
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only copy a device buffer of this many MiB (calibration of memory counters) and exit")
@@ -308,6 +314,10 @@ def main():
         torch.cuda.synchronize()
         out["dW"] = rel_errors(h64(layer.dW), ref["dW"])
         return out
+
+    if args.model_only:
+        print(json.dumps({"model": model_section(args, dev, log)}), flush=True)
+        return
 
     # ------------------------------------------------------------ headline
     wl = workload("sweep_32k")
@@ -534,7 +544,116 @@ def main():
         out["square_paper_shapes"] = sq
         log("square map: " + ", ".join(f"L={s['L']} H={s['H']}: {s['tokens_per_s']:.3e} tok/s" for s in sq))
 
+    if not args.no_model:
+        out["model"] = model_section(args, dev, log)
+
     print(json.dumps(out), flush=True)
+
+
+def model_flops(cfg, C):
+    """Algorithmic flops of one step of Algorithm 1 over the model (2 per
+    multiply-add): the forward, and in the backward the recomputation plus
+    twice the forward's products, so four times the forward's GEMMs
+    (Q/K/V, FFN, logits) and, per head, the attention's forward three times
+    (forward, the slice's own sum, recomputation) and its backward once, with
+    the in-slice block of TILE_ROWS rows the attention kernels execute."""
+    D, F, V, s, L, B = cfg.D, cfg.F, cfg.vocab, cfg.s, cfg.L, cfg.B
+    gemm = 2 * (3 * D * D + 2 * D * F) * s + 2 * D * V
+    af, ab = flops_per_token_head(64, 64, min(C, L, TILE_ROWS))
+    return B * L * (4 * gemm + s * cfg.k * (3 * af + ab))
+
+
+def model_section(args, dev, log):
+    """The paper's language-model experiment (Sec. 4, configurations I-IV:
+    s = 3 layers, d_ff = 4 d_model, 256-symbol alphabet, B = 1, random
+    initialisation, random byte strings): time and device memory of one
+    step of Algorithm 1 per slice length C, the lower bound "L/B" (the same
+    step on an input of length C), and the relative gradient discrepancy
+    ||g_C - g_full|| / ||g_full|| against the one-slice step (C = L) and,
+    where the host can afford it, against the fp64 oracle."""
+    import numpy as np
+    import torch
+
+    from paper_2012_11346_amd import slim
+    from synth import MODEL_CONFIGS, make_model, make_tokens
+
+    stream = torch.cuda.current_stream()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(cfg, P, tok, C, steps, warmup):
+        """median-free timing: warmup, then `steps` steps between two events;
+        returns (ms, peak bytes beyond parameters/gradients/tokens, workspace
+        bytes, loss, grads)"""
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        pre = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        m = slim.model_desc(cfg.B, tok.shape[1], cfg.D, cfg.s, cfg.vocab, cfg.F, C)
+        ws = torch.empty(slim.model_workspace_bytes(m), dtype=torch.uint8, device=dev)
+        grads = {k: torch.empty_like(v) for k, v in P.items()}
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        io = sum(g.numel() * 4 for g in grads.values()) + 4
+        for _ in range(warmup):
+            slim.model_step(P, tok, C, ws=ws, grads=grads, loss=loss)
+        a, b = mk(), mk()
+        a.record(stream)
+        for _ in range(steps):
+            slim.model_step(P, tok, C, ws=ws, grads=grads, loss=loss)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        extra = torch.cuda.max_memory_allocated() - pre - io
+        return ms, extra, ws.numel(), float(loss.item()), grads
+
+    def disc(g, ref):
+        num = sum(float(torch.sum((g[k].double() - ref[k].double()) ** 2)) for k in ref)
+        den = sum(float(torch.sum(ref[k].double() ** 2)) for k in ref)
+        return (num / den) ** 0.5
+
+    rows = []
+    for name in args.model_configs.split(","):
+        cfg = MODEL_CONFIGS[name]
+        Cs = [c for c in (64, 256, 1024, 4096) if c < cfg.L] + [cfg.L]
+        if args.model_C:
+            Cs = sorted({min(int(c), cfg.L) for c in args.model_C.split(",")} | {cfg.L})
+        steps = 5 if cfg.L * cfg.D <= (1 << 22) else 2
+        for seed in range(args.model_seeds):
+            P = {k: v.to(dev) for k, v in make_model(cfg, seed=seed).items()}
+            tok = make_tokens(cfg, seed=seed).to(dev)
+            ms_f, ex_f, ws_f, loss_f, g_full = step(cfg, P, tok, cfg.L, steps, 1)
+            g_full = {k: v.clone() for k, v in g_full.items()}
+            ref64 = None
+            if cfg.L * cfg.D <= (1 << 19) and not args.no_cpu:
+                import oracle as O
+
+                t0 = time.perf_counter()
+                lo, go = O.model_full({k: v.cpu() for k, v in P.items()}, tok.cpu())
+                ref64 = {k: torch.from_numpy(v) for k, v in go.items()}
+                log(f"model {name}: fp64 oracle in {time.perf_counter() - t0:.1f}s")
+            for C in Cs:
+                ms, extra, wsb, loss, g = (ms_f, ex_f, ws_f, loss_f, g_full) if C == cfg.L else step(cfg, P, tok, C, steps, 1)
+                rec = {"config": name, "L": cfg.L, "d_model": cfg.D, "s": cfg.s, "heads": cfg.k, "d_ff": cfg.F,
+                       "vocab": cfg.vocab, "B": cfg.B, "C": C, "seed": seed, "loss": loss,
+                       "grad_discrepancy_vs_C_eq_L": disc(g, g_full)}
+                if ref64 is not None:
+                    rec["grad_discrepancy_vs_fp64_oracle"] = disc({k: v.cpu() for k, v in g.items()}, ref64)
+                if seed == 0:
+                    fl = model_flops(cfg, C)
+                    rec.update(ms_per_step=ms, tokens_per_s=cfg.B * cfg.L / (ms / 1e3), flops=fl,
+                               fp32_frac=fl / (ms / 1e3) / PEAK_FP32_FLOPS, beyond_io_bytes=extra, workspace_bytes=wsb)
+                    if C < cfg.L:  # lower bound "L/B": the same step on an input of length C
+                        _, lb, _, _, _ = step(cfg, P, tok[:, :C].contiguous(), C, 1, 1)
+                        rec["lower_bound_beyond_io_bytes"] = lb
+                rows.append(rec)
+                log(f"model {name} C={C} seed={seed}: " + (f"{ms:.2f} ms/step, " if seed == 0 else "")
+                    + f"discrepancy {rec['grad_discrepancy_vs_C_eq_L']:.2e}"
+                    + (f" (fp64: {rec['grad_discrepancy_vs_fp64_oracle']:.2e})" if ref64 is not None else "")
+                    + (f", beyond io {extra / 2**20:.0f} MiB" if seed == 0 else ""))
+            del P, tok, g_full, ref64
+            torch.cuda.empty_cache()
+    return {"workload": "s-layer Performer language model (square map, M = d = 64), float32, Algorithm 1; "
+                        "configurations I-IV (L, d_model) = (512, 256), (1024, 512), (4096, 1024), (16384, 1024)",
+            "rows": rows}
 
 
 if __name__ == "__main__":

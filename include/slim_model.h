@@ -31,7 +31,8 @@
  * with C and not with L.
  *
  * Everything is float32.  Matrix products run on the float32 matrix cores
- * in the library's own kernels; every call is asynchronous on `stream`; the
+ * in the library's own kernels (long reductions split over workgroups and
+ * summed in a fixed order); every call is asynchronous on `stream`; the
  * library allocates nothing; results are deterministic (fixed summation
  * orders, no atomics).
  */
@@ -51,7 +52,7 @@ extern "C" {
  *   s       layers (>= 1)
  *   vocab   alphabet size (2 .. 65536)
  *   F       d_ff (the paper uses 4 D): a multiple of 4
- *   C       slice length (>= 1; values above L act as L)
+ *   C       slice length (>= 1; values above L act as L; B * min(C, L) <= 2^22)
  *   ln_eps  layer-normalisation epsilon (the usual value is 1e-5) */
 typedef struct {
   int64_t B, L;

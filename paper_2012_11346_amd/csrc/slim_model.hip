@@ -12,10 +12,12 @@
 // through all layers, and back-propagates through it with the state
 // cotangents G_r carried from the later slices (eq. 18).
 //
-// Kernels here: a float32 matrix-core GEMM (v_mfma_f32_16x16x4_f32, 64 x 64
-// tiles), row-wise layer normalisation and its backward, bias + GeLU,
-// cross-entropy, the embedding and its deterministic backward, head
-// split/merge copies and fixed-order column sums.
+// Kernels here: a float32 matrix-core GEMM (v_mfma_f32_16x16x4_f32, 128 x 128
+// and 64 x 128 tiles, split K with a fixed-order reduction, epilogues for
+// bias, bias + GeLU, GeLU's derivative and residual sums), row-wise layer
+// normalisation and its backward, cross-entropy, the embedding and its
+// deterministic backward, head split/merge copies and fixed-order column
+// sums.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -34,97 +36,286 @@ namespace model {
 typedef float f4 __attribute__((ext_vector_type(4)));
 constexpr int kHead = 64;  // head dimension (d = M = 64)
 
-// ---------------------------------------------------------------- GEMM
-// C = alpha op(A) op(B) + beta C, row-major: op(A)[m][k] = TA ? A[k lda + m]
-// : A[m lda + k], op(B)[k][n] = TB ? B[n ldb + k] : B[k ldb + n].  One
-// workgroup per 64 x 64 tile of C; four waves of 32 x 32, each 2 x 2 matrix
-// tiles of 16 x 16; K in steps of 16 through LDS ([k][m] and [k][n], rows
-// padded so that the four k rows a product reads fall in distinct banks).
-constexpr int GT = 64, GK = 16, GLD = GT + 16;
+__device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+__device__ __forceinline__ float gelu_d(float x) {
+  return 0.5f * (1.f + erff(x * 0.70710678118654752f)) + x * expf(-0.5f * x * x) * 0.39894228040143268f;
+}
 
-template <bool TA, bool TB>
-__global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, float alpha, const float* __restrict__ A,
-                                                   int lda, const float* __restrict__ B, int ldb, float beta,
-                                                   float* __restrict__ C, int ldc) {
-  __shared__ float As[GK][GLD];
-  __shared__ float Bs[GK][GLD];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
-  const int wm = (w >> 1) * 32, wn = (w & 1) * 32;
-  f4 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < K; k0 += GK) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = tid + 256 * i;
-      int m, ka;
-      if (TA) {
-        m = e % GT;
-        ka = e / GT;
-      } else {
-        ka = e % GK;
-        m = e / GK;
-      }
-      const int gm = m0 + m, gka = k0 + ka;
-      float v = 0.f;
-      if (gm < M && gka < K) v = TA ? A[(size_t)gka * lda + gm] : A[(size_t)gm * lda + gka];
-      As[ka][m] = v;
-      int n, kb;
-      if (TB) {
-        kb = e % GK;
-        n = e / GK;
-      } else {
-        n = e % GT;
-        kb = e / GT;
-      }
-      const int gn = n0 + n, gkb = k0 + kb;
-      float u = 0.f;
-      if (gn < N && gkb < K) u = TB ? B[(size_t)gn * ldb + gkb] : B[(size_t)gkb * ldb + gn];
-      Bs[kb][n] = u;
+// ---------------------------------------------------------------- GEMM
+// C = epilogue(op(A) op(B)), row-major: op(A)[m][k] = TA ? A[k lda + m] :
+// A[m lda + k], op(B)[k][n] = TB ? B[n ldb + k] : B[k ldb + n].
+//
+// Workgroup tile BM x 128 (BM = 128 or 64), four waves in 2 x 2, each wave
+// (BM / 2) x 64 as (BM / 32) x 4 matrix tiles of 16 x 16 on
+// v_mfma_f32_16x16x4_f32.  K runs in tiles of 16 through double-buffered
+// LDS held [m][k] and [n][k] (rows padded to 20 floats): the summation index
+// of the four products of one k tile is permuted so that lane group g
+// (lane / 16) takes k = 4 g + j in product j, and one 16-byte LDS read then
+// feeds four products.  Global loads are 16-byte vectors where the strides
+// allow, prefetched one k tile ahead.  Long K is split over blockIdx.y; the
+// partial products are summed in a fixed order by gemm_reduce_kernel, which
+// then applies the epilogue (no atomics: results are reproducible).
+constexpr int GBN = 128, GBK = 16, GKP = GBK + 4;
+
+enum EpiOp { EPI_STORE = 0, EPI_ACC = 1, EPI_BIAS = 2, EPI_BIAS_GELU = 3, EPI_GELU_BWD = 4, EPI_ADD = 5 };
+// STORE: C = v; ACC: C += v; BIAS: C = v + bias[n]; BIAS_GELU: C = z = v +
+// bias[n], C2 = GeLU(z); GELU_BWD: C = v GeLU'(aux); ADD: C = v + aux.
+// aux and C2 share C's leading dimension.
+struct Epi {
+  int op;
+  const float* bias;
+  const float* aux;
+  float* C2;
+};
+
+__device__ __forceinline__ void epi_store(const Epi& e, float* C, int ldc, int m, int n, float v) {
+  const size_t o = (size_t)m * ldc + n;
+  switch (e.op) {
+    case EPI_STORE: C[o] = v; break;
+    case EPI_ACC: C[o] += v; break;
+    case EPI_BIAS: C[o] = v + e.bias[n]; break;
+    case EPI_BIAS_GELU: {
+      const float z = v + e.bias[n];
+      C[o] = z;
+      e.C2[o] = gelu_f(z);
+      break;
     }
-    __syncthreads();
-    const int c = lane & 15, g = lane >> 4;
-#pragma unroll
-    for (int ks = 0; ks < GK; ks += 4) {
-      float a[2], b[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = As[ks + g][wm + 16 * i + c];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = Bs[ks + g][wn + 16 * j + c];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    __syncthreads();
+    case EPI_GELU_BWD: C[o] = v * gelu_d(e.aux[o]); break;
+    default: C[o] = v + e.aux[o]; break;
   }
-  const int c = lane & 15, g = lane >> 4;
+}
+
+struct GemmArgs {
+  int M, N, K;
+  const float* A;
+  int lda;
+  const float* B;
+  int ldb;
+  float* C;
+  int ldc;
+  Epi epi;
+  int kchunk;   // k per split (a multiple of GBK)
+  float* part;  // [splits][M][N] partial products when gridDim.y > 1
+  int tiles_n;
+};
+
+// four consecutive floats, `avail` of them valid (zeros beyond)
+template <bool VEC>
+__device__ __forceinline__ float4 ld4(const float* p, int avail) {
+  if (VEC && avail >= 4) return *reinterpret_cast<const float4*>(p);
+  float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (avail > 0) r.x = p[0];
+  if (avail > 1) r.y = p[1];
+  if (avail > 2) r.z = p[2];
+  if (avail > 3) r.w = p[3];
+  return r;
+}
+
+template <int BM, bool TA, bool TB, bool VEC>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
+  constexpr int AV = BM * GBK / 4 / 256;  // float4 loads per thread per k tile (A)
+  constexpr int BV = GBN * GBK / 4 / 256;  // (B)
+  constexpr int TI = BM / 32;              // matrix tiles per wave along m
+  __shared__ __align__(16) float As[2][BM][GKP];
+  __shared__ __align__(16) float Bs[2][GBN][GKP];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // XCD-aware order: consecutive tiles (sharing rows of A) on one XCD
+  int tile = blockIdx.x;
+  const int nt = gridDim.x;
+  if ((nt & 7) == 0) tile = (tile & 7) * (nt >> 3) + (tile >> 3);
+  const int m0 = (tile / g.tiles_n) * BM, n0 = (tile % g.tiles_n) * GBN;
+  const int kbeg = blockIdx.y * g.kchunk, kend = min(g.K, kbeg + g.kchunk);
+  const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * 64;
+  const int M = g.M, N = g.N;
+
+  float4 ra[AV], rb[BV];
+  auto load = [&](int k0) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < AV; ++i) {
+      const int f = tid + 256 * i;
+      if (!TA) {  // rows of A: 4 k per vector
+        const int m = f >> 2, k = k0 + 4 * (f & 3);
+        ra[i] = (m0 + m < M) ? ld4<VEC>(g.A + (size_t)(m0 + m) * g.lda + k, kend - k) : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {  // rows of A^T: 4 m per vector
+        const int k = k0 + f / (BM / 4), m = m0 + 4 * (f % (BM / 4));
+        ra[i] = (k < kend) ? ld4<VEC>(g.A + (size_t)k * g.lda + m, M - m) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int i = 0; i < BV; ++i) {
+      const int f = tid + 256 * i;
+      if (TB) {  // rows of B^T: 4 k per vector
+        const int n = f >> 2, k = k0 + 4 * (f & 3);
+        rb[i] = (n0 + n < N) ? ld4<VEC>(g.B + (size_t)(n0 + n) * g.ldb + k, kend - k) : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {  // rows of B: 4 n per vector
+        const int k = k0 + f / (GBN / 4), n = n0 + 4 * (f % (GBN / 4));
+        rb[i] = (k < kend) ? ld4<VEC>(g.B + (size_t)k * g.ldb + n, N - n) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int f = tid + 256 * i;
+      if (!TA) {
+        *reinterpret_cast<float4*>(&As[buf][f >> 2][4 * (f & 3)]) = ra[i];
+      } else {
+        const int k = f / (BM / 4), m = 4 * (f % (BM / 4));
+        As[buf][m][k] = ra[i].x;
+        As[buf][m + 1][k] = ra[i].y;
+        As[buf][m + 2][k] = ra[i].z;
+        As[buf][m + 3][k] = ra[i].w;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < BV; ++i) {
+      const int f = tid + 256 * i;
+      if (TB) {
+        *reinterpret_cast<float4*>(&Bs[buf][f >> 2][4 * (f & 3)]) = rb[i];
+      } else {
+        const int k = f / (GBN / 4), n = 4 * (f % (GBN / 4));
+        Bs[buf][n][k] = rb[i].x;
+        Bs[buf][n + 1][k] = rb[i].y;
+        Bs[buf][n + 2][k] = rb[i].z;
+        Bs[buf][n + 3][k] = rb[i].w;
+      }
+    }
+  };
+
+  f4 acc[TI][4];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  const int c = lane & 15, q = lane >> 4;
+  int buf = 0;
+  if (kbeg < kend) {
+    load(kbeg);
+    store(0);
+  }
+  __syncthreads();
+  for (int k0 = kbeg; k0 < kend; k0 += GBK) {
+    const bool more = k0 + GBK < kend;
+    if (more) load(k0 + GBK);
+    float4 a[TI], b[4];
+#pragma unroll
+    for (int i = 0; i < TI; ++i) a[i] = *reinterpret_cast<const float4*>(&As[buf][wm + 16 * i + c][4 * q]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const float4*>(&Bs[buf][wn + 16 * j + c][4 * q]);
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[i][j], 0, 0, 0);
+      }
+    if (more) store(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+  const bool split = gridDim.y > 1;
+  float* part = g.part + (size_t)blockIdx.y * M * N;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm + 16 * i + 4 * g + r, col = n0 + wn + 16 * j + c;
-        if (row < M && col < N) {
-          float* p = C + (size_t)row * ldc + col;
-          *p = beta != 0.f ? alpha * acc[i][j][r] + beta * *p : alpha * acc[i][j][r];
+        const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
+        if (m < M && n < N) {
+          if (split) part[(size_t)m * N + n] = acc[i][j][r];
+          else epi_store(g.epi, g.C, g.ldc, m, n, acc[i][j][r]);
         }
       }
 }
 
-hipError_t gemm(bool ta, bool tb, int M, int N, int K, float alpha, const float* A, int lda, const float* B, int ldb,
-                float beta, float* C, int ldc, hipStream_t s) {
+// C = epilogue(sum over splits of the partial products, in split order)
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* part, int splits, int M, int N, float* C, int ldc,
+                                                          Epi epi) {
+  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x, MN = (size_t)M * N;
+  if (e >= MN) return;
+  float v = 0.f;
+  for (int s = 0; s < splits; ++s) v += part[s * MN + e];
+  epi_store(epi, C, ldc, (int)(e / N), (int)(e % N), v);
+}
+
+// Launch plan of one product: tile height, k per split and split count.
+struct GemmPlan {
+  int BM, kchunk, splits, tiles_n, tiles;
+};
+inline GemmPlan gemm_plan(int M, int N, int K) {
+  GemmPlan p;
+  p.tiles_n = (N + GBN - 1) / GBN;
+  const int t128 = ((M + 127) / 128) * p.tiles_n;
+  p.BM = t128 >= 256 ? 128 : 64;
+  p.tiles = ((M + p.BM - 1) / p.BM) * p.tiles_n;
+  const int kt = (K + GBK - 1) / GBK;
+  int s = 1;
+  // split long K until about 512 workgroups run, keeping >= 8 k tiles each
+  while (p.tiles * s < 512 && kt >= 16 * s && s < 64) s *= 2;  // next split keeps >= 8 k tiles
+  const int per = std::max(1, (kt + s - 1) / s);
+  p.kchunk = per * GBK;
+  p.splits = (kt + per - 1) / per;
+  return p;
+}
+inline size_t gemm_part_bytes(int M, int N, int K) {
+  const GemmPlan p = gemm_plan(M, N, K);
+  return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
+}
+
+template <int BM, bool TA, bool TB>
+void gemm_launch(const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
+  if (vec) hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, true>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, false>), grid, dim3(256), 0, s, a);
+}
+template <int BM>
+void gemm_launch(bool ta, bool tb, const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
+  if (ta && tb) gemm_launch<BM, true, true>(a, grid, vec, s);
+  else if (ta) gemm_launch<BM, true, false>(a, grid, vec, s);
+  else if (tb) gemm_launch<BM, false, true>(a, grid, vec, s);
+  else gemm_launch<BM, false, false>(a, grid, vec, s);
+}
+
+// part: workspace for the partial products (gemm_part_bytes of the shape)
+hipError_t gemm(bool ta, bool tb, int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
+                int ldc, Epi epi, float* part, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  const dim3 grid((N + GT - 1) / GT, (M + GT - 1) / GT);
-  if (ta && tb) hipLaunchKernelGGL((gemm_kernel<true, true>), grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc);
-  else if (ta) hipLaunchKernelGGL((gemm_kernel<true, false>), grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc);
-  else if (tb) hipLaunchKernelGGL((gemm_kernel<false, true>), grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc);
-  else hipLaunchKernelGGL((gemm_kernel<false, false>), grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc);
+  const GemmPlan p = gemm_plan(M, N, K);
+  GemmArgs a;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.A = A;
+  a.lda = lda;
+  a.B = B;
+  a.ldb = ldb;
+  a.C = C;
+  a.ldc = ldc;
+  a.epi = epi;
+  a.kchunk = p.kchunk;
+  a.part = part;
+  a.tiles_n = p.tiles_n;
+  const bool vec = lda % 4 == 0 && ldb % 4 == 0 && ((uintptr_t)A & 15) == 0 && ((uintptr_t)B & 15) == 0;
+  const dim3 grid(p.tiles, p.splits);
+  if (p.BM == 128) gemm_launch<128>(ta, tb, a, grid, vec, s);
+  else gemm_launch<64>(ta, tb, a, grid, vec, s);
+  if (p.splits > 1) {
+    const size_t MN = (size_t)M * N;
+    hipLaunchKernelGGL(gemm_reduce_kernel, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, p.splits, M, N, C,
+                       ldc, epi);
+  }
   return hipGetLastError();
+}
+
+inline Epi epi(int op, const float* bias = nullptr, const float* aux = nullptr, float* C2 = nullptr) {
+  Epi e;
+  e.op = op;
+  e.bias = bias;
+  e.aux = aux;
+  e.C2 = C2;
+  return e;
 }
 
 // ---------------------------------------------------------------- row-wise kernels
@@ -215,39 +406,31 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* x, const float
   }
 }
 
-// out[j] += sum_i P[i][j], rows in order (one thread per column)
-__global__ __launch_bounds__(256) void colsum_kernel(const float* P, int rows, int n, float* out) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
+// Column sums in a fixed order, two stages: part[z][c][j] = sum of rows
+// [64 c, 64 c + 64) of src_z's column j (rows in order), then out_z[j] +=
+// sum over c in order.  z selects one of two independent sums.
+constexpr int kColChunk = 64;
+struct ColsumArgs {
+  const float* src[2];
+  float* out[2];
+};
+__global__ __launch_bounds__(256) void colsum_part_kernel(ColsumArgs a, int rows, int n, float* part) {
+  const int j = blockIdx.x * 256 + threadIdx.x, c = blockIdx.y, z = blockIdx.z;
+  if (j >= n) return;
+  const float* src = a.src[z];
+  const int r1 = min(rows, (c + 1) * kColChunk);
+  float s = 0.f;
+  for (int r = c * kColChunk; r < r1; ++r) s += src[(size_t)r * n + j];
+  part[((size_t)z * gridDim.y + c) * n + j] = s;
+}
+__global__ __launch_bounds__(256) void colsum_final_kernel(ColsumArgs a, int chunks, int n, const float* part) {
+  const int j = blockIdx.x * 256 + threadIdx.x, z = blockIdx.y;
   if (j >= n) return;
   float s = 0.f;
-  for (int i = 0; i < rows; ++i) s += P[(size_t)i * n + j];
-  out[j] += s;
+  for (int c = 0; c < chunks; ++c) s += part[((size_t)z * chunks + c) * n + j];
+  a.out[z][j] += s;
 }
 
-__device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
-__device__ __forceinline__ float gelu_d(float x) {
-  return 0.5f * (1.f + erff(x * 0.70710678118654752f)) + x * expf(-0.5f * x * x) * 0.39894228040143268f;
-}
-
-// Z += b (the pre-activation, kept), G = GeLU(Z)
-__global__ __launch_bounds__(256) void bias_gelu_kernel(float* Z, const float* b, float* G, int n, size_t total) {
-  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= total) return;
-  const float z = Z[e] + b[e % n];
-  Z[e] = z;
-  G[e] = gelu_f(z);
-}
-// dZ = dG GeLU'(Z), in place of dG
-__global__ __launch_bounds__(256) void gelu_bwd_kernel(float* dG, const float* Z, size_t total) {
-  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= total) return;
-  dG[e] *= gelu_d(Z[e]);
-}
-__global__ __launch_bounds__(256) void bias_add_kernel(float* Y, const float* b, int n, size_t total) {
-  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= total) return;
-  Y[e] += b[e % n];
-}
 __global__ __launch_bounds__(256) void copy_kernel(float* dst, const float* src, size_t total) {
   const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (e < total) dst[e] = src[e];
@@ -397,7 +580,7 @@ slim_problem att_problem(const Dims& m, int n) {
 struct Layout {
   size_t ident, attws, attws_bytes, states, gstates, bprev, delta, snew, wd;
   size_t X, QKV, Qh, Yh, A, st1, H, Z1, G1, Fo, st2;
-  size_t logits, rowloss, dX, dH, dF, dG1, dA, dYh, dQh, dQKV, P;
+  size_t logits, rowloss, dX, dH, dF, dG1, dA, dYh, dQh, dQKV, P, part, part_bytes, red;
   size_t total;
 };
 
@@ -448,6 +631,18 @@ Layout layout(const Dims& m) {
   take(l.dQh, 3 * HF * 4);
   take(l.dQKV, R * 3 * D * 4);
   take(l.P, R * std::max(D, std::max(F, (size_t)m.V)) * 4);
+  // split-K partial products: the largest over the step's products, for
+  // the full slice and the ragged last one
+  size_t pb = 0;
+  for (int n : {m.nmax, last}) {
+    const int rows = (int)(m.B * n), d = m.D, f = m.F, v = m.V;
+    const int shapes[][3] = {{rows, d, d}, {rows, f, d}, {rows, d, f}, {rows, v, d}, {rows, d, v},
+                             {d, v, rows}, {f, d, rows}, {d, f, rows}, {d, d, rows}};
+    for (const auto& sh : shapes) pb = std::max(pb, gemm_part_bytes(sh[0], sh[1], sh[2]));
+  }
+  l.part_bytes = pb;
+  take(l.part, std::max<size_t>(pb, 256));
+  take(l.red, 2 * ((R + kColChunk - 1) / kColChunk) * std::max(D, std::max(F, (size_t)m.V)) * 4);
   l.total = off;
   return l;
 }
@@ -470,7 +665,7 @@ int check(const slim_model* mm, Dims* out) {
   if (!(m.eps > 0.f)) return report(SLIM_EINVAL, "ln_eps must be > 0");
   m.k = m.D / kHead;
   m.nmax = (int)std::min<int64_t>(m.C, m.L);
-  if ((int64_t)m.B * m.nmax > (1 << 24) || m.L > ((int64_t)1 << 30) || m.B * m.L > ((int64_t)1 << 31) - 1)
+  if ((int64_t)m.B * m.nmax > (1 << 22) || m.L > ((int64_t)1 << 30) || m.B * m.L > ((int64_t)1 << 31) - 1)
     return report(SLIM_EUNSUPPORTED, "too many rows");
   if (m.B * m.k > 65535) return report(SLIM_EUNSUPPORTED, "B * heads above 65535");
   *out = m;
@@ -545,6 +740,22 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
   float* rowloss = f(lay.rowloss);
   float *dX = f(lay.dX), *dH = f(lay.dH), *dF = f(lay.dF), *dG1 = f(lay.dG1), *dA = f(lay.dA);
   float *dYh = f(lay.dYh), *dQh = f(lay.dQh), *dQKV = f(lay.dQKV), *Pp = f(lay.P);
+  float* part = f(lay.part);
+  float* red = f(lay.red);
+  auto mm = [&](bool ta, bool tb, int M_, int N_, int K_, const float* A_, int lda, const float* B_, int ldb, float* C_,
+                int ldc, Epi e) { return gemm(ta, tb, M_, N_, K_, A_, lda, B_, ldb, C_, ldc, e, part, s); };
+  // out0 += column sums of src0 (and out1 += those of src1), rows in order
+  auto colsum = [&](int rows, int n, const float* src0, float* out0, const float* src1 = nullptr,
+                    float* out1 = nullptr) {
+    ColsumArgs ca;
+    ca.src[0] = src0;
+    ca.out[0] = out0;
+    ca.src[1] = src1;
+    ca.out[1] = out1;
+    const int nz = src1 ? 2 : 1, chunks = (rows + kColChunk - 1) / kColChunk;
+    hipLaunchKernelGGL(colsum_part_kernel, dim3((n + 255) / 256, chunks, nz), dim3(256), 0, s, ca, rows, n, red);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((n + 255) / 256, nz), dim3(256), 0, s, ca, chunks, n, red);
+  };
 
   // identity W of the square map: g(x) = (x_i^2)
   hipLaunchKernelGGL(identity_kernel, grid1(kHead * kHead), dim3(256), 0, s, ident, kHead);
@@ -556,9 +767,9 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     const int rows = (int)(m.B * n);
     const size_t hf = (size_t)m.B * k * n * kHead;
     const float* X = Xr(r);
-    CHECK_HIP(gemm(false, false, rows, D, D, 1.f, X, D, P.l[r].Wq, D, 0.f, QKV, 3 * D, s));
-    CHECK_HIP(gemm(false, false, rows, D, D, 1.f, X, D, P.l[r].Wk, D, 0.f, QKV + D, 3 * D, s));
-    CHECK_HIP(gemm(false, false, rows, D, D, 1.f, X, D, P.l[r].Wv, D, 0.f, QKV + 2 * D, 3 * D, s));
+    CHECK_HIP(mm(false, false, rows, D, D, X, D, P.l[r].Wq, D, QKV, 3 * D, epi(EPI_STORE)));
+    CHECK_HIP(mm(false, false, rows, D, D, X, D, P.l[r].Wk, D, QKV + D, 3 * D, epi(EPI_STORE)));
+    CHECK_HIP(mm(false, false, rows, D, D, X, D, P.l[r].Wv, D, QKV + 2 * D, 3 * D, epi(EPI_STORE)));
     for (int part = 0; part < 3; ++part)
       hipLaunchKernelGGL(rows_to_heads_kernel, grid1(hf), dim3(256), 0, s, QKV, 3 * D, part * D, Qhr(r, part), k, n, hf);
     CHECK_HIP(hipGetLastError());
@@ -575,11 +786,8 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     hipLaunchKernelGGL(heads_to_rows_kernel, grid1(hf), dim3(256), 0, s, Yh, Ar(r), D, 0, k, n, hf);
     hipLaunchKernelGGL(ln_fwd_kernel, dim3(rows), dim3(256), 0, s, Ar(r), P.l[r].g1, P.l[r].b1n, X, Hr(r), s1r(r), D,
                        m.eps);
-    CHECK_HIP(gemm(false, false, rows, F, D, 1.f, Hr(r), D, P.l[r].W1, F, 0.f, Z1r(r), F, s));
-    hipLaunchKernelGGL(bias_gelu_kernel, grid1((size_t)rows * F), dim3(256), 0, s, Z1r(r), P.l[r].b1, G1r(r), F,
-                       (size_t)rows * F);
-    CHECK_HIP(gemm(false, false, rows, D, F, 1.f, G1r(r), F, P.l[r].W2, D, 0.f, For(r), D, s));
-    hipLaunchKernelGGL(bias_add_kernel, grid1((size_t)rows * D), dim3(256), 0, s, For(r), P.l[r].b2, D, (size_t)rows * D);
+    CHECK_HIP(mm(false, false, rows, F, D, Hr(r), D, P.l[r].W1, F, Z1r(r), F, epi(EPI_BIAS_GELU, P.l[r].b1, nullptr, G1r(r))));
+    CHECK_HIP(mm(false, false, rows, D, F, G1r(r), F, P.l[r].W2, D, For(r), D, epi(EPI_BIAS, P.l[r].b2)));
     hipLaunchKernelGGL(ln_fwd_kernel, dim3(rows), dim3(256), 0, s, For(r), P.l[r].g2, P.l[r].b2n, Hr(r), Xr(r + 1),
                        s2r(r), D, m.eps);
     CHECK_HIP(hipGetLastError());
@@ -587,8 +795,7 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
   };
   auto head_logits = [&](int a, int n) -> int {
     const int rows = (int)(m.B * n);
-    CHECK_HIP(gemm(false, false, rows, V, D, 1.f, Xr(m.s), D, P.Wout, V, 0.f, logits, V, s));
-    hipLaunchKernelGGL(bias_add_kernel, grid1((size_t)rows * V), dim3(256), 0, s, logits, P.bout, V, (size_t)rows * V);
+    CHECK_HIP(mm(false, false, rows, V, D, Xr(m.s), D, P.Wout, V, logits, V, epi(EPI_BIAS, P.bout)));
     hipLaunchKernelGGL(ce_kernel, dim3(rows), dim3(256), 0, s, logits, tokens, m.L, a, n, (int)m.B, V, rowloss);
     CHECK_HIP(hipGetLastError());
     return SLIM_OK;
@@ -643,30 +850,26 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     }
     CHECK_SLIM(head_logits(a, n));
     // output layer
-    CHECK_HIP(gemm(true, false, D, V, rows, 1.f, Xr(m.s), D, logits, V, 1.f, G.Wout, V, s));
-    hipLaunchKernelGGL(colsum_kernel, grid1(V), dim3(256), 0, s, logits, rows, V, G.bout);
-    CHECK_HIP(gemm(false, true, rows, D, V, 1.f, logits, V, P.Wout, V, 0.f, dX, D, s));
+    CHECK_HIP(mm(true, false, D, V, rows, Xr(m.s), D, logits, V, G.Wout, V, epi(EPI_ACC)));
+    colsum(rows, V, logits, G.bout);
+    CHECK_HIP(mm(false, true, rows, D, V, logits, V, P.Wout, V, dX, D, epi(EPI_STORE)));
     for (int r = m.s - 1; r >= 0; --r) {
       const Params::Layer& pl = P.l[r];
       const Grads::Layer& gl = G.l[r];
       // X_{r+1} = LN2(Fo) + H
       hipLaunchKernelGGL(ln_bwd_kernel, dim3(rows), dim3(256), 0, s, For(r), s2r(r), pl.g2, dX, nullptr, dF, Pp, D);
-      hipLaunchKernelGGL(colsum_kernel, grid1(D), dim3(256), 0, s, Pp, rows, D, gl.g2);
-      hipLaunchKernelGGL(colsum_kernel, grid1(D), dim3(256), 0, s, dX, rows, D, gl.b2n);
+      colsum(rows, D, Pp, gl.g2, dX, gl.b2n);
       // Fo = GeLU(Z1) W2 + b2
-      CHECK_HIP(gemm(true, false, F, D, rows, 1.f, G1r(r), F, dF, D, 1.f, gl.W2, D, s));
-      hipLaunchKernelGGL(colsum_kernel, grid1(D), dim3(256), 0, s, dF, rows, D, gl.b2);
-      CHECK_HIP(gemm(false, true, rows, F, D, 1.f, dF, D, pl.W2, D, 0.f, dG1, F, s));
-      hipLaunchKernelGGL(gelu_bwd_kernel, grid1((size_t)rows * F), dim3(256), 0, s, dG1, Z1r(r), (size_t)rows * F);
+      CHECK_HIP(mm(true, false, F, D, rows, G1r(r), F, dF, D, gl.W2, D, epi(EPI_ACC)));
+      colsum(rows, D, dF, gl.b2);
+      CHECK_HIP(mm(false, true, rows, F, D, dF, D, pl.W2, D, dG1, F, epi(EPI_GELU_BWD, nullptr, Z1r(r))));
       // Z1 = H W1 + b1; dH = dX (residual) + dZ1 W1^T
-      CHECK_HIP(gemm(true, false, D, F, rows, 1.f, Hr(r), D, dG1, F, 1.f, gl.W1, F, s));
-      hipLaunchKernelGGL(colsum_kernel, grid1(F), dim3(256), 0, s, dG1, rows, F, gl.b1);
-      hipLaunchKernelGGL(copy_kernel, grid1((size_t)rows * D), dim3(256), 0, s, dH, dX, (size_t)rows * D);
-      CHECK_HIP(gemm(false, true, rows, D, F, 1.f, dG1, F, pl.W1, F, 1.f, dH, D, s));
+      CHECK_HIP(mm(true, false, D, F, rows, Hr(r), D, dG1, F, gl.W1, F, epi(EPI_ACC)));
+      colsum(rows, F, dG1, gl.b1);
+      CHECK_HIP(mm(false, true, rows, D, F, dG1, F, pl.W1, F, dH, D, epi(EPI_ADD, nullptr, dX)));
       // H = LN1(A) + X
       hipLaunchKernelGGL(ln_bwd_kernel, dim3(rows), dim3(256), 0, s, Ar(r), s1r(r), pl.g1, dH, nullptr, dA, Pp, D);
-      hipLaunchKernelGGL(colsum_kernel, grid1(D), dim3(256), 0, s, Pp, rows, D, gl.g1);
-      hipLaunchKernelGGL(colsum_kernel, grid1(D), dim3(256), 0, s, dH, rows, D, gl.b1n);
+      colsum(rows, D, Pp, gl.g1, dH, gl.b1n);
       CHECK_HIP(hipGetLastError());
       // attention: the slice's gradient with the state cotangent after it
       // (eq. 18 gives the one before it)
@@ -681,13 +884,12 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
       CHECK_HIP(hipGetLastError());
       // Q, K, V = X Wq, X Wk, X Wv; dX = dH + sum dZ W^T
       const float* X = Xr(r);
-      CHECK_HIP(gemm(true, false, D, D, rows, 1.f, X, D, dQKV, 3 * D, 1.f, gl.Wq, D, s));
-      CHECK_HIP(gemm(true, false, D, D, rows, 1.f, X, D, dQKV + D, 3 * D, 1.f, gl.Wk, D, s));
-      CHECK_HIP(gemm(true, false, D, D, rows, 1.f, X, D, dQKV + 2 * D, 3 * D, 1.f, gl.Wv, D, s));
-      hipLaunchKernelGGL(copy_kernel, grid1((size_t)rows * D), dim3(256), 0, s, dX, dH, (size_t)rows * D);
-      CHECK_HIP(gemm(false, true, rows, D, D, 1.f, dQKV, 3 * D, pl.Wq, D, 1.f, dX, D, s));
-      CHECK_HIP(gemm(false, true, rows, D, D, 1.f, dQKV + D, 3 * D, pl.Wk, D, 1.f, dX, D, s));
-      CHECK_HIP(gemm(false, true, rows, D, D, 1.f, dQKV + 2 * D, 3 * D, pl.Wv, D, 1.f, dX, D, s));
+      CHECK_HIP(mm(true, false, D, D, rows, X, D, dQKV, 3 * D, gl.Wq, D, epi(EPI_ACC)));
+      CHECK_HIP(mm(true, false, D, D, rows, X, D, dQKV + D, 3 * D, gl.Wk, D, epi(EPI_ACC)));
+      CHECK_HIP(mm(true, false, D, D, rows, X, D, dQKV + 2 * D, 3 * D, gl.Wv, D, epi(EPI_ACC)));
+      CHECK_HIP(mm(false, true, rows, D, D, dQKV, 3 * D, pl.Wq, D, dX, D, epi(EPI_ADD, nullptr, dH)));
+      CHECK_HIP(mm(false, true, rows, D, D, dQKV + D, 3 * D, pl.Wk, D, dX, D, epi(EPI_ACC)));
+      CHECK_HIP(mm(false, true, rows, D, D, dQKV + 2 * D, 3 * D, pl.Wv, D, dX, D, epi(EPI_ACC)));
     }
     hipLaunchKernelGGL(embed_bwd_kernel, dim3(V, (D + 255) / 256), dim3(256), 0, s, tokens, m.L, a, n, rows, dX, D, G.emb);
     // the states before this slice become the states after the earlier one

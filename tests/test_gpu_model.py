@@ -31,6 +31,10 @@ CASES = [
     (ModelConfig("heads2", L=70, D=128, s=3, vocab=256, B=1), [7, 32, 70]),
     (ModelConfig("short", L=2, D=64, s=1, vocab=5, B=3), [1, 2]),
     (ModelConfig("wide", L=130, D=192, s=2, vocab=300, B=2), [64, 33]),
+    # products long enough to split their reduction over workgroups
+    (ModelConfig("split", L=600, D=128, s=2, vocab=50, B=2), [600, 256]),
+    # the 128-row product tiles (at least 256 of them)
+    (ModelConfig("big", L=2048, D=512, s=1, vocab=256, B=1), [2048, 1000]),
 ]
 
 LOSS_TOL = 2e-5  # relative
