@@ -48,11 +48,15 @@ __device__ __forceinline__ float gelu_d(float x) {
 // Workgroup tile BM x 128 (BM = 128 or 64), four waves in 2 x 2, each wave
 // (BM / 2) x 64 as (BM / 32) x 4 matrix tiles of 16 x 16 on
 // v_mfma_f32_16x16x4_f32.  K runs in tiles of 16 through double-buffered
-// LDS held [m][k] and [n][k] (rows padded to 20 floats): the summation index
-// of the four products of one k tile is permuted so that lane group g
-// (lane / 16) takes k = 4 g + j in product j, and one 16-byte LDS read then
-// feeds four products.  Global loads are 16-byte vectors where the strides
-// allow, prefetched one k tile ahead.  Long K is split over blockIdx.y; the
+// LDS.  The summation index of the four products of one k tile is permuted
+// so that lane group g (lane / 16) takes k = 4 g + j in product j.  An
+// operand whose rows run along k in memory is held [m][k] (rows padded to 20
+// floats): one 16-byte LDS read feeds a lane's four products.  An operand
+// whose rows run along m (or n) is held as it is in memory, [k][m] (rows
+// padded by 4 floats, so the four k rows a read touches fall in different
+// banks), and a lane reads its four values one by one.  Either way the
+// global tile lands in LDS with 16-byte writes.  Global loads are 16-byte
+// vectors where the strides allow, prefetched one k tile ahead.  Long K is split over blockIdx.y; the
 // partial products are summed in a fixed order by gemm_reduce_kernel, which
 // then applies the epilogue (no atomics: results are reproducible).
 constexpr int GBN = 128, GBK = 16, GKP = GBK + 4;
@@ -116,8 +120,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int AV = BM * GBK / 4 / 256;  // float4 loads per thread per k tile (A)
   constexpr int BV = GBN * GBK / 4 / 256;  // (B)
   constexpr int TI = BM / 32;              // matrix tiles per wave along m
-  __shared__ __align__(16) float As[2][BM][GKP];
-  __shared__ __align__(16) float Bs[2][GBN][GKP];
+  // [m][k] (k-contiguous source) or [k][m] (m-contiguous source) per buffer
+  constexpr int ALD = TA ? BM + 4 : GKP, BLD = TB ? GKP : GBN + 4;
+  constexpr int ASZ = TA ? GBK * ALD : BM * ALD, BSZ = TB ? GBN * BLD : GBK * BLD;
+  __shared__ __align__(16) float As[2][ASZ];
+  __shared__ __align__(16) float Bs[2][BSZ];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   // XCD-aware order: consecutive tiles (sharing rows of A) on one XCD
   int tile = blockIdx.x;
@@ -157,28 +164,14 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
       const int f = tid + 256 * i;
-      if (!TA) {
-        *reinterpret_cast<float4*>(&As[buf][f >> 2][4 * (f & 3)]) = ra[i];
-      } else {
-        const int k = f / (BM / 4), m = 4 * (f % (BM / 4));
-        As[buf][m][k] = ra[i].x;
-        As[buf][m + 1][k] = ra[i].y;
-        As[buf][m + 2][k] = ra[i].z;
-        As[buf][m + 3][k] = ra[i].w;
-      }
+      const int at = TA ? (f / (BM / 4)) * ALD + 4 * (f % (BM / 4)) : (f >> 2) * ALD + 4 * (f & 3);
+      *reinterpret_cast<float4*>(&As[buf][at]) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
       const int f = tid + 256 * i;
-      if (TB) {
-        *reinterpret_cast<float4*>(&Bs[buf][f >> 2][4 * (f & 3)]) = rb[i];
-      } else {
-        const int k = f / (GBN / 4), n = 4 * (f % (GBN / 4));
-        Bs[buf][n][k] = rb[i].x;
-        Bs[buf][n + 1][k] = rb[i].y;
-        Bs[buf][n + 2][k] = rb[i].z;
-        Bs[buf][n + 3][k] = rb[i].w;
-      }
+      const int at = TB ? (f >> 2) * BLD + 4 * (f & 3) : (f / (GBN / 4)) * BLD + 4 * (f % (GBN / 4));
+      *reinterpret_cast<float4*>(&Bs[buf][at]) = rb[i];
     }
   };
 
@@ -199,9 +192,23 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     if (more) load(k0 + GBK);
     float4 a[TI], b[4];
 #pragma unroll
-    for (int i = 0; i < TI; ++i) a[i] = *reinterpret_cast<const float4*>(&As[buf][wm + 16 * i + c][4 * q]);
+    for (int i = 0; i < TI; ++i) {
+      if (TA) {
+        const float* p = &As[buf][4 * q * ALD + wm + 16 * i + c];
+        a[i] = make_float4(p[0], p[ALD], p[2 * ALD], p[3 * ALD]);
+      } else {
+        a[i] = *reinterpret_cast<const float4*>(&As[buf][(wm + 16 * i + c) * ALD + 4 * q]);
+      }
+    }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const float4*>(&Bs[buf][wn + 16 * j + c][4 * q]);
+    for (int j = 0; j < 4; ++j) {
+      if (TB) {
+        b[j] = *reinterpret_cast<const float4*>(&Bs[buf][(wn + 16 * j + c) * BLD + 4 * q]);
+      } else {
+        const float* p = &Bs[buf][4 * q * BLD + wn + 16 * j + c];
+        b[j] = make_float4(p[0], p[BLD], p[2 * BLD], p[3 * BLD]);
+      }
+    }
     // each accumulator's four products are TI * 4 issues apart
 #pragma unroll
     for (int i = 0; i < TI; ++i)
