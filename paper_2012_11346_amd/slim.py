@@ -352,6 +352,17 @@ def model_param_names(s: int):
     return names + ["Wout", "bout"]
 
 
+def model_param_shapes(s: int, vocab: int, D: int, F: int) -> dict:
+    """Shapes of slim_model_step's parameter tensors (include/slim_model.h)."""
+    shp = {"emb": (vocab, D), "Wout": (D, vocab), "bout": (vocab,)}
+    for r in range(s):
+        shp.update({f"Wq{r}": (D, D), f"Wk{r}": (D, D), f"Wv{r}": (D, D), f"W1{r}": (D, F), f"b1{r}": (F,),
+                    f"W2{r}": (F, D), f"b2{r}": (D,)})
+        for n in ("ln1_g", "ln1_b", "ln2_g", "ln2_b"):
+            shp[f"{n}{r}"] = (D,)
+    return shp
+
+
 def model_desc(B, L, D, s, vocab, F, C, ln_eps=1e-5) -> ModelDesc:
     return ModelDesc(int(B), int(L), int(D), int(s), int(vocab), int(F), int(C), float(ln_eps))
 
@@ -374,22 +385,33 @@ def model_step(params: dict, tokens, C: int, ln_eps: float = 1e-5, ws=None, grad
         tokens = tokens[None]
     B, L = tokens.shape
     m = model_desc(B, L, D, s, vocab, F, C, ln_eps)
-    _need(tokens, "tokens", torch.int32, (B, L))
     dev = emb.device
+    if tokens.device != dev:
+        raise ValueError(f"tokens must be on {dev}")
+    _need(tokens, "tokens", torch.int32, (B, L))
+    shapes = model_param_shapes(s, vocab, D, F)
     for n in names:
         t = params[n]
-        if t.dtype != torch.float32 or not t.is_contiguous() or t.device != dev:
-            raise ValueError(f"{n} must be a contiguous float32 tensor on {dev}")
+        if t.device != dev:
+            raise ValueError(f"{n} must be on {dev}")
+        _need(t, n, torch.float32, shapes[n])
     if grads is None:
         grads = {n: torch.empty_like(params[n]) for n in names}
     for n in names:
-        _need(grads[n], f"grad {n}", torch.float32, tuple(params[n].shape))
+        if grads[n].device != dev:
+            raise ValueError(f"grad {n} must be on {dev}")
+        _need(grads[n], f"grad {n}", torch.float32, shapes[n])
     loss = torch.empty(1, dtype=torch.float32, device=dev) if loss is None else loss
+    _need(loss, "loss", torch.float32, (1,))
     need = model_workspace_bytes(m)
     if need == 0:
         raise SlimError(SLIM_EINVAL, LIB.slim_last_error().decode())
-    if ws is None or ws.numel() * ws.element_size() < need:
+    if ws is None:
         ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    else:
+        _need(ws, "ws", ws.dtype)
+        if _nbytes(ws) < need:
+            raise ValueError(f"workspace needs {need} bytes, got {_nbytes(ws)}")
     P = (ctypes.c_void_p * len(names))(*[params[n].data_ptr() for n in names])
     G = (ctypes.c_void_p * len(names))(*[grads[n].data_ptr() for n in names])
     _check(LIB.slim_model_step(ctypes.byref(m), _ptr(tokens), P, G, _ptr(loss), _ptr(ws), _nbytes(ws), _stream()))

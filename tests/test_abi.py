@@ -223,3 +223,14 @@ def test_model_step_checks_pointers_and_workspace(S):
     assert st == S.SLIM_EWORKSPACE
     st = S.LIB.slim_model_step(ctypes.byref(m), A, arr, arr, A, A + 16, need, None)
     assert st == S.SLIM_EINVAL  # not 256-byte aligned
+
+
+def test_model_param_shapes_match_the_synthetic_model(S):
+    from synth import ModelConfig, make_model
+
+    cfg = ModelConfig("shapes", L=8, D=128, s=2, vocab=37, B=1)
+    P = make_model(cfg)
+    shp = S.model_param_shapes(cfg.s, cfg.vocab, cfg.D, cfg.F)
+    assert list(P) == S.model_param_names(cfg.s) and set(shp) == set(P)
+    for k, v in P.items():
+        assert tuple(v.shape) == shp[k], k
