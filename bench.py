@@ -120,7 +120,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the slice-length sweep")
     ap.add_argument("--no-configs", action="store_true", help="skip the other workloads and memory-vs-L")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing and the parity checks")
-    ap.add_argument("--quick", action="store_true", help="headline only (= --no-sweep --no-configs --no-cpu)")
+    ap.add_argument("--quick", action="store_true", help="headline only (= --no-sweep --no-configs --no-cpu --no-model)")
     ap.add_argument("--no-model", action="store_true", help="skip the s-layer language model (Algorithm 1 over eqs. 5-10)")
     ap.add_argument("--model-only", action="store_true", help="only the s-layer language model section")
     ap.add_argument("--model-seeds", type=int, default=1, help="seeds of the model's gradient discrepancy")
@@ -132,7 +132,7 @@ def main():
                     help="only copy a device buffer of this many MiB (calibration of memory counters) and exit")
     args = ap.parse_args()
     if args.quick:
-        args.no_sweep = args.no_configs = args.no_cpu = True
+        args.no_sweep = args.no_configs = args.no_cpu = args.no_model = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path runs on a single "
               "MI355X; sharded, GPUs would split the heads and batch rows and sum dW with one all-reduce)",
