@@ -52,7 +52,7 @@ extern "C" {
  *   s       layers (>= 1)
  *   vocab   alphabet size (2 .. 65536)
  *   F       d_ff (the paper uses 4 D): a multiple of 4
- *   C       slice length (>= 1; values above L act as L; B * min(C, L) <= 2^22)
+ *   C       slice length (>= 1; values above L act as L; B * min(C, L) <= 65535 * 64)
  *   ln_eps  layer-normalisation epsilon (the usual value is 1e-5) */
 typedef struct {
   int64_t B, L;

@@ -680,7 +680,8 @@ int check(const slim_model* mm, Dims* out) {
   if (!(m.eps > 0.f)) return report(SLIM_EINVAL, "ln_eps must be > 0");
   m.k = m.D / kHead;
   m.nmax = (int)std::min<int64_t>(m.C, m.L);
-  if ((int64_t)m.B * m.nmax > (1 << 22) || m.L > ((int64_t)1 << 30) || m.B * m.L > ((int64_t)1 << 31) - 1)
+  // (rows of a slice: the column sums run one workgroup row per 64 rows, at most 65535 of them)
+  if ((int64_t)m.B * m.nmax > (int64_t)65535 * kColChunk || m.L > ((int64_t)1 << 30) || m.B * m.L > ((int64_t)1 << 31) - 1)
     return report(SLIM_EUNSUPPORTED, "too many rows");
   if (m.B * m.k > 65535) return report(SLIM_EUNSUPPORTED, "B * heads above 65535");
   *out = m;

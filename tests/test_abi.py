@@ -198,7 +198,7 @@ def test_model_workspace_grows_with_C_not_L(S):
 @pytest.mark.parametrize(
     "kw",
     [dict(D=96), dict(D=0), dict(D=8192), dict(vocab=1), dict(vocab=70000), dict(F=6), dict(C=0), dict(L=1),
-     dict(s=0), dict(B=0), dict(ln_eps=0.0)],
+     dict(s=0), dict(B=0), dict(ln_eps=0.0), dict(L=1 << 22, C=1 << 22)],
 )
 def test_invalid_models_are_rejected(S, kw):
     m = _m(S, **kw)
