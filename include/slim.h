@@ -81,8 +81,15 @@ typedef enum { SLIM_PHASE_FWD = 0, SLIM_PHASE_BWD = 1 } slim_phase;
  *                          inside the slice), slices one after another and the
  *                          32-row tiles of a slice in parallel: the work per
  *                          row grows with C (bf16 problems with M of 128 or
- *                          256, FAVOR+ or ReLU) */
-typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1 } slim_within;
+ *                          256, FAVOR+ or ReLU)
+ *   SLIM_WITHIN_PS         the explicit prefix sum the paper benchmarks as
+ *                          "PS": the state after every row of a slice is
+ *                          written out (C M (d + 1) floats per head, twice in
+ *                          the backward, in the workspace), then used; slices
+ *                          one after another.  Memory grows with C.  Any
+ *                          dtype, map and shape (float32 with d M up to 16384
+ *                          included); no dropout (SLIM_EUNSUPPORTED) */
+typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1, SLIM_WITHIN_PS = 2 } slim_within;
 
 /* Problem description shared by all entry points.
  *   B, H, L  batch, heads, sequence length (each >= 1; B H <= 65535 and one

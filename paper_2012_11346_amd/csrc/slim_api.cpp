@@ -93,10 +93,13 @@ int check_problem(const slim_problem* p) {
   if (p->kind == SLIM_SQUARE && p->M != 64)
     return fail(SLIM_EUNSUPPORTED, "the square map is built for M=64 (got M=%d)", (int)p->M);
   if (!(p->dropout >= 0.f && p->dropout < 1.f)) return fail(SLIM_EINVAL, "dropout must be in [0, 1)");
-  if (p->dtype == SLIM_F32 && (int64_t)p->d * p->M > 4096)
-    return fail(SLIM_EUNSUPPORTED, "fp32 problems need d*M <= 4096 (got d=%d, M=%d)", (int)p->d, (int)p->M);
-  if (p->within != SLIM_WITHIN_ITER && p->within != SLIM_WITHIN_QUADRATIC)
+  if (p->within != SLIM_WITHIN_ITER && p->within != SLIM_WITHIN_QUADRATIC && p->within != SLIM_WITHIN_PS)
     return fail(SLIM_EINVAL, "unknown within-slice mode %d", (int)p->within);
+  if (p->dtype == SLIM_F32 && (int64_t)p->d * p->M > 4096 && p->within != SLIM_WITHIN_PS)
+    return fail(SLIM_EUNSUPPORTED, "fp32 problems need d*M <= 4096 (got d=%d, M=%d) outside the PS mode", (int)p->d,
+                (int)p->M);
+  if (p->within == SLIM_WITHIN_PS && p->dropout != 0.f)
+    return fail(SLIM_EUNSUPPORTED, "the PS within-slice mode has no dropout");
   if (p->reserved != 0) return fail(SLIM_EINVAL, "reserved field must be 0");
   if (p->within == SLIM_WITHIN_QUADRATIC &&
       (p->dtype != SLIM_BF16 || (p->M != 128 && p->M != 256) || p->kind == SLIM_SQUARE))
@@ -105,6 +108,7 @@ int check_problem(const slim_problem* p) {
 }
 
 bool quad(const slim_problem* p) { return p->within == SLIM_WITHIN_QUADRATIC; }
+bool ps(const slim_problem* p) { return p->within == SLIM_WITHIN_PS; }
 
 // value dropout parameters of the kernels: keep threshold t = round(p 65536)
 // on 16-bit fields (0: nothing dropped) and the output scale 1 / (1 - p)
@@ -230,7 +234,8 @@ int bwd_parts(const slim_problem* p) {
 // The forward hands its boundary states to the backward (slim_context_bytes)
 // when it computes them with one key shift per head (the key-sum kernel):
 // then its segments are the backward's parts.
-bool context_used(const slim_problem* p) { return !quad(p) && has_ksum(p) && plan_fwd_segments(p) > 1; }
+bool context_used(const slim_problem* p) { return !quad(p) && !ps(p) && has_ksum(p) && plan_fwd_segments(p) > 1; }
+
 // Parts of the forward's boundaries on the one-shift path
 int fwd_parts(const slim_problem* p) { return plan_fwd_segments(p); }
 
@@ -510,11 +515,54 @@ size_t context_bytes(const slim_problem* p) {
   return (size_t)p->B * p->H * (bwd_parts(p) + 1) * state_elems(p) * sizeof(float);
 }
 
+// ---- the explicit prefix-sum within-slice mode: slices one after another;
+// the row kernels run ps_workgroups per head (rows dealt round-robin), the
+// backward restarts from exact states at ps_parts part boundaries (whole
+// slices) and downdates inside a part (eq. 17)
+int ps_slices(const slim_problem* p) { return (int)((p->L + clamp_C(p) - 1) / clamp_C(p)); }
+int ps_workgroups(const slim_problem* p) {
+  const int64_t BH = p->B * p->H;
+  return (int)std::max<int64_t>(1, std::min<int64_t>(64, (1024 + BH - 1) / BH));
+}
+int ps_parts(const slim_problem* p) { return std::min(ps_slices(p), 64); }
+struct PsLayout {
+  size_t kmax, U, Gh, s[2], g[2], parts, bounds, dw, total;
+};
+PsLayout ps_layout(const slim_problem* p, int phase) {
+  PsLayout l;
+  std::memset(&l, 0, sizeof(l));
+  size_t off = 0;
+  auto take = [&](size_t& at, size_t bytes) {
+    at = off;
+    off += align256(bytes);
+  };
+  const size_t BH = (size_t)p->B * p->H, SZ = state_elems(p), NW = ps_workgroups(p);
+  const size_t rows = (size_t)clamp_C(p) * BH * SZ * sizeof(float);  // one slice's states
+  take(l.U, rows);
+  take(l.s[0], BH * SZ * sizeof(float));
+  take(l.s[1], BH * SZ * sizeof(float));
+  if (phase == SLIM_PHASE_FWD) {
+    take(l.kmax, BH * NW * sizeof(float));
+  } else {
+    const size_t P2 = ps_parts(p);
+    take(l.Gh, rows);
+    take(l.g[0], BH * SZ * sizeof(float));
+    take(l.g[1], BH * SZ * sizeof(float));
+    take(l.parts, BH * P2 * SZ * sizeof(float));
+    take(l.bounds, BH * (P2 + 1) * SZ * sizeof(float));
+    take(l.dw, 2 * BH * NW * (size_t)p->M * p->d * sizeof(float));
+  }
+  l.total = off;
+  return l;
+}
+
 size_t fwd_ws_bytes(const slim_problem* p) {
+  if (ps(p)) return ps_layout(p, SLIM_PHASE_FWD).total;
   if (quad(p)) return quad_fwd_layout(p).total;
   return fwd_layout(p, plan_fwd_segments(p)).total;
 }
 size_t bwd_ws_bytes(const slim_problem* p) {
+  if (ps(p)) return ps_layout(p, SLIM_PHASE_BWD).total;
   if (quad(p)) return quad_bwd_layout(p).total;
   return bwd_layout(p, plan_segments(p)).total;
 }
@@ -839,6 +887,194 @@ int quad_bwd_impl(const slim_problem* p, const Dispatch& dp, const void* Q, cons
   return ok();
 }
 
+// Arguments common to the PS kernels
+slim::PsArgs ps_args(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W) {
+  slim::PsArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.W = W;
+  a.B = (int)p->B;
+  a.H = (int)p->H;
+  a.L = (int)p->L;
+  a.d = (int)p->d;
+  a.M = (int)p->M;
+  a.C = clamp_C(p);
+  a.kind = p->kind == SLIM_FAVOR_PLUS ? slim::kFavor : p->kind == SLIM_RELU ? slim::kRelu : slim::kSquare;
+  a.relu_eps = p->relu_eps;
+  a.bf16 = p->dtype == SLIM_BF16 ? 1 : 0;
+  a.nslot = ps_workgroups(p);
+  return a;
+}
+
+// Forward in the explicit prefix-sum mode (arguments checked by fwd_impl):
+//   (0) FAVOR+: one key shift per head, the largest key exponent over all
+//       rows and the initial state's;
+//   (1) the state before the first slice: the initial state at that shift;
+//   (2) per slice: each row's term g(k)^T [v | 1]; their prefix sums from the
+//       state before the slice, written out for every row (the last is the
+//       state after the slice); the outputs from them.
+int ps_fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+                const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, char* w,
+                hipStream_t s) {
+  const PsLayout lay = ps_layout(p, SLIM_PHASE_FWD);
+  const bool favor = p->kind == SLIM_FAVOR_PLUS;
+  const int BH = (int)(p->B * p->H), SZ = (int)state_elems(p), C = clamp_C(p), NS = ps_slices(p);
+  const int NW = ps_workgroups(p);
+  slim::PsArgs a = ps_args(p, Q, K, V, W);
+  a.U = (float*)(w + lay.U);
+  a.Y = Y;
+  hipError_t e;
+  if (favor) {
+    a.part = (float*)(w + lay.kmax);
+    e = slim::launch_ps(slim::kPsKmax, a, NW, 0, s);
+    if (e != hipSuccess) return hip_fail(e, "key-maximum launch");
+    e = slim::launch_kshift_reduce(a.part, NW, state_in != nullptr ? kshift_in : nullptr, kshift_out, BH, s);
+    if (e != hipSuccess) return hip_fail(e, "key-shift launch");
+    a.kshift = kshift_out;
+  }
+  float* S[2] = {(float*)(w + lay.s[0]), (float*)(w + lay.s[1])};
+  e = slim::launch_state_combine(state_in, SZ, favor ? kshift_in : nullptr, favor ? kshift_out : nullptr, nullptr, 0,
+                                 1.f, S[0], BH, SZ, s);
+  if (e != hipSuccess) return hip_fail(e, "state launch");
+  e = timed_launch(SLIM_PHASE_FWD, s, [&]() -> hipError_t {
+    int cur = 0;
+    for (int n = 0; n < NS; ++n) {
+      a.row0 = n * C;
+      a.rows = (int)std::min<int64_t>(C, p->L - (int64_t)n * C);
+      const int nwg = std::min(NW, a.rows);
+      hipError_t er = slim::launch_ps(slim::kPsTerms, a, nwg, 0, s);
+      if (er != hipSuccess) return er;
+      a.S_in = S[cur];
+      a.in_stride = (size_t)SZ;
+      a.S_out = (n == NS - 1 && state_out != nullptr) ? state_out : S[cur ^ 1];
+      er = slim::launch_ps(slim::kPsScan0, a, 0, 0, s);
+      if (er != hipSuccess) return er;
+      er = slim::launch_ps(slim::kPsOut, a, nwg, 0, s);
+      if (er != hipSuccess) return er;
+      cur ^= 1;
+    }
+    return hipSuccess;
+  });
+  if (e != hipSuccess) return hip_fail(e, "PS-mode forward launches");
+  return ok();
+}
+
+// Backward in the explicit prefix-sum mode (arguments checked by slim_bwd):
+//   (1) exact states at the boundaries of P2 parts of whole slices (what
+//       each part's rows add, then their prefix from the initial state);
+//   (2) the slices in reverse: each row's term again, the state before the
+//       slice (the exact one at a part's first slice, else the state after
+//       it minus the slice's terms, eq. 17) and the prefix sums from it; the
+//       queries' gradient and their terms g(q) [dN | dD]; the reverse prefix
+//       sums of those from the cotangent after the slice (the last is the
+//       cotangent before it, eq. 18); the keys' and values' gradient;
+//   (3) dstate_in, and dW from the workgroups' partials in a fixed order.
+int ps_bwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
+                const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
+                const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in, char* w,
+                hipStream_t s) {
+  const PsLayout lay = ps_layout(p, SLIM_PHASE_BWD);
+  const bool favor = p->kind == SLIM_FAVOR_PLUS;
+  const int BH = (int)(p->B * p->H), SZ = (int)state_elems(p), C = clamp_C(p), NS = ps_slices(p);
+  const int NW = ps_workgroups(p), P2 = ps_parts(p);
+  const size_t MD = (size_t)p->M * p->d;
+  slim::PsArgs a = ps_args(p, Q, K, V, W);
+  a.kshift = favor ? kshift : nullptr;
+  a.U = (float*)(w + lay.U);
+  a.Gh = (float*)(w + lay.Gh);
+  a.dY = dY;
+  a.dQ = dQ;
+  a.dK = dK;
+  a.dV = dV;
+  hipError_t e;
+  // (1)
+  a.part = (float*)(w + lay.parts);
+  e = slim::launch_ps(slim::kPsSum, a, P2, NS, s);
+  if (e != hipSuccess) return hip_fail(e, "part-sum launch");
+  const float* bounds = (const float*)(w + lay.bounds);
+  {
+    slim::ScanArgs sc;
+    std::memset(&sc, 0, sizeof(sc));
+    sc.seg = a.part;
+    sc.init = state_in;
+    sc.init_shift = favor ? kshift_in : nullptr;
+    sc.shift = favor ? kshift : nullptr;
+    sc.out = (float*)(w + lay.bounds);
+    sc.BH = BH;
+    sc.P = P2;
+    sc.SZ = SZ;
+    sc.favor = favor ? 1 : 0;
+    e = slim::launch_scan_bwd(sc, s);
+    if (e != hipSuccess) return hip_fail(e, "boundary-scan launch");
+  }
+  float* dw_part = (float*)(w + lay.dw);
+  e = slim::launch_state_combine(nullptr, 0, nullptr, nullptr, nullptr, 0, 1.f, dw_part, 2 * BH * NW, (int)MD, s);
+  if (e != hipSuccess) return hip_fail(e, "dW-partial launch");
+  float* sb[2] = {(float*)(w + lay.s[0]), (float*)(w + lay.s[1])};
+  float* gb[2] = {(float*)(w + lay.g[0]), (float*)(w + lay.g[1])};
+  const size_t bstride = (size_t)(P2 + 1) * SZ;  // between heads of one boundary
+  auto first_of_part = [&](int r) { return (int)((int64_t)r * NS / P2); };
+  const float* Gafter = dstate_out;  // nullptr: zero
+  // (2)
+  e = timed_launch(SLIM_PHASE_BWD, s, [&]() -> hipError_t {
+    hipError_t er;
+    int r = P2 - 1, cs = 0, cg = 0;
+    const float* Safter = nullptr;
+    for (int n = NS - 1; n >= 0; --n) {
+      while (first_of_part(r) > n) --r;
+      a.row0 = n * C;
+      a.rows = (int)std::min<int64_t>(C, p->L - (int64_t)n * C);
+      const int nwg = std::min(NW, a.rows);
+      er = slim::launch_ps(slim::kPsTerms, a, nwg, 0, s);
+      if (er != hipSuccess) return er;
+      int mode;
+      if (n == first_of_part(r)) {
+        mode = slim::kPsScan2;
+        a.S_in = bounds + (size_t)r * SZ;
+        a.in_stride = bstride;
+      } else if (n == first_of_part(r + 1) - 1) {
+        mode = slim::kPsScan1;
+        a.S_in = bounds + (size_t)(r + 1) * SZ;
+        a.in_stride = bstride;
+      } else {
+        mode = slim::kPsScan1;
+        a.S_in = Safter;
+        a.in_stride = (size_t)SZ;
+      }
+      a.S_out = sb[cs];
+      er = slim::launch_ps(mode, a, 0, 0, s);
+      if (er != hipSuccess) return er;
+      Safter = sb[cs];
+      cs ^= 1;
+      a.dW_part = dw_part;
+      er = slim::launch_ps(slim::kPsGq, a, nwg, 0, s);
+      if (er != hipSuccess) return er;
+      a.G_in = Gafter;
+      a.G_out = gb[cg];
+      er = slim::launch_ps(slim::kPsRscan, a, 0, 0, s);
+      if (er != hipSuccess) return er;
+      Gafter = gb[cg];
+      cg ^= 1;
+      a.dW_part = dw_part + (size_t)BH * NW * MD;
+      er = slim::launch_ps(slim::kPsGk, a, nwg, 0, s);
+      if (er != hipSuccess) return er;
+    }
+    return hipSuccess;
+  });
+  if (e != hipSuccess) return hip_fail(e, "PS-mode backward launches");
+  // (3) the cotangent of state_in, relative to kshift_in (FAVOR+ with an initial state)
+  if (dstate_in != nullptr) {
+    e = slim::launch_state_combine(Gafter, SZ, favor ? kshift_in : nullptr, favor ? kshift : nullptr, nullptr, 0, 1.f,
+                                   dstate_in, BH, SZ, s);
+    if (e != hipSuccess) return hip_fail(e, "dstate_in launch");
+  }
+  e = slim::launch_dw_reduce(dw_part, 2 * BH * NW, (int)MD, dW, s);
+  if (e != hipSuccess) return hip_fail(e, "dW-reduction launch");
+  return ok();
+}
+
 // The forward of slim_fwd on a given workspace (the caller's, or the
 // library's static scratch for slim_fwd_noalloc).
 int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
@@ -858,6 +1094,8 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
   const size_t need = fwd_ws_bytes(p);
   if (need > 0 && (ws == nullptr || ws_bytes < need))
     return fail(SLIM_EWORKSPACE, "forward workspace needs %zu bytes, got %zu", need, ws == nullptr ? 0 : ws_bytes);
+  if (ps(p))
+    return ps_fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, (char*)ws, (hipStream_t)stream);
   const Dispatch dp = dispatch(p);
   if (quad(p))
     return quad_fwd_impl(p, dp, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, (char*)ws,
@@ -1065,6 +1303,9 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   const size_t need = bwd_ws_bytes(p);
   if (ws == nullptr || ws_bytes < need)
     return fail(SLIM_EWORKSPACE, "backward workspace needs %zu bytes, got %zu", need, ws == nullptr ? 0 : ws_bytes);
+  if (ps(p))
+    return ps_bwd_impl(p, Q, K, V, W, state_in, kshift_in, kshift, dY, dstate_out, dQ, dK, dV, dW, dstate_in, (char*)ws,
+                       (hipStream_t)stream);
   const Dispatch dp = dispatch(p);
   if (quad(p))
     return quad_bwd_impl(p, dp, Q, K, V, W, state_in, kshift_in, kshift, dY, dstate_out, dQ, dK, dV, dW, dstate_in,

@@ -237,6 +237,51 @@ hipError_t launch_dw_reduce(const float* part, int n_parts, int n, float* dW, hi
   X(bf16, 64, 16, 32, kSquare) X(bf16, 32, 16, 32, kSquare)                               \
   X(float, 64, 16, 32, kSquare) X(float, 32, 16, 32, kSquare)
 
+// Explicit prefix-sum within-slice mode (slim_ps.hip): the states of every
+// row of a slice written out, then used; streaming kernels for any
+// configuration.  Launch selector `which`:
+enum PsKernel {
+  kPsKmax = 0,   // part[head][wg]: largest key exponent of the rows a workgroup visits
+  kPsTerms = 1,  // U[head][i] = g(k)^T [v | 1] for the slice's rows
+  kPsScan0 = 2,  // prefix sums of U from S_in (or zero); S_out = the last
+  kPsScan1 = 3,  // S_out = S_in - sum U (eq. 17), then prefix sums from it
+  kPsScan2 = 4,  // S_out = S_in (exact), then prefix sums from it
+  kPsOut = 5,    // Y of the slice's rows from U
+  kPsGq = 6,     // dq, dW (queries), query terms g(q) [dN | dD] -> Gh
+  kPsRscan = 7,  // reverse prefix sums of Gh from G_in (or zero); G_out = the first
+  kPsGk = 8,     // dk, dv, dW (keys) from Gh
+  kPsSum = 9     // part[head][r][m][e]: what the rows of slices [r NS / P2, (r + 1) NS / P2) add
+};
+struct PsArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const void* dY;
+  const float* W;       // [M, d]
+  const float* kshift;  // [B H] FAVOR+ key shift
+  void* Y;
+  void* dQ;
+  void* dK;
+  void* dV;
+  float* U;             // [B H][C][d + 1][M] the slice's states (or its rows' terms)
+  float* Gh;            // [B H][C][d + 1][M] query terms, then the states' cotangents
+  const float* S_in;    // state of head h at S_in + h in_stride ([m][d + 1])
+  size_t in_stride;
+  float* S_out;         // [B H][M][d + 1]
+  const float* G_in;    // [B H][M][d + 1] cotangent after the slice, or nullptr (zero)
+  float* G_out;         // [B H][M][d + 1] cotangent before the slice
+  float* part;          // kPsKmax: [B H][workgroups]; kPsSum: [B H][P2][M][d + 1]
+  float* dW_part;       // [B H][nslot][M][d], added to (workgroup w of head h: slot h nslot + w)
+  int nslot;
+  int B, H, L, d, M, C;  // C: rows of U and Gh per head (the longest slice)
+  int row0, rows;        // the slice
+  int kind;              // Kind
+  float relu_eps;
+  int bf16;              // element type of Q, K, V, dY, Y, dQ, dK, dV: bf16 (1) or float (0)
+};
+// grid (nwg, B H); extra: kPsSum's slice count
+hipError_t launch_ps(int which, const PsArgs& a, int nwg, int extra, hipStream_t s);
+
 // configurations of the whole-slice quadratic form (bf16, 32 or 64 features
 // per wave)
 #define SLIM_FOR_EACH_QUAD_CONFIG(X)                                                  \

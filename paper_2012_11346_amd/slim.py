@@ -21,8 +21,8 @@ FAVOR_PLUS, RELU, SQUARE = 0, 1, 2
 F32, BF16 = 0, 1
 QUERY, KEY = 0, 1
 PHASE_FWD, PHASE_BWD = 0, 1
-WITHIN_ITER, WITHIN_QUADRATIC = 0, 1
-WITHINS = {"iter": WITHIN_ITER, "quadratic": WITHIN_QUADRATIC}
+WITHIN_ITER, WITHIN_QUADRATIC, WITHIN_PS = 0, 1, 2
+WITHINS = {"iter": WITHIN_ITER, "quadratic": WITHIN_QUADRATIC, "ps": WITHIN_PS}
 
 KINDS = {"favor+": FAVOR_PLUS, "relu": RELU, "square": SQUARE}
 DTYPES = {torch.float32: F32, torch.bfloat16: BF16}

@@ -234,3 +234,23 @@ def test_model_param_shapes_match_the_synthetic_model(S):
     assert list(P) == S.model_param_names(cfg.s) and set(shp) == set(P)
     for k, v in P.items():
         assert tuple(v.shape) == shp[k], k
+
+
+def test_ps_mode_sizing_and_checks(S):
+    """The explicit prefix-sum mode: any dtype and shape (float32 at d = 64,
+    M = 256 included), its states written out for C rows (the workspace grows
+    with C, and is flat in L once the sequence has at least 64 slices); no
+    dropout."""
+    p = lambda **kw: _p(S, within=S.WITHIN_PS, **kw)
+    f32 = p(dtype=S.F32, L=4096)
+    assert S.workspace_bytes(f32, S.PHASE_FWD) > 0 and S.workspace_bytes(f32, S.PHASE_BWD) > 0
+    ws0 = lambda q, ph: S.LIB.slim_workspace_bytes(ctypes.byref(q), ph)  # 0 for a rejected problem
+    assert ws0(_p(S, dtype=S.F32, L=4096), S.PHASE_FWD) == 0  # the other modes reject it
+    a, b = (S.workspace_bytes(p(C=c, L=1 << 16), S.PHASE_FWD) for c in (64, 128))
+    assert 1.8 * a < b < 2.2 * a
+    # the backward's grows linearly in C (twice the rows' states, plus parts of fixed size)
+    w = [S.workspace_bytes(p(C=c, L=1 << 16), S.PHASE_BWD) for c in (64, 128, 192)]
+    assert abs((w[2] - w[1]) - (w[1] - w[0])) <= 1024 and w[1] - w[0] > 1.9 * (b - a)
+    assert len({S.workspace_bytes(p(C=64, L=L), S.PHASE_BWD) for L in (1 << 13, 1 << 16, 1 << 19)}) == 1
+    assert ws0(p(dropout=0.1), S.PHASE_FWD) == 0
+    assert S.context_bytes(p(L=1 << 16)) == 0
