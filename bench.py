@@ -12,7 +12,9 @@ whole batch, and, unless switched off:
   walk, peak device memory beyond inputs and outputs, the lower bound "L/B"
   (the same measured on an input of length C) and the L2-relative gradient
   error against the oracle; then the same slice lengths with each slice
-  evaluated as one masked quadratic form (the within-slice quadratic mode);
+  evaluated as one masked quadratic form (the within-slice quadratic mode),
+  and, up to C = 4096, with every row's state written out (the explicit
+  prefix-sum mode, "PS");
 * configs: the other workloads (tiny fp32 exactness check, B8 H8 L4096,
   L=262144 long context, the six-layer ReLU stack run forward r=1..6 then
   backward r=6..1), each with time, roofline and parity on sampled heads;
@@ -439,6 +441,25 @@ def main():
             qsweep.append(rec)
             log(f"quadratic sweep C={Cs}: {rs['ms']:.3f} ms/step, beyond inputs/outputs {rs['extra'] / 2**20:.1f} MiB")
         out["sweep_quadratic"] = qsweep
+        # the explicit prefix-sum mode ("PS"): every row's state of a slice
+        # written out (C M (d + 1) floats per head, twice in the backward);
+        # C = 32768 would hold 2 x 70 GB of states and is left out
+        psweep = []
+        for Cs in [c for c in wl.C if c <= 4096]:
+            ly = Layer(x, Cs, kind, within="ps")
+            rs = timed([ly], 2, 1)
+            rec = {"C": Cs, "tokens_per_s": tokens / (rs["ms"] / 1e3), "ms_per_step": rs["ms"], "steps": 2,
+                   "peak_bytes": rs["peak"], "beyond_io_bytes": rs["extra"], "workspace_bytes": rs["ws"]}
+            if ref is not None:
+                e = parity(ly, sample, ref)
+                rec["grad_l2_rel"] = {k: v["l2_rel"] for k, v in e.items() if k != "Y"}
+                rec["max_rel"] = {k: v["max_rel"] for k, v in e.items()}
+            ly.free()
+            del ly
+            torch.cuda.empty_cache()
+            psweep.append(rec)
+            log(f"PS sweep C={Cs}: {rs['ms']:.3f} ms/step, beyond inputs/outputs {rs['extra'] / 2**20:.1f} MiB")
+        out["sweep_ps"] = psweep
 
     # ------------------------------------------------------------ headline parity and oracle timing
     if not args.no_cpu:
