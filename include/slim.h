@@ -95,7 +95,8 @@ typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1, SLIM_WITHIN_PS =
  *   B, H, L  batch, heads, sequence length (each >= 1; B H <= 65535 and one
  *            head's rows, L d elements, within 1 GiB, else SLIM_EUNSUPPORTED)
  *   d        head dimension: 32 or 64
- *   M        number of features: 64, 128 or 256 (SLIM_SQUARE: 64)
+ *   M        number of features: 64, 128 or 256 (SLIM_SQUARE: 64); with
+ *            SLIM_F32, d M <= 4096 except in SLIM_WITHIN_PS
  *   C        slice length (Sec. 3.2): >= 1; values above L act as L.  The
  *            sequence is cut into N = ceil(L / C) slices, the last one ragged.
  *   dtype    slim_dtype of Q, K, V, Y, dY, dQ, dK, dV.  With SLIM_BF16 every
@@ -103,7 +104,8 @@ typedef enum { SLIM_WITHIN_ITER = 0, SLIM_WITHIN_QUADRATIC = 1, SLIM_WITHIN_PS =
  *            enters the logits w_m . x as the pair hi = bf16(w), lo =
  *            bf16(w - hi) (one product each, about 16 significant bits of
  *            W) and the chain rule (dq, dk) as hi; with SLIM_F32 products
- *            are float32.
+ *            are float32.  SLIM_WITHIN_PS computes everything in float32
+ *            from the float32 W for either dtype.
  *   kind     slim_kind
  *   relu_eps additive constant of the ReLU map (the usual value is 1e-3)
  *   dropout  probability p in [0, 1) of value dropout (0: none), and
