@@ -17,7 +17,8 @@ whole batch, and, unless switched off:
   prefix-sum mode, "PS");
 * configs: the other workloads (tiny fp32 exactness check, B8 H8 L4096,
   L=262144 long context, the six-layer ReLU stack run forward r=1..6 then
-  backward r=6..1), each with time, roofline and parity on sampled heads;
+  backward r=6..1), each with time, roofline and parity on sampled heads,
+  and the headline shape in float32 (explicit prefix-sum mode);
 * peak memory versus L at fixed C;
 * the paper's own feature map (element-wise square, M = d = 64, W = I) at
   its per-layer shapes.
@@ -531,6 +532,23 @@ def main():
                 ly.free()
             del layers, xs
             torch.cuda.empty_cache()
+        # the headline shape in float32: of the three within-slice modes only
+        # the explicit prefix-sum one takes float32 with d M > 4096
+        w32 = workload("sweep_32k").with_(name="sweep_32k_f32", dtype="f32")
+        x32 = make_inputs(w32)
+        ly = Layer(x32, 64, w32.kind, within="ps")
+        rc = timed([ly], 2, 1)
+        rec = {"workload": f"sweep_32k_f32: {KIND_LABEL[w32.kind]}, B={w32.B} H={w32.H} L={w32.L} d={w32.d} M={w32.M}, "
+                           "float32, C=64, explicit prefix-sum within-slice mode",
+               "C": 64, "ms_per_step": rc["ms"], "tokens_per_s": w32.B * w32.L / (rc["ms"] / 1e3),
+               "peak_bytes": rc["peak"], "beyond_io_bytes": rc["extra"]}
+        if not args.no_cpu:
+            rec["parity_sampled_head"] = parity(ly, [(2, 5)], oracle_heads(x32, [(2, 5)], w32.kind))
+        configs.append(rec)
+        log(f"sweep_32k_f32 (PS mode): {rc['ms']:.3f} ms/step")
+        ly.free()
+        del ly, x32
+        torch.cuda.empty_cache()
         out["configs"] = configs
 
         # peak memory beyond inputs and outputs versus L at fixed C
