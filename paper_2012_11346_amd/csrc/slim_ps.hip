@@ -165,6 +165,15 @@ __global__ __launch_bounds__(kPsThreads) void ps_terms_kernel(PsArgs a) {
   }
 }
 
+// s += x with the rounding error carried in c (Kahan's compensated sum: the
+// running sums over a slice's rows keep float32 accuracy instead of losing
+// it in proportion to the row count)
+__device__ __forceinline__ void kahan_add(float& s, float& c, float x) {
+  const float y = x - c, t = s + y;
+  c = (t - s) - y;
+  s = t;
+}
+
 // ---- prefix sums over the slice's rows, one thread per state entry (e, m):
 //   mode 0: u = S_in (zero if NULL), U[i] <- u += U[i], S_out = the last u
 //   mode 1: S_out = S_in - sum_i U[i] (eq. 17: the state before the slice
@@ -182,13 +191,14 @@ __global__ __launch_bounds__(kPsThreads) void ps_scan_kernel(PsArgs a, int mode)
   const size_t step = (size_t)E * M;
   float u = a.S_in != nullptr ? a.S_in[head * a.in_stride + sidx] : 0.f;
   if (mode == 1) {
-    float s = 0.f;
-    for (int i = 0; i < a.rows; ++i) s += U[i * step];
+    float s = 0.f, c = 0.f;
+    for (int i = 0; i < a.rows; ++i) kahan_add(s, c, U[i * step]);
     u -= s;
   }
   if (mode != 0) a.S_out[head * (size_t)M * E + sidx] = u;
+  float c = 0.f;
   for (int i = 0; i < a.rows; ++i) {
-    u += U[i * step];
+    kahan_add(u, c, U[i * step]);
     U[i * step] = u;
   }
   if (mode == 0 && a.S_out != nullptr) a.S_out[head * (size_t)M * E + sidx] = u;
@@ -205,9 +215,9 @@ __global__ __launch_bounds__(kPsThreads) void ps_rscan_kernel(PsArgs a) {
   const size_t sidx = head * (size_t)M * E + (size_t)m * E + e;
   float* Gh = a.Gh + (size_t)head * a.C * E * M + el;
   const size_t step = (size_t)E * M;
-  float g = a.G_in != nullptr ? a.G_in[sidx] : 0.f;
+  float g = a.G_in != nullptr ? a.G_in[sidx] : 0.f, c = 0.f;
   for (int i = a.rows - 1; i >= 0; --i) {
-    g += Gh[i * step];
+    kahan_add(g, c, Gh[i * step]);
     Gh[i * step] = g;
   }
   a.G_out[sidx] = g;
@@ -404,9 +414,9 @@ __global__ __launch_bounds__(kPsThreads) void ps_sum_kernel(PsArgs a, int NS, in
   const float shift = a.kind == kFavor ? a.kshift[head] : 0.f, ism = rsqrtf((float)M);
   const int s0 = (int)((int64_t)r * NS / P2), s1 = (int)((int64_t)(r + 1) * NS / P2);
   const int l0 = s0 * a.C, l1 = (int)min((int64_t)a.L, (int64_t)s1 * a.C);
-  float acc[D + 1];
+  float acc[D + 1], cmp[D + 1];
 #pragma unroll
-  for (int e = 0; e <= D; ++e) acc[e] = 0.f;
+  for (int e = 0; e <= D; ++e) acc[e] = cmp[e] = 0.f;
   for (int l = l0; l < l1; ++l) {
     const size_t row = head * a.L + l;
     __syncthreads();
@@ -416,8 +426,8 @@ __global__ __launch_bounds__(kPsThreads) void ps_sum_kernel(PsArgs a, int NS, in
     if (m < M) {
       const float phi = ps_key_feature(a.kind, ps_logit<D>(Wt, M, x, m), ps_norm2<D>(x), shift, ism, a.relu_eps);
 #pragma unroll
-      for (int e = 0; e < D; ++e) acc[e] = fmaf(phi, v[e], acc[e]);
-      acc[D] += phi;
+      for (int e = 0; e < D; ++e) kahan_add(acc[e], cmp[e], phi * v[e]);
+      kahan_add(acc[D], cmp[D], phi);
     }
   }
   if (m < M) {

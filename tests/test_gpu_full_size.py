@@ -37,14 +37,14 @@ def _oracle(x, heads, kind):
     return Y, dQ, dK, dV, dW
 
 
-def _check(tag, x, heads, C, kind, ref):
+def _check(tag, x, heads, C, kind, ref, within="iter"):
     from paper_2012_11346_amd import slim
 
     tol = TOL[{torch.bfloat16: "bf16", torch.float32: "f32"}[x["Q"].dtype]]
-    print(f"[full size] {tag} C={C}: forward + backward on the whole batch", flush=True)
+    print(f"[full size] {tag} C={C} {within}: forward + backward on the whole batch", flush=True)
     Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
-    Y, st, ks = slim.fwd(Q, K, V, W, C, kind)
-    g = slim.bwd(Q, K, V, W, dY, C, ks, kind)
+    Y, st, ks = slim.fwd(Q, K, V, W, C, kind, within=within)
+    g = slim.bwd(Q, K, V, W, dY, C, ks, kind, within=within)
     torch.cuda.synchronize()
     Yr, dQr, dKr, dVr, dWr = ref
     report(f"{tag} C={C} Y (sampled heads)", _sample(Y, heads), Yr, tol)
@@ -56,7 +56,7 @@ def _check(tag, x, heads, C, kind, ref):
     for b, h in heads:
         mask[b, h] = True
     dYm = torch.where(mask[:, :, None, None], dY, torch.zeros_like(dY))
-    gm = slim.bwd(Q, K, V, W, dYm, C, ks, kind)
+    gm = slim.bwd(Q, K, V, W, dYm, C, ks, kind, within=within)
     torch.cuda.synchronize()
     report(f"{tag} C={C} dW (sampled heads' share)", host64(gm[3]), dWr, tol)
     for n, a, full in zip(("dQ", "dK", "dV"), gm[:3], g[:3]):
@@ -99,6 +99,19 @@ def test_slice_sweep_full_size_rounded_w():
     print("[full size] oracle on the sampled head (rounded W)", flush=True)
     ref = _oracle(x, heads, wl.kind)
     _check(wl.name + " rounded W", x, heads, 64, wl.kind, ref)
+
+
+def test_headline_shape_float32_ps_mode():
+    """The headline problem in float32 (B=4, H=8, L=32768, d=64, M=256,
+    C=64): the explicit prefix-sum mode, the one that takes float32 at
+    d M > 4096, at the float32 bar."""
+    need_gpu()
+    wl = workload("sweep_32k").with_(name="sweep_32k_f32", dtype="f32")
+    heads = [(2, 5)]
+    x = make_inputs(wl)
+    print("[full size] oracle on the sampled head (float32 inputs)", flush=True)
+    ref = _oracle(x, heads, wl.kind)
+    _check(wl.name, x, heads, 64, wl.kind, ref, within="ps")
 
 
 def test_long_context_full_size():
