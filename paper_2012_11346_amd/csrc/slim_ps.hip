@@ -190,16 +190,36 @@ __global__ __launch_bounds__(kPsThreads) void ps_scan_kernel(PsArgs a, int mode)
   float* U = a.U + (size_t)head * a.C * E * M + el;
   const size_t step = (size_t)E * M;
   float u = a.S_in != nullptr ? a.S_in[head * a.in_stride + sidx] : 0.f;
+  constexpr int U8 = 8;  // rows whose loads are issued together
   if (mode == 1) {
     float s = 0.f, c = 0.f;
-    for (int i = 0; i < a.rows; ++i) kahan_add(s, c, U[i * step]);
+    int i = 0;
+    for (; i + U8 <= a.rows; i += U8) {
+      float t[U8];
+#pragma unroll
+      for (int j = 0; j < U8; ++j) t[j] = U[(size_t)(i + j) * step];
+#pragma unroll
+      for (int j = 0; j < U8; ++j) kahan_add(s, c, t[j]);
+    }
+    for (; i < a.rows; ++i) kahan_add(s, c, U[(size_t)i * step]);
     u -= s;
   }
   if (mode != 0) a.S_out[head * (size_t)M * E + sidx] = u;
   float c = 0.f;
-  for (int i = 0; i < a.rows; ++i) {
-    kahan_add(u, c, U[i * step]);
-    U[i * step] = u;
+  int i = 0;
+  for (; i + U8 <= a.rows; i += U8) {
+    float t[U8];
+#pragma unroll
+    for (int j = 0; j < U8; ++j) t[j] = U[(size_t)(i + j) * step];
+#pragma unroll
+    for (int j = 0; j < U8; ++j) {
+      kahan_add(u, c, t[j]);
+      U[(size_t)(i + j) * step] = u;
+    }
+  }
+  for (; i < a.rows; ++i) {
+    kahan_add(u, c, U[(size_t)i * step]);
+    U[(size_t)i * step] = u;
   }
   if (mode == 0 && a.S_out != nullptr) a.S_out[head * (size_t)M * E + sidx] = u;
 }
@@ -216,9 +236,21 @@ __global__ __launch_bounds__(kPsThreads) void ps_rscan_kernel(PsArgs a) {
   float* Gh = a.Gh + (size_t)head * a.C * E * M + el;
   const size_t step = (size_t)E * M;
   float g = a.G_in != nullptr ? a.G_in[sidx] : 0.f, c = 0.f;
-  for (int i = a.rows - 1; i >= 0; --i) {
-    kahan_add(g, c, Gh[i * step]);
-    Gh[i * step] = g;
+  constexpr int U8 = 8;  // rows whose loads are issued together
+  int i = a.rows - 1;
+  for (; i - U8 + 1 >= 0; i -= U8) {
+    float t[U8];
+#pragma unroll
+    for (int j = 0; j < U8; ++j) t[j] = Gh[(size_t)(i - j) * step];
+#pragma unroll
+    for (int j = 0; j < U8; ++j) {
+      kahan_add(g, c, t[j]);
+      Gh[(size_t)(i - j) * step] = g;
+    }
+  }
+  for (; i >= 0; --i) {
+    kahan_add(g, c, Gh[(size_t)i * step]);
+    Gh[(size_t)i * step] = g;
   }
   a.G_out[sidx] = g;
 }
