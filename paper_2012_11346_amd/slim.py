@@ -247,8 +247,8 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
         Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0, within="iter"):
     """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None).
     ctx (optional, from new_context) receives the segment boundary states for bwd.
-    dropout / seed: value dropout with per-slice seeds; within: "iter" or
-    "quadratic" (include/slim.h)."""
+    dropout / seed: value dropout with per-slice seeds; within: "iter",
+    "quadratic" or "ps" (include/slim.h)."""
     p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed, within)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V)):
@@ -309,6 +309,37 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
                         _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
                         _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
     return dQ, dK, dV, dW, dstate_in
+
+
+class _Attention(torch.autograd.Function):
+    """slim_fwd as a torch operation whose backward is slim_bwd: between the
+    two only the key shift and the state-sized context are kept (with the
+    inputs, which autograd holds anyway)."""
+
+    @staticmethod
+    def forward(fctx, Q, K, V, W, C, kind, relu_eps, dropout, seed, within):
+        c = new_context(Q, W, C, kind, relu_eps, within)
+        Y, _, ks = fwd(Q, K, V, W, C, kind, relu_eps=relu_eps, ctx=c, dropout=dropout, seed=seed, within=within)
+        fctx.save_for_backward(Q, K, V, W)
+        fctx.args = (C, kind, relu_eps, dropout, seed, within, ks, c)
+        return Y
+
+    @staticmethod
+    def backward(fctx, dY):
+        Q, K, V, W = fctx.saved_tensors
+        C, kind, relu_eps, dropout, seed, within, ks, c = fctx.args
+        dQ, dK, dV, dW, _ = bwd(Q, K, V, W, dY.contiguous(), C, ks, kind, relu_eps=relu_eps, ctx=c, dropout=dropout,
+                                seed=seed, within=within)
+        return dQ, dK, dV, dW, None, None, None, None, None, None
+
+
+def attention(Q, K, V, W, C: int, kind="favor+", relu_eps: float = 1e-3, dropout: float = 0.0, seed: int = 0,
+              within="iter"):
+    """Causal linear attention Y (eq. 2) of Q, K, V [B, H, L, d] with the
+    features of W [M, d], computed slice by slice (Algorithm 1), as a
+    differentiable torch operation: gradients reach Q, K, V and W through
+    slim_bwd.  Arguments as in fwd."""
+    return _Attention.apply(Q, K, V, W, C, kind, relu_eps, dropout, seed, within)
 
 
 def fwd_noalloc(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3,
