@@ -65,15 +65,28 @@ enum EpiOp { EPI_STORE = 0, EPI_ACC = 1, EPI_BIAS = 2, EPI_BIAS_GELU = 3, EPI_GE
 // STORE: C = v; ACC: C += v; BIAS: C = v + bias[n]; BIAS_GELU: C = z = v +
 // bias[n], C2 = GeLU(z); GELU_BWD: C = v GeLU'(aux); ADD: C = v + aux.
 // aux and C2 share C's leading dimension.
+// Where C lives: one row-major matrix (layout 0); or the columns cut into
+// groups of gcols, group g a row-major matrix of its own at Cg[g] (layout 1),
+// or a [B][heads][hrows][64] head-split tensor at Cg[g] for row m = b hrows +
+// t, column h 64 + c of the group (layout 2).  bias, aux and C2 serve layout 0.
 struct Epi {
   int op;
   const float* bias;
   const float* aux;
   float* C2;
+  int layout, gcols, hrows, heads;
+  float *Cg0, *Cg1, *Cg2;  // separate members: an indexed array would go to scratch
 };
 
-__device__ __forceinline__ void epi_store(const Epi& e, float* C, int ldc, int m, int n, float v) {
-  const size_t o = (size_t)m * ldc + n;
+// group of column (or row) i for groups of g: 0, 1 or 2 (selects, no divide)
+__device__ __forceinline__ int group3(int i, int g) { return (i >= g) + (i >= 2 * g); }
+template <typename T>
+__device__ __forceinline__ T pick3(int grp, T a, T b, T c) {
+  return grp == 0 ? a : (grp == 1 ? b : c);
+}
+
+// the epilogue's operation on element o of C (n: the column, for the bias)
+__device__ __forceinline__ void epi_op(const Epi& e, float* C, size_t o, int n, float v) {
   switch (e.op) {
     case EPI_STORE: C[o] = v; break;
     case EPI_ACC: C[o] += v; break;
@@ -88,6 +101,26 @@ __device__ __forceinline__ void epi_store(const Epi& e, float* C, int ldc, int m
     default: C[o] = v + e.aux[o]; break;
   }
 }
+// where element (m, n) of the product goes: its matrix (C or a group's) and
+// the offset in it; the row's and the column's parts of the offset add
+__device__ __forceinline__ size_t epi_row(const Epi& e, int ldc, int m) {
+  if (e.layout == 2) {
+    const int b = m / e.hrows, t = m - b * e.hrows;
+    return ((size_t)b * e.heads * e.hrows + t) * 64;
+  }
+  return (size_t)m * ldc;
+}
+__device__ __forceinline__ size_t epi_col(const Epi& e, float*& C, int n) {
+  if (e.layout == 0) return n;
+  const int grp = group3(n, e.gcols), col = n - grp * e.gcols;
+  C = pick3(grp, e.Cg0, e.Cg1, e.Cg2);
+  return e.layout == 1 ? (size_t)col : (size_t)(col >> 6) * e.hrows * 64 + (col & 63);
+}
+__device__ __forceinline__ void epi_store(const Epi& e, float* C, int ldc, int m, int n, float v) {
+  const size_t ro = epi_row(e, ldc, m);
+  const size_t co = epi_col(e, C, n);
+  epi_op(e, C, ro + co, n, v);
+}
 
 struct GemmArgs {
   int M, N, K;
@@ -101,6 +134,11 @@ struct GemmArgs {
   int kchunk;   // k per split (a multiple of GBK)
   float* part;  // [splits][M][N] partial products when gridDim.y > 1
   int tiles_n;
+  // grouped B (gN > 0: columns of op(B) in groups of gN, group g at Bg[g],
+  // each with leading dimension ldb; gK > 0: rows of op(B) in groups of gK,
+  // a multiple of GBK, likewise)
+  const float *Bg0, *Bg1, *Bg2;
+  int gN, gK;
 };
 
 // four consecutive floats, `avail` of them valid (zeros beyond)
@@ -115,7 +153,9 @@ __device__ __forceinline__ float4 ld4(const float* p, int avail) {
   return r;
 }
 
-template <int BM, bool TA, bool TB, bool VEC>
+// GRP: grouped B and grouped / head-split C (the kernels without it carry no
+// code, and no registers, for either)
+template <int BM, bool TA, bool TB, bool VEC, bool GRP>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int AV = BM * GBK / 4 / 256;  // float4 loads per thread per k tile (A)
   constexpr int BV = GBN * GBK / 4 / 256;  // (B)
@@ -135,6 +175,19 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * 64;
   const int M = g.M, N = g.N;
 
+  // grouped B along n: each thread's columns are the same in every k tile,
+  // so its group's base pointer is fixed before the loop
+  const float* bcol[BV];
+#pragma unroll
+  for (int i = 0; i < BV; ++i) {
+    const int n = n0 + 4 * ((tid + 256 * i) % (GBN / 4));
+    bcol[i] = g.B + n;
+    if (GRP && !TB && g.gN > 0 && n < N) {
+      const int grp = group3(n, g.gN);
+      bcol[i] = pick3(grp, g.Bg0, g.Bg1, g.Bg2) + (n - grp * g.gN);
+    }
+  }
+
   float4 ra[AV], rb[BV];
   auto load = [&](int k0) {
 #pragma unroll
@@ -153,10 +206,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       const int f = tid + 256 * i;
       if (TB) {  // rows of B^T: 4 k per vector
         const int n = f >> 2, k = k0 + 4 * (f & 3);
-        rb[i] = (n0 + n < N) ? ld4<VEC>(g.B + (size_t)(n0 + n) * g.ldb + k, kend - k) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float* Bb = g.B;
+        int kk = k;
+        if (GRP && g.gK > 0) {  // the k tile lies in one group (k0 is uniform)
+          const int grp = group3(k0, g.gK);
+          Bb = pick3(grp, g.Bg0, g.Bg1, g.Bg2);
+          kk = k - grp * g.gK;
+        }
+        rb[i] = (n0 + n < N) ? ld4<VEC>(Bb + (size_t)(n0 + n) * g.ldb + kk, kend - k) : make_float4(0.f, 0.f, 0.f, 0.f);
       } else {  // rows of B: 4 n per vector
         const int k = k0 + f / (GBN / 4), n = n0 + 4 * (f % (GBN / 4));
-        rb[i] = (k < kend) ? ld4<VEC>(g.B + (size_t)k * g.ldb + n, N - n) : make_float4(0.f, 0.f, 0.f, 0.f);
+        rb[i] = (k < kend) ? ld4<VEC>(bcol[i] + (size_t)k * g.ldb, N - n) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
   };
@@ -231,6 +291,28 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     buf ^= 1;
   }
   const bool split = gridDim.y > 1;
+  if (GRP && !split) {
+    // the tile's row offsets once, in LDS (the operand buffers are free
+    // after the loop's last barrier), the column offsets once per j
+    size_t* rowoff = reinterpret_cast<size_t*>(&As[0][0]);
+    for (int i = tid; i < BM; i += 256) rowoff[i] = epi_row(g.epi, g.ldc, min(m0 + i, M - 1));
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + wn + 16 * j + c;
+      if (n >= N) continue;
+      float* Cj = g.C;
+      const size_t co = epi_col(g.epi, Cj, n);
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int mm = wm + 16 * i + 4 * q + r;
+          if (m0 + mm < M) epi_op(g.epi, Cj, rowoff[mm] + co, n, acc[i][j][r]);
+        }
+    }
+    return;
+  }
   float* part = g.part + (size_t)blockIdx.y * M * N;
 #pragma unroll
   for (int i = 0; i < TI; ++i)
@@ -241,7 +323,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
         if (m < M && n < N) {
           if (split) part[(size_t)m * N + n] = acc[i][j][r];
-          else epi_store(g.epi, g.C, g.ldc, m, n, acc[i][j][r]);
+          else epi_op(g.epi, g.C, (size_t)m * g.ldc + n, n, acc[i][j][r]);
         }
       }
 }
@@ -280,22 +362,27 @@ inline size_t gemm_part_bytes(int M, int N, int K) {
   return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
 }
 
-template <int BM, bool TA, bool TB>
+template <int BM, bool TA, bool TB, bool GRP>
 void gemm_launch(const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
-  if (vec) hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, true>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, false>), grid, dim3(256), 0, s, a);
+  if (vec) hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, true, GRP>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, false, GRP>), grid, dim3(256), 0, s, a);
 }
-template <int BM>
+template <int BM, bool GRP>
 void gemm_launch(bool ta, bool tb, const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
-  if (ta && tb) gemm_launch<BM, true, true>(a, grid, vec, s);
-  else if (ta) gemm_launch<BM, true, false>(a, grid, vec, s);
-  else if (tb) gemm_launch<BM, false, true>(a, grid, vec, s);
-  else gemm_launch<BM, false, false>(a, grid, vec, s);
+  if (ta && tb) gemm_launch<BM, true, true, GRP>(a, grid, vec, s);
+  else if (ta) gemm_launch<BM, true, false, GRP>(a, grid, vec, s);
+  else if (tb) gemm_launch<BM, false, true, GRP>(a, grid, vec, s);
+  else gemm_launch<BM, false, false, GRP>(a, grid, vec, s);
 }
 
-// part: workspace for the partial products (gemm_part_bytes of the shape)
+// part: workspace for the partial products (gemm_part_bytes of the shape);
+// grp: grouped B (Bg, gN, gK of GemmArgs), or nullptr
+struct GroupB {
+  const float* Bg[3];
+  int gN, gK;
+};
 hipError_t gemm(bool ta, bool tb, int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
-                int ldc, Epi epi, float* part, hipStream_t s) {
+                int ldc, Epi epi, float* part, hipStream_t s, const GroupB* grp = nullptr) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const GemmPlan p = gemm_plan(M, N, K);
   GemmArgs a;
@@ -312,10 +399,29 @@ hipError_t gemm(bool ta, bool tb, int M, int N, int K, const float* A, int lda, 
   a.kchunk = p.kchunk;
   a.part = part;
   a.tiles_n = p.tiles_n;
-  const bool vec = lda % 4 == 0 && ldb % 4 == 0 && ((uintptr_t)A & 15) == 0 && ((uintptr_t)B & 15) == 0;
+  a.gN = a.gK = 0;
+  a.Bg0 = a.Bg1 = a.Bg2 = nullptr;
+  bool bal = ((uintptr_t)B & 15) == 0;
+  if (grp != nullptr) {
+    // a float4 of B, or a k tile, must not straddle two groups
+    if (grp->gN % 4 != 0 || grp->gK % GBK != 0) return hipErrorInvalidValue;
+    a.gN = grp->gN;
+    a.gK = grp->gK;
+    a.Bg0 = grp->Bg[0];
+    a.Bg1 = grp->Bg[1];
+    a.Bg2 = grp->Bg[2];
+    for (int i = 0; i < 3; ++i) bal = bal && ((uintptr_t)grp->Bg[i] & 15) == 0;
+  }
+  const bool vec = lda % 4 == 0 && ldb % 4 == 0 && ((uintptr_t)A & 15) == 0 && bal;
   const dim3 grid(p.tiles, p.splits);
-  if (p.BM == 128) gemm_launch<128>(ta, tb, a, grid, vec, s);
-  else gemm_launch<64>(ta, tb, a, grid, vec, s);
+  const bool grouped = a.gN > 0 || a.gK > 0 || epi.layout != 0;
+  if (p.BM == 128) {
+    if (grouped) gemm_launch<128, true>(ta, tb, a, grid, vec, s);
+    else gemm_launch<128, false>(ta, tb, a, grid, vec, s);
+  } else {
+    if (grouped) gemm_launch<64, true>(ta, tb, a, grid, vec, s);
+    else gemm_launch<64, false>(ta, tb, a, grid, vec, s);
+  }
   if (p.splits > 1) {
     const size_t MN = (size_t)M * N;
     hipLaunchKernelGGL(gemm_reduce_kernel, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, p.splits, M, N, C,
@@ -326,10 +432,24 @@ hipError_t gemm(bool ta, bool tb, int M, int N, int K, const float* A, int lda, 
 
 inline Epi epi(int op, const float* bias = nullptr, const float* aux = nullptr, float* C2 = nullptr) {
   Epi e;
+  std::memset(&e, 0, sizeof(e));
   e.op = op;
   e.bias = bias;
   e.aux = aux;
   e.C2 = C2;
+  return e;
+}
+// C in column groups of gcols: row-major matrices (ldc of the call), or
+// head-split tensors of hrows rows and `heads` heads
+inline Epi epi_groups(int op, float* C0, float* C1, float* C2_, int gcols, int hrows = 0, int heads = 0) {
+  Epi e = epi(op);
+  e.layout = hrows > 0 ? 2 : 1;
+  e.gcols = gcols;
+  e.hrows = hrows;
+  e.heads = heads;
+  e.Cg0 = C0;
+  e.Cg1 = C1;
+  e.Cg2 = C2_;
   return e;
 }
 
@@ -515,17 +635,21 @@ __global__ __launch_bounds__(256) void rows_to_heads_kernel(const float* src, in
   const int b = (int)(r / k);
   dst[e] = src[((size_t)b * n + t) * ld + col0 + h * kHead + c];
 }
-__global__ __launch_bounds__(256) void heads_to_rows_kernel(const float* src, float* dst, int ld, int col0, int k, int n,
-                                                            size_t total) {
+// parts consecutive head tensors of `per` floats each: part p goes to the
+// columns from col0 + p colstep
+__global__ __launch_bounds__(256) void heads_to_rows_kernel(const float* src, float* dst, int ld, int col0, int colstep,
+                                                            int k, int n, size_t per, size_t total) {
   const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (e >= total) return;
-  const int c = (int)(e % kHead);
-  size_t r = e / kHead;
+  const int p = (int)(e / per);
+  const size_t ep = e - (size_t)p * per;
+  const int c = (int)(ep % kHead);
+  size_t r = ep / kHead;
   const int t = (int)(r % n);
   r /= n;
   const int h = (int)(r % k);
   const int b = (int)(r / k);
-  dst[((size_t)b * n + t) * ld + col0 + h * kHead + c] = src[e];
+  dst[((size_t)b * n + t) * ld + col0 + p * colstep + h * kHead + c] = src[e];
 }
 
 // dE[v] += sum over the slice's rows with token v of dX0[row], rows in
@@ -594,7 +718,7 @@ slim_problem att_problem(const Dims& m, int n) {
 // workspace regions (byte offsets)
 struct Layout {
   size_t ident, attws, attws_bytes, states, gstates, bprev, delta, snew, wd;
-  size_t X, QKV, Qh, Yh, A, st1, H, Z1, G1, Fo, st2;
+  size_t X, Qh, Yh, A, st1, H, Z1, G1, Fo, st2;
   size_t logits, rowloss, dX, dH, dF, dG1, dA, dYh, dQh, dQKV, P, part, part_bytes, red;
   size_t total;
 };
@@ -625,7 +749,6 @@ Layout layout(const Dims& m) {
   take(l.snew, S * 4);
   take(l.wd, kHead * kHead * 4);
   take(l.X, (s + 1) * R * D * 4);
-  take(l.QKV, R * 3 * D * 4);
   take(l.Qh, s * 3 * HF * 4);
   take(l.Yh, HF * 4);
   take(l.A, s * R * D * 4);
@@ -651,8 +774,8 @@ Layout layout(const Dims& m) {
   size_t pb = 0;
   for (int n : {m.nmax, last}) {
     const int rows = (int)(m.B * n), d = m.D, f = m.F, v = m.V;
-    const int shapes[][3] = {{rows, d, d}, {rows, f, d}, {rows, d, f}, {rows, v, d}, {rows, d, v},
-                             {d, v, rows}, {f, d, rows}, {d, f, rows}, {d, d, rows}};
+    const int shapes[][3] = {{rows, 3 * d, d}, {rows, f, d}, {rows, d, f}, {rows, v, d}, {rows, d, v},
+                             {d, v, rows}, {f, d, rows}, {d, f, rows}, {d, 3 * d, rows}, {rows, d, 3 * d}};
     for (const auto& sh : shapes) pb = std::max(pb, gemm_part_bytes(sh[0], sh[1], sh[2]));
   }
   l.part_bytes = pb;
@@ -750,7 +873,6 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
   auto s1r = [&](int r) { return f(lay.st1) + (size_t)r * R * 2; };
   auto s2r = [&](int r) { return f(lay.st2) + (size_t)r * R * 2; };
   auto Qhr = [&](int r, int part) { return f(lay.Qh) + ((size_t)r * 3 + part) * HF; };
-  float* QKV = f(lay.QKV);
   float* Yh = f(lay.Yh);
   float* logits = f(lay.logits);
   float* rowloss = f(lay.rowloss);
@@ -759,7 +881,20 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
   float* part = f(lay.part);
   float* red = f(lay.red);
   auto mm = [&](bool ta, bool tb, int M_, int N_, int K_, const float* A_, int lda, const float* B_, int ldb, float* C_,
-                int ldc, Epi e) { return gemm(ta, tb, M_, N_, K_, A_, lda, B_, ldb, C_, ldc, e, part, s); };
+                int ldc, Epi e, const GroupB* grp = nullptr) {
+    return gemm(ta, tb, M_, N_, K_, A_, lda, B_, ldb, C_, ldc, e, part, s, grp);
+  };
+  // the three projection weights of layer r as one operand: columns (or
+  // rows) D g .. D g + D - 1 of the grouped operand are those of Wq, Wk, Wv
+  auto wqkv = [&](const float* Wq, const float* Wk, const float* Wv, bool along_k) {
+    GroupB gb;
+    gb.Bg[0] = Wq;
+    gb.Bg[1] = Wk;
+    gb.Bg[2] = Wv;
+    gb.gN = along_k ? 0 : D;
+    gb.gK = along_k ? D : 0;
+    return gb;
+  };
   // out0 += column sums of src0 (and out1 += those of src1), rows in order
   auto colsum = [&](int rows, int n, const float* src0, float* out0, const float* src1 = nullptr,
                     float* out1 = nullptr) {
@@ -781,14 +916,10 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
   // activations of every layer stay in its buffers for the backward)
   auto layer_qkv = [&](int r, int n) -> int {
     const int rows = (int)(m.B * n);
-    const size_t hf = (size_t)m.B * k * n * kHead;
-    const float* X = Xr(r);
-    CHECK_HIP(mm(false, false, rows, D, D, X, D, P.l[r].Wq, D, QKV, 3 * D, epi(EPI_STORE)));
-    CHECK_HIP(mm(false, false, rows, D, D, X, D, P.l[r].Wk, D, QKV + D, 3 * D, epi(EPI_STORE)));
-    CHECK_HIP(mm(false, false, rows, D, D, X, D, P.l[r].Wv, D, QKV + 2 * D, 3 * D, epi(EPI_STORE)));
-    for (int part = 0; part < 3; ++part)
-      hipLaunchKernelGGL(rows_to_heads_kernel, grid1(hf), dim3(256), 0, s, QKV, 3 * D, part * D, Qhr(r, part), k, n, hf);
-    CHECK_HIP(hipGetLastError());
+    // [Q K V] = X [Wq Wk Wv], stored straight into the per-head tensors
+    const GroupB gb = wqkv(P.l[r].Wq, P.l[r].Wk, P.l[r].Wv, false);
+    CHECK_HIP(mm(false, false, rows, 3 * D, D, Xr(r), D, nullptr, D, nullptr, 0,
+                 epi_groups(EPI_STORE, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), D, n, k), &gb));
     return SLIM_OK;
   };
   // the rest of layer r (eqs. 5-9) from the state before the slice
@@ -799,7 +930,7 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     const slim_problem p = att_problem(m, n);
     CHECK_SLIM(slim_fwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, state_in, nullptr, Yh, state_out, nullptr, nullptr,
                         attws, lay.attws_bytes, s));
-    hipLaunchKernelGGL(heads_to_rows_kernel, grid1(hf), dim3(256), 0, s, Yh, Ar(r), D, 0, k, n, hf);
+    hipLaunchKernelGGL(heads_to_rows_kernel, grid1(hf), dim3(256), 0, s, Yh, Ar(r), D, 0, 0, k, n, hf, hf);
     hipLaunchKernelGGL(ln_fwd_kernel, dim3(rows), dim3(256), 0, s, Ar(r), P.l[r].g1, P.l[r].b1n, X, Hr(r), s1r(r), D,
                        m.eps);
     CHECK_HIP(mm(false, false, rows, F, D, Hr(r), D, P.l[r].W1, F, Z1r(r), F, epi(EPI_BIAS_GELU, P.l[r].b1, nullptr, G1r(r))));
@@ -894,18 +1025,14 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
       float* gout = gst + ((size_t)(1 - gcur) * m.s + r) * S;
       CHECK_SLIM(slim_bwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, bprev + r * S, nullptr, nullptr, dYh, gin, dQh,
                           dQh + hf, dQh + 2 * hf, wd, gout, nullptr, attws, lay.attws_bytes, s));
-      for (int part = 0; part < 3; ++part)
-        hipLaunchKernelGGL(heads_to_rows_kernel, grid1(hf), dim3(256), 0, s, dQh + part * hf, dQKV, 3 * D, part * D, k, n,
-                           hf);
+      hipLaunchKernelGGL(heads_to_rows_kernel, grid1(3 * hf), dim3(256), 0, s, dQh, dQKV, 3 * D, 0, D, k, n, hf, 3 * hf);
       CHECK_HIP(hipGetLastError());
-      // Q, K, V = X Wq, X Wk, X Wv; dX = dH + sum dZ W^T
-      const float* X = Xr(r);
-      CHECK_HIP(mm(true, false, D, D, rows, X, D, dQKV, 3 * D, gl.Wq, D, epi(EPI_ACC)));
-      CHECK_HIP(mm(true, false, D, D, rows, X, D, dQKV + D, 3 * D, gl.Wk, D, epi(EPI_ACC)));
-      CHECK_HIP(mm(true, false, D, D, rows, X, D, dQKV + 2 * D, 3 * D, gl.Wv, D, epi(EPI_ACC)));
-      CHECK_HIP(mm(false, true, rows, D, D, dQKV, 3 * D, pl.Wq, D, dX, D, epi(EPI_ADD, nullptr, dH)));
-      CHECK_HIP(mm(false, true, rows, D, D, dQKV + D, 3 * D, pl.Wk, D, dX, D, epi(EPI_ACC)));
-      CHECK_HIP(mm(false, true, rows, D, D, dQKV + 2 * D, 3 * D, pl.Wv, D, dX, D, epi(EPI_ACC)));
+      // [Q K V] = X [Wq Wk Wv]: [dWq dWk dWv] += X^T [dQ dK dV];
+      // dX = dH + [dQ dK dV] [Wq Wk Wv]^T
+      CHECK_HIP(mm(true, false, D, 3 * D, rows, Xr(r), D, dQKV, 3 * D, nullptr, D,
+                   epi_groups(EPI_ACC, gl.Wq, gl.Wk, gl.Wv, D)));
+      const GroupB gb = wqkv(pl.Wq, pl.Wk, pl.Wv, true);
+      CHECK_HIP(mm(false, true, rows, D, 3 * D, dQKV, 3 * D, nullptr, D, dX, D, epi(EPI_ADD, nullptr, dH), &gb));
     }
     hipLaunchKernelGGL(embed_bwd_kernel, dim3(V, (D + 255) / 256), dim3(256), 0, s, tokens, m.L, a, n, rows, dX, D, G.emb);
     // the states before this slice become the states after the earlier one
