@@ -3,7 +3,7 @@
 
 One step = slim_fwd + slim_bwd over one batch of the L = 32768 workload
 (B=4, H=8, d=64, M=256, bf16 inputs, FAVOR+), inputs resident in device
-memory.  Prints one JSON line with throughput (tokens/s = B*L / step time),
+memory; the backward gets the forward's outputs Y, key shift and context.  Prints one JSON line with throughput (tokens/s = B*L / step time),
 a roofline entry for the dominant kernel, the fp64 CPU oracle timed on the
 whole batch, and, unless switched off:
 
@@ -217,7 +217,8 @@ def main():
 
         def bwd(self, dY=None):
             slim.bwd(self.Q, self.K, self.V, self.W, self.dY if dY is None else dY, self.C, self.ks, self.kind,
-                     ws=self.wsb, dQ=self.dQ, dK=self.dK, dV=self.dV, dW=self.dW, ctx=self.ctx, within=self.within)
+                     ws=self.wsb, dQ=self.dQ, dK=self.dK, dV=self.dV, dW=self.dW, ctx=self.ctx, within=self.within,
+                     Y=self.Y)
 
     def run_step(layers):
         """forward r = 1..n, then backward r = n..1"""

@@ -224,6 +224,15 @@ int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const 
  *   Q, K, V, W, state_in, kshift_in  as given to slim_fwd
  *   kshift     [B, H]: kshift_out of slim_fwd (FAVOR+; ignored for ReLU)
  *   dY         [B, H, L, d] cotangent of Y
+ *   Y          optional [B, H, L, d]: the Y slim_fwd wrote for these inputs
+ *              (and the same seed), or NULL.  Given, the row cotangents of
+ *              the recomputed slice (dN = dY / D, dD = -rowdot(dY, Y) / D,
+ *              from eq. 2) take the rowdot from it, so the walk recomputes
+ *              only the denominators D, not the numerators N.  Used by the
+ *              bf16 tile walk with d = 32 or 64 and M / 4 in {32, 64}; the
+ *              other configurations and within-slice modes recompute N and
+ *              ignore it.  Y is rounded to the dtype, so the results differ
+ *              from those without it within that rounding.
  *   dstate_out optional [B, H, M, d + 1]: cotangent G^(N) of state_out (in the
  *              same kshift scaling as state_out); NULL means zero
  *   dQ, dK, dV out [B, H, L, d]
@@ -242,7 +251,7 @@ int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const 
  * slim_bwd.  The key shifts are constants of the computation
  * (stop-gradient); they cancel exactly in Y. */
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
+             const float* state_in, const float* kshift_in, const float* kshift, const void* dY, const void* Y,
              const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
              const float* ctx, void* ws, size_t ws_bytes, void* stream);
 

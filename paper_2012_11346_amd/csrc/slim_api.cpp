@@ -1284,7 +1284,7 @@ int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const 
 }
 
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, const float* kshift, const void* dY,
+             const float* state_in, const float* kshift_in, const float* kshift, const void* dY, const void* Y,
              const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
              const float* ctx, void* ws, size_t ws_bytes, void* stream) {
   int st = check_problem(p);
@@ -1297,7 +1297,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift (kshift_out of slim_fwd)");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
-  st = check_alignment({Q, K, V, dY, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in, ctx});
+  st = check_alignment({Q, K, V, dY, Y, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in, ctx});
   if (st != SLIM_OK) return st;
   if (!context_used(p)) ctx = nullptr;
   const size_t need = bwd_ws_bytes(p);
@@ -1396,6 +1396,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.K = K;
   a.V = V;
   a.dY = dY;
+  a.Y = Y;  // read by the 8-wave walk (the other walks recompute N)
   a.W = W;
   a.Wfrag = wf.out;
   a.kshift = favor ? kshift : nullptr;

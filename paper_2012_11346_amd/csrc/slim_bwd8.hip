@@ -79,7 +79,9 @@ struct Bwd8Lds {
 };
 
 // DROP: value dropout on (its masks are generated only in that instantiation)
-template <class G, bool DROP>
+// HY: the forward's output Y is given; dD = -rowdot(dY, Y) / D then needs
+// only the ones column of N (the denominators), not its value columns
+template <class G, bool DROP, bool HY>
 __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -180,6 +182,7 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const T* Kh = (const T*)a.K + hoff;
   const T* Vh = (const T*)a.V + hoff;
   const T* dYh = (const T*)a.dY + hoff;
+  const T* Yh = HY ? (const T*)a.Y + hoff : nullptr;
   T* dQh = (T*)a.dQ + hoff;
   T* dKh = (T*)a.dK + hoff;
   T* dVh = (T*)a.dV + hoff;
@@ -438,6 +441,16 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // dk of the previous tile (an empty range before the first)
     store_piece(dk_hold, dk_rs, dk_off);
 
+    // Y (given): the EPT entries of its row that this thread takes in the
+    // dN, dD phase, loaded here so that the load is complete by then (rows
+    // past the tile read row 0 of the tile and are not used)
+    u32e yv = {};
+    if constexpr (HY) {
+      const int tid = fresh_tid();
+      const int t = red_row(tid);
+      yv = *(const u32e*)(Yh + (size_t)(start + (t < count ? t : 0)) * D + (tid % TPR) * EPT);
+    }
+
     // ---- Q~ of this wave's feature tiles -> Zq[t][m].  Rows past the tile
     //      (zero in LDS) get finite features and need no mask: their dN, dD
     //      are zero, so they add nothing to G, dA, P or dW.
@@ -524,9 +537,9 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     for (int kb = 0; kb < MB; ++kb)
 #pragma unroll
       for (int st = 0; st < RT; ++st) kT[kb][st] = sfrag_tr(oK, Zk, 32 * kb, 16 * st);
-    F vT[EH];  // V contracting over the tile's rows, own value columns
+    F vT[EH];  // V contracting over the tile's rows, own value columns (for N)
 #pragma unroll
-    for (int el = 0; el < EH; ++el) vT[el] = v_frag(e0 + 16 * el);
+    for (int el = 0; el < EH; ++el) vT[el] = HY ? F{} : v_frag(e0 + 16 * el);
     // (every operand of the phase is read before its first product)
     __builtin_amdgcn_sched_barrier(0);
 
@@ -558,10 +571,11 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       }
     }
     // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
+    // (with Y given only the ones column, D)
 #pragma unroll
     for (int tt = 0; tt < RT; ++tt) {
 #pragma unroll
-      for (int el = 0; el <= EH; ++el) {
+      for (int el = HY ? EH : 0; el <= EH; ++el) {
         if (el == EH && !zown) break;
         f32x4 acc = mma(zero4(), el < EH ? vT[el < EH ? el : 0] : ones_frag(L, count), af[tt]);
 #pragma unroll
@@ -589,13 +603,23 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
       // (value dropout: Y = s N / D with the output scale s; 1 without dropout)
       const float invs = inv * a.drop_scale;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
-      const fvec n = sum_y(hh, t * LDRH + col);
       float dy[EPT];
       float dot = 0.f;
+      if constexpr (HY) {
+        // Y = s N / D as the forward wrote it
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) {
-        dy[i] = to_f32(dYs[swz_off<LDQ, kSwzRows>(t, e) + i]);
-        dot += dy[i] * (n[i] * invs);
+        for (int i = 0; i < EPT; ++i) {
+          dy[i] = to_f32(dYs[swz_off<LDQ, kSwzRows>(t, e) + i]);
+          const unsigned u = yv[i / 2];
+          dot += dy[i] * __uint_as_float((i & 1) ? (u & 0xFFFF0000u) : (u << 16));
+        }
+      } else {
+        const fvec n = sum_y(hh, t * LDRH + col);
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          dy[i] = to_f32(dYs[swz_off<LDQ, kSwzRows>(t, e) + i]);
+          dot += dy[i] * (n[i] * invs);
+        }
       }
       dot = sum_lane_group<TPR>(dot);
       u32e dn;
@@ -1081,8 +1105,14 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 
 template <class G>
 hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s) {
-  if (a.drop_t != 0) hipLaunchKernelGGL((bwd_walk8_kernel<G, true>), dim3(a.P, a.H, a.B), dim3(512), 0, s, a);
-  else hipLaunchKernelGGL((bwd_walk8_kernel<G, false>), dim3(a.P, a.H, a.B), dim3(512), 0, s, a);
+  const dim3 grid(a.P, a.H, a.B);
+  if (a.drop_t != 0) {
+    if (a.Y != nullptr) hipLaunchKernelGGL((bwd_walk8_kernel<G, true, true>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((bwd_walk8_kernel<G, true, false>), grid, dim3(512), 0, s, a);
+  } else {
+    if (a.Y != nullptr) hipLaunchKernelGGL((bwd_walk8_kernel<G, false, true>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((bwd_walk8_kernel<G, false, false>), grid, dim3(512), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -72,6 +72,7 @@ struct BwdArgs {
   const void* K;
   const void* V;
   const void* dY;
+  const void* Y;            // [B,H,L,d] the forward's output, or nullptr (recomputed); 8-wave walk only
   const float* W;
   const void* Wfrag;        // fragment-ordered W (WFragLayout)
   const float* kshift;      // [B,H] key shift of every state below (FAVOR+)

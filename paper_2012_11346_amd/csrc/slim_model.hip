@@ -1023,8 +1023,8 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
       hipLaunchKernelGGL(rows_to_heads_kernel, grid1(hf), dim3(256), 0, s, dA, D, 0, dYh, k, n, hf);
       float* gin = gst + ((size_t)gcur * m.s + r) * S;
       float* gout = gst + ((size_t)(1 - gcur) * m.s + r) * S;
-      CHECK_SLIM(slim_bwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, bprev + r * S, nullptr, nullptr, dYh, gin, dQh,
-                          dQh + hf, dQh + 2 * hf, wd, gout, nullptr, attws, lay.attws_bytes, s));
+      CHECK_SLIM(slim_bwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, bprev + r * S, nullptr, nullptr, dYh, nullptr,
+                          gin, dQh, dQh + hf, dQh + 2 * hf, wd, gout, nullptr, attws, lay.attws_bytes, s));
       hipLaunchKernelGGL(heads_to_rows_kernel, grid1(3 * hf), dim3(256), 0, s, dQh, dQKV, 3 * D, 0, D, k, n, hf, 3 * hf);
       CHECK_HIP(hipGetLastError());
       // [Q K V] = X [Wq Wk Wv]: [dWq dWk dWv] += X^T [dQ dK dV];

@@ -86,7 +86,7 @@ def _load() -> ctypes.CDLL:
     lib.slim_context_bytes.restype = sz
     lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, vp, sz, vp]
     lib.slim_fwd.restype = i32
-    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, fp, vp, vp, vp, fp, fp, fp, vp, sz, vp]
+    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, vp, fp, vp, vp, vp, fp, fp, fp, vp, sz, vp]
     lib.slim_bwd.restype = i32
     lib.slim_status_string.argtypes = [i32]
     lib.slim_status_string.restype = ctypes.c_char_p
@@ -277,15 +277,19 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
 
 def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshift_in=None, dstate_out=None,
         want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None,
-        ctx=None, dropout: float = 0.0, seed: int = 0, within="iter"):
+        ctx=None, dropout: float = 0.0, seed: int = 0, within="iter", Y=None):
     """Backward sweep; kshift is the forward's kshift_out (FAVOR+); ctx (optional)
-    is the context the forward wrote for the same inputs.
+    is the context the forward wrote for the same inputs; Y (optional) the
+    forward's output, from which the row cotangents of the recomputed slices
+    are taken (the bf16 tile walk; elsewhere ignored).
 
     Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
     p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed, within)
     shp = (p.B, p.H, p.L, p.d)
     for n, t in (("Q", Q), ("K", K), ("V", V), ("dY", dY)):
         _need(t, n, Q.dtype, shp)
+    if Y is not None:
+        _need(Y, "Y", Q.dtype, shp)
     _need(W, "W", torch.float32, (p.M, p.d))
     sshape = (p.B, p.H, p.M, p.d + 1)
     for n, t in (("state_in", state_in), ("dstate_out", dstate_out)):
@@ -306,7 +310,7 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
     _need_ctx(p, ctx)
     ws = _workspace(p, PHASE_BWD, dev, ws)
     _check(LIB.slim_bwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
-                        _ptr(kshift), _ptr(dY), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
+                        _ptr(kshift), _ptr(dY), _ptr(Y), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
                         _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
     return dQ, dK, dV, dW, dstate_in
 
@@ -314,22 +318,22 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
 class _Attention(torch.autograd.Function):
     """slim_fwd as a torch operation whose backward is slim_bwd: between the
     two only the key shift and the state-sized context are kept (with the
-    inputs, which autograd holds anyway)."""
+    inputs and the output Y, which autograd holds anyway; slim_bwd reads Y)."""
 
     @staticmethod
     def forward(fctx, Q, K, V, W, C, kind, relu_eps, dropout, seed, within):
         c = new_context(Q, W, C, kind, relu_eps, within)
         Y, _, ks = fwd(Q, K, V, W, C, kind, relu_eps=relu_eps, ctx=c, dropout=dropout, seed=seed, within=within)
-        fctx.save_for_backward(Q, K, V, W)
+        fctx.save_for_backward(Q, K, V, W, Y)
         fctx.args = (C, kind, relu_eps, dropout, seed, within, ks, c)
         return Y
 
     @staticmethod
     def backward(fctx, dY):
-        Q, K, V, W = fctx.saved_tensors
+        Q, K, V, W, Y = fctx.saved_tensors
         C, kind, relu_eps, dropout, seed, within, ks, c = fctx.args
         dQ, dK, dV, dW, _ = bwd(Q, K, V, W, dY.contiguous(), C, ks, kind, relu_eps=relu_eps, ctx=c, dropout=dropout,
-                                seed=seed, within=within)
+                                seed=seed, within=within, Y=Y)
         return dQ, dK, dV, dW, None, None, None, None, None, None
 
 

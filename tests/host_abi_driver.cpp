@@ -95,10 +95,12 @@ int main() {
   EXPECT(slim_fwd(&p, A, A, A, F, nullptr, nullptr, A, F, F, nullptr, A, 0, nullptr) == SLIM_EWORKSPACE);
   EXPECT(slim_fwd(&p, (char*)A + 2, A, A, F, nullptr, nullptr, A, F, F, nullptr, A, 1 << 20, nullptr) ==
          SLIM_EINVAL);
-  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, A, A, F, nullptr, nullptr, A, 1 << 20,
-                  nullptr) == SLIM_EINVAL);
-  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, A, A, A, F, nullptr, nullptr, A, 0, nullptr) ==
-         SLIM_EWORKSPACE);
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, nullptr, A, A, F, nullptr, nullptr, A,
+                  1 << 20, nullptr) == SLIM_EINVAL);
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, A, A, A, F, nullptr, nullptr, A, 0,
+                  nullptr) == SLIM_EWORKSPACE);
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, (char*)A + 2, nullptr, A, A, A, F, nullptr, nullptr, A,
+                  1 << 20, nullptr) == SLIM_EINVAL);
   EXPECT(slim_featmap(&p, nullptr, F, SLIM_QUERY, F, F, nullptr) == SLIM_EINVAL);
   EXPECT(slim_featmap(&p, A, F, 5, F, F, nullptr) == SLIM_EINVAL);
   {

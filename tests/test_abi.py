@@ -111,15 +111,18 @@ def test_null_pointers_are_rejected_before_any_launch(S):
     # a state without its shift
     st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, A, None, A, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
-    # arguments: p, Q, K, V, W, state_in, kshift_in, kshift, dY, dstate_out, dQ, dK, dV, dW, dstate_in,
-    # ws, ws_bytes, stream
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, A, A, None, None, A, 1 << 30, None)
+    # arguments: p, Q, K, V, W, state_in, kshift_in, kshift, dY, Y, dstate_out, dQ, dK, dV, dW, dstate_in,
+    # ctx, ws, ws_bytes, stream
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, None, A, A, A,
+                        None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # dQ missing
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, A, A, A, A, None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, None, A, A, A, A,
+                        None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # kshift missing (FAVOR+)
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, A, A, A, A, None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, None, A, A, A, A,
+                        None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # state_in without kshift_in
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, A, A, A, None, None, A, 0, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, A, A, A, None, None, A, 0, None)
     assert st == S.SLIM_EWORKSPACE
     st = S.LIB.slim_featmap(ctypes.byref(p), None, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL
@@ -130,7 +133,12 @@ def test_null_pointers_are_rejected_before_any_launch(S):
 def test_misaligned_tensors_are_rejected_before_any_launch(S):
     p = _p(S)
     # a row tensor (dY) 8 bytes off a 16-byte boundary
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, A, A, A, A, None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, None, A, A, A, A,
+                        None, None, A, 1 << 30, None)
+    assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
+    # the optional Y, likewise
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A + 8, None, A, A, A, A,
+                        None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
     # the workspace
     st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A, None, A + 4, 1 << 30, None)

@@ -16,13 +16,13 @@ from tests.test_gpu_forward import CASES, _inputs
 pytestmark = pytest.mark.gpu
 
 
-def _run(x, C, kind, state_in=None, kshift_in=None, dstate_out=None, want_dstate_in=False):
+def _run(x, C, kind, state_in=None, kshift_in=None, dstate_out=None, want_dstate_in=False, given_y=False):
     from paper_2012_11346_amd import slim
 
     Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
     Y, st, ks = slim.fwd(Q, K, V, W, C, kind, state_in=state_in, kshift_in=kshift_in)
     g = slim.bwd(Q, K, V, W, dY, C, ks, kind, state_in=state_in, kshift_in=kshift_in, dstate_out=dstate_out,
-                 want_dstate_in=want_dstate_in)
+                 want_dstate_in=want_dstate_in, Y=Y if given_y else None)
     torch.cuda.synchronize()
     return Y, st, ks, g
 
@@ -40,15 +40,38 @@ def test_backward_matches_definition(i):
         report(n, host64(a), r, tol)
 
 
-@pytest.mark.parametrize("i", [0, 1, 4])
-def test_state_cotangent_and_chaining(i):
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_backward_given_y(i):
+    """slim_bwd given the forward's Y (the row cotangents dD from it, eq. 2:
+    dD = -rowdot(dY, Y) / D) against the definition; on bf16 problems (the
+    tile walk that reads Y) also against the same call without Y."""
+    need_gpu()
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[backward given Y] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    _, _, _, gy = _run(x, C, kind, given_y=True)
+    ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
+    tol = TOL[dtype]
+    for n, a, r in zip(("dQ", "dK", "dV", "dW"), gy[:4], ref):
+        report(n, host64(a), r, tol)
+    _, _, _, g = _run(x, C, kind)
+    for n, a, b in zip(("dQ", "dK", "dV", "dW"), gy[:4], g[:4]):
+        if dtype == "f32":
+            assert torch.equal(a, b), n  # the float32 walks recompute N and ignore Y
+        else:
+            report(n + " with Y vs without", host64(a), host64(b), tol)
+
+
+@pytest.mark.parametrize("i, given_y", [(0, False), (1, False), (4, False), (4, True)])
+def test_state_cotangent_and_chaining(i, given_y):
     """Backward of the second half, fed G^(0) into the backward of the first
-    half, equals the backward of the whole sequence; G^(0) matches Algorithm 1."""
+    half, equals the backward of the whole sequence; G^(0) matches Algorithm 1.
+    given_y: each backward also gets its forward's Y."""
     need_gpu()
     from paper_2012_11346_amd import slim
 
     name, B, H, L, d, M, C, dtype, kind = CASES[i]
-    print(f"[chaining] case={name}", flush=True)
+    print(f"[chaining] case={name} given_y={given_y}", flush=True)
     x = _inputs(i, B, H, L, d, M, C, dtype, kind)
     cut = (L // 2) // 16 * 16 + 3
     tol = TOL[dtype]
@@ -58,9 +81,9 @@ def test_state_cotangent_and_chaining(i):
     Y2, st2, ks2 = slim.fwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, C, kind, state_in=st1,
                             kshift_in=ks1)
     g2 = slim.bwd(half(Q, cut, L), half(K, cut, L), half(V, cut, L), W, half(dY, cut, L), C, ks2, kind,
-                  state_in=st1, kshift_in=ks1, want_dstate_in=True)
+                  state_in=st1, kshift_in=ks1, want_dstate_in=True, Y=Y2 if given_y else None)
     g1 = slim.bwd(half(Q, 0, cut), half(K, 0, cut), half(V, 0, cut), W, half(dY, 0, cut), C, ks1, kind,
-                  dstate_out=g2[4])
+                  dstate_out=g2[4], Y=Y1 if given_y else None)
     torch.cuda.synchronize()
     ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], kind, mask_W=mask_w(x))
     report("dQ (chained)", np.concatenate([host64(g1[0]), host64(g2[0])], axis=2), ref[0], tol)
@@ -118,10 +141,11 @@ def test_backward_rounded_w(i):
         report(n, host64(a), r, TOL[dtype])
 
 
-@pytest.mark.parametrize("L, late, scale, segments",
-                         [(160, False, 3.0, None), (4096, False, 2.0, None), (4096, False, 2.5, 128),
-                          (4096, True, 2.0, 128)])
-def test_backward_stress_large_logits(L, late, scale, segments):
+@pytest.mark.parametrize("L, late, scale, segments, given_y",
+                         [(160, False, 3.0, None, False), (4096, False, 2.0, None, False),
+                          (4096, False, 2.5, 128, False), (4096, True, 2.0, 128, False),
+                          (4096, False, 2.0, None, True), (160, False, 3.0, None, True)])
+def test_backward_stress_large_logits(L, late, scale, segments, given_y):
     """Q, K scaled by 2 to 3 (exponents of size ~50), through the whole
     backward.  (At 3 the chain rule of the key features, a difference of two
     large sums over features of bf16 operands, reaches ~2e-2 of dK.)
@@ -144,7 +168,7 @@ def test_backward_stress_large_logits(L, late, scale, segments):
     import torch as _t
 
     B, H, d, M, C = 1, 2, 64, 256, 64
-    print(f"[backward stress] L={L} late={late} scale={scale} segments={segments}", flush=True)
+    print(f"[backward stress] L={L} late={late} scale={scale} segments={segments} given_y={given_y}", flush=True)
     x = _inputs(51 + L, B, H, L, d, M, C, "bf16", "favor+", scale_qk=scale, round_w=True)
     if late:
         m = int(_t.argmax((x["W"] ** 2).sum(1)))
@@ -155,7 +179,7 @@ def test_backward_stress_large_logits(L, late, scale, segments):
     if segments is not None:
         os.environ["SLIM_SEGMENTS"] = str(segments)
     try:
-        Y, _, ks, (dQ, dK, dV, dW, _) = _run(x, C, "favor+")
+        Y, _, ks, (dQ, dK, dV, dW, _) = _run(x, C, "favor+", given_y=given_y)
     finally:
         if old is None:
             os.environ.pop("SLIM_SEGMENTS", None)

@@ -26,14 +26,15 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("i", range(len(CASES)))
-def test_dropout_forward_backward(i):
+@pytest.mark.parametrize("i, given_y", [(i, False) for i in range(len(CASES))] + [(1, True), (3, True), (4, True)])
+def test_dropout_forward_backward(i, given_y):
+    """given_y: the backward also gets the forward's Y (with its dropout)."""
     need_gpu()
     from paper_2012_11346_amd import slim
 
     name, B, H, L, d, M, C, dtype, kind, p, seed, segs = CASES[i]
-    print(f"[dropout] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind} p={p} segments={segs}",
-          flush=True)
+    print(f"[dropout] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind} p={p} segments={segs} "
+          f"given_y={given_y}", flush=True)
     x = make_inputs(Workload(name, 600 + i, B, H, L, d, M, (C,), dtype, kind))
     old = os.environ.get("SLIM_SEGMENTS")
     if segs is not None:
@@ -41,7 +42,7 @@ def test_dropout_forward_backward(i):
     try:
         Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
         Y, st, ks = slim.fwd(Q, K, V, W, C, kind, dropout=p, seed=seed)
-        dQ, dK, dV, dW, _ = slim.bwd(Q, K, V, W, dY, C, ks, kind, dropout=p, seed=seed)
+        dQ, dK, dV, dW, _ = slim.bwd(Q, K, V, W, dY, C, ks, kind, dropout=p, seed=seed, Y=Y if given_y else None)
         torch.cuda.synchronize()
     finally:
         if old is None:
