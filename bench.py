@@ -3,7 +3,8 @@
 
 One step = slim_fwd + slim_bwd over one batch of the L = 32768 workload
 (B=4, H=8, d=64, M=256, bf16 inputs, FAVOR+), inputs resident in device
-memory; the backward gets the forward's outputs Y, key shift and context.  Prints one JSON line with throughput (tokens/s = B*L / step time),
+memory; the backward gets the forward's outputs Y, logD (row normalisers),
+key shift and context.  Prints one JSON line with throughput (tokens/s = B*L / step time),
 a roofline entry for the dominant kernel, the fp64 CPU oracle timed on the
 whole batch, and, unless switched off:
 
@@ -194,12 +195,15 @@ def main():
             p = slim.problem(B, H, L, d, M, self.C, self.Q.dtype, self.kind, within=self.within)
             self.p = p
             self.Y = torch.empty_like(self.Q)
+            # the row normalisers (tile-walk mode), an output like Y
+            self.lD = torch.empty((B, H, L), dtype=torch.float32, device=dev) if self.within == "iter" else None
             self.st = torch.empty((B, H, M, d + 1), dtype=torch.float32, device=dev)
             self.ks = torch.empty((B, H), dtype=torch.float32, device=dev) if self.kind == "favor+" else None
             self.dQ, self.dK, self.dV = (torch.empty_like(self.Q) for _ in range(3))
             self.dW = torch.empty((M, d), dtype=torch.float32, device=dev)
             self.out_bytes = sum(t.numel() * t.element_size() for t in
-                                 (self.Y, self.st, self.dQ, self.dK, self.dV, self.dW) + ((self.ks,) if self.ks is not None else ()))
+                                 (self.Y, self.st, self.dQ, self.dK, self.dV, self.dW) +
+                                 tuple(t for t in (self.ks, self.lD) if t is not None))
             self.wsf = torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_FWD)), dtype=torch.uint8, device=dev)
             self.wsb = torch.empty(max(1, slim.workspace_bytes(p, slim.PHASE_BWD)), dtype=torch.uint8, device=dev)
             n_ctx = slim.context_bytes(p)
@@ -208,17 +212,17 @@ def main():
             return self
 
         def free(self):
-            for n in ("Y", "st", "ks", "dQ", "dK", "dV", "dW", "wsf", "wsb", "ctx"):
+            for n in ("Y", "lD", "st", "ks", "dQ", "dK", "dV", "dW", "wsf", "wsb", "ctx"):
                 setattr(self, n, None)
 
         def fwd(self):
             slim.fwd(self.Q, self.K, self.V, self.W, self.C, self.kind, ws=self.wsf, Y=self.Y, state_out=self.st,
-                     kshift_out=self.ks, ctx=self.ctx, within=self.within)
+                     kshift_out=self.ks, ctx=self.ctx, within=self.within, logD=self.lD)
 
         def bwd(self, dY=None):
             slim.bwd(self.Q, self.K, self.V, self.W, self.dY if dY is None else dY, self.C, self.ks, self.kind,
                      ws=self.wsb, dQ=self.dQ, dK=self.dK, dV=self.dV, dW=self.dW, ctx=self.ctx, within=self.within,
-                     Y=self.Y)
+                     Y=self.Y, logD=self.lD)
 
     def run_step(layers):
         """forward r = 1..n, then backward r = n..1"""

@@ -185,6 +185,16 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
  *   kshift_in  [B, H], required with state_in for FAVOR+: the key shift
  *              state_in is relative to
  *   Y          out [B, H, L, d]
+ *   logD       optional out [B, H, L] float32 (NULL: not written): for each row
+ *              t the row normaliser log2(D_t) of eq. 4, Y_t = N_t / D_t, in
+ *              the units of the true feature map g (its key shifts added
+ *              back), so that g(q_t)_m / D_t = exp2(w_m . q_t log2(e) - logD_t)
+ *              for FAVOR+ and g(q_t)_m exp2(-logD_t) for ReLU and the square
+ *              map.  An output like Y (4 bytes per row): slim_bwd given Y and
+ *              logD finds the state cotangent of every segment before its
+ *              reverse walk.  Written by the tile-walk mode only: the
+ *              quadratic and prefix-sum modes return SLIM_EUNSUPPORTED for a
+ *              non-NULL logD
  *   state_out  out [B, H, M, d + 1], may be NULL: B^(N) relative to kshift_out
  *   kshift_out out [B, H] (FAVOR+: required; ReLU: ignored, may be NULL)
  *   ctx        optional out of slim_context_bytes(p) bytes (NULL: none): the
@@ -192,7 +202,7 @@ int slim_featmap(const slim_problem* p, const void* X, const float* W, int role,
  *              inputs
  *   ws         workspace of at least slim_workspace_bytes(p, SLIM_PHASE_FWD) */
 int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, void* Y, float* state_out,
+             const float* state_in, const float* kshift_in, void* Y, float* logD, float* state_out,
              float* kshift_out, float* ctx, void* ws, size_t ws_bytes, void* stream);
 
 /* Bytes of the static device scratch slim_fwd_noalloc uses (a compile-time
@@ -216,7 +226,7 @@ size_t slim_noalloc_scratch_bytes(void);
  * one device (other host threads, or streams not ordered with each other)
  * race and must be serialised by the caller. */
 int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-                     const float* state_in, const float* kshift_in, void* Y, float* state_out,
+                     const float* state_in, const float* kshift_in, void* Y, float* logD, float* state_out,
                      float* kshift_out, float* ctx, void* stream);
 
 /* Backward sweep of Algorithm 1 (one layer) for the loss
@@ -233,6 +243,14 @@ int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const 
  *              other configurations and within-slice modes recompute N and
  *              ignore it.  Y is rounded to the dtype, so the results differ
  *              from those without it within that rounding.
+ *   logD       optional [B, H, L]: the logD slim_fwd wrote with Y (requires
+ *              Y; SLIM_EINVAL otherwise), or NULL.  Given to the bf16 tile
+ *              walk on a sequence split into several segments, the state
+ *              cotangent after every segment (eq. 18 summed over the later
+ *              rows) is summed from Q, dY, Y and logD before the walks, each
+ *              walk starts from it, and the pass that otherwise adds the later
+ *              segments' cotangent to every earlier row is skipped.  Ignored
+ *              elsewhere.
  *   dstate_out optional [B, H, M, d + 1]: cotangent G^(N) of state_out (in the
  *              same kshift scaling as state_out); NULL means zero
  *   dQ, dK, dV out [B, H, L, d]
@@ -252,7 +270,7 @@ int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const 
  * (stop-gradient); they cancel exactly in Y. */
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, const float* kshift, const void* dY, const void* Y,
-             const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
+             const float* logD, const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
              const float* ctx, void* ws, size_t ws_bytes, void* stream);
 
 /* Kernel-timing instrumentation.  before and after are hipEvent_t handles

@@ -1078,8 +1078,8 @@ int ps_bwd_impl(const slim_problem* p, const void* Q, const void* K, const void*
 // The forward of slim_fwd on a given workspace (the caller's, or the
 // library's static scratch for slim_fwd_noalloc).
 int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, float* ctx,
-             void* ws, size_t ws_bytes, void* stream) {
+             const float* state_in, const float* kshift_in, void* Y, float* logD, float* state_out, float* kshift_out,
+             float* ctx, void* ws, size_t ws_bytes, void* stream) {
   int st = check_problem(p);
   if (st != SLIM_OK) return st;
   if (Q == nullptr || K == nullptr || V == nullptr || W == nullptr || Y == nullptr)
@@ -1088,8 +1088,10 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift_out == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift_out");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
-  st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out, ctx});
+  st = check_alignment({Q, K, V, Y, ws}, {W, state_in, kshift_in, state_out, kshift_out, ctx, logD});
   if (st != SLIM_OK) return st;
+  if (logD != nullptr && (ps(p) || quad(p)))
+    return fail(SLIM_EUNSUPPORTED, "logD is written by the tile-walk mode (within = SLIM_WITHIN_ITER) only");
   if (!context_used(p)) ctx = nullptr;
   const size_t need = fwd_ws_bytes(p);
   if (need > 0 && (ws == nullptr || ws_bytes < need))
@@ -1178,6 +1180,7 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
     a.fixed_shift = favor ? kshift_out : nullptr;
     a.Y = Y;
     a.state_out = state_out;
+    a.logD = logD;
     e = timed_launch(SLIM_PHASE_FWD, s, [&] { return dp.fwd(a, slim::kWalkOutputs, s); });
     if (e != hipSuccess) return hip_fail(e, "forward launch");
     return ok();
@@ -1218,6 +1221,7 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
   }
   // (3) the walk proper
   a.Y = Y;
+  a.logD = logD;
   a.state_out = state_out;
   a.kshift_out = favor ? kshift_out : nullptr;
   e = timed_launch(SLIM_PHASE_FWD, s, [&] { return dp.fwd(a, slim::kWalkOutputs, s); });
@@ -1259,16 +1263,16 @@ int scratch_address(void** out) {
 extern "C" {
 
 int slim_fwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-             const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out, float* ctx,
-             void* ws, size_t ws_bytes, void* stream) {
-  return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ctx, ws, ws_bytes, stream);
+             const float* state_in, const float* kshift_in, void* Y, float* logD, float* state_out, float* kshift_out,
+             float* ctx, void* ws, size_t ws_bytes, void* stream) {
+  return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, logD, state_out, kshift_out, ctx, ws, ws_bytes, stream);
 }
 
 size_t slim_noalloc_scratch_bytes(void) { return kNoallocScratchBytes; }
 
 int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
-                     const float* state_in, const float* kshift_in, void* Y, float* state_out, float* kshift_out,
-                     float* ctx, void* stream) {
+                     const float* state_in, const float* kshift_in, void* Y, float* logD, float* state_out,
+                     float* kshift_out, float* ctx, void* stream) {
   int st = check_problem(p);
   if (st != SLIM_OK) return st;
   const size_t need = fwd_ws_bytes(p);
@@ -1280,12 +1284,13 @@ int slim_fwd_noalloc(const slim_problem* p, const void* Q, const void* K, const 
     st = scratch_address(&ws);
     if (st != SLIM_OK) return st;
   }
-  return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ctx, ws, kNoallocScratchBytes, stream);
+  return fwd_impl(p, Q, K, V, W, state_in, kshift_in, Y, logD, state_out, kshift_out, ctx, ws, kNoallocScratchBytes,
+                  stream);
 }
 
 int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V, const float* W,
              const float* state_in, const float* kshift_in, const float* kshift, const void* dY, const void* Y,
-             const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
+             const float* logD, const float* dstate_out, void* dQ, void* dK, void* dV, float* dW, float* dstate_in,
              const float* ctx, void* ws, size_t ws_bytes, void* stream) {
   int st = check_problem(p);
   if (st != SLIM_OK) return st;
@@ -1297,7 +1302,9 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     if (kshift == nullptr) return fail(SLIM_EINVAL, "FAVOR+ needs kshift (kshift_out of slim_fwd)");
     if (state_in != nullptr && kshift_in == nullptr) return fail(SLIM_EINVAL, "state_in needs kshift_in (FAVOR+)");
   }
-  st = check_alignment({Q, K, V, dY, Y, dQ, dK, dV, ws}, {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in, ctx});
+  if (logD != nullptr && Y == nullptr) return fail(SLIM_EINVAL, "logD is used together with Y");
+  st = check_alignment({Q, K, V, dY, Y, dQ, dK, dV, ws},
+                       {W, state_in, kshift_in, kshift, dstate_out, dW, dstate_in, ctx, logD});
   if (st != SLIM_OK) return st;
   if (!context_used(p)) ctx = nullptr;
   const size_t need = bwd_ws_bytes(p);
@@ -1419,9 +1426,53 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.P = P;
   a.relu_eps = p->relu_eps;
   const bwd_fn walk = pick_bwd(dp);
+  // With the forward's Y and logD the cotangent after every segment is known
+  // before the walks (eq. 18 summed over the later rows, the row cotangents
+  // from Y and D): a query-sum pass and a reverse scan give it, each walk
+  // starts from it, and no carry pass follows.
+  const bool direct = P > 1 && logD != nullptr && dp.ksum != nullptr && walk == dp.bwd8;
+  if (direct) {
+    slim::KsumArgs qs;
+    std::memset(&qs, 0, sizeof(qs));
+    qs.K = Q;
+    qs.V = dY;
+    qs.Y = Y;
+    qs.logD = logD;
+    qs.W = W;
+    qs.Wfrag = wf.out;
+    qs.shift = favor ? kshift : nullptr;
+    qs.out = (float*)(w + lay.seg_sum);
+    qs.B = (int)p->B;
+    qs.H = (int)p->H;
+    qs.L = (int)p->L;
+    qs.C = clamp_C(p);
+    qs.P2 = P2;
+    qs.relu_eps = p->relu_eps;
+    qs.drop_scale = drop_plan(p).scale;
+    e = dp.ksum(qs, slim::kSumQuery, s);
+    if (e != hipSuccess) return hip_fail(e, "query-sum launch");
+    slim::ScanArgs rv;
+    std::memset(&rv, 0, sizeof(rv));
+    rv.seg = qs.out;
+    rv.init = dstate_out;
+    rv.out = (float*)(w + lay.gend);
+    rv.total = dstate_in;
+    rv.init_shift = favor ? kshift_in : nullptr;
+    rv.shift = favor ? kshift : nullptr;
+    rv.BH = BH;
+    rv.P = P2;
+    rv.SZ = SZ;
+    rv.favor = favor ? 1 : 0;
+    rv.step = S2;
+    e = slim::launch_scan_rev(rv, s);
+    if (e != hipSuccess) return hip_fail(e, "cotangent-scan launch");
+    a.g_init = rv.out;
+    a.g_final = nullptr;
+    a.dstate_in = nullptr;
+  }
   e = timed_launch(SLIM_PHASE_BWD, s, [&] { return walk(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward launch");
-  if (P > 1) {
+  if (P > 1 && !direct) {
     // (4) cotangent after each segment (reverse scan of what the walks ended
     //     with; eq. 18 summed over the later segments) and before the
     //     sequence; then its contribution to the rows of each earlier segment
@@ -1465,8 +1516,10 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
     }
     if (e != hipSuccess) return hip_fail(e, "carry launch");
   }
-  // (5) dW: the workgroups' partials summed in a fixed order
-  e = slim::launch_dw_reduce(a.dW_part, (int)dw_slots(p, P), (int)(p->M * p->d), dW, s);
+  // (5) dW: the workgroups' partials summed in a fixed order (the walks'
+  //     only, without the carry pass)
+  const int slots = direct ? BH * P : (int)dw_slots(p, P);
+  e = slim::launch_dw_reduce(a.dW_part, slots, (int)(p->M * p->d), dW, s);
   if (e != hipSuccess) return hip_fail(e, "dW-reduction launch");
   return ok();
 }

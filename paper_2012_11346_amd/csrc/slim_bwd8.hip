@@ -209,9 +209,11 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const size_t sidx = (head * a.P + p) * SZ;
   const float* bend = a.bounds + (head * a.bound_stride + (size_t)(p + 1) * a.bound_step) * SZ;
 
-  // the cotangent starts at dstate_out in the last segment, else at zero
-  // (earlier segments get the cotangent of later ones added by carry_kernel)
-  const float* g0 = (p == a.P - 1 && a.dstate_out != nullptr) ? a.dstate_out + head * SZ : nullptr;
+  // the cotangent starts at the cotangent after the segment when the caller
+  // has it (g_init); else at dstate_out in the last segment and at zero in
+  // the others (they get the cotangent of later ones added by the carry pass)
+  const float* g0 = a.g_init != nullptr ? a.g_init + (head * a.P + p) * SZ
+                    : ((p == a.P - 1 && a.dstate_out != nullptr) ? a.dstate_out + head * SZ : nullptr);
   // running state after the current tile (this wave's columns), its cotangent, dW rows
   f32x4 S[MT][EH], Sz[MT], Gs[MT][EH], Gz[MT], dWacc[MT][EH];
 #pragma unroll

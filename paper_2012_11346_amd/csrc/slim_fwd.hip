@@ -125,7 +125,10 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) T Zk[4][QSIDE ? ZR * LDZ : 8];
   __shared__ __attribute__((aligned(16))) float Red[4][QSIDE ? TR * LDR : 4];
   __shared__ __attribute__((aligned(16))) float knb[2][TR];  // key row norms, read as 16-byte vectors
-  __shared__ float qmx[4][TR], kmx[4];
+  // row maxima of the query logits per wave, double-buffered by tile: the
+  // output phase of a tile reads them (for logD) while a faster wave may
+  // already write the next tile's
+  __shared__ float qmx[2][4][TR], kmx[4];
 
   const int w = wave_id(), g = lane_g(), c = lane_c();
   const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -313,7 +316,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) v = fmaxf(v, Lq[mt][tt][r]);
           v = wave_max_over_g(v);
-          if (g == 0) qmx[w][16 * tt + c] = v;
+          if (g == 0) qmx[bf][w][16 * tt + c] = v;
         }
       }
       if (!fixed) {
@@ -372,7 +375,7 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
         for (int tt = 0; tt < RT; ++tt) {
           const int t = 16 * tt + c;
-          const float qs = fmaxf(fmaxf(qmx[0][t], qmx[1][t]), fmaxf(qmx[2][t], qmx[3][t])) * kLog2e;
+          const float qs = fmaxf(fmaxf(qmx[bf][0][t], qmx[bf][1][t]), fmaxf(qmx[bf][2][t], qmx[bf][3][t])) * kLog2e;
           // (rows past the tile get finite features; their outputs are not stored)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
@@ -497,7 +500,8 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
       const int tid = fresh_tid();
       const int t = tid / TPR, q = tid % TPR;
       // (value dropout: the output scale 1 / (1 - p) folded in)
-      const float inv = a.drop_scale / ((Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]));
+      const float den = (Red[0][t * LDR + D] + Red[1][t * LDR + D]) + (Red[2][t * LDR + D] + Red[3][t * LDR + D]);
+      const float inv = a.drop_scale / den;
       tvec o;
 #pragma unroll
       for (int h4 = 0; h4 < EPT / 4; ++h4) {
@@ -521,6 +525,21 @@ __global__ __launch_bounds__(256, 2) void fwd_walk_kernel(FwdArgs a) {
 #pragma unroll
       for (int v = 0; v < NV; ++v) y_hold[v] = ov[v];
       flush_y();
+      // logD: log2 of the row's denominator D in the units of the true
+      // features phi (the row shift and the key shift added back), so that
+      // phi(q)_m / D = exp2(w_m.q log2(e) - logD) for FAVOR+ and
+      // phi(q)_m exp2(-logD) otherwise; one thread per row, rows past the
+      // tile dropped by the range check
+      {
+        const float qs = (G::KIND == kFavor)
+                             ? fmaxf(fmaxf(qmx[bf][0][t], qmx[bf][1][t]), fmaxf(qmx[bf][2][t], qmx[bf][3][t])) * kLog2e
+                             : 0.f;
+        const float l2 = (G::KIND == kFavor) ? qs + __log2f(den) + cur * kLog2e : __log2f(den);
+        const __amdgpu_buffer_rsrc_t lrs =
+            range_rsrc(a.logD != nullptr ? a.logD + head * (size_t)a.L + start : nullptr,
+                       a.logD != nullptr ? (size_t)count * sizeof(float) : 0);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(l2), lrs, q == 0 ? t * 4 : INT_MAX - 3, 0, 0);
+      }
     }
   }
 

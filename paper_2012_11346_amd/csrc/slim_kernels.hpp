@@ -24,6 +24,7 @@ struct FwdArgs {
   const float* W;
   const void* Wfrag;        // fragment-ordered W (WFragLayout)
   void* Y;                  // kWalkOutputs
+  float* logD;              // kWalkOutputs: [B,H,L] row normalisers (slim_fwd's logD), or nullptr
   float* state_out;         // kWalkOutputs: [B,H,M,D+1] or nullptr (written by the last segment)
   float* kshift_out;        // kWalkOutputs: [B,H] or nullptr
   const float* seg_state;   // [B,H,seg_stride,M,D+1] state each segment starts from, or nullptr (zero)
@@ -51,6 +52,7 @@ struct ScanArgs {
   float* out_shift;        // forward: [B,H,P]
   float* total;            // reverse scan: [B,H,M,D+1] scaled total, or nullptr
   int BH, P, SZ, favor;
+  int step;                // reverse scan: out holds every step-th entry (P / step per head); 0 or 1: all
 };
 
 struct WfragArgs {
@@ -80,6 +82,8 @@ struct BwdArgs {
   int bound_stride, bound_step;  // segment p spans boundaries p * bound_step .. (p + 1) * bound_step
   const float* dstate_out;  // [B,H,M,D+1] cotangent of the final state (segment P-1 starts from it), or nullptr
   float* g_final;           // [B,H,P,M,D+1] cotangent each segment's walk ends with (P > 1), or nullptr
+  const float* g_init;      // [B,H,P,M,D+1] cotangent after each segment, which its walk starts from
+                            // (8-wave walk; then g_final, dstate_in and the carry are not used), or nullptr
   const float* init_shift;  // [B,H] key shift of the caller's initial state (scales dstate_in), or nullptr
   float* dstate_in;         // [B,H,M,D+1] state cotangent before the sequence (P == 1 only), or nullptr
   void* dQ;
@@ -119,14 +123,16 @@ struct CarryArgs {
 
 // Key sums of contiguous parts of each head (ksum_kernel): per part, the
 // state it adds relative to a fixed key shift, or the largest key exponent.
-enum KsumMode { kSumStates = 0, kSumMax = 1 };
+enum KsumMode { kSumStates = 0, kSumMax = 1, kSumQuery = 2 };
 struct KsumArgs {
-  const void* K;
-  const void* V;
+  const void* K;       // keys (kSumQuery: the queries)
+  const void* V;       // values (kSumQuery: dY)
+  const void* Y;       // kSumQuery: the forward's Y
+  const float* logD;   // kSumQuery: [B,H,L] the forward's row normalisers
   const float* W;
   const void* Wfrag;   // fragment-ordered W (WFragLayout)
-  const float* shift;  // kSumStates, FAVOR+: [B,H] key shift of the sums
-  float* out;          // kSumStates: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
+  const float* shift;  // kSumStates, kSumQuery, FAVOR+: [B,H] key shift of the sums
+  float* out;          // kSumStates, kSumQuery: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
   int B, H, L, C, P2;
   int tile_begin, tile_end;  // the parts cover tiles [tile_begin, tile_end) of each head (0, 0: all)
   int align;                 // > 0: parts start at multiples of `align` tiles from tile_begin (slices)

@@ -19,6 +19,17 @@
 // KS_MAX mode computes only the logits and returns, per part, the maximum of
 // w_m.k - |k|^2/2 over its rows and all features: the maximum over a head's
 // parts is the key shift of that head.
+//
+// kSumQuery mode (backward) sums the state cotangent a part's rows add
+// (eq. 18 summed over the part), from the forward's outputs Y and logD:
+//   G = sum_t u[t]^T [s dY[t] | -rowdot(dY[t], Y[t])],  u[t]_m = phi(q_t)_m / D_t,
+// the row cotangents of eq. 2 (dN = s dY / D, dD = -rowdot(dY, Y) / D, s the
+// dropout scale) with D known, so no state is needed: the same stream of
+// 64-row chunks with the queries in place of the keys, dY in place of the
+// values and the row dots in place of the ones column.  u comes from the
+// query logits and logD (exp2(w_m.q log2(e) - logD) for FAVOR+, with the
+// head's key shift folded in so that G is in the units of the walk's
+// cotangent).
 #include <type_traits>
 
 #include "slim_common.hpp"
@@ -36,13 +47,16 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   constexpr int CT = CR / 16;     // 16-row tiles per chunk
   constexpr int LDQ = D + 16;     // row tiles, swizzled (kSwzRows)
   constexpr int TQ = CR * LDQ;
-  constexpr bool SUMS = MODE == kSumStates;
+  constexpr bool QRY = MODE == kSumQuery;
+  constexpr bool SUMS = MODE != kSumMax;  // state sums (of keys, or of queries)
   typedef SwzLane<LDQ, kSwzRows> OR;
   static_assert(sizeof(T) == 2 && (MT % 2) == 0, "bf16, 32-feature blocks");
 
   __shared__ __attribute__((aligned(16))) T Kb[2 * TQ];
   __shared__ __attribute__((aligned(16))) T Vb[SUMS ? 2 * TQ : 8];
-  __shared__ __attribute__((aligned(16))) float knb[2][CR];  // key row norms, read as 16-byte vectors
+  // key row norms (kSumQuery: logD of the rows), read as 16-byte vectors
+  __shared__ __attribute__((aligned(16))) float knb[2][CR];
+  __shared__ float ddb[QRY ? 2 : 1][QRY ? CR : 1];  // kSumQuery: -rowdot(dY, Y) of the rows
   __shared__ float wmax[4];
 
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -101,9 +115,17 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   const size_t nbytes = (size_t)nrows * D * sizeof(T);
   const __amdgpu_buffer_rsrc_t rK = range_rsrc(Kh + (size_t)r0 * D, nbytes);
   const __amdgpu_buffer_rsrc_t rV = range_rsrc(Vh + (size_t)r0 * D, nbytes);
+  const __amdgpu_buffer_rsrc_t rY =
+      range_rsrc(QRY ? (const T*)a.Y + head * (size_t)a.L * D + (size_t)r0 * D : nullptr, QRY ? nbytes : 0);
+  const __amdgpu_buffer_rsrc_t rL = range_rsrc(QRY ? a.logD + head * (size_t)a.L + r0 : nullptr,
+                                               QRY ? (size_t)nrows * sizeof(float) : 0);
 
+  // row exponent offsets: keys exp2(x log2(e) - koff - 0.5 log2(e) |k|^2);
+  // queries (kSumQuery) exp2(x log2(e) - (logD - kshift log2(e)))
   const float half_log2M = 0.5f * __log2f((float)M);
-  const float koff = (SUMS && G::KIND == kFavor) ? a.shift[head] * kLog2e + half_log2M : 0.f;
+  const float koff = (SUMS && G::KIND == kFavor)
+                         ? (QRY ? -a.shift[head] * kLog2e : a.shift[head] * kLog2e + half_log2M) : 0.f;
+  constexpr float kscale = QRY ? 1.f : 0.5f * kLog2e;
 
   f32x4 S[SUMS ? MT : 1][SUMS ? ET : 1], Sz[SUMS ? MT : 1];
   if constexpr (SUMS) {
@@ -116,20 +138,72 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   }
   float vmax = -INFINITY;
 
-  RowStage<T, D, CR, 256> sk, sv;
+  RowStage<T, D, CR, 256> sk, sv, sy;
   const int tid = threadIdx.x;
-  float* const knorm = G::KIND == kFavor ? knb[0] : nullptr;
+  // (kSumQuery: no norms; knb holds the rows' logD)
+  constexpr bool NORMS = G::KIND == kFavor && !QRY;
+  float* const knorm = NORMS ? knb[0] : nullptr;
+  // kSumQuery: the rows' logD and their dots rowdot(dY, Y), from the
+  // staged dY and Y chunks (a row's chunks sit in consecutive lanes).
+  // FAVOR+: logD enters the exponent of the features (threads 0 .. CR-1
+  // hold one row each, for knb); ReLU: the staged dY rows and the dots are
+  // divided by D instead (each thread holds the logD of its chunks' rows),
+  // as the walk rounds dN = dY / D.
+  typedef RowStage<T, D, CR, 256> RS;
+  float lreg[G::KIND == kFavor ? 1 : RS::PER] = {};
+  auto fetch_q = [&](int row0, int t) {
+    if constexpr (QRY) {
+      sy.fetch(rY, row0, t);
+      if constexpr (G::KIND == kFavor) {
+        lreg[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rL, t < CR ? (row0 + t) * 4 : INT_MAX - 3, 0, 0));
+      } else {
+#pragma unroll
+        for (int i = 0; i < RS::PER; ++i) {
+          const int ch = t + i * 256;
+          lreg[i] = __uint_as_float(
+              __builtin_amdgcn_raw_buffer_load_b32(rL, ch < RS::NCH ? (row0 + ch / RS::CPR) * 4 : INT_MAX - 3, 0, 0));
+        }
+      }
+    }
+  };
+  // (before the dY chunks are written to LDS: with ReLU it scales them)
+  auto store_q = [&](int buf, int t) {
+    if constexpr (QRY) {
+      if (G::KIND == kFavor && t < CR) knb[buf][t] = lreg[0];
+#pragma unroll
+      for (int i = 0; i < RS::PER; ++i) {
+        const int ch = t + i * 256;
+        const int r = ch / RS::CPR, cc = ch - r * RS::CPR;
+        T* dy = reinterpret_cast<T*>(&sv.v[i]);
+        const T* yy = reinterpret_cast<const T*>(&sy.v[i]);
+        float d = 0.f;
+#pragma unroll
+        for (int k = 0; k < RS::VEC; ++k) d += to_f32(dy[k]) * to_f32(yy[k]);
+        if constexpr (G::KIND != kFavor) {
+          const float rd = fast_exp2(-lreg[i]);  // 1 / D
+#pragma unroll
+          for (int k = 0; k < RS::VEC; ++k) dy[k] = cvt<T>(to_f32(dy[k]) * rd);
+          d *= rd;
+        }
+        d = sum_lane_group<RS::CPR>(d);
+        if (ch < RS::NCH && cc == 0) ddb[buf][r] = -d;
+      }
+    }
+  };
   // value dropout: dropped elements of the value rows are zeroed when staged
   const Drop drop{a.drop_seed, a.drop_t, a.C, head};
   sk.fetch(rK, 0, tid);
   if constexpr (SUMS) sv.fetch(rV, 0, tid);
+  fetch_q(0, tid);
   sk.template store_swz<LDQ>(Kb, knorm, tid);
+  store_q(0, tid);
   if constexpr (SUMS) {
     if (DROP) sv.drop(drop, r0, tid);
     sv.template store_swz<LDQ>(Vb, nullptr, tid);
   }
   sk.fetch(rK, CR, tid);
   if constexpr (SUMS) sv.fetch(rV, CR, tid);
+  fetch_q(CR, tid);
   __syncthreads();
 
   for (int ci = 0; ci < nch; ++ci) {
@@ -139,13 +213,15 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
     // finished before the last barrier); rows of chunk ci + 2 into registers
     {
       const int t2 = fresh_tid();
-      sk.template store_swz<LDQ>(Kb + (bf ^ 1) * TQ, G::KIND == kFavor ? knb[bf ^ 1] : nullptr, t2);
+      sk.template store_swz<LDQ>(Kb + (bf ^ 1) * TQ, NORMS ? knb[bf ^ 1] : nullptr, t2);
+      store_q(bf ^ 1, t2);
       if constexpr (SUMS) {
         if (DROP) sv.drop(drop, r0 + (ci + 1) * CR, t2);
         sv.template store_swz<LDQ>(Vb + (bf ^ 1) * TQ, nullptr, t2);
       }
       sk.fetch(rK, (ci + 2) * CR, t2);
       if constexpr (SUMS) sv.fetch(rV, (ci + 2) * CR, t2);
+      fetch_q((ci + 2) * CR, t2);
     }
     const T* Ks = Kb + bf * TQ;
     const T* Vs = Vb + bf * TQ;
@@ -182,7 +258,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool ok = 16 * st + 4 * L.g + r < cnt;
-          const float kc = ok ? koff + 0.5f * kLog2e * knv[st][r] : INFINITY;
+          const float kc = ok ? koff + kscale * knv[st][r] : INFINITY;
 #pragma unroll
           for (int mt = m0; mt < m1; ++mt) {
             float x = Lk[st][mt][r];
@@ -194,10 +270,14 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
       }
 #pragma unroll
       for (int rb = 0; rb < CT / 2; ++rb) {
-        F ones;
+        F ones;  // the ones column of [V | 1] (kSumQuery: -rowdot(dY, Y))
         const int rem = cnt - 32 * rb - 4 * L.g;  // rows 32 rb + kp(g, s) < cnt
 #pragma unroll
-        for (int s = 0; s < 8; ++s) ones[s] = cvt<T>((s & 3) + 16 * (s >> 2) < rem ? 1.f : 0.f);
+        for (int s = 0; s < 8; ++s) {
+          const int rr = (s & 3) + 16 * (s >> 2);
+          const float one = QRY ? ddb[bf][32 * rb + 4 * L.g + rr] : 1.f;
+          ones[s] = cvt<T>(rr < rem ? one : 0.f);
+        }
 #pragma unroll
         for (int mt = m0; mt < m1; ++mt) {
           const F kt = tile_pair_frag<T>(Lk[2 * rb][mt], Lk[2 * rb + 1][mt]);
@@ -279,13 +359,14 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   if constexpr (SUMS) {
     float* out = a.out + (head * a.P2 + part) * (size_t)M * (D + 1);
     const Lane L = this_lane();
+    const float vs = QRY ? a.drop_scale : 1.f;  // dN = s dY / D
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const size_t row = (size_t)(w * FW + 16 * mt + 4 * L.g + r) * (D + 1);
 #pragma unroll
-        for (int et = 0; et < ET; ++et) out[row + 16 * et + L.c] = S[mt][et][r];
+        for (int et = 0; et < ET; ++et) out[row + 16 * et + L.c] = vs * S[mt][et][r];
         if (L.c == 0) out[row + D] = Sz[mt][r];
       }
   } else {
@@ -311,6 +392,9 @@ hipError_t launch_ksum(const KsumArgs& a, int mode, hipStream_t s) {
   if (mode == kSumStates) {
     if (a.drop_t != 0) hipLaunchKernelGGL((ksum_kernel<G, kSumStates, true>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((ksum_kernel<G, kSumStates, false>), grid, dim3(256), 0, s, a);
+  } else if (mode == kSumQuery) {
+    // (dY is not masked: the dropout scale enters the output, the masks the walk)
+    hipLaunchKernelGGL((ksum_kernel<G, kSumQuery, false>), grid, dim3(256), 0, s, a);
   } else {
     hipLaunchKernelGGL((ksum_kernel<G, kSumMax, false>), grid, dim3(256), 0, s, a);
   }

@@ -928,8 +928,8 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     const size_t hf = (size_t)m.B * k * n * kHead;
     const float* X = Xr(r);
     const slim_problem p = att_problem(m, n);
-    CHECK_SLIM(slim_fwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, state_in, nullptr, Yh, state_out, nullptr, nullptr,
-                        attws, lay.attws_bytes, s));
+    CHECK_SLIM(slim_fwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, state_in, nullptr, Yh, nullptr, state_out, nullptr,
+                        nullptr, attws, lay.attws_bytes, s));
     hipLaunchKernelGGL(heads_to_rows_kernel, grid1(hf), dim3(256), 0, s, Yh, Ar(r), D, 0, 0, k, n, hf, hf);
     hipLaunchKernelGGL(ln_fwd_kernel, dim3(rows), dim3(256), 0, s, Ar(r), P.l[r].g1, P.l[r].b1n, X, Hr(r), s1r(r), D,
                        m.eps);
@@ -989,8 +989,8 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     hipLaunchKernelGGL(embed_kernel, dim3((unsigned)rows), dim3(256), 0, s, tokens, m.L, a, n, P.emb, D, V, Xr(0));
     for (int r = 0; r < m.s; ++r) {
       CHECK_SLIM(layer_qkv(r, n));
-      CHECK_SLIM(slim_fwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, nullptr, nullptr, Yh, delta, nullptr, nullptr,
-                          attws, lay.attws_bytes, s));
+      CHECK_SLIM(slim_fwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, nullptr, nullptr, Yh, nullptr, delta, nullptr,
+                          nullptr, attws, lay.attws_bytes, s));
       hipLaunchKernelGGL(sub_kernel, grid1(S), dim3(256), 0, s, bprev + r * S, states + r * S, delta, S);
       CHECK_HIP(hipGetLastError());
       CHECK_SLIM(layer_fwd(r, a, n, bprev + r * S, snew));
@@ -1024,7 +1024,7 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
       float* gin = gst + ((size_t)gcur * m.s + r) * S;
       float* gout = gst + ((size_t)(1 - gcur) * m.s + r) * S;
       CHECK_SLIM(slim_bwd(&p, Qhr(r, 0), Qhr(r, 1), Qhr(r, 2), ident, bprev + r * S, nullptr, nullptr, dYh, nullptr,
-                          gin, dQh, dQh + hf, dQh + 2 * hf, wd, gout, nullptr, attws, lay.attws_bytes, s));
+                          nullptr, gin, dQh, dQh + hf, dQh + 2 * hf, wd, gout, nullptr, attws, lay.attws_bytes, s));
       hipLaunchKernelGGL(heads_to_rows_kernel, grid1(3 * hf), dim3(256), 0, s, dQh, dQKV, 3 * D, 0, D, k, n, hf, 3 * hf);
       CHECK_HIP(hipGetLastError());
       // [Q K V] = X [Wq Wk Wv]: [dWq dWk dWv] += X^T [dQ dK dV];

@@ -53,16 +53,19 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(ScanArgs a) {
 }
 
 // out[p] = init + sum_{q > p} seg[q]: the state cotangent after segment p;
-// total = r0 (init + sum over all segments): the cotangent before segment 0
+// total = r0 (init + sum over all segments): the cotangent before segment 0.
+// With step > 1 the P entries are parts of P / step segments and out holds
+// the cotangent after each segment: out[i] = init + sum_{q >= (i + 1) step} seg[q].
 __global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
   const int head = blockIdx.y;
   const size_t SZ = a.SZ;
+  const int st = a.step > 1 ? a.step : 1, no = a.P / st;
   const int el = blockIdx.x * 256 + threadIdx.x;
   if (el < a.SZ) {
     float v = a.init ? a.init[head * SZ + el] : 0.f;
     for (int p = a.P - 1; p >= 0; --p) {
       const size_t idx = ((size_t)head * a.P + p) * SZ + el;
-      a.out[idx] = v;
+      if ((p + 1) % st == 0) a.out[((size_t)head * no + (p + 1) / st - 1) * SZ + el] = v;
       v += a.seg[idx];
     }
     if (a.total != nullptr) {

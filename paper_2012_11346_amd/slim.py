@@ -84,9 +84,9 @@ def _load() -> ctypes.CDLL:
     lib.slim_featmap.restype = i32
     lib.slim_context_bytes.argtypes = [P]
     lib.slim_context_bytes.restype = sz
-    lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, vp, sz, vp]
+    lib.slim_fwd.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, fp, vp, sz, vp]
     lib.slim_fwd.restype = i32
-    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, vp, fp, vp, vp, vp, fp, fp, fp, vp, sz, vp]
+    lib.slim_bwd.argtypes = [P, vp, vp, vp, fp, fp, fp, fp, vp, vp, fp, fp, vp, vp, vp, fp, fp, fp, vp, sz, vp]
     lib.slim_bwd.restype = i32
     lib.slim_status_string.argtypes = [i32]
     lib.slim_status_string.restype = ctypes.c_char_p
@@ -96,7 +96,7 @@ def _load() -> ctypes.CDLL:
     lib.slim_time_walk.restype = i32
     lib.slim_noalloc_scratch_bytes.argtypes = []
     lib.slim_noalloc_scratch_bytes.restype = sz
-    lib.slim_fwd_noalloc.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, vp]
+    lib.slim_fwd_noalloc.argtypes = [P, vp, vp, vp, fp, fp, fp, vp, fp, fp, fp, fp, vp]
     lib.slim_fwd_noalloc.restype = i32
     MP = ctypes.POINTER(ModelDesc)
     lib.slim_model_num_params.argtypes = [MP]
@@ -244,9 +244,11 @@ def _need_ctx(p: Problem, ctx: Optional[torch.Tensor]):
 
 
 def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3, ws=None,
-        Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0, within="iter"):
+        Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0, within="iter",
+        logD=None):
     """Forward sweep.  Returns (Y, state_out [B,H,M,d+1], kshift_out [B,H] or None).
-    ctx (optional, from new_context) receives the segment boundary states for bwd.
+    ctx (optional, from new_context) receives the segment boundary states for bwd;
+    logD (optional float32 [B,H,L], tile-walk mode only) the row normalisers.
     dropout / seed: value dropout with per-slice seeds; within: "iter",
     "quadratic" or "ps" (include/slim.h)."""
     p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed, within)
@@ -269,19 +271,24 @@ def fwd(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_e
     if kshift_out is not None:
         _need(kshift_out, "kshift_out", torch.float32, (p.B, p.H))
     _need_ctx(p, ctx)
+    if logD is not None:
+        _need(logD, "logD", torch.float32, (p.B, p.H, p.L))
     ws = _workspace(p, PHASE_FWD, dev, ws)
     _check(LIB.slim_fwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
-                        _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
+                        _ptr(Y), _ptr(logD), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _ptr(ws), _nbytes(ws),
+                        _stream()))
     return Y, state_out, kshift_out
 
 
 def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshift_in=None, dstate_out=None,
         want_dstate_in: bool = False, relu_eps: float = 1e-3, ws=None, dQ=None, dK=None, dV=None, dW=None,
-        ctx=None, dropout: float = 0.0, seed: int = 0, within="iter", Y=None):
+        ctx=None, dropout: float = 0.0, seed: int = 0, within="iter", Y=None, logD=None):
     """Backward sweep; kshift is the forward's kshift_out (FAVOR+); ctx (optional)
     is the context the forward wrote for the same inputs; Y (optional) the
     forward's output, from which the row cotangents of the recomputed slices
-    are taken (the bf16 tile walk; elsewhere ignored).
+    are taken, and logD (optional, with Y) its row normalisers, from which the
+    state cotangents of the segments are summed before the walks (the bf16
+    tile walk; elsewhere ignored).
 
     Returns (dQ, dK, dV, dW [M, d] float32, dstate_in or None)."""
     p = _problem_of(Q, W, C, kind, relu_eps, dropout, seed, within)
@@ -290,6 +297,8 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
         _need(t, n, Q.dtype, shp)
     if Y is not None:
         _need(Y, "Y", Q.dtype, shp)
+    if logD is not None:
+        _need(logD, "logD", torch.float32, (p.B, p.H, p.L))
     _need(W, "W", torch.float32, (p.M, p.d))
     sshape = (p.B, p.H, p.M, p.d + 1)
     for n, t in (("state_in", state_in), ("dstate_out", dstate_out)):
@@ -310,7 +319,7 @@ def bwd(Q, K, V, W, dY, C: int, kshift=None, kind="favor+", state_in=None, kshif
     _need_ctx(p, ctx)
     ws = _workspace(p, PHASE_BWD, dev, ws)
     _check(LIB.slim_bwd(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in), _ptr(kshift_in),
-                        _ptr(kshift), _ptr(dY), _ptr(Y), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
+                        _ptr(kshift), _ptr(dY), _ptr(Y), _ptr(logD), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
                         _ptr(dW), _ptr(dstate_in), _ptr(ctx), _ptr(ws), _nbytes(ws), _stream()))
     return dQ, dK, dV, dW, dstate_in
 
@@ -323,17 +332,20 @@ class _Attention(torch.autograd.Function):
     @staticmethod
     def forward(fctx, Q, K, V, W, C, kind, relu_eps, dropout, seed, within):
         c = new_context(Q, W, C, kind, relu_eps, within)
-        Y, _, ks = fwd(Q, K, V, W, C, kind, relu_eps=relu_eps, ctx=c, dropout=dropout, seed=seed, within=within)
+        # the row normalisers (tile-walk mode): 4 bytes per row, kept like Y
+        lD = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device) if within == "iter" else None
+        Y, _, ks = fwd(Q, K, V, W, C, kind, relu_eps=relu_eps, ctx=c, dropout=dropout, seed=seed, within=within,
+                       logD=lD)
         fctx.save_for_backward(Q, K, V, W, Y)
-        fctx.args = (C, kind, relu_eps, dropout, seed, within, ks, c)
+        fctx.args = (C, kind, relu_eps, dropout, seed, within, ks, c, lD)
         return Y
 
     @staticmethod
     def backward(fctx, dY):
         Q, K, V, W, Y = fctx.saved_tensors
-        C, kind, relu_eps, dropout, seed, within, ks, c = fctx.args
+        C, kind, relu_eps, dropout, seed, within, ks, c, lD = fctx.args
         dQ, dK, dV, dW, _ = bwd(Q, K, V, W, dY.contiguous(), C, ks, kind, relu_eps=relu_eps, ctx=c, dropout=dropout,
-                                seed=seed, within=within, Y=Y)
+                                seed=seed, within=within, Y=Y, logD=lD)
         return dQ, dK, dV, dW, None, None, None, None, None, None
 
 
@@ -347,7 +359,7 @@ def attention(Q, K, V, W, C: int, kind="favor+", relu_eps: float = 1e-3, dropout
 
 
 def fwd_noalloc(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None, relu_eps: float = 1e-3,
-                Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0):
+                Y=None, state_out=None, kshift_out=None, ctx=None, dropout: float = 0.0, seed: int = 0, logD=None):
     """fwd through slim_fwd_noalloc: the library's static device scratch
     replaces the workspace (outputs not passed in are allocated here, by
     torch, before the call; the call itself allocates nothing)."""
@@ -371,8 +383,11 @@ def fwd_noalloc(Q, K, V, W, C: int, kind="favor+", state_in=None, kshift_in=None
     if kshift_out is not None:
         _need(kshift_out, "kshift_out", torch.float32, (p.B, p.H))
     _need_ctx(p, ctx)
+    if logD is not None:
+        _need(logD, "logD", torch.float32, (p.B, p.H, p.L))
     _check(LIB.slim_fwd_noalloc(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(state_in),
-                                _ptr(kshift_in), _ptr(Y), _ptr(state_out), _ptr(kshift_out), _ptr(ctx), _stream()))
+                                _ptr(kshift_in), _ptr(Y), _ptr(logD), _ptr(state_out), _ptr(kshift_out), _ptr(ctx),
+                                _stream()))
     return Y, state_out, kshift_out
 
 

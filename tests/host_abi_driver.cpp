@@ -90,24 +90,39 @@ int main() {
   // ---- entry points rejected before any device call
   const slim_problem p = problem(2, 3, 1000, 64, 256, 64, SLIM_BF16, SLIM_FAVOR_PLUS, SLIM_WITHIN_ITER);
   float* F = (float*)block;
-  EXPECT(slim_fwd(&p, nullptr, A, A, F, nullptr, nullptr, A, F, F, nullptr, A, 1 << 20, nullptr) == SLIM_EINVAL);
-  EXPECT(slim_fwd(&p, A, A, A, F, nullptr, nullptr, A, F, nullptr, nullptr, A, 1 << 20, nullptr) == SLIM_EINVAL);
-  EXPECT(slim_fwd(&p, A, A, A, F, nullptr, nullptr, A, F, F, nullptr, A, 0, nullptr) == SLIM_EWORKSPACE);
-  EXPECT(slim_fwd(&p, (char*)A + 2, A, A, F, nullptr, nullptr, A, F, F, nullptr, A, 1 << 20, nullptr) ==
+  EXPECT(slim_fwd(&p, nullptr, A, A, F, nullptr, nullptr, A, nullptr, F, F, nullptr, A, 1 << 20, nullptr) ==
          SLIM_EINVAL);
-  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, nullptr, A, A, F, nullptr, nullptr, A,
-                  1 << 20, nullptr) == SLIM_EINVAL);
-  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, A, A, A, F, nullptr, nullptr, A, 0,
-                  nullptr) == SLIM_EWORKSPACE);
-  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, (char*)A + 2, nullptr, A, A, A, F, nullptr, nullptr, A,
+  EXPECT(slim_fwd(&p, A, A, A, F, nullptr, nullptr, A, nullptr, F, nullptr, nullptr, A, 1 << 20, nullptr) ==
+         SLIM_EINVAL);
+  EXPECT(slim_fwd(&p, A, A, A, F, nullptr, nullptr, A, nullptr, F, F, nullptr, A, 0, nullptr) == SLIM_EWORKSPACE);
+  EXPECT(slim_fwd(&p, (char*)A + 2, A, A, F, nullptr, nullptr, A, nullptr, F, F, nullptr, A, 1 << 20, nullptr) ==
+         SLIM_EINVAL);
+  {
+    // logD: misaligned; and in a mode that does not write it
+    EXPECT(slim_fwd(&p, A, A, A, F, nullptr, nullptr, A, (float*)((char*)A + 2), F, F, nullptr, A, 1 << 20,
+                    nullptr) == SLIM_EINVAL);
+    slim_problem q = p;
+    q.within = SLIM_WITHIN_QUADRATIC;
+    EXPECT(slim_fwd(&q, A, A, A, F, nullptr, nullptr, A, F, F, F, nullptr, A, 1 << 30, nullptr) ==
+           SLIM_EUNSUPPORTED);
+  }
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, nullptr, nullptr, A, A, F, nullptr,
+                  nullptr, A, 1 << 20, nullptr) == SLIM_EINVAL);
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, nullptr, nullptr, A, A, A, F, nullptr, nullptr, A,
+                  0, nullptr) == SLIM_EWORKSPACE);
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, (char*)A + 2, nullptr, nullptr, A, A, A, F, nullptr,
+                  nullptr, A, 1 << 20, nullptr) == SLIM_EINVAL);
+  // logD without Y
+  EXPECT(slim_bwd(&p, A, A, A, F, nullptr, nullptr, F, A, nullptr, F, nullptr, A, A, A, F, nullptr, nullptr, A,
                   1 << 20, nullptr) == SLIM_EINVAL);
   EXPECT(slim_featmap(&p, nullptr, F, SLIM_QUERY, F, F, nullptr) == SLIM_EINVAL);
   EXPECT(slim_featmap(&p, A, F, 5, F, F, nullptr) == SLIM_EINVAL);
   {
     const slim_problem bad = problem(1, 1, 0, 64, 256, 64, SLIM_BF16, SLIM_FAVOR_PLUS, SLIM_WITHIN_ITER);
-    EXPECT(slim_fwd_noalloc(&bad, A, A, A, F, nullptr, nullptr, A, F, F, nullptr, nullptr) == SLIM_EINVAL);
+    EXPECT(slim_fwd_noalloc(&bad, A, A, A, F, nullptr, nullptr, A, nullptr, F, F, nullptr, nullptr) == SLIM_EINVAL);
     const slim_problem big = problem(64, 64, 262144, 64, 256, 64, SLIM_BF16, SLIM_FAVOR_PLUS, SLIM_WITHIN_ITER);
-    EXPECT(slim_fwd_noalloc(&big, A, A, A, F, nullptr, nullptr, A, F, F, nullptr, nullptr) == SLIM_EUNSUPPORTED);
+    EXPECT(slim_fwd_noalloc(&big, A, A, A, F, nullptr, nullptr, A, nullptr, F, F, nullptr, nullptr) ==
+           SLIM_EUNSUPPORTED);
   }
   EXPECT(slim_time_walk(9, nullptr, nullptr) == SLIM_EINVAL);
   EXPECT(slim_time_walk(SLIM_PHASE_FWD, A, nullptr) == SLIM_EINVAL);

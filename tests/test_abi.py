@@ -91,7 +91,7 @@ def test_invalid_problems_are_rejected(S, kw, code):
     p = _p(S, **kw)
     assert S.LIB.slim_workspace_bytes(ctypes.byref(p), 0) == 0
     assert S.LIB.slim_num_segments(ctypes.byref(p)) == 0
-    st = S.LIB.slim_fwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, 1, 1, None, 1, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), 1, 1, 1, 1, None, None, 1, None, 1, 1, None, 1, 1 << 30, None)
     assert st == code
     assert S.LIB.slim_last_error().decode()
 
@@ -102,27 +102,28 @@ A = 1 << 12
 
 def test_null_pointers_are_rejected_before_any_launch(S):
     p = _p(S)
-    # arguments: p, Q, K, V, W, state_in, kshift_in, Y, state_out, kshift_out, ws, ws_bytes, stream
-    st = S.LIB.slim_fwd(ctypes.byref(p), None, A, A, A, None, None, A, A, A, None, A, 1 << 30, None)
+    # arguments: p, Q, K, V, W, state_in, kshift_in, Y, logD, state_out, kshift_out, ctx, ws, ws_bytes, stream
+    st = S.LIB.slim_fwd(ctypes.byref(p), None, A, A, A, None, None, A, None, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # FAVOR+ needs a key-shift output
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, None, A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # a state without its shift
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, A, None, A, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, A, None, A, None, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
-    # arguments: p, Q, K, V, W, state_in, kshift_in, kshift, dY, Y, dstate_out, dQ, dK, dV, dW, dstate_in,
-    # ctx, ws, ws_bytes, stream
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, None, A, A, A,
-                        None, None, A, 1 << 30, None)
+    # arguments: p, Q, K, V, W, state_in, kshift_in, kshift, dY, Y, logD, dstate_out, dQ, dK, dV, dW,
+    # dstate_in, ctx, ws, ws_bytes, stream
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, None, None, A, A,
+                        A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # dQ missing
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, None, A, A, A, A,
-                        None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, None, A, None, None, None, A, A, A,
+                        A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # kshift missing (FAVOR+)
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, None, A, A, A, A,
-                        None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, A, None, A, A, None, None, None, A, A, A,
+                        A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL  # state_in without kshift_in
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, A, A, A, A, None, None, A, 0, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, None, None, A, A, A,
+                        A, None, None, A, 0, None)
     assert st == S.SLIM_EWORKSPACE
     st = S.LIB.slim_featmap(ctypes.byref(p), None, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL
@@ -133,18 +134,27 @@ def test_null_pointers_are_rejected_before_any_launch(S):
 def test_misaligned_tensors_are_rejected_before_any_launch(S):
     p = _p(S)
     # a row tensor (dY) 8 bytes off a 16-byte boundary
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, None, A, A, A, A,
-                        None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 8, None, None, None, A, A, A,
+                        A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
     # the optional Y, likewise
-    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A + 8, None, A, A, A, A,
-                        None, None, A, 1 << 30, None)
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A + 8, None, None, A, A, A,
+                        A, None, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
+    # logD: 4-byte aligned; only with Y in the backward; only in the tile-walk mode
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A + 2, A, A, None, A, 1 << 30, None)
+    assert st == S.SLIM_EINVAL and "aligned" in S.LIB.slim_last_error().decode()
+    st = S.LIB.slim_bwd(ctypes.byref(p), A, A, A, A, None, None, A, A, None, A, None, A, A, A,
+                        A, None, None, A, 1 << 30, None)
+    assert st == S.SLIM_EINVAL and "with Y" in S.LIB.slim_last_error().decode()
+    q = _p(S, within=S.WITHIN_QUADRATIC)
+    st = S.LIB.slim_fwd(ctypes.byref(q), A, A, A, A, None, None, A, A, A, A, None, A, 1 << 30, None)
+    assert st == S.SLIM_EUNSUPPORTED and "logD" in S.LIB.slim_last_error().decode()
     # the workspace
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, A, A, None, A + 4, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A, None, None, A, None, A, A, None, A + 4, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     # a float tensor (W) off a 4-byte boundary
-    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A + 2, None, None, A, A, A, None, A, 1 << 30, None)
+    st = S.LIB.slim_fwd(ctypes.byref(p), A, A, A, A + 2, None, None, A, None, A, A, None, A, 1 << 30, None)
     assert st == S.SLIM_EINVAL
     st = S.LIB.slim_featmap(ctypes.byref(p), A + 8, A, 0, A, A, None)
     assert st == S.SLIM_EINVAL

@@ -1,7 +1,7 @@
 """slim.attention as a torch operation: autograd's gradients are those of
-slim_bwd given the forward's Y (bitwise) and match the fp64 oracle within the
-bars, in every within-slice mode; dropout draws the same masks in the
-backward."""
+slim_bwd given the forward's Y and (tile-walk mode) logD, bitwise, and match
+the fp64 oracle within the bars, in every within-slice mode; dropout draws
+the same masks in the backward."""
 
 import pytest
 import torch
@@ -25,8 +25,9 @@ def test_autograd_equals_the_backward_call(within):
     leaves = [t.clone().requires_grad_(True) for t in (Q, K, V, W)]
     Y = slim.attention(*leaves, C, within=within)
     (Y.float() * dY.float()).sum().backward()
-    Y2, _, ks = slim.fwd(Q, K, V, W, C, within=within)
-    g = slim.bwd(Q, K, V, W, dY, C, ks, within=within, Y=Y2)
+    lD = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device) if within == "iter" else None
+    Y2, _, ks = slim.fwd(Q, K, V, W, C, within=within, logD=lD)
+    g = slim.bwd(Q, K, V, W, dY, C, ks, within=within, Y=Y2, logD=lD)
     torch.cuda.synchronize()
     assert torch.equal(Y.detach(), Y2)
     for n, leaf, ref in zip(("dQ", "dK", "dV", "dW"), leaves, g[:4]):
@@ -47,8 +48,9 @@ def test_autograd_with_dropout():
     leaves = [t.clone().requires_grad_(True) for t in (Q, K, V, W)]
     Y = slim.attention(*leaves, C, dropout=p, seed=seed)
     (Y.float() * dY.float()).sum().backward()
-    Y2, _, ks = slim.fwd(Q, K, V, W, C, dropout=p, seed=seed)
-    g = slim.bwd(Q, K, V, W, dY, C, ks, dropout=p, seed=seed, Y=Y2)
+    lD = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
+    Y2, _, ks = slim.fwd(Q, K, V, W, C, dropout=p, seed=seed, logD=lD)
+    g = slim.bwd(Q, K, V, W, dY, C, ks, dropout=p, seed=seed, Y=Y2, logD=lD)
     torch.cuda.synchronize()
     for n, leaf, ref in zip(("dQ", "dK", "dV", "dW"), leaves, g[:4]):
         assert torch.equal(leaf.grad, ref), n

@@ -26,9 +26,11 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("i, given_y", [(i, False) for i in range(len(CASES))] + [(1, True), (3, True), (4, True)])
+@pytest.mark.parametrize("i, given_y", [(i, False) for i in range(len(CASES))] + [(1, True), (3, True), (4, True)] +
+                         [(1, "logD"), (2, "logD"), (3, "logD")])
 def test_dropout_forward_backward(i, given_y):
-    """given_y: the backward also gets the forward's Y (with its dropout)."""
+    """given_y: the backward also gets the forward's Y (with its dropout);
+    "logD": and its logD (the carry-free backward)."""
     need_gpu()
     from paper_2012_11346_amd import slim
 
@@ -41,8 +43,10 @@ def test_dropout_forward_backward(i, given_y):
         os.environ["SLIM_SEGMENTS"] = str(segs)
     try:
         Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
-        Y, st, ks = slim.fwd(Q, K, V, W, C, kind, dropout=p, seed=seed)
-        dQ, dK, dV, dW, _ = slim.bwd(Q, K, V, W, dY, C, ks, kind, dropout=p, seed=seed, Y=Y if given_y else None)
+        lD = torch.empty((B, H, L), dtype=torch.float32, device=Q.device) if given_y == "logD" else None
+        Y, st, ks = slim.fwd(Q, K, V, W, C, kind, dropout=p, seed=seed, logD=lD)
+        dQ, dK, dV, dW, _ = slim.bwd(Q, K, V, W, dY, C, ks, kind, dropout=p, seed=seed, Y=Y if given_y else None,
+                                     logD=lD)
         torch.cuda.synchronize()
     finally:
         if old is None:

@@ -86,6 +86,63 @@ def test_forward_two_calls_equal_one(i):
     report("state_out (two calls)", a, b, TOL[dtype])
 
 
+def _logD_ref(x, kind, M):
+    """log2 of each row's denominator D_t = g(q_t) . sum_{j <= t} g(k_j)
+    (eq. 2), in the units slim_fwd states for logD: for FAVOR+ the terms
+    |q_t|^2 / 2 log2(e) + log2(M) / 2 that cancel between g(q)_m and D are
+    added back."""
+    Pq = O.feature_map(x["Q"], x["W"], kind)
+    Pk = O.feature_map(x["K"], x["W"], kind)
+    Dt = np.einsum("bhlm,bhlm->bhl", Pq, np.cumsum(Pk, axis=2))
+    ref = np.log2(Dt)
+    if kind == "favor+":
+        q = host64(x["Q"])
+        ref = ref + 0.5 * np.sum(q * q, axis=-1) / np.log(2.0) + 0.5 * np.log2(M)
+    return ref
+
+
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_forward_logD(i):
+    """The row normalisers logD against the definition (eq. 2): D from them
+    within the bar, relative (|2^(logD - ref) - 1|); a second call resuming
+    from the first's state writes those of its rows."""
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    name, B, H, L, d, M, C, dtype, kind = CASES[i]
+    print(f"[forward logD] case={name} B={B} H={H} L={L} d={d} M={M} C={C} {dtype} {kind}", flush=True)
+    x = _inputs(i, B, H, L, d, M, C, dtype, kind)
+    Q, K, V, W = (dev(x[k]) for k in ("Q", "K", "V", "W"))
+    lD = torch.full((B, H, L), float("nan"), dtype=torch.float32, device=Q.device)
+    slim.fwd(Q, K, V, W, C, kind, logD=lD)
+    cut = (L // 3) // 16 * 16 + 5
+    sl = lambda t, a, b: t[:, :, a:b].contiguous()
+    l1 = torch.full((B, H, cut), float("nan"), dtype=torch.float32, device=Q.device)
+    l2 = torch.full((B, H, L - cut), float("nan"), dtype=torch.float32, device=Q.device)
+    _, st1, ks1 = slim.fwd(sl(Q, 0, cut), sl(K, 0, cut), sl(V, 0, cut), W, C, kind, logD=l1)
+    slim.fwd(sl(Q, cut, L), sl(K, cut, L), sl(V, cut, L), W, C, kind, state_in=st1, kshift_in=ks1, logD=l2)
+    torch.cuda.synchronize()
+    ref = _logD_ref(x, kind, M)
+    tol = TOL[dtype]
+    for tag, got in (("logD", host64(lD)), ("logD (two calls)", np.concatenate([host64(l1), host64(l2)], axis=2))):
+        assert np.all(np.isfinite(got)), tag
+        err = float(np.max(np.abs(np.exp2(got - ref) - 1.0)))
+        print(f"  {tag}: max |D / D_ref - 1| = {err:.3e} (tol {tol})", flush=True)
+        assert err <= tol, tag
+
+
+def test_forward_logD_only_in_the_tile_walk_mode():
+    need_gpu()
+    from paper_2012_11346_amd import slim
+
+    x = _inputs(4, 1, 1, 64, 64, 256, 32, "bf16", "favor+")
+    Q, K, V, W = (dev(x[k]) for k in ("Q", "K", "V", "W"))
+    lD = torch.empty((1, 1, 64), dtype=torch.float32, device=Q.device)
+    for within in ("quadratic", "ps"):
+        with pytest.raises(RuntimeError, match="logD"):
+            slim.fwd(Q, K, V, W, 32, logD=lD, within=within)
+
+
 def test_forward_stress_large_logits():
     """Q, K scaled by 3: exponents of size ~50; the shifts keep fp32 in range.
     Rounded W: at this scale the bf16 rounding of a general float32 W alone

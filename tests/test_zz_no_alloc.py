@@ -19,7 +19,7 @@ from tests.gpu_common import TOL, dev, host64, need_gpu, report
 
 
 def _abi_fwd(S, p, Q, K, V, W, Y, st, ks, ctx, ws):
-    args = [ctypes.byref(p), S._ptr(Q), S._ptr(K), S._ptr(V), S._ptr(W), None, None, S._ptr(Y), S._ptr(st),
+    args = [ctypes.byref(p), S._ptr(Q), S._ptr(K), S._ptr(V), S._ptr(W), None, None, S._ptr(Y), None, S._ptr(st),
             S._ptr(ks), S._ptr(ctx)]
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     if ws is None:
@@ -36,7 +36,7 @@ def test_noalloc_rejects_problems_beyond_the_scratch():
     big = S.problem(64, 8, 4096, 64, 256, 64, S.BF16, S.FAVOR_PLUS)
     assert S.workspace_bytes(big, S.PHASE_FWD) > cap
     st = S.LIB.slim_fwd_noalloc(ctypes.byref(big), *([ctypes.c_void_p(16)] * 4), None, None,
-                                ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.c_void_p(16), None, None)
+                                ctypes.c_void_p(16), None, ctypes.c_void_p(16), ctypes.c_void_p(16), None, None)
     assert st == S.SLIM_EUNSUPPORTED
     assert "static scratch" in S.LIB.slim_last_error().decode()
 
