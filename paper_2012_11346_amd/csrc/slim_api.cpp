@@ -1404,6 +1404,7 @@ int slim_bwd(const slim_problem* p, const void* Q, const void* K, const void* V,
   a.V = V;
   a.dY = dY;
   a.Y = Y;  // read by the 8-wave walk (the other walks recompute N)
+  a.logD = logD;
   a.W = W;
   a.Wfrag = wf.out;
   a.kshift = favor ? kshift : nullptr;

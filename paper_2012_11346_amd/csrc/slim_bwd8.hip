@@ -80,8 +80,11 @@ struct Bwd8Lds {
 
 // DROP: value dropout on (its masks are generated only in that instantiation)
 // HY: the forward's output Y is given; dD = -rowdot(dY, Y) / D then needs
-// only the ones column of N (the denominators), not its value columns
-template <class G, bool DROP, bool HY>
+// only the ones column of N (the denominators), not its value columns.
+// HL (with HY): the forward's logD too; then D comes from it, N is not
+// recomputed at all, and the row cotangents are formed in the scores phase
+// (one barrier fewer per tile).
+template <class G, bool DROP, bool HY, bool HL>
 __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   typedef typename G::T T;
   typedef typename FragT<T>::type F;
@@ -183,6 +186,10 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
   const T* Vh = (const T*)a.V + hoff;
   const T* dYh = (const T*)a.dY + hoff;
   const T* Yh = HY ? (const T*)a.Y + hoff : nullptr;
+  const float* lDh = HL ? a.logD + head * (size_t)a.L : nullptr;
+  // 1 / D of the walk's units from logD: the row shift and the key shift
+  // (FAVOR+) taken out again
+  const float kshl = (HL && G::KIND == kFavor) ? a.kshift[head] * kLog2e : 0.f;
   T* dQh = (T*)a.dQ + hoff;
   T* dKh = (T*)a.dK + hoff;
   T* dVh = (T*)a.dV + hoff;
@@ -447,10 +454,12 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
     // dN, dD phase, loaded here so that the load is complete by then (rows
     // past the tile read row 0 of the tile and are not used)
     u32e yv = {};
+    float lv = 0.f;
     if constexpr (HY) {
       const int tid = fresh_tid();
-      const int t = red_row(tid);
-      yv = *(const u32e*)(Yh + (size_t)(start + (t < count ? t : 0)) * D + (tid % TPR) * EPT);
+      const int t = red_row(tid), tc = t < count ? t : 0;
+      yv = *(const u32e*)(Yh + (size_t)(start + tc) * D + (tid % TPR) * EPT);
+      if constexpr (HL) lv = lDh[start + tc];
     }
 
     // ---- Q~ of this wave's feature tiles -> Zq[t][m].  Rows past the tile
@@ -572,36 +581,25 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         sstore_half_T(oK, ZA, frag_hi(af[tt]), 16, 16 * tt);
       }
     }
-    // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
-    // (with Y given only the ones column, D)
-#pragma unroll
-    for (int tt = 0; tt < RT; ++tt) {
-#pragma unroll
-      for (int el = HY ? EH : 0; el <= EH; ++el) {
-        if (el == EH && !zown) break;
-        f32x4 acc = mma(zero4(), el < EH ? vT[el < EH ? el : 0] : ones_frag(L, count), af[tt]);
-#pragma unroll
-        for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
-        if (el < EH) {
-          store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * tt);
-        } else if (g == 0) {
-          RedYz[16 * tt + c] = acc[0];
-        }
-      }
-    }
-    __syncthreads();
-    L = fresh_lane();
-    g = L.g;
-    c = L.c;
-    fresh_offsets();
-
     // ---- dN = dY / D, dD = -(dY . N) / D^2 per row (TPR threads per row)
-    {
+    auto row_cotangents = [&]() {
       const int tid = fresh_tid();
       const int t = red_row(tid), q = tid % TPR;
       const bool ok = t < count;
-      const float den = sum_y1(t);
-      const float inv = ok ? 1.f / den : 0.f;
+      float inv;
+      if constexpr (HL) {
+        // D from logD, in the walk's units: 2^(row shift + key shift - logD)
+        float qsh = 0.f;
+        if (G::KIND == kFavor) {
+          const f32x4 m0 = *(const f32x4*)&qmx[t * 8], m1 = *(const f32x4*)&qmx[t * 8 + 4];
+          qsh = fmaxf(fmaxf(fmaxf(m0[0], m0[1]), fmaxf(m0[2], m0[3])), fmaxf(fmaxf(m1[0], m1[1]), fmaxf(m1[2], m1[3]))) *
+                    kLog2e + kshl;
+        }
+        inv = ok ? fast_exp2(qsh - lv) : 0.f;
+      } else {
+        const float den = sum_y1(t);
+        inv = ok ? 1.f / den : 0.f;
+      }
       // (value dropout: Y = s N / D with the output scale s; 1 without dropout)
       const float invs = inv * a.drop_scale;
       const int e = q * EPT, hh = e / (16 * EH), col = e - hh * 16 * EH;
@@ -633,6 +631,34 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
         dDs[t] = dd;
         dDb[t] = cvt<T>(dd);
       }
+    };
+    if constexpr (HL) {
+      // (nothing of N is needed; dY is not read before this point of the tile)
+      row_cotangents();
+    } else {
+      // N^T[e][t] = [V|1]^T A^T + [S|z]^T Q~^T over this slice, own columns -> RedY[t][e']
+      // (with Y given only the ones column, D)
+#pragma unroll
+      for (int tt = 0; tt < RT; ++tt) {
+#pragma unroll
+        for (int el = HY ? EH : 0; el <= EH; ++el) {
+          if (el == EH && !zown) break;
+          f32x4 acc = mma(zero4(), el < EH ? vT[el < EH ? el : 0] : ones_frag(L, count), af[tt]);
+#pragma unroll
+          for (int kb = 0; kb < MB; ++kb) acc = mma(acc, feat_frag(S, Sz, el, kb), qf[kb][tt]);
+          if (el < EH) {
+            store_tile_T<float>(L, RedY, LDRH, acc, 16 * el, 16 * tt);
+          } else if (g == 0) {
+            RedYz[16 * tt + c] = acc[0];
+          }
+        }
+      }
+      __syncthreads();
+      L = fresh_lane();
+      g = L.g;
+      c = L.c;
+      fresh_offsets();
+      row_cotangents();
     }
     __syncthreads();
     L = fresh_lane();
@@ -1108,12 +1134,15 @@ __global__ __launch_bounds__(512, 1) void bwd_walk8_kernel(BwdArgs a) {
 template <class G>
 hipError_t launch_bwd_walk8(const BwdArgs& a, hipStream_t s) {
   const dim3 grid(a.P, a.H, a.B);
+  const bool hy = a.Y != nullptr, hl = hy && a.logD != nullptr;
   if (a.drop_t != 0) {
-    if (a.Y != nullptr) hipLaunchKernelGGL((bwd_walk8_kernel<G, true, true>), grid, dim3(512), 0, s, a);
-    else hipLaunchKernelGGL((bwd_walk8_kernel<G, true, false>), grid, dim3(512), 0, s, a);
+    if (hl) hipLaunchKernelGGL((bwd_walk8_kernel<G, true, true, true>), grid, dim3(512), 0, s, a);
+    else if (hy) hipLaunchKernelGGL((bwd_walk8_kernel<G, true, true, false>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((bwd_walk8_kernel<G, true, false, false>), grid, dim3(512), 0, s, a);
   } else {
-    if (a.Y != nullptr) hipLaunchKernelGGL((bwd_walk8_kernel<G, false, true>), grid, dim3(512), 0, s, a);
-    else hipLaunchKernelGGL((bwd_walk8_kernel<G, false, false>), grid, dim3(512), 0, s, a);
+    if (hl) hipLaunchKernelGGL((bwd_walk8_kernel<G, false, true, true>), grid, dim3(512), 0, s, a);
+    else if (hy) hipLaunchKernelGGL((bwd_walk8_kernel<G, false, true, false>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((bwd_walk8_kernel<G, false, false, false>), grid, dim3(512), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -75,6 +75,7 @@ struct BwdArgs {
   const void* V;
   const void* dY;
   const void* Y;            // [B,H,L,d] the forward's output, or nullptr (recomputed); 8-wave walk only
+  const float* logD;        // [B,H,L] the forward's row normalisers (with Y), or nullptr; 8-wave walk only
   const float* W;
   const void* Wfrag;        // fragment-ordered W (WFragLayout)
   const float* kshift;      // [B,H] key shift of every state below (FAVOR+)
