@@ -85,21 +85,36 @@ __device__ __forceinline__ T pick3(int grp, T a, T b, T c) {
   return grp == 0 ? a : (grp == 1 ? b : c);
 }
 
-// the epilogue's operation on element o of C (n: the column, for the bias)
-__device__ __forceinline__ void epi_op(const Epi& e, float* C, size_t o, int n, float v) {
+// The epilogue's operation on element o of C (n: the column, for the bias),
+// split into its read (C for EPI_ACC, the bias, aux) and its write, so that
+// a tile's reads can all be issued before its first store (interleaved,
+// each store might alias the next read and they would run one at a time).
+__device__ __forceinline__ float epi_read(const Epi& e, const float* C, size_t o, int n) {
+  switch (e.op) {
+    case EPI_STORE: return 0.f;
+    case EPI_ACC: return C[o];
+    case EPI_BIAS:
+    case EPI_BIAS_GELU: return e.bias[n];
+    default: return e.aux[o];
+  }
+}
+__device__ __forceinline__ void epi_write(const Epi& e, float* C, size_t o, float v, float x) {
   switch (e.op) {
     case EPI_STORE: C[o] = v; break;
-    case EPI_ACC: C[o] += v; break;
-    case EPI_BIAS: C[o] = v + e.bias[n]; break;
+    case EPI_ACC: C[o] = x + v; break;
+    case EPI_BIAS: C[o] = v + x; break;
     case EPI_BIAS_GELU: {
-      const float z = v + e.bias[n];
+      const float z = v + x;
       C[o] = z;
       e.C2[o] = gelu_f(z);
       break;
     }
-    case EPI_GELU_BWD: C[o] = v * gelu_d(e.aux[o]); break;
-    default: C[o] = v + e.aux[o]; break;
+    case EPI_GELU_BWD: C[o] = v * gelu_d(x); break;
+    default: C[o] = v + x; break;
   }
+}
+__device__ __forceinline__ void epi_op(const Epi& e, float* C, size_t o, int n, float v) {
+  epi_write(e, C, o, v, epi_read(e, C, o, n));
 }
 // where element (m, n) of the product goes: its matrix (C or a group's) and
 // the offset in it; the row's and the column's parts of the offset add
@@ -297,35 +312,70 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     size_t* rowoff = reinterpret_cast<size_t*>(&As[0][0]);
     for (int i = tid; i < BM; i += 256) rowoff[i] = epi_row(g.epi, g.ldc, min(m0 + i, M - 1));
     __syncthreads();
+    // (per 16 x 32 block: its reads, then its writes; the column offsets are
+    // recomputed per block rather than held)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + wn + 16 * j + c;
-      if (n >= N) continue;
-      float* Cj = g.C;
-      const size_t co = epi_col(g.epi, Cj, n);
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int i = 0; i < TI; ++i)
+      for (int j2 = 0; j2 < 4; j2 += 2) {
+        float x[2][4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int mm = wm + 16 * i + 4 * q + r;
-          if (m0 + mm < M) epi_op(g.epi, Cj, rowoff[mm] + co, n, acc[i][j][r]);
+        for (int jj = 0; jj < 2; ++jj) {
+          const int n = n0 + wn + 16 * (j2 + jj) + c;
+          float* Cj = g.C;
+          const size_t co = epi_col(g.epi, Cj, min(n, N - 1));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int mm = wm + 16 * i + 4 * q + r;
+            x[jj][r] = (m0 + mm < M && n < N) ? epi_read(g.epi, Cj, rowoff[mm] + co, n) : 0.f;
+          }
         }
-    }
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int n = n0 + wn + 16 * (j2 + jj) + c;
+          float* Cj = g.C;
+          const size_t co = epi_col(g.epi, Cj, min(n, N - 1));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int mm = wm + 16 * i + 4 * q + r;
+            if (m0 + mm < M && n < N) epi_write(g.epi, Cj, rowoff[mm] + co, acc[i][j2 + jj][r], x[jj][r]);
+          }
+        }
+      }
     return;
   }
-  float* part = g.part + (size_t)blockIdx.y * M * N;
+  if (split) {
+    float* part = g.part + (size_t)blockIdx.y * M * N;
 #pragma unroll
-  for (int i = 0; i < TI; ++i)
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
+          if (m < M && n < N) part[(size_t)m * N + n] = acc[i][j][r];
+        }
+    return;
+  }
+  // the epilogue's reads first, then its writes, per 16-row block
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    float x[4][4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
-        if (m < M && n < N) {
-          if (split) part[(size_t)m * N + n] = acc[i][j][r];
-          else epi_op(g.epi, g.C, (size_t)m * g.ldc + n, n, acc[i][j][r]);
-        }
+        x[j][r] = (m < M && n < N) ? epi_read(g.epi, g.C, (size_t)m * g.ldc + n, n) : 0.f;
       }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
+        if (m < M && n < N) epi_write(g.epi, g.C, (size_t)m * g.ldc + n, acc[i][j][r], x[j][r]);
+      }
+  }
 }
 
 // C = epilogue(sum over splits of the partial products, in split order)
