@@ -8,6 +8,10 @@ zero outside the sampled heads isolates their share: its dW must match the
 oracle's dW of the sample, every other head's dQ, dK, dV must be exactly zero
 (dY = 0 makes every cotangent zero), and the sampled heads' dQ, dK, dV must
 be bitwise those of the first backward (heads do not interact).
+
+As in the benchmark, the backward gets the forward's Y and (tile-walk mode)
+logD, unless `given` is off (then it recomputes them and carries the
+segments' cotangents, D6).
 """
 
 import numpy as np
@@ -37,14 +41,16 @@ def _oracle(x, heads, kind):
     return Y, dQ, dK, dV, dW
 
 
-def _check(tag, x, heads, C, kind, ref, within="iter"):
+def _check(tag, x, heads, C, kind, ref, within="iter", given=True):
     from paper_2012_11346_amd import slim
 
     tol = TOL[{torch.bfloat16: "bf16", torch.float32: "f32"}[x["Q"].dtype]]
-    print(f"[full size] {tag} C={C} {within}: forward + backward on the whole batch", flush=True)
+    print(f"[full size] {tag} C={C} {within} given={given}: forward + backward on the whole batch", flush=True)
     Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
-    Y, st, ks = slim.fwd(Q, K, V, W, C, kind, within=within)
-    g = slim.bwd(Q, K, V, W, dY, C, ks, kind, within=within)
+    lD = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device) if given and within == "iter" else None
+    Y, st, ks = slim.fwd(Q, K, V, W, C, kind, within=within, logD=lD)
+    Yg = Y if given else None
+    g = slim.bwd(Q, K, V, W, dY, C, ks, kind, within=within, Y=Yg, logD=lD)
     torch.cuda.synchronize()
     Yr, dQr, dKr, dVr, dWr = ref
     report(f"{tag} C={C} Y (sampled heads)", _sample(Y, heads), Yr, tol)
@@ -56,13 +62,13 @@ def _check(tag, x, heads, C, kind, ref, within="iter"):
     for b, h in heads:
         mask[b, h] = True
     dYm = torch.where(mask[:, :, None, None], dY, torch.zeros_like(dY))
-    gm = slim.bwd(Q, K, V, W, dYm, C, ks, kind, within=within)
+    gm = slim.bwd(Q, K, V, W, dYm, C, ks, kind, within=within, Y=Yg, logD=lD)
     torch.cuda.synchronize()
     report(f"{tag} C={C} dW (sampled heads' share)", host64(gm[3]), dWr, tol)
     for n, a, full in zip(("dQ", "dK", "dV"), gm[:3], g[:3]):
         assert torch.count_nonzero(a[~mask]).item() == 0, f"{n}: heads with dY = 0 must get exact zeros"
         assert torch.equal(a[mask], full[mask]), f"{n}: sampled heads differ between the two backward calls"
-    del Q, K, V, W, dY, dYm, Y, st, ks, g, gm
+    del Q, K, V, W, dY, dYm, Y, Yg, lD, st, ks, g, gm
     torch.cuda.empty_cache()
 
 
@@ -87,6 +93,18 @@ def test_slice_sweep_full_size():
     ref = _oracle(x, heads, wl.kind)
     for C in wl.C:
         _check(wl.name, x, heads, C, wl.kind, ref)
+
+
+def test_slice_sweep_full_size_without_forward_outputs():
+    """The headline problem at C=64 with the backward recomputing N and D
+    and carrying the segments' cotangents (no Y, no logD)."""
+    need_gpu()
+    wl = workload("sweep_32k")
+    heads = [(2, 1)]
+    x = make_inputs(wl)
+    print("[full size] oracle on the sampled head", flush=True)
+    ref = _oracle(x, heads, wl.kind)
+    _check(wl.name, x, heads, 64, wl.kind, ref, given=False)
 
 
 def test_slice_sweep_full_size_rounded_w():
