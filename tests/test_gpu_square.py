@@ -42,12 +42,19 @@ def test_square_map_forward_backward(i):
     print(f"[square] case={name} B={B} H={H} L={L} d={d} M=64 C={C} {dtype}", flush=True)
     x = _inputs(i, B, H, L, d, dtype, identity)
     Q, K, V, W, dY = (dev(x[k]) for k in ("Q", "K", "V", "W", "dY"))
-    Y, st, ks = slim.fwd(Q, K, V, W, C, "square")
-    dQ, dK, dV, dW, _ = slim.bwd(Q, K, V, W, dY, C, ks, "square")
+    lD = torch.empty((B, H, L), dtype=torch.float32, device=Q.device)
+    Y, st, ks = slim.fwd(Q, K, V, W, C, "square", logD=lD)
+    dQ, dK, dV, dW, _ = slim.bwd(Q, K, V, W, dY, C, ks, "square", Y=Y, logD=lD)
     torch.cuda.synchronize()
     assert ks is None
     tol = TOL[dtype]
     report("Y", host64(Y), O.attention_forward(x["Q"], x["K"], x["V"], x["W"], O.SQUARE), tol)
+    # logD = log2 of D_t = g(q_t) . sum_{j <= t} g(k_j) (eq. 2; no shifts for this map)
+    Pq, Pk = (O.feature_map(x[n], x["W"], O.SQUARE) for n in ("Q", "K"))
+    Dt = np.einsum("bhlm,bhlm->bhl", Pq, np.cumsum(Pk, axis=2))
+    err = float(np.max(np.abs(np.exp2(host64(lD) - np.log2(Dt)) - 1.0)))
+    print(f"  logD: max |D / D_ref - 1| = {err:.3e} (tol {tol})", flush=True)
+    assert err <= tol
     _, stref = O.slim_forward(x["Q"], x["K"], x["V"], x["W"], C, O.SQUARE, within="quadratic")
     report("state_out", host64(st), stref, tol)
     ref = O.attention_backward(x["Q"], x["K"], x["V"], x["W"], x["dY"], O.SQUARE)
