@@ -62,6 +62,21 @@ def flops_per_token_head(d: int, M: int, c: int):
     return fwd, bwd
 
 
+def walk_takes_forward_outputs(dtype: str, M: int, kind: str) -> bool:
+    """Whether the reverse walk, given the forward's Y and logD (as the
+    benchmark's backward is), recomputes neither N nor D: the 8-wave walk
+    (bf16, M in {128, 256}, FAVOR+ or ReLU)."""
+    return dtype == "bf16" and M in (128, 256) and kind in ("favor+", "relu")
+
+
+def executed_bwd_flops(d: int, M: int, c: int, given: bool) -> int:
+    """The reverse walk's executed flops per token-head with its c-row block;
+    given the forward's Y and logD it skips the numerators and denominators
+    N = Q~[S|z] + A[V|1] of the recomputed block: 2M(d+1) + (d+1)(c+1)."""
+    b = flops_per_token_head(d, M, c)[1]
+    return b - (2 * M * (d + 1) + (d + 1) * (c + 1)) if given else b
+
+
 def kernel_sources_sha() -> str:
     """Hash of the sources the attention kernels are compiled from (every
     file under csrc/ but the model step's own translation unit, which they
@@ -347,13 +362,15 @@ def main():
     value = tokens / (r["ms"] / 1e3)
     alg_f, alg_b = flops_per_token_head(d, M, C)
     blk = min(C, TILE_ROWS)
-    ex_f, ex_b = flops_per_token_head(d, M, blk)
+    given = walk_takes_forward_outputs(wl.dtype, M, kind)
+    ex_b = executed_bwd_flops(d, M, blk, given)
     dominant = bwd_walk_name(wl.dtype, M, kind)
     rl = roofline(dominant, wl.dtype, units, alg_b, r["bwd_walk_ms"])
     rl["traffic"] = load_traffic(dominant)
     rl["flops_basis"] = (f"algorithmic count with the slice as one quadratic form (c = C = {C}); the kernel "
-                         f"executes {ex_b} flops per token-head with its {blk}-row in-slice block, frac "
-                         f"{units * ex_b / (r['bwd_walk_ms'] / 1e3) / PEAK_BF16_FLOPS:.3f} on that count")
+                         f"executes {ex_b} flops per token-head with its {blk}-row in-slice block"
+                         + (" (N and D from the forward's Y and logD, not recomputed)" if given else "")
+                         + f", frac {units * ex_b / (r['bwd_walk_ms'] / 1e3) / PEAK_BF16_FLOPS:.3f} on that count")
     out = {
         "metric": METRIC,
         "value": value,
@@ -399,7 +416,7 @@ def main():
             ly = Layer(x, Cs, kind)
             rs = timed([ly], args.sweep_steps, 5)
             blk_s = min(Cs, TILE_ROWS)
-            exf, exb = flops_per_token_head(d, M, blk_s)
+            exb = executed_bwd_flops(d, M, blk_s, walk_takes_forward_outputs(wl.dtype, M, kind))
             algf, algb = flops_per_token_head(d, M, Cs)
             rec = {"C": Cs, "in_slice_block": blk_s, "tokens_per_s": tokens / (rs["ms"] / 1e3),
                    "ms_per_step": rs["ms"], "bwd_walk_ms": rs["bwd_walk_ms"],
@@ -515,7 +532,7 @@ def main():
             rc = timed(layers, steps, 5)
             u = w2.B * w2.H * w2.L
             blk_w = min(Cw, TILE_ROWS)
-            exf, exb = flops_per_token_head(w2.d, w2.M, blk_w)
+            exb = executed_bwd_flops(w2.d, w2.M, blk_w, walk_takes_forward_outputs(w2.dtype, w2.M, w2.kind))
             algf, algb = flops_per_token_head(w2.d, w2.M, Cw)
             kname = bwd_walk_name(w2.dtype, w2.M, w2.kind)
             rec = {"workload": f"{name}: {KIND_LABEL[w2.kind]}, {w2.layers} layer(s) x (B={w2.B} H={w2.H} L={w2.L} "
