@@ -591,29 +591,57 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* x, const float
   }
 }
 
-// Column sums in a fixed order, two stages: part[z][c][j] = sum of rows
-// [64 c, 64 c + 64) of src_z's column j (rows in order), then out_z[j] +=
-// sum over c in order.  z selects one of two independent sums.
+// Column sums in a fixed order.  A workgroup takes 64 columns; its four
+// waves take interleaved quarters of the rows (wave q: rows q, q + 4, ...
+// of the range, eight loads in flight per lane), and the four partial sums
+// are added in wave order through LDS.  One stage when the rows fit one
+// chunk of 64 (out_z[j] += the sum); else part[z][c][j] = the sum of chunk c
+// and a second stage adds the chunks the same way (wave q: chunks q, q + 4,
+// ...).  z selects one of two independent sums.
 constexpr int kColChunk = 64;
 struct ColsumArgs {
   const float* src[2];
   float* out[2];
 };
-__global__ __launch_bounds__(256) void colsum_part_kernel(ColsumArgs a, int rows, int n, float* part) {
-  const int j = blockIdx.x * 256 + threadIdx.x, c = blockIdx.y, z = blockIdx.z;
-  if (j >= n) return;
-  const float* src = a.src[z];
-  const int r1 = min(rows, (c + 1) * kColChunk);
+// sum of rows r0, r0 + 4, r0 + 8, ... < r1 of column j (stride n), in order
+__device__ __forceinline__ float colsum_strided(const float* src, int r0, int r1, size_t n, int j) {
   float s = 0.f;
-  for (int r = c * kColChunk; r < r1; ++r) s += src[(size_t)r * n + j];
-  part[((size_t)z * gridDim.y + c) * n + j] = s;
+  int r = r0;
+  for (; r + 28 < r1; r += 32) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = src[(size_t)(r + 4 * k) * n + j];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += v[k];
+  }
+  for (; r < r1; r += 4) s += src[(size_t)r * n + j];
+  return s;
+}
+// the four waves' sums of each column, added in wave order
+__device__ __forceinline__ float colsum_waves(float v, float (*red)[64], int q, int jj) {
+  red[q][jj] = v;
+  __syncthreads();
+  return ((red[0][jj] + red[1][jj]) + red[2][jj]) + red[3][jj];
+}
+__global__ __launch_bounds__(256) void colsum_part_kernel(ColsumArgs a, int rows, int n, float* part) {
+  __shared__ float red[4][64];
+  const int q = threadIdx.x >> 6, jj = threadIdx.x & 63;
+  const int j = blockIdx.x * 64 + jj, c = blockIdx.y, z = blockIdx.z;
+  const int r1 = min(rows, (c + 1) * kColChunk);
+  const float v = j < n ? colsum_strided(a.src[z], c * kColChunk + q, r1, n, j) : 0.f;
+  const float t = colsum_waves(v, red, q, jj);
+  if (q == 0 && j < n) {
+    if (gridDim.y == 1) a.out[z][j] += t;  // one chunk: the sum itself
+    else part[((size_t)z * gridDim.y + c) * n + j] = t;
+  }
 }
 __global__ __launch_bounds__(256) void colsum_final_kernel(ColsumArgs a, int chunks, int n, const float* part) {
-  const int j = blockIdx.x * 256 + threadIdx.x, z = blockIdx.y;
-  if (j >= n) return;
-  float s = 0.f;
-  for (int c = 0; c < chunks; ++c) s += part[((size_t)z * chunks + c) * n + j];
-  a.out[z][j] += s;
+  __shared__ float red[4][64];
+  const int q = threadIdx.x >> 6, jj = threadIdx.x & 63;
+  const int j = blockIdx.x * 64 + jj, z = blockIdx.y;
+  const float v = j < n ? colsum_strided(part + (size_t)z * chunks * n, q, chunks, n, j) : 0.f;
+  const float t = colsum_waves(v, red, q, jj);
+  if (q == 0 && j < n) a.out[z][j] += t;
 }
 
 __global__ __launch_bounds__(256) void copy_kernel(float* dst, const float* src, size_t total) {
@@ -954,8 +982,9 @@ int step(const Dims& m, const int* tokens, const Params& P, const Grads& G, floa
     ca.src[1] = src1;
     ca.out[1] = out1;
     const int nz = src1 ? 2 : 1, chunks = (rows + kColChunk - 1) / kColChunk;
-    hipLaunchKernelGGL(colsum_part_kernel, dim3((n + 255) / 256, chunks, nz), dim3(256), 0, s, ca, rows, n, red);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((n + 255) / 256, nz), dim3(256), 0, s, ca, chunks, n, red);
+    hipLaunchKernelGGL(colsum_part_kernel, dim3((n + 63) / 64, chunks, nz), dim3(256), 0, s, ca, rows, n, red);
+    if (chunks > 1)
+      hipLaunchKernelGGL(colsum_final_kernel, dim3((n + 63) / 64, nz), dim3(256), 0, s, ca, chunks, n, red);
   };
 
   // identity W of the square map: g(x) = (x_i^2)
