@@ -357,24 +357,30 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         }
     return;
   }
-  // the epilogue's reads first, then its writes, per 16-row block
+  // the epilogue's reads first, then its writes: all of a lane's with the
+  // 64-row tile, per 16-row block with the 128-row one (registers)
+  constexpr int IB = TI <= 2 ? TI : 1;
 #pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    float x[4][4];
+  for (int i0 = 0; i0 < TI; i0 += IB) {
+    float x[IB][4][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int ii = 0; ii < IB; ++ii)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
-        x[j][r] = (m < M && n < N) ? epi_read(g.epi, g.C, (size_t)m * g.ldc + n, n) : 0.f;
-      }
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + wm + 16 * (i0 + ii) + 4 * q + r, n = n0 + wn + 16 * j + c;
+          x[ii][j][r] = (m < M && n < N) ? epi_read(g.epi, g.C, (size_t)m * g.ldc + n, n) : 0.f;
+        }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
-        if (m < M && n < N) epi_write(g.epi, g.C, (size_t)m * g.ldc + n, acc[i][j][r], x[j][r]);
-      }
+    for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + wm + 16 * (i0 + ii) + 4 * q + r, n = n0 + wn + 16 * j + c;
+          if (m < M && n < N) epi_write(g.epi, g.C, (size_t)m * g.ldc + n, acc[i0 + ii][j][r], x[ii][j][r]);
+        }
   }
 }
 
@@ -396,9 +402,11 @@ inline GemmPlan gemm_plan(int M, int N, int K) {
   GemmPlan p;
   p.tiles_n = (N + GBN - 1) / GBN;
   const int t128 = ((M + 127) / 128) * p.tiles_n;
-  p.BM = t128 >= 256 ? 128 : 64;
-  p.tiles = ((M + p.BM - 1) / p.BM) * p.tiles_n;
   const int kt = (K + GBK - 1) / GBK;
+  // (a short reduction leaves the epilogue's reads and writes of C to set
+  // the pace: the smaller tile gives twice the workgroups in flight)
+  p.BM = (t128 >= 256 && kt > 8) ? 128 : 64;
+  p.tiles = ((M + p.BM - 1) / p.BM) * p.tiles_n;
   int s = 1;
   // split long K until about 512 workgroups run, keeping >= 8 k tiles each
   while (p.tiles * s < 512 && kt >= 16 * s && s < 64) s *= 2;  // next split keeps >= 8 k tiles
