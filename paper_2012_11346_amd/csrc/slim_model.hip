@@ -389,8 +389,15 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* part, int
                                                           Epi epi) {
   const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x, MN = (size_t)M * N;
   if (e >= MN) return;
+  // (four partials loaded at a time, added in split order)
   float v = 0.f;
-  for (int s = 0; s < splits; ++s) v += part[s * MN + e];
+  int s = 0;
+  for (; s + 4 <= splits; s += 4) {
+    const float p0 = part[s * MN + e], p1 = part[(s + 1) * MN + e], p2 = part[(s + 2) * MN + e],
+                p3 = part[(s + 3) * MN + e];
+    v = (((v + p0) + p1) + p2) + p3;
+  }
+  for (; s < splits; ++s) v += part[s * MN + e];
   epi_store(epi, C, ldc, (int)(e / N), (int)(e % N), v);
 }
 
