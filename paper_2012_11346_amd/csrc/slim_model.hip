@@ -389,9 +389,16 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* part, int
                                                           Epi epi) {
   const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x, MN = (size_t)M * N;
   if (e >= MN) return;
-  // (four partials loaded at a time, added in split order)
+  // (eight, then four partials loaded at a time, added in split order)
   float v = 0.f;
   int s = 0;
+  for (; s + 8 <= splits; s += 8) {
+    float q[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) q[i] = part[(s + i) * MN + e];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v += q[i];
+  }
   for (; s + 4 <= splits; s += 4) {
     const float p0 = part[s * MN + e], p1 = part[(s + 1) * MN + e], p2 = part[(s + 2) * MN + e],
                 p3 = part[(s + 3) * MN + e];
