@@ -89,6 +89,18 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   typedef WFragLayout<G> WL;
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(a.Wfrag), (short)0, LO_TABLE ? (int)(WL::TOTAL * 64 * sizeof(F)) : 0, 0x00020000);
+  // With the fragment table, the high parts of the wave's fragments are
+  // staged once into LDS (8 KiB per wave; each wave reads back only its
+  // own), so each chunk fetches only the low parts from memory.
+  __shared__ __attribute__((aligned(16))) F Wsh[LO_TABLE ? 4 * WL::NA * 64 : 1];
+  if constexpr (LO_TABLE) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < WL::NA; ++i)
+      Wsh[(w * WL::NA + i) * 64 + lane] = __builtin_bit_cast(
+          F, __builtin_amdgcn_raw_buffer_load_b128(wrs, lane * (int)sizeof(F),
+                                                   WL::a(w, i / EB, i % EB) * 64 * (int)sizeof(F), 0));
+  }
 
   // rows of this part
   const TileMap tm(a.L, a.C, 32);
@@ -292,7 +304,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
     f32x4 Lk[CT][MT];
     if constexpr (LO_TABLE) {
       typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-      const int wlane = (fresh_tid() & 63) * (int)sizeof(F);
+      const int lane = fresh_tid() & 63, wlane = lane * (int)sizeof(F);
 #pragma unroll
       for (int m2 = 0; m2 < MT; m2 += 2) {
         F Wh[2][EB], Wt[2][EB];
@@ -300,8 +312,7 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int kb = 0; kb < EB; ++kb) {
-            Wh[i][kb] = __builtin_bit_cast(
-                F, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, WL::a(w, m2 + i, kb) * 64 * (int)sizeof(F), 0));
+            Wh[i][kb] = Wsh[(w * WL::NA + (m2 + i) * EB + kb) * 64 + lane];
             Wt[i][kb] = __builtin_bit_cast(
                 F, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, WL::alo(w, m2 + i, kb) * 64 * (int)sizeof(F), 0));
           }
