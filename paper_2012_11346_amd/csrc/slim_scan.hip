@@ -44,11 +44,25 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(ScanArgs a) {
   const int el = blockIdx.x * 256 + threadIdx.x;
   if (el < a.SZ) {
     float v = a.init ? r0 * a.init[head * SZ + el] : 0.f;
-    for (int p = 0; p < a.P; ++p) {
-      a.out[((size_t)head * (a.P + 1) + p) * SZ + el] = v;
-      v += a.seg[((size_t)head * a.P + p) * SZ + el];
+    const float* seg = a.seg + (size_t)head * a.P * SZ + el;
+    float* out = a.out + (size_t)head * (a.P + 1) * SZ + el;
+    // (eight segments' loads issued together; the sums stay in order)
+    int p = 0;
+    for (; p + 8 <= a.P; p += 8) {
+      float x[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = seg[(size_t)(p + i) * SZ];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        out[(size_t)(p + i) * SZ] = v;
+        v += x[i];
+      }
     }
-    a.out[((size_t)head * (a.P + 1) + a.P) * SZ + el] = v;
+    for (; p < a.P; ++p) {
+      out[(size_t)p * SZ] = v;
+      v += seg[(size_t)p * SZ];
+    }
+    out[(size_t)a.P * SZ] = v;
   }
 }
 
@@ -63,11 +77,21 @@ __global__ __launch_bounds__(256) void scan_rev_kernel(ScanArgs a) {
   const int el = blockIdx.x * 256 + threadIdx.x;
   if (el < a.SZ) {
     float v = a.init ? a.init[head * SZ + el] : 0.f;
-    for (int p = a.P - 1; p >= 0; --p) {
-      const size_t idx = ((size_t)head * a.P + p) * SZ + el;
+    const float* seg = a.seg + (size_t)head * a.P * SZ + el;
+    auto step_to = [&](int p, float x) {
       if ((p + 1) % st == 0) a.out[((size_t)head * no + (p + 1) / st - 1) * SZ + el] = v;
-      v += a.seg[idx];
+      v += x;
+    };
+    // (eight segments' loads issued together; the sums stay in order)
+    int p = a.P - 1;
+    for (; p >= 7; p -= 8) {
+      float x[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = seg[(size_t)(p - i) * SZ];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) step_to(p - i, x[i]);
     }
+    for (; p >= 0; --p) step_to(p, seg[(size_t)p * SZ]);
     if (a.total != nullptr) {
       float r0 = 1.f;
       if (a.favor && a.init_shift != nullptr) r0 = fast_exp2((a.init_shift[head] - a.shift[head]) * kLog2e);
