@@ -655,8 +655,18 @@ __global__ __launch_bounds__(1024) void dw_reduce_kernel(const float* part, int 
   const int e = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int i = (blockIdx.x * 64 + e) * 4;  // n is a multiple of 4
   f32x4 s = zero4();
-  if (i < n)
-    for (int k = q; k < nparts; k += 16) s += *(const f32x4*)&part[(size_t)k * n + i];
+  if (i < n) {
+    // (four partials' loads issued together, added in the same order)
+    int k = q;
+    for (; k + 48 < nparts; k += 64) {
+      f32x4 x[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = *(const f32x4*)&part[(size_t)(k + 16 * j) * n + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s += x[j];
+    }
+    for (; k < nparts; k += 16) s += *(const f32x4*)&part[(size_t)k * n + i];
+  }
   acc[q][e] = s;
   __syncthreads();
   if (q == 0 && i < n) {

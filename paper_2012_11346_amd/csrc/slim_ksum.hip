@@ -393,7 +393,17 @@ __global__ void kshift_reduce_kernel(const float* part_max, int P2, const float*
   const int head = blockIdx.x * blockDim.x + threadIdx.x;
   if (head >= BH) return;
   float v = init_shift != nullptr ? init_shift[head] : -INFINITY;
-  for (int p = 0; p < P2; ++p) v = fmaxf(v, part_max[(size_t)head * P2 + p]);
+  const float* pm = part_max + (size_t)head * P2;
+  // (eight parts' loads issued together)
+  int p = 0;
+  for (; p + 8 <= P2; p += 8) {
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = pm[p + i];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v = fmaxf(v, x[i]);
+  }
+  for (; p < P2; ++p) v = fmaxf(v, pm[p]);
   kshift[head] = v;
 }
 
