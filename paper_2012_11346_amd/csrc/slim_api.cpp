@@ -1154,9 +1154,12 @@ int fwd_impl(const slim_problem* p, const void* Q, const void* K, const void* V,
       ks.out = (float*)(w + lay.seg_shift);
       e = dp.ksum(ks, slim::kSumMax, s);
       if (e != hipSuccess) return hip_fail(e, "key-maximum launch");
-      e = slim::launch_kshift_reduce(ks.out, P2, state_in != nullptr ? kshift_in : nullptr, kshift_out, BH, s);
-      if (e != hipSuccess) return hip_fail(e, "key-shift launch");
-      ks.shift = kshift_out;
+      // (the sums take the head's shift as the largest part maximum
+      // themselves and write it to kshift_out)
+      ks.part_max = ks.out;
+      ks.n_part_max = P2;
+      ks.init_shift = state_in != nullptr ? kshift_in : nullptr;
+      ks.shift_out = kshift_out;
     }
     ks.out = (float*)(w + lay.seg_sum);
     e = dp.ksum(ks, slim::kSumStates, s);

@@ -133,6 +133,13 @@ struct KsumArgs {
   const float* W;
   const void* Wfrag;   // fragment-ordered W (WFragLayout)
   const float* shift;  // kSumStates, kSumQuery, FAVOR+: [B,H] key shift of the sums
+  // kSumStates, FAVOR+, instead of `shift`: the key maxima of n_part_max
+  // parts per head ([B,H,n_part_max], from kSumMax) and init_shift ([B,H] or
+  // nullptr); the shift is their largest, written to shift_out by part 0
+  const float* part_max;
+  const float* init_shift;
+  float* shift_out;
+  int n_part_max;
   float* out;          // kSumStates, kSumQuery: [B,H,P2,M,D+1]; kSumMax: [B,H,P2]
   int B, H, L, C, P2;
   int tile_begin, tile_end;  // the parts cover tiles [tile_begin, tile_end) of each head (0, 0: all)

@@ -135,8 +135,28 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
   // row exponent offsets: keys exp2(x log2(e) - koff - 0.5 log2(e) |k|^2);
   // queries (kSumQuery) exp2(x log2(e) - (logD - kshift log2(e)))
   const float half_log2M = 0.5f * __log2f((float)M);
-  const float koff = (SUMS && G::KIND == kFavor)
-                         ? (QRY ? -a.shift[head] * kLog2e : a.shift[head] * kLog2e + half_log2M) : 0.f;
+  float sh = 0.f;  // the head's key shift (FAVOR+)
+  if constexpr (SUMS && G::KIND == kFavor) {
+    if (!QRY && a.part_max != nullptr) {
+      // the largest of the parts' key maxima and the initial state's shift
+      // (every workgroup of the head takes the same maximum)
+      sh = a.init_shift != nullptr ? a.init_shift[head] : -INFINITY;
+      const float* pm = a.part_max + head * (size_t)a.n_part_max;
+      int i = 0;
+      for (; i + 8 <= a.n_part_max; i += 8) {
+        float x[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[k] = pm[i + k];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) sh = fmaxf(sh, x[k]);
+      }
+      for (; i < a.n_part_max; ++i) sh = fmaxf(sh, pm[i]);
+      if (part == 0 && threadIdx.x == 0) a.shift_out[head] = sh;
+    } else {
+      sh = a.shift[head];
+    }
+  }
+  const float koff = (SUMS && G::KIND == kFavor) ? (QRY ? -sh * kLog2e : sh * kLog2e + half_log2M) : 0.f;
   constexpr float kscale = QRY ? 1.f : 0.5f * kLog2e;
 
   f32x4 S[SUMS ? MT : 1][SUMS ? ET : 1], Sz[SUMS ? MT : 1];
