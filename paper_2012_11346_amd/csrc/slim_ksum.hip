@@ -10,7 +10,8 @@
 // with no causal structure, so this pass streams the part's rows in 64-row
 // chunks with one barrier per chunk.  Four waves split the M features; per
 // chunk a wave computes the key logits of its features on the matrix cores
-// (W in registers), the features (FAVOR+: exp2 of the logit shifted by the
+// (W fragments in registers, or at 64 features per wave read per chunk),
+// the features (FAVOR+: exp2 of the logit shifted by the
 // head's fixed key shift and the row's -|k|^2/2; ReLU: max(., 0) + eps) and
 // accumulates K~^T [V|1] into its share of the state in registers.  Rows
 // move through double-buffered, swizzled LDS tiles; the rows two chunks
@@ -67,9 +68,10 @@ __global__ __launch_bounds__(256, 2) void ksum_kernel(KsumArgs a) {
 
   // W fragments of this wave's features: slot s = W[w FW + 16 mt + c][32 kb + kp(g, s)],
   // with the low parts of a bf16 split (see w_lo).  With 64 features per
-  // wave and sums (where registers are short) both parts come from the
-  // fragment table a.Wfrag at every chunk, half of the feature tiles at a
-  // time; otherwise they are held in registers.
+  // wave and sums (where registers are short) they are read at every chunk,
+  // half of the feature tiles at a time: the high parts from a copy in LDS
+  // (staged below), the low parts from the fragment table a.Wfrag;
+  // otherwise they are held in registers.
   constexpr bool LO_TABLE = kSplitW<T> && MT == 4 && SUMS;
   constexpr int MR = LO_TABLE ? 1 : MT;
   F Wf[MR][EB], Wl[SUMS ? MR : 1][EB];
