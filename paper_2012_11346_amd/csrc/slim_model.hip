@@ -170,14 +170,15 @@ __device__ __forceinline__ float4 ld4(const float* p, int avail) {
 
 // GRP: grouped B and grouped / head-split C (the kernels without it carry no
 // code, and no registers, for either)
-template <int BM, bool TA, bool TB, bool VEC, bool GRP>
+template <int BM, int BN, bool TA, bool TB, bool VEC, bool GRP>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int AV = BM * GBK / 4 / 256;  // float4 loads per thread per k tile (A)
-  constexpr int BV = GBN * GBK / 4 / 256;  // (B)
-  constexpr int TI = BM / 32;              // matrix tiles per wave along m
+  constexpr int BV = BN * GBK / 4 / 256;  // (B)
+  constexpr int TI = BM / 32;             // matrix tiles per wave along m
+  constexpr int TJ = BN / 32;             // and along n
   // [m][k] (k-contiguous source) or [k][m] (m-contiguous source) per buffer
-  constexpr int ALD = TA ? BM + 4 : GKP, BLD = TB ? GKP : GBN + 4;
-  constexpr int ASZ = TA ? GBK * ALD : BM * ALD, BSZ = TB ? GBN * BLD : GBK * BLD;
+  constexpr int ALD = TA ? BM + 4 : GKP, BLD = TB ? GKP : BN + 4;
+  constexpr int ASZ = TA ? GBK * ALD : BM * ALD, BSZ = TB ? BN * BLD : GBK * BLD;
   __shared__ __align__(16) float As[2][ASZ];
   __shared__ __align__(16) float Bs[2][BSZ];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -185,9 +186,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   int tile = blockIdx.x;
   const int nt = gridDim.x;
   if ((nt & 7) == 0) tile = (tile & 7) * (nt >> 3) + (tile >> 3);
-  const int m0 = (tile / g.tiles_n) * BM, n0 = (tile % g.tiles_n) * GBN;
+  const int m0 = (tile / g.tiles_n) * BM, n0 = (tile % g.tiles_n) * BN;
   const int kbeg = blockIdx.y * g.kchunk, kend = min(g.K, kbeg + g.kchunk);
-  const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * 64;
+  const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * (BN / 2);
   const int M = g.M, N = g.N;
 
   // grouped B along n: each thread's columns are the same in every k tile,
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const float* bcol[BV];
 #pragma unroll
   for (int i = 0; i < BV; ++i) {
-    const int n = n0 + 4 * ((tid + 256 * i) % (GBN / 4));
+    const int n = n0 + 4 * ((tid + 256 * i) % (BN / 4));
     bcol[i] = g.B + n;
     if (GRP && !TB && g.gN > 0 && n < N) {
       const int grp = group3(n, g.gN);
@@ -230,7 +231,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         }
         rb[i] = (n0 + n < N) ? ld4<VEC>(Bb + (size_t)(n0 + n) * g.ldb + kk, kend - k) : make_float4(0.f, 0.f, 0.f, 0.f);
       } else {  // rows of B: 4 n per vector
-        const int k = k0 + f / (GBN / 4), n = n0 + 4 * (f % (GBN / 4));
+        const int k = k0 + f / (BN / 4), n = n0 + 4 * (f % (BN / 4));
         rb[i] = (k < kend) ? ld4<VEC>(bcol[i] + (size_t)k * g.ldb, N - n) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
@@ -245,16 +246,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
       const int f = tid + 256 * i;
-      const int at = TB ? (f >> 2) * BLD + 4 * (f & 3) : (f / (GBN / 4)) * BLD + 4 * (f % (GBN / 4));
+      const int at = TB ? (f >> 2) * BLD + 4 * (f & 3) : (f / (BN / 4)) * BLD + 4 * (f % (BN / 4));
       *reinterpret_cast<float4*>(&Bs[buf][at]) = rb[i];
     }
   };
 
-  f4 acc[TI][4];
+  f4 acc[TI][TJ];
 #pragma unroll
   for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TJ; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
   const int c = lane & 15, q = lane >> 4;
   int buf = 0;
   if (kbeg < kend) {
@@ -265,7 +266,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   for (int k0 = kbeg; k0 < kend; k0 += GBK) {
     const bool more = k0 + GBK < kend;
     if (more) load(k0 + GBK);
-    float4 a[TI], b[4];
+    float4 a[TI], b[TJ];
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
       if (TA) {
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < TJ; ++j) {
       if (TB) {
         b[j] = *reinterpret_cast<const float4*>(&Bs[buf][(wn + 16 * j + c) * BLD + 4 * q]);
       } else {
@@ -288,19 +289,19 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[i][j], 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[i][j], 0, 0, 0);
     if (more) store(buf ^ 1);
     __syncthreads();
     buf ^= 1;
@@ -317,7 +318,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int j2 = 0; j2 < 4; j2 += 2) {
+      for (int j2 = 0; j2 < TJ; j2 += 2) {
         float x[2][4];
 #pragma unroll
         for (int jj = 0; jj < 2; ++jj) {
@@ -349,7 +350,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < TI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < TJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = m0 + wm + 16 * i + 4 * q + r, n = n0 + wn + 16 * j + c;
@@ -362,11 +363,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int IB = TI <= 2 ? TI : 1;
 #pragma unroll
   for (int i0 = 0; i0 < TI; i0 += IB) {
-    float x[IB][4][4];
+    float x[IB][TJ][4];
 #pragma unroll
     for (int ii = 0; ii < IB; ++ii)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < TJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = m0 + wm + 16 * (i0 + ii) + 4 * q + r, n = n0 + wn + 16 * j + c;
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int ii = 0; ii < IB; ++ii)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < TJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = m0 + wm + 16 * (i0 + ii) + 4 * q + r, n = n0 + wn + 16 * j + c;
@@ -410,23 +411,32 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* part, int
 
 // Launch plan of one product: tile height, k per split and split count.
 struct GemmPlan {
-  int BM, kchunk, splits, tiles_n, tiles;
+  int BM, BN, kchunk, splits, tiles_n, tiles;
 };
 inline GemmPlan gemm_plan(int M, int N, int K) {
-  GemmPlan p;
-  p.tiles_n = (N + GBN - 1) / GBN;
-  const int t128 = ((M + 127) / 128) * p.tiles_n;
   const int kt = (K + GBK - 1) / GBK;
-  // (a short reduction leaves the epilogue's reads and writes of C to set
-  // the pace: the smaller tile gives twice the workgroups in flight)
-  p.BM = (t128 >= 256 && kt > 8) ? 128 : 64;
-  p.tiles = ((M + p.BM - 1) / p.BM) * p.tiles_n;
-  int s = 1;
-  // split long K until about 512 workgroups run, keeping >= 8 k tiles each
-  while (p.tiles * s < 512 && kt >= 16 * s && s < 64) s *= 2;  // next split keeps >= 8 k tiles
-  const int per = std::max(1, (kt + s - 1) / s);
-  p.kchunk = per * GBK;
-  p.splits = (kt + per - 1) / per;
+  const int t128 = ((M + 127) / 128) * ((N + GBN - 1) / GBN);
+  auto plan = [&](int BN) {
+    GemmPlan p;
+    // (a short reduction leaves the epilogue's reads and writes of C to set
+    // the pace: the smaller tile gives twice the workgroups in flight)
+    p.BM = (t128 >= 256 && kt > 8) ? 128 : 64;
+    p.BN = BN;
+    p.tiles_n = (N + BN - 1) / BN;
+    p.tiles = ((M + p.BM - 1) / p.BM) * p.tiles_n;
+    int s = 1;
+    // split long K until about 512 workgroups run, keeping >= 8 k tiles each
+    while (p.tiles * s < 512 && kt >= 16 * s && s < 64) s *= 2;  // next split keeps >= 8 k tiles
+    const int per = std::max(1, (kt + s - 1) / s);
+    p.kchunk = per * GBK;
+    p.splits = (kt + per - 1) / per;
+    return p;
+  };
+  const GemmPlan p = plan(GBN);
+  // fewer workgroups than the split aims for (a short row count, or a
+  // reduction too short to split further): 64-column tiles double them
+  // (64-row tiles; 128-row ones only come with at least 256 tiles)
+  if (p.BM == 64 && p.tiles * p.splits < 512) return plan(64);
   return p;
 }
 inline size_t gemm_part_bytes(int M, int N, int K) {
@@ -434,17 +444,17 @@ inline size_t gemm_part_bytes(int M, int N, int K) {
   return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
 }
 
-template <int BM, bool TA, bool TB, bool GRP>
+template <int BM, int BN, bool TA, bool TB, bool GRP>
 void gemm_launch(const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
-  if (vec) hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, true, GRP>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((gemm_kernel<BM, TA, TB, false, GRP>), grid, dim3(256), 0, s, a);
+  if (vec) hipLaunchKernelGGL((gemm_kernel<BM, BN, TA, TB, true, GRP>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((gemm_kernel<BM, BN, TA, TB, false, GRP>), grid, dim3(256), 0, s, a);
 }
-template <int BM, bool GRP>
+template <int BM, int BN, bool GRP>
 void gemm_launch(bool ta, bool tb, const GemmArgs& a, dim3 grid, bool vec, hipStream_t s) {
-  if (ta && tb) gemm_launch<BM, true, true, GRP>(a, grid, vec, s);
-  else if (ta) gemm_launch<BM, true, false, GRP>(a, grid, vec, s);
-  else if (tb) gemm_launch<BM, false, true, GRP>(a, grid, vec, s);
-  else gemm_launch<BM, false, false, GRP>(a, grid, vec, s);
+  if (ta && tb) gemm_launch<BM, BN, true, true, GRP>(a, grid, vec, s);
+  else if (ta) gemm_launch<BM, BN, true, false, GRP>(a, grid, vec, s);
+  else if (tb) gemm_launch<BM, BN, false, true, GRP>(a, grid, vec, s);
+  else gemm_launch<BM, BN, false, false, GRP>(a, grid, vec, s);
 }
 
 // part: workspace for the partial products (gemm_part_bytes of the shape);
@@ -487,12 +497,16 @@ hipError_t gemm(bool ta, bool tb, int M, int N, int K, const float* A, int lda, 
   const bool vec = lda % 4 == 0 && ldb % 4 == 0 && ((uintptr_t)A & 15) == 0 && bal;
   const dim3 grid(p.tiles, p.splits);
   const bool grouped = a.gN > 0 || a.gK > 0 || epi.layout != 0;
+  // (128-row tiles only come with 128-column ones: they need 256 tiles)
   if (p.BM == 128) {
-    if (grouped) gemm_launch<128, true>(ta, tb, a, grid, vec, s);
-    else gemm_launch<128, false>(ta, tb, a, grid, vec, s);
+    if (grouped) gemm_launch<128, 128, true>(ta, tb, a, grid, vec, s);
+    else gemm_launch<128, 128, false>(ta, tb, a, grid, vec, s);
+  } else if (p.BN == 128) {
+    if (grouped) gemm_launch<64, 128, true>(ta, tb, a, grid, vec, s);
+    else gemm_launch<64, 128, false>(ta, tb, a, grid, vec, s);
   } else {
-    if (grouped) gemm_launch<64, true>(ta, tb, a, grid, vec, s);
-    else gemm_launch<64, false>(ta, tb, a, grid, vec, s);
+    if (grouped) gemm_launch<64, 64, true>(ta, tb, a, grid, vec, s);
+    else gemm_launch<64, 64, false>(ta, tb, a, grid, vec, s);
   }
   if (p.splits > 1) {
     const size_t MN = (size_t)M * N;
